@@ -1,0 +1,132 @@
+/*
+ * ssdref — plain CPU oracle for the tree-verification hot path of staged
+ * speculative decoding (Spector & Re, "Accelerating LLM Inference with Staged
+ * Speculative Decoding", arXiv 2308.04623).
+ *
+ * TEST INFRASTRUCTURE ONLY.  This library exists so that tests, the smoke
+ * check and the benchmark's CPU-baseline leg can compare the GPU library
+ * against a slow, obviously correct reference.  No product code path may
+ * call it.  It shares no source, header, table or helper with the GPU
+ * library.
+ *
+ * Arithmetic: activations, dot products, softmax and LayerNorm in fp64.
+ * Stored parameters and K/V are read as their exact stored values (float32,
+ * or bfloat16 bit patterns widened exactly).  K and V are rounded to the
+ * storage type when produced (round-to-nearest-even), because those rounded
+ * values are what every later node and later step reads from the cache.
+ * Logits are rounded to float32 at the end.
+ *
+ * Every element is computed by one thread with a fixed summation order
+ * (ascending index), so results are bitwise independent of the OpenMP thread
+ * count, of the number of tree nodes and of a node's slot in the tree.
+ *
+ * Paper passages followed:
+ *  - Sec. 2.1 (autoregressive inference): prefill builds the KV cache; each
+ *    decode step feeds one token and reads the cache.
+ *  - Sec. 3.1 (tree-structured batches): attention of a batch node is split
+ *    into attention over the KV cache plus attention within the batch, masked
+ *    by the tree; positional embeddings are set per node; the batch K/V is
+ *    kept apart and the accepted slices are appended to the cache after
+ *    sampling.
+ *  - Sec. 2.3 (speculative decoding): draft tokens are checked in one batch;
+ *    everything after the first rejection is dropped; rejection sampling
+ *    keeps the oracle model's distribution.
+ *
+ * All pointers are host memory.  Functions return 0 on success and a
+ * negative code on invalid input (nothing is written in that case).
+ */
+#ifndef SSDREF_H
+#define SSDREF_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SSDREF_OK 0
+#define SSDREF_E_ARG (-1)
+#define SSDREF_E_TREE (-2)
+#define SSDREF_E_CAPACITY (-3)
+
+/* Storage type of every parameter and of the K/V cache. */
+#define SSDREF_F32 0
+#define SSDREF_BF16 1
+
+#define SSDREF_ACCEPT_GREEDY 0
+#define SSDREF_ACCEPT_SAMPLE_WOR 1 /* siblings were drawn without replacement */
+#define SSDREF_ACCEPT_SAMPLE_IID 2 /* siblings were drawn independently      */
+
+typedef struct {
+  int32_t n_layer, d_model, n_head, d_mlp, vocab, n_pos;
+  int32_t dtype; /* SSDREF_F32 or SSDREF_BF16 */
+  double ln_eps;
+} ssdref_config;
+
+/* GPT-2 parameters.  Matrices are [out][in] row-major; element type per
+ * config.dtype (bf16 = uint16 bit pattern).  Per-layer entries are arrays of
+ * n_layer pointers.  The LM head is tied to wte. */
+typedef struct {
+  const void *wte;   /* [vocab][d]  */
+  const void *wpe;   /* [n_pos][d]  */
+  const void *lnf_g; /* [d]         */
+  const void *lnf_b; /* [d]         */
+  const void *const *ln1_g, *const *ln1_b; /* [d]              */
+  const void *const *w_qkv, *const *b_qkv; /* [3d][d], [3d]    */
+  const void *const *w_o, *const *b_o;     /* [d][d], [d]      */
+  const void *const *ln2_g, *const *ln2_b; /* [d]              */
+  const void *const *w_fc, *const *b_fc;   /* [d_mlp][d], [d_mlp] */
+  const void *const *w_pr, *const *b_pr;   /* [d][d_mlp], [d]  */
+} ssdref_weights;
+
+/* Tree bookkeeping (Sec. 3.1).  parent_idx[0] must be -1 and
+ * 0 <= parent_idx[i] < i for i > 0 (topological order).  Writes
+ * depth[n] (root depth 0) and anc[n*n] with anc[i*n+j] = 1 iff j is i or an
+ * ancestor of i.  Either output may be NULL.  Returns SSDREF_E_TREE on a
+ * malformed tree. */
+int ssdref_tree_info(const int32_t *parent_idx, int32_t n, int32_t *depth, uint8_t *anc);
+
+/* Tree verification pass (Sec. 3.1).
+ *  k_cache, v_cache: [n_layer][n_head][max_ctx][head_dim], rows 0..prefix_len-1 hold the prefix.
+ *  k_tree, v_tree:   [n_layer][n_head][max_nodes][head_dim], written for rows 0..n_nodes-1.
+ *  Node i sits at position prefix_len + depth(i) and attends to the prefix_len
+ *  cached keys followed by its ancestors root..parent and itself.
+ *  logits: [n_nodes][vocab] float32.
+ *  n_threads <= 0 uses the OpenMP default. */
+int ssdref_tree_verify(const ssdref_config *cfg, const ssdref_weights *w,
+                       const void *k_cache, const void *v_cache, int32_t max_ctx, int32_t prefix_len,
+                       const int32_t *tokens, const int32_t *parent_idx, int32_t n_nodes,
+                       void *k_tree, void *v_tree, int32_t max_nodes,
+                       float *logits, int32_t n_threads);
+
+/* Appends the accepted nodes' K/V (path[0..path_len-1], root first) to the
+ * cache at rows prefix_len..prefix_len+path_len-1 (Sec. 3.1, last sentence). */
+int ssdref_kv_commit(const ssdref_config *cfg, void *k_cache, void *v_cache, int32_t max_ctx,
+                     int32_t prefix_len, const void *k_tree, const void *v_tree, int32_t max_nodes,
+                     const int32_t *path, int32_t path_len);
+
+/* Accept/reject walk over the verified tree (Sec. 2.3 and 3.1).
+ *  mode GREEDY: draft_probs may be NULL; temperature and seed are ignored.
+ *  mode SAMPLE_*: draft_probs[u][v] is the distribution node u's children
+ *  were drawn from; the target at node u is softmax(logits[u] / temperature).
+ * Outputs: path[0..*path_len-1] (root first, path[0] = 0) and the one extra
+ * token (bonus or corrected) in *next_token. */
+int ssdref_tree_accept(int32_t mode, const int32_t *tokens, const int32_t *parent_idx, int32_t n_nodes,
+                       int32_t vocab, const float *draft_probs, const float *logits, double temperature,
+                       uint64_t seed, int32_t *path, int32_t *path_len, int32_t *next_token);
+
+/* Philox4x64-10 (Salmon, Moraes, Dror, Shaw, SC'11): out = bijection(ctr; key). */
+void ssdref_philox4x64_10(const uint64_t key[2], const uint64_t ctr[4], uint64_t out[4]);
+
+/* Uniform double in [0,1): top 53 bits of word 0 of Philox4x64-10 with
+ * key (seed, stream) and counter (n, 0, 0, 0). */
+double ssdref_uniform(uint64_t seed, uint64_t stream, uint64_t n);
+
+/* float32 -> bfloat16 and fp64 -> bfloat16, round-to-nearest-even. */
+uint16_t ssdref_round_bf16(double x);
+
+#ifdef __cplusplus
+}
+#endif
+#endif
