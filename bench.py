@@ -1,0 +1,217 @@
+#!/usr/bin/env python
+"""Benchmark of the tree-verification hot path on one MI355X.
+
+Workload: GPT-2-L shape (36 x 1280, 20 heads of 64, MLP 5120, vocab 50257),
+random N(0, 0.02) bf16 weights, a synthetic 512-token prefix cache and a
+32-node tree (branching 4,2,2,1 breadth-first, truncated), greedy acceptance.
+One step = the whole hot path on that input: the captured verification pass,
+the accept walk and the KV commit (commit rewrites the same rows past the
+prefix every step, and verification never reads them, so steps repeat
+exactly).  Inputs are resident in HBM before timing starts.
+
+Prints one JSON line on stdout; progress goes to stderr.
+"""
+import argparse
+import hashlib
+import json
+import os
+import platform
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0
+METRIC = "µs per tree-verify pass + verified tree tokens/s, GPT-2-L shape; HBM GB/s"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def pass_bytes(cfg, n, P):
+    """Algorithmic HBM bytes of one verification pass: every parameter once
+    (matrices, tied LM head, vectors; the embedding rows gathered are
+    negligible), the prefix K/V once, the tree K/V written once and the
+    float32 logits written once."""
+    d, m, L, V = cfg.d_model, cfg.d_mlp, cfg.n_layer, cfg.vocab
+    es = 2 if cfg.dtype == "bf16" else 4
+    mats = L * (3 * d * d + d * d + m * d + d * m) * es
+    head = V * d * es
+    vecs = (L * (2 * d + 3 * d + d + 2 * d + m + d) + 2 * d) * es
+    kv_row = L * 2 * d * es
+    return mats + head + vecs + kv_row * P + (kv_row + V * 4) * n
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    with open(os.path.join(ROOT, "paper_2308_04623_amd", "csrc", "kernels.hip"), "rb") as f:
+        h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor()
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--nodes", type=int, default=32)
+    ap.add_argument("--prefix", type=int, default=512)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-sweep", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for {args.gpus}): this build has no multi-GPU path; "
+              "the pass would shard by tensor parallelism, see DESIGN.md", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2308_04623_amd import ssd
+    from paper_2308_04623_amd import workloads as W
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    cfg = W.GPT2L
+    N, P = args.nodes, args.prefix
+    max_ctx, max_nodes = 1024 + 64, 128
+    log("generating GPT-2-L weights")
+    w = W.make_weights(cfg, 0)
+    model = ssd.Model(cfg, w)
+    kc, vc = W.random_kv_cache(cfg, max_ctx, 1024, seed=3)
+    sess = ssd.Session(model, max_ctx, max_nodes, ssd.to_device(kc, cfg), ssd.to_device(vc, cfg))
+    par = W.branching_tree([4, 2, 2, 1], N)
+    toks = W.tree_tokens(par, cfg.vocab, seed=2)
+    logits = torch.empty((N, cfg.vocab), dtype=torch.float32, device="cuda")
+    graph = sess.capture_verify(P, toks, par, logits)
+    outs = (torch.zeros(N, dtype=torch.int32, device="cuda"), torch.zeros(1, dtype=torch.int32, device="cuda"),
+            torch.zeros(1, dtype=torch.int32, device="cuda"))
+    stream = torch.cuda.current_stream()
+
+    def step():
+        graph.launch()
+        path, plen, _ = sess.accept(toks, par, logits, out=outs)
+        sess.commit(P, path, plen)
+
+    log(f"warmup {args.warmup}")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms_step = e0.elapsed_time(e1) / args.steps
+    log(f"step {ms_step * 1e3:.1f} us")
+
+    def time_graph(g, reps):
+        for _ in range(5):
+            g.launch()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(reps):
+            g.launch()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps * 1e3  # us
+
+    us_pass = time_graph(graph, max(args.steps, 50))
+    B = pass_bytes(cfg, N, P)
+    log(f"verify pass {us_pass:.1f} us, {B / us_pass / 1e3:.0f} GB/s")
+
+    # dominant kernel: the MLP up-projection GEMM (13.1 MB of weights per
+    # launch), launched on its own for every layer in turn so its weights
+    # stream from HBM; HIP events on the stream it runs on
+    reps = 4
+    for l in range(cfg.n_layer):
+        sess.launch_gemm(2, l, N)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    for _ in range(reps):
+        for l in range(cfg.n_layer):
+            sess.launch_gemm(2, l, N)
+    b.record(stream)
+    torch.cuda.synchronize()
+    us_fc = a.elapsed_time(b) * 1e3 / (reps * cfg.n_layer)
+    fc_bytes = cfg.d_mlp * cfg.d_model * 2 + N * cfg.d_model * 2 + N * cfg.d_mlp * 2
+    fc_gbs = fc_bytes / us_fc / 1e3
+    traffic = None
+    tpath = os.path.join(ROOT, "profiles", "traffic_fc_gemm.json")
+    if os.path.exists(tpath):
+        t = json.load(open(tpath))
+        if t.get("kernel_source") == kernel_source_hash() and t.get("nodes") == N:
+            traffic = t.get("bytes_per_launch")
+    roofline = {"bound": "hbm", "achieved": round(fc_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(fc_gbs / PEAK_HBM_GBS, 4), "traffic": traffic,
+                "kernel": "gemm (MLP up-projection + GELU), 5120x1280 bf16",
+                "bytes_per_launch": fc_bytes, "us_per_launch": round(us_fc, 2)}
+
+    sweep = []
+    if not args.no_sweep:
+        for n_s, p_s in [(1, 512), (8, 512), (16, 512), (64, 512), (128, 512), (64, 128), (64, 1024)]:
+            tt, pp = W.best_first_tree(n_s, seed=3, vocab=cfg.vocab)
+            tt[0] = int(toks[0])
+            lg = torch.empty((n_s, cfg.vocab), dtype=torch.float32, device="cuda")
+            g = sess.capture_verify(p_s, tt, pp, lg)
+            us = time_graph(g, 50)
+            g.close()
+            bb = pass_bytes(cfg, n_s, p_s)
+            sweep.append({"nodes": n_s, "prefix": p_s, "us": round(us, 1), "GB/s": round(bb / us / 1e3, 1),
+                          "frac": round(bb / us / 1e3 / PEAK_HBM_GBS, 4)})
+            log(f"sweep N={n_s} P={p_s}: {us:.1f} us")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        threads = int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or (os.cpu_count() or 1)
+        om = oracle.Model(cfg, w)
+        okt, ovt = om.kv(max_nodes), om.kv(max_nodes)
+        times = []
+        t_start = time.time()
+        while len(times) < 5 and (time.time() - t_start) < 12.0:
+            t0 = time.time()
+            oracle.tree_verify(om, kc, vc, P, toks, par, okt, ovt, threads)
+            times.append(time.time() - t0)
+        tpass = sorted(times)[len(times) // 2]
+        cpu = {"value": round(N / tpass, 3), "unit": "verified tree tokens/s", "cores": threads, "kind": "oracle",
+               "sample": f"{len(times)} full oracle verification passes of this workload (fp64, {N} nodes, "
+                         f"prefix {P}), median {tpass:.2f} s each; host {cpu_model()}"}
+        log(f"oracle pass {tpass:.2f} s on {threads} threads")
+
+    value = N / (us_pass * 1e-6)
+    line = {
+        "metric": METRIC, "value": round(value, 1), "unit": "verified tree tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"GPT-2-L shape tree verification, {N}-node tree (branching 4,2,2,1), "
+                               f"{P}-token prefix, greedy accept + commit",
+                   "nodes": N, "prefix": P, "layers": cfg.n_layer, "d_model": cfg.d_model, "vocab": cfg.vocab},
+        "us_per_verify_pass": round(us_pass, 2),
+        "pass_hbm_GBs": round(B / us_pass / 1e3, 1),
+        "pass_frac_of_peak": round(B / us_pass / 1e3 / PEAK_HBM_GBS, 4),
+        "pass_algorithmic_bytes": B,
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "sweep": sweep,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,200 @@
+/*
+ * ssd.h — C ABI of libssd, the MI355X (gfx950) tree-verification library for
+ * staged speculative decoding (Spector & Re, arXiv 2308.04623).
+ *
+ * One decoding step of the paper's method, on one GPU:
+ *   ssd_tree_verify  scores every node of a speculative token tree against the
+ *                    KV cache of the accepted prefix in one decoder pass
+ *                    (Sec. 3.1: attention split into attention over the cache
+ *                    plus tree-masked attention inside the batch, positions
+ *                    set per node, the batch's own K/V kept apart);
+ *   ssd_tree_accept  walks the tree and keeps the longest path the model
+ *                    agrees with, plus one extra token (Sec. 2.3; greedy, or
+ *                    rejection sampling that keeps the model's distribution);
+ *   ssd_kv_commit    appends the accepted nodes' K/V to the cache (Sec. 3.1,
+ *                    last step).
+ *
+ * Conventions shared by every call:
+ *  - Device pointers are HIP device memory owned by the caller (for example
+ *    torch tensors' data_ptr()); the library never frees them.  Host
+ *    pointers are ordinary host memory, read before the call returns.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *    Work is enqueued asynchronously; no call synchronises the host except
+ *    ssd_model_create (which waits for its one-time weight repacking).
+ *  - Every argument, tree and capacity check runs on the host before anything
+ *    is enqueued; on error nothing is enqueued and outputs are untouched.
+ *    Statuses are negative on error; ssd_last_error() gives a thread-local
+ *    message.  Asynchronous device faults surface as SSD_E_DEVICE later.
+ *  - A handle is used by one host thread and one stream at a time.
+ *
+ * Model: GPT-2, pre-LayerNorm blocks, tanh GELU, learned absolute positions,
+ * LM head tied to the token embedding.  All parameters and the K/V cache use
+ * one storage type (float32 or bfloat16); accumulation is float32.
+ */
+#ifndef SSD_H
+#define SSD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SSD_OK = 0,
+  SSD_E_INVALID_ARG = -1,  /* null pointer, bad size, bad config, bad token id  */
+  SSD_E_INVALID_TREE = -2, /* parent_idx[0] != -1 or parent_idx[i] not in [0,i)  */
+  SSD_E_CAPACITY = -3,     /* more nodes / context / positions than allocated     */
+  SSD_E_DEVICE = -4,       /* a HIP runtime call failed                           */
+  SSD_E_UNSUPPORTED = -5   /* shape the kernels do not handle (see ssd_model_create) */
+} ssd_status;
+
+typedef enum { SSD_F32 = 0, SSD_BF16 = 1 } ssd_dtype;
+
+typedef enum {
+  SSD_ACCEPT_GREEDY = 0,     /* argmax walk                                          */
+  SSD_ACCEPT_SAMPLE_WOR = 1, /* rejection sampling; siblings were drawn without replacement */
+  SSD_ACCEPT_SAMPLE_IID = 2  /* rejection sampling; siblings were drawn independently       */
+} ssd_accept_mode;
+
+typedef struct {
+  int32_t n_layer, d_model, n_head, d_mlp, vocab, n_pos;
+  ssd_dtype dtype; /* storage type of every parameter and of the K/V cache */
+  float ln_eps;    /* LayerNorm epsilon (GPT-2: 1e-5) */
+} ssd_config;
+
+/* Device pointers to the parameters, caller-owned, in the config's storage
+ * type.  Matrices are [out][in] row-major; per-layer entries are HOST arrays
+ * of n_layer device pointers.  Must stay valid until ssd_model_destroy. */
+typedef struct {
+  const void *wte;   /* [vocab][d_model]: token embedding and tied LM head */
+  const void *wpe;   /* [n_pos][d_model]                                   */
+  const void *lnf_g; /* [d_model]                                          */
+  const void *lnf_b; /* [d_model]                                          */
+  const void *const *ln1_g, *const *ln1_b; /* [d_model]                           */
+  const void *const *w_qkv, *const *b_qkv; /* [3 d_model][d_model], [3 d_model]   */
+  const void *const *w_o, *const *b_o;     /* [d_model][d_model], [d_model]       */
+  const void *const *ln2_g, *const *ln2_b; /* [d_model]                           */
+  const void *const *w_fc, *const *b_fc;   /* [d_mlp][d_model], [d_mlp]           */
+  const void *const *w_pr, *const *b_pr;   /* [d_model][d_mlp], [d_model]         */
+} ssd_weights;
+
+typedef struct ssd_model ssd_model; /* opaque */
+typedef struct ssd_kv ssd_kv;       /* opaque: one decoding session's cache + workspaces */
+typedef struct ssd_graph ssd_graph; /* opaque: a captured verification pass */
+
+/* A token tree in host memory (Sec. 3.1).  Node 0 is the root: the last
+ * emitted token, not yet in the cache.  parent_idx[0] = -1 and
+ * 0 <= parent_idx[i] < i (topological order). */
+typedef struct {
+  const int32_t *tokens;     /* [n_nodes] */
+  const int32_t *parent_idx; /* [n_nodes] */
+  int32_t n_nodes;
+  int32_t vocab;
+  ssd_accept_mode mode;
+  float temperature; /* sampling modes: target = softmax(logits / temperature) */
+} ssd_tree;
+
+/* Loads a model.  Supported shapes: d_model % 32 == 0, d_mlp % 32 == 0,
+ * head_dim (= d_model / n_head) of 32 or 64.  For bfloat16 the library
+ * repacks every matrix (and the LM head) once into a private copy laid out in
+ * matrix-core tile order (freed by ssd_model_destroy); this call waits for it.
+ * Errors: SSD_E_INVALID_ARG, SSD_E_UNSUPPORTED, SSD_E_DEVICE. */
+ssd_status ssd_model_create(const ssd_config *cfg, const ssd_weights *w, void *stream, ssd_model **out);
+void ssd_model_destroy(ssd_model *m);
+
+/* Bytes the caller must allocate for the cache (each of K and V:
+ * [n_layer][n_head][max_ctx][head_dim]) and the tree scratch (each of K and V:
+ * [n_layer][n_head][max_nodes][head_dim]) in the storage type. */
+ssd_status ssd_kv_bytes(const ssd_config *cfg, int32_t max_ctx, int32_t max_nodes, size_t *cache_bytes,
+                        size_t *tree_bytes);
+
+/* Binds caller-owned K/V buffers to a session and allocates the session's
+ * workspaces (activations, attention partials, accept scratch, pinned
+ * staging).  max_nodes <= 1024.  Errors: SSD_E_INVALID_ARG, SSD_E_CAPACITY,
+ * SSD_E_DEVICE. */
+ssd_status ssd_kv_create(const ssd_model *m, int32_t max_ctx, int32_t max_nodes, void *k_cache, void *v_cache,
+                         void *k_tree, void *v_tree, ssd_kv **out);
+void ssd_kv_destroy(ssd_kv *kv);
+
+/* Tree verification pass (Sec. 3.1).  Node i sits at position
+ * prefix_len + depth(i) and attends to cache rows 0..prefix_len-1, then to
+ * its ancestors root..parent and itself in the tree scratch.  Writes every
+ * node's K/V to the tree scratch rows 0..n_nodes-1 and
+ * logits[n_nodes][vocab] (float32, device).  Never modifies the cache, so
+ * repeating a call gives the same result.
+ * Errors: SSD_E_INVALID_ARG (null, token out of range), SSD_E_INVALID_TREE,
+ * SSD_E_CAPACITY (n_nodes > max_nodes, prefix_len > max_ctx,
+ * prefix_len + max depth >= n_pos), SSD_E_DEVICE. */
+ssd_status ssd_tree_verify(const ssd_model *m, ssd_kv *kv, int32_t prefix_len, const int32_t *tree_tokens,
+                           const int32_t *parent_idx, int32_t n_nodes, float *logits, void *stream);
+
+/* Accept/reject walk (Sec. 2.3, 3.1) over logits from ssd_tree_verify.
+ *  greedy: a node is kept when its parent is kept and its token is the
+ *    parent's argmax (lowest token id on ties); the deepest kept node (lowest
+ *    index on ties) ends the path and its argmax is the extra token.
+ *  sampling: recursive rejection sampling down the tree.  draft_probs
+ *    ([n_nodes][vocab], device) row u is the distribution node u's children
+ *    were drawn from.  Uniforms come from Philox4x64-10 keyed by
+ *    (rng_seed, 0) with counter (child index, 0, 0, 0) for the test of that
+ *    child, and (rng_seed, 1) with counter (last node) for the extra token.
+ * Outputs (device): accepted_path[0..*path_len-1] root first (path[0] = 0),
+ * *next_token.  Emitted tokens are tokens[path[1..]] then next_token.
+ * draft_probs must be NULL for greedy and non-NULL for sampling. */
+ssd_status ssd_tree_accept(ssd_kv *kv, const ssd_tree *tree, const float *draft_probs, const float *oracle_logits,
+                           uint64_t rng_seed, int32_t *accepted_path, int32_t *path_len, int32_t *next_token,
+                           void *stream);
+
+/* Appends tree scratch rows accepted_path[0..*path_len-1] (device arrays, as
+ * written by ssd_tree_accept) to cache rows prefix_len.. (Sec. 3.1).  Reads
+ * the path on the device, so no host sync is needed between accept and
+ * commit.  Rows that would fall past max_ctx, or path entries outside
+ * [0, max_nodes), are skipped and counted; ssd_kv_error_count reports them. */
+ssd_status ssd_kv_commit(ssd_kv *kv, int32_t prefix_len, const int32_t *accepted_path, const int32_t *path_len,
+                         void *stream);
+
+/* Number of commit rows skipped as out of range since the session began
+ * (synchronises the stream). */
+ssd_status ssd_kv_error_count(ssd_kv *kv, void *stream, uint32_t *count);
+
+/* Captures one verification pass (same arguments as ssd_tree_verify) into a
+ * HIP graph; ssd_graph_launch replays it on the given stream with the same
+ * tree and prefix.  Capture runs on a library-private stream (nothing
+ * executes during capture; `stream` is unused).  Used to run the pass
+ * without per-kernel host launch overhead. */
+ssd_status ssd_graph_capture_verify(const ssd_model *m, ssd_kv *kv, int32_t prefix_len, const int32_t *tree_tokens,
+                                    const int32_t *parent_idx, int32_t n_nodes, float *logits, void *stream,
+                                    ssd_graph **out);
+ssd_status ssd_graph_launch(ssd_graph *g, void *stream);
+void ssd_graph_destroy(ssd_graph *g);
+
+/* Launches one weight GEMM of the verification pass on its own, exactly as
+ * the pass launches it, for measurement: which = 0 QKV, 1 attention output,
+ * 2 MLP up (FC + GELU), 3 MLP down, 4 LM head; layer in [0, n_layer).  Reads
+ * and writes only the session's workspaces and tree scratch (never the cache
+ * or caller buffers), so results are meaningless outside a pass. */
+ssd_status ssd_launch_gemm(const ssd_model *m, ssd_kv *kv, int32_t which, int32_t layer, int32_t n_nodes,
+                           void *stream);
+
+/* Host-only tree checks (no GPU needed).  Validates topology and token ids;
+ * writes the maximum depth. */
+ssd_status ssd_validate_tree(const int32_t *tokens, const int32_t *parent_idx, int32_t n, int32_t vocab,
+                             int32_t *max_depth);
+
+/* Host-only tree bookkeeping as used by ssd_tree_verify: depth[n] and the
+ * ancestor-or-self bitmask anc[n][ceil(n/64)] (bit j of word j/64 of row i
+ * is set iff node j is node i or one of its ancestors). */
+ssd_status ssd_tree_prep(const int32_t *parent_idx, int32_t n, int32_t *depth, uint64_t *anc);
+
+/* Verification-pass GEMM path: 0 = automatic (by node count), 1 = vector
+ * ALU, 2 = matrix cores.  Process-wide; bfloat16 models only. */
+ssd_status ssd_set_gemm_path(int32_t path);
+
+const char *ssd_status_string(ssd_status s);
+const char *ssd_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

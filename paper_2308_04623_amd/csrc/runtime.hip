@@ -1,0 +1,702 @@
+// Host runtime of libssd: the C ABI declared in include/ssd.h.
+//
+// Validation and tree bookkeeping run on the host before anything is
+// enqueued; the per-call tree description (tokens, positions, depths,
+// parents, ancestor bitmask) is staged through pinned memory and copied to
+// the device on the caller's stream; the pass is a fixed sequence of kernel
+// launches on that stream, so it can be captured into a HIP graph.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/ssd.h"
+#include "ssd_internal.h"
+
+using namespace ssd;
+
+namespace {
+
+thread_local std::string g_last_error;
+int g_gemm_path = 0;  // 0 auto, 1 vector ALU, 2 matrix cores
+
+// Node counts up to this use the vector-ALU GEMM on the automatic path.
+constexpr int kVecMaxNodes = 4;
+constexpr int kMaxNodes = 1024;
+constexpr int kStageSlots = 4;
+
+ssd_status fail(ssd_status st, const std::string& msg) {
+  g_last_error = msg;
+  return st;
+}
+
+#define HIP_TRY(expr)                                                                          \
+  do {                                                                                         \
+    hipError_t e_ = (expr);                                                                    \
+    if (e_ != hipSuccess)                                                                      \
+      return fail(SSD_E_DEVICE, std::string(#expr) + ": " + hipGetErrorString(e_));            \
+  } while (0)
+
+int round_up(int a, int b) { return (a + b - 1) / b * b; }
+
+}  // namespace
+
+struct ssd_model {
+  ssd_config cfg;
+  int dh = 0;
+  bool f32 = false;
+  const void *wte = nullptr, *wpe = nullptr, *lnf_g = nullptr, *lnf_b = nullptr;
+  std::vector<const void*> ln1_g, ln1_b, w_qkv, b_qkv, w_o, b_o, ln2_g, ln2_b, w_fc, b_fc, w_pr, b_pr;
+  // bf16 only: packed copies
+  void* pack = nullptr;
+  std::vector<const void*> p_qkv, p_o, p_fc, p_pr;
+  const void* p_head = nullptr;
+};
+
+struct ssd_kv {
+  const ssd_model* m = nullptr;
+  int max_ctx = 0, max_nodes = 0, npad = 0, ns_max = 0, W = 0;
+  void *kc = nullptr, *vc = nullptr, *kt = nullptr, *vt = nullptr;
+  void* ws = nullptr;  // one device allocation for every workspace below
+  float* x = nullptr;
+  float* q = nullptr;
+  void* act_a = nullptr;  // LN outputs [npad][d]
+  void* act_o = nullptr;  // attention outputs [npad][d]
+  void* act_f = nullptr;  // GELU outputs [npad][d_mlp]
+  float* part = nullptr;  // attention partials
+  // tokens, positions, depths, parents (max_nodes each), then ancestor masks [n][ceil(n/64)]
+  int* d_tree = nullptr;
+  int* d_accept_tree = nullptr;  // tokens[N] parents[N] depth[N] for accept
+  int* d_argmax = nullptr;
+  double *d_r = nullptr, *d_p = nullptr, *d_qq = nullptr;
+  unsigned* d_err = nullptr;
+  // pinned staging ring
+  char* pinned = nullptr;
+  size_t slot_bytes = 0;
+  int next_slot = 0;
+  hipEvent_t slot_ev[kStageSlots] = {};
+  bool slot_used[kStageSlots] = {};
+};
+
+struct ssd_graph {
+  hipGraph_t graph = nullptr;
+  hipGraphExec_t exec = nullptr;
+  char* pinned = nullptr;
+};
+
+// ------------------------------------------------------------------ small host helpers
+
+extern "C" const char* ssd_status_string(ssd_status s) {
+  switch (s) {
+    case SSD_OK: return "ok";
+    case SSD_E_INVALID_ARG: return "invalid argument";
+    case SSD_E_INVALID_TREE: return "invalid tree";
+    case SSD_E_CAPACITY: return "capacity exceeded";
+    case SSD_E_DEVICE: return "device error";
+    case SSD_E_UNSUPPORTED: return "unsupported shape";
+  }
+  return "unknown status";
+}
+
+extern "C" const char* ssd_last_error(void) { return g_last_error.c_str(); }
+
+extern "C" ssd_status ssd_set_gemm_path(int32_t path) {
+  if (path < 0 || path > 2) return fail(SSD_E_INVALID_ARG, "gemm path must be 0, 1 or 2");
+  g_gemm_path = path;
+  return SSD_OK;
+}
+
+extern "C" ssd_status ssd_validate_tree(const int32_t* tokens, const int32_t* parent_idx, int32_t n, int32_t vocab,
+                                        int32_t* max_depth) {
+  if (!tokens || !parent_idx) return fail(SSD_E_INVALID_ARG, "null tree array");
+  if (n <= 0) return fail(SSD_E_INVALID_ARG, "n_nodes must be positive");
+  if (parent_idx[0] != -1) return fail(SSD_E_INVALID_TREE, "parent_idx[0] must be -1");
+  std::vector<int32_t> depth(n, 0);
+  int32_t md = 0;
+  for (int32_t i = 0; i < n; ++i) {
+    if (tokens[i] < 0 || tokens[i] >= vocab)
+      return fail(SSD_E_INVALID_ARG, "token " + std::to_string(i) + " out of range");
+    if (i > 0) {
+      const int32_t p = parent_idx[i];
+      if (p < 0 || p >= i) return fail(SSD_E_INVALID_TREE, "parent_idx[" + std::to_string(i) + "] not in [0, i)");
+      depth[i] = depth[p] + 1;
+      md = std::max(md, depth[i]);
+    }
+  }
+  if (max_depth) *max_depth = md;
+  return SSD_OK;
+}
+
+extern "C" ssd_status ssd_tree_prep(const int32_t* parent_idx, int32_t n, int32_t* depth, uint64_t* anc) {
+  if (!parent_idx || n <= 0) return fail(SSD_E_INVALID_ARG, "bad tree arguments");
+  if (parent_idx[0] != -1) return fail(SSD_E_INVALID_TREE, "parent_idx[0] must be -1");
+  for (int32_t i = 1; i < n; ++i)
+    if (parent_idx[i] < 0 || parent_idx[i] >= i) return fail(SSD_E_INVALID_TREE, "parent_idx not in [0, i)");
+  const int W = (n + 63) / 64;
+  std::vector<int32_t> dep(n, 0);
+  for (int32_t i = 0; i < n; ++i) {
+    uint64_t* row = anc ? anc + (size_t)i * W : nullptr;
+    if (i == 0) {
+      if (row) std::fill(row, row + W, 0ull);
+    } else {
+      const int32_t p = parent_idx[i];
+      dep[i] = dep[p] + 1;
+      if (row) std::copy(anc + (size_t)p * W, anc + (size_t)p * W + W, row);  // ancestors of the parent
+    }
+    if (row) row[i >> 6] |= 1ull << (i & 63);
+  }
+  if (depth) std::copy(dep.begin(), dep.end(), depth);
+  return SSD_OK;
+}
+
+// ------------------------------------------------------------------ model
+
+static bool cfg_ok(const ssd_config* c, std::string* why) {
+  if (!c) return *why = "null config", false;
+  if (c->n_layer <= 0 || c->d_model <= 0 || c->n_head <= 0 || c->d_mlp <= 0 || c->vocab <= 0 || c->n_pos <= 0)
+    return *why = "config sizes must be positive", false;
+  if (c->d_model % c->n_head) return *why = "d_model must divide by n_head", false;
+  if (c->dtype != SSD_F32 && c->dtype != SSD_BF16) return *why = "dtype must be SSD_F32 or SSD_BF16", false;
+  return true;
+}
+
+extern "C" ssd_status ssd_model_create(const ssd_config* cfg, const ssd_weights* w, void* stream, ssd_model** out) {
+  std::string why;
+  if (!out || !w) return fail(SSD_E_INVALID_ARG, "null argument");
+  if (!cfg_ok(cfg, &why)) return fail(SSD_E_INVALID_ARG, why);
+  const int d = cfg->d_model, dh = d / cfg->n_head, L = cfg->n_layer;
+  if (d % 32 || cfg->d_mlp % 32 || (dh != 32 && dh != 64))
+    return fail(SSD_E_UNSUPPORTED, "need d_model % 32 == 0, d_mlp % 32 == 0, head_dim 32 or 64");
+  if (!w->wte || !w->wpe || !w->lnf_g || !w->lnf_b) return fail(SSD_E_INVALID_ARG, "null embedding / ln_f pointer");
+  const void* const* per[12] = {w->ln1_g, w->ln1_b, w->w_qkv, w->b_qkv, w->w_o, w->b_o,
+                                w->ln2_g, w->ln2_b, w->w_fc, w->b_fc, w->w_pr, w->b_pr};
+  for (auto a : per) {
+    if (!a) return fail(SSD_E_INVALID_ARG, "null per-layer pointer array");
+    for (int l = 0; l < L; ++l)
+      if (!a[l]) return fail(SSD_E_INVALID_ARG, "null per-layer parameter pointer");
+  }
+  ssd_model* m = new ssd_model();
+  m->cfg = *cfg;
+  m->dh = dh;
+  m->f32 = cfg->dtype == SSD_F32;
+  m->wte = w->wte;
+  m->wpe = w->wpe;
+  m->lnf_g = w->lnf_g;
+  m->lnf_b = w->lnf_b;
+  std::vector<const void*>* dst[12] = {&m->ln1_g, &m->ln1_b, &m->w_qkv, &m->b_qkv, &m->w_o, &m->b_o,
+                                       &m->ln2_g, &m->ln2_b, &m->w_fc, &m->b_fc, &m->w_pr, &m->b_pr};
+  for (int i = 0; i < 12; ++i) dst[i]->assign(per[i], per[i] + L);
+  if (!m->f32) {
+    const int M = cfg->d_mlp, V = cfg->vocab;
+    const size_t b_qkv = packed_bytes(3 * d, d), b_o = packed_bytes(d, d), b_fc = packed_bytes(M, d),
+                 b_pr = packed_bytes(d, M), b_head = packed_bytes(V, d);
+    const size_t total = (b_qkv + b_o + b_fc + b_pr) * L + b_head;
+    hipError_t e = hipMalloc(&m->pack, total);
+    if (e != hipSuccess) {
+      delete m;
+      return fail(SSD_E_DEVICE, std::string("hipMalloc(packed weights): ") + hipGetErrorString(e));
+    }
+    hipStream_t s = (hipStream_t)stream;
+    char* p = (char*)m->pack;
+    auto pack = [&](const void* src, int rows, int cols, size_t bytes) -> const void* {
+      if (e == hipSuccess) e = launch_pack_bf16((const uint16_t*)src, rows, cols, p, s);
+      const void* r = p;
+      p += bytes;
+      return r;
+    };
+    for (int l = 0; l < L; ++l) {
+      m->p_qkv.push_back(pack(m->w_qkv[l], 3 * d, d, b_qkv));
+      m->p_o.push_back(pack(m->w_o[l], d, d, b_o));
+      m->p_fc.push_back(pack(m->w_fc[l], M, d, b_fc));
+      m->p_pr.push_back(pack(m->w_pr[l], d, M, b_pr));
+    }
+    m->p_head = pack(m->wte, V, d, b_head);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) {
+      (void)hipFree(m->pack);
+      delete m;
+      return fail(SSD_E_DEVICE, std::string("weight packing: ") + hipGetErrorString(e));
+    }
+  }
+  *out = m;
+  return SSD_OK;
+}
+
+extern "C" void ssd_model_destroy(ssd_model* m) {
+  if (!m) return;
+  if (m->pack) (void)hipFree(m->pack);
+  delete m;
+}
+
+// ------------------------------------------------------------------ session
+
+extern "C" ssd_status ssd_kv_bytes(const ssd_config* cfg, int32_t max_ctx, int32_t max_nodes, size_t* cache_bytes,
+                                   size_t* tree_bytes) {
+  std::string why;
+  if (!cfg_ok(cfg, &why)) return fail(SSD_E_INVALID_ARG, why);
+  if (max_ctx < 0 || max_nodes <= 0) return fail(SSD_E_INVALID_ARG, "bad sizes");
+  const size_t es = cfg->dtype == SSD_F32 ? 4 : 2;
+  const size_t per_row = (size_t)cfg->n_layer * cfg->d_model * es;  // all heads of all layers
+  if (cache_bytes) *cache_bytes = per_row * max_ctx;
+  if (tree_bytes) *tree_bytes = per_row * max_nodes;
+  return SSD_OK;
+}
+
+static size_t stage_bytes(int max_nodes) {
+  const int W = (max_nodes + 63) / 64;
+  return (size_t)4 * max_nodes * 4 + (size_t)max_nodes * W * 8;
+}
+
+extern "C" ssd_status ssd_kv_create(const ssd_model* m, int32_t max_ctx, int32_t max_nodes, void* k_cache,
+                                    void* v_cache, void* k_tree, void* v_tree, ssd_kv** out) {
+  if (!m || !out || !k_tree || !v_tree) return fail(SSD_E_INVALID_ARG, "null argument");
+  if (max_ctx < 0 || max_nodes <= 0) return fail(SSD_E_INVALID_ARG, "bad sizes");
+  if (max_ctx > 0 && (!k_cache || !v_cache)) return fail(SSD_E_INVALID_ARG, "null cache with max_ctx > 0");
+  if (max_nodes > kMaxNodes) return fail(SSD_E_CAPACITY, "max_nodes above 1024");
+  const ssd_config& c = m->cfg;
+  ssd_kv* kv = new ssd_kv();
+  kv->m = m;
+  kv->max_ctx = max_ctx;
+  kv->max_nodes = max_nodes;
+  kv->kc = k_cache;
+  kv->vc = v_cache;
+  kv->kt = k_tree;
+  kv->vt = v_tree;
+  // GEMMs read activation rows in power-of-two node tiles (16..256), or in
+  // groups of 256 beyond that, so pad the row count to cover the last tile.
+  if (max_nodes <= 256) {
+    int p2 = 16;
+    while (p2 < max_nodes) p2 *= 2;
+    kv->npad = p2;
+  } else {
+    kv->npad = round_up(max_nodes, 256);
+  }
+  kv->W = (max_nodes + 63) / 64;
+  kv->ns_max = (max_ctx + 63) / 64 + (max_nodes + 63) / 64;
+  const size_t es = m->f32 ? 4 : 2;
+  const int d = c.d_model, M = c.d_mlp, V = c.vocab;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t o = off;
+    off += (bytes + 255) / 256 * 256;
+    return o;
+  };
+  const size_t o_x = take((size_t)max_nodes * d * 4), o_q = take((size_t)max_nodes * d * 4);
+  // bf16 models keep every GEMM input as a hi plane and a lo plane
+  const size_t planes = m->f32 ? 1 : 2;
+  const size_t o_a = take(planes * kv->npad * d * es), o_o = take(planes * kv->npad * d * es);
+  const size_t o_f = take(planes * kv->npad * M * es);
+  const size_t o_part = take((size_t)c.n_head * kv->ns_max * max_nodes * (m->dh + 2) * 4);
+  const size_t o_tree = take(stage_bytes(max_nodes));
+  const size_t o_at = take((size_t)3 * max_nodes * 4), o_am = take((size_t)max_nodes * 4);
+  const size_t o_r = take((size_t)V * 8), o_p = take((size_t)V * 8), o_qq = take((size_t)V * 8);
+  const size_t o_err = take(256);
+  hipError_t e = hipMalloc(&kv->ws, off);
+  if (e == hipSuccess) e = hipMemset(kv->ws, 0, off);
+  if (e != hipSuccess) {
+    if (kv->ws) (void)hipFree(kv->ws);
+    delete kv;
+    return fail(SSD_E_DEVICE, std::string("workspace allocation: ") + hipGetErrorString(e));
+  }
+  char* b = (char*)kv->ws;
+  kv->x = (float*)(b + o_x);
+  kv->q = (float*)(b + o_q);
+  kv->act_a = b + o_a;
+  kv->act_o = b + o_o;
+  kv->act_f = b + o_f;
+  kv->part = (float*)(b + o_part);
+  kv->d_tree = (int*)(b + o_tree);
+  kv->d_accept_tree = (int*)(b + o_at);
+  kv->d_argmax = (int*)(b + o_am);
+  kv->d_r = (double*)(b + o_r);
+  kv->d_p = (double*)(b + o_p);
+  kv->d_qq = (double*)(b + o_qq);
+  kv->d_err = (unsigned*)(b + o_err);
+  kv->slot_bytes = (stage_bytes(max_nodes) + 255) / 256 * 256;
+  e = hipHostMalloc((void**)&kv->pinned, kv->slot_bytes * kStageSlots, hipHostMallocDefault);
+  for (int i = 0; i < kStageSlots && e == hipSuccess; ++i) e = hipEventCreateWithFlags(&kv->slot_ev[i], hipEventDisableTiming);
+  if (e != hipSuccess) {
+    ssd_kv_destroy(kv);
+    return fail(SSD_E_DEVICE, std::string("staging allocation: ") + hipGetErrorString(e));
+  }
+  *out = kv;
+  return SSD_OK;
+}
+
+extern "C" void ssd_kv_destroy(ssd_kv* kv) {
+  if (!kv) return;
+  for (int i = 0; i < kStageSlots; ++i)
+    if (kv->slot_ev[i]) {
+      (void)hipEventSynchronize(kv->slot_ev[i]);
+      (void)hipEventDestroy(kv->slot_ev[i]);
+    }
+  if (kv->pinned) (void)hipHostFree(kv->pinned);
+  if (kv->ws) (void)hipFree(kv->ws);
+  delete kv;
+}
+
+// Picks a pinned staging slot that no pending copy still reads.  Inside a
+// stream capture the caller supplies its own buffer instead.
+static ssd_status acquire_slot(ssd_kv* kv, char** host, int* slot) {
+  const int i = kv->next_slot;
+  kv->next_slot = (kv->next_slot + 1) % kStageSlots;
+  if (kv->slot_used[i]) HIP_TRY(hipEventSynchronize(kv->slot_ev[i]));
+  *host = kv->pinned + (size_t)i * kv->slot_bytes;
+  *slot = i;
+  return SSD_OK;
+}
+
+static ssd_status release_slot(ssd_kv* kv, int slot, hipStream_t s) {
+  if (slot < 0) return SSD_OK;
+  HIP_TRY(hipEventRecord(kv->slot_ev[slot], s));
+  kv->slot_used[slot] = true;
+  return SSD_OK;
+}
+
+// ------------------------------------------------------------------ verification pass
+
+static ssd_status check_verify_args(const ssd_model* m, const ssd_kv* kv, int32_t P, const int32_t* tokens,
+                                    const int32_t* parents, int32_t n, const float* logits, int32_t* max_depth) {
+  if (!m || !kv || !tokens || !parents || !logits) return fail(SSD_E_INVALID_ARG, "null argument");
+  if (kv->m != m && kv->m->cfg.n_layer < m->cfg.n_layer) return fail(SSD_E_INVALID_ARG, "session/model mismatch");
+  if (n <= 0) return fail(SSD_E_INVALID_ARG, "n_nodes must be positive");
+  if (P < 0) return fail(SSD_E_INVALID_ARG, "negative prefix_len");
+  if (n > kv->max_nodes) return fail(SSD_E_CAPACITY, "n_nodes above the session's max_nodes");
+  if (P > kv->max_ctx) return fail(SSD_E_CAPACITY, "prefix_len above the session's max_ctx");
+  ssd_status st = ssd_validate_tree(tokens, parents, n, m->cfg.vocab, max_depth);
+  if (st != SSD_OK) return st;
+  if (P + *max_depth >= m->cfg.n_pos) return fail(SSD_E_CAPACITY, "prefix_len + tree depth past the position table");
+  return SSD_OK;
+}
+
+// Fills a staging buffer: tokens, positions, depths, parents, ancestor masks.
+static void fill_stage(char* host, int P, const int32_t* tokens, const int32_t* parents, int n, int max_nodes) {
+  int32_t* t = (int32_t*)host;
+  int32_t* pos = t + max_nodes;
+  int32_t* dep = pos + max_nodes;
+  int32_t* par = dep + max_nodes;
+  uint64_t* anc = (uint64_t*)(par + max_nodes);
+  ssd_tree_prep(parents, n, dep, anc);  // validated by the caller
+  for (int i = 0; i < n; ++i) {
+    t[i] = tokens[i];
+    pos[i] = P + dep[i];
+    par[i] = parents[i];
+  }
+}
+
+// One weight GEMM of the pass over n nodes: fp32 models use the plain
+// kernel; bf16 models the vector-ALU kernel for small node counts (or when
+// pinned) and the matrix-core kernel otherwise, in node groups.
+static hipError_t run_gemm(const ssd_model* m, int n, int kind, const void* Wraw, const void* Wp, int rows, int K,
+                           const void* act, int lda, size_t plane, const Epi& ep, hipStream_t s) {
+  if (m->f32) return launch_gemm_f32(kind, (const float*)Wraw, rows, K, (const float*)act, lda, ep, s);
+  const int path = g_gemm_path == 0 ? (n <= kVecMaxNodes ? 1 : 2) : g_gemm_path;
+  const int group = path == 1 ? 16 : 256;
+  for (int n0 = 0; n0 < n; n0 += group) {
+    Epi e2 = ep;
+    e2.node0 = n0;
+    e2.N = std::min(group, n - n0);
+    const uint16_t* a = (const uint16_t*)act + (size_t)n0 * lda;
+    hipError_t r = path == 1 ? launch_gemm_vec(kind, Wp, rows, K, a, lda, plane, e2, s)
+                             : launch_gemm_mfma(kind, Wp, rows, K, a, lda, plane, e2, s);
+    if (r != hipSuccess) return r;
+  }
+  return hipSuccess;
+}
+
+static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int32_t n, const char* stage_host,
+                                 float* logits, hipStream_t s) {
+  const ssd_config& c = m->cfg;
+  const int d = c.d_model, H = c.n_head, DH = m->dh, M = c.d_mlp, V = c.vocab, L = c.n_layer;
+  const int maxn = kv->max_nodes, W = (n + 63) / 64;
+  const int f32 = m->f32 ? 1 : 0;
+  const size_t es = f32 ? 4 : 2;
+  // device copy of the staged tree; anc rows are packed with W = ceil(n/64)
+  const size_t head_bytes = (size_t)4 * maxn * 4;
+  HIP_TRY(hipMemcpyAsync(kv->d_tree, stage_host, head_bytes + (size_t)n * W * 8, hipMemcpyHostToDevice, s));
+  const int* d_tok = kv->d_tree;
+  const int* d_pos = kv->d_tree + maxn;
+  HIP_TRY(launch_embed(f32, m->wte, m->wpe, d_tok, d_pos, n, d, kv->x, s));
+
+  const int S = (P + 63) / 64, T = (n + 63) / 64, NS = S + T;
+  // element distance between the hi and lo planes of each activation buffer
+  const size_t pl_d = (size_t)kv->npad * d, pl_m = (size_t)kv->npad * M;
+  auto gemm = [&](int kind, const void* Wraw, const void* Wp, int rows, int K, const void* act, int lda,
+                  const Epi& ep) -> hipError_t {
+    return run_gemm(m, n, kind, Wraw, Wp, rows, K, act, lda, lda == d ? pl_d : pl_m, ep, s);
+  };
+
+  const size_t kv_layer = (size_t)H * DH;  // elements per row across heads
+  for (int l = 0; l < L; ++l) {
+    HIP_TRY(launch_ln(f32, kv->x, n, d, m->ln1_g[l], m->ln1_b[l], c.ln_eps, kv->act_a, d, pl_d, s));
+    Epi e{};
+    e.bias = m->b_qkv[l];
+    e.N = n;
+    e.M = 3 * d;
+    e.q = kv->q;
+    e.kt = (char*)kv->kt + (size_t)l * kv_layer * maxn * es;
+    e.vt = (char*)kv->vt + (size_t)l * kv_layer * maxn * es;
+    e.d = d;
+    e.H = H;
+    e.DH = DH;
+    e.max_nodes = maxn;
+    HIP_TRY(gemm(EPI_QKV, m->w_qkv[l], f32 ? nullptr : m->p_qkv[l], 3 * d, d, kv->act_a, d, e));
+
+    AttnArgs a{};
+    a.q = kv->q;
+    a.kc = kv->kc ? (const char*)kv->kc + (size_t)l * kv_layer * kv->max_ctx * es : nullptr;
+    a.vc = kv->vc ? (const char*)kv->vc + (size_t)l * kv_layer * kv->max_ctx * es : nullptr;
+    a.kt = e.kt;
+    a.vt = e.vt;
+    a.anc = (const uint64_t*)((const char*)kv->d_tree + head_bytes);
+    a.part = kv->part;
+    a.N = n;
+    a.P = P;
+    a.d = d;
+    a.H = H;
+    a.max_ctx = kv->max_ctx;
+    a.max_nodes = maxn;
+    a.W = W;
+    a.S = S;
+    a.NS = NS;
+    a.scale = 1.0f / std::sqrt((float)DH);
+    HIP_TRY(launch_attn(f32, DH, a, s));
+    HIP_TRY(launch_attn_combine(f32, DH, kv->part, NS, n, H, d, kv->act_o, d, pl_d, s));
+
+    Epi eo{};
+    eo.bias = m->b_o[l];
+    eo.N = n;
+    eo.M = d;
+    eo.d = d;
+    eo.x = kv->x;
+    HIP_TRY(gemm(EPI_RESID, m->w_o[l], f32 ? nullptr : m->p_o[l], d, d, kv->act_o, d, eo));
+
+    HIP_TRY(launch_ln(f32, kv->x, n, d, m->ln2_g[l], m->ln2_b[l], c.ln_eps, kv->act_a, d, pl_d, s));
+    Epi ef{};
+    ef.bias = m->b_fc[l];
+    ef.N = n;
+    ef.M = M;
+    ef.d = d;
+    ef.out = kv->act_f;
+    ef.ldo = M;
+    ef.out_plane = (long long)pl_m;
+    HIP_TRY(gemm(EPI_GELU, m->w_fc[l], f32 ? nullptr : m->p_fc[l], M, d, kv->act_a, d, ef));
+
+    Epi ep{};
+    ep.bias = m->b_pr[l];
+    ep.N = n;
+    ep.M = d;
+    ep.d = d;
+    ep.x = kv->x;
+    HIP_TRY(gemm(EPI_RESID, m->w_pr[l], f32 ? nullptr : m->p_pr[l], d, M, kv->act_f, M, ep));
+  }
+  HIP_TRY(launch_ln(f32, kv->x, n, d, m->lnf_g, m->lnf_b, c.ln_eps, kv->act_a, d, pl_d, s));
+  Epi eh{};
+  eh.bias = nullptr;
+  eh.N = n;
+  eh.M = V;
+  eh.d = d;
+  eh.logits = logits;
+  eh.ldl = V;
+  HIP_TRY(gemm(EPI_LOGITS, m->wte, f32 ? nullptr : m->p_head, V, d, kv->act_a, d, eh));
+  return SSD_OK;
+}
+
+extern "C" ssd_status ssd_tree_verify(const ssd_model* m, ssd_kv* kv, int32_t prefix_len, const int32_t* tree_tokens,
+                                      const int32_t* parent_idx, int32_t n_nodes, float* logits, void* stream) {
+  int32_t md = 0;
+  ssd_status st = check_verify_args(m, kv, prefix_len, tree_tokens, parent_idx, n_nodes, logits, &md);
+  if (st != SSD_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  char* host = nullptr;
+  int slot = -1;
+  st = acquire_slot(kv, &host, &slot);
+  if (st != SSD_OK) return st;
+  fill_stage(host, prefix_len, tree_tokens, parent_idx, n_nodes, kv->max_nodes);
+  st = enqueue_verify(m, kv, prefix_len, n_nodes, host, logits, s);
+  ssd_status st2 = release_slot(kv, slot, s);
+  return st != SSD_OK ? st : st2;
+}
+
+extern "C" ssd_status ssd_graph_capture_verify(const ssd_model* m, ssd_kv* kv, int32_t prefix_len,
+                                               const int32_t* tree_tokens, const int32_t* parent_idx,
+                                               int32_t n_nodes, float* logits, void* stream, ssd_graph** out) {
+  if (!out) return fail(SSD_E_INVALID_ARG, "null output");
+  int32_t md = 0;
+  ssd_status st = check_verify_args(m, kv, prefix_len, tree_tokens, parent_idx, n_nodes, logits, &md);
+  if (st != SSD_OK) return st;
+  ssd_graph* g = new ssd_graph();
+  hipError_t e = hipHostMalloc((void**)&g->pinned, kv->slot_bytes, hipHostMallocDefault);
+  if (e != hipSuccess) {
+    delete g;
+    return fail(SSD_E_DEVICE, std::string("hipHostMalloc: ") + hipGetErrorString(e));
+  }
+  fill_stage(g->pinned, prefix_len, tree_tokens, parent_idx, n_nodes, kv->max_nodes);
+  // capture on a private stream (the legacy null stream cannot be captured);
+  // the graph is later launched on the caller's stream
+  (void)stream;
+  hipStream_t cs = nullptr;
+  e = hipStreamCreateWithFlags(&cs, hipStreamNonBlocking);
+  if (e == hipSuccess) e = hipStreamBeginCapture(cs, hipStreamCaptureModeThreadLocal);
+  if (e != hipSuccess) {
+    if (cs) (void)hipStreamDestroy(cs);
+    ssd_graph_destroy(g);
+    return fail(SSD_E_DEVICE, std::string("hipStreamBeginCapture: ") + hipGetErrorString(e));
+  }
+  st = enqueue_verify(m, kv, prefix_len, n_nodes, g->pinned, logits, cs);
+  hipGraph_t graph = nullptr;
+  e = hipStreamEndCapture(cs, &graph);
+  (void)hipStreamDestroy(cs);
+  if (st != SSD_OK || e != hipSuccess) {
+    if (graph) (void)hipGraphDestroy(graph);
+    ssd_graph_destroy(g);
+    return st != SSD_OK ? st : fail(SSD_E_DEVICE, std::string("hipStreamEndCapture: ") + hipGetErrorString(e));
+  }
+  g->graph = graph;
+  e = hipGraphInstantiate(&g->exec, graph, nullptr, nullptr, 0);
+  if (e != hipSuccess) {
+    ssd_graph_destroy(g);
+    return fail(SSD_E_DEVICE, std::string("hipGraphInstantiate: ") + hipGetErrorString(e));
+  }
+  *out = g;
+  return SSD_OK;
+}
+
+extern "C" ssd_status ssd_graph_launch(ssd_graph* g, void* stream) {
+  if (!g || !g->exec) return fail(SSD_E_INVALID_ARG, "null graph");
+  HIP_TRY(hipGraphLaunch(g->exec, (hipStream_t)stream));
+  return SSD_OK;
+}
+
+extern "C" void ssd_graph_destroy(ssd_graph* g) {
+  if (!g) return;
+  if (g->exec) (void)hipGraphExecDestroy(g->exec);
+  if (g->graph) (void)hipGraphDestroy(g->graph);
+  if (g->pinned) (void)hipHostFree(g->pinned);
+  delete g;
+}
+
+extern "C" ssd_status ssd_launch_gemm(const ssd_model* m, ssd_kv* kv, int32_t which, int32_t layer, int32_t n_nodes,
+                                      void* stream) {
+  if (!m || !kv) return fail(SSD_E_INVALID_ARG, "null argument");
+  const ssd_config& c = m->cfg;
+  if (which < 0 || which > 4 || layer < 0 || layer >= c.n_layer) return fail(SSD_E_INVALID_ARG, "bad matrix id");
+  if (n_nodes <= 0 || n_nodes > kv->max_nodes) return fail(SSD_E_CAPACITY, "n_nodes outside the session");
+  const int d = c.d_model, M = c.d_mlp, es = m->f32 ? 4 : 2;
+  // outputs land in the session's own buffers: q / tree scratch, x, act_f, or
+  // the attention-partials buffer reused as a logits sink
+  Epi e{};
+  e.N = n_nodes;
+  e.d = d;
+  e.H = c.n_head;
+  e.DH = m->dh;
+  e.max_nodes = kv->max_nodes;
+  const void *Wraw = nullptr, *Wp = nullptr, *act = kv->act_a;
+  int rows = d, K = d, lda = d, kind = EPI_RESID;
+  switch (which) {
+    case 0:
+      kind = EPI_QKV; rows = 3 * d; Wraw = m->w_qkv[layer]; e.bias = m->b_qkv[layer]; e.q = kv->q;
+      e.kt = (char*)kv->kt + (size_t)layer * c.n_head * m->dh * kv->max_nodes * es;
+      e.vt = (char*)kv->vt + (size_t)layer * c.n_head * m->dh * kv->max_nodes * es;
+      if (!m->f32) Wp = m->p_qkv[layer];
+      break;
+    case 1:
+      Wraw = m->w_o[layer]; e.bias = m->b_o[layer]; e.x = kv->x; act = kv->act_o;
+      if (!m->f32) Wp = m->p_o[layer];
+      break;
+    case 2:
+      kind = EPI_GELU; rows = M; Wraw = m->w_fc[layer]; e.bias = m->b_fc[layer]; e.out = kv->act_f; e.ldo = M;
+      e.out_plane = (long long)kv->npad * M;
+      if (!m->f32) Wp = m->p_fc[layer];
+      break;
+    case 3:
+      K = M; lda = M; Wraw = m->w_pr[layer]; e.bias = m->b_pr[layer]; e.x = kv->x; act = kv->act_f;
+      if (!m->f32) Wp = m->p_pr[layer];
+      break;
+    default: {
+      kind = EPI_LOGITS; rows = c.vocab; Wraw = m->wte; Wp = m->p_head;
+      const size_t need = (size_t)n_nodes * c.vocab * 4;
+      const size_t have = (size_t)c.n_head * kv->ns_max * kv->max_nodes * (m->dh + 2) * 4;
+      if (need > have) return fail(SSD_E_CAPACITY, "logits sink too small for this node count");
+      e.logits = kv->part;
+      e.ldl = c.vocab;
+      break;
+    }
+  }
+  e.M = rows;
+  const size_t plane = (size_t)kv->npad * lda;
+  HIP_TRY(run_gemm(m, n_nodes, kind, Wraw, Wp, rows, K, act, lda, plane, e, (hipStream_t)stream));
+  return SSD_OK;
+}
+
+// ------------------------------------------------------------------ accept
+
+extern "C" ssd_status ssd_tree_accept(ssd_kv* kv, const ssd_tree* tree, const float* draft_probs,
+                                      const float* oracle_logits, uint64_t rng_seed, int32_t* accepted_path,
+                                      int32_t* path_len, int32_t* next_token, void* stream) {
+  if (!kv || !tree || !oracle_logits || !accepted_path || !path_len || !next_token)
+    return fail(SSD_E_INVALID_ARG, "null argument");
+  const int n = tree->n_nodes, V = tree->vocab;
+  if (n <= 0 || V <= 0) return fail(SSD_E_INVALID_ARG, "n_nodes and vocab must be positive");
+  if (n > kv->max_nodes) return fail(SSD_E_CAPACITY, "n_nodes above the session's max_nodes");
+  if (V > kv->m->cfg.vocab) return fail(SSD_E_CAPACITY, "vocab above the model's vocab");
+  const bool greedy = tree->mode == SSD_ACCEPT_GREEDY;
+  if (!greedy && tree->mode != SSD_ACCEPT_SAMPLE_WOR && tree->mode != SSD_ACCEPT_SAMPLE_IID)
+    return fail(SSD_E_INVALID_ARG, "unknown accept mode");
+  if (greedy && draft_probs) return fail(SSD_E_INVALID_ARG, "draft_probs must be NULL for greedy acceptance");
+  if (!greedy && !draft_probs) return fail(SSD_E_INVALID_ARG, "draft_probs required for sampling");
+  if (!greedy && !(tree->temperature > 0.f)) return fail(SSD_E_INVALID_ARG, "temperature must be positive");
+  int32_t md = 0;
+  ssd_status st = ssd_validate_tree(tree->tokens, tree->parent_idx, n, V, &md);
+  if (st != SSD_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  char* host = nullptr;
+  int slot = -1;
+  st = acquire_slot(kv, &host, &slot);
+  if (st != SSD_OK) return st;
+  int32_t* t = (int32_t*)host;
+  int32_t* par = t + n;
+  int32_t* dep = par + n;
+  for (int i = 0; i < n; ++i) {
+    t[i] = tree->tokens[i];
+    par[i] = tree->parent_idx[i];
+    dep[i] = i == 0 ? 0 : dep[par[i]] + 1;
+  }
+  int* dt = kv->d_accept_tree;
+  HIP_TRY(hipMemcpyAsync(dt, host, (size_t)3 * n * 4, hipMemcpyHostToDevice, s));
+  if (greedy) {
+    HIP_TRY(launch_argmax(oracle_logits, n, V, kv->d_argmax, s));
+    HIP_TRY(launch_greedy_walk(dt, dt + n, dt + 2 * n, n, kv->d_argmax, accepted_path, path_len, next_token, s));
+  } else {
+    HIP_TRY(launch_sample_accept(dt, dt + n, n, V, oracle_logits, draft_probs, (double)tree->temperature, rng_seed,
+                                 tree->mode == SSD_ACCEPT_SAMPLE_WOR ? 1 : 0, kv->d_r, kv->d_p, kv->d_qq,
+                                 accepted_path, path_len, next_token, s));
+  }
+  return release_slot(kv, slot, s);
+}
+
+// ------------------------------------------------------------------ commit
+
+extern "C" ssd_status ssd_kv_commit(ssd_kv* kv, int32_t prefix_len, const int32_t* accepted_path,
+                                    const int32_t* path_len, void* stream) {
+  if (!kv || !accepted_path || !path_len) return fail(SSD_E_INVALID_ARG, "null argument");
+  if (prefix_len < 0 || prefix_len > kv->max_ctx) return fail(SSD_E_CAPACITY, "prefix_len outside the cache");
+  if (!kv->kc) return fail(SSD_E_CAPACITY, "session has no cache");
+  const ssd_model* m = kv->m;
+  HIP_TRY(launch_commit(m->f32 ? 1 : 0, kv->kc, kv->vc, kv->kt, kv->vt, m->cfg.n_layer * m->cfg.n_head, kv->max_ctx,
+                        kv->max_nodes, m->dh, prefix_len, accepted_path, path_len, kv->d_err, (hipStream_t)stream));
+  return SSD_OK;
+}
+
+extern "C" ssd_status ssd_kv_error_count(ssd_kv* kv, void* stream, uint32_t* count) {
+  if (!kv || !count) return fail(SSD_E_INVALID_ARG, "null argument");
+  unsigned h = 0;
+  HIP_TRY(hipMemcpyAsync(&h, kv->d_err, 4, hipMemcpyDeviceToHost, (hipStream_t)stream));
+  HIP_TRY(hipStreamSynchronize((hipStream_t)stream));
+  *count = h;
+  return SSD_OK;
+}

@@ -1,0 +1,139 @@
+"""Full-size parity on the GPT-2-L shape (36 x 1280, 20 heads, MLP 5120,
+vocab 50257, bf16), in the launch configuration the benchmark times (the
+captured graph of the whole pass).
+
+- 32-node tree [4,2,2,1] over a 512-token prefix: every logit against the
+  oracle (2e-2 max-abs); accept bit-exact on the GPU's logits; per-node
+  argmax equal to the oracle's except at precision ties.
+- 256-node tree [8,4,2,2,1,...] over a 2048-token prefix: the oracle
+  recomputes one root-to-leaf path node by node (a node's logits depend only
+  on its root path); sampling accept bit-exact on the GPU's logits.
+- node counts 1, 17 and 64 on the 512-token prefix: sampled root paths.
+The prefix caches are synthetic N(0, 0.7) K/V (a prefill would not change
+what the pass computes from them)."""
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2308_04623_amd import workloads as W
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+TOL = 2e-2
+THREADS = int(os.environ.get("OMP_NUM_THREADS", "0") or 0)
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as t
+    assert t.cuda.is_available()
+    return t
+
+
+@pytest.fixture(scope="module")
+def big(torch):
+    from paper_2308_04623_amd import ssd
+    cfg = W.GPT2L_LONG
+    print("generating GPT-2-L weights", flush=True)
+    w = W.make_weights(cfg, 0)
+    om = oracle.Model(cfg, w)
+    m = ssd.Model(cfg, w)
+    return cfg, w, om, m, ssd
+
+
+def _root_path(par, i):
+    out = []
+    while i != -1:
+        out.append(int(i))
+        i = int(par[i])
+    return out[::-1]
+
+
+def _session(big, torch, P, max_ctx, max_nodes, seed):
+    cfg, w, om, m, ssd = big
+    kc, vc = W.random_kv_cache(cfg, max_ctx, P, seed=seed)
+    s = ssd.Session(m, max_ctx, max_nodes, ssd.to_device(kc, cfg), ssd.to_device(vc, cfg))
+    return s, kc, vc
+
+
+def _graph_logits(s, torch, P, toks, par):
+    lg = torch.zeros((len(par), s.model.cfg.vocab), dtype=torch.float32, device="cuda")
+    g = s.capture_verify(P, toks, par, lg)
+    g.launch()
+    torch.cuda.synchronize()
+    out = lg.cpu().numpy()
+    g.close()
+    return out
+
+
+def _oracle_path_rows(om, kc, vc, P, toks, par, node):
+    """The oracle's logits for every node on node's root path, computed as a
+    chain (a node's logits depend only on its root path)."""
+    path = _root_path(par, node)
+    kt, vt = om.kv(len(path)), om.kv(len(path))
+    return path, oracle.tree_verify(om, kc, vc, P, toks[path], W.chain_tree(len(path)), kt, vt, THREADS)
+
+
+def test_c2_full_tree(big, torch):
+    cfg, w, om, m, ssd = big
+    P = 512
+    s, kc, vc = _session(big, torch, P, 1024, 64, seed=3)
+    par = W.branching_tree([4, 2, 2, 1], 32)
+    toks = W.tree_tokens(par, cfg.vocab, seed=2)
+    got = _graph_logits(s, torch, P, toks, par)
+    print("oracle verify (32 nodes)", flush=True)
+    ref = oracle.tree_verify(om, kc, vc, P, toks, par, om.kv(64), om.kv(64), THREADS)
+    err = np.abs(got - ref)
+    print(f"C2 max|d| {err.max():.3e} mean {err.mean():.3e}", flush=True)
+    assert err.max() < TOL
+    # argmax agreement, except where the oracle's top-2 gap is within the error
+    ga, ra = got.argmax(1), ref.argmax(1)
+    srt = np.sort(ref, 1)
+    gap = srt[:, -1] - srt[:, -2]
+    for i in np.flatnonzero(ga != ra):
+        assert gap[i] <= 2 * err[i].max(), (i, gap[i])
+    # greedy accept on the GPU's logits is bit-exact
+    dlg = torch.from_numpy(got).cuda()
+    path, plen, nxt = s.accept(toks, par, dlg)
+    op, on = oracle.tree_accept(oracle.GREEDY, toks, par, got)
+    assert path[:int(plen.item())].cpu().numpy().tolist() == op.tolist() and int(nxt.item()) == on
+
+
+@pytest.mark.parametrize("n", [1, 17, 64])
+def test_sampled_paths_prefix512(big, torch, n):
+    cfg, w, om, m, ssd = big
+    P = 512
+    s, kc, vc = _session(big, torch, P, 1024, 128, seed=4)
+    toks, par = W.best_first_tree(n, seed=3, vocab=cfg.vocab)
+    toks[0] = 17
+    got = _graph_logits(s, torch, P, toks, par)
+    leaf = n - 1
+    path, ref = _oracle_path_rows(om, kc, vc, P, toks, par, leaf)
+    err = np.abs(got[path] - ref).max()
+    print(f"n={n} path {path} max|d| {err:.3e}", flush=True)
+    assert err < TOL
+
+
+def test_c5_sampled_path_and_sampling_accept(big, torch):
+    cfg, w, om, m, ssd = big
+    P = 2048
+    s, kc, vc = _session(big, torch, P, 2048 + 256, 256, seed=5)
+    par = W.branching_tree([8, 4, 2, 2, 1], 256)
+    toks = W.tree_tokens(par, cfg.vocab, seed=6)
+    got = _graph_logits(s, torch, P, toks, par)
+    for leaf in (255, 100):
+        path, ref = _oracle_path_rows(om, kc, vc, P, toks, par, leaf)
+        err = np.abs(got[path] - ref).max()
+        print(f"C5 path {path} max|d| {err:.3e}", flush=True)
+        assert err < TOL
+    # temperature-1 recursive rejection sampling on the GPU's logits
+    g = np.random.default_rng(7)
+    p = np.exp(got - got.max(1, keepdims=True))
+    p /= p.sum(1, keepdims=True)
+    q = (0.5 * p + 0.5 * g.dirichlet(np.full(cfg.vocab, 0.1), size=len(par))).astype(np.float32)
+    dlg, dq = torch.from_numpy(got).cuda(), torch.from_numpy(q).cuda()
+    for seed in range(4):
+        path, plen, nxt = s.accept(toks, par, dlg, mode=ssd.SAMPLE_WOR, draft_probs=dq, seed=seed)
+        op, on = oracle.tree_accept(oracle.SAMPLE_WOR, toks, par, got, q, 1.0, seed)
+        assert path[:int(plen.item())].cpu().numpy().tolist() == op.tolist() and int(nxt.item()) == on

@@ -1,0 +1,265 @@
+"""GPU parity: libssd (HIP, through the C ABI) against the CPU oracle on the
+same seeded inputs.
+
+Bars: float32 models within 1e-4 max-abs on logits and K/V; bfloat16 models
+within 2e-2 on logits; tree bookkeeping, accepted paths, greedy and sampled
+tokens and committed cache rows bit-exact (accept is compared on identical
+logits, the GPU's own copied to the host)."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2308_04623_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+TOL_F32, TOL_BF16 = 1e-4, 2e-2
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as t
+    assert t.cuda.is_available()
+    return t
+
+
+@pytest.fixture(scope="module")
+def ssd(torch):
+    from paper_2308_04623_amd import ssd as s
+    s.lib()
+    yield s
+    s.set_gemm_path(s.GEMM_AUTO)
+
+
+class Tiny:
+    """TINY model on both sides, with a prefix cache."""
+
+    def __init__(self, ssd, dtype="f32", max_ctx=160, max_nodes=128, P=64):
+        self.cfg = cfg = W.TINY.with_(dtype=dtype)
+        self.w = W.make_weights(cfg, 0, perturb_affine=True)
+        self.om = oracle.Model(cfg, self.w)
+        self.P, self.max_ctx, self.max_nodes = P, max_ctx, max_nodes
+        self.kc, self.vc = W.random_kv_cache(cfg, max_ctx, P, seed=3)
+        self.m = ssd.Model(cfg, self.w)
+        self.s = ssd.Session(self.m, max_ctx, max_nodes, ssd.to_device(self.kc, cfg), ssd.to_device(self.vc, cfg))
+
+    def oracle_verify(self, toks, parents, P=None):
+        P = self.P if P is None else P
+        kt, vt = self.om.kv(self.max_nodes), self.om.kv(self.max_nodes)
+        lg = oracle.tree_verify(self.om, self.kc, self.vc, P, toks, parents, kt, vt)
+        return lg, kt, vt
+
+
+@pytest.fixture(scope="module")
+def tiny32(ssd):
+    return Tiny(ssd, "f32")
+
+
+@pytest.fixture(scope="module")
+def tiny16(ssd):
+    return Tiny(ssd, "bf16")
+
+
+def _trees():
+    g = np.random.default_rng(5)
+    rnd = lambda n: np.array([-1] + [int(g.integers(max(0, i - 8), i)) for i in range(1, n)], np.int32)
+    return {"binary15": W.complete_binary_tree(15), "single": np.array([-1], np.int32),
+            "chain17": W.chain_tree(17), "chain64": W.chain_tree(64), "branch32": W.branching_tree([4, 2, 2, 1], 32),
+            "random100": rnd(100), "random128": rnd(128)}
+
+
+TREES = _trees()
+
+
+@pytest.mark.parametrize("name", list(TREES))
+@pytest.mark.parametrize("P", [0, 64])
+def test_tiny_f32_verify(tiny32, ssd, torch, name, P):
+    t = tiny32
+    par = TREES[name]
+    toks = W.tree_tokens(par, t.cfg.vocab, seed=len(par))
+    ref, kt, vt = t.oracle_verify(toks, par, P)
+    lg = t.s.verify(P, toks, par)
+    torch.cuda.synchronize()
+    got = lg.cpu().numpy()
+    assert np.abs(got - ref).max() < TOL_F32
+    n = len(par)
+    for a, b in ((t.s.k_tree, kt), (t.s.v_tree, vt)):
+        assert np.abs(ssd.to_host_bits(a)[:, :, :n] - b[:, :, :n]).max() < TOL_F32
+    # greedy accept on the GPU's own logits is bit-exact with the oracle's walk
+    path, plen, nxt = t.s.accept(toks, par, lg)
+    op, on = oracle.tree_accept(oracle.GREEDY, toks, par, got)
+    assert path[:int(plen.item())].cpu().numpy().tolist() == op.tolist() and int(nxt.item()) == on
+
+
+@pytest.mark.parametrize("gemm", ["vec", "mfma"])
+@pytest.mark.parametrize("name", ["binary15", "single", "chain17", "random100"])
+def test_tiny_bf16_verify(tiny16, ssd, torch, gemm, name):
+    t = tiny16
+    par = TREES[name]
+    if gemm == "vec" and len(par) > 16:
+        par = par[:16]
+    ssd.set_gemm_path(ssd.GEMM_VEC if gemm == "vec" else ssd.GEMM_MFMA)
+    try:
+        toks = W.tree_tokens(par, t.cfg.vocab, seed=7)
+        ref, kt, vt = t.oracle_verify(toks, par)
+        lg = t.s.verify(t.P, toks, par)
+        torch.cuda.synchronize()
+    finally:
+        ssd.set_gemm_path(ssd.GEMM_AUTO)
+    assert np.abs(lg.cpu().numpy() - ref).max() < TOL_BF16
+    n = len(par)
+    kg = W.bf16_bits_to_f32(ssd.to_host_bits(t.s.k_tree)[:, :, :n])
+    assert np.abs(kg - W.bf16_bits_to_f32(kt[:, :, :n])).max() < TOL_BF16
+
+
+def test_determinism_and_graph_replay(tiny16, ssd, torch):
+    t = tiny16
+    par = TREES["random100"]
+    toks = W.tree_tokens(par, t.cfg.vocab, seed=9)
+    a = t.s.verify(t.P, toks, par).clone()
+    b = t.s.verify(t.P, toks, par).clone()
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+    out = torch.zeros_like(a)
+    g = t.s.capture_verify(t.P, toks, par, out)
+    other = W.tree_tokens(TREES["binary15"], t.cfg.vocab, seed=1)
+    for _ in range(3):
+        out.zero_()
+        g.launch()
+        torch.cuda.synchronize()
+        assert torch.equal(out, a)
+        t.s.verify(t.P, other, TREES["binary15"])      # eager work between replays
+        torch.cuda.synchronize()
+    g.close()
+
+
+@pytest.mark.parametrize("gemm", ["vec", "mfma"])
+def test_node_result_independent_of_tree_and_slot(tiny16, ssd, torch, gemm):
+    """A node's logits depend only on its root path, bitwise, whatever the
+    other nodes and its index (one GEMM path pinned)."""
+    t = tiny16
+    ssd.set_gemm_path(ssd.GEMM_VEC if gemm == "vec" else ssd.GEMM_MFMA)
+    try:
+        toks_a = np.array([5, 6, 7, 8], np.int32)
+        lg_a = t.s.verify(t.P, toks_a, W.chain_tree(4)).clone()
+        # same chain at slots 0, 2, 5, 9 with decoy siblings
+        par_b = np.array([-1, 0, 0, 1, 2, 2, 3, 5, 4, 5], np.int32)
+        toks_b = np.array([5, 100, 6, 101, 102, 7, 103, 104, 105, 8], np.int32)
+        lg_b = t.s.verify(t.P, toks_b, par_b).clone()
+        torch.cuda.synchronize()
+    finally:
+        ssd.set_gemm_path(ssd.GEMM_AUTO)
+    for i, j in zip([0, 1, 2, 3], [0, 2, 5, 9]):
+        assert torch.equal(lg_a[i], lg_b[j]), (i, j)
+
+
+def test_commit_bitwise_and_continue(tiny32, ssd, torch):
+    t = tiny32
+    par = TREES["binary15"]
+    toks = W.tree_tokens(par, t.cfg.vocab, seed=2)
+    lg = t.s.verify(t.P, toks, par)
+    path = torch.tensor([0, 1, 4, 9, 0, 0], dtype=torch.int32, device="cuda")
+    plen = torch.tensor([4], dtype=torch.int32, device="cuda")
+    kc0 = ssd.to_host_bits(t.s.k_cache).copy()
+    t.s.commit(t.P, path, plen)
+    torch.cuda.synchronize()
+    kc1, kt = ssd.to_host_bits(t.s.k_cache), ssd.to_host_bits(t.s.k_tree)
+    for j, node in enumerate([0, 1, 4, 9]):
+        assert np.array_equal(kc1[:, :, t.P + j], kt[:, :, node])
+    assert np.array_equal(kc1[:, :, :t.P], kc0[:, :, :t.P])
+    assert np.array_equal(kc1[:, :, t.P + 4:], kc0[:, :, t.P + 4:])
+    # continuing from the committed cache matches the oracle doing the same
+    ref_lg, okt, ovt = t.oracle_verify(toks, par)
+    assert np.abs(lg.cpu().numpy() - ref_lg).max() < TOL_F32
+    okc, ovc = t.kc.copy(), t.vc.copy()
+    oracle.kv_commit(t.om, okc, ovc, t.P, okt, ovt, [0, 1, 4, 9])
+    nxt = [int(toks[3])]
+    want = oracle.tree_verify(t.om, okc, ovc, t.P + 4, nxt, [-1], t.om.kv(1), t.om.kv(1))
+    got = t.s.verify(t.P + 4, nxt, [-1])
+    torch.cuda.synchronize()
+    assert np.abs(got.cpu().numpy() - want).max() < TOL_F32
+    # commit rows past max_ctx are skipped and counted, never written
+    before = t.s.error_count()
+    far = torch.tensor([0, 1, 2], dtype=torch.int32, device="cuda")
+    t.s.commit(t.max_ctx - 1, far, torch.tensor([3], dtype=torch.int32, device="cuda"))
+    assert t.s.error_count() == before + 2
+    # restore the cache for the other tests
+    t.s.k_cache.copy_(ssd.to_device(t.kc, t.cfg))
+    t.s.v_cache.copy_(ssd.to_device(t.vc, t.cfg))
+
+
+def test_error_paths_enqueue_nothing(tiny32, ssd, torch):
+    t = tiny32
+    cases = [(dict(P=0, toks=[1, 2], par=[0, 0]), ssd.E_INVALID_TREE),
+             (dict(P=0, toks=[1, 99999], par=[-1, 0]), ssd.E_INVALID_ARG),
+             (dict(P=t.max_ctx + 1, toks=[1], par=[-1]), ssd.E_CAPACITY),
+             (dict(P=0, toks=[1] * (t.max_nodes + 1), par=W.chain_tree(t.max_nodes + 1)), ssd.E_CAPACITY),
+             (dict(P=t.cfg.n_pos - 1, toks=[1, 2], par=[-1, 0]), ssd.E_CAPACITY)]
+    for c, st in cases:
+        with pytest.raises(ssd.SSDError) as e:
+            t.s.verify(c["P"], c["toks"], c["par"])
+        assert e.value.status == st
+    lg = torch.zeros((2, t.cfg.vocab), device="cuda")
+    with pytest.raises(ssd.SSDError):
+        t.s.accept([0, 1], [-1, 0], lg, mode=ssd.SAMPLE_WOR)             # no draft probs
+    with pytest.raises(ssd.SSDError):
+        t.s.accept([0, 1], [-1, 0], lg, mode=ssd.GREEDY, draft_probs=lg)  # greedy with draft probs
+
+
+# ---------------------------------------------------------------- sampling accept
+
+@pytest.fixture(scope="module")
+def wide(ssd):
+    """A small model whose vocabulary is GPT-2's, for accept-only tests."""
+    cfg = W.TINY.with_(vocab=50257, n_layer=1)
+    m = ssd.Model(cfg, W.make_weights(cfg, 1))
+    return cfg, ssd.Session(m, 8, 256)
+
+
+def _draft_tree(g, V, branching, n_max):
+    par = W.branching_tree(branching, n_max)
+    toks = g.integers(0, V, len(par)).astype(np.int32)
+    return toks, par
+
+
+@pytest.mark.parametrize("V", [512, 50257])
+@pytest.mark.parametrize("mode", ["wor", "iid"])
+def test_sampling_accept_bit_exact(wide, ssd, torch, V, mode):
+    cfg, s = wide
+    g = np.random.default_rng(V + len(mode))
+    md = ssd.SAMPLE_WOR if mode == "wor" else ssd.SAMPLE_IID
+    for trial in range(12):
+        toks, par = _draft_tree(g, V, [4, 2, 2, 1], 32 if trial % 2 else 256)
+        n = len(par)
+        lg = (g.standard_normal((n, V)) * 2.0).astype(np.float32)
+        q = g.dirichlet(np.ones(V) * 0.3, size=n).astype(np.float32)
+        # make acceptance likely somewhere: copy target mass into the draft
+        q = (0.5 * q + 0.5 * np.exp(lg - lg.max(1, keepdims=True)) /
+             np.exp(lg - lg.max(1, keepdims=True)).sum(1, keepdims=True)).astype(np.float32)
+        # children of the root: draw the top target tokens so paths get long
+        for c in range(1, n):
+            if g.random() < 0.7:
+                toks[c] = int(np.argmax(lg[par[c]] + g.gumbel(size=V)))
+        dlg, dq = torch.from_numpy(lg).cuda(), torch.from_numpy(q).cuda()
+        path, plen, nxt = s.accept(toks, par, dlg, mode=md, draft_probs=dq, temperature=1.0, seed=trial)
+        op, on = oracle.tree_accept(oracle.SAMPLE_WOR if mode == "wor" else oracle.SAMPLE_IID, toks, par, lg, q,
+                                    1.0, trial)
+        assert path[:int(plen.item())].cpu().numpy().tolist() == op.tolist(), trial
+        assert int(nxt.item()) == on, trial
+
+
+def test_greedy_accept_full_vocab_ties(wide, ssd, torch):
+    cfg, s = wide
+    V = 50257
+    g = np.random.default_rng(1)
+    n = 64
+    par = W.branching_tree([4, 2, 2, 1], n)
+    lg = g.integers(-3, 3, (n, V)).astype(np.float32)    # many exact ties
+    am = np.array([np.flatnonzero(r == r.max())[0] for r in lg])
+    toks = g.integers(0, V, n).astype(np.int32)
+    for c in range(1, n):
+        if g.random() < 0.8:
+            toks[c] = am[par[c]]
+    path, plen, nxt = s.accept(toks, par, torch.from_numpy(lg).cuda())
+    op, on = oracle.tree_accept(oracle.GREEDY, toks, par, lg)
+    assert path[:int(plen.item())].cpu().numpy().tolist() == op.tolist() and int(nxt.item()) == on
