@@ -171,9 +171,9 @@ void ssd_graph_destroy(ssd_graph *g);
 
 /* Launches one weight GEMM of the verification pass on its own, exactly as
  * the pass launches it, for measurement: which = 0 QKV, 1 attention output,
- * 2 MLP up (FC + GELU), 3 MLP down, 4 LM head; layer in [0, n_layer).  Reads
- * and writes only the session's workspaces and tree scratch (never the cache
- * or caller buffers), so results are meaningless outside a pass. */
+ * 2 MLP up (FC + GELU), 3 MLP down; layer in [0, n_layer).  Reads and writes
+ * only the session's workspaces and tree scratch (never the cache or caller
+ * buffers), so results are meaningless outside a pass. */
 ssd_status ssd_launch_gemm(const ssd_model *m, ssd_kv *kv, int32_t which, int32_t layer, int32_t n_nodes,
                            void *stream);
 

@@ -5,7 +5,9 @@
 // Data layout (HBM):
 //   x        fp32 [N][d]         residual stream
 //   q        fp32 [N][d]         queries of the current layer
-//   act_*    bf16 (or fp32 for fp32 models) [Npad][d or d_mlp], GEMM inputs
+//   act_*    GEMM inputs [Npad][d or d_mlp]: fp32 for fp32 models; for bf16
+//            models two bf16 planes, hi = bf16(v) and lo = bf16(v - hi)
+//   part     fp32 [S][N][d]      split-K partial sums of the residual GEMMs
 //   K/V      storage type [L][H][rows][DH] (cache rows: positions; scratch rows: nodes)
 //   packed W 16x32 bf16 fragments; fragment (rb, kc) holds rows 16rb.., k 32kc..,
 //            lane l's 16 bytes = W[16rb + l%16][32kc + 8(l/16) .. +8], fragments
@@ -39,18 +41,27 @@ template <> __device__ __forceinline__ float ldT<float>(const float* p, size_t i
 template <> __device__ __forceinline__ float ldT<uint16_t>(const uint16_t* p, size_t i) { return bf2f(p[i]); }
 
 template <typename T> __device__ __forceinline__ void stT(T* p, size_t i, float v);
+template <typename T, int E> __device__ __forceinline__ float ldT(const T (&r)[E], int i) { return ldT((const T*)r, (size_t)i); }
 template <> __device__ __forceinline__ void stT<float>(float* p, size_t i, float v) { p[i] = v; }
 template <> __device__ __forceinline__ void stT<uint16_t>(uint16_t* p, size_t i, float v) { p[i] = f2bf(v); }
 
-// GEMM inputs of bf16 models are stored as two bf16 planes, hi = bf16(v) and
-// lo = bf16(v - hi), `plane` elements apart; the GEMMs multiply both, which
-// keeps about 16 significant bits of every activation.
-template <typename T> __device__ __forceinline__ void st_act(T* p, size_t i, size_t plane, float v);
-template <> __device__ __forceinline__ void st_act<float>(float* p, size_t i, size_t, float v) { p[i] = v; }
-template <> __device__ __forceinline__ void st_act<uint16_t>(uint16_t* p, size_t i, size_t plane, float v) {
+// GEMM inputs.  fp32 models: plain rows, element (n, k) at n * ld + k.
+// bf16 models: matrix-core fragment order, so that one wave's load of a
+// 16-node x 32-k operand fragment is 1 KB contiguous: element (n, k) lives in
+// fragment f = (n/16) * ld + k/32 (ld = K/32), lane (n%16) + 16 ((k%32)/8),
+// position k%8.  Each fragment holds a hi plane bf16(v) and, 512 elements
+// later, a lo plane bf16(v - hi); the GEMMs multiply both, which keeps about
+// 16 significant bits of every activation.
+template <typename T> __device__ __forceinline__ void st_act(T* p, int n, int k, int ld, float v);
+template <> __device__ __forceinline__ void st_act<float>(float* p, int n, int k, int ld, float v) {
+  p[(size_t)n * ld + k] = v;
+}
+template <> __device__ __forceinline__ void st_act<uint16_t>(uint16_t* p, int n, int k, int ld, float v) {
+  const size_t f = (size_t)(n >> 4) * ld + (k >> 5);
+  const size_t off = f * 1024 + ((n & 15) + 16 * ((k & 31) >> 3)) * 8 + (k & 7);
   const uint16_t hi = f2bf(v);
-  p[i] = hi;
-  p[i + plane] = f2bf(v - bf2f(hi));
+  p[off] = hi;
+  p[off + 512] = f2bf(v - bf2f(hi));
 }
 
 __device__ __forceinline__ float wave_sum(float v) {
@@ -99,46 +110,124 @@ hipError_t launch_embed(int f32, const void* wte, const void* wpe, const int* to
   return hipGetLastError();
 }
 
-// ------------------------------------------------------------------ LayerNorm
+// ------------------------------------------------------------------ residual + LayerNorm
+//
+// One workgroup per node, the row held in registers (E = ceil(d / 256)
+// elements per thread):
+//   if S > 0:  x[n] += bias + part[0][n] + ... + part[S-1][n]   (split-K sums of the
+//              previous residual GEMM, added in split order), written back;
+//   a[n] = (x[n] - mean) / sqrt(var + eps) * g + b   (biased variance).
+// Every load is issued (clamped to the row) before any of them is used, so
+// the row costs one memory round trip.  SPL is the split count when known at
+// compile time (0, 4 or 8), else -1 and the loop runs to S.
 
-// a[n] = (x[n] - mean) / sqrt(var + eps) * g + b   (biased variance, fp32)
-template <typename T, typename OUT>
-__global__ __launch_bounds__(256) void ln_kernel(const float* __restrict__ x, int d, const T* __restrict__ g,
-                                                 const T* __restrict__ b, float eps, OUT* __restrict__ a, int lda,
-                                                 size_t plane) {
+template <typename T, typename OUT, int E, int SPL>
+__global__ __launch_bounds__(256) void ln_resid_kernel(float* __restrict__ x, int d, const float* __restrict__ part,
+                                                       int S, size_t pstride, const T* __restrict__ bias,
+                                                       const T* __restrict__ g, const T* __restrict__ b, float eps,
+                                                       OUT* __restrict__ a, int lda) {
+  constexpr int PS = SPL > 0 ? SPL : 1;
   __shared__ float red[4];
-  const int n = blockIdx.x;
-  const float* xr = x + (size_t)n * d;
-  float s = 0.f;
-  for (int k = threadIdx.x; k < d; k += 256) s += xr[k];
-  const float mean = block_sum256(s, red) / d;
-  float v = 0.f;
-  for (int k = threadIdx.x; k < d; k += 256) {
-    const float t = xr[k] - mean;
-    v += t * t;
+  const int n = blockIdx.x, tid = threadIdx.x;
+  float* xr = x + (size_t)n * d;
+  const float* pr = part + (size_t)n * d;
+  float v[E];
+  T gw[E], bw[E], cw[E];
+  float pv[E][PS];
+#pragma unroll
+  for (int i = 0; i < E; ++i) {
+    const int k = min(tid + i * 256, d - 1);
+    v[i] = xr[k];
+    gw[i] = g[k];
+    bw[i] = b[k];
+    if constexpr (SPL > 0) {
+      cw[i] = bias[k];
+#pragma unroll
+      for (int sp = 0; sp < SPL; ++sp) pv[i][sp] = pr[sp * pstride + k];
+    }
   }
-  const float var = block_sum256(v, red) / d;
-  const float den = sqrtf(var + eps);
-  for (int k = threadIdx.x; k < d; k += 256)
-    st_act(a, (size_t)n * lda + k, plane, (xr[k] - mean) / den * ldT(g, k) + ldT(b, k));
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < E; ++i) {
+    const int k = tid + i * 256;
+    if constexpr (SPL != 0) {
+      float acc;
+      if constexpr (SPL > 0) {
+        acc = ldT(cw, i);
+#pragma unroll
+        for (int sp = 0; sp < SPL; ++sp) acc += pv[i][sp];
+      } else {
+        acc = ldT(bias, min(k, d - 1));
+        for (int sp = 0; sp < S; ++sp) acc += pr[sp * pstride + min(k, d - 1)];
+      }
+      v[i] += acc;
+      if (k < d) xr[k] = v[i];
+    }
+    if (k < d) s += v[i];
+  }
+  const float mean = block_sum256(s, red) / d;
+  float q = 0.f;
+#pragma unroll
+  for (int i = 0; i < E; ++i)
+    if (tid + i * 256 < d) q += (v[i] - mean) * (v[i] - mean);
+  const float den = sqrtf(block_sum256(q, red) / d + eps);
+#pragma unroll
+  for (int i = 0; i < E; ++i) {
+    const int k = tid + i * 256;
+    if (k < d) st_act(a, n, k, lda, (v[i] - mean) / den * ldT(gw, i) + ldT(bw, i));
+  }
 }
 
-hipError_t launch_ln(int f32, const float* x, int N, int d, const void* g, const void* b, float eps, void* a,
-                     int lda, size_t plane, hipStream_t s) {
-  if (f32)
-    ln_kernel<float, float><<<N, 256, 0, s>>>(x, d, (const float*)g, (const float*)b, eps, (float*)a, lda, 0);
-  else
-    ln_kernel<uint16_t, uint16_t><<<N, 256, 0, s>>>(x, d, (const uint16_t*)g, (const uint16_t*)b, eps,
-                                                     (uint16_t*)a, lda, plane);
+template <typename T, int E, int SPL>
+static void ln_go(float* x, int N, int d, const float* part, int S, size_t pstride, const void* bias, const void* g,
+                  const void* b, float eps, void* a, int lda, hipStream_t s) {
+  ln_resid_kernel<T, T, E, SPL><<<N, 256, 0, s>>>(x, d, part, S, pstride, (const T*)bias, (const T*)g, (const T*)b,
+                                                  eps, (T*)a, lda);
+}
+
+template <typename T, int E>
+static void ln_go_s(float* x, int N, int d, const float* part, int S, size_t pstride, const void* bias,
+                    const void* g, const void* b, float eps, void* a, int lda, hipStream_t s) {
+  if (S == 0) ln_go<T, E, 0>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, s);
+  else if (S == 4) ln_go<T, E, 4>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, s);
+  else if (S == 8) ln_go<T, E, 8>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, s);
+  else ln_go<T, E, -1>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, s);
+}
+
+template <typename T>
+static hipError_t ln_go_e(float* x, int N, int d, const float* part, int S, size_t pstride, const void* bias,
+                          const void* g, const void* b, float eps, void* a, int lda, hipStream_t s) {
+  switch ((d + 255) / 256) {
+    case 1: ln_go_s<T, 1>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, s); break;
+    case 2: ln_go_s<T, 2>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, s); break;
+    case 3: ln_go_s<T, 3>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, s); break;
+    case 4: ln_go_s<T, 4>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, s); break;
+    case 5: ln_go_s<T, 5>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, s); break;
+    case 6: ln_go_s<T, 6>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, s); break;
+    case 7: ln_go_s<T, 7>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, s); break;
+    case 8: ln_go_s<T, 8>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, s); break;
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
+}
+
+hipError_t launch_ln(int f32, float* x, int N, int d, const float* part, int S, size_t pstride, const void* bias,
+                     const void* g, const void* b, float eps, void* a, int lda, hipStream_t s) {
+  if (S > 0 && !bias) return hipErrorInvalidValue;
+  if (f32) return ln_go_e<float>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, s);
+  return ln_go_e<uint16_t>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, s);
 }
 
 // ------------------------------------------------------------------ GEMM epilogues
 
 template <typename T, int KIND>
 __device__ __forceinline__ void epilogue(const Epi& e, int n, int o, float acc) {
-  const float y = acc + (e.bias ? ldT((const T*)e.bias, o) : 0.f);
   const int nn = e.node0 + n;
+  if (KIND == EPI_PARTIAL) {
+    e.part[(size_t)e.split * e.part_stride + (size_t)nn * e.d + o] = acc;
+    return;
+  }
+  const float y = acc + (e.bias ? ldT((const T*)e.bias, o) : 0.f);
   if (KIND == EPI_QKV) {
     if (o < e.d) {
       e.q[(size_t)nn * e.d + o] = y;
@@ -151,7 +240,7 @@ __device__ __forceinline__ void epilogue(const Epi& e, int n, int o, float acc) 
   } else if (KIND == EPI_RESID) {
     e.x[(size_t)nn * e.d + o] += y;
   } else if (KIND == EPI_GELU) {
-    st_act((T*)e.out, (size_t)nn * e.ldo + o, (size_t)e.out_plane, gelu_tanh(y));
+    st_act((T*)e.out, nn, o, e.ldo, gelu_tanh(y));
   } else {
     e.logits[(size_t)nn * e.ldl + o] = acc;
   }
@@ -210,312 +299,420 @@ hipError_t launch_pack_bf16(const uint16_t* W, int M, int K, void* out, hipStrea
   return hipGetLastError();
 }
 
-// ------------------------------------------------------------------ GEMM, bf16 on matrix cores
+// ------------------------------------------------------------------ GEMM, bf16 weights
 //
-// Y^T[o][n] = sum_k W[o][k] A[n][k] with v_mfma_f32_16x16x32_bf16: W fragment
-// is the A operand (16 rows x 32 k), activations the B operand (32 k x 16
-// nodes).  One workgroup owns a 16-row block and every node; its 4 waves take
-// consecutive quarters of K and reduce through LDS in a fixed order, so every
-// output is computed the same way whatever the node count or a node's slot.
+// Y[n][o] = sum_k A[n][k] W[o][k] over packed weight fragments.
+// A workgroup (4 waves) owns RB consecutive 16-row blocks and the k-steps
+// [kc0, kc1) of its split (grid.y); wave w takes k-steps kc0 + w, kc0 + w + 4,
+// ...  Per k-step a wave loads the RB weight fragments and the activation
+// fragments of every node tile (hi and lo planes, 1 KB contiguous each, see
+// st_act) and multiplies each activation fragment into all RB row blocks, so
+// activations are read once per RB row blocks.  U k-steps stay in flight
+// (loads issued U steps ahead, unconditionally: a step past the end re-reads
+// the last valid step and its weights are replaced by zeros when used), and
+// scheduling barriers keep the compiler from sinking those loads next to
+// their use.  After the loop the 4 waves are summed in wave order through
+// LDS, so every output is computed the same way whatever the node count or a
+// node's slot.
+//  matrix cores: v_mfma_f32_16x16x32_bf16, weight fragment as A (16 rows x 32
+//    k), activations as B (32 k x 16 nodes), hi then lo plane;
+//  vector ALU (few nodes): each lane multiplies its 8 weights into fp32
+//    accumulators per node; the 4 lanes of a row are summed (xor 16, xor 32).
+// Occupancy is traded for registers (1-2 waves per SIMD).
 
-template <int NT, int KIND>
-__global__ __launch_bounds__(256) void gemm_mfma_kernel(const u32x4* __restrict__ Wp, int KC,
-                                                        const uint16_t* __restrict__ act, int lda, size_t plane,
-                                                        Epi ep) {
-  __shared__ f32x4 red[4][NT][64];
-  const int rb = blockIdx.x, w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int kc0 = (w * KC) >> 2, kc1 = ((w + 1) * KC) >> 2;
-  f32x4 acc[NT];
+template <int NT, int RB, int KIND, bool VEC, int NV, int U>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) void gemm_kernel(
+    const u32x4* __restrict__ Wp, int KC, int RBtot, int kc_split, const uint16_t* __restrict__ act, Epi ep) {
+  static_assert(!VEC || RB == 1, "vector path: one row block per workgroup");
+  constexpr int NB = VEC ? 2 * NV : 2 * NT;  // activation fragments per k-step
+  constexpr int NN = VEC ? NV : 16 * NT;     // output nodes
+  __shared__ float red[4 * RB * NN * 16];
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+  const int rb0 = blockIdx.x * RB;
+  const int kc0 = blockIdx.y * kc_split;
+  const int kc1 = min(KC, kc0 + kc_split);
+  const int nsteps = kc1 - kc0 > w ? (kc1 - kc0 - w + 3) / 4 : 0;
+  // weight rows past the matrix (last workgroup) read row block rb0 instead
+  // and are never stored
+  const u32x4* wb[RB];
 #pragma unroll
-  for (int t = 0; t < NT; ++t) acc[t] = (f32x4){0.f, 0.f, 0.f, 0.f};
-  const u32x4* wp = Wp + (size_t)rb * KC * 64 + lane;
-  const uint16_t* ap = act + (size_t)(lane & 15) * lda + 8 * (lane >> 4);
-  constexpr int U = 8;
-  int kc = kc0;
-  for (; kc + U <= kc1; kc += U) {
-    u32x4 wf[U];
+  for (int r = 0; r < RB; ++r) wb[r] = Wp + (size_t)min(rb0 + r, RBtot - 1) * KC * 64 + lane;
+  // activation fragments (see st_act): MFMA lanes read their own slot; in the
+  // vector path lane l reads node n's slot in its 8-k group, 16 (l/16) + n
+  const u32x4* abase = (const u32x4*)act + (VEC ? 16 * (lane >> 4) : lane);
+
+  u32x4 wq[U][RB];
+  u32x4 bq[U][NB];
+  const int klast = kc1 - 1;
+  auto load_step = [&](int s, int u) {
+    const int kc = min(kc0 + w + 4 * s, klast);
 #pragma unroll
-    for (int u = 0; u < U; ++u) wf[u] = __builtin_nontemporal_load(wp + (size_t)(kc + u) * 64);
+    for (int r = 0; r < RB; ++r) wq[u][r] = wb[r][(size_t)kc * 64];
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-#pragma unroll
-      for (int t = 0; t < NT; ++t) {
-        const uint16_t* at = ap + (size_t)16 * t * lda + (kc + u) * 32;
-        const u32x4 b = *(const u32x4*)at;
-        const u32x4 bl = *(const u32x4*)(at + plane);
-        acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, wf[u]),
-                                                         __builtin_bit_cast(bf16x8, b), acc[t], 0, 0, 0);
-        acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, wf[u]),
-                                                         __builtin_bit_cast(bf16x8, bl), acc[t], 0, 0, 0);
-      }
+    for (int b = 0; b < NB; ++b) {
+      // b = 2 * (node tile or node) + plane
+      bq[u][b] = VEC ? abase[((size_t)kc * 2 + (b & 1)) * 64 + (b >> 1)]
+                     : abase[((size_t)(b >> 1) * KC + kc) * 2 * 64 + (b & 1) * 64];
     }
-  }
-  for (; kc < kc1; ++kc) {
-    const u32x4 wf = __builtin_nontemporal_load(wp + (size_t)kc * 64);
-#pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      const uint16_t* at = ap + (size_t)16 * t * lda + kc * 32;
-      const u32x4 b = *(const u32x4*)at;
-      const u32x4 bl = *(const u32x4*)(at + plane);
-      acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, wf),
-                                                       __builtin_bit_cast(bf16x8, b), acc[t], 0, 0, 0);
-      acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, wf),
-                                                       __builtin_bit_cast(bf16x8, bl), acc[t], 0, 0, 0);
-    }
-  }
-#pragma unroll
-  for (int t = 0; t < NT; ++t) red[w][t][lane] = acc[t];
-  __syncthreads();
-  // D layout: lane l holds rows 4(l/16)+r, column (node) l%16
-  const int l2 = threadIdx.x >> 2, r = threadIdx.x & 3;
-  const int row = 4 * (l2 >> 4) + r, o = rb * 16 + row;
-#pragma unroll
-  for (int t = 0; t < NT; ++t) {
-    const float s = ((red[0][t][l2][r] + red[1][t][l2][r]) + red[2][t][l2][r]) + red[3][t][l2][r];
-    const int node = 16 * t + (l2 & 15);
-    if (o < ep.M && node < ep.N) epilogue<uint16_t, KIND>(ep, node, o, s);
-  }
-}
+  };
 
-template <int NT>
-static void gemm_mfma_nt(int kind, const void* Wp, int M, int KC, const uint16_t* act, int lda, size_t plane,
-                         const Epi& ep, hipStream_t s) {
-  const int RB = (M + 15) / 16;
-  const u32x4* w = (const u32x4*)Wp;
-  switch (kind) {
-    case EPI_QKV: gemm_mfma_kernel<NT, EPI_QKV><<<RB, 256, 0, s>>>(w, KC, act, lda, plane, ep); break;
-    case EPI_RESID: gemm_mfma_kernel<NT, EPI_RESID><<<RB, 256, 0, s>>>(w, KC, act, lda, plane, ep); break;
-    case EPI_GELU: gemm_mfma_kernel<NT, EPI_GELU><<<RB, 256, 0, s>>>(w, KC, act, lda, plane, ep); break;
-    default: gemm_mfma_kernel<NT, EPI_LOGITS><<<RB, 256, 0, s>>>(w, KC, act, lda, plane, ep); break;
-  }
-}
+  f32x4 acc[RB][VEC ? 1 : NT];
+  float vacc[VEC ? NV : 1];
+#pragma unroll
+  for (int r = 0; r < RB; ++r)
+#pragma unroll
+    for (int t = 0; t < (VEC ? 1 : NT); ++t) acc[r][t] = (f32x4){0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int n = 0; n < (VEC ? NV : 1); ++n) vacc[n] = 0.f;
 
-hipError_t launch_gemm_mfma(int kind, const void* Wp, int M, int K, const uint16_t* act, int lda, size_t plane,
-                            const Epi& ep, hipStream_t s) {
-  const int KC = K / 32;
-  if (ep.N <= 16) gemm_mfma_nt<1>(kind, Wp, M, KC, act, lda, plane, ep, s);
-  else if (ep.N <= 32) gemm_mfma_nt<2>(kind, Wp, M, KC, act, lda, plane, ep, s);
-  else if (ep.N <= 64) gemm_mfma_nt<4>(kind, Wp, M, KC, act, lda, plane, ep, s);
-  else if (ep.N <= 128) gemm_mfma_nt<8>(kind, Wp, M, KC, act, lda, plane, ep, s);
-  else if (ep.N <= 256) gemm_mfma_nt<16>(kind, Wp, M, KC, act, lda, plane, ep, s);
-  else return hipErrorInvalidValue;
-  return hipGetLastError();
-}
-
-// ------------------------------------------------------------------ GEMM, bf16 on the vector ALU
-//
-// Same packed fragments and work split as the matrix-core kernel; each lane
-// multiplies its 8 weights into fp32 accumulators for every node, then the 4
-// lanes sharing a row and the 4 waves are reduced in a fixed order.
-
-template <int NV, int KIND>
-__global__ __launch_bounds__(256) void gemm_vec_kernel(const u32x4* __restrict__ Wp, int KC,
-                                                       const uint16_t* __restrict__ act, int lda, size_t plane,
-                                                       Epi ep) {
-  __shared__ float red[4][NV][16];
-  const int rb = blockIdx.x, w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int kc0 = (w * KC) >> 2, kc1 = ((w + 1) * KC) >> 2;
-  float acc[NV];
+  if (nsteps > 0) {
 #pragma unroll
-  for (int n = 0; n < NV; ++n) acc[n] = 0.f;
-  const u32x4* wp = Wp + (size_t)rb * KC * 64 + lane;
-  const uint16_t* ap = act + 8 * (lane >> 4);
-  constexpr int U = 4;
-  int kc = kc0;
-  for (; kc < kc1; kc += U) {
-    u32x4 wf[U];
+    for (int u = 0; u < U; ++u) load_step(u, u);
+    __builtin_amdgcn_sched_barrier(0);
+    for (int s0 = 0; s0 < nsteps; s0 += U) {
 #pragma unroll
-    for (int u = 0; u < U; ++u)
-      wf[u] = (kc + u < kc1) ? __builtin_nontemporal_load(wp + (size_t)(kc + u) * 64) : (u32x4){0, 0, 0, 0};
+      for (int u = 0; u < U; ++u) {
+        const int s = s0 + u;
+        const bool ok = s < nsteps;
+        if constexpr (!VEC) {
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      if (kc + u >= kc1) break;
-      float wv[8];
+          for (int r = 0; r < RB; ++r) {
+            const u32x4 wf = ok ? wq[u][r] : (u32x4){0, 0, 0, 0};
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        wv[2 * e] = __uint_as_float(wf[u][e] << 16);
-        wv[2 * e + 1] = __uint_as_float(wf[u][e] & 0xffff0000u);
-      }
+            for (int t = 0; t < NT; ++t) {
+              acc[r][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                  __builtin_bit_cast(bf16x8, wf), __builtin_bit_cast(bf16x8, bq[u][2 * t]), acc[r][t], 0, 0, 0);
+              acc[r][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                  __builtin_bit_cast(bf16x8, wf), __builtin_bit_cast(bf16x8, bq[u][2 * t + 1]), acc[r][t], 0, 0, 0);
+            }
+          }
+        } else {
+          const u32x4 wf = ok ? wq[u][0] : (u32x4){0, 0, 0, 0};
 #pragma unroll
-      for (int n = 0; n < NV; ++n) {
-        const uint16_t* an = ap + (size_t)n * lda + (kc + u) * 32;
-        const u32x4 av = *(const u32x4*)an;
-        const u32x4 al = *(const u32x4*)(an + plane);
+          for (int n = 0; n < NV; ++n) {
+            const u32x4 ah = bq[u][2 * n], al = bq[u][2 * n + 1];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float a0 = __uint_as_float(av[e] << 16) + __uint_as_float(al[e] << 16);
-          const float a1 = __uint_as_float(av[e] & 0xffff0000u) + __uint_as_float(al[e] & 0xffff0000u);
-          acc[n] = fmaf(wv[2 * e], a0, acc[n]);
-          acc[n] = fmaf(wv[2 * e + 1], a1, acc[n]);
+            for (int e = 0; e < 4; ++e) {
+              const float a0 = __uint_as_float(ah[e] << 16) + __uint_as_float(al[e] << 16);
+              const float a1 = __uint_as_float(ah[e] & 0xffff0000u) + __uint_as_float(al[e] & 0xffff0000u);
+              vacc[n] = fmaf(__uint_as_float(wf[e] << 16), a0, vacc[n]);
+              vacc[n] = fmaf(__uint_as_float(wf[e] & 0xffff0000u), a1, vacc[n]);
+            }
+          }
         }
+        __builtin_amdgcn_sched_barrier(0);
+        load_step(s + U, u);
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
   }
+
+  // per-wave tiles -> LDS [wave][row block][node][16 rows], then the 4 waves summed in order
+  if constexpr (!VEC) {
 #pragma unroll
-  for (int n = 0; n < NV; ++n) {
-    acc[n] += __shfl_xor(acc[n], 16);
-    acc[n] += __shfl_xor(acc[n], 32);
-  }
-  if (lane < 16) {
+    for (int r = 0; r < RB; ++r)
 #pragma unroll
-    for (int n = 0; n < NV; ++n) red[w][n][lane] = acc[n];
+      for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          red[((w * RB + r) * NN + 16 * t + (lane & 15)) * 16 + 4 * (lane >> 4) + q] = acc[r][t][q];
+  } else {
+#pragma unroll
+    for (int n = 0; n < NV; ++n) {
+      float v = vacc[n];
+      v += __shfl_xor(v, 16);
+      v += __shfl_xor(v, 32);
+      if (lane < 16) red[(w * NN + n) * 16 + lane] = v;
+    }
   }
   __syncthreads();
-  for (int idx = threadIdx.x; idx < NV * 16; idx += 256) {
-    const int n = idx >> 4, row = idx & 15, o = rb * 16 + row;
-    const float s = ((red[0][n][row] + red[1][n][row]) + red[2][n][row]) + red[3][n][row];
-    if (o < ep.M && n < ep.N) epilogue<uint16_t, KIND>(ep, n, o, s);
+  Epi e2 = ep;
+  e2.split = blockIdx.y;
+  for (int idx = tid; idx < RB * NN * 16; idx += 256) {
+    const int row = idx & 15, node = (idx >> 4) % NN, r = idx / (16 * NN);
+    const size_t st = (size_t)RB * NN * 16;
+    const size_t base = ((size_t)r * NN + node) * 16 + row;
+    const float s = ((red[base] + red[st + base]) + red[2 * st + base]) + red[3 * st + base];
+    const int o = (rb0 + r) * 16 + row;
+    if (rb0 + r < RBtot && o < ep.M && node < ep.N) epilogue<uint16_t, KIND>(e2, node, o, s);
   }
 }
 
-template <int NV>
-static void gemm_vec_nv(int kind, const void* Wp, int M, int KC, const uint16_t* act, int lda, size_t plane,
-                        const Epi& ep, hipStream_t s) {
-  const int RB = (M + 15) / 16;
+GemmCfg gemm_cfg(int N, int vec) {
+  GemmCfg c{};
+  c.rb = 1;
+  c.ck = 1;
+  if (vec) {
+    int nv = 1;
+    while (nv < N) nv *= 2;
+    c.nt = 1;
+    c.nv = nv;
+    return c;
+  }
+  int nt = 1;
+  while (nt * 16 < N) nt *= 2;
+  c.nt = nt;
+  c.nv = 0;
+  c.rb = nt <= 4 ? 2 : 1;
+  return c;
+}
+
+int gemm_split_kc(int M, int K, int N, int vec, int want_split, int* splits) {
+  const int KC = K / 32;
+  if (!want_split) {
+    *splits = 1;
+    return KC;
+  }
+  const int gx = ((M + 15) / 16 + gemm_cfg(N, vec).rb - 1) / gemm_cfg(N, vec).rb;
+  int S = 1;  // a power of two with S * gx >= 256 workgroups
+  while (S * gx < 256 && S < kMaxSplits) S *= 2;
+  const int kcs = (KC + S - 1) / S;
+  *splits = (KC + kcs - 1) / kcs;
+  return kcs;
+}
+
+template <int NT, int RB, bool VEC, int NV, int U>
+static void gemm_go(int kind, const void* Wp, int M, int K, int kcs, const uint16_t* act, const Epi& ep,
+                    hipStream_t s) {
+  const int KC = K / 32, RBtot = (M + 15) / 16;
+  dim3 grid((RBtot + RB - 1) / RB, (KC + kcs - 1) / kcs);
   const u32x4* w = (const u32x4*)Wp;
   switch (kind) {
-    case EPI_QKV: gemm_vec_kernel<NV, EPI_QKV><<<RB, 256, 0, s>>>(w, KC, act, lda, plane, ep); break;
-    case EPI_RESID: gemm_vec_kernel<NV, EPI_RESID><<<RB, 256, 0, s>>>(w, KC, act, lda, plane, ep); break;
-    case EPI_GELU: gemm_vec_kernel<NV, EPI_GELU><<<RB, 256, 0, s>>>(w, KC, act, lda, plane, ep); break;
-    default: gemm_vec_kernel<NV, EPI_LOGITS><<<RB, 256, 0, s>>>(w, KC, act, lda, plane, ep); break;
+    case EPI_QKV: gemm_kernel<NT, RB, EPI_QKV, VEC, NV, U><<<grid, 256, 0, s>>>(w, KC, RBtot, kcs, act, ep); break;
+    case EPI_PARTIAL: gemm_kernel<NT, RB, EPI_PARTIAL, VEC, NV, U><<<grid, 256, 0, s>>>(w, KC, RBtot, kcs, act, ep); break;
+    case EPI_GELU: gemm_kernel<NT, RB, EPI_GELU, VEC, NV, U><<<grid, 256, 0, s>>>(w, KC, RBtot, kcs, act, ep); break;
+    default: gemm_kernel<NT, RB, EPI_LOGITS, VEC, NV, U><<<grid, 256, 0, s>>>(w, KC, RBtot, kcs, act, ep); break;
   }
 }
 
-hipError_t launch_gemm_vec(int kind, const void* Wp, int M, int K, const uint16_t* act, int lda, size_t plane,
-                           const Epi& ep, hipStream_t s) {
-  const int KC = K / 32;
-  if (ep.N <= 1) gemm_vec_nv<1>(kind, Wp, M, KC, act, lda, plane, ep, s);
-  else if (ep.N <= 2) gemm_vec_nv<2>(kind, Wp, M, KC, act, lda, plane, ep, s);
-  else if (ep.N <= 4) gemm_vec_nv<4>(kind, Wp, M, KC, act, lda, plane, ep, s);
-  else if (ep.N <= 8) gemm_vec_nv<8>(kind, Wp, M, KC, act, lda, plane, ep, s);
-  else if (ep.N <= 16) gemm_vec_nv<16>(kind, Wp, M, KC, act, lda, plane, ep, s);
-  else return hipErrorInvalidValue;
+hipError_t launch_gemm_bf16(int kind, int vec, const void* Wp, int M, int K, const uint16_t* act, int kcs,
+                            const Epi& ep, hipStream_t s) {
+  if (kcs <= 0) return hipErrorInvalidValue;
+  if (vec) {
+    if (ep.N > 16) return hipErrorInvalidValue;
+    switch (gemm_cfg(ep.N, 1).nv) {
+      case 1: gemm_go<1, 1, true, 1, 8>(kind, Wp, M, K, kcs, act, ep, s); break;
+      case 2: gemm_go<1, 1, true, 2, 8>(kind, Wp, M, K, kcs, act, ep, s); break;
+      case 4: gemm_go<1, 1, true, 4, 6>(kind, Wp, M, K, kcs, act, ep, s); break;
+      case 8: gemm_go<1, 1, true, 8, 4>(kind, Wp, M, K, kcs, act, ep, s); break;
+      default: gemm_go<1, 1, true, 16, 2>(kind, Wp, M, K, kcs, act, ep, s); break;
+    }
+  } else {
+    if (ep.N > 256) return hipErrorInvalidValue;
+    switch (gemm_cfg(ep.N, 0).nt) {
+      case 1: gemm_go<1, 2, false, 0, 6>(kind, Wp, M, K, kcs, act, ep, s); break;
+      case 2: gemm_go<2, 2, false, 0, 4>(kind, Wp, M, K, kcs, act, ep, s); break;
+      case 4: gemm_go<4, 2, false, 0, 3>(kind, Wp, M, K, kcs, act, ep, s); break;
+      case 8: gemm_go<8, 1, false, 0, 2>(kind, Wp, M, K, kcs, act, ep, s); break;
+      default: gemm_go<16, 1, false, 0, 1>(kind, Wp, M, K, kcs, act, ep, s); break;
+    }
+  }
   return hipGetLastError();
 }
 
 // ------------------------------------------------------------------ tree attention
 //
-// Keys of node i: cache rows 0..P-1, then its ancestors and itself in the tree
-// scratch (ancestor bitmask).  Grid (head, split): splits 0..S-1 take 64
-// cache rows each, splits S.. take 64 tree rows each.  A split loads its K/V
-// tile into LDS once and scores it against every node; each (node, head,
-// split) leaves a partial (max, sum of exp, unnormalised output) that the
-// combine kernel merges in split order.  Split boundaries are absolute key
-// positions, so a node's result does not depend on the node count.
+// Node i, head h attends to cache rows 0..P-1 and then to its root path in the
+// tree scratch (root first, itself last).  Two kernels:
+//  prefix: workgroup (head h, tile s) stages cache rows 64s..64s+63 of head h
+//    in LDS once and scores them against every node (one wave per node at a
+//    time), leaving per (node, head, tile) the partial (max m, sum of exp z,
+//    unnormalised output o[DH]);
+//  combine: one wave per (node, head) merges the tiles' partials in tile order
+//    with the node's root-path keys (read from the tree scratch) and writes
+//    the normalised output into the next GEMM's input layout.
+// Tiles are fixed by absolute key position, so a node's result does not
+// depend on the other nodes.  Softmax in fp32; the 1/sqrt(head_dim) scale is
+// applied to the dot products.
+
+constexpr int ATT_WAVES = 16;
 
 template <typename T, int DH>
-__global__ __launch_bounds__(256) void attn_partial_kernel(AttnArgs a) {
+__global__ __launch_bounds__(64 * ATT_WAVES) void attn_prefix_kernel(AttnArgs a) {
+  constexpr int NT = 64 * ATT_WAVES;
+  constexpr int EPU = 16 / sizeof(T);  // elements per 16-byte unit
+  constexpr int UPR = DH / EPU;        // units per key row
+  constexpr int TU = (64 * UPR + NT - 1) / NT;
   __shared__ float Ks[64][DH + 1];
   __shared__ float Vs[64][DH + 1];
-  __shared__ float es[4][64];
-  const int h = blockIdx.x, s = blockIdx.y;
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const bool tree = s >= a.S;
-  const int key0 = tree ? (s - a.S) * 64 : s * 64;
-  const int nk = tree ? min(64, a.N - key0) : min(64, a.P - key0);
-  const T* kb = tree ? (const T*)a.kt + ((size_t)h * a.max_nodes + key0) * DH
-                     : (const T*)a.kc + ((size_t)h * a.max_ctx + key0) * DH;
-  const T* vb = tree ? (const T*)a.vt + ((size_t)h * a.max_nodes + key0) * DH
-                     : (const T*)a.vc + ((size_t)h * a.max_ctx + key0) * DH;
-  for (int idx = threadIdx.x; idx < 64 * DH; idx += 256) {
-    const int j = idx / DH, c = idx - j * DH;
-    float kv = 0.f, vv = 0.f;
-    if (j < nk) {
-      kv = ldT(kb, (size_t)j * DH + c);
-      vv = ldT(vb, (size_t)j * DH + c);
+  __shared__ float qs[64][DH];
+  __shared__ float es[ATT_WAVES][64];
+  const int h = blockIdx.x, s = blockIdx.y, tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+  const int key0 = s * 64, nk = min(64, a.P - key0);
+  const T* kc = (const T*)a.kc + ((size_t)h * a.max_ctx + key0) * DH;
+  const T* vc = (const T*)a.vc + ((size_t)h * a.max_ctx + key0) * DH;
+  {
+    u32x4 kr[TU], vr[TU];
+#pragma unroll
+    for (int i = 0; i < TU; ++i) {
+      const int idx = min(tid + i * NT, 64 * UPR - 1);
+      const int j = min(idx / UPR, nk - 1), c = (idx % UPR) * EPU;
+      kr[i] = *(const u32x4*)(kc + (size_t)j * DH + c);
+      vr[i] = *(const u32x4*)(vc + (size_t)j * DH + c);
     }
-    Ks[j][c] = kv;
-    Vs[j][c] = vv;
+#pragma unroll
+    for (int i = 0; i < TU; ++i) {
+      const int idx = tid + i * NT;
+      if (idx < 64 * UPR) {
+        const int j = idx / UPR, c = (idx % UPR) * EPU;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          if constexpr (sizeof(T) == 2) {
+            Ks[j][c + 2 * e] = __uint_as_float(kr[i][e] << 16);
+            Ks[j][c + 2 * e + 1] = __uint_as_float(kr[i][e] & 0xffff0000u);
+            Vs[j][c + 2 * e] = __uint_as_float(vr[i][e] << 16);
+            Vs[j][c + 2 * e + 1] = __uint_as_float(vr[i][e] & 0xffff0000u);
+          } else {
+            Ks[j][c + e] = __uint_as_float(kr[i][e]);
+            Vs[j][c + e] = __uint_as_float(vr[i][e]);
+          }
+        }
+      }
+    }
   }
-  __syncthreads();
-  for (int n0 = 0; n0 < a.N; n0 += 4) {
-    const int n = n0 + w;
-    if (n < a.N) {
-      const float* qn = a.q + (size_t)n * a.d + h * DH;
-      bool valid = lane < nk;
-      if (tree && valid) {
-        const int j = key0 + lane;
-        valid = (a.anc[(size_t)n * a.W + (j >> 6)] >> (j & 63)) & 1ull;
-      }
-      float dot = 0.f;
-#pragma unroll 8
-      for (int c = 0; c < DH; ++c) dot = fmaf(qn[c], Ks[lane][c], dot);
-      const float sc = valid ? dot * a.scale : -INFINITY;
-      const float m = wave_max(sc);
-      float* out = a.part + (((size_t)h * a.NS + s) * a.N + n) * (DH + 2);
-      if (m == -INFINITY) {
-        if (lane < DH) out[2 + lane] = 0.f;
-        if (lane == 0) {
-          out[0] = -INFINITY;
-          out[1] = 0.f;
-        }
-      } else {
-        const float e = valid ? expf(sc - m) : 0.f;
-        const float z = wave_sum(e);
-        es[w][lane] = e;
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-        if (lane < DH) {
-          float o = 0.f;
-#pragma unroll 8
-          for (int j = 0; j < 64; ++j) o = fmaf(es[w][j], Vs[j][lane], o);
-          out[2 + lane] = o;
-        }
-        if (lane == 0) {
-          out[0] = m;
-          out[1] = z;
-        }
-      }
+  for (int n0 = 0; n0 < a.N; n0 += 64) {
+    const int nn = min(64, a.N - n0);
+    __syncthreads();  // tile staged / previous node chunk done with qs
+    for (int idx = tid; idx < 64 * DH / 4; idx += NT) {
+      const int r = idx / (DH / 4), c = (idx % (DH / 4)) * 4;
+      const float4 v4 = *(const float4*)(a.q + (size_t)(n0 + min(r, nn - 1)) * a.d + h * DH + c);
+      qs[r][c] = v4.x;
+      qs[r][c + 1] = v4.y;
+      qs[r][c + 2] = v4.z;
+      qs[r][c + 3] = v4.w;
     }
     __syncthreads();
+    for (int r = w; r < nn; r += ATT_WAVES) {
+      const int n = n0 + r;
+      float dot = 0.f;
+#pragma unroll 16
+      for (int c = 0; c < DH; ++c) dot = fmaf(qs[r][c], Ks[lane][c], dot);
+      const bool valid = lane < nk;
+      const float sc = valid ? dot * a.scale : -INFINITY;
+      const float m = wave_max(sc);
+      const float e = valid ? expf(sc - m) : 0.f;
+      const float z = wave_sum(e);
+      es[w][lane] = e;
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      float* out = a.part + (((size_t)h * a.S + s) * a.N + n) * (DH + 2);
+      if (lane < DH) {
+        float o = 0.f;
+#pragma unroll 16
+        for (int j = 0; j < 64; ++j) o = fmaf(es[w][j], Vs[j][lane], o);
+        out[2 + lane] = o;
+      }
+      if (lane == 0) {
+        out[0] = m;
+        out[1] = z;
+      }
+      __builtin_amdgcn_wave_barrier();
+    }
   }
 }
 
-template <int DH, typename OUT>
-__global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restrict__ part, int NS, int N, int H,
-                                                           int d, OUT* __restrict__ out, int ldo, size_t plane) {
+template <typename T, int DH>
+__global__ __launch_bounds__(256) void attn_combine_kernel(AttnArgs a) {
+  constexpr int EPU = 16 / sizeof(T);
   const int pair = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
-  if (pair >= N * H) return;
-  const int n = pair / H, h = pair - n * H;
-  const size_t stride = (size_t)N * (DH + 2);
-  const float* p = part + ((size_t)h * NS * N + n) * (DH + 2);
-  float m = -INFINITY;
-  for (int s = 0; s < NS; ++s) m = fmaxf(m, p[s * stride]);
-  float z = 0.f, o = 0.f;
-  for (int s = 0; s < NS; ++s) {
-    const float ms = p[s * stride];
-    if (ms == -INFINITY) continue;
-    const float wgt = expf(ms - m);
-    z = fmaf(p[s * stride + 1], wgt, z);
-    if (lane < DH) o = fmaf(p[s * stride + 2 + lane], wgt, o);
+  if (pair >= a.N * a.H) return;
+  const int n = pair / a.H, h = pair - n * a.H;
+  float qv[DH];
+#pragma unroll
+  for (int c = 0; c < DH; c += 4) {
+    const float4 t4 = *(const float4*)(a.q + (size_t)n * a.d + h * DH + c);
+    qv[c] = t4.x;
+    qv[c + 1] = t4.y;
+    qv[c + 2] = t4.z;
+    qv[c + 3] = t4.w;
   }
-  if (lane < DH) st_act(out, (size_t)n * ldo + h * DH + lane, plane, o / z);
+  const int dn = a.depth[n];
+  const int* al = a.ancl + a.anc_off[n];
+  const T* kt = (const T*)a.kt + (size_t)h * a.max_nodes * DH;
+  const T* vt = (const T*)a.vt + (size_t)h * a.max_nodes * DH;
+  const size_t pstride = (size_t)a.N * (DH + 2);  // between tiles
+  const float* pp = a.part + ((size_t)h * a.S * a.N + n) * (DH + 2);
+
+  // running (max, sum, output) over prefix tiles, then tree keys; values are
+  // fetched 16 at a time (clamped) with every load issued before any use
+  constexpr int B = 16;
+  float m = -INFINITY, l = 0.f, o = 0.f;
+  const int lc = min(lane, DH - 1);
+  for (int s0 = 0; s0 < a.S; s0 += B) {
+    const int cnt = min(B, a.S - s0);
+    const int sl = s0 + min(lane, cnt - 1);
+    const float ms0 = pp[(size_t)sl * pstride], zs0 = pp[(size_t)sl * pstride + 1];
+    float ov[B];
+#pragma unroll
+    for (int j = 0; j < B; ++j) ov[j] = pp[(size_t)(s0 + min(j, cnt - 1)) * pstride + 2 + lc];
+    const float ms = lane < cnt ? ms0 : -INFINITY;
+    const float mn = fmaxf(m, wave_max(ms));
+    const float alpha = expf(m - mn);
+    const float ws = lane < cnt ? expf(ms - mn) : 0.f;
+    l = l * alpha + wave_sum(lane < cnt ? zs0 * ws : 0.f);
+    float acc = 0.f;
+#pragma unroll
+    for (int j = 0; j < B; ++j) acc = fmaf(ov[j], __shfl(ws, j), acc);
+    o = o * alpha + acc;
+    m = mn;
+  }
+  for (int t0 = 0; t0 <= dn; t0 += B) {
+    const int cnt = min(B, dn + 1 - t0);
+    const int t = t0 + min(lane, cnt - 1);
+    const int key = al[t];
+    float vv[B];
+#pragma unroll
+    for (int j = 0; j < B; ++j) vv[j] = ldT(vt, (size_t)__shfl(key, j) * DH + lc);
+    float dot = 0.f;
+    const T* kr = kt + (size_t)key * DH;
+#pragma unroll
+    for (int c = 0; c < DH; c += EPU) {
+      const u32x4 ku = *(const u32x4*)(kr + c);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        if constexpr (sizeof(T) == 2) {
+          dot = fmaf(qv[c + 2 * e], __uint_as_float(ku[e] << 16), dot);
+          dot = fmaf(qv[c + 2 * e + 1], __uint_as_float(ku[e] & 0xffff0000u), dot);
+        } else {
+          dot = fmaf(qv[c + e], __uint_as_float(ku[e]), dot);
+        }
+      }
+    }
+    const bool valid = lane < cnt;
+    const float sc = valid ? dot * a.scale : -INFINITY;
+    const float mn = fmaxf(m, wave_max(sc));
+    const float alpha = expf(m - mn);
+    const float p = valid ? expf(sc - mn) : 0.f;
+    l = l * alpha + wave_sum(p);
+    float acc = 0.f;
+#pragma unroll
+    for (int j = 0; j < B; ++j) acc = fmaf(__shfl(p, j), vv[j], acc);
+    o = o * alpha + acc;
+    m = mn;
+  }
+  if (lane < DH) st_act((T*)a.out, n, h * DH + lane, a.ldo, o / l);
 }
 
 hipError_t launch_attn(int f32, int DH, const AttnArgs& a, hipStream_t s) {
-  dim3 grid(a.H, a.NS);
-  if (f32) {
-    if (DH == 64) attn_partial_kernel<float, 64><<<grid, 256, 0, s>>>(a);
-    else attn_partial_kernel<float, 32><<<grid, 256, 0, s>>>(a);
-  } else {
-    if (DH == 64) attn_partial_kernel<uint16_t, 64><<<grid, 256, 0, s>>>(a);
-    else attn_partial_kernel<uint16_t, 32><<<grid, 256, 0, s>>>(a);
+  if (a.S > 0) {
+    dim3 grid(a.H, a.S);
+    const int nt = 64 * ATT_WAVES;
+    if (f32) {
+      if (DH == 64) attn_prefix_kernel<float, 64><<<grid, nt, 0, s>>>(a);
+      else attn_prefix_kernel<float, 32><<<grid, nt, 0, s>>>(a);
+    } else {
+      if (DH == 64) attn_prefix_kernel<uint16_t, 64><<<grid, nt, 0, s>>>(a);
+      else attn_prefix_kernel<uint16_t, 32><<<grid, nt, 0, s>>>(a);
+    }
   }
-  return hipGetLastError();
-}
-
-hipError_t launch_attn_combine(int f32, int DH, const float* part, int NS, int N, int H, int d, void* out, int ldo,
-                               size_t plane, hipStream_t s) {
-  const int blocks = (N * H + 3) / 4;
+  const int blocks = (a.N * a.H + 3) / 4;
   if (f32) {
-    if (DH == 64) attn_combine_kernel<64, float><<<blocks, 256, 0, s>>>(part, NS, N, H, d, (float*)out, ldo, 0);
-    else attn_combine_kernel<32, float><<<blocks, 256, 0, s>>>(part, NS, N, H, d, (float*)out, ldo, 0);
+    if (DH == 64) attn_combine_kernel<float, 64><<<blocks, 256, 0, s>>>(a);
+    else attn_combine_kernel<float, 32><<<blocks, 256, 0, s>>>(a);
   } else {
-    if (DH == 64)
-      attn_combine_kernel<64, uint16_t><<<blocks, 256, 0, s>>>(part, NS, N, H, d, (uint16_t*)out, ldo, plane);
-    else
-      attn_combine_kernel<32, uint16_t><<<blocks, 256, 0, s>>>(part, NS, N, H, d, (uint16_t*)out, ldo, plane);
+    if (DH == 64) attn_combine_kernel<uint16_t, 64><<<blocks, 256, 0, s>>>(a);
+    else attn_combine_kernel<uint16_t, 32><<<blocks, 256, 0, s>>>(a);
   }
   return hipGetLastError();
 }

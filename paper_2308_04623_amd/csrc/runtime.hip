@@ -59,7 +59,7 @@ struct ssd_model {
 
 struct ssd_kv {
   const ssd_model* m = nullptr;
-  int max_ctx = 0, max_nodes = 0, npad = 0, ns_max = 0, W = 0;
+  int max_ctx = 0, max_nodes = 0, npad = 0;
   void *kc = nullptr, *vc = nullptr, *kt = nullptr, *vt = nullptr;
   void* ws = nullptr;  // one device allocation for every workspace below
   float* x = nullptr;
@@ -67,9 +67,9 @@ struct ssd_kv {
   void* act_a = nullptr;  // LN outputs [npad][d]
   void* act_o = nullptr;  // attention outputs [npad][d]
   void* act_f = nullptr;  // GELU outputs [npad][d_mlp]
-  float* part = nullptr;  // attention partials
-  // tokens, positions, depths, parents (max_nodes each), then ancestor masks [n][ceil(n/64)]
-  int* d_tree = nullptr;
+  float* part = nullptr;  // split-K partial sums [kMaxSplits][max_nodes][d]
+  float* apart = nullptr; // attention prefix partials [H][ceil(max_ctx/64)][max_nodes][head_dim + 2]
+  int* d_tree = nullptr;  // the staged tree (see stage_bytes)
   int* d_accept_tree = nullptr;  // tokens[N] parents[N] depth[N] for accept
   int* d_argmax = nullptr;
   double *d_r = nullptr, *d_p = nullptr, *d_qq = nullptr;
@@ -246,9 +246,10 @@ extern "C" ssd_status ssd_kv_bytes(const ssd_config* cfg, int32_t max_ctx, int32
   return SSD_OK;
 }
 
+// staged tree: tokens, positions, depths, parents, root-path offsets
+// (max_nodes each), then the root paths themselves (at most n(n+1)/2 entries)
 static size_t stage_bytes(int max_nodes) {
-  const int W = (max_nodes + 63) / 64;
-  return (size_t)4 * max_nodes * 4 + (size_t)max_nodes * W * 8;
+  return (size_t)5 * max_nodes * 4 + (size_t)max_nodes * (max_nodes + 1) / 2 * 4;
 }
 
 extern "C" ssd_status ssd_kv_create(const ssd_model* m, int32_t max_ctx, int32_t max_nodes, void* k_cache,
@@ -275,8 +276,6 @@ extern "C" ssd_status ssd_kv_create(const ssd_model* m, int32_t max_ctx, int32_t
   } else {
     kv->npad = round_up(max_nodes, 256);
   }
-  kv->W = (max_nodes + 63) / 64;
-  kv->ns_max = (max_ctx + 63) / 64 + (max_nodes + 63) / 64;
   const size_t es = m->f32 ? 4 : 2;
   const int d = c.d_model, M = c.d_mlp, V = c.vocab;
   size_t off = 0;
@@ -286,11 +285,12 @@ extern "C" ssd_status ssd_kv_create(const ssd_model* m, int32_t max_ctx, int32_t
     return o;
   };
   const size_t o_x = take((size_t)max_nodes * d * 4), o_q = take((size_t)max_nodes * d * 4);
-  // bf16 models keep every GEMM input as a hi plane and a lo plane
+  // bf16 models keep every GEMM input as hi and lo bf16 planes
   const size_t planes = m->f32 ? 1 : 2;
   const size_t o_a = take(planes * kv->npad * d * es), o_o = take(planes * kv->npad * d * es);
   const size_t o_f = take(planes * kv->npad * M * es);
-  const size_t o_part = take((size_t)c.n_head * kv->ns_max * max_nodes * (m->dh + 2) * 4);
+  const size_t o_part = take((size_t)kMaxSplits * max_nodes * d * 4);  // split-K partials
+  const size_t o_apart = take((size_t)c.n_head * ((max_ctx + 63) / 64) * max_nodes * (m->dh + 2) * 4);
   const size_t o_tree = take(stage_bytes(max_nodes));
   const size_t o_at = take((size_t)3 * max_nodes * 4), o_am = take((size_t)max_nodes * 4);
   const size_t o_r = take((size_t)V * 8), o_p = take((size_t)V * 8), o_qq = take((size_t)V * 8);
@@ -309,6 +309,7 @@ extern "C" ssd_status ssd_kv_create(const ssd_model* m, int32_t max_ctx, int32_t
   kv->act_o = b + o_o;
   kv->act_f = b + o_f;
   kv->part = (float*)(b + o_part);
+  kv->apart = (float*)(b + o_apart);
   kv->d_tree = (int*)(b + o_tree);
   kv->d_accept_tree = (int*)(b + o_at);
   kv->d_argmax = (int*)(b + o_am);
@@ -373,66 +374,93 @@ static ssd_status check_verify_args(const ssd_model* m, const ssd_kv* kv, int32_
   return SSD_OK;
 }
 
-// Fills a staging buffer: tokens, positions, depths, parents, ancestor masks.
-static void fill_stage(char* host, int P, const int32_t* tokens, const int32_t* parents, int n, int max_nodes) {
+// Fills a staging buffer (see stage_bytes); returns the bytes used.
+static size_t fill_stage(char* host, int P, const int32_t* tokens, const int32_t* parents, int n, int max_nodes) {
   int32_t* t = (int32_t*)host;
   int32_t* pos = t + max_nodes;
   int32_t* dep = pos + max_nodes;
   int32_t* par = dep + max_nodes;
-  uint64_t* anc = (uint64_t*)(par + max_nodes);
-  ssd_tree_prep(parents, n, dep, anc);  // validated by the caller
+  int32_t* off = par + max_nodes;
+  int32_t* paths = off + max_nodes;
+  ssd_tree_prep(parents, n, dep, nullptr);  // validated by the caller
+  int32_t total = 0;
   for (int i = 0; i < n; ++i) {
     t[i] = tokens[i];
     pos[i] = P + dep[i];
     par[i] = parents[i];
+    off[i] = total;
+    // root path of node i: walk up, filling from the end
+    int32_t j = i;
+    for (int k = dep[i]; k >= 0; --k) {
+      paths[total + k] = j;
+      j = parents[j];
+    }
+    total += dep[i] + 1;
   }
+  return (size_t)5 * max_nodes * 4 + (size_t)total * 4;
 }
 
 // One weight GEMM of the pass over n nodes: fp32 models use the plain
-// kernel; bf16 models the vector-ALU kernel for small node counts (or when
-// pinned) and the matrix-core kernel otherwise, in node groups.
+// kernel; bf16 models the vector-ALU kernel for few nodes (or when pinned)
+// and the matrix-core kernel otherwise, in node groups of 16 / 256.
 static hipError_t run_gemm(const ssd_model* m, int n, int kind, const void* Wraw, const void* Wp, int rows, int K,
-                           const void* act, int lda, size_t plane, const Epi& ep, hipStream_t s) {
-  if (m->f32) return launch_gemm_f32(kind, (const float*)Wraw, rows, K, (const float*)act, lda, ep, s);
-  const int path = g_gemm_path == 0 ? (n <= kVecMaxNodes ? 1 : 2) : g_gemm_path;
-  const int group = path == 1 ? 16 : 256;
+                           const void* act, const Epi& ep, hipStream_t s) {
+  if (m->f32) return launch_gemm_f32(kind, (const float*)Wraw, rows, K, (const float*)act, K, ep, s);
+  const int vec = (g_gemm_path == 0 ? (n <= kVecMaxNodes ? 1 : 2) : g_gemm_path) == 1;
+  const int group = vec ? 16 : 256;
+  // one k-split for every node group, so all nodes leave the same partials
+  int S = 1;
+  const int kcs = gemm_split_kc(rows, K, std::min(n, group), vec, kind == EPI_PARTIAL, &S);
   for (int n0 = 0; n0 < n; n0 += group) {
     Epi e2 = ep;
     e2.node0 = n0;
     e2.N = std::min(group, n - n0);
-    const uint16_t* a = (const uint16_t*)act + (size_t)n0 * lda;
-    hipError_t r = path == 1 ? launch_gemm_vec(kind, Wp, rows, K, a, lda, plane, e2, s)
-                             : launch_gemm_mfma(kind, Wp, rows, K, a, lda, plane, e2, s);
+    // fragment tiles of 16 nodes, each K/32 fragment pairs of 1024 elements
+    const uint16_t* a = (const uint16_t*)act + (size_t)(n0 / 16) * (K / 32) * 1024;
+    hipError_t r = launch_gemm_bf16(kind, vec, Wp, rows, K, a, kcs, e2, s);
     if (r != hipSuccess) return r;
   }
   return hipSuccess;
 }
 
+// number of split-K partials a residual GEMM leaves for the next LayerNorm
+static int resid_splits(const ssd_model* m, int n, int rows, int K) {
+  if (m->f32) return 0;
+  const int vec = (g_gemm_path == 0 ? (n <= kVecMaxNodes ? 1 : 2) : g_gemm_path) == 1;
+  int S = 1;
+  gemm_split_kc(rows, K, std::min(n, vec ? 16 : 256), vec, 1, &S);
+  return S;
+}
+
 static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int32_t n, const char* stage_host,
-                                 float* logits, hipStream_t s) {
+                                 size_t stage_used, float* logits, hipStream_t s) {
   const ssd_config& c = m->cfg;
   const int d = c.d_model, H = c.n_head, DH = m->dh, M = c.d_mlp, V = c.vocab, L = c.n_layer;
-  const int maxn = kv->max_nodes, W = (n + 63) / 64;
+  const int maxn = kv->max_nodes;
   const int f32 = m->f32 ? 1 : 0;
   const size_t es = f32 ? 4 : 2;
-  // device copy of the staged tree; anc rows are packed with W = ceil(n/64)
-  const size_t head_bytes = (size_t)4 * maxn * 4;
-  HIP_TRY(hipMemcpyAsync(kv->d_tree, stage_host, head_bytes + (size_t)n * W * 8, hipMemcpyHostToDevice, s));
+  HIP_TRY(hipMemcpyAsync(kv->d_tree, stage_host, stage_used, hipMemcpyHostToDevice, s));
   const int* d_tok = kv->d_tree;
   const int* d_pos = kv->d_tree + maxn;
+  const int* d_dep = kv->d_tree + 2 * maxn;
+  const int* d_off = kv->d_tree + 4 * maxn;
+  const int* d_paths = kv->d_tree + 5 * maxn;
   HIP_TRY(launch_embed(f32, m->wte, m->wpe, d_tok, d_pos, n, d, kv->x, s));
 
-  const int S = (P + 63) / 64, T = (n + 63) / 64, NS = S + T;
-  // element distance between the hi and lo planes of each activation buffer
-  const size_t pl_d = (size_t)kv->npad * d, pl_m = (size_t)kv->npad * M;
-  auto gemm = [&](int kind, const void* Wraw, const void* Wp, int rows, int K, const void* act, int lda,
-                  const Epi& ep) -> hipError_t {
-    return run_gemm(m, n, kind, Wraw, Wp, rows, K, act, lda, lda == d ? pl_d : pl_m, ep, s);
-  };
+  // GEMM-input leading dimensions (fp32: row stride; bf16: k-steps)
+  const int ld_d = f32 ? d : d / 32, ld_m = f32 ? M : M / 32;
+  const size_t pstride = (size_t)maxn * d;
+  // fp32 models add residuals inside the GEMM; bf16 models leave split-K
+  // partials that the next LayerNorm adds (with the bias)
+  const int kind_res = f32 ? EPI_RESID : EPI_PARTIAL;
+  const int s_o = resid_splits(m, n, d, d), s_pr = resid_splits(m, n, d, M);
+  const size_t kv_layer = (size_t)H * DH;  // elements per K/V row across heads
 
-  const size_t kv_layer = (size_t)H * DH;  // elements per row across heads
+  int pend_S = 0;               // partials waiting to be added to x
+  const void* pend_bias = nullptr;
   for (int l = 0; l < L; ++l) {
-    HIP_TRY(launch_ln(f32, kv->x, n, d, m->ln1_g[l], m->ln1_b[l], c.ln_eps, kv->act_a, d, pl_d, s));
+    HIP_TRY(launch_ln(f32, kv->x, n, d, kv->part, pend_S, pstride, pend_bias, m->ln1_g[l], m->ln1_b[l], c.ln_eps,
+                      kv->act_a, ld_d, s));
     Epi e{};
     e.bias = m->b_qkv[l];
     e.N = n;
@@ -444,7 +472,7 @@ static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int3
     e.H = H;
     e.DH = DH;
     e.max_nodes = maxn;
-    HIP_TRY(gemm(EPI_QKV, m->w_qkv[l], f32 ? nullptr : m->p_qkv[l], 3 * d, d, kv->act_a, d, e));
+    HIP_TRY(run_gemm(m, n, EPI_QKV, m->w_qkv[l], f32 ? nullptr : m->p_qkv[l], 3 * d, d, kv->act_a, e, s));
 
     AttnArgs a{};
     a.q = kv->q;
@@ -452,49 +480,57 @@ static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int3
     a.vc = kv->vc ? (const char*)kv->vc + (size_t)l * kv_layer * kv->max_ctx * es : nullptr;
     a.kt = e.kt;
     a.vt = e.vt;
-    a.anc = (const uint64_t*)((const char*)kv->d_tree + head_bytes);
-    a.part = kv->part;
+    a.depth = d_dep;
+    a.anc_off = d_off;
+    a.ancl = d_paths;
+    a.out = kv->act_o;
+    a.ldo = ld_d;
+    a.part = kv->apart;
+    a.S = (P + 63) / 64;
     a.N = n;
     a.P = P;
     a.d = d;
     a.H = H;
     a.max_ctx = kv->max_ctx;
     a.max_nodes = maxn;
-    a.W = W;
-    a.S = S;
-    a.NS = NS;
     a.scale = 1.0f / std::sqrt((float)DH);
     HIP_TRY(launch_attn(f32, DH, a, s));
-    HIP_TRY(launch_attn_combine(f32, DH, kv->part, NS, n, H, d, kv->act_o, d, pl_d, s));
 
     Epi eo{};
-    eo.bias = m->b_o[l];
+    eo.bias = f32 ? m->b_o[l] : nullptr;
     eo.N = n;
     eo.M = d;
     eo.d = d;
     eo.x = kv->x;
-    HIP_TRY(gemm(EPI_RESID, m->w_o[l], f32 ? nullptr : m->p_o[l], d, d, kv->act_o, d, eo));
+    eo.part = kv->part;
+    eo.part_stride = (long long)pstride;
+    HIP_TRY(run_gemm(m, n, kind_res, m->w_o[l], f32 ? nullptr : m->p_o[l], d, d, kv->act_o, eo, s));
 
-    HIP_TRY(launch_ln(f32, kv->x, n, d, m->ln2_g[l], m->ln2_b[l], c.ln_eps, kv->act_a, d, pl_d, s));
+    HIP_TRY(launch_ln(f32, kv->x, n, d, kv->part, f32 ? 0 : s_o, pstride, m->b_o[l], m->ln2_g[l], m->ln2_b[l],
+                      c.ln_eps, kv->act_a, ld_d, s));
     Epi ef{};
     ef.bias = m->b_fc[l];
     ef.N = n;
     ef.M = M;
     ef.d = d;
     ef.out = kv->act_f;
-    ef.ldo = M;
-    ef.out_plane = (long long)pl_m;
-    HIP_TRY(gemm(EPI_GELU, m->w_fc[l], f32 ? nullptr : m->p_fc[l], M, d, kv->act_a, d, ef));
+    ef.ldo = ld_m;
+    HIP_TRY(run_gemm(m, n, EPI_GELU, m->w_fc[l], f32 ? nullptr : m->p_fc[l], M, d, kv->act_a, ef, s));
 
     Epi ep{};
-    ep.bias = m->b_pr[l];
+    ep.bias = f32 ? m->b_pr[l] : nullptr;
     ep.N = n;
     ep.M = d;
     ep.d = d;
     ep.x = kv->x;
-    HIP_TRY(gemm(EPI_RESID, m->w_pr[l], f32 ? nullptr : m->p_pr[l], d, M, kv->act_f, M, ep));
+    ep.part = kv->part;
+    ep.part_stride = (long long)pstride;
+    HIP_TRY(run_gemm(m, n, kind_res, m->w_pr[l], f32 ? nullptr : m->p_pr[l], d, M, kv->act_f, ep, s));
+    pend_S = f32 ? 0 : s_pr;
+    pend_bias = m->b_pr[l];
   }
-  HIP_TRY(launch_ln(f32, kv->x, n, d, m->lnf_g, m->lnf_b, c.ln_eps, kv->act_a, d, pl_d, s));
+  HIP_TRY(launch_ln(f32, kv->x, n, d, kv->part, pend_S, pstride, pend_bias, m->lnf_g, m->lnf_b, c.ln_eps, kv->act_a,
+                    ld_d, s));
   Epi eh{};
   eh.bias = nullptr;
   eh.N = n;
@@ -502,7 +538,7 @@ static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int3
   eh.d = d;
   eh.logits = logits;
   eh.ldl = V;
-  HIP_TRY(gemm(EPI_LOGITS, m->wte, f32 ? nullptr : m->p_head, V, d, kv->act_a, d, eh));
+  HIP_TRY(run_gemm(m, n, EPI_LOGITS, m->wte, f32 ? nullptr : m->p_head, V, d, kv->act_a, eh, s));
   return SSD_OK;
 }
 
@@ -516,8 +552,8 @@ extern "C" ssd_status ssd_tree_verify(const ssd_model* m, ssd_kv* kv, int32_t pr
   int slot = -1;
   st = acquire_slot(kv, &host, &slot);
   if (st != SSD_OK) return st;
-  fill_stage(host, prefix_len, tree_tokens, parent_idx, n_nodes, kv->max_nodes);
-  st = enqueue_verify(m, kv, prefix_len, n_nodes, host, logits, s);
+  const size_t used = fill_stage(host, prefix_len, tree_tokens, parent_idx, n_nodes, kv->max_nodes);
+  st = enqueue_verify(m, kv, prefix_len, n_nodes, host, used, logits, s);
   ssd_status st2 = release_slot(kv, slot, s);
   return st != SSD_OK ? st : st2;
 }
@@ -535,7 +571,7 @@ extern "C" ssd_status ssd_graph_capture_verify(const ssd_model* m, ssd_kv* kv, i
     delete g;
     return fail(SSD_E_DEVICE, std::string("hipHostMalloc: ") + hipGetErrorString(e));
   }
-  fill_stage(g->pinned, prefix_len, tree_tokens, parent_idx, n_nodes, kv->max_nodes);
+  const size_t used = fill_stage(g->pinned, prefix_len, tree_tokens, parent_idx, n_nodes, kv->max_nodes);
   // capture on a private stream (the legacy null stream cannot be captured);
   // the graph is later launched on the caller's stream
   (void)stream;
@@ -547,7 +583,7 @@ extern "C" ssd_status ssd_graph_capture_verify(const ssd_model* m, ssd_kv* kv, i
     ssd_graph_destroy(g);
     return fail(SSD_E_DEVICE, std::string("hipStreamBeginCapture: ") + hipGetErrorString(e));
   }
-  st = enqueue_verify(m, kv, prefix_len, n_nodes, g->pinned, logits, cs);
+  st = enqueue_verify(m, kv, prefix_len, n_nodes, g->pinned, used, logits, cs);
   hipGraph_t graph = nullptr;
   e = hipStreamEndCapture(cs, &graph);
   (void)hipStreamDestroy(cs);
@@ -584,19 +620,23 @@ extern "C" ssd_status ssd_launch_gemm(const ssd_model* m, ssd_kv* kv, int32_t wh
                                       void* stream) {
   if (!m || !kv) return fail(SSD_E_INVALID_ARG, "null argument");
   const ssd_config& c = m->cfg;
-  if (which < 0 || which > 4 || layer < 0 || layer >= c.n_layer) return fail(SSD_E_INVALID_ARG, "bad matrix id");
+  if (which < 0 || which > 3 || layer < 0 || layer >= c.n_layer) return fail(SSD_E_INVALID_ARG, "bad matrix id");
   if (n_nodes <= 0 || n_nodes > kv->max_nodes) return fail(SSD_E_CAPACITY, "n_nodes outside the session");
   const int d = c.d_model, M = c.d_mlp, es = m->f32 ? 4 : 2;
-  // outputs land in the session's own buffers: q / tree scratch, x, act_f, or
-  // the attention-partials buffer reused as a logits sink
+  // outputs land in the session's own workspaces (q and tree scratch, split-K
+  // partials or x, the MLP activation buffer)
   Epi e{};
   e.N = n_nodes;
   e.d = d;
   e.H = c.n_head;
   e.DH = m->dh;
   e.max_nodes = kv->max_nodes;
+  e.x = kv->x;
+  e.part = kv->part;
+  e.part_stride = (long long)kv->max_nodes * d;
+  const int kind_res = m->f32 ? EPI_RESID : EPI_PARTIAL;
   const void *Wraw = nullptr, *Wp = nullptr, *act = kv->act_a;
-  int rows = d, K = d, lda = d, kind = EPI_RESID;
+  int rows = d, K = d, lda = d, kind = kind_res;
   switch (which) {
     case 0:
       kind = EPI_QKV; rows = 3 * d; Wraw = m->w_qkv[layer]; e.bias = m->b_qkv[layer]; e.q = kv->q;
@@ -605,31 +645,22 @@ extern "C" ssd_status ssd_launch_gemm(const ssd_model* m, ssd_kv* kv, int32_t wh
       if (!m->f32) Wp = m->p_qkv[layer];
       break;
     case 1:
-      Wraw = m->w_o[layer]; e.bias = m->b_o[layer]; e.x = kv->x; act = kv->act_o;
+      Wraw = m->w_o[layer]; act = kv->act_o; if (m->f32) e.bias = m->b_o[layer];
       if (!m->f32) Wp = m->p_o[layer];
       break;
     case 2:
-      kind = EPI_GELU; rows = M; Wraw = m->w_fc[layer]; e.bias = m->b_fc[layer]; e.out = kv->act_f; e.ldo = M;
-      e.out_plane = (long long)kv->npad * M;
+      kind = EPI_GELU; rows = M; Wraw = m->w_fc[layer]; e.bias = m->b_fc[layer]; e.out = kv->act_f;
+      e.ldo = m->f32 ? M : M / 32;
       if (!m->f32) Wp = m->p_fc[layer];
       break;
-    case 3:
-      K = M; lda = M; Wraw = m->w_pr[layer]; e.bias = m->b_pr[layer]; e.x = kv->x; act = kv->act_f;
+    default:
+      K = M; lda = M; Wraw = m->w_pr[layer]; act = kv->act_f; if (m->f32) e.bias = m->b_pr[layer];
       if (!m->f32) Wp = m->p_pr[layer];
       break;
-    default: {
-      kind = EPI_LOGITS; rows = c.vocab; Wraw = m->wte; Wp = m->p_head;
-      const size_t need = (size_t)n_nodes * c.vocab * 4;
-      const size_t have = (size_t)c.n_head * kv->ns_max * kv->max_nodes * (m->dh + 2) * 4;
-      if (need > have) return fail(SSD_E_CAPACITY, "logits sink too small for this node count");
-      e.logits = kv->part;
-      e.ldl = c.vocab;
-      break;
-    }
   }
   e.M = rows;
-  const size_t plane = (size_t)kv->npad * lda;
-  HIP_TRY(run_gemm(m, n_nodes, kind, Wraw, Wp, rows, K, act, lda, plane, e, (hipStream_t)stream));
+  (void)lda;
+  HIP_TRY(run_gemm(m, n_nodes, kind, Wraw, Wp, rows, K, act, e, (hipStream_t)stream));
   return SSD_OK;
 }
 

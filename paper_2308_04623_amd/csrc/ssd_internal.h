@@ -12,8 +12,12 @@ enum EpiKind : int {
   EPI_QKV = 0,    // +bias; o < d -> q (fp32); d <= o < 2d -> K scratch; 2d <= o -> V scratch
   EPI_RESID = 1,  // x[n][o] += y + bias[o]
   EPI_GELU = 2,   // out[n][o] = gelu_tanh(y + bias[o])  (storage of the activation buffer)
-  EPI_LOGITS = 3  // logits[n][o] = y
+  EPI_LOGITS = 3,  // logits[n][o] = y
+  EPI_PARTIAL = 4  // part[split][n][o] = y (split-K sum of a residual GEMM, no bias)
 };
+
+// most k-splits a residual GEMM uses
+constexpr int kMaxSplits = 8;
 
 struct Epi {
   const void* bias;  // storage type, or nullptr
@@ -29,42 +33,57 @@ struct Epi {
   float* x;
   // EPI_GELU
   void* out;
-  int ldo;
-  long long out_plane;  // bf16 models: elements from the hi plane to the lo plane
+  int ldo;  // GEMM-input leading dimension: fp32 row stride, bf16 k-steps (K/32)
   // EPI_LOGITS
   float* logits;
   long long ldl;
+  // EPI_PARTIAL
+  float* part;
+  long long part_stride;  // elements between splits
+  int split;              // set by the kernel from blockIdx.y
+};
+
+// tile shape of the bf16 GEMM for a node count: node tiles of 16, row blocks
+// per workgroup, k-steps per staged chunk, nodes of the vector path
+struct GemmCfg {
+  int nt, rb, ck, nv;
 };
 
 struct AttnArgs {
-  const float* q;    // [N][d]
-  const void* kc;    // cache, this layer: [H][max_ctx][DH]
+  const float* q;       // [N][d]
+  const void* kc;       // cache, this layer: [H][max_ctx][DH]
   const void* vc;
-  const void* kt;    // tree scratch, this layer: [H][max_nodes][DH]
+  const void* kt;       // tree scratch, this layer: [H][max_nodes][DH]
   const void* vt;
-  const uint64_t* anc;  // [N][W]
-  float* part;       // [H][NS][N][DH + 2]
-  int N, P, d, H, max_ctx, max_nodes, W, S, NS;
+  const int* depth;     // [N]
+  const int* anc_off;   // [N] offset of node n's root path in ancl
+  const int* ancl;      // root paths, root first, node itself last
+  void* out;            // attention output in the GEMM-input layout
+  int ldo;              // GEMM-input leading dimension (fp32: d, bf16: d / 32)
+  float* part;          // prefix partials [H][S][N][DH + 2]: max, sum of exp, output
+  int S;                // prefix tiles of 64 cache rows
+  int N, P, d, H, max_ctx, max_nodes;
   float scale;
 };
 
 // ---- launchers (kernels.hip); all enqueue on `s` and return the launch status
 hipError_t launch_embed(int f32, const void* wte, const void* wpe, const int* tokens, const int* pos, int N, int d,
                         float* x, hipStream_t s);
-// bf16 activation buffers hold a hi plane and, `plane` elements later, a lo plane
-hipError_t launch_ln(int f32, const float* x, int N, int d, const void* g, const void* b, float eps, void* a,
-                     int lda, size_t plane, hipStream_t s);
+// x += bias + part[0..S-1] (if S > 0), then LayerNorm into the GEMM-input
+// buffer a (lda: fp32 row stride, or bf16 k-steps d / 32; see st_act)
+hipError_t launch_ln(int f32, float* x, int N, int d, const float* part, int S, size_t pstride, const void* bias,
+                     const void* g, const void* b, float eps, void* a, int lda, hipStream_t s);
 hipError_t launch_gemm_f32(int kind, const float* W, int M, int K, const float* act, int lda, const Epi& ep,
                            hipStream_t s);
-// Wp: weights packed in 16x32 bf16 fragments (see pack); act: bf16 hi plane [>= 16*NT rows][lda],
-// lo plane `plane` elements later
-hipError_t launch_gemm_mfma(int kind, const void* Wp, int M, int K, const uint16_t* act, int lda, size_t plane,
+GemmCfg gemm_cfg(int N, int vec);
+// k-steps per split and number of splits (EPI_PARTIAL only; 1 otherwise)
+int gemm_split_kc(int M, int K, int N, int vec, int want_split, int* splits);
+// Wp: weights packed in 16x32 bf16 fragments (see pack); act: activations of
+// this launch's first node in fragment order (see st_act); kcs k-steps per
+// split (grid.y = ceil(K/32 / kcs))
+hipError_t launch_gemm_bf16(int kind, int vec, const void* Wp, int M, int K, const uint16_t* act, int kcs,
                             const Epi& ep, hipStream_t s);
-hipError_t launch_gemm_vec(int kind, const void* Wp, int M, int K, const uint16_t* act, int lda, size_t plane,
-                           const Epi& ep, hipStream_t s);
 hipError_t launch_attn(int f32, int DH, const AttnArgs& a, hipStream_t s);
-hipError_t launch_attn_combine(int f32, int DH, const float* part, int NS, int N, int H, int d, void* out, int ldo,
-                               size_t plane, hipStream_t s);
 hipError_t launch_pack_bf16(const uint16_t* W, int M, int K, void* out, hipStream_t s);
 size_t packed_bytes(int M, int K);
 hipError_t launch_argmax(const float* logits, int N, int V, int* g, hipStream_t s);
