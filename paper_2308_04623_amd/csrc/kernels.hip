@@ -694,26 +694,353 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnArgs a) {
   if (lane < DH) st_act((T*)a.out, n, h * DH + lane, a.ldo, o / l);
 }
 
+// ---- bf16 models: one kernel on the matrix cores
+//
+// Work items (one wavefront each):
+//  prefix (head h, chunk c, node tile j): cache rows c*CL .. c*CL+CL-1 against
+//    16 nodes.  The workgroup (4 node tiles) stages the chunk's K rows and the
+//    transposed V rows in LDS once.  S^T = K Q^T and O^T = V^T P^T run on
+//    v_mfma_f32_16x16x32_bf16 (q and p split into bf16 hi + lo, K and V exact),
+//    32 keys at a time with an online softmax.  Rows of the K operand are
+//    ordered so that lane l ends up holding the scores of keys 8(l/16)..+7 of
+//    node l%16, which is exactly its slot of the P^T operand: no shuffles.
+//  root path (head h, node n): the node's ancestors and itself from the tree
+//    scratch, vector ALU.
+// Each item writes (max, sum of exp, unnormalised output) for its nodes and
+// bumps the counter of (h, j); the last arrival merges the nsplit + 1 parts of
+// its 16 nodes in slot order and writes the attention output.  Chunks depend
+// on P only, so a node's result does not depend on the rest of the tree.
+
+constexpr int ATM_WAVES = 4;
+
+__device__ __forceinline__ void pack_hilo8(const float (&v)[8], u32x4& hi, u32x4& lo) {
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const uint16_t h0 = f2bf(v[2 * e]), h1 = f2bf(v[2 * e + 1]);
+    const uint16_t l0 = f2bf(v[2 * e] - bf2f(h0)), l1 = f2bf(v[2 * e + 1] - bf2f(h1));
+    hi[e] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+    lo[e] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+  }
+}
+
+// eight consecutive k (k0 % 8 == 0) of node n in the bf16 GEMM-input layout (see st_act)
+__device__ __forceinline__ void st_act8(uint16_t* p, int n, int k0, int ld, const float (&v)[8]) {
+  const size_t f = (size_t)(n >> 4) * ld + (k0 >> 5);
+  const size_t off = f * 1024 + ((n & 15) + 16 * ((k0 & 31) >> 3)) * 8;
+  u32x4 hi, lo;
+  pack_hilo8(v, hi, lo);
+  *(u32x4*)(p + off) = hi;
+  *(u32x4*)(p + off + 512) = lo;
+}
+
+__device__ __forceinline__ f32x4 mfma16(const u32x4& a, const u32x4& b, const f32x4& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c, 0,
+                                                  0, 0);
+}
+
+// Parts are exchanged between workgroups without cache-wide fences: they are
+// written and read with device-scope (sc1) buffer accesses, which go to the
+// device's point of coherence instead of a per-XCD L2, and a part's stores
+// have completed (s_waitcnt) before its counter is bumped.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* p) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, 0x7fffffff, 0x00020000);
+}
+constexpr int kSc1 = 16;  // cache-policy bits of a device-scope access
+
+// part of (h, slot c, node): m, l at [0], [1]; output at [4 .. 4 + DH)
+template <int DH>
+__device__ __forceinline__ void attn_store_part(const AttnArgs& a, int h, int c, int node, int g, float m, float l,
+                                                const f32x4* o4, int no4, int d0) {
+  constexpr size_t PSTR = DH + 4;
+  const __amdgpu_buffer_rsrc_t r = buf_rsrc(a.part);
+  const unsigned off = (unsigned)((((size_t)h * (a.nsplit + 1) + c) * a.N + node) * PSTR * 4);
+  if (g == 0) {
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(m), r, off, 0, kSc1);
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(l), r, off + 4, 0, kSc1);
+  }
+  for (int t = 0; t < no4; ++t)
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, o4[t]), r, off + (4 + d0 + 16 * t) * 4, 0, kSc1);
+}
+
+// after a wave has written its part for (h, tile): count it, and if it is the
+// last part, merge all parts of the tile's nodes in slot order
+template <int DH>
+__device__ void attn_finish_tile(const AttnArgs& a, int h, int tile, int lane) {
+  __builtin_amdgcn_s_waitcnt(0);
+  unsigned old = 0;
+  unsigned* cnt = a.cnt + (size_t)h * a.cnt_ld + tile;
+  if (lane == 0) old = __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  old = __shfl(old, 0);
+  const int nv = min(16, a.N - 16 * tile);
+  if (old != (unsigned)(a.nsplit + nv - 1)) return;
+  constexpr int QD = DH / 4;
+  constexpr size_t PSTR = DH + 4;
+  constexpr int BATCH = 9;  // parts fetched per round trip (6 loads each)
+  const int NSP = a.nsplit + 1;
+  const int i = lane & 15, g = lane >> 4;
+  const int node = 16 * tile + i;
+  if (node < a.N) {
+    const __amdgpu_buffer_rsrc_t r = buf_rsrc(a.part);
+    const unsigned cstr = (unsigned)((size_t)a.N * PSTR * 4);
+    const unsigned base = (unsigned)(((size_t)h * NSP * a.N + node) * PSTR * 4);
+    float M = -INFINITY, L = 0.f, O[QD];
+#pragma unroll
+    for (int e = 0; e < QD; ++e) O[e] = 0.f;
+    for (int c0 = 0; c0 < NSP; c0 += BATCH) {
+      float mc[BATCH], lc[BATCH];
+      f32x4 v[BATCH][QD / 4];
+#pragma unroll
+      for (int j = 0; j < BATCH; ++j) {
+        const unsigned pc = base + min(c0 + j, NSP - 1) * cstr;
+        mc[j] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, pc, 0, kSc1));
+        lc[j] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, pc + 4, 0, kSc1));
+#pragma unroll
+        for (int e = 0; e < QD / 4; ++e)
+          v[j][e] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, pc + (4 + QD * g + 4 * e) * 4, 0, kSc1));
+      }
+      float mb = M;
+#pragma unroll
+      for (int j = 0; j < BATCH; ++j) mb = c0 + j < NSP ? fmaxf(mb, mc[j]) : mb;
+      const float alpha = __expf(M - mb);
+      L *= alpha;
+#pragma unroll
+      for (int e = 0; e < QD; ++e) O[e] *= alpha;
+#pragma unroll
+      for (int j = 0; j < BATCH; ++j) {
+        const float wgt = c0 + j < NSP ? __expf(mc[j] - mb) : 0.f;
+        L = fmaf(lc[j], wgt, L);
+#pragma unroll
+        for (int e = 0; e < QD / 4; ++e) {
+          O[4 * e] = fmaf(v[j][e][0], wgt, O[4 * e]);
+          O[4 * e + 1] = fmaf(v[j][e][1], wgt, O[4 * e + 1]);
+          O[4 * e + 2] = fmaf(v[j][e][2], wgt, O[4 * e + 2]);
+          O[4 * e + 3] = fmaf(v[j][e][3], wgt, O[4 * e + 3]);
+        }
+      }
+      M = mb;
+    }
+    const float inv = 1.f / L;
+#pragma unroll
+    for (int e0 = 0; e0 < QD; e0 += 8) {
+      float v[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = O[e0 + e] * inv;
+      st_act8((uint16_t*)a.out, node, h * DH + QD * g + e0, a.ldo, v);
+    }
+  }
+  if (lane == 0) __hip_atomic_store(cnt, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+template <int DH>
+__global__ __launch_bounds__(64 * ATM_WAVES) void attn_mfma_kernel(AttnArgs a) {
+  extern __shared__ __align__(16) uint16_t att_lds[];
+  constexpr int KS = DH + 8;  // LDS row stride of K (elements)
+  constexpr int UPR = DH / 8;  // 16-byte units per key row
+  constexpr size_t PSTR = DH + 4;
+  const int CL = a.CL, VS = CL + 8;  // LDS row stride of V^T
+  uint16_t* Ks = att_lds;            // [CL][KS]
+  uint16_t* Vt = att_lds + CL * KS;  // [DH][VS]
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, i = lane & 15, g = lane >> 4;
+  const int ntiles = (a.N + 15) >> 4, ngroups = (ntiles + ATM_WAVES - 1) / ATM_WAVES;
+  const int ntree = (a.H * a.N + ATM_WAVES - 1) / ATM_WAVES;  // root-path blocks come first
+  const int NSP = a.nsplit + 1;
+  if ((int)blockIdx.x >= ntree) {
+    const int b = blockIdx.x - ntree;
+    const int gi = b % ngroups, c = (b / ngroups) % a.nsplit, h = b / (ngroups * a.nsplit);
+    const int k0 = c * CL, nk = min(CL, a.P - k0);
+    const int tile = gi * ATM_WAVES + w;
+    // this wave's queries (node 16 tile + i, dims 32 kc + 8 g .. +8), fetched with the staging loads
+    const int qn = min(16 * tile + i, a.N - 1);
+    f32x4 qf[DH / 32][2];
+#pragma unroll
+    for (int kc2 = 0; kc2 < DH / 32; ++kc2) {
+      const float* qp = a.q + (size_t)qn * a.d + h * DH + 32 * kc2 + 8 * g;
+      qf[kc2][0] = *(const f32x4*)qp;
+      qf[kc2][1] = *(const f32x4*)(qp + 4);
+    }
+    const uint16_t* kc = (const uint16_t*)a.kc + ((size_t)h * a.max_ctx + k0) * DH;
+    const uint16_t* vc = (const uint16_t*)a.vc + ((size_t)h * a.max_ctx + k0) * DH;
+    // stage: K unit u = (row u / UPR, columns 8 (u % UPR)); V unit u = (row u % CL,
+    // columns 8 (u / CL)) so that the transposed LDS writes of a wave are contiguous
+    const int units = CL * UPR;
+    for (int u0 = 0; u0 < units; u0 += 4 * 64 * ATM_WAVES) {
+      u32x4 kr[4], vr[4];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const int u = u0 + tid + t * 64 * ATM_WAVES;
+        const int kk = u / UPR, kd = (u % UPR) * 8;
+        const int vk = u % CL, vd = (u / CL) * 8;
+        const bool kin = u < units && kk < nk, vin = u < units && vk < nk;
+        kr[t] = kin ? *(const u32x4*)(kc + (size_t)kk * DH + kd) : (u32x4){0, 0, 0, 0};
+        vr[t] = vin ? *(const u32x4*)(vc + (size_t)vk * DH + vd) : (u32x4){0, 0, 0, 0};
+      }
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const int u = u0 + tid + t * 64 * ATM_WAVES;
+        if (u < units) {
+          const int kk = u / UPR, kd = (u % UPR) * 8;
+          *(u32x4*)(Ks + kk * KS + kd) = kr[t];
+          const int vk = u % CL, vd = (u / CL) * 8;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            Vt[(vd + 2 * e) * VS + vk] = (uint16_t)(vr[t][e] & 0xffffu);
+            Vt[(vd + 2 * e + 1) * VS + vk] = (uint16_t)(vr[t][e] >> 16);
+          }
+        }
+      }
+    }
+    __syncthreads();
+    if (tile >= ntiles) return;
+    u32x4 qh[DH / 32], ql[DH / 32];
+#pragma unroll
+    for (int kc2 = 0; kc2 < DH / 32; ++kc2) {
+      const f32x4 f0 = qf[kc2][0], f1 = qf[kc2][1];
+      const float v[8] = {f0[0], f0[1], f0[2], f0[3], f1[0], f1[1], f1[2], f1[3]};
+      pack_hilo8(v, qh[kc2], ql[kc2]);
+    }
+    float m = -INFINITY, l = 0.f;
+    f32x4 o[DH / 16];
+#pragma unroll
+    for (int t = 0; t < DH / 16; ++t) o[t] = (f32x4){0, 0, 0, 0};
+    for (int kb = 0; kb < nk; kb += 32) {
+      // operand row i of the two key tiles: keys kb + 8 (i/4) + i%4 and that + 4
+      const int r0 = kb + 8 * (i >> 2) + (i & 3), r1 = r0 + 4;
+      f32x4 s0 = (f32x4){0, 0, 0, 0}, s1 = (f32x4){0, 0, 0, 0};
+#pragma unroll
+      for (int kc2 = 0; kc2 < DH / 32; ++kc2) {
+        const u32x4 ka = *(const u32x4*)(Ks + r0 * KS + 32 * kc2 + 8 * g);
+        const u32x4 kb4 = *(const u32x4*)(Ks + r1 * KS + 32 * kc2 + 8 * g);
+        s0 = mfma16(ka, qh[kc2], s0);
+        s0 = mfma16(ka, ql[kc2], s0);
+        s1 = mfma16(kb4, qh[kc2], s1);
+        s1 = mfma16(kb4, ql[kc2], s1);
+      }
+      // lane: node 16 tile + i, keys kb + 8 g + e (e < 4 from s0, e >= 4 from s1)
+      float sv[8];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int key = kb + 8 * g + r;
+        sv[r] = key < nk ? s0[r] * a.scale : -INFINITY;
+        sv[4 + r] = key + 4 < nk ? s1[r] * a.scale : -INFINITY;
+      }
+      float mb = sv[0];
+#pragma unroll
+      for (int e = 1; e < 8; ++e) mb = fmaxf(mb, sv[e]);
+      mb = fmaxf(mb, __shfl_xor(mb, 16));
+      mb = fmaxf(mb, __shfl_xor(mb, 32));
+      const float mn = fmaxf(m, mb);
+      const float alpha = __expf(m - mn);
+      float pv[8], ps = 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        pv[e] = __expf(sv[e] - mn);
+        ps += pv[e];
+      }
+      ps += __shfl_xor(ps, 16);
+      ps += __shfl_xor(ps, 32);
+      l = fmaf(l, alpha, ps);
+      m = mn;
+      u32x4 ph, pl;
+      pack_hilo8(pv, ph, pl);
+#pragma unroll
+      for (int t = 0; t < DH / 16; ++t) {
+        const u32x4 va = *(const u32x4*)(Vt + (16 * t + i) * VS + kb + 8 * g);
+        o[t] = o[t] * alpha;
+        o[t] = mfma16(va, ph, o[t]);
+        o[t] = mfma16(va, pl, o[t]);
+      }
+    }
+    // lane holds O^T rows 16 t + 4 g + r for node 16 tile + i
+    const int node = 16 * tile + i;
+    if (node < a.N) attn_store_part<DH>(a, h, c, node, g, m, l, o, DH / 16, 4 * g);
+    attn_finish_tile<DH>(a, h, tile, lane);
+    return;
+  }
+  // root-path items: one (head, node) per wave
+  const int pair = (int)blockIdx.x * ATM_WAVES + w;
+  if (pair >= a.H * a.N) return;
+  const int n = pair / a.H, h = pair - n * a.H;
+  float qv[DH];
+#pragma unroll
+  for (int c4 = 0; c4 < DH; c4 += 4) {
+    const f32x4 t4 = *(const f32x4*)(a.q + (size_t)n * a.d + h * DH + c4);
+    qv[c4] = t4[0];
+    qv[c4 + 1] = t4[1];
+    qv[c4 + 2] = t4[2];
+    qv[c4 + 3] = t4[3];
+  }
+  const int dn = a.depth[n];
+  const int* al = a.ancl + a.anc_off[n];
+  const uint16_t* kt = (const uint16_t*)a.kt + (size_t)h * a.max_nodes * DH;
+  const uint16_t* vt = (const uint16_t*)a.vt + (size_t)h * a.max_nodes * DH;
+  constexpr int B = 16;
+  const int lc = min(lane, DH - 1);
+  float m = -INFINITY, l = 0.f, o = 0.f;
+  for (int t0 = 0; t0 <= dn; t0 += B) {
+    const int cnt = min(B, dn + 1 - t0);
+    const int key = al[t0 + min(lane, cnt - 1)];
+    float vv[B];
+#pragma unroll
+    for (int j = 0; j < B; ++j) vv[j] = bf2f(vt[(size_t)__shfl(key, j) * DH + lc]);
+    float dot = 0.f;
+    const uint16_t* kr = kt + (size_t)key * DH;
+#pragma unroll
+    for (int c8 = 0; c8 < DH; c8 += 8) {
+      const u32x4 ku = *(const u32x4*)(kr + c8);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        dot = fmaf(qv[c8 + 2 * e], __uint_as_float(ku[e] << 16), dot);
+        dot = fmaf(qv[c8 + 2 * e + 1], __uint_as_float(ku[e] & 0xffff0000u), dot);
+      }
+    }
+    const bool valid = lane < cnt;
+    const float sc = valid ? dot * a.scale : -INFINITY;
+    const float mn = fmaxf(m, wave_max(sc));
+    const float alpha = __expf(m - mn);
+    const float p = valid ? __expf(sc - mn) : 0.f;
+    l = l * alpha + wave_sum(p);
+    float acc = 0.f;
+#pragma unroll
+    for (int j = 0; j < B; ++j) acc = fmaf(__shfl(p, j), vv[j], acc);
+    o = o * alpha + acc;
+    m = mn;
+  }
+  {
+    const __amdgpu_buffer_rsrc_t r = buf_rsrc(a.part);
+    const unsigned off = (unsigned)((((size_t)h * NSP + a.nsplit) * a.N + n) * PSTR * 4);
+    if (lane == 0) {
+      __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(m), r, off, 0, kSc1);
+      __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(l), r, off + 4, 0, kSc1);
+    }
+    if (lane < DH) __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(o), r, off + (4 + lane) * 4, 0, kSc1);
+  }
+  attn_finish_tile<DH>(a, h, n >> 4, lane);
+}
+
+size_t attn_mfma_lds(int DH, int CL) { return ((size_t)CL * (DH + 8) + (size_t)DH * (CL + 8)) * 2; }
+
 hipError_t launch_attn(int f32, int DH, const AttnArgs& a, hipStream_t s) {
+  if (!f32) {
+    if (a.CL % 32 || a.CL > kAttnMaxChunk || a.N <= 0) return hipErrorInvalidValue;
+    // parts are addressed with 32-bit buffer offsets
+    if ((size_t)a.H * (a.nsplit + 1) * a.N * (DH + 4) * 4 > 0x7fffffffu) return hipErrorInvalidValue;
+    const int ntiles = (a.N + 15) / 16, ngroups = (ntiles + ATM_WAVES - 1) / ATM_WAVES;
+    const int blocks = a.H * a.nsplit * ngroups + (a.H * a.N + ATM_WAVES - 1) / ATM_WAVES;
+    const size_t lds = attn_mfma_lds(DH, a.CL);
+    if (DH == 64) attn_mfma_kernel<64><<<blocks, 64 * ATM_WAVES, lds, s>>>(a);
+    else if (DH == 32) attn_mfma_kernel<32><<<blocks, 64 * ATM_WAVES, lds, s>>>(a);
+    else return hipErrorInvalidValue;
+    return hipGetLastError();
+  }
   if (a.S > 0) {
     dim3 grid(a.H, a.S);
     const int nt = 64 * ATT_WAVES;
-    if (f32) {
-      if (DH == 64) attn_prefix_kernel<float, 64><<<grid, nt, 0, s>>>(a);
-      else attn_prefix_kernel<float, 32><<<grid, nt, 0, s>>>(a);
-    } else {
-      if (DH == 64) attn_prefix_kernel<uint16_t, 64><<<grid, nt, 0, s>>>(a);
-      else attn_prefix_kernel<uint16_t, 32><<<grid, nt, 0, s>>>(a);
-    }
+    if (DH == 64) attn_prefix_kernel<float, 64><<<grid, nt, 0, s>>>(a);
+    else attn_prefix_kernel<float, 32><<<grid, nt, 0, s>>>(a);
   }
   const int blocks = (a.N * a.H + 3) / 4;
-  if (f32) {
-    if (DH == 64) attn_combine_kernel<float, 64><<<blocks, 256, 0, s>>>(a);
-    else attn_combine_kernel<float, 32><<<blocks, 256, 0, s>>>(a);
-  } else {
-    if (DH == 64) attn_combine_kernel<uint16_t, 64><<<blocks, 256, 0, s>>>(a);
-    else attn_combine_kernel<uint16_t, 32><<<blocks, 256, 0, s>>>(a);
-  }
+  if (DH == 64) attn_combine_kernel<float, 64><<<blocks, 256, 0, s>>>(a);
+  else attn_combine_kernel<float, 32><<<blocks, 256, 0, s>>>(a);
   return hipGetLastError();
 }
 

@@ -68,7 +68,9 @@ struct ssd_kv {
   void* act_o = nullptr;  // attention outputs [npad][d]
   void* act_f = nullptr;  // GELU outputs [npad][d_mlp]
   float* part = nullptr;  // split-K partial sums [kMaxSplits][max_nodes][d]
-  float* apart = nullptr; // attention prefix partials [H][ceil(max_ctx/64)][max_nodes][head_dim + 2]
+  float* apart = nullptr;  // attention partials (see AttnArgs::part)
+  unsigned* acnt = nullptr;  // attention tile counters [H][acnt_ld]
+  int acnt_ld = 0;
   int* d_tree = nullptr;  // the staged tree (see stage_bytes)
   int* d_accept_tree = nullptr;  // tokens[N] parents[N] depth[N] for accept
   int* d_argmax = nullptr;
@@ -290,7 +292,13 @@ extern "C" ssd_status ssd_kv_create(const ssd_model* m, int32_t max_ctx, int32_t
   const size_t o_a = take(planes * kv->npad * d * es), o_o = take(planes * kv->npad * d * es);
   const size_t o_f = take(planes * kv->npad * M * es);
   const size_t o_part = take((size_t)kMaxSplits * max_nodes * d * 4);  // split-K partials
-  const size_t o_apart = take((size_t)c.n_head * ((max_ctx + 63) / 64) * max_nodes * (m->dh + 2) * 4);
+  // attention partials: fp32 models (H, 64-row tiles, node, DH + 2); bf16
+  // models (H, prefix chunks + root path, node, DH + 4) and tile counters
+  const size_t ap_f32 = (size_t)c.n_head * ((max_ctx + 63) / 64) * max_nodes * (m->dh + 2);
+  const size_t ap_bf16 = (size_t)c.n_head * (attn_max_nsplit(max_ctx) + 1) * max_nodes * (m->dh + 4);
+  const size_t o_apart = take((m->f32 ? ap_f32 : ap_bf16) * 4);
+  const int cnt_ld = (max_nodes + 15) / 16;
+  const size_t o_acnt = take((size_t)c.n_head * cnt_ld * 4);
   const size_t o_tree = take(stage_bytes(max_nodes));
   const size_t o_at = take((size_t)3 * max_nodes * 4), o_am = take((size_t)max_nodes * 4);
   const size_t o_r = take((size_t)V * 8), o_p = take((size_t)V * 8), o_qq = take((size_t)V * 8);
@@ -310,6 +318,8 @@ extern "C" ssd_status ssd_kv_create(const ssd_model* m, int32_t max_ctx, int32_t
   kv->act_f = b + o_f;
   kv->part = (float*)(b + o_part);
   kv->apart = (float*)(b + o_apart);
+  kv->acnt = (unsigned*)(b + o_acnt);
+  kv->acnt_ld = cnt_ld;
   kv->d_tree = (int*)(b + o_tree);
   kv->d_accept_tree = (int*)(b + o_at);
   kv->d_argmax = (int*)(b + o_am);
@@ -494,6 +504,10 @@ static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int3
     a.max_ctx = kv->max_ctx;
     a.max_nodes = maxn;
     a.scale = 1.0f / std::sqrt((float)DH);
+    a.cnt = kv->acnt;
+    a.cnt_ld = kv->acnt_ld;
+    a.CL = attn_chunk(P);
+    a.nsplit = attn_nsplit(P);
     HIP_TRY(launch_attn(f32, DH, a, s));
 
     Epi eo{};

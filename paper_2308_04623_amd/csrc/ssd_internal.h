@@ -60,11 +60,37 @@ struct AttnArgs {
   const int* ancl;      // root paths, root first, node itself last
   void* out;            // attention output in the GEMM-input layout
   int ldo;              // GEMM-input leading dimension (fp32: d, bf16: d / 32)
-  float* part;          // prefix partials [H][S][N][DH + 2]: max, sum of exp, output
-  int S;                // prefix tiles of 64 cache rows
+  float* part;          // fp32 models: prefix partials [H][S][N][DH + 2] (max, sum of exp, output);
+                        // bf16 models: partials [H][nsplit + 1][N][DH + 4] (max, sum, -, -, output),
+                        // slot nsplit holding the root-path part
+  int S;                // fp32 models: prefix tiles of 64 cache rows
   int N, P, d, H, max_ctx, max_nodes;
   float scale;
+  // bf16 models
+  unsigned* cnt;        // arrival counters [H][cnt_ld], zero between launches
+  int cnt_ld;           // counters per head (>= node tiles of 16)
+  int CL;               // cache rows per prefix chunk (multiple of 32, <= kAttnMaxChunk)
+  int nsplit;           // prefix chunks (ceil(P / CL))
 };
+
+// bf16 attention: cache rows per prefix chunk (about P / 8, so that the parts
+// of a node fit one round trip of the merge), a function of the prefix length
+// only, so that a node's result does not depend on the tree
+constexpr int kAttnMaxChunk = 128;
+inline int attn_chunk(int P) {
+  int c = (P + 7) / 8;
+  c = (c + 31) / 32 * 32;
+  if (c < 32) c = 32;
+  if (c > kAttnMaxChunk) c = kAttnMaxChunk;
+  return c;
+}
+inline int attn_nsplit(int P) { return P > 0 ? (P + attn_chunk(P) - 1) / attn_chunk(P) : 0; }
+// most prefix chunks for any P <= max_ctx
+inline int attn_max_nsplit(int max_ctx) {
+  int mx = 0;
+  for (int P = 1; P <= max_ctx; P += (P < 8192 ? 1 : 256)) mx = attn_nsplit(P) > mx ? attn_nsplit(P) : mx;
+  return attn_nsplit(max_ctx) > mx ? attn_nsplit(max_ctx) : mx;
+}
 
 // ---- launchers (kernels.hip); all enqueue on `s` and return the launch status
 hipError_t launch_embed(int f32, const void* wte, const void* wpe, const int* tokens, const int* pos, int N, int d,
