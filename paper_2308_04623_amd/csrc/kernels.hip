@@ -28,12 +28,13 @@ typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float bf2f(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
 
-// float -> bfloat16, round to nearest even
-__device__ __forceinline__ uint16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)0x7fc0;
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
+// float -> bfloat16, round to nearest even (v_cvt_pk_bf16_f32)
+__device__ __forceinline__ uint16_t f2bf(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+// two floats -> packed bfloat16 pair (first in the low half), one instruction
+__device__ __forceinline__ uint32_t f2bf2(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){a, b}, bf16x2_t));
 }
 
 template <typename T> __device__ __forceinline__ float ldT(const T* p, size_t i);
@@ -696,41 +697,32 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnArgs a) {
 
 // ---- bf16 models: one kernel on the matrix cores
 //
-// Work items (one wavefront each):
-//  prefix (head h, chunk c, node tile j): cache rows c*CL .. c*CL+CL-1 against
-//    16 nodes.  The workgroup (4 node tiles) stages the chunk's K rows and the
-//    transposed V rows in LDS once.  S^T = K Q^T and O^T = V^T P^T run on
-//    v_mfma_f32_16x16x32_bf16 (q and p split into bf16 hi + lo, K and V exact),
-//    32 keys at a time with an online softmax.  Rows of the K operand are
-//    ordered so that lane l ends up holding the scores of keys 8(l/16)..+7 of
-//    node l%16, which is exactly its slot of the P^T operand: no shuffles.
-//  root path (head h, node n): the node's ancestors and itself from the tree
-//    scratch, vector ALU.
-// Each item writes (max, sum of exp, unnormalised output) for its nodes and
-// bumps the counter of (h, j); the last arrival merges the nsplit + 1 parts of
-// its 16 nodes in slot order and writes the attention output.  Chunks depend
-// on P only, so a node's result does not depend on the rest of the tree.
+// Workgroup (head h, node tile j of 16 nodes), 8 waves:
+//  prefix: wave w takes cache rows 64 c .. 64 c + 63 for chunks c = w, w + 8,
+//    ...  S^T = K Q^T and O^T = V^T P^T run on v_mfma_f32_16x16x32_bf16 (q and
+//    p split into bf16 hi + lo, K and V exact) 32 keys at a time with an online
+//    softmax.  K operand rows come straight from the cache, ordered so that
+//    lane l ends up holding the scores of keys 8(l/16)..+7 of node l%16, which
+//    is exactly its slot of the P^T operand; V rows are transposed through
+//    the wave's own LDS.
+//  root path: half-wave (w, 0/1) takes node 16 j + 2 w + (0/1): its ancestors
+//    and itself from the tree scratch on the vector ALU, root first.  Its index
+//    and row loads are issued before the prefix work so they overlap it.
+//  merge: the 8 prefix parts and the root-path part of every node are merged
+//    through LDS in that fixed order and written in the next GEMM's input
+//    layout.  The split of the prefix depends on P only, so a node's result
+//    does not depend on the rest of the tree.
 
-constexpr int ATM_WAVES = 4;
+constexpr int AT_WAVES = 8;
+constexpr int AT_KEYS = 64;
 
 __device__ __forceinline__ void pack_hilo8(const float (&v)[8], u32x4& hi, u32x4& lo) {
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
-    const uint16_t h0 = f2bf(v[2 * e]), h1 = f2bf(v[2 * e + 1]);
-    const uint16_t l0 = f2bf(v[2 * e] - bf2f(h0)), l1 = f2bf(v[2 * e + 1] - bf2f(h1));
-    hi[e] = (uint32_t)h0 | ((uint32_t)h1 << 16);
-    lo[e] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+    const uint32_t hp = f2bf2(v[2 * e], v[2 * e + 1]);
+    hi[e] = hp;
+    lo[e] = f2bf2(v[2 * e] - __uint_as_float(hp << 16), v[2 * e + 1] - __uint_as_float(hp & 0xffff0000u));
   }
-}
-
-// eight consecutive k (k0 % 8 == 0) of node n in the bf16 GEMM-input layout (see st_act)
-__device__ __forceinline__ void st_act8(uint16_t* p, int n, int k0, int ld, const float (&v)[8]) {
-  const size_t f = (size_t)(n >> 4) * ld + (k0 >> 5);
-  const size_t off = f * 1024 + ((n & 15) + 16 * ((k0 & 31) >> 3)) * 8;
-  u32x4 hi, lo;
-  pack_hilo8(v, hi, lo);
-  *(u32x4*)(p + off) = hi;
-  *(u32x4*)(p + off + 512) = lo;
 }
 
 __device__ __forceinline__ f32x4 mfma16(const u32x4& a, const u32x4& b, const f32x4& c) {
@@ -738,188 +730,123 @@ __device__ __forceinline__ f32x4 mfma16(const u32x4& a, const u32x4& b, const f3
                                                   0, 0);
 }
 
-// Parts are exchanged between workgroups without cache-wide fences: they are
-// written and read with device-scope (sc1) buffer accesses, which go to the
-// device's point of coherence instead of a per-XCD L2, and a part's stores
-// have completed (s_waitcnt) before its counter is bumped.
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* p) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, 0x7fffffff, 0x00020000);
-}
-constexpr int kSc1 = 16;  // cache-policy bits of a device-scope access
-
-// part of (h, slot c, node): m, l at [0], [1]; output at [4 .. 4 + DH)
 template <int DH>
-__device__ __forceinline__ void attn_store_part(const AttnArgs& a, int h, int c, int node, int g, float m, float l,
-                                                const f32x4* o4, int no4, int d0) {
-  constexpr size_t PSTR = DH + 4;
-  const __amdgpu_buffer_rsrc_t r = buf_rsrc(a.part);
-  const unsigned off = (unsigned)((((size_t)h * (a.nsplit + 1) + c) * a.N + node) * PSTR * 4);
-  if (g == 0) {
-    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(m), r, off, 0, kSc1);
-    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(l), r, off + 4, 0, kSc1);
-  }
-  for (int t = 0; t < no4; ++t)
-    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, o4[t]), r, off + (4 + d0 + 16 * t) * 4, 0, kSc1);
-}
-
-// after a wave has written its part for (h, tile): count it, and if it is the
-// last part, merge all parts of the tile's nodes in slot order
-template <int DH>
-__device__ void attn_finish_tile(const AttnArgs& a, int h, int tile, int lane) {
-  __builtin_amdgcn_s_waitcnt(0);
-  unsigned old = 0;
-  unsigned* cnt = a.cnt + (size_t)h * a.cnt_ld + tile;
-  if (lane == 0) old = __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  old = __shfl(old, 0);
-  const int nv = min(16, a.N - 16 * tile);
-  if (old != (unsigned)(a.nsplit + nv - 1)) return;
-  constexpr int QD = DH / 4;
-  constexpr size_t PSTR = DH + 4;
-  constexpr int BATCH = 9;  // parts fetched per round trip (6 loads each)
-  const int NSP = a.nsplit + 1;
-  const int i = lane & 15, g = lane >> 4;
-  const int node = 16 * tile + i;
-  if (node < a.N) {
-    const __amdgpu_buffer_rsrc_t r = buf_rsrc(a.part);
-    const unsigned cstr = (unsigned)((size_t)a.N * PSTR * 4);
-    const unsigned base = (unsigned)(((size_t)h * NSP * a.N + node) * PSTR * 4);
-    float M = -INFINITY, L = 0.f, O[QD];
-#pragma unroll
-    for (int e = 0; e < QD; ++e) O[e] = 0.f;
-    for (int c0 = 0; c0 < NSP; c0 += BATCH) {
-      float mc[BATCH], lc[BATCH];
-      f32x4 v[BATCH][QD / 4];
-#pragma unroll
-      for (int j = 0; j < BATCH; ++j) {
-        const unsigned pc = base + min(c0 + j, NSP - 1) * cstr;
-        mc[j] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, pc, 0, kSc1));
-        lc[j] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, pc + 4, 0, kSc1));
-#pragma unroll
-        for (int e = 0; e < QD / 4; ++e)
-          v[j][e] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, pc + (4 + QD * g + 4 * e) * 4, 0, kSc1));
-      }
-      float mb = M;
-#pragma unroll
-      for (int j = 0; j < BATCH; ++j) mb = c0 + j < NSP ? fmaxf(mb, mc[j]) : mb;
-      const float alpha = __expf(M - mb);
-      L *= alpha;
-#pragma unroll
-      for (int e = 0; e < QD; ++e) O[e] *= alpha;
-#pragma unroll
-      for (int j = 0; j < BATCH; ++j) {
-        const float wgt = c0 + j < NSP ? __expf(mc[j] - mb) : 0.f;
-        L = fmaf(lc[j], wgt, L);
-#pragma unroll
-        for (int e = 0; e < QD / 4; ++e) {
-          O[4 * e] = fmaf(v[j][e][0], wgt, O[4 * e]);
-          O[4 * e + 1] = fmaf(v[j][e][1], wgt, O[4 * e + 1]);
-          O[4 * e + 2] = fmaf(v[j][e][2], wgt, O[4 * e + 2]);
-          O[4 * e + 3] = fmaf(v[j][e][3], wgt, O[4 * e + 3]);
-        }
-      }
-      M = mb;
-    }
-    const float inv = 1.f / L;
-#pragma unroll
-    for (int e0 = 0; e0 < QD; e0 += 8) {
-      float v[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) v[e] = O[e0 + e] * inv;
-      st_act8((uint16_t*)a.out, node, h * DH + QD * g + e0, a.ldo, v);
-    }
-  }
-  if (lane == 0) __hip_atomic_store(cnt, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-template <int DH>
-__global__ __launch_bounds__(64 * ATM_WAVES) void attn_mfma_kernel(AttnArgs a) {
-  extern __shared__ __align__(16) uint16_t att_lds[];
-  constexpr int KS = DH + 8;  // LDS row stride of K (elements)
-  constexpr int UPR = DH / 8;  // 16-byte units per key row
-  constexpr size_t PSTR = DH + 4;
-  const int CL = a.CL, VS = CL + 8;  // LDS row stride of V^T
-  uint16_t* Ks = att_lds;            // [CL][KS]
-  uint16_t* Vt = att_lds + CL * KS;  // [DH][VS]
+__global__ __launch_bounds__(64 * AT_WAVES) void attn_tile_kernel(AttnArgs a) {
+  constexpr int VS = AT_KEYS + 8;  // LDS row stride of V^T (elements)
+  constexpr int VT = DH * VS;      // V^T elements per wave
+  constexpr int PSTR = DH + 2;     // merge record: m, l, o[DH]
+  constexpr int NSLOT = AT_WAVES + 1;
+  constexpr int DPL = DH / 32;     // root-path output dims per lane of a half-wave
+  __shared__ __align__(16) uint16_t vt_lds[AT_WAVES * VT];
+  __shared__ float qrow[AT_WAVES][2][DH];
+  float* mrg = (float*)vt_lds;  // after the prefix work: [NSLOT][16][PSTR]
+  static_assert(NSLOT * 16 * PSTR * 4 <= AT_WAVES * VT * 2, "merge area");
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, i = lane & 15, g = lane >> 4;
-  const int ntiles = (a.N + 15) >> 4, ngroups = (ntiles + ATM_WAVES - 1) / ATM_WAVES;
-  const int ntree = (a.H * a.N + ATM_WAVES - 1) / ATM_WAVES;  // root-path blocks come first
-  const int NSP = a.nsplit + 1;
-  if ((int)blockIdx.x >= ntree) {
-    const int b = blockIdx.x - ntree;
-    const int gi = b % ngroups, c = (b / ngroups) % a.nsplit, h = b / (ngroups * a.nsplit);
-    const int k0 = c * CL, nk = min(CL, a.P - k0);
-    const int tile = gi * ATM_WAVES + w;
-    // this wave's queries (node 16 tile + i, dims 32 kc + 8 g .. +8), fetched with the staging loads
-    const int qn = min(16 * tile + i, a.N - 1);
-    f32x4 qf[DH / 32][2];
+  const int h = blockIdx.x % a.H, tile = blockIdx.x / a.H, n0 = 16 * tile;
+
+  // root-path node of this half-wave: its first 32 path entries (fixed
+  // stride, no dependent index load), depth and query
+  const int hw = lane >> 5, hl = lane & 31;
+  const int rnc = min(n0 + 2 * w + hw, a.N - 1);
+  int rkey = a.path32[(size_t)rnc * kPath32 + hl];
+  const int rdep = a.depth[rnc];
+  float rq[DPL];
+  {
+    const float* qp = a.q + (size_t)rnc * a.d + h * DH + hl * DPL;
 #pragma unroll
-    for (int kc2 = 0; kc2 < DH / 32; ++kc2) {
-      const float* qp = a.q + (size_t)qn * a.d + h * DH + 32 * kc2 + 8 * g;
-      qf[kc2][0] = *(const f32x4*)qp;
-      qf[kc2][1] = *(const f32x4*)(qp + 4);
-    }
-    const uint16_t* kc = (const uint16_t*)a.kc + ((size_t)h * a.max_ctx + k0) * DH;
-    const uint16_t* vc = (const uint16_t*)a.vc + ((size_t)h * a.max_ctx + k0) * DH;
-    // stage: K unit u = (row u / UPR, columns 8 (u % UPR)); V unit u = (row u % CL,
-    // columns 8 (u / CL)) so that the transposed LDS writes of a wave are contiguous
-    const int units = CL * UPR;
-    for (int u0 = 0; u0 < units; u0 += 4 * 64 * ATM_WAVES) {
-      u32x4 kr[4], vr[4];
+    for (int e = 0; e < DPL; ++e) rq[e] = qp[e];
+  }
+  // tile queries (B operand): node n0 + i, dims 32 kc + 8 g .. +8
+  const int qn = min(n0 + i, a.N - 1);
+  f32x4 qf[DH / 32][2];
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const int u = u0 + tid + t * 64 * ATM_WAVES;
-        const int kk = u / UPR, kd = (u % UPR) * 8;
-        const int vk = u % CL, vd = (u / CL) * 8;
-        const bool kin = u < units && kk < nk, vin = u < units && vk < nk;
-        kr[t] = kin ? *(const u32x4*)(kc + (size_t)kk * DH + kd) : (u32x4){0, 0, 0, 0};
-        vr[t] = vin ? *(const u32x4*)(vc + (size_t)vk * DH + vd) : (u32x4){0, 0, 0, 0};
+  for (int kc2 = 0; kc2 < DH / 32; ++kc2) {
+    const float* qp = a.q + (size_t)qn * a.d + h * DH + 32 * kc2 + 8 * g;
+    qf[kc2][0] = *(const f32x4*)qp;
+    qf[kc2][1] = *(const f32x4*)(qp + 4);
+  }
+  const uint16_t* kc = (const uint16_t*)a.kc + (size_t)h * a.max_ctx * DH;
+  const uint16_t* vc = (const uint16_t*)a.vc + (size_t)h * a.max_ctx * DH;
+  uint16_t* vt = vt_lds + w * VT;
+  const int npass = (a.P + AT_WAVES * AT_KEYS - 1) / (AT_WAVES * AT_KEYS);
+
+  // first pass's rows, then the root-path rows (one round trip behind)
+  u32x4 kf[2][2][DH / 32], vr[DH / 8];
+  auto load_chunk = [&](int k0) {
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const int key = min(k0 + 32 * sb + 8 * (i >> 2) + (i & 3) + 4 * t, a.P - 1);
+#pragma unroll
+        for (int kc2 = 0; kc2 < DH / 32; ++kc2) kf[sb][t][kc2] = *(const u32x4*)(kc + (size_t)key * DH + 32 * kc2 + 8 * g);
       }
+    // V: the chunk's rows are contiguous; load j covers 1 KB (lane l: 16 bytes
+    // at (64 j + l) * 8 elements, i.e. row 8 j + l / (DH / 8) of the chunk)
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const int u = u0 + tid + t * 64 * ATM_WAVES;
-        if (u < units) {
-          const int kk = u / UPR, kd = (u % UPR) * 8;
-          *(u32x4*)(Ks + kk * KS + kd) = kr[t];
-          const int vk = u % CL, vd = (u / CL) * 8;
+    for (int j = 0; j < DH / 8; ++j) {
+      const int e0 = (64 * j + lane) * 8;
+      const int vk = min(k0 + e0 / DH, a.P - 1);
+      vr[j] = *(const u32x4*)(vc + (size_t)vk * DH + e0 % DH);
+    }
+  };
+  if (a.P > 0 && w * AT_KEYS < a.P) load_chunk(w * AT_KEYS);
+  const uint16_t* ktb = (const uint16_t*)a.kt + (size_t)h * a.max_nodes * DH;
+  const uint16_t* vtb = (const uint16_t*)a.vt + (size_t)h * a.max_nodes * DH;
+  u32x4 rk[DH / 8], rv[DH / 8];
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            Vt[(vd + 2 * e) * VS + vk] = (uint16_t)(vr[t][e] & 0xffffu);
-            Vt[(vd + 2 * e + 1) * VS + vk] = (uint16_t)(vr[t][e] >> 16);
-          }
-        }
+  for (int j = 0; j < DH / 8; ++j) {
+    rk[j] = *(const u32x4*)(ktb + (size_t)rkey * DH + 8 * j);
+    rv[j] = *(const u32x4*)(vtb + (size_t)rkey * DH + 8 * j);
+  }
+#pragma unroll
+  for (int e = 0; e < DPL; ++e) qrow[w][hw][hl * DPL + e] = rq[e];
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  u32x4 qh[DH / 32], ql[DH / 32];
+#pragma unroll
+  for (int kc2 = 0; kc2 < DH / 32; ++kc2) {
+    const f32x4 f0 = qf[kc2][0], f1 = qf[kc2][1];
+    const float v[8] = {f0[0], f0[1], f0[2], f0[3], f1[0], f1[1], f1[2], f1[3]};
+    pack_hilo8(v, qh[kc2], ql[kc2]);
+  }
+  float m = -INFINITY, l = 0.f;
+  f32x4 o[DH / 16];
+#pragma unroll
+  for (int t = 0; t < DH / 16; ++t) o[t] = (f32x4){0, 0, 0, 0};
+  // one chunk of nk (> 0) cache rows whose K fragments and V rows are in kf, vr
+  auto do_chunk = [&](int nk) {
+    // V rows -> this wave's V^T (rows past the prefix as zeros)
+#pragma unroll
+    for (int j = 0; j < DH / 8; ++j) {
+      const int e0 = (64 * j + lane) * 8, key = e0 / DH, d0 = e0 % DH;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const uint32_t u = key < nk ? vr[j][e] : 0u;
+        vt[(d0 + 2 * e) * VS + key] = (uint16_t)(u & 0xffffu);
+        vt[(d0 + 2 * e + 1) * VS + key] = (uint16_t)(u >> 16);
       }
     }
-    __syncthreads();
-    if (tile >= ntiles) return;
-    u32x4 qh[DH / 32], ql[DH / 32];
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 #pragma unroll
-    for (int kc2 = 0; kc2 < DH / 32; ++kc2) {
-      const f32x4 f0 = qf[kc2][0], f1 = qf[kc2][1];
-      const float v[8] = {f0[0], f0[1], f0[2], f0[3], f1[0], f1[1], f1[2], f1[3]};
-      pack_hilo8(v, qh[kc2], ql[kc2]);
-    }
-    float m = -INFINITY, l = 0.f;
-    f32x4 o[DH / 16];
-#pragma unroll
-    for (int t = 0; t < DH / 16; ++t) o[t] = (f32x4){0, 0, 0, 0};
-    for (int kb = 0; kb < nk; kb += 32) {
-      // operand row i of the two key tiles: keys kb + 8 (i/4) + i%4 and that + 4
-      const int r0 = kb + 8 * (i >> 2) + (i & 3), r1 = r0 + 4;
+    for (int sb = 0; sb < 2; ++sb) {
+      if (32 * sb >= nk) break;
       f32x4 s0 = (f32x4){0, 0, 0, 0}, s1 = (f32x4){0, 0, 0, 0};
 #pragma unroll
       for (int kc2 = 0; kc2 < DH / 32; ++kc2) {
-        const u32x4 ka = *(const u32x4*)(Ks + r0 * KS + 32 * kc2 + 8 * g);
-        const u32x4 kb4 = *(const u32x4*)(Ks + r1 * KS + 32 * kc2 + 8 * g);
-        s0 = mfma16(ka, qh[kc2], s0);
-        s0 = mfma16(ka, ql[kc2], s0);
-        s1 = mfma16(kb4, qh[kc2], s1);
-        s1 = mfma16(kb4, ql[kc2], s1);
+        s0 = mfma16(kf[sb][0][kc2], qh[kc2], s0);
+        s0 = mfma16(kf[sb][0][kc2], ql[kc2], s0);
+        s1 = mfma16(kf[sb][1][kc2], qh[kc2], s1);
+        s1 = mfma16(kf[sb][1][kc2], ql[kc2], s1);
       }
-      // lane: node 16 tile + i, keys kb + 8 g + e (e < 4 from s0, e >= 4 from s1)
+      // lane: node n0 + i, keys 32 sb + 8 g + e of the chunk (e < 4 from s0, e >= 4 from s1)
       float sv[8];
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int key = kb + 8 * g + r;
+        const int key = 32 * sb + 8 * g + r;
         sv[r] = key < nk ? s0[r] * a.scale : -INFINITY;
         sv[4 + r] = key + 4 < nk ? s1[r] * a.scale : -INFINITY;
       }
@@ -944,91 +871,145 @@ __global__ __launch_bounds__(64 * ATM_WAVES) void attn_mfma_kernel(AttnArgs a) {
       pack_hilo8(pv, ph, pl);
 #pragma unroll
       for (int t = 0; t < DH / 16; ++t) {
-        const u32x4 va = *(const u32x4*)(Vt + (16 * t + i) * VS + kb + 8 * g);
+        const u32x4 va = *(const u32x4*)(vt + (16 * t + i) * VS + 32 * sb + 8 * g);
         o[t] = o[t] * alpha;
         o[t] = mfma16(va, ph, o[t]);
         o[t] = mfma16(va, pl, o[t]);
       }
     }
-    // lane holds O^T rows 16 t + 4 g + r for node 16 tile + i
-    const int node = 16 * tile + i;
-    if (node < a.N) attn_store_part<DH>(a, h, c, node, g, m, l, o, DH / 16, 4 * g);
-    attn_finish_tile<DH>(a, h, tile, lane);
-    return;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  };
+  // pass 0 in straight-line code (its loads were issued first), later passes
+  // (P > 512) in a loop
+  {
+    const int nk0 = min(AT_KEYS, a.P - w * AT_KEYS);
+    if (nk0 > 0) do_chunk(nk0);
   }
-  // root-path items: one (head, node) per wave
-  const int pair = (int)blockIdx.x * ATM_WAVES + w;
-  if (pair >= a.H * a.N) return;
-  const int n = pair / a.H, h = pair - n * a.H;
-  float qv[DH];
-#pragma unroll
-  for (int c4 = 0; c4 < DH; c4 += 4) {
-    const f32x4 t4 = *(const f32x4*)(a.q + (size_t)n * a.d + h * DH + c4);
-    qv[c4] = t4[0];
-    qv[c4 + 1] = t4[1];
-    qv[c4 + 2] = t4[2];
-    qv[c4 + 3] = t4[3];
+  for (int pass = 1; pass < npass; ++pass) {
+    const int k0 = (pass * AT_WAVES + w) * AT_KEYS;
+    const int nk = min(AT_KEYS, a.P - k0);
+    if (nk <= 0) break;
+    load_chunk(k0);
+    do_chunk(nk);
   }
-  const int dn = a.depth[n];
-  const int* al = a.ancl + a.anc_off[n];
-  const uint16_t* kt = (const uint16_t*)a.kt + (size_t)h * a.max_nodes * DH;
-  const uint16_t* vt = (const uint16_t*)a.vt + (size_t)h * a.max_nodes * DH;
-  constexpr int B = 16;
-  const int lc = min(lane, DH - 1);
-  float m = -INFINITY, l = 0.f, o = 0.f;
-  for (int t0 = 0; t0 <= dn; t0 += B) {
-    const int cnt = min(B, dn + 1 - t0);
-    const int key = al[t0 + min(lane, cnt - 1)];
-    float vv[B];
+
+  // root path on the vector ALU: 32 keys per batch per half-wave, lane hl =
+  // key; the batch's V rows go through the wave's (now free) LDS
+  uint16_t* rvl = vt + hw * 32 * DH;  // [32 keys][DH] of this half-wave
+  static_assert(2 * 32 * DH <= VT, "root-path rows fit the wave's LDS");
+  float rm = -INFINITY, rl = 0.f, ro[DPL];
 #pragma unroll
-    for (int j = 0; j < B; ++j) vv[j] = bf2f(vt[(size_t)__shfl(key, j) * DH + lc]);
-    float dot = 0.f;
-    const uint16_t* kr = kt + (size_t)key * DH;
+  for (int e = 0; e < DPL; ++e) ro[e] = 0.f;
+  const int rbatches = (max(rdep, __shfl_xor(rdep, 32)) + 32) / 32;  // wave-uniform
+  for (int bt = 0; bt < rbatches; ++bt) {
+    const int j = 32 * bt + hl;
+    if (bt > 0) {
+      rkey = a.ancl[a.anc_off[rnc] + min(j, rdep)];
 #pragma unroll
-    for (int c8 = 0; c8 < DH; c8 += 8) {
-      const u32x4 ku = *(const u32x4*)(kr + c8);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        dot = fmaf(qv[c8 + 2 * e], __uint_as_float(ku[e] << 16), dot);
-        dot = fmaf(qv[c8 + 2 * e + 1], __uint_as_float(ku[e] & 0xffff0000u), dot);
+      for (int jj = 0; jj < DH / 8; ++jj) {
+        rk[jj] = *(const u32x4*)(ktb + (size_t)rkey * DH + 8 * jj);
+        rv[jj] = *(const u32x4*)(vtb + (size_t)rkey * DH + 8 * jj);
       }
     }
-    const bool valid = lane < cnt;
-    const float sc = valid ? dot * a.scale : -INFINITY;
-    const float mn = fmaxf(m, wave_max(sc));
-    const float alpha = __expf(m - mn);
-    const float p = valid ? __expf(sc - mn) : 0.f;
-    l = l * alpha + wave_sum(p);
-    float acc = 0.f;
 #pragma unroll
-    for (int j = 0; j < B; ++j) acc = fmaf(__shfl(p, j), vv[j], acc);
-    o = o * alpha + acc;
-    m = mn;
-  }
-  {
-    const __amdgpu_buffer_rsrc_t r = buf_rsrc(a.part);
-    const unsigned off = (unsigned)((((size_t)h * NSP + a.nsplit) * a.N + n) * PSTR * 4);
-    if (lane == 0) {
-      __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(m), r, off, 0, kSc1);
-      __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(l), r, off + 4, 0, kSc1);
+    for (int jj = 0; jj < DH / 8; ++jj) *(u32x4*)(rvl + hl * DH + 8 * jj) = rv[jj];
+    float dot = 0.f;
+#pragma unroll
+    for (int c8 = 0; c8 < DH / 8; ++c8) {
+      const f32x4 qa = *(const f32x4*)&qrow[w][hw][8 * c8];
+      const f32x4 qb = *(const f32x4*)&qrow[w][hw][8 * c8 + 4];
+      const u32x4 ku = rk[c8];
+      dot = fmaf(qa[0], __uint_as_float(ku[0] << 16), dot);
+      dot = fmaf(qa[1], __uint_as_float(ku[0] & 0xffff0000u), dot);
+      dot = fmaf(qa[2], __uint_as_float(ku[1] << 16), dot);
+      dot = fmaf(qa[3], __uint_as_float(ku[1] & 0xffff0000u), dot);
+      dot = fmaf(qb[0], __uint_as_float(ku[2] << 16), dot);
+      dot = fmaf(qb[1], __uint_as_float(ku[2] & 0xffff0000u), dot);
+      dot = fmaf(qb[2], __uint_as_float(ku[3] << 16), dot);
+      dot = fmaf(qb[3], __uint_as_float(ku[3] & 0xffff0000u), dot);
     }
-    if (lane < DH) __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(o), r, off + (4 + lane) * 4, 0, kSc1);
+    const bool kvalid = j <= rdep;
+    const float sc = kvalid ? dot * a.scale : -INFINITY;
+    float mb = sc;
+#pragma unroll
+    for (int off = 1; off < 32; off <<= 1) mb = fmaxf(mb, __shfl_xor(mb, off));
+    const float mn = fmaxf(rm, mb);
+    const float alpha = __expf(rm - mn);
+    const float p = kvalid ? __expf(sc - mn) : 0.f;
+    float ps = p;
+#pragma unroll
+    for (int off = 1; off < 32; off <<= 1) ps += __shfl_xor(ps, off);
+    rl = fmaf(rl, alpha, ps);
+    rm = mn;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    // lane hl covers dims DPL hl .. +DPL; keys of the batch in order
+    const int cnt = min(32, rdep + 1 - 32 * bt);
+    const int cmax = max(cnt, __shfl_xor(cnt, 32));  // wave-uniform
+    float acc[DPL];
+#pragma unroll
+    for (int e = 0; e < DPL; ++e) acc[e] = 0.f;
+    for (int jj = 0; jj < cmax; ++jj) {
+      const float pj = jj < cnt ? __shfl(p, (hw << 5) + jj) : 0.f;
+      const uint16_t* vr2 = rvl + jj * DH + DPL * hl;
+#pragma unroll
+      for (int e = 0; e < DPL; ++e) acc[e] = fmaf(pj, bf2f(vr2[e]), acc[e]);
+    }
+#pragma unroll
+    for (int e = 0; e < DPL; ++e) ro[e] = fmaf(ro[e], alpha, acc[e]);
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
-  attn_finish_tile<DH>(a, h, n >> 4, lane);
-}
 
-size_t attn_mfma_lds(int DH, int CL) { return ((size_t)CL * (DH + 8) + (size_t)DH * (CL + 8)) * 2; }
+  // merge through LDS: slots 0..7 the prefix waves, slot 8 the root paths
+  __syncthreads();  // every wave is done with its V^T
+  {
+    float* rec = mrg + ((size_t)w * 16 + i) * PSTR;
+    if (g == 0) {
+      rec[0] = m;
+      rec[1] = l;
+    }
+#pragma unroll
+    for (int t = 0; t < DH / 16; ++t)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) rec[2 + 16 * t + 4 * g + r] = o[t][r];
+    float* rr = mrg + ((size_t)AT_WAVES * 16 + 2 * w + hw) * PSTR;
+    if (hl == 0) {
+      rr[0] = rm;
+      rr[1] = rl;
+    }
+#pragma unroll
+    for (int e = 0; e < DPL; ++e) rr[2 + DPL * hl + e] = ro[e];
+  }
+  __syncthreads();
+  for (int idx = tid; idx < 16 * DH; idx += 64 * AT_WAVES) {
+    const int node = idx / DH, dd = idx - node * DH;
+    if (n0 + node >= a.N) continue;
+    float M = -INFINITY;
+#pragma unroll
+    for (int c = 0; c < NSLOT; ++c) M = fmaxf(M, mrg[((size_t)c * 16 + node) * PSTR]);
+    float L = 0.f, O = 0.f;
+#pragma unroll
+    for (int c = 0; c < NSLOT; ++c) {
+      const float* rc = mrg + ((size_t)c * 16 + node) * PSTR;
+      const float wgt = __expf(rc[0] - M);
+      L = fmaf(rc[1], wgt, L);
+      O = fmaf(rc[2 + dd], wgt, O);
+    }
+    st_act((uint16_t*)a.out, n0 + node, h * DH + dd, a.ldo, O / L);
+  }
+}
 
 hipError_t launch_attn(int f32, int DH, const AttnArgs& a, hipStream_t s) {
   if (!f32) {
-    if (a.CL % 32 || a.CL > kAttnMaxChunk || a.N <= 0) return hipErrorInvalidValue;
-    // parts are addressed with 32-bit buffer offsets
-    if ((size_t)a.H * (a.nsplit + 1) * a.N * (DH + 4) * 4 > 0x7fffffffu) return hipErrorInvalidValue;
-    const int ntiles = (a.N + 15) / 16, ngroups = (ntiles + ATM_WAVES - 1) / ATM_WAVES;
-    const int blocks = a.H * a.nsplit * ngroups + (a.H * a.N + ATM_WAVES - 1) / ATM_WAVES;
-    const size_t lds = attn_mfma_lds(DH, a.CL);
-    if (DH == 64) attn_mfma_kernel<64><<<blocks, 64 * ATM_WAVES, lds, s>>>(a);
-    else if (DH == 32) attn_mfma_kernel<32><<<blocks, 64 * ATM_WAVES, lds, s>>>(a);
+    if (a.N <= 0) return hipErrorInvalidValue;
+    const int blocks = a.H * ((a.N + 15) / 16);
+    if (DH == 64) attn_tile_kernel<64><<<blocks, 64 * AT_WAVES, 0, s>>>(a);
+    else if (DH == 32) attn_tile_kernel<32><<<blocks, 64 * AT_WAVES, 0, s>>>(a);
     else return hipErrorInvalidValue;
     return hipGetLastError();
   }

@@ -250,8 +250,12 @@ extern "C" ssd_status ssd_kv_bytes(const ssd_config* cfg, int32_t max_ctx, int32
 
 // staged tree: tokens, positions, depths, parents, root-path offsets
 // (max_nodes each), then the root paths themselves (at most n(n+1)/2 entries)
+// Staged tree: tokens, positions, depths, parents, root-path offsets
+// ([max_nodes] each); then for the n nodes the first kPath32 entries of each
+// root path ([n][kPath32], root first, padded with the node itself); then all
+// root paths back to back (offsets above).
 static size_t stage_bytes(int max_nodes) {
-  return (size_t)5 * max_nodes * 4 + (size_t)max_nodes * (max_nodes + 1) / 2 * 4;
+  return (size_t)5 * max_nodes * 4 + (size_t)max_nodes * kPath32 * 4 + (size_t)max_nodes * (max_nodes + 1) / 2 * 4;
 }
 
 extern "C" ssd_status ssd_kv_create(const ssd_model* m, int32_t max_ctx, int32_t max_nodes, void* k_cache,
@@ -391,7 +395,8 @@ static size_t fill_stage(char* host, int P, const int32_t* tokens, const int32_t
   int32_t* dep = pos + max_nodes;
   int32_t* par = dep + max_nodes;
   int32_t* off = par + max_nodes;
-  int32_t* paths = off + max_nodes;
+  int32_t* p32 = off + max_nodes;
+  int32_t* paths = p32 + (size_t)n * kPath32;
   ssd_tree_prep(parents, n, dep, nullptr);  // validated by the caller
   int32_t total = 0;
   for (int i = 0; i < n; ++i) {
@@ -405,9 +410,10 @@ static size_t fill_stage(char* host, int P, const int32_t* tokens, const int32_t
       paths[total + k] = j;
       j = parents[j];
     }
+    for (int k = 0; k < kPath32; ++k) p32[(size_t)i * kPath32 + k] = paths[total + std::min(k, (int)dep[i])];
     total += dep[i] + 1;
   }
-  return (size_t)5 * max_nodes * 4 + (size_t)total * 4;
+  return (size_t)5 * max_nodes * 4 + (size_t)n * kPath32 * 4 + (size_t)total * 4;
 }
 
 // One weight GEMM of the pass over n nodes: fp32 models use the plain
@@ -454,7 +460,8 @@ static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int3
   const int* d_pos = kv->d_tree + maxn;
   const int* d_dep = kv->d_tree + 2 * maxn;
   const int* d_off = kv->d_tree + 4 * maxn;
-  const int* d_paths = kv->d_tree + 5 * maxn;
+  const int* d_path32 = kv->d_tree + 5 * maxn;
+  const int* d_paths = d_path32 + (size_t)n * kPath32;
   HIP_TRY(launch_embed(f32, m->wte, m->wpe, d_tok, d_pos, n, d, kv->x, s));
 
   // GEMM-input leading dimensions (fp32: row stride; bf16: k-steps)
@@ -493,6 +500,7 @@ static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int3
     a.depth = d_dep;
     a.anc_off = d_off;
     a.ancl = d_paths;
+    a.path32 = d_path32;
     a.out = kv->act_o;
     a.ldo = ld_d;
     a.part = kv->apart;

@@ -16,6 +16,9 @@ enum EpiKind : int {
   EPI_PARTIAL = 4  // part[split][n][o] = y (split-K sum of a residual GEMM, no bias)
 };
 
+// root-path entries staged per node at a fixed stride
+constexpr int kPath32 = 32;
+
 // most k-splits a residual GEMM uses
 constexpr int kMaxSplits = 8;
 
@@ -58,6 +61,7 @@ struct AttnArgs {
   const int* depth;     // [N]
   const int* anc_off;   // [N] offset of node n's root path in ancl
   const int* ancl;      // root paths, root first, node itself last
+  const int* path32;    // [N][kPath32]: first entries of each root path, padded with the node
   void* out;            // attention output in the GEMM-input layout
   int ldo;              // GEMM-input leading dimension (fp32: d, bf16: d / 32)
   float* part;          // fp32 models: prefix partials [H][S][N][DH + 2] (max, sum of exp, output);
