@@ -61,6 +61,79 @@ def cpu_model():
     return platform.processor()
 
 
+COPY_BYTES = 256 << 20
+FC_KERNEL = "gemm_kernel<2, 2, 2,"  # MLP up-projection + GELU at 17..32 nodes (matrix cores)
+
+
+def probe_traffic(sess, cfg, n):
+    """Kernels for the HBM-traffic counters: a plain device-to-device copy of
+    COPY_BYTES (reads and writes exactly that much), then the MLP
+    up-projection GEMM of every layer twice."""
+    import torch
+    src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    for _ in range(2):
+        for l in range(cfg.n_layer):
+            sess.launch_gemm(2, l, n)
+    torch.cuda.synchronize()
+    log("traffic probe done")
+
+
+def _counter_rows(d):
+    import csv
+    import glob
+    files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no counter_collection.csv under {d}")
+    rows = []
+    for f in files:
+        with open(f, newline="") as fh:
+            rows += list(csv.DictReader(fh))
+    return rows
+
+
+def _per_kernel(rows, counter):
+    """{(kernel name, grid size): [value per dispatch]} for one counter
+    (values summed over the rows of a dispatch)."""
+    per = {}
+    for r in rows:
+        if r.get("Counter_Name") != counter:
+            continue
+        key = (r.get("Dispatch_Id"), r.get("Kernel_Name", ""), int(r.get("Grid_Size", 0) or 0))
+        per[key] = per.get(key, 0.0) + float(r["Counter_Value"])
+    out = {}
+    for (_, name, grid), v in per.items():
+        out.setdefault((name, grid), []).append(v)
+    return out
+
+
+def write_traffic(fetch_dir, write_dir, n):
+    out = {"kernel_source": kernel_source_hash(), "nodes": n, "copy_bytes": COPY_BYTES}
+    for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+        per = _per_kernel(_counter_rows(d), counter)
+        # the probe's copy is the largest-grid copy kernel of the run (set-up copies are small)
+        grids = [g for (k, g) in per if "copyBuffer" in k]
+        copy = [v for (k, g), vs in per.items() if "copyBuffer" in k and grids and g == max(grids) for v in vs]
+        fc = [v for (k, g), vs in per.items() if FC_KERNEL in k for v in vs]
+        if not copy or not fc:
+            raise SystemExit(f"{counter}: copy or GEMM dispatches missing ({sorted(per)})")
+        copy_kib = sorted(copy)[len(copy) // 2]
+        scale = COPY_BYTES / (copy_kib * 1024.0)  # bytes per counted KiB unit, from the copy of known size
+        fc_kib = sum(fc) / len(fc)
+        out[counter.lower()] = {"copy_kib_per_dispatch": copy_kib, "gemm_kib_per_dispatch": round(fc_kib, 1),
+                                "scale": round(scale, 4), "gemm_bytes_per_launch": round(fc_kib * 1024 * scale),
+                                "gemm_dispatches": len(fc)}
+    out["bytes_per_launch"] = out["fetch_size"]["gemm_bytes_per_launch"] + out["write_size"]["gemm_bytes_per_launch"]
+    path = os.path.join(ROOT, "profiles", "traffic_fc_gemm.json")
+    with open(path, "w") as fh:
+        json.dump(out, fh, indent=1)
+    print(json.dumps(out))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -70,7 +143,16 @@ def main():
     ap.add_argument("--prefix", type=int, default=512)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--traffic-probe", action="store_true",
+                    help="only run the kernels the HBM-traffic counters are read on (a 256 MiB device copy, then "
+                         "the MLP up-projection GEMM over every layer); meant to run under rocprofv3 --pmc")
+    ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="read two rocprofv3 --pmc outputs (FETCH_SIZE, WRITE_SIZE) of --traffic-probe and write "
+                         "profiles/traffic_fc_gemm.json; no GPU needed")
     args = ap.parse_args()
+    if args.traffic_from:
+        write_traffic(args.traffic_from[0], args.traffic_from[1], args.nodes)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}): this build has no multi-GPU path; "
               "the pass would shard by tensor parallelism, see DESIGN.md", file=sys.stderr)
@@ -95,6 +177,9 @@ def main():
     par = W.branching_tree([4, 2, 2, 1], N)
     toks = W.tree_tokens(par, cfg.vocab, seed=2)
     logits = torch.empty((N, cfg.vocab), dtype=torch.float32, device="cuda")
+    if args.traffic_probe:
+        probe_traffic(sess, cfg, N)
+        return
     graph = sess.capture_verify(P, toks, par, logits)
     outs = (torch.zeros(N, dtype=torch.int32, device="cuda"), torch.zeros(1, dtype=torch.int32, device="cuda"),
             torch.zeros(1, dtype=torch.int32, device="cuda"))
@@ -184,7 +269,7 @@ def main():
         okt, ovt = om.kv(max_nodes), om.kv(max_nodes)
         times = []
         t_start = time.time()
-        while len(times) < 5 and (time.time() - t_start) < 12.0:
+        while len(times) < 30 and (time.time() - t_start) < 12.0:
             t0 = time.time()
             oracle.tree_verify(om, kc, vc, P, toks, par, okt, ovt, threads)
             times.append(time.time() - t0)
