@@ -482,13 +482,35 @@ static void gemm_go(int kind, const void* Wp, int M, int K, int kcs, const uint1
     case EPI_QKV: gemm_kernel<NT, RB, EPI_QKV, VEC, NV, U><<<grid, 256, 0, s>>>(w, KC, RBtot, kcs, act, ep); break;
     case EPI_PARTIAL: gemm_kernel<NT, RB, EPI_PARTIAL, VEC, NV, U><<<grid, 256, 0, s>>>(w, KC, RBtot, kcs, act, ep); break;
     case EPI_GELU: gemm_kernel<NT, RB, EPI_GELU, VEC, NV, U><<<grid, 256, 0, s>>>(w, KC, RBtot, kcs, act, ep); break;
-    default: gemm_kernel<NT, RB, EPI_LOGITS, VEC, NV, U><<<grid, 256, 0, s>>>(w, KC, RBtot, kcs, act, ep); break;
+    default:
+      if constexpr (VEC) gemm_kernel<NT, RB, EPI_LOGITS, VEC, NV, U><<<grid, 256, 0, s>>>(w, KC, RBtot, kcs, act, ep);
+      break;
   }
+}
+
+// The LM head has thousands of row blocks: more of them per workgroup so the
+// activations (read once per workgroup) cost less than the weights.
+template <int NT, int RB, int U>
+static void gemm_head_go(const void* Wp, int M, int K, int kcs, const uint16_t* act, const Epi& ep, hipStream_t s) {
+  const int KC = K / 32, RBtot = (M + 15) / 16;
+  dim3 grid((RBtot + RB - 1) / RB, (KC + kcs - 1) / kcs);
+  gemm_kernel<NT, RB, EPI_LOGITS, false, 0, U><<<grid, 256, 0, s>>>((const u32x4*)Wp, KC, RBtot, kcs, act, ep);
 }
 
 hipError_t launch_gemm_bf16(int kind, int vec, const void* Wp, int M, int K, const uint16_t* act, int kcs,
                             const Epi& ep, hipStream_t s) {
   if (kcs <= 0) return hipErrorInvalidValue;
+  if (kind == EPI_LOGITS && !vec) {
+    if (ep.N > 256) return hipErrorInvalidValue;
+    switch (gemm_cfg(ep.N, 0).nt) {
+      case 1: gemm_head_go<1, 8, 3>(Wp, M, K, kcs, act, ep, s); break;
+      case 2: gemm_head_go<2, 8, 2>(Wp, M, K, kcs, act, ep, s); break;
+      case 4: gemm_head_go<4, 4, 2>(Wp, M, K, kcs, act, ep, s); break;
+      case 8: gemm_head_go<8, 2, 1>(Wp, M, K, kcs, act, ep, s); break;
+      default: gemm_head_go<16, 1, 1>(Wp, M, K, kcs, act, ep, s); break;
+    }
+    return hipGetLastError();
+  }
   if (vec) {
     if (ep.N > 16) return hipErrorInvalidValue;
     switch (gemm_cfg(ep.N, 1).nv) {
@@ -1028,35 +1050,78 @@ hipError_t launch_attn(int f32, int DH, const AttnArgs& a, hipStream_t s) {
 // ------------------------------------------------------------------ accept: greedy
 
 // argmax of each logits row, lowest index among equal maxima
-__global__ __launch_bounds__(256) void argmax_kernel(const float* __restrict__ logits, int V, int* __restrict__ g) {
-  __shared__ float sv[256];
-  __shared__ int si[256];
-  const int n = blockIdx.x;
+// greedy argmax per node (ties to the lowest token), in two stages so that
+// the logits stream through many workgroups: chunks of kArgmaxChunk logits
+// leave (value, index) pairs, then one wave per node merges its chunks
+constexpr int kArgmaxChunk = 2048;
+
+__device__ __forceinline__ bool better(float v, int i, float bv, int bi) { return v > bv || (v == bv && i < bi); }
+
+__global__ __launch_bounds__(256) void argmax_part_kernel(const float* __restrict__ logits, int V, int C,
+                                                          float* __restrict__ pv, int* __restrict__ pi) {
+  __shared__ float sv[4];
+  __shared__ int si[4];
+  const int c = blockIdx.x, n = blockIdx.y, tid = threadIdx.x;
   const float* row = logits + (size_t)n * V;
+  const int v0 = c * kArgmaxChunk;
+  float x[kArgmaxChunk / 256];
+#pragma unroll
+  for (int k = 0; k < kArgmaxChunk / 256; ++k) x[k] = row[min(v0 + tid + 256 * k, V - 1)];
   float best = -INFINITY;
   int bi = V;
-  for (int v = threadIdx.x; v < V; v += 256) {
-    const float x = row[v];
-    if (x > best || (x == best && v < bi)) {
-      best = x;
+#pragma unroll
+  for (int k = 0; k < kArgmaxChunk / 256; ++k) {
+    const int v = v0 + tid + 256 * k;
+    if (v < V && better(x[k], v, best, bi)) {
+      best = x[k];
       bi = v;
     }
   }
-  sv[threadIdx.x] = best;
-  si[threadIdx.x] = bi;
-  __syncthreads();
-  for (int off = 128; off > 0; off >>= 1) {
-    if (threadIdx.x < off) {
-      const float ov = sv[threadIdx.x + off];
-      const int oi = si[threadIdx.x + off];
-      if (ov > sv[threadIdx.x] || (ov == sv[threadIdx.x] && oi < si[threadIdx.x])) {
-        sv[threadIdx.x] = ov;
-        si[threadIdx.x] = oi;
-      }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    const float ov = __shfl_xor(best, off);
+    const int oi = __shfl_xor(bi, off);
+    if (better(ov, oi, best, bi)) {
+      best = ov;
+      bi = oi;
     }
-    __syncthreads();
   }
-  if (threadIdx.x == 0) g[n] = si[0] < V ? si[0] : 0;
+  if ((tid & 63) == 0) {
+    sv[tid >> 6] = best;
+    si[tid >> 6] = bi;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    for (int w = 1; w < 4; ++w)
+      if (better(sv[w], si[w], best, bi)) {
+        best = sv[w];
+        bi = si[w];
+      }
+    pv[(size_t)n * C + c] = best;
+    pi[(size_t)n * C + c] = bi;
+  }
+}
+
+__global__ __launch_bounds__(64) void argmax_final_kernel(const float* __restrict__ pv, const int* __restrict__ pi,
+                                                          int V, int C, int* __restrict__ g) {
+  const int n = blockIdx.x, lane = threadIdx.x;
+  float best = -INFINITY;
+  int bi = V;
+  for (int c = lane; c < C; c += 64)
+    if (better(pv[(size_t)n * C + c], pi[(size_t)n * C + c], best, bi)) {
+      best = pv[(size_t)n * C + c];
+      bi = pi[(size_t)n * C + c];
+    }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    const float ov = __shfl_xor(best, off);
+    const int oi = __shfl_xor(bi, off);
+    if (better(ov, oi, best, bi)) {
+      best = ov;
+      bi = oi;
+    }
+  }
+  if (lane == 0) g[n] = bi < V ? bi : 0;
 }
 
 // one thread: matched = parent matched and token == parent's argmax; keep the
@@ -1083,8 +1148,14 @@ __global__ void greedy_walk_kernel(const int* __restrict__ tokens, const int* __
   *next = g[best];
 }
 
-hipError_t launch_argmax(const float* logits, int N, int V, int* g, hipStream_t s) {
-  argmax_kernel<<<N, 256, 0, s>>>(logits, V, g);
+size_t argmax_work_bytes(int N, int V) { return (size_t)N * ((V + kArgmaxChunk - 1) / kArgmaxChunk) * 8; }
+
+hipError_t launch_argmax(const float* logits, int N, int V, int* g, void* work, hipStream_t s) {
+  const int C = (V + kArgmaxChunk - 1) / kArgmaxChunk;
+  float* pv = (float*)work;
+  int* pi = (int*)(pv + (size_t)N * C);
+  argmax_part_kernel<<<dim3(C, N), 256, 0, s>>>(logits, V, C, pv, pi);
+  argmax_final_kernel<<<N, 64, 0, s>>>(pv, pi, V, C, g);
   return hipGetLastError();
 }
 

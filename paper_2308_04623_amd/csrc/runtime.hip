@@ -74,6 +74,7 @@ struct ssd_kv {
   int* d_tree = nullptr;  // the staged tree (see stage_bytes)
   int* d_accept_tree = nullptr;  // tokens[N] parents[N] depth[N] for accept
   int* d_argmax = nullptr;
+  void* d_amwork = nullptr;  // argmax partials
   double *d_r = nullptr, *d_p = nullptr, *d_qq = nullptr;
   unsigned* d_err = nullptr;
   // pinned staging ring
@@ -305,6 +306,7 @@ extern "C" ssd_status ssd_kv_create(const ssd_model* m, int32_t max_ctx, int32_t
   const size_t o_acnt = take((size_t)c.n_head * cnt_ld * 4);
   const size_t o_tree = take(stage_bytes(max_nodes));
   const size_t o_at = take((size_t)3 * max_nodes * 4), o_am = take((size_t)max_nodes * 4);
+  const size_t o_amw = take(argmax_work_bytes(max_nodes, V));
   const size_t o_r = take((size_t)V * 8), o_p = take((size_t)V * 8), o_qq = take((size_t)V * 8);
   const size_t o_err = take(256);
   hipError_t e = hipMalloc(&kv->ws, off);
@@ -327,6 +329,7 @@ extern "C" ssd_status ssd_kv_create(const ssd_model* m, int32_t max_ctx, int32_t
   kv->d_tree = (int*)(b + o_tree);
   kv->d_accept_tree = (int*)(b + o_at);
   kv->d_argmax = (int*)(b + o_am);
+  kv->d_amwork = b + o_amw;
   kv->d_r = (double*)(b + o_r);
   kv->d_p = (double*)(b + o_p);
   kv->d_qq = (double*)(b + o_qq);
@@ -722,7 +725,7 @@ extern "C" ssd_status ssd_tree_accept(ssd_kv* kv, const ssd_tree* tree, const fl
   int* dt = kv->d_accept_tree;
   HIP_TRY(hipMemcpyAsync(dt, host, (size_t)3 * n * 4, hipMemcpyHostToDevice, s));
   if (greedy) {
-    HIP_TRY(launch_argmax(oracle_logits, n, V, kv->d_argmax, s));
+    HIP_TRY(launch_argmax(oracle_logits, n, V, kv->d_argmax, kv->d_amwork, s));
     HIP_TRY(launch_greedy_walk(dt, dt + n, dt + 2 * n, n, kv->d_argmax, accepted_path, path_len, next_token, s));
   } else {
     HIP_TRY(launch_sample_accept(dt, dt + n, n, V, oracle_logits, draft_probs, (double)tree->temperature, rng_seed,

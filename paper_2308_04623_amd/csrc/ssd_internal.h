@@ -116,7 +116,9 @@ hipError_t launch_gemm_bf16(int kind, int vec, const void* Wp, int M, int K, con
 hipError_t launch_attn(int f32, int DH, const AttnArgs& a, hipStream_t s);
 hipError_t launch_pack_bf16(const uint16_t* W, int M, int K, void* out, hipStream_t s);
 size_t packed_bytes(int M, int K);
-hipError_t launch_argmax(const float* logits, int N, int V, int* g, hipStream_t s);
+// greedy argmax per node; work: argmax_work_bytes(N, V) bytes of device scratch
+size_t argmax_work_bytes(int N, int V);
+hipError_t launch_argmax(const float* logits, int N, int V, int* g, void* work, hipStream_t s);
 hipError_t launch_greedy_walk(const int* tokens, const int* parents, const int* depth, int N, const int* g,
                               int* path, int* path_len, int* next, hipStream_t s);
 hipError_t launch_sample_accept(const int* tokens, const int* parents, int N, int V, const float* logits,
