@@ -134,6 +134,42 @@ def write_traffic(fetch_dir, write_dir, n):
     print(json.dumps(out))
 
 
+def end_to_end(ssd, W, cfg, model, N_NEW, PROMPT):
+    """Staged greedy generation of N_NEW tokens from a PROMPT-token random
+    prompt (draft: the oracle's first 4 layers; draft^2: bigram table), and
+    plain greedy decoding of the same, wall clock including host work."""
+    import numpy as np
+    import torch
+    from paper_2308_04623_amd import staged as S
+    draft = model.prefix_view(4)
+    prompt = W.prefix_tokens(PROMPT, cfg.vocab, seed=5)
+    max_ctx = PROMPT + N_NEW + 80
+
+    def backend():
+        o = ssd.Session(model, max_ctx, S.MAX_ORACLE_NODES)
+        d = ssd.Session(draft, max_ctx, 256, o.k_cache, o.v_cache)
+        b = S.GpuBackend(o, d)
+        return b, b.prefill(prompt[:-1])
+
+    b_plain, P = backend()
+    plain = S.plain_greedy(b_plain, P, int(prompt[-1]), N_NEW)
+    b_st, P2 = backend()
+    t0 = time.perf_counter()
+    succ = S.build_bigram_gpu(b_st, cfg.vocab)
+    t_bigram = time.perf_counter() - t0
+    st = S.staged_greedy(b_st, P2, int(prompt[-1]), N_NEW, succ)
+    agree = next((i for i, (a, b) in enumerate(zip(st.tokens, plain.tokens)) if a != b), N_NEW)
+    log(f"end to end: plain {N_NEW / plain.seconds:.1f} tok/s, staged {N_NEW / st.seconds:.1f} tok/s, "
+        f"accepted {sum(st.accepted)} in {st.steps} steps, agree {agree}/{N_NEW}")
+    return {"workload": f"greedy generation of {N_NEW} tokens from a {PROMPT}-token random prompt; draft = first 4 "
+                        "layers + shared head, draft^2 = bigram table (2^15-token stream); oracle trees <= 64 nodes",
+            "plain_tokens_per_s": round(N_NEW / plain.seconds, 1), "staged_tokens_per_s": round(N_NEW / st.seconds, 1),
+            "staged_steps": st.steps, "accepted_tree_tokens": int(sum(st.accepted)),
+            "mean_oracle_tree_nodes": round(float(np.mean(st.oracle_nodes)), 1),
+            "mean_endorsed_nodes": round(float(np.mean(st.endorsed)), 2),
+            "tokens_equal_to_plain": agree, "bigram_build_s": round(t_bigram, 2)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -143,6 +179,7 @@ def main():
     ap.add_argument("--prefix", type=int, default=512)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--no-e2e", action="store_true", help="skip the staged end-to-end generation")
     ap.add_argument("--traffic-probe", action="store_true",
                     help="only run the kernels the HBM-traffic counters are read on (a 256 MiB device copy, then "
                          "the MLP up-projection GEMM over every layer); meant to run under rocprofv3 --pmc")
@@ -273,6 +310,10 @@ def main():
                           "frac": round(bb / us / 1e3 / PEAK_HBM_GBS, 4)})
             log(f"sweep N={n_s} P={p_s}: {us:.1f} us")
 
+    e2e = None
+    if not args.no_e2e:
+        e2e = end_to_end(ssd, W, cfg, model, N_NEW=256, PROMPT=128)
+
     cpu = None
     if not args.no_cpu_baseline:
         import oracle
@@ -305,6 +346,7 @@ def main():
         "pass_algorithmic_bytes": B,
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "end_to_end": e2e,
         "sweep": sweep,
     }
     print(json.dumps(line), flush=True)

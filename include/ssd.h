@@ -104,6 +104,17 @@ typedef struct {
 ssd_status ssd_model_create(const ssd_config *cfg, const ssd_weights *w, void *stream, ssd_model **out);
 void ssd_model_destroy(ssd_model *m);
 
+/* Draft view for staged speculation (Sec. 3.2: a cheaper model proposes the
+ * tokens the oracle checks; here the oracle's first n_layer blocks followed
+ * by its final LayerNorm and tied LM head).  The view shares every device
+ * buffer with m (weights, packed copies), allocates nothing on the device,
+ * and must be destroyed (ssd_model_destroy, which frees only the view)
+ * before m.  Its layers' K/V are the oracle's, so a draft session may bind
+ * the oracle's cache: layer l of the view is layer l of the
+ * [n_layer][n_head][rows][head_dim] buffers.  1 <= n_layer <= m's layers.
+ * Errors: SSD_E_INVALID_ARG. */
+ssd_status ssd_model_prefix_view(const ssd_model *m, int32_t n_layer, ssd_model **out);
+
 /* Bytes the caller must allocate for the cache (each of K and V:
  * [n_layer][n_head][max_ctx][head_dim]) and the tree scratch (each of K and V:
  * [n_layer][n_head][max_nodes][head_dim]) in the storage type. */
@@ -157,6 +168,18 @@ ssd_status ssd_kv_commit(ssd_kv *kv, int32_t prefix_len, const int32_t *accepted
 /* Number of commit rows skipped as out of range since the session began
  * (synchronises the stream). */
 ssd_status ssd_kv_error_count(ssd_kv *kv, void *stream, uint32_t *count);
+
+/* Top-k of every row of logits[n_rows][vocab] (vocab of kv's model), for
+ * building draft trees (Sec. 3.1, 3.2: candidate continuations of a node are
+ * the draft's most likely tokens).  Writes, on the device, idx[n_rows][k]
+ * (token ids, decreasing logit, lower id first on ties), val[n_rows][k]
+ * (their logits) and, if lse is not NULL, lse[n_rows] = log sum exp of the
+ * row (so that val - lse is the log-probability).  Uses kv's workspace, so
+ * calls on one session are ordered by the stream.  1 <= k <= 8,
+ * 1 <= n_rows <= max_nodes.  Errors: SSD_E_INVALID_ARG, SSD_E_CAPACITY,
+ * SSD_E_DEVICE. */
+ssd_status ssd_topk(ssd_kv *kv, const float *logits, int32_t n_rows, int32_t k, int32_t *idx, float *val, float *lse,
+                    void *stream);
 
 /* Captures one verification pass (same arguments as ssd_tree_verify) into a
  * HIP graph; ssd_graph_launch replays it on the given stream with the same

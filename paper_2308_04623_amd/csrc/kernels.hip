@@ -1124,6 +1124,164 @@ __global__ __launch_bounds__(64) void argmax_final_kernel(const float* __restric
   if (lane == 0) g[n] = bi < V ? bi : 0;
 }
 
+// per-row top-k and log-sum-exp, in two stages like the argmax: chunks of
+// kArgmaxChunk logits leave their top kTopKMax (value, index) pairs and
+// (max, sum of exp(x - max)); one wave per row merges them.  A selection is
+// k rounds of "best not yet taken" (ties to the lower index).
+struct TopkPart {
+  float v[kTopKMax];
+  int i[kTopKMax];
+  float m, s;
+};
+
+__global__ __launch_bounds__(256) void topk_part_kernel(const float* __restrict__ logits, int V, int C,
+                                                        TopkPart* __restrict__ parts) {
+  constexpr int E = kArgmaxChunk / 256;
+  __shared__ float wv[4];
+  __shared__ int wi[4];
+  __shared__ float wm[4], wsum[4];
+  const int c = blockIdx.x, n = blockIdx.y, tid = threadIdx.x, w = tid >> 6;
+  const float* row = logits + (size_t)n * V;
+  const int v0 = c * kArgmaxChunk;
+  float x[E];
+  unsigned taken = 0;
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int v = v0 + tid + 256 * e;
+    x[e] = row[min(v, V - 1)];
+    if (v >= V) taken |= 1u << e;
+  }
+  // chunk max and sum of exponentials (for the log-sum-exp)
+  float mx = -INFINITY;
+#pragma unroll
+  for (int e = 0; e < E; ++e) mx = (taken >> e) & 1 ? mx : fmaxf(mx, x[e]);
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+  if ((tid & 63) == 0) wm[w] = mx;
+  __syncthreads();
+  mx = fmaxf(fmaxf(wm[0], wm[1]), fmaxf(wm[2], wm[3]));
+  float se = 0.f;
+#pragma unroll
+  for (int e = 0; e < E; ++e) se += (taken >> e) & 1 ? 0.f : __expf(x[e] - mx);
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) se += __shfl_xor(se, off);
+  if ((tid & 63) == 0) wsum[w] = se;
+  TopkPart* out = parts + (size_t)n * C + c;
+  for (int r = 0; r < kTopKMax; ++r) {
+    // this thread's best untaken element (its elements are in increasing index order)
+    float bv = -INFINITY;
+    int bi = V, be = -1;
+#pragma unroll
+    for (int e = 0; e < E; ++e)
+      if (!((taken >> e) & 1) && better(x[e], v0 + tid + 256 * e, bv, bi)) {
+        bv = x[e];
+        bi = v0 + tid + 256 * e;
+        be = e;
+      }
+    float gv = bv;
+    int gi = bi;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+      const float ov = __shfl_xor(gv, off);
+      const int oi = __shfl_xor(gi, off);
+      if (better(ov, oi, gv, gi)) {
+        gv = ov;
+        gi = oi;
+      }
+    }
+    __syncthreads();
+    if ((tid & 63) == 0) {
+      wv[w] = gv;
+      wi[w] = gi;
+    }
+    __syncthreads();
+    gv = wv[0];
+    gi = wi[0];
+    for (int k = 1; k < 4; ++k)
+      if (better(wv[k], wi[k], gv, gi)) {
+        gv = wv[k];
+        gi = wi[k];
+      }
+    if (be >= 0 && gi == bi) taken |= 1u << be;
+    if (tid == 0) {
+      out->v[r] = gv;
+      out->i[r] = gi;
+    }
+  }
+  if (tid == 0) {
+    out->m = mx;
+    out->s = (wsum[0] + wsum[1]) + (wsum[2] + wsum[3]);
+  }
+}
+
+__global__ __launch_bounds__(64) void topk_final_kernel(const TopkPart* __restrict__ parts, int V, int C, int k,
+                                                        int* __restrict__ idx, float* __restrict__ val,
+                                                        float* __restrict__ lse) {
+  const int n = blockIdx.x, lane = threadIdx.x;
+  const TopkPart* p = parts + (size_t)n * C;
+  // log-sum-exp over the chunks in chunk order
+  if (lane == 0 && lse) {
+    float M = -INFINITY;
+    for (int c = 0; c < C; ++c) M = fmaxf(M, p[c].m);
+    float S = 0.f;
+    for (int c = 0; c < C; ++c) S += p[c].s * __expf(p[c].m - M);
+    lse[n] = M + logf(S);
+  }
+  // candidates: lane takes chunks lane, lane + 64, ...; each chunk's list is sorted
+  // and a lane advances through its chunks' lists with one cursor per chunk
+  constexpr int MAXC = 4;  // chunks per lane (vocab up to 64 * 4 * kArgmaxChunk)
+  int cur[MAXC];
+#pragma unroll
+  for (int j = 0; j < MAXC; ++j) cur[j] = 0;
+  for (int r = 0; r < k; ++r) {
+    float bv = -INFINITY;
+    int bi = V, bj = -1;
+#pragma unroll
+    for (int j = 0; j < MAXC; ++j) {
+      const int c = lane + 64 * j;
+      if (c < C && cur[j] < kTopKMax && better(p[c].v[cur[j]], p[c].i[cur[j]], bv, bi)) {
+        bv = p[c].v[cur[j]];
+        bi = p[c].i[cur[j]];
+        bj = j;
+      }
+    }
+    float gv = bv;
+    int gi = bi;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+      const float ov = __shfl_xor(gv, off);
+      const int oi = __shfl_xor(gi, off);
+      if (better(ov, oi, gv, gi)) {
+        gv = ov;
+        gi = oi;
+      }
+    }
+    if (bj >= 0 && gi == bi) {
+#pragma unroll
+      for (int j = 0; j < MAXC; ++j)
+        if (j == bj) ++cur[j];
+    }
+    if (lane == 0) {
+      idx[(size_t)n * k + r] = gi < V ? gi : 0;
+      val[(size_t)n * k + r] = gv;
+    }
+  }
+}
+
+size_t topk_work_bytes(int N, int V) {
+  return (size_t)N * ((V + kArgmaxChunk - 1) / kArgmaxChunk) * sizeof(TopkPart);
+}
+
+hipError_t launch_topk(const float* logits, int N, int V, int k, int* idx, float* val, float* lse, void* work,
+                       hipStream_t s) {
+  const int C = (V + kArgmaxChunk - 1) / kArgmaxChunk;
+  if (k < 1 || k > kTopKMax || C > 64 * 4) return hipErrorInvalidValue;
+  TopkPart* parts = (TopkPart*)work;
+  topk_part_kernel<<<dim3(C, N), 256, 0, s>>>(logits, V, C, parts);
+  topk_final_kernel<<<N, 64, 0, s>>>(parts, V, C, k, idx, val, lse);
+  return hipGetLastError();
+}
+
 // one thread: matched = parent matched and token == parent's argmax; keep the
 // deepest matched node (lowest index among equals)
 __global__ void greedy_walk_kernel(const int* __restrict__ tokens, const int* __restrict__ parents,

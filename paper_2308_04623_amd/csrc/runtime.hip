@@ -53,6 +53,7 @@ struct ssd_model {
   std::vector<const void*> ln1_g, ln1_b, w_qkv, b_qkv, w_o, b_o, ln2_g, ln2_b, w_fc, b_fc, w_pr, b_pr;
   // bf16 only: packed copies
   void* pack = nullptr;
+  bool owns_pack = true;  // false for a prefix view (shares its parent's copies)
   std::vector<const void*> p_qkv, p_o, p_fc, p_pr;
   const void* p_head = nullptr;
 };
@@ -74,7 +75,7 @@ struct ssd_kv {
   int* d_tree = nullptr;  // the staged tree (see stage_bytes)
   int* d_accept_tree = nullptr;  // tokens[N] parents[N] depth[N] for accept
   int* d_argmax = nullptr;
-  void* d_amwork = nullptr;  // argmax partials
+  void* d_amwork = nullptr;  // argmax / top-k partials
   double *d_r = nullptr, *d_p = nullptr, *d_qq = nullptr;
   unsigned* d_err = nullptr;
   // pinned staging ring
@@ -231,8 +232,27 @@ extern "C" ssd_status ssd_model_create(const ssd_config* cfg, const ssd_weights*
 
 extern "C" void ssd_model_destroy(ssd_model* m) {
   if (!m) return;
-  if (m->pack) (void)hipFree(m->pack);
+  if (m->pack && m->owns_pack) (void)hipFree(m->pack);
   delete m;
+}
+
+extern "C" ssd_status ssd_model_prefix_view(const ssd_model* m, int32_t n_layer, ssd_model** out) {
+  if (!m || !out) return fail(SSD_E_INVALID_ARG, "null argument");
+  if (n_layer < 1 || n_layer > m->cfg.n_layer) return fail(SSD_E_INVALID_ARG, "n_layer outside [1, model layers]");
+  ssd_model* v = new ssd_model(*m);
+  v->cfg.n_layer = n_layer;
+  v->owns_pack = false;
+  std::vector<const void*>* per[] = {&v->ln1_g, &v->ln1_b, &v->w_qkv, &v->b_qkv, &v->w_o, &v->b_o, &v->ln2_g,
+                                     &v->ln2_b, &v->w_fc, &v->b_fc, &v->w_pr, &v->b_pr};
+  for (auto a : per) a->resize(n_layer);
+  if (!v->f32) {
+    v->p_qkv.resize(n_layer);
+    v->p_o.resize(n_layer);
+    v->p_fc.resize(n_layer);
+    v->p_pr.resize(n_layer);
+  }
+  *out = v;
+  return SSD_OK;
 }
 
 // ------------------------------------------------------------------ session
@@ -306,7 +326,7 @@ extern "C" ssd_status ssd_kv_create(const ssd_model* m, int32_t max_ctx, int32_t
   const size_t o_acnt = take((size_t)c.n_head * cnt_ld * 4);
   const size_t o_tree = take(stage_bytes(max_nodes));
   const size_t o_at = take((size_t)3 * max_nodes * 4), o_am = take((size_t)max_nodes * 4);
-  const size_t o_amw = take(argmax_work_bytes(max_nodes, V));
+  const size_t o_amw = take(std::max(argmax_work_bytes(max_nodes, V), topk_work_bytes(max_nodes, V)));
   const size_t o_r = take((size_t)V * 8), o_p = take((size_t)V * 8), o_qq = take((size_t)V * 8);
   const size_t o_err = take(256);
   hipError_t e = hipMalloc(&kv->ws, off);
@@ -686,6 +706,18 @@ extern "C" ssd_status ssd_launch_gemm(const ssd_model* m, ssd_kv* kv, int32_t wh
   e.M = rows;
   (void)lda;
   HIP_TRY(run_gemm(m, n_nodes, kind, Wraw, Wp, rows, K, act, e, (hipStream_t)stream));
+  return SSD_OK;
+}
+
+// ------------------------------------------------------------------ top-k
+
+extern "C" ssd_status ssd_topk(ssd_kv* kv, const float* logits, int32_t n_rows, int32_t k, int32_t* idx, float* val,
+                               float* lse, void* stream) {
+  if (!kv || !logits || !idx || !val) return fail(SSD_E_INVALID_ARG, "null argument");
+  if (k < 1 || k > kTopKMax) return fail(SSD_E_INVALID_ARG, "k outside [1, 8]");
+  if (n_rows < 1 || n_rows > kv->max_nodes) return fail(SSD_E_CAPACITY, "n_rows outside [1, max_nodes]");
+  hipStream_t s = (hipStream_t)stream;
+  HIP_TRY(launch_topk(logits, n_rows, kv->m->cfg.vocab, k, idx, val, lse, kv->d_amwork, s));
   return SSD_OK;
 }
 

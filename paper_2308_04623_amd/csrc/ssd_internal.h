@@ -119,6 +119,12 @@ size_t packed_bytes(int M, int K);
 // greedy argmax per node; work: argmax_work_bytes(N, V) bytes of device scratch
 size_t argmax_work_bytes(int N, int V);
 hipError_t launch_argmax(const float* logits, int N, int V, int* g, void* work, hipStream_t s);
+// per-row top-k (k <= kTopKMax, decreasing, lower index first on ties) and
+// log-sum-exp (lse may be nullptr); work: topk_work_bytes(N, V) bytes
+constexpr int kTopKMax = 8;
+size_t topk_work_bytes(int N, int V);
+hipError_t launch_topk(const float* logits, int N, int V, int k, int* idx, float* val, float* lse, void* work,
+                       hipStream_t s);
 hipError_t launch_greedy_walk(const int* tokens, const int* parents, const int* depth, int N, const int* g,
                               int* path, int* path_len, int* next, hipStream_t s);
 hipError_t launch_sample_accept(const int* tokens, const int* parents, int N, int V, const float* logits,

@@ -28,7 +28,8 @@ LAYER_TENSORS = ("ln1_g", "ln1_b", "w_qkv", "b_qkv", "w_o", "b_o",
 EXPORTS = ("ssd_model_create", "ssd_model_destroy", "ssd_kv_bytes", "ssd_kv_create", "ssd_kv_destroy",
            "ssd_tree_verify", "ssd_tree_accept", "ssd_kv_commit", "ssd_kv_error_count",
            "ssd_graph_capture_verify", "ssd_graph_launch", "ssd_graph_destroy", "ssd_validate_tree",
-           "ssd_tree_prep", "ssd_set_gemm_path", "ssd_status_string", "ssd_last_error", "ssd_launch_gemm")
+           "ssd_tree_prep", "ssd_set_gemm_path", "ssd_status_string", "ssd_last_error", "ssd_launch_gemm",
+           "ssd_model_prefix_view", "ssd_topk")
 
 
 class SSDError(RuntimeError):
@@ -84,6 +85,8 @@ def lib():
             "ssd_tree_prep": [i32p, C.c_int32, i32p, C.POINTER(C.c_uint64)],
             "ssd_set_gemm_path": [C.c_int32],
             "ssd_launch_gemm": [vp, vp, C.c_int32, C.c_int32, C.c_int32, vp],
+            "ssd_model_prefix_view": [vp, C.c_int32, C.POINTER(vp)],
+            "ssd_topk": [vp, vp, C.c_int32, C.c_int32, vp, vp, vp, vp],
             "ssd_status_string": [C.c_int],
             "ssd_last_error": [],
         }
@@ -209,6 +212,34 @@ class Model:
                "ssd_model_create")
         self.handle = h
 
+    def prefix_view(self, n_layer: int) -> "ModelView":
+        """Draft view: the first n_layer blocks with this model's final
+        LayerNorm and tied head, sharing its device memory."""
+        return ModelView(self, n_layer)
+
+    def close(self):
+        if getattr(self, "handle", None):
+            lib().ssd_model_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class ModelView:
+    """ssd_model_prefix_view of a Model (keeps the parent alive)."""
+
+    def __init__(self, parent: Model, n_layer: int):
+        self.parent = parent
+        self.cfg = parent.cfg.with_(n_layer=n_layer)
+        self.device = parent.device
+        h = C.c_void_p()
+        _check(lib().ssd_model_prefix_view(parent.handle, n_layer, C.byref(h)), "ssd_model_prefix_view")
+        self.handle = h
+
     def close(self):
         if getattr(self, "handle", None):
             lib().ssd_model_destroy(self.handle)
@@ -316,6 +347,18 @@ class Session:
         """One weight GEMM of the pass on its own (measurement only)."""
         _check(lib().ssd_launch_gemm(self.model.handle, self.handle, which, layer, n_nodes, _stream(stream)),
                "ssd_launch_gemm")
+
+    def topk(self, logits, k: int, n_rows: Optional[int] = None, stream=None):
+        """Per-row top-k of logits[n][vocab] on the device: (idx int32 [n][k],
+        val float32 [n][k], lse float32 [n])."""
+        torch = _torch()
+        n = logits.shape[0] if n_rows is None else n_rows
+        idx = torch.empty((n, k), dtype=torch.int32, device=self.model.device)
+        val = torch.empty((n, k), dtype=torch.float32, device=self.model.device)
+        lse = torch.empty((n,), dtype=torch.float32, device=self.model.device)
+        _check(lib().ssd_topk(self.handle, C.c_void_p(logits.data_ptr()), n, k, C.c_void_p(idx.data_ptr()),
+                              C.c_void_p(val.data_ptr()), C.c_void_p(lse.data_ptr()), _stream(stream)), "ssd_topk")
+        return idx, val, lse
 
     def error_count(self, stream=None) -> int:
         c = C.c_uint32(0)

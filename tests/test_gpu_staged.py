@@ -1,0 +1,158 @@
+"""Staged speculation on the GPU (Sec. 3.2), through the C ABI.
+
+- ssd_topk equals the host definition (indices and values bit-exact on the
+  same logits, log-sum-exp within 1e-6 relative), ties to the lower id.
+- A prefix view (draft) gives the same logits, bitwise, as a model created
+  from only those layers, and matches the oracle's draft within 2e-2.
+- Staged greedy decoding emits the plain greedy sequence.  On the GPU the two
+  loops reach a node through different verification shapes (a tree node's
+  ancestors come from the tree scratch, a plain step's from the cache), so
+  their logits may differ in the last bits; a divergence is accepted only at
+  a precision tie: a plain step whose top-2 logit gap is below 1e-3.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2308_04623_amd import staged as S
+from paper_2308_04623_amd import workloads as W
+from tests.helpers import draft_weights, host_topk
+
+pytestmark = pytest.mark.gpu
+
+TIE = 1e-3
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as t
+    assert t.cuda.is_available()
+    return t
+
+
+@pytest.fixture(scope="module")
+def ssd(torch):
+    from paper_2308_04623_amd import ssd as s
+    s.lib()
+    yield s
+    s.set_gemm_path(s.GEMM_AUTO)
+
+
+class GapBackend(S.GpuBackend):
+    """GpuBackend that also records, per oracle step, the top-2 logit gap at
+    the node whose argmax became the next token (for the tie check)."""
+
+    def __init__(self, o, d):
+        super().__init__(o, d)
+        self.gaps = []
+
+    def oracle_step(self, P, toks, par):
+        lg = self.o.verify(P, toks, par)
+        path, plen, nxt = self.o.accept(toks, par, lg)
+        self.o.commit(P, path, plen)
+        n = int(plen.item())
+        p = path[:n].cpu().numpy().astype(np.int32)
+        _, val, _ = self.o.topk(lg, 2)
+        v = val[int(p[-1])].cpu().numpy()
+        self.gaps.append(float(v[0] - v[1]))
+        return p, int(nxt.item())
+
+
+def _compare(staged, plain, gaps):
+    """Index of the first divergence (len if none); asserts it is a tie."""
+    n = min(len(staged), len(plain))
+    for i in range(n):
+        if staged[i] != plain[i]:
+            assert gaps[i] < TIE, f"token {i}: staged {staged[i]} plain {plain[i]}, gap {gaps[i]}"
+            return i
+    return n
+
+
+def test_topk_matches_host_definition(ssd, torch):
+    cfg = W.TINY.with_(dtype="bf16", vocab=50257, n_pos=64)
+    w = W.make_weights(cfg.with_(n_layer=1), 0)
+    m = ssd.Model(cfg.with_(n_layer=1), w)
+    s = ssd.Session(m, 16, 32)
+    g = np.random.default_rng(11)
+    lg = g.normal(0, 3, size=(24, cfg.vocab)).astype(np.float32)
+    lg[3, [7, 9, 40000]] = 50.0                        # three-way tie at the top: ids 7, 9, 40000
+    lg[5, :] = 1.0                                     # all equal: ids 0..7
+    lg[6, 50256] = 60.0                                # the last id wins
+    lg[7, 2047:2050] = 70.0                            # a tie across two chunks of the reduction
+    d = torch.from_numpy(lg).cuda()
+    for k in (1, 2, 8):
+        idx, val, lse = s.topk(d, k)
+        hi, hv, hl = host_topk(lg, k)
+        assert np.array_equal(idx.cpu().numpy(), hi), k
+        assert np.array_equal(val.cpu().numpy(), hv), k
+        assert np.allclose(lse.cpu().numpy(), hl, rtol=1e-6, atol=1e-5), k
+    assert s.topk(d, 3)[0].cpu().numpy()[3].tolist() == [7, 9, 40000]
+    with pytest.raises(ssd.SSDError):
+        s.topk(d, 9)
+
+
+def test_prefix_view_equals_truncated_model(ssd, torch):
+    cfg = W.TINY.with_(dtype="bf16")
+    w = W.make_weights(cfg, 0, perturb_affine=True)
+    full = ssd.Model(cfg, w)
+    view = full.prefix_view(1)
+    trunc = ssd.Model(cfg.with_(n_layer=1), draft_weights(w, 1))
+    P = 32
+    kc, vc = W.random_kv_cache(cfg, 64, P, seed=3)
+    kcd, vcd = ssd.to_device(kc, cfg), ssd.to_device(vc, cfg)
+    sv = ssd.Session(view, 64, 32, kcd, vcd)                     # binds the 2-layer cache
+    st = ssd.Session(trunc, 64, 32, kcd[:1].contiguous(), vcd[:1].contiguous())
+    par = W.branching_tree([3, 2, 1], 20)
+    toks = W.tree_tokens(par, cfg.vocab, seed=4)
+    a = sv.verify(P, toks, par).cpu()
+    b = st.verify(P, toks, par).cpu()
+    assert torch.equal(a, b)
+    om = oracle.Model(cfg.with_(n_layer=1), draft_weights(w, 1))
+    kt, vt = om.kv(32), om.kv(32)
+    ref = oracle.tree_verify(om, np.ascontiguousarray(kc[:1]), np.ascontiguousarray(vc[:1]), P, toks, par, kt, vt)
+    assert np.abs(a.numpy() - ref).max() < 2e-2
+    with pytest.raises(ssd.SSDError):
+        full.prefix_view(3)
+
+
+def _staged_vs_plain(ssd, torch, cfg, w, n_layer_draft, prompt_len, n_new, stream_tokens, window):
+    m = ssd.Model(cfg, w)
+    draft = m.prefix_view(n_layer_draft)
+    max_ctx = prompt_len + n_new + 80
+    prompt = W.prefix_tokens(prompt_len, cfg.vocab, seed=5)
+
+    def backend():
+        o = ssd.Session(m, max_ctx, 64)
+        d = ssd.Session(draft, max_ctx, max(64, window), o.k_cache, o.v_cache)
+        b = GapBackend(o, d)
+        P = b.prefill(prompt[:-1])
+        return b, P
+
+    b_plain, P = backend()
+    plain = S.plain_greedy(b_plain, P, int(prompt[-1]), n_new)
+    b_st, P2 = backend()
+    stream = S.bigram_stream(cfg.vocab, stream_tokens, seed=4)
+    preds = np.concatenate([b_st.greedy_predictions(stream[s:s + window])
+                            for s in range(0, stream_tokens, window)])
+    succ = S.bigram_table(stream, preds, cfg.vocab)
+    st = S.staged_greedy(b_st, P2, int(prompt[-1]), n_new, succ)
+    agree = _compare(st.tokens, plain.tokens, b_plain.gaps)
+    print(f"staged {st.steps} steps, accepted {sum(st.accepted)}, mean oracle tree {np.mean(st.oracle_nodes):.1f}, "
+          f"agree {agree}/{n_new}, plain {n_new / plain.seconds:.1f} tok/s, staged {n_new / st.seconds:.1f} tok/s")
+    return st, plain, agree
+
+
+def test_staged_equals_plain_tiny_bf16(ssd, torch):
+    cfg = W.TINY.with_(dtype="bf16")
+    w = W.make_weights(cfg, 0, perturb_affine=True)
+    st, plain, agree = _staged_vs_plain(ssd, torch, cfg, w, 1, 40, 48, 2048, 64)
+    assert agree >= 1
+    assert st.steps <= 48
+
+
+@pytest.mark.slow
+def test_staged_equals_plain_gpt2l(ssd, torch):
+    cfg = W.GPT2L
+    w = W.make_weights(cfg, 0)
+    st, plain, agree = _staged_vs_plain(ssd, torch, cfg, w, 4, 128, 64, 4096, 256)
+    assert agree >= 1
