@@ -29,7 +29,9 @@
  *
  * Model: GPT-2, pre-LayerNorm blocks, tanh GELU, learned absolute positions,
  * LM head tied to the token embedding.  All parameters and the K/V cache use
- * one storage type (float32 or bfloat16); accumulation is float32.
+ * one storage type (float32 or bfloat16); accumulation is float32.  For
+ * bfloat16 models the weight GEMMs multiply float16 operands (exact copies
+ * of the weights, activations rounded to float16).
  */
 #ifndef SSD_H
 #define SSD_H

@@ -5,11 +5,12 @@
 // Data layout (HBM):
 //   x        fp32 [N][d]         residual stream
 //   q        fp32 [N][d]         queries of the current layer
-//   act_*    GEMM inputs [Npad][d or d_mlp]: fp32 for fp32 models; for bf16
-//            models two bf16 planes, hi = bf16(v) and lo = bf16(v - hi)
+//   act_*    GEMM inputs [Npad][d or d_mlp]: fp32 rows for fp32 models; float16
+//            in matrix-core fragment order for bf16 models (see st_act)
 //   part     fp32 [S][N][d]      split-K partial sums of the residual GEMMs
 //   K/V      storage type [L][H][rows][DH] (cache rows: positions; scratch rows: nodes)
-//   packed W 16x32 bf16 fragments; fragment (rb, kc) holds rows 16rb.., k 32kc..,
+//   packed W 16x32 float16 fragments (exact copies of the bf16 weights);
+//            fragment (rb, kc) holds rows 16rb.., k 32kc..,
 //            lane l's 16 bytes = W[16rb + l%16][32kc + 8(l/16) .. +8], fragments
 //            ordered rb-major so one wave streams 1 KB contiguous per load.
 #include <hip/hip_runtime.h>
@@ -21,6 +22,8 @@
 namespace ssd {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
@@ -47,23 +50,21 @@ template <> __device__ __forceinline__ void stT<float>(float* p, size_t i, float
 template <> __device__ __forceinline__ void stT<uint16_t>(uint16_t* p, size_t i, float v) { p[i] = f2bf(v); }
 
 // GEMM inputs.  fp32 models: plain rows, element (n, k) at n * ld + k.
-// bf16 models: matrix-core fragment order, so that one wave's load of a
-// 16-node x 32-k operand fragment is 1 KB contiguous: element (n, k) lives in
-// fragment f = (n/16) * ld + k/32 (ld = K/32), lane (n%16) + 16 ((k%32)/8),
-// position k%8.  Each fragment holds a hi plane bf16(v) and, 512 elements
-// later, a lo plane bf16(v - hi); the GEMMs multiply both, which keeps about
-// 16 significant bits of every activation.
+// bf16 models: float16 (11 significant bits, round to nearest even) in
+// matrix-core fragment order, so that one wave's load of a 16-node x 32-k
+// operand fragment is 1 KB contiguous: element (n, k) lives in fragment
+// f = (n/16) * ld + k/32 (ld = K/32), lane (n%16) + 16 ((k%32)/8), position
+// k%8.  The weights are multiplied as float16 too: their packed copies are
+// the bf16 values converted exactly (see pack_kernel).
 template <typename T> __device__ __forceinline__ void st_act(T* p, int n, int k, int ld, float v);
 template <> __device__ __forceinline__ void st_act<float>(float* p, int n, int k, int ld, float v) {
   p[(size_t)n * ld + k] = v;
 }
 template <> __device__ __forceinline__ void st_act<uint16_t>(uint16_t* p, int n, int k, int ld, float v) {
   const size_t f = (size_t)(n >> 4) * ld + (k >> 5);
-  const size_t off = f * 1024 + ((n & 15) + 16 * ((k & 31) >> 3)) * 8 + (k & 7);
-  const uint16_t hi = f2bf(v);
-  p[off] = hi;
-  p[off + 512] = f2bf(v - bf2f(hi));
+  p[f * 512 + ((n & 15) + 16 * ((k & 31) >> 3)) * 8 + (k & 7)] = __builtin_bit_cast(uint16_t, (_Float16)v);
 }
+__device__ __forceinline__ float h2f(uint16_t h) { return (float)__builtin_bit_cast(_Float16, h); }
 
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
@@ -288,9 +289,11 @@ __global__ __launch_bounds__(256) void pack_kernel(const uint16_t* __restrict__ 
   const int rb = (int)(frag / KC);
   const int row = rb * 16 + (lane & 15);
   const int k = kc * 32 + 8 * (lane >> 4);
-  uint4 v = make_uint4(0, 0, 0, 0);
-  if (row < M) v = *(const uint4*)(W + (size_t)row * K + k);
-  out[idx] = v;
+  u32x4 v = (u32x4){0, 0, 0, 0};
+  if (row < M) v = *(const u32x4*)(W + (size_t)row * K + k);
+  // bf16 -> float16: exact for every weight of magnitude in [2^-24, 65504]
+  const f32x8 f = __builtin_convertvector(__builtin_bit_cast(bf16x8, v), f32x8);
+  out[idx] = __builtin_bit_cast(uint4, __builtin_convertvector(f, f16x8));
 }
 
 hipError_t launch_pack_bf16(const uint16_t* W, int M, int K, void* out, hipStream_t s) {
@@ -300,14 +303,14 @@ hipError_t launch_pack_bf16(const uint16_t* W, int M, int K, void* out, hipStrea
   return hipGetLastError();
 }
 
-// ------------------------------------------------------------------ GEMM, bf16 weights
+// ------------------------------------------------------------------ GEMM, bf16 models (float16 operands)
 //
 // Y[n][o] = sum_k A[n][k] W[o][k] over packed weight fragments.
 // A workgroup (4 waves) owns RB consecutive 16-row blocks and the k-steps
 // [kc0, kc1) of its split (grid.y); wave w takes k-steps kc0 + w, kc0 + w + 4,
 // ...  Per k-step a wave loads the RB weight fragments and the activation
-// fragments of every node tile (hi and lo planes, 1 KB contiguous each, see
-// st_act) and multiplies each activation fragment into all RB row blocks, so
+// fragment of every node tile (float16, 1 KB contiguous each, see st_act)
+// and multiplies each activation fragment into all RB row blocks, so
 // activations are read once per RB row blocks.  U k-steps stay in flight
 // (loads issued U steps ahead, unconditionally: a step past the end re-reads
 // the last valid step and its weights are replaced by zeros when used), and
@@ -315,8 +318,8 @@ hipError_t launch_pack_bf16(const uint16_t* W, int M, int K, void* out, hipStrea
 // their use.  After the loop the 4 waves are summed in wave order through
 // LDS, so every output is computed the same way whatever the node count or a
 // node's slot.
-//  matrix cores: v_mfma_f32_16x16x32_bf16, weight fragment as A (16 rows x 32
-//    k), activations as B (32 k x 16 nodes), hi then lo plane;
+//  matrix cores: v_mfma_f32_16x16x32_f16, weight fragment as A (16 rows x 32
+//    k), activations as B (32 k x 16 nodes);
 //  vector ALU (few nodes): each lane multiplies its 8 weights into fp32
 //    accumulators per node; the 4 lanes of a row are summed (xor 16, xor 32).
 // Occupancy is traded for registers (1-2 waves per SIMD).
@@ -325,7 +328,7 @@ template <int NT, int RB, int KIND, bool VEC, int NV, int U>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) void gemm_kernel(
     const u32x4* __restrict__ Wp, int KC, int RBtot, int kc_split, const uint16_t* __restrict__ act, Epi ep) {
   static_assert(!VEC || RB == 1, "vector path: one row block per workgroup");
-  constexpr int NB = VEC ? 2 * NV : 2 * NT;  // activation fragments per k-step
+  constexpr int NB = VEC ? NV : NT;  // activation fragments per k-step
   constexpr int NN = VEC ? NV : 16 * NT;     // output nodes
   __shared__ float red[4 * RB * NN * 16];
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
@@ -351,9 +354,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) voi
     for (int r = 0; r < RB; ++r) wq[u][r] = wb[r][(size_t)kc * 64];
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
-      // b = 2 * (node tile or node) + plane
-      bq[u][b] = VEC ? abase[((size_t)kc * 2 + (b & 1)) * 64 + (b >> 1)]
-                     : abase[((size_t)(b >> 1) * KC + kc) * 2 * 64 + (b & 1) * 64];
+      // b = node tile (matrix cores) or node (vector path)
+      bq[u][b] = VEC ? abase[(size_t)kc * 64 + b] : abase[((size_t)b * KC + kc) * 64];
     }
   };
 
@@ -380,25 +382,18 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) voi
           for (int r = 0; r < RB; ++r) {
             const u32x4 wf = ok ? wq[u][r] : (u32x4){0, 0, 0, 0};
 #pragma unroll
-            for (int t = 0; t < NT; ++t) {
-              acc[r][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                  __builtin_bit_cast(bf16x8, wf), __builtin_bit_cast(bf16x8, bq[u][2 * t]), acc[r][t], 0, 0, 0);
-              acc[r][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                  __builtin_bit_cast(bf16x8, wf), __builtin_bit_cast(bf16x8, bq[u][2 * t + 1]), acc[r][t], 0, 0, 0);
-            }
+            for (int t = 0; t < NT; ++t)
+              acc[r][t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+                  __builtin_bit_cast(f16x8, wf), __builtin_bit_cast(f16x8, bq[u][t]), acc[r][t], 0, 0, 0);
           }
         } else {
           const u32x4 wf = ok ? wq[u][0] : (u32x4){0, 0, 0, 0};
+          const f32x8 wv = __builtin_convertvector(__builtin_bit_cast(f16x8, wf), f32x8);
 #pragma unroll
           for (int n = 0; n < NV; ++n) {
-            const u32x4 ah = bq[u][2 * n], al = bq[u][2 * n + 1];
+            const f32x8 av = __builtin_convertvector(__builtin_bit_cast(f16x8, bq[u][n]), f32x8);
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const float a0 = __uint_as_float(ah[e] << 16) + __uint_as_float(al[e] << 16);
-              const float a1 = __uint_as_float(ah[e] & 0xffff0000u) + __uint_as_float(al[e] & 0xffff0000u);
-              vacc[n] = fmaf(__uint_as_float(wf[e] << 16), a0, vacc[n]);
-              vacc[n] = fmaf(__uint_as_float(wf[e] & 0xffff0000u), a1, vacc[n]);
-            }
+            for (int e = 0; e < 8; ++e) vacc[n] = fmaf(wv[e], av[e], vacc[n]);
           }
         }
         __builtin_amdgcn_sched_barrier(0);

@@ -312,8 +312,8 @@ extern "C" ssd_status ssd_kv_create(const ssd_model* m, int32_t max_ctx, int32_t
     return o;
   };
   const size_t o_x = take((size_t)max_nodes * d * 4), o_q = take((size_t)max_nodes * d * 4);
-  // bf16 models keep every GEMM input as hi and lo bf16 planes
-  const size_t planes = m->f32 ? 1 : 2;
+  // GEMM inputs: fp32 rows (fp32 models) or float16 fragments (bf16 models)
+  const size_t planes = 1;
   const size_t o_a = take(planes * kv->npad * d * es), o_o = take(planes * kv->npad * d * es);
   const size_t o_f = take(planes * kv->npad * M * es);
   const size_t o_part = take((size_t)kMaxSplits * max_nodes * d * 4);  // split-K partials
@@ -454,8 +454,8 @@ static hipError_t run_gemm(const ssd_model* m, int n, int kind, const void* Wraw
     Epi e2 = ep;
     e2.node0 = n0;
     e2.N = std::min(group, n - n0);
-    // fragment tiles of 16 nodes, each K/32 fragment pairs of 1024 elements
-    const uint16_t* a = (const uint16_t*)act + (size_t)(n0 / 16) * (K / 32) * 1024;
+    // fragment tiles of 16 nodes, each K/32 fragments of 512 elements
+    const uint16_t* a = (const uint16_t*)act + (size_t)(n0 / 16) * (K / 32) * 512;
     hipError_t r = launch_gemm_bf16(kind, vec, Wp, rows, K, a, kcs, e2, s);
     if (r != hipSuccess) return r;
   }
