@@ -145,10 +145,10 @@ def end_to_end(ssd, W, cfg, model, N_NEW, PROMPT):
     prompt = W.prefix_tokens(PROMPT, cfg.vocab, seed=5)
     max_ctx = PROMPT + N_NEW + 80
 
-    def backend():
+    def backend(record_gaps=False):
         o = ssd.Session(model, max_ctx, S.MAX_ORACLE_NODES)
         d = ssd.Session(draft, max_ctx, 256, o.k_cache, o.v_cache)
-        b = S.GpuBackend(o, d)
+        b = S.GpuBackend(o, d, record_gaps)
         return b, b.prefill(prompt[:-1])
 
     b_plain, P = backend()
@@ -159,15 +159,26 @@ def end_to_end(ssd, W, cfg, model, N_NEW, PROMPT):
     t_bigram = time.perf_counter() - t0
     st = S.staged_greedy(b_st, P2, int(prompt[-1]), N_NEW, succ)
     agree = next((i for i, (a, b) in enumerate(zip(st.tokens, plain.tokens)) if a != b), N_NEW)
+    gap = None
+    if agree < N_NEW:
+        # untimed replay of plain decoding up to the divergence, recording the
+        # top-2 logit gap of each step: a gap under 1e-3 is a precision tie
+        # between the two verification shapes, anything larger a real mismatch
+        b_gap, P3 = backend(record_gaps=True)
+        S.plain_greedy(b_gap, P3, int(prompt[-1]), agree + 1)
+        gap = b_gap.gaps[agree]
     log(f"end to end: plain {N_NEW / plain.seconds:.1f} tok/s, staged {N_NEW / st.seconds:.1f} tok/s, "
-        f"accepted {sum(st.accepted)} in {st.steps} steps, agree {agree}/{N_NEW}")
+        f"accepted {sum(st.accepted)} in {st.steps} steps, agree {agree}/{N_NEW}"
+        + ("" if gap is None else f", plain top-2 gap at the divergence {gap:.3g}"))
     return {"workload": f"greedy generation of {N_NEW} tokens from a {PROMPT}-token random prompt; draft = first 4 "
                         "layers + shared head, draft^2 = bigram table (2^15-token stream); oracle trees <= 64 nodes",
             "plain_tokens_per_s": round(N_NEW / plain.seconds, 1), "staged_tokens_per_s": round(N_NEW / st.seconds, 1),
             "staged_steps": st.steps, "accepted_tree_tokens": int(sum(st.accepted)),
             "mean_oracle_tree_nodes": round(float(np.mean(st.oracle_nodes)), 1),
             "mean_endorsed_nodes": round(float(np.mean(st.endorsed)), 2),
-            "tokens_equal_to_plain": agree, "bigram_build_s": round(t_bigram, 2)}
+            "tokens_equal_to_plain": agree,
+            "plain_top2_gap_at_divergence": None if gap is None else round(gap, 6),
+            "bigram_build_s": round(t_bigram, 2)}
 
 
 def main():

@@ -201,8 +201,11 @@ class GpuBackend:
     oracle session's cache (the draft's layers are the oracle's first ones),
     so the oracle's commit serves both."""
 
-    def __init__(self, oracle_session, draft_session):
+    def __init__(self, oracle_session, draft_session, record_gaps: bool = False):
         self.o, self.d = oracle_session, draft_session
+        # per oracle step, the top-2 logit gap at the node whose argmax became
+        # the next token (to tell precision ties from real divergences)
+        self.gaps = [] if record_gaps else None
 
     def prefill(self, tokens: np.ndarray, P: int = 0) -> int:
         """Cache `tokens` after P cached ones, in chains of at most max_nodes
@@ -231,7 +234,12 @@ class GpuBackend:
         path, plen, nxt = self.o.accept(toks, par, lg)
         self.o.commit(P, path, plen)
         n = int(plen.item())
-        return path[:n].cpu().numpy().astype(np.int32), int(nxt.item())
+        p = path[:n].cpu().numpy().astype(np.int32)
+        if self.gaps is not None:
+            _, val, _ = self.o.topk(lg, 2)
+            v = val[int(p[-1])].cpu().numpy()
+            self.gaps.append(float(v[0] - v[1]))
+        return p, int(nxt.item())
 
     def greedy_predictions(self, window_tokens: np.ndarray) -> np.ndarray:
         """The draft's greedy next token at every position of a window fed as

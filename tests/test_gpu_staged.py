@@ -38,26 +38,6 @@ def ssd(torch):
     s.set_gemm_path(s.GEMM_AUTO)
 
 
-class GapBackend(S.GpuBackend):
-    """GpuBackend that also records, per oracle step, the top-2 logit gap at
-    the node whose argmax became the next token (for the tie check)."""
-
-    def __init__(self, o, d):
-        super().__init__(o, d)
-        self.gaps = []
-
-    def oracle_step(self, P, toks, par):
-        lg = self.o.verify(P, toks, par)
-        path, plen, nxt = self.o.accept(toks, par, lg)
-        self.o.commit(P, path, plen)
-        n = int(plen.item())
-        p = path[:n].cpu().numpy().astype(np.int32)
-        _, val, _ = self.o.topk(lg, 2)
-        v = val[int(p[-1])].cpu().numpy()
-        self.gaps.append(float(v[0] - v[1]))
-        return p, int(nxt.item())
-
-
 def _compare(staged, plain, gaps):
     """Index of the first divergence (len if none); asserts it is a tie."""
     n = min(len(staged), len(plain))
@@ -124,7 +104,7 @@ def _staged_vs_plain(ssd, torch, cfg, w, n_layer_draft, prompt_len, n_new, strea
     def backend():
         o = ssd.Session(m, max_ctx, 64)
         d = ssd.Session(draft, max_ctx, max(64, window), o.k_cache, o.v_cache)
-        b = GapBackend(o, d)
+        b = S.GpuBackend(o, d, record_gaps=True)
         P = b.prefill(prompt[:-1])
         return b, P
 
