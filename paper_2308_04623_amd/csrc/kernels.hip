@@ -77,6 +77,39 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
+// ------------------------------------------------------------------ weight prefetch
+//
+// Worker w of a launch (its block nmain + w) loads the weight fragments of
+// the next GEMM's blocks L = w (mod 8), the j-th of them for j = w / 8 (mod
+// nworkers / 8), exactly the fragments that block will read, with direct-to-LDS
+// 16-byte loads into a 1 KB area per wave that nothing reads: no registers,
+// up to 48 loads in flight per wave.
+constexpr int kPrefetchLdsWords = 4 * 256;  // 1 KB per wave, 4 waves
+
+__device__ __forceinline__ void prefetch_weights(const Prefetch& pf, int worker, uint32_t* lds) {
+  const int tid = threadIdx.x, nw = min((int)(blockDim.x >> 6), 4), w = tid >> 6, lane = tid & 63;
+  if (w >= nw) return;
+  const int r = worker & 7, step = pf.nworkers >> 3;
+  const u32x4* W = (const u32x4*)pf.Wp + lane;
+  __attribute__((address_space(3))) void* dst = (__attribute__((address_space(3))) void*)(lds + w * 256);
+  int issued = 0;
+  for (int j = worker >> 3;; j += step) {
+    const int L = r + 8 * j;
+    if (L >= pf.nblk) break;
+    const int bx = L % pf.gx, by = L / pf.gx;
+    const int kc0 = by * pf.kcs, nk = min(pf.KC, kc0 + pf.kcs) - kc0;
+    for (int f = w; f < pf.RB * nk; f += nw) {
+      const int row = min(bx * pf.RB + f / nk, pf.RBtot - 1), kc = kc0 + f % nk;
+      __builtin_amdgcn_global_load_lds((const void*)(W + ((size_t)row * pf.KC + kc) * 64), dst, 16, 0, 0);
+      if (++issued == 48) {
+        __builtin_amdgcn_s_waitcnt(0x4F70);  // vmcnt(16)
+        issued = 16;
+      }
+    }
+  }
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+}
+
 // sum over a 256-thread block, identical result in every thread, fixed order
 __device__ __forceinline__ float block_sum256(float v, float* red4) {
   v = wave_sum(v);
@@ -127,10 +160,15 @@ template <typename T, typename OUT, int E, int SPL>
 __global__ __launch_bounds__(256) void ln_resid_kernel(float* __restrict__ x, int d, const float* __restrict__ part,
                                                        int S, size_t pstride, const T* __restrict__ bias,
                                                        const T* __restrict__ g, const T* __restrict__ b, float eps,
-                                                       OUT* __restrict__ a, int lda) {
+                                                       OUT* __restrict__ a, int lda, int N, Prefetch pf) {
   constexpr int PS = SPL > 0 ? SPL : 1;
   __shared__ float red[4];
+  __shared__ uint32_t pf_lds[kPrefetchLdsWords];
   const int n = blockIdx.x, tid = threadIdx.x;
+  if (n >= N) {
+    if (n >= pf.nmain) prefetch_weights(pf, n - pf.nmain, pf_lds);
+    return;
+  }
   float* xr = x + (size_t)n * d;
   const float* pr = part + (size_t)n * d;
   float v[E];
@@ -182,42 +220,56 @@ __global__ __launch_bounds__(256) void ln_resid_kernel(float* __restrict__ x, in
 
 template <typename T, int E, int SPL>
 static void ln_go(float* x, int N, int d, const float* part, int S, size_t pstride, const void* bias, const void* g,
-                  const void* b, float eps, void* a, int lda, hipStream_t s) {
-  ln_resid_kernel<T, T, E, SPL><<<N, 256, 0, s>>>(x, d, part, S, pstride, (const T*)bias, (const T*)g, (const T*)b,
-                                                  eps, (T*)a, lda);
+                  const void* b, float eps, void* a, int lda, const Prefetch& pf, hipStream_t s) {
+  const int grid = pf.nworkers ? pf.nmain + pf.nworkers : N;
+  ln_resid_kernel<T, T, E, SPL><<<grid, 256, 0, s>>>(x, d, part, S, pstride, (const T*)bias, (const T*)g,
+                                                     (const T*)b, eps, (T*)a, lda, N, pf);
 }
 
 template <typename T, int E>
 static void ln_go_s(float* x, int N, int d, const float* part, int S, size_t pstride, const void* bias,
-                    const void* g, const void* b, float eps, void* a, int lda, hipStream_t s) {
-  if (S == 0) ln_go<T, E, 0>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, s);
-  else if (S == 4) ln_go<T, E, 4>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, s);
-  else if (S == 8) ln_go<T, E, 8>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, s);
-  else ln_go<T, E, -1>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, s);
+                    const void* g, const void* b, float eps, void* a, int lda, const Prefetch& pf, hipStream_t s) {
+  if (S == 0) ln_go<T, E, 0>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, pf, s);
+  else if (S == 4) ln_go<T, E, 4>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, pf, s);
+  else if (S == 8) ln_go<T, E, 8>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, pf, s);
+  else ln_go<T, E, -1>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, pf, s);
 }
 
 template <typename T>
 static hipError_t ln_go_e(float* x, int N, int d, const float* part, int S, size_t pstride, const void* bias,
-                          const void* g, const void* b, float eps, void* a, int lda, hipStream_t s) {
+                          const void* g, const void* b, float eps, void* a, int lda, const Prefetch& pf,
+                          hipStream_t s) {
   switch ((d + 255) / 256) {
-    case 1: ln_go_s<T, 1>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, s); break;
-    case 2: ln_go_s<T, 2>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, s); break;
-    case 3: ln_go_s<T, 3>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, s); break;
-    case 4: ln_go_s<T, 4>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, s); break;
-    case 5: ln_go_s<T, 5>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, s); break;
-    case 6: ln_go_s<T, 6>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, s); break;
-    case 7: ln_go_s<T, 7>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, s); break;
-    case 8: ln_go_s<T, 8>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, s); break;
+    case 1: ln_go_s<T, 1>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, pf, s); break;
+    case 2: ln_go_s<T, 2>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, pf, s); break;
+    case 3: ln_go_s<T, 3>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, pf, s); break;
+    case 4: ln_go_s<T, 4>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, pf, s); break;
+    case 5: ln_go_s<T, 5>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, pf, s); break;
+    case 6: ln_go_s<T, 6>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, pf, s); break;
+    case 7: ln_go_s<T, 7>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, pf, s); break;
+    case 8: ln_go_s<T, 8>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, pf, s); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
+// blocks [0, nmain) of a launch with a prefetch: nmain = N rounded up to 8
+static Prefetch pf_after(Prefetch pf, int nmain) {
+  if (!pf.Wp || pf.nworkers <= 0 || pf.nworkers % 8) {
+    pf.nworkers = 0;
+    pf.nmain = 1 << 30;
+  } else {
+    pf.nmain = (nmain + 7) / 8 * 8;
+  }
+  return pf;
+}
+
 hipError_t launch_ln(int f32, float* x, int N, int d, const float* part, int S, size_t pstride, const void* bias,
-                     const void* g, const void* b, float eps, void* a, int lda, hipStream_t s) {
+                     const void* g, const void* b, float eps, void* a, int lda, const Prefetch& pf0, hipStream_t s) {
   if (S > 0 && !bias) return hipErrorInvalidValue;
-  if (f32) return ln_go_e<float>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, s);
-  return ln_go_e<uint16_t>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, s);
+  const Prefetch pf = pf_after(pf0, N);
+  if (f32) return ln_go_e<float>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, pf, s);
+  return ln_go_e<uint16_t>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, pf, s);
 }
 
 // ------------------------------------------------------------------ GEMM epilogues
@@ -326,13 +378,20 @@ hipError_t launch_pack_bf16(const uint16_t* W, int M, int K, void* out, hipStrea
 
 template <int NT, int RB, int KIND, bool VEC, int NV, int U>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) void gemm_kernel(
-    const u32x4* __restrict__ Wp, int KC, int RBtot, int kc_split, const uint16_t* __restrict__ act, Epi ep) {
+    const u32x4* __restrict__ Wp, int KC, int RBtot, int kc_split, const uint16_t* __restrict__ act, Epi ep,
+    Prefetch pf) {
   static_assert(!VEC || RB == 1, "vector path: one row block per workgroup");
   constexpr int NB = VEC ? NV : NT;  // activation fragments per k-step
   constexpr int NN = VEC ? NV : 16 * NT;     // output nodes
   __shared__ float red[4 * RB * NN * 16];
+  __shared__ uint32_t pf_lds[kPrefetchLdsWords];
+  if ((int)blockIdx.x >= pf.nmain) {
+    prefetch_weights(pf, blockIdx.x - pf.nmain, pf_lds);
+    return;
+  }
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
   const int rb0 = blockIdx.x * RB;
+  if (rb0 >= RBtot) return;  // padding block of a launch with a prefetch
   const int kc0 = blockIdx.y * kc_split;
   const int kc1 = min(KC, kc0 + kc_split);
   const int nsteps = kc1 - kc0 > w ? (kc1 - kc0 - w + 3) / 4 : 0;
@@ -467,62 +526,77 @@ int gemm_split_kc(int M, int K, int N, int vec, int want_split, int* splits) {
   return kcs;
 }
 
+// row blocks per workgroup of the LM head (EPI_LOGITS on the matrix cores):
+// it has thousands of row blocks, so more of them per workgroup make the
+// activations (read once per workgroup) cost less than the weights
+static int head_rb(int nt) { return nt <= 2 ? 8 : nt == 4 ? 4 : nt == 8 ? 2 : 1; }
+
+GemmGeom gemm_geom(int kind, int vec, int M, int K, int N, int kcs) {
+  GemmGeom g{};
+  g.KC = K / 32;
+  g.RBtot = (M + 15) / 16;
+  g.kcs = kcs;
+  if (vec) g.RB = 1;
+  else if (kind == EPI_LOGITS) g.RB = head_rb(gemm_cfg(N, 0).nt);
+  else g.RB = gemm_cfg(N, 0).rb;
+  g.gx = (g.RBtot + g.RB - 1) / g.RB;
+  g.gy = (g.KC + kcs - 1) / kcs;
+  return g;
+}
+
+template <int NT, int RB, int KIND, bool VEC, int NV, int U>
+static void gemm_launch(const GemmGeom& g, const void* Wp, const uint16_t* act, const Epi& ep, const Prefetch& pf,
+                        hipStream_t s) {
+  dim3 grid(pf.nworkers ? pf.nmain + pf.nworkers : g.gx, g.gy);
+  gemm_kernel<NT, RB, KIND, VEC, NV, U><<<grid, 256, 0, s>>>((const u32x4*)Wp, g.KC, g.RBtot, g.kcs, act, ep, pf);
+}
+
 template <int NT, int RB, bool VEC, int NV, int U>
-static void gemm_go(int kind, const void* Wp, int M, int K, int kcs, const uint16_t* act, const Epi& ep,
-                    hipStream_t s) {
-  const int KC = K / 32, RBtot = (M + 15) / 16;
-  dim3 grid((RBtot + RB - 1) / RB, (KC + kcs - 1) / kcs);
-  const u32x4* w = (const u32x4*)Wp;
+static void gemm_go(int kind, const GemmGeom& g, const void* Wp, const uint16_t* act, const Epi& ep,
+                    const Prefetch& pf, hipStream_t s) {
   switch (kind) {
-    case EPI_QKV: gemm_kernel<NT, RB, EPI_QKV, VEC, NV, U><<<grid, 256, 0, s>>>(w, KC, RBtot, kcs, act, ep); break;
-    case EPI_PARTIAL: gemm_kernel<NT, RB, EPI_PARTIAL, VEC, NV, U><<<grid, 256, 0, s>>>(w, KC, RBtot, kcs, act, ep); break;
-    case EPI_GELU: gemm_kernel<NT, RB, EPI_GELU, VEC, NV, U><<<grid, 256, 0, s>>>(w, KC, RBtot, kcs, act, ep); break;
+    case EPI_QKV: gemm_launch<NT, RB, EPI_QKV, VEC, NV, U>(g, Wp, act, ep, pf, s); break;
+    case EPI_PARTIAL: gemm_launch<NT, RB, EPI_PARTIAL, VEC, NV, U>(g, Wp, act, ep, pf, s); break;
+    case EPI_GELU: gemm_launch<NT, RB, EPI_GELU, VEC, NV, U>(g, Wp, act, ep, pf, s); break;
     default:
-      if constexpr (VEC) gemm_kernel<NT, RB, EPI_LOGITS, VEC, NV, U><<<grid, 256, 0, s>>>(w, KC, RBtot, kcs, act, ep);
+      if constexpr (VEC) gemm_launch<NT, RB, EPI_LOGITS, VEC, NV, U>(g, Wp, act, ep, pf, s);
       break;
   }
 }
 
-// The LM head has thousands of row blocks: more of them per workgroup so the
-// activations (read once per workgroup) cost less than the weights.
-template <int NT, int RB, int U>
-static void gemm_head_go(const void* Wp, int M, int K, int kcs, const uint16_t* act, const Epi& ep, hipStream_t s) {
-  const int KC = K / 32, RBtot = (M + 15) / 16;
-  dim3 grid((RBtot + RB - 1) / RB, (KC + kcs - 1) / kcs);
-  gemm_kernel<NT, RB, EPI_LOGITS, false, 0, U><<<grid, 256, 0, s>>>((const u32x4*)Wp, KC, RBtot, kcs, act, ep);
-}
-
 hipError_t launch_gemm_bf16(int kind, int vec, const void* Wp, int M, int K, const uint16_t* act, int kcs,
-                            const Epi& ep, hipStream_t s) {
+                            const Epi& ep, const Prefetch& pf0, hipStream_t s) {
   if (kcs <= 0) return hipErrorInvalidValue;
+  if (ep.N > (vec ? 16 : 256)) return hipErrorInvalidValue;
+  const GemmGeom g = gemm_geom(kind, vec, M, K, ep.N, kcs);
+  // a prefetch rides along only on a launch with one k-split (its blocks
+  // are then appended in x and the GEMM's own block ids stay bx)
+  const Prefetch pf = pf_after(g.gy == 1 ? pf0 : Prefetch{}, g.gx);
   if (kind == EPI_LOGITS && !vec) {
-    if (ep.N > 256) return hipErrorInvalidValue;
     switch (gemm_cfg(ep.N, 0).nt) {
-      case 1: gemm_head_go<1, 8, 3>(Wp, M, K, kcs, act, ep, s); break;
-      case 2: gemm_head_go<2, 8, 2>(Wp, M, K, kcs, act, ep, s); break;
-      case 4: gemm_head_go<4, 4, 2>(Wp, M, K, kcs, act, ep, s); break;
-      case 8: gemm_head_go<8, 2, 1>(Wp, M, K, kcs, act, ep, s); break;
-      default: gemm_head_go<16, 1, 1>(Wp, M, K, kcs, act, ep, s); break;
+      case 1: gemm_launch<1, 8, EPI_LOGITS, false, 0, 3>(g, Wp, act, ep, pf, s); break;
+      case 2: gemm_launch<2, 8, EPI_LOGITS, false, 0, 2>(g, Wp, act, ep, pf, s); break;
+      case 4: gemm_launch<4, 4, EPI_LOGITS, false, 0, 2>(g, Wp, act, ep, pf, s); break;
+      case 8: gemm_launch<8, 2, EPI_LOGITS, false, 0, 1>(g, Wp, act, ep, pf, s); break;
+      default: gemm_launch<16, 1, EPI_LOGITS, false, 0, 1>(g, Wp, act, ep, pf, s); break;
     }
     return hipGetLastError();
   }
   if (vec) {
-    if (ep.N > 16) return hipErrorInvalidValue;
     switch (gemm_cfg(ep.N, 1).nv) {
-      case 1: gemm_go<1, 1, true, 1, 8>(kind, Wp, M, K, kcs, act, ep, s); break;
-      case 2: gemm_go<1, 1, true, 2, 8>(kind, Wp, M, K, kcs, act, ep, s); break;
-      case 4: gemm_go<1, 1, true, 4, 6>(kind, Wp, M, K, kcs, act, ep, s); break;
-      case 8: gemm_go<1, 1, true, 8, 4>(kind, Wp, M, K, kcs, act, ep, s); break;
-      default: gemm_go<1, 1, true, 16, 2>(kind, Wp, M, K, kcs, act, ep, s); break;
+      case 1: gemm_go<1, 1, true, 1, 8>(kind, g, Wp, act, ep, pf, s); break;
+      case 2: gemm_go<1, 1, true, 2, 8>(kind, g, Wp, act, ep, pf, s); break;
+      case 4: gemm_go<1, 1, true, 4, 6>(kind, g, Wp, act, ep, pf, s); break;
+      case 8: gemm_go<1, 1, true, 8, 4>(kind, g, Wp, act, ep, pf, s); break;
+      default: gemm_go<1, 1, true, 16, 2>(kind, g, Wp, act, ep, pf, s); break;
     }
   } else {
-    if (ep.N > 256) return hipErrorInvalidValue;
     switch (gemm_cfg(ep.N, 0).nt) {
-      case 1: gemm_go<1, 2, false, 0, 6>(kind, Wp, M, K, kcs, act, ep, s); break;
-      case 2: gemm_go<2, 2, false, 0, 4>(kind, Wp, M, K, kcs, act, ep, s); break;
-      case 4: gemm_go<4, 2, false, 0, 3>(kind, Wp, M, K, kcs, act, ep, s); break;
-      case 8: gemm_go<8, 1, false, 0, 2>(kind, Wp, M, K, kcs, act, ep, s); break;
-      default: gemm_go<16, 1, false, 0, 1>(kind, Wp, M, K, kcs, act, ep, s); break;
+      case 1: gemm_go<1, 2, false, 0, 6>(kind, g, Wp, act, ep, pf, s); break;
+      case 2: gemm_go<2, 2, false, 0, 4>(kind, g, Wp, act, ep, pf, s); break;
+      case 4: gemm_go<4, 2, false, 0, 3>(kind, g, Wp, act, ep, pf, s); break;
+      case 8: gemm_go<8, 1, false, 0, 2>(kind, g, Wp, act, ep, pf, s); break;
+      default: gemm_go<16, 1, false, 0, 1>(kind, g, Wp, act, ep, pf, s); break;
     }
   }
   return hipGetLastError();
@@ -712,26 +786,28 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnArgs a) {
   if (lane < DH) st_act((T*)a.out, n, h * DH + lane, a.ldo, o / l);
 }
 
-// ---- bf16 models: one kernel on the matrix cores
+// ---- bf16 models: two kernels, the first on the matrix cores
 //
-// Workgroup (head h, node tile j of 16 nodes), 8 waves:
-//  prefix: wave w takes cache rows 64 c .. 64 c + 63 for chunks c = w, w + 8,
-//    ...  S^T = K Q^T and O^T = V^T P^T run on v_mfma_f32_16x16x32_bf16 (q and
-//    p split into bf16 hi + lo, K and V exact) 32 keys at a time with an online
-//    softmax.  K operand rows come straight from the cache, ordered so that
-//    lane l ends up holding the scores of keys 8(l/16)..+7 of node l%16, which
-//    is exactly its slot of the P^T operand; V rows are transposed through
-//    the wave's own LDS.
-//  root path: half-wave (w, 0/1) takes node 16 j + 2 w + (0/1): its ancestors
-//    and itself from the tree scratch on the vector ALU, root first.  Its index
-//    and row loads are issued before the prefix work so they overlap it.
-//  merge: the 8 prefix parts and the root-path part of every node are merged
-//    through LDS in that fixed order and written in the next GEMM's input
-//    layout.  The split of the prefix depends on P only, so a node's result
-//    does not depend on the rest of the tree.
+// attn_split_kernel, blocks [0, H * nsplit): (head h, prefix chunk c) of CL
+//   cache rows.  The chunk's K rows and V^T are staged in LDS once; wave w
+//   takes the 16-node tiles w, w + nw, ... of the tree against them.
+//   S^T = K Q^T and O^T = V^T P^T run on v_mfma_f32_16x16x32_bf16 (q and p
+//   split into bf16 hi + lo, K and V exact) 32 keys at a time with an online
+//   softmax.  The K operand's rows are ordered so that lane l ends up holding
+//   the scores of keys 8(l/16)..+7 of node l%16, which is exactly its slot of
+//   the P^T operand.
+// attn_split_kernel, blocks [H * nsplit, ...): the root paths.  Half-wave per
+//   (node, head): its ancestors and itself from the tree scratch on the vector
+//   ALU, root first, 32 keys per batch with the batch's V rows in LDS.
+// Each leaves a part (max, sum of exponentials, unnormalised output) per
+// (head, slot, node): slots 0 .. nsplit-1 the prefix chunks, slot nsplit the
+// root path.
+// attn_merge_kernel: per (node, head), the parts merged in slot order and
+// written in the next GEMM's input layout.  The chunking depends on P only,
+// so a node's result does not depend on the rest of the tree.
 
-constexpr int AT_WAVES = 8;
-constexpr int AT_KEYS = 64;
+constexpr int AT_STAGE = kAttnMaxChunk;  // cache rows staged per block
+constexpr int AT_MAXW = 8;               // waves per block
 
 __device__ __forceinline__ void pack_hilo8(const float (&v)[8], u32x4& hi, u32x4& lo) {
 #pragma unroll
@@ -747,119 +823,96 @@ __device__ __forceinline__ f32x4 mfma16(const u32x4& a, const u32x4& b, const f3
                                                   0, 0);
 }
 
-template <int DH>
-__global__ __launch_bounds__(64 * AT_WAVES) void attn_tile_kernel(AttnArgs a) {
-  constexpr int VS = AT_KEYS + 8;  // LDS row stride of V^T (elements)
-  constexpr int VT = DH * VS;      // V^T elements per wave
-  constexpr int PSTR = DH + 2;     // merge record: m, l, o[DH]
-  constexpr int NSLOT = AT_WAVES + 1;
-  constexpr int DPL = DH / 32;     // root-path output dims per lane of a half-wave
-  __shared__ __align__(16) uint16_t vt_lds[AT_WAVES * VT];
-  __shared__ float qrow[AT_WAVES][2][DH];
-  float* mrg = (float*)vt_lds;  // after the prefix work: [NSLOT][16][PSTR]
-  static_assert(NSLOT * 16 * PSTR * 4 <= AT_WAVES * VT * 2, "merge area");
-  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, i = lane & 15, g = lane >> 4;
-  const int h = blockIdx.x % a.H, tile = blockIdx.x / a.H, n0 = 16 * tile;
-
-  // root-path node of this half-wave: its first 32 path entries (fixed
-  // stride, no dependent index load), depth and query
-  const int hw = lane >> 5, hl = lane & 31;
-  const int rnc = min(n0 + 2 * w + hw, a.N - 1);
-  int rkey = a.path32[(size_t)rnc * kPath32 + hl];
-  const int rdep = a.depth[rnc];
-  float rq[DPL];
-  {
-    const float* qp = a.q + (size_t)rnc * a.d + h * DH + hl * DPL;
-#pragma unroll
-    for (int e = 0; e < DPL; ++e) rq[e] = qp[e];
-  }
-  // tile queries (B operand): node n0 + i, dims 32 kc + 8 g .. +8
-  const int qn = min(n0 + i, a.N - 1);
-  f32x4 qf[DH / 32][2];
-#pragma unroll
-  for (int kc2 = 0; kc2 < DH / 32; ++kc2) {
-    const float* qp = a.q + (size_t)qn * a.d + h * DH + 32 * kc2 + 8 * g;
-    qf[kc2][0] = *(const f32x4*)qp;
-    qf[kc2][1] = *(const f32x4*)(qp + 4);
-  }
-  const uint16_t* kc = (const uint16_t*)a.kc + (size_t)h * a.max_ctx * DH;
-  const uint16_t* vc = (const uint16_t*)a.vc + (size_t)h * a.max_ctx * DH;
-  uint16_t* vt = vt_lds + w * VT;
-  const int npass = (a.P + AT_WAVES * AT_KEYS - 1) / (AT_WAVES * AT_KEYS);
-
-  // first pass's rows, then the root-path rows (one round trip behind)
-  u32x4 kf[2][2][DH / 32], vr[DH / 8];
-  auto load_chunk = [&](int k0) {
-#pragma unroll
-    for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        const int key = min(k0 + 32 * sb + 8 * (i >> 2) + (i & 3) + 4 * t, a.P - 1);
-#pragma unroll
-        for (int kc2 = 0; kc2 < DH / 32; ++kc2) kf[sb][t][kc2] = *(const u32x4*)(kc + (size_t)key * DH + 32 * kc2 + 8 * g);
-      }
-    // V: the chunk's rows are contiguous; load j covers 1 KB (lane l: 16 bytes
-    // at (64 j + l) * 8 elements, i.e. row 8 j + l / (DH / 8) of the chunk)
-#pragma unroll
-    for (int j = 0; j < DH / 8; ++j) {
-      const int e0 = (64 * j + lane) * 8;
-      const int vk = min(k0 + e0 / DH, a.P - 1);
-      vr[j] = *(const u32x4*)(vc + (size_t)vk * DH + e0 % DH);
-    }
-  };
-  if (a.P > 0 && w * AT_KEYS < a.P) load_chunk(w * AT_KEYS);
-  const uint16_t* ktb = (const uint16_t*)a.kt + (size_t)h * a.max_nodes * DH;
-  const uint16_t* vtb = (const uint16_t*)a.vt + (size_t)h * a.max_nodes * DH;
-  u32x4 rk[DH / 8], rv[DH / 8];
-#pragma unroll
-  for (int j = 0; j < DH / 8; ++j) {
-    rk[j] = *(const u32x4*)(ktb + (size_t)rkey * DH + 8 * j);
-    rv[j] = *(const u32x4*)(vtb + (size_t)rkey * DH + 8 * j);
-  }
-#pragma unroll
-  for (int e = 0; e < DPL; ++e) qrow[w][hw][hl * DPL + e] = rq[e];
+__device__ __forceinline__ void wave_sync_lds() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-  u32x4 qh[DH / 32], ql[DH / 32];
+}
+
+template <int DH>
+__device__ __forceinline__ void attn_prefix_chunk(const AttnArgs& a, uint16_t* lds, int h, int c) {
+  constexpr int KS = DH + 8;        // LDS row stride of K (elements)
+  constexpr int VS = AT_STAGE + 8;  // LDS row stride of V^T (elements)
+  constexpr int REC = DH + 4;
+  constexpr int MAXU = AT_STAGE * DH / 8 / 64;  // 16-byte units per thread, one wave
+  uint16_t* ks = lds;
+  uint16_t* vts = lds + AT_STAGE * KS;
+  const int tid = threadIdx.x, nt = blockDim.x, nw = nt >> 6, w = tid >> 6, lane = tid & 63;
+  const int i = lane & 15, g = lane >> 4;
+  const int kbeg = c * a.CL, nk = min(a.CL, a.P - kbeg), nkr = (nk + 31) & ~31;
+  const uint16_t* kc = (const uint16_t*)a.kc + ((size_t)h * a.max_ctx + kbeg) * DH;
+  const uint16_t* vc = (const uint16_t*)a.vc + ((size_t)h * a.max_ctx + kbeg) * DH;
+  const int units = nkr * (DH / 8);
+  // the chunk's rows, all loads in flight at once (rows past the prefix
+  // re-read the last row and are zeroed below)
+  u32x4 kr[MAXU], vr[MAXU];
 #pragma unroll
-  for (int kc2 = 0; kc2 < DH / 32; ++kc2) {
-    const f32x4 f0 = qf[kc2][0], f1 = qf[kc2][1];
-    const float v[8] = {f0[0], f0[1], f0[2], f0[3], f1[0], f1[1], f1[2], f1[3]};
-    pack_hilo8(v, qh[kc2], ql[kc2]);
+  for (int j = 0; j < MAXU; ++j) {
+    const int e = tid + j * nt;
+    if (e < units) {
+      const int r = min(e / (DH / 8), nk - 1), c8 = e % (DH / 8);
+      kr[j] = *(const u32x4*)(kc + (size_t)r * DH + 8 * c8);
+      vr[j] = *(const u32x4*)(vc + (size_t)r * DH + 8 * c8);
+    }
   }
-  float m = -INFINITY, l = 0.f;
-  f32x4 o[DH / 16];
+  // queries of the wave's first tile (B operand: node 16 t + i, dims 32 kc2 + 8 g .. +8)
+  const int ntiles = (a.N + 15) >> 4;
+  f32x4 qf[DH / 32][2];
+  auto load_q = [&](int t) {
+    const int qn = min(16 * t + i, a.N - 1);
 #pragma unroll
-  for (int t = 0; t < DH / 16; ++t) o[t] = (f32x4){0, 0, 0, 0};
-  // one chunk of nk (> 0) cache rows whose K fragments and V rows are in kf, vr
-  auto do_chunk = [&](int nk) {
-    // V rows -> this wave's V^T (rows past the prefix as zeros)
+    for (int kc2 = 0; kc2 < DH / 32; ++kc2) {
+      const float* qp = a.q + (size_t)qn * a.d + h * DH + 32 * kc2 + 8 * g;
+      qf[kc2][0] = *(const f32x4*)qp;
+      qf[kc2][1] = *(const f32x4*)(qp + 4);
+    }
+  };
+  if (w < ntiles) load_q(w);
 #pragma unroll
-    for (int j = 0; j < DH / 8; ++j) {
-      const int e0 = (64 * j + lane) * 8, key = e0 / DH, d0 = e0 % DH;
+  for (int j = 0; j < MAXU; ++j) {
+    const int e = tid + j * nt;
+    if (e < units) {
+      const int r = e / (DH / 8), c8 = e % (DH / 8);
+      const bool ok = r < nk;
+      const u32x4 kk = ok ? kr[j] : (u32x4){0, 0, 0, 0};
+      const u32x4 vv = ok ? vr[j] : (u32x4){0, 0, 0, 0};
+      *(u32x4*)(ks + r * KS + 8 * c8) = kk;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const uint32_t u = key < nk ? vr[j][e] : 0u;
-        vt[(d0 + 2 * e) * VS + key] = (uint16_t)(u & 0xffffu);
-        vt[(d0 + 2 * e + 1) * VS + key] = (uint16_t)(u >> 16);
+      for (int e2 = 0; e2 < 4; ++e2) {
+        vts[(8 * c8 + 2 * e2) * VS + r] = (uint16_t)(vv[e2] & 0xffffu);
+        vts[(8 * c8 + 2 * e2 + 1) * VS + r] = (uint16_t)(vv[e2] >> 16);
       }
     }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
+  __syncthreads();
+  const int ns = a.nsplit + 1;
+  for (int t = w; t < ntiles; t += nw) {
+    if (t != w) load_q(t);
+    u32x4 qh[DH / 32], ql[DH / 32];
 #pragma unroll
-    for (int sb = 0; sb < 2; ++sb) {
-      if (32 * sb >= nk) break;
+    for (int kc2 = 0; kc2 < DH / 32; ++kc2) {
+      const f32x4 f0 = qf[kc2][0], f1 = qf[kc2][1];
+      const float v[8] = {f0[0], f0[1], f0[2], f0[3], f1[0], f1[1], f1[2], f1[3]};
+      pack_hilo8(v, qh[kc2], ql[kc2]);
+    }
+    float m = -INFINITY, l = 0.f;
+    f32x4 o[DH / 16];
+#pragma unroll
+    for (int tt = 0; tt < DH / 16; ++tt) o[tt] = (f32x4){0, 0, 0, 0};
+    for (int sb = 0; sb < nkr / 32; ++sb) {
+      // K operand rows: key 32 sb + 8 (i / 4) + i % 4 (+ 4 for s1)
+      const uint16_t* kb = ks + (32 * sb + 8 * (i >> 2) + (i & 3)) * KS + 8 * g;
       f32x4 s0 = (f32x4){0, 0, 0, 0}, s1 = (f32x4){0, 0, 0, 0};
 #pragma unroll
       for (int kc2 = 0; kc2 < DH / 32; ++kc2) {
-        s0 = mfma16(kf[sb][0][kc2], qh[kc2], s0);
-        s0 = mfma16(kf[sb][0][kc2], ql[kc2], s0);
-        s1 = mfma16(kf[sb][1][kc2], qh[kc2], s1);
-        s1 = mfma16(kf[sb][1][kc2], ql[kc2], s1);
+        const u32x4 k0 = *(const u32x4*)(kb + 32 * kc2);
+        const u32x4 k1 = *(const u32x4*)(kb + 4 * KS + 32 * kc2);
+        s0 = mfma16(k0, qh[kc2], s0);
+        s0 = mfma16(k0, ql[kc2], s0);
+        s1 = mfma16(k1, qh[kc2], s1);
+        s1 = mfma16(k1, ql[kc2], s1);
       }
-      // lane: node n0 + i, keys 32 sb + 8 g + e of the chunk (e < 4 from s0, e >= 4 from s1)
+      // lane: node 16 t + i, keys 32 sb + 8 g + e (e < 4 from s0, e >= 4 from s1)
       float sv[8];
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
@@ -887,35 +940,49 @@ __global__ __launch_bounds__(64 * AT_WAVES) void attn_tile_kernel(AttnArgs a) {
       u32x4 ph, pl;
       pack_hilo8(pv, ph, pl);
 #pragma unroll
-      for (int t = 0; t < DH / 16; ++t) {
-        const u32x4 va = *(const u32x4*)(vt + (16 * t + i) * VS + 32 * sb + 8 * g);
-        o[t] = o[t] * alpha;
-        o[t] = mfma16(va, ph, o[t]);
-        o[t] = mfma16(va, pl, o[t]);
+      for (int tt = 0; tt < DH / 16; ++tt) {
+        const u32x4 va = *(const u32x4*)(vts + (16 * tt + i) * VS + 32 * sb + 8 * g);
+        o[tt] = o[tt] * alpha;
+        o[tt] = mfma16(va, ph, o[tt]);
+        o[tt] = mfma16(va, pl, o[tt]);
       }
     }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-  };
-  // pass 0 in straight-line code (its loads were issued first), later passes
-  // (P > 512) in a loop
-  {
-    const int nk0 = min(AT_KEYS, a.P - w * AT_KEYS);
-    if (nk0 > 0) do_chunk(nk0);
+    // part of node 16 t + i: lane (i, g) holds dims 16 tt + 4 g + r
+    const int n = 16 * t + i;
+    if (n < a.N) {
+      float* rec = a.part + (((size_t)h * ns + c) * a.N + n) * REC;
+      if (g == 0) *(f32x4*)rec = (f32x4){m, l, 0.f, 0.f};
+#pragma unroll
+      for (int tt = 0; tt < DH / 16; ++tt) *(f32x4*)(rec + 4 + 16 * tt + 4 * g) = o[tt];
+    }
   }
-  for (int pass = 1; pass < npass; ++pass) {
-    const int k0 = (pass * AT_WAVES + w) * AT_KEYS;
-    const int nk = min(AT_KEYS, a.P - k0);
-    if (nk <= 0) break;
-    load_chunk(k0);
-    do_chunk(nk);
-  }
+}
 
-  // root path on the vector ALU: 32 keys per batch per half-wave, lane hl =
-  // key; the batch's V rows go through the wave's (now free) LDS
-  uint16_t* rvl = vt + hw * 32 * DH;  // [32 keys][DH] of this half-wave
-  static_assert(2 * 32 * DH <= VT, "root-path rows fit the wave's LDS");
+template <int DH>
+__device__ __forceinline__ void attn_root_path(const AttnArgs& a, uint16_t* lds, float (*qrow)[2][DH], int h, int grp) {
+  constexpr int DPL = DH / 32;  // output dims per lane of a half-wave
+  constexpr int REC = DH + 4;
+  const int tid = threadIdx.x, nw = blockDim.x >> 6, w = tid >> 6, lane = tid & 63;
+  const int hw = lane >> 5, hl = lane & 31;
+  const int n = grp * 2 * nw + 2 * w + hw;  // this half-wave's node
+  const int rnc = min(n, a.N - 1);
+  // first 32 path entries at a fixed stride: no dependent index load
+  int rkey = a.path32[(size_t)rnc * kPath32 + hl];
+  const int rdep = a.depth[rnc];
+  {
+    const float* qp = a.q + (size_t)rnc * a.d + h * DH + hl * DPL;
+#pragma unroll
+    for (int e = 0; e < DPL; ++e) qrow[w][hw][hl * DPL + e] = qp[e];
+  }
+  const uint16_t* ktb = (const uint16_t*)a.kt + (size_t)h * a.max_nodes * DH;
+  const uint16_t* vtb = (const uint16_t*)a.vt + (size_t)h * a.max_nodes * DH;
+  u32x4 rk[DH / 8], rv[DH / 8];
+#pragma unroll
+  for (int j = 0; j < DH / 8; ++j) {
+    rk[j] = *(const u32x4*)(ktb + (size_t)rkey * DH + 8 * j);
+    rv[j] = *(const u32x4*)(vtb + (size_t)rkey * DH + 8 * j);
+  }
+  uint16_t* rvl = lds + (2 * w + hw) * 32 * DH;  // [32 keys][DH] of this half-wave
   float rm = -INFINITY, rl = 0.f, ro[DPL];
 #pragma unroll
   for (int e = 0; e < DPL; ++e) ro[e] = 0.f;
@@ -932,6 +999,7 @@ __global__ __launch_bounds__(64 * AT_WAVES) void attn_tile_kernel(AttnArgs a) {
     }
 #pragma unroll
     for (int jj = 0; jj < DH / 8; ++jj) *(u32x4*)(rvl + hl * DH + 8 * jj) = rv[jj];
+    wave_sync_lds();  // qrow (first batch) and this batch's V rows
     float dot = 0.f;
 #pragma unroll
     for (int c8 = 0; c8 < DH / 8; ++c8) {
@@ -960,9 +1028,6 @@ __global__ __launch_bounds__(64 * AT_WAVES) void attn_tile_kernel(AttnArgs a) {
     for (int off = 1; off < 32; off <<= 1) ps += __shfl_xor(ps, off);
     rl = fmaf(rl, alpha, ps);
     rm = mn;
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     // lane hl covers dims DPL hl .. +DPL; keys of the batch in order
     const int cnt = min(32, rdep + 1 - 32 * bt);
     const int cmax = max(cnt, __shfl_xor(cnt, 32));  // wave-uniform
@@ -977,57 +1042,80 @@ __global__ __launch_bounds__(64 * AT_WAVES) void attn_tile_kernel(AttnArgs a) {
     }
 #pragma unroll
     for (int e = 0; e < DPL; ++e) ro[e] = fmaf(ro[e], alpha, acc[e]);
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    wave_sync_lds();  // the batch's V rows are read before the next batch overwrites them
   }
-
-  // merge through LDS: slots 0..7 the prefix waves, slot 8 the root paths
-  __syncthreads();  // every wave is done with its V^T
-  {
-    float* rec = mrg + ((size_t)w * 16 + i) * PSTR;
-    if (g == 0) {
-      rec[0] = m;
-      rec[1] = l;
-    }
+  if (n < a.N) {
+    float* rec = a.part + (((size_t)h * (a.nsplit + 1) + a.nsplit) * a.N + n) * REC;
+    if (hl == 0) *(f32x4*)rec = (f32x4){rm, rl, 0.f, 0.f};
 #pragma unroll
-    for (int t = 0; t < DH / 16; ++t)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) rec[2 + 16 * t + 4 * g + r] = o[t][r];
-    float* rr = mrg + ((size_t)AT_WAVES * 16 + 2 * w + hw) * PSTR;
-    if (hl == 0) {
-      rr[0] = rm;
-      rr[1] = rl;
-    }
-#pragma unroll
-    for (int e = 0; e < DPL; ++e) rr[2 + DPL * hl + e] = ro[e];
-  }
-  __syncthreads();
-  for (int idx = tid; idx < 16 * DH; idx += 64 * AT_WAVES) {
-    const int node = idx / DH, dd = idx - node * DH;
-    if (n0 + node >= a.N) continue;
-    float M = -INFINITY;
-#pragma unroll
-    for (int c = 0; c < NSLOT; ++c) M = fmaxf(M, mrg[((size_t)c * 16 + node) * PSTR]);
-    float L = 0.f, O = 0.f;
-#pragma unroll
-    for (int c = 0; c < NSLOT; ++c) {
-      const float* rc = mrg + ((size_t)c * 16 + node) * PSTR;
-      const float wgt = __expf(rc[0] - M);
-      L = fmaf(rc[1], wgt, L);
-      O = fmaf(rc[2 + dd], wgt, O);
-    }
-    st_act((uint16_t*)a.out, n0 + node, h * DH + dd, a.ldo, O / L);
+    for (int e = 0; e < DPL; ++e) rec[4 + DPL * hl + e] = ro[e];
   }
 }
 
-hipError_t launch_attn(int f32, int DH, const AttnArgs& a, hipStream_t s) {
+template <int DH>
+__global__ __launch_bounds__(64 * AT_MAXW) void attn_split_kernel(AttnArgs a) {
+  constexpr int PFX = AT_STAGE * (DH + 8) + DH * (AT_STAGE + 8);  // K rows + V^T
+  constexpr int ROOT = AT_MAXW * 2 * 32 * DH;                     // 32 V rows per half-wave
+  __shared__ __align__(16) uint16_t lds[PFX > ROOT ? PFX : ROOT];
+  __shared__ __align__(16) float qrow[AT_MAXW][2][DH];
+  const int npre = a.H * a.nsplit;
+  if ((int)blockIdx.x < npre) attn_prefix_chunk<DH>(a, lds, blockIdx.x % a.H, blockIdx.x / a.H);
+  else attn_root_path<DH>(a, lds, qrow, (blockIdx.x - npre) % a.H, (blockIdx.x - npre) / a.H);
+}
+
+template <int DH>
+__global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a, Prefetch pf) {
+  constexpr int REC = DH + 4, PER = 256 / DH, B = 16;
+  __shared__ uint32_t pf_lds[kPrefetchLdsWords];
+  if ((int)blockIdx.x >= pf.nmain) {
+    prefetch_weights(pf, blockIdx.x - pf.nmain, pf_lds);
+    return;
+  }
+  const int pair = blockIdx.x * PER + threadIdx.x / DH, dd = threadIdx.x % DH;
+  if (pair >= a.N * a.H) return;
+  const int n = pair / a.H, h = pair - n * a.H, ns = a.nsplit + 1;
+  const size_t cs = (size_t)a.N * REC;
+  const float* rec = a.part + ((size_t)h * ns * a.N + n) * REC;
+  float M = -INFINITY, L = 0.f, O = 0.f;
+  for (int c0 = 0; c0 < ns; c0 += B) {
+    f32x2_t ml[B];
+    float ov[B];
+#pragma unroll
+    for (int j = 0; j < B; ++j) {
+      const int cc = min(c0 + j, ns - 1);
+      ml[j] = *(const f32x2_t*)(rec + cc * cs);
+      ov[j] = rec[cc * cs + 4 + dd];
+    }
+#pragma unroll
+    for (int j = 0; j < B; ++j) {
+      if (c0 + j >= ns) break;
+      const float mn = fmaxf(M, ml[j][0]);
+      const float al = __expf(M - mn), wj = __expf(ml[j][0] - mn);
+      L = fmaf(L, al, ml[j][1] * wj);
+      O = fmaf(O, al, ov[j] * wj);
+      M = mn;
+    }
+  }
+  st_act((uint16_t*)a.out, n, h * DH + dd, a.ldo, O / L);
+}
+
+hipError_t launch_attn(int f32, int DH, const AttnArgs& a, const Prefetch& pf0, hipStream_t s) {
   if (!f32) {
-    if (a.N <= 0) return hipErrorInvalidValue;
-    const int blocks = a.H * ((a.N + 15) / 16);
-    if (DH == 64) attn_tile_kernel<64><<<blocks, 64 * AT_WAVES, 0, s>>>(a);
-    else if (DH == 32) attn_tile_kernel<32><<<blocks, 64 * AT_WAVES, 0, s>>>(a);
-    else return hipErrorInvalidValue;
+    if (a.N <= 0 || a.N > a.max_nodes || (DH != 64 && DH != 32)) return hipErrorInvalidValue;
+    if (a.P > 0 && (a.CL <= 0 || a.CL > AT_STAGE || a.CL % 32 || a.nsplit != (a.P + a.CL - 1) / a.CL))
+      return hipErrorInvalidValue;
+    const int nw = min(AT_MAXW, (a.N + 15) / 16);
+    const int blocks = a.H * a.nsplit + a.H * ((a.N + 2 * nw - 1) / (2 * nw));
+    const int mblocks = (a.N * a.H * DH + 255) / 256;
+    const Prefetch pf = pf_after(pf0, mblocks);
+    const int mgrid = pf.nworkers ? pf.nmain + pf.nworkers : mblocks;
+    if (DH == 64) {
+      attn_split_kernel<64><<<blocks, 64 * nw, 0, s>>>(a);
+      attn_merge_kernel<64><<<mgrid, 256, 0, s>>>(a, pf);
+    } else {
+      attn_split_kernel<32><<<blocks, 64 * nw, 0, s>>>(a);
+      attn_merge_kernel<32><<<mgrid, 256, 0, s>>>(a, pf);
+    }
     return hipGetLastError();
   }
   if (a.S > 0) {

@@ -23,6 +23,7 @@ namespace {
 
 thread_local std::string g_last_error;
 int g_gemm_path = 0;  // 0 auto, 1 vector ALU, 2 matrix cores
+int g_prefetch = 1;   // warm each weight GEMM's L2 from the kernel before it
 
 // Node counts up to this use the vector-ALU GEMM on the automatic path.
 constexpr int kVecMaxNodes = 4;
@@ -70,8 +71,6 @@ struct ssd_kv {
   void* act_f = nullptr;  // GELU outputs [npad][d_mlp]
   float* part = nullptr;  // split-K partial sums [kMaxSplits][max_nodes][d]
   float* apart = nullptr;  // attention partials (see AttnArgs::part)
-  unsigned* acnt = nullptr;  // attention tile counters [H][acnt_ld]
-  int acnt_ld = 0;
   int* d_tree = nullptr;  // the staged tree (see stage_bytes)
   int* d_accept_tree = nullptr;  // tokens[N] parents[N] depth[N] for accept
   int* d_argmax = nullptr;
@@ -111,6 +110,12 @@ extern "C" const char* ssd_last_error(void) { return g_last_error.c_str(); }
 extern "C" ssd_status ssd_set_gemm_path(int32_t path) {
   if (path < 0 || path > 2) return fail(SSD_E_INVALID_ARG, "gemm path must be 0, 1 or 2");
   g_gemm_path = path;
+  return SSD_OK;
+}
+
+extern "C" ssd_status ssd_set_weight_prefetch(int32_t on) {
+  if (on != 0 && on != 1) return fail(SSD_E_INVALID_ARG, "weight prefetch must be 0 or 1");
+  g_prefetch = on;
   return SSD_OK;
 }
 
@@ -318,12 +323,10 @@ extern "C" ssd_status ssd_kv_create(const ssd_model* m, int32_t max_ctx, int32_t
   const size_t o_f = take(planes * kv->npad * M * es);
   const size_t o_part = take((size_t)kMaxSplits * max_nodes * d * 4);  // split-K partials
   // attention partials: fp32 models (H, 64-row tiles, node, DH + 2); bf16
-  // models (H, prefix chunks + root path, node, DH + 4) and tile counters
+  // models (H, prefix chunks + root path, node, DH + 4)
   const size_t ap_f32 = (size_t)c.n_head * ((max_ctx + 63) / 64) * max_nodes * (m->dh + 2);
   const size_t ap_bf16 = (size_t)c.n_head * (attn_max_nsplit(max_ctx) + 1) * max_nodes * (m->dh + 4);
   const size_t o_apart = take((m->f32 ? ap_f32 : ap_bf16) * 4);
-  const int cnt_ld = (max_nodes + 15) / 16;
-  const size_t o_acnt = take((size_t)c.n_head * cnt_ld * 4);
   const size_t o_tree = take(stage_bytes(max_nodes));
   const size_t o_at = take((size_t)3 * max_nodes * 4), o_am = take((size_t)max_nodes * 4);
   const size_t o_amw = take(std::max(argmax_work_bytes(max_nodes, V), topk_work_bytes(max_nodes, V)));
@@ -344,8 +347,6 @@ extern "C" ssd_status ssd_kv_create(const ssd_model* m, int32_t max_ctx, int32_t
   kv->act_f = b + o_f;
   kv->part = (float*)(b + o_part);
   kv->apart = (float*)(b + o_apart);
-  kv->acnt = (unsigned*)(b + o_acnt);
-  kv->acnt_ld = cnt_ld;
   kv->d_tree = (int*)(b + o_tree);
   kv->d_accept_tree = (int*)(b + o_at);
   kv->d_argmax = (int*)(b + o_am);
@@ -442,21 +443,47 @@ static size_t fill_stage(char* host, int P, const int32_t* tokens, const int32_t
 // One weight GEMM of the pass over n nodes: fp32 models use the plain
 // kernel; bf16 models the vector-ALU kernel for few nodes (or when pinned)
 // and the matrix-core kernel otherwise, in node groups of 16 / 256.
-static hipError_t run_gemm(const ssd_model* m, int n, int kind, const void* Wraw, const void* Wp, int rows, int K,
-                           const void* act, const Epi& ep, hipStream_t s) {
-  if (m->f32) return launch_gemm_f32(kind, (const float*)Wraw, rows, K, (const float*)act, K, ep, s);
-  const int vec = (g_gemm_path == 0 ? (n <= kVecMaxNodes ? 1 : 2) : g_gemm_path) == 1;
-  const int group = vec ? 16 : 256;
-  // one k-split for every node group, so all nodes leave the same partials
+static int gemm_vec(int n) { return (g_gemm_path == 0 ? (n <= kVecMaxNodes ? 1 : 2) : g_gemm_path) == 1; }
+
+// k-steps per split of a weight GEMM over n nodes (one k-split for every
+// node group, so all nodes leave the same partials)
+static int gemm_kcs(int n, int kind, int rows, int K) {
+  const int vec = gemm_vec(n);
   int S = 1;
-  const int kcs = gemm_split_kc(rows, K, std::min(n, group), vec, kind == EPI_PARTIAL, &S);
+  return gemm_split_kc(rows, K, std::min(n, vec ? 16 : 256), vec, kind == EPI_PARTIAL, &S);
+}
+
+// The weight fragments the first launch of run_gemm(m, n, kind, Wp, rows, K)
+// reads, for the kernel enqueued just before it to warm (bf16 models).
+static Prefetch next_gemm(const ssd_model* m, int n, int kind, const void* Wp, int rows, int K) {
+  Prefetch pf{};
+  if (m->f32 || !g_prefetch || !Wp) return pf;
+  const int vec = gemm_vec(n);
+  const GemmGeom g = gemm_geom(kind, vec, rows, K, std::min(n, vec ? 16 : 256), gemm_kcs(n, kind, rows, K));
+  pf.Wp = Wp;
+  pf.KC = g.KC;
+  pf.RBtot = g.RBtot;
+  pf.RB = g.RB;
+  pf.kcs = g.kcs;
+  pf.gx = g.gx;
+  pf.nblk = g.gx * g.gy;
+  pf.nworkers = std::min((pf.nblk + 7) / 8 * 8, 256);
+  return pf;
+}
+
+static hipError_t run_gemm(const ssd_model* m, int n, int kind, const void* Wraw, const void* Wp, int rows, int K,
+                           const void* act, const Epi& ep, hipStream_t s, const Prefetch& pf = Prefetch{}) {
+  if (m->f32) return launch_gemm_f32(kind, (const float*)Wraw, rows, K, (const float*)act, K, ep, s);
+  const int vec = gemm_vec(n);
+  const int group = vec ? 16 : 256;
+  const int kcs = gemm_kcs(n, kind, rows, K);
   for (int n0 = 0; n0 < n; n0 += group) {
     Epi e2 = ep;
     e2.node0 = n0;
     e2.N = std::min(group, n - n0);
     // fragment tiles of 16 nodes, each K/32 fragments of 512 elements
     const uint16_t* a = (const uint16_t*)act + (size_t)(n0 / 16) * (K / 32) * 512;
-    hipError_t r = launch_gemm_bf16(kind, vec, Wp, rows, K, a, kcs, e2, s);
+    hipError_t r = launch_gemm_bf16(kind, vec, Wp, rows, K, a, kcs, e2, n0 == 0 ? pf : Prefetch{}, s);
     if (r != hipSuccess) return r;
   }
   return hipSuccess;
@@ -465,7 +492,7 @@ static hipError_t run_gemm(const ssd_model* m, int n, int kind, const void* Wraw
 // number of split-K partials a residual GEMM leaves for the next LayerNorm
 static int resid_splits(const ssd_model* m, int n, int rows, int K) {
   if (m->f32) return 0;
-  const int vec = (g_gemm_path == 0 ? (n <= kVecMaxNodes ? 1 : 2) : g_gemm_path) == 1;
+  const int vec = gemm_vec(n);
   int S = 1;
   gemm_split_kc(rows, K, std::min(n, vec ? 16 : 256), vec, 1, &S);
   return S;
@@ -500,7 +527,7 @@ static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int3
   const void* pend_bias = nullptr;
   for (int l = 0; l < L; ++l) {
     HIP_TRY(launch_ln(f32, kv->x, n, d, kv->part, pend_S, pstride, pend_bias, m->ln1_g[l], m->ln1_b[l], c.ln_eps,
-                      kv->act_a, ld_d, s));
+                      kv->act_a, ld_d, next_gemm(m, n, EPI_QKV, f32 ? nullptr : m->p_qkv[l], 3 * d, d), s));
     Epi e{};
     e.bias = m->b_qkv[l];
     e.N = n;
@@ -535,11 +562,9 @@ static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int3
     a.max_ctx = kv->max_ctx;
     a.max_nodes = maxn;
     a.scale = 1.0f / std::sqrt((float)DH);
-    a.cnt = kv->acnt;
-    a.cnt_ld = kv->acnt_ld;
     a.CL = attn_chunk(P);
     a.nsplit = attn_nsplit(P);
-    HIP_TRY(launch_attn(f32, DH, a, s));
+    HIP_TRY(launch_attn(f32, DH, a, next_gemm(m, n, kind_res, f32 ? nullptr : m->p_o[l], d, d), s));
 
     Epi eo{};
     eo.bias = f32 ? m->b_o[l] : nullptr;
@@ -552,7 +577,7 @@ static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int3
     HIP_TRY(run_gemm(m, n, kind_res, m->w_o[l], f32 ? nullptr : m->p_o[l], d, d, kv->act_o, eo, s));
 
     HIP_TRY(launch_ln(f32, kv->x, n, d, kv->part, f32 ? 0 : s_o, pstride, m->b_o[l], m->ln2_g[l], m->ln2_b[l],
-                      c.ln_eps, kv->act_a, ld_d, s));
+                      c.ln_eps, kv->act_a, ld_d, next_gemm(m, n, EPI_GELU, f32 ? nullptr : m->p_fc[l], M, d), s));
     Epi ef{};
     ef.bias = m->b_fc[l];
     ef.N = n;
@@ -560,7 +585,8 @@ static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int3
     ef.d = d;
     ef.out = kv->act_f;
     ef.ldo = ld_m;
-    HIP_TRY(run_gemm(m, n, EPI_GELU, m->w_fc[l], f32 ? nullptr : m->p_fc[l], M, d, kv->act_a, ef, s));
+    HIP_TRY(run_gemm(m, n, EPI_GELU, m->w_fc[l], f32 ? nullptr : m->p_fc[l], M, d, kv->act_a, ef, s,
+                     next_gemm(m, n, kind_res, f32 ? nullptr : m->p_pr[l], d, M)));
 
     Epi ep{};
     ep.bias = f32 ? m->b_pr[l] : nullptr;
@@ -575,7 +601,7 @@ static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int3
     pend_bias = m->b_pr[l];
   }
   HIP_TRY(launch_ln(f32, kv->x, n, d, kv->part, pend_S, pstride, pend_bias, m->lnf_g, m->lnf_b, c.ln_eps, kv->act_a,
-                    ld_d, s));
+                    ld_d, Prefetch{}, s));
   Epi eh{};
   eh.bias = nullptr;
   eh.N = n;

@@ -52,6 +52,27 @@ struct GemmCfg {
   int nt, rb, ck, nv;
 };
 
+// launch geometry of one bf16 GEMM: block (bx, by) owns weight row blocks
+// bx RB .. bx RB + RB - 1 (rows past RBtot read row block RBtot - 1 and are
+// never stored) and k-steps by kcs .. by kcs + kcs - 1 (clamped to KC)
+struct GemmGeom {
+  int RB, kcs, gx, gy, KC, RBtot;
+};
+
+// Weight prefetch into the L2 of the XCD that will read it.  Block b of a
+// launch runs on XCD (b + c) mod 8, with the same c for every launch of a
+// queue (whatever the grid), so block B of one launch and block L of the
+// next share an L2 when B = L (mod 8).  A launch carrying a Prefetch runs its
+// own work in blocks [0, nmain) and, in blocks nmain + w (w < nworkers, both
+// multiples of 8), loads the weight fragments of the next GEMM's blocks
+// L = w (mod 8) into LDS that nothing reads: the bytes stay in that L2.
+struct Prefetch {
+  const void* Wp;  // packed weights of the next GEMM (nullptr: no prefetch)
+  int KC, RBtot, RB, kcs, gx, nblk;  // its geometry; its block L = bx + gx by, L < nblk
+  int nmain;       // set by the launcher
+  int nworkers;
+};
+
 struct AttnArgs {
   const float* q;       // [N][d]
   const void* kc;       // cache, this layer: [H][max_ctx][DH]
@@ -65,26 +86,25 @@ struct AttnArgs {
   void* out;            // attention output in the GEMM-input layout
   int ldo;              // GEMM-input leading dimension (fp32: d, bf16: d / 32)
   float* part;          // fp32 models: prefix partials [H][S][N][DH + 2] (max, sum of exp, output);
-                        // bf16 models: partials [H][nsplit + 1][N][DH + 4] (max, sum, -, -, output),
-                        // slot nsplit holding the root-path part
+                        // bf16 models: parts [H][nsplit + 1][N][DH + 4] (max, sum, -, -, output),
+                        // slots 0 .. nsplit-1 the prefix chunks, slot nsplit the root path
   int S;                // fp32 models: prefix tiles of 64 cache rows
   int N, P, d, H, max_ctx, max_nodes;
   float scale;
   // bf16 models
-  unsigned* cnt;        // arrival counters [H][cnt_ld], zero between launches
-  int cnt_ld;           // counters per head (>= node tiles of 16)
-  int CL;               // cache rows per prefix chunk (multiple of 32, <= kAttnMaxChunk)
-  int nsplit;           // prefix chunks (ceil(P / CL))
+  int CL;               // cache rows per prefix chunk (attn_chunk(P))
+  int nsplit;           // prefix chunks (attn_nsplit(P))
 };
 
-// bf16 attention: cache rows per prefix chunk (about P / 8, so that the parts
-// of a node fit one round trip of the merge), a function of the prefix length
-// only, so that a node's result does not depend on the tree
+// bf16 attention: cache rows per prefix chunk, a multiple of 32 between 64
+// and kAttnMaxChunk: 64 up to P = 1024, then about P / 16 (at most 16 chunks
+// up to P = 2048).  A function of the prefix length only, so that a node's
+// result does not depend on the tree.
 constexpr int kAttnMaxChunk = 128;
 inline int attn_chunk(int P) {
-  int c = (P + 7) / 8;
+  int c = (P + 15) / 16;
   c = (c + 31) / 32 * 32;
-  if (c < 32) c = 32;
+  if (c < 64) c = 64;
   if (c > kAttnMaxChunk) c = kAttnMaxChunk;
   return c;
 }
@@ -102,18 +122,20 @@ hipError_t launch_embed(int f32, const void* wte, const void* wpe, const int* to
 // x += bias + part[0..S-1] (if S > 0), then LayerNorm into the GEMM-input
 // buffer a (lda: fp32 row stride, or bf16 k-steps d / 32; see st_act)
 hipError_t launch_ln(int f32, float* x, int N, int d, const float* part, int S, size_t pstride, const void* bias,
-                     const void* g, const void* b, float eps, void* a, int lda, hipStream_t s);
+                     const void* g, const void* b, float eps, void* a, int lda, const Prefetch& pf, hipStream_t s);
 hipError_t launch_gemm_f32(int kind, const float* W, int M, int K, const float* act, int lda, const Epi& ep,
                            hipStream_t s);
 GemmCfg gemm_cfg(int N, int vec);
 // k-steps per split and number of splits (EPI_PARTIAL only; 1 otherwise)
 int gemm_split_kc(int M, int K, int N, int vec, int want_split, int* splits);
-// Wp: weights packed in 16x32 bf16 fragments (see pack); act: activations of
-// this launch's first node in fragment order (see st_act); kcs k-steps per
-// split (grid.y = ceil(K/32 / kcs))
+GemmGeom gemm_geom(int kind, int vec, int M, int K, int N, int kcs);
+// Wp: weights packed in 16x32 float16 fragments (see pack); act: activations
+// of this launch's first node in fragment order (see st_act); kcs k-steps per
+// split (grid.y = ceil(K/32 / kcs)); pf: weights of the next GEMM to warm
+// (only honoured when grid.y = 1)
 hipError_t launch_gemm_bf16(int kind, int vec, const void* Wp, int M, int K, const uint16_t* act, int kcs,
-                            const Epi& ep, hipStream_t s);
-hipError_t launch_attn(int f32, int DH, const AttnArgs& a, hipStream_t s);
+                            const Epi& ep, const Prefetch& pf, hipStream_t s);
+hipError_t launch_attn(int f32, int DH, const AttnArgs& a, const Prefetch& pf, hipStream_t s);
 hipError_t launch_pack_bf16(const uint16_t* W, int M, int K, void* out, hipStream_t s);
 size_t packed_bytes(int M, int K);
 // greedy argmax per node; work: argmax_work_bytes(N, V) bytes of device scratch

@@ -28,7 +28,7 @@ LAYER_TENSORS = ("ln1_g", "ln1_b", "w_qkv", "b_qkv", "w_o", "b_o",
 EXPORTS = ("ssd_model_create", "ssd_model_destroy", "ssd_kv_bytes", "ssd_kv_create", "ssd_kv_destroy",
            "ssd_tree_verify", "ssd_tree_accept", "ssd_kv_commit", "ssd_kv_error_count",
            "ssd_graph_capture_verify", "ssd_graph_launch", "ssd_graph_destroy", "ssd_validate_tree",
-           "ssd_tree_prep", "ssd_set_gemm_path", "ssd_status_string", "ssd_last_error", "ssd_launch_gemm",
+           "ssd_tree_prep", "ssd_set_gemm_path", "ssd_set_weight_prefetch", "ssd_status_string", "ssd_last_error", "ssd_launch_gemm",
            "ssd_model_prefix_view", "ssd_topk")
 
 
@@ -65,6 +65,9 @@ def lib():
     if _lib is None:
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build()")
+        # torch first: libssd then binds to the HIP runtime torch has loaded
+        # instead of bringing up a second one that sees no device
+        import torch  # noqa: F401
         L = C.CDLL(LIB_PATH)
         i32p, vp = C.POINTER(C.c_int32), C.c_void_p
         sig = {
@@ -84,6 +87,7 @@ def lib():
             "ssd_validate_tree": [i32p, i32p, C.c_int32, C.c_int32, i32p],
             "ssd_tree_prep": [i32p, C.c_int32, i32p, C.POINTER(C.c_uint64)],
             "ssd_set_gemm_path": [C.c_int32],
+            "ssd_set_weight_prefetch": [C.c_int32],
             "ssd_launch_gemm": [vp, vp, C.c_int32, C.c_int32, C.c_int32, vp],
             "ssd_model_prefix_view": [vp, C.c_int32, C.POINTER(vp)],
             "ssd_topk": [vp, vp, C.c_int32, C.c_int32, vp, vp, vp, vp],
@@ -137,6 +141,10 @@ def tree_prep(parent_idx) -> Tuple[np.ndarray, np.ndarray]:
 
 def set_gemm_path(path: int):
     _check(lib().ssd_set_gemm_path(path), "ssd_set_gemm_path")
+
+
+def set_weight_prefetch(on: bool):
+    _check(lib().ssd_set_weight_prefetch(1 if on else 0), "ssd_set_weight_prefetch")
 
 
 def kv_bytes(cfg, max_ctx: int, max_nodes: int) -> Tuple[int, int]:

@@ -137,3 +137,27 @@ def test_c5_sampled_path_and_sampling_accept(big, torch):
         path, plen, nxt = s.accept(toks, par, dlg, mode=ssd.SAMPLE_WOR, draft_probs=dq, seed=seed)
         op, on = oracle.tree_accept(oracle.SAMPLE_WOR, toks, par, got, q, 1.0, seed)
         assert path[:int(plen.item())].cpu().numpy().tolist() == op.tolist() and int(nxt.item()) == on
+
+
+@pytest.mark.parametrize("n", [3, 32, 100])
+def test_weight_prefetch_is_bitwise_neutral(big, torch, n):
+    """The L2 warm-up of each weight GEMM (loads into LDS nothing reads) must
+    not change a single bit of the logits, eagerly and in the captured graph,
+    on the vector-ALU (3 nodes) and matrix-core (32, 100) GEMM shapes."""
+    cfg, w, om, m, ssd = big
+    P = 512
+    s, kc, vc = _session(big, torch, P, 1024, 128, seed=5)
+    par = W.branching_tree([4, 2, 2, 1], n)
+    toks = W.tree_tokens(par, cfg.vocab, seed=6)
+    try:
+        ssd.set_weight_prefetch(False)
+        off_eager = s.verify(P, toks, par).cpu()
+        off_graph = _graph_logits(s, torch, P, toks, par)
+        ssd.set_weight_prefetch(True)
+        on_eager = s.verify(P, toks, par).cpu()
+        on_graph = _graph_logits(s, torch, P, toks, par)
+    finally:
+        ssd.set_weight_prefetch(True)
+    assert torch.equal(off_eager, on_eager)
+    assert np.array_equal(off_graph, on_graph)
+    assert np.array_equal(off_graph, on_eager.numpy())

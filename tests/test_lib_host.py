@@ -70,3 +70,9 @@ def test_gemm_path_switch_validates():
     with pytest.raises(ssd.SSDError):
         ssd.set_gemm_path(7)
     ssd.set_gemm_path(ssd.GEMM_AUTO)
+
+
+def test_weight_prefetch_switch_validates():
+    assert ssd.lib().ssd_set_weight_prefetch(2) != 0
+    ssd.set_weight_prefetch(False)
+    ssd.set_weight_prefetch(True)
