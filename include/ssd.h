@@ -216,12 +216,16 @@ ssd_status ssd_tree_prep(const int32_t *parent_idx, int32_t n, int32_t *depth, u
  * ALU, 2 = matrix cores.  Process-wide; bfloat16 models only. */
 ssd_status ssd_set_gemm_path(int32_t path);
 
-/* Weight prefetch across kernel boundaries: 1 (default) = the kernel
- * enqueued before each weight GEMM of the pass (LayerNorm, attention merge,
- * MLP up-projection) also loads that GEMM's weight fragments into the L2 of
- * the XCD whose workgroups will read them; 0 = off.  Results are bitwise the
- * same either way; process-wide; bfloat16 models only.  Errors:
- * SSD_E_INVALID_ARG (not 0 or 1). */
+/* Weight prefetch beside each pass: 1 (default) = every bfloat16 pass that
+ * ssd_tree_verify enqueues, or that ssd_graph_launch replays, gets a
+ * prefetcher kernel on a stream of the session's own; it follows progress
+ * signals the pass's kernels raise and loads each weight GEMM's fragments
+ * into the L2 of the XCD whose workgroups will read them, a few kernels
+ * ahead.  The pass never waits for it; it stops waiting for signals 50 ms
+ * after it starts.  0 = off.  Results are bitwise the same either way; process-wide.
+ * ssd_kv_destroy waits for the session's prefetchers; the model must outlive
+ * its sessions' pending passes as always.  Errors: SSD_E_INVALID_ARG (not 0
+ * or 1). */
 ssd_status ssd_set_weight_prefetch(int32_t on);
 
 const char *ssd_status_string(ssd_status s);

@@ -77,37 +77,18 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
-// ------------------------------------------------------------------ weight prefetch
-//
-// Worker w of a launch (its block nmain + w) loads the weight fragments of
-// the next GEMM's blocks L = w (mod 8), the j-th of them for j = w / 8 (mod
-// nworkers / 8), exactly the fragments that block will read, with direct-to-LDS
-// 16-byte loads into a 1 KB area per wave that nothing reads: no registers,
-// up to 48 loads in flight per wave.
-constexpr int kPrefetchLdsWords = 4 * 256;  // 1 KB per wave, 4 waves
+// ------------------------------------------------------------------ pass signals
 
-__device__ __forceinline__ void prefetch_weights(const Prefetch& pf, int worker, uint32_t* lds) {
-  const int tid = threadIdx.x, nw = min((int)(blockDim.x >> 6), 4), w = tid >> 6, lane = tid & 63;
-  if (w >= nw) return;
-  const int r = worker & 7, step = pf.nworkers >> 3;
-  const u32x4* W = (const u32x4*)pf.Wp + lane;
-  __attribute__((address_space(3))) void* dst = (__attribute__((address_space(3))) void*)(lds + w * 256);
-  int issued = 0;
-  for (int j = worker >> 3;; j += step) {
-    const int L = r + 8 * j;
-    if (L >= pf.nblk) break;
-    const int bx = L % pf.gx, by = L / pf.gx;
-    const int kc0 = by * pf.kcs, nk = min(pf.KC, kc0 + pf.kcs) - kc0;
-    for (int f = w; f < pf.RB * nk; f += nw) {
-      const int row = min(bx * pf.RB + f / nk, pf.RBtot - 1), kc = kc0 + f % nk;
-      __builtin_amdgcn_global_load_lds((const void*)(W + ((size_t)row * pf.KC + kc) * 64), dst, 16, 0, 0);
-      if (++issued == 48) {
-        __builtin_amdgcn_s_waitcnt(0x4F70);  // vmcnt(16)
-        issued = 16;
-      }
-    }
-  }
-  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+__device__ __forceinline__ unsigned xcc_id() {
+  unsigned x;
+  asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(x));
+  return x & 15;
+}
+
+// one relaxed device-scope increment by thread 0 of block (0, 0)
+__device__ __forceinline__ void pass_signal(unsigned long long* sig) {
+  if (sig && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0)
+    __hip_atomic_fetch_add(sig, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // sum over a 256-thread block, identical result in every thread, fixed order
@@ -130,18 +111,26 @@ __device__ __forceinline__ float gelu_tanh(float x) {
 template <typename T>
 __global__ __launch_bounds__(256) void embed_kernel(const T* __restrict__ wte, const T* __restrict__ wpe,
                                                     const int* __restrict__ tokens, const int* __restrict__ pos,
-                                                    int d, float* __restrict__ x) {
+                                                    int d, float* __restrict__ x, unsigned long long* sig,
+                                                    unsigned* xcc0) {
+  if (sig && blockIdx.x == 0 && threadIdx.x == 0) {
+    // the XCD of block 0, stored before the first signal of the pass is released
+    __hip_atomic_store(xcc0, xcc_id(), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_fetch_add(sig, 1ull, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+  }
   const int n = blockIdx.x;
   const size_t t = (size_t)tokens[n] * d, p = (size_t)pos[n] * d;
   for (int k = threadIdx.x; k < d; k += blockDim.x) x[(size_t)n * d + k] = ldT(wte, t + k) + ldT(wpe, p + k);
 }
 
 hipError_t launch_embed(int f32, const void* wte, const void* wpe, const int* tokens, const int* pos, int N, int d,
-                        float* x, hipStream_t s) {
+                        float* x, unsigned long long* sig, unsigned* xcc0, hipStream_t s) {
+  if (sig && !xcc0) return hipErrorInvalidValue;
   if (f32)
-    embed_kernel<float><<<N, 256, 0, s>>>((const float*)wte, (const float*)wpe, tokens, pos, d, x);
+    embed_kernel<float><<<N, 256, 0, s>>>((const float*)wte, (const float*)wpe, tokens, pos, d, x, sig, xcc0);
   else
-    embed_kernel<uint16_t><<<N, 256, 0, s>>>((const uint16_t*)wte, (const uint16_t*)wpe, tokens, pos, d, x);
+    embed_kernel<uint16_t><<<N, 256, 0, s>>>((const uint16_t*)wte, (const uint16_t*)wpe, tokens, pos, d, x, sig,
+                                             xcc0);
   return hipGetLastError();
 }
 
@@ -160,15 +149,11 @@ template <typename T, typename OUT, int E, int SPL>
 __global__ __launch_bounds__(256) void ln_resid_kernel(float* __restrict__ x, int d, const float* __restrict__ part,
                                                        int S, size_t pstride, const T* __restrict__ bias,
                                                        const T* __restrict__ g, const T* __restrict__ b, float eps,
-                                                       OUT* __restrict__ a, int lda, int N, Prefetch pf) {
+                                                       OUT* __restrict__ a, int lda, unsigned long long* sig) {
   constexpr int PS = SPL > 0 ? SPL : 1;
   __shared__ float red[4];
-  __shared__ uint32_t pf_lds[kPrefetchLdsWords];
+  pass_signal(sig);
   const int n = blockIdx.x, tid = threadIdx.x;
-  if (n >= N) {
-    if (n >= pf.nmain) prefetch_weights(pf, n - pf.nmain, pf_lds);
-    return;
-  }
   float* xr = x + (size_t)n * d;
   const float* pr = part + (size_t)n * d;
   float v[E];
@@ -220,56 +205,45 @@ __global__ __launch_bounds__(256) void ln_resid_kernel(float* __restrict__ x, in
 
 template <typename T, int E, int SPL>
 static void ln_go(float* x, int N, int d, const float* part, int S, size_t pstride, const void* bias, const void* g,
-                  const void* b, float eps, void* a, int lda, const Prefetch& pf, hipStream_t s) {
-  const int grid = pf.nworkers ? pf.nmain + pf.nworkers : N;
-  ln_resid_kernel<T, T, E, SPL><<<grid, 256, 0, s>>>(x, d, part, S, pstride, (const T*)bias, (const T*)g,
-                                                     (const T*)b, eps, (T*)a, lda, N, pf);
+                  const void* b, float eps, void* a, int lda, unsigned long long* sig, hipStream_t s) {
+  ln_resid_kernel<T, T, E, SPL><<<N, 256, 0, s>>>(x, d, part, S, pstride, (const T*)bias, (const T*)g, (const T*)b,
+                                                  eps, (T*)a, lda, sig);
 }
 
 template <typename T, int E>
 static void ln_go_s(float* x, int N, int d, const float* part, int S, size_t pstride, const void* bias,
-                    const void* g, const void* b, float eps, void* a, int lda, const Prefetch& pf, hipStream_t s) {
-  if (S == 0) ln_go<T, E, 0>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, pf, s);
-  else if (S == 4) ln_go<T, E, 4>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, pf, s);
-  else if (S == 8) ln_go<T, E, 8>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, pf, s);
-  else ln_go<T, E, -1>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, pf, s);
+                    const void* g, const void* b, float eps, void* a, int lda, unsigned long long* sig,
+                    hipStream_t s) {
+  if (S == 0) ln_go<T, E, 0>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, s);
+  else if (S == 4) ln_go<T, E, 4>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, s);
+  else if (S == 8) ln_go<T, E, 8>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, s);
+  else ln_go<T, E, -1>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, s);
 }
 
 template <typename T>
 static hipError_t ln_go_e(float* x, int N, int d, const float* part, int S, size_t pstride, const void* bias,
-                          const void* g, const void* b, float eps, void* a, int lda, const Prefetch& pf,
+                          const void* g, const void* b, float eps, void* a, int lda, unsigned long long* sig,
                           hipStream_t s) {
   switch ((d + 255) / 256) {
-    case 1: ln_go_s<T, 1>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, pf, s); break;
-    case 2: ln_go_s<T, 2>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, pf, s); break;
-    case 3: ln_go_s<T, 3>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, pf, s); break;
-    case 4: ln_go_s<T, 4>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, pf, s); break;
-    case 5: ln_go_s<T, 5>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, pf, s); break;
-    case 6: ln_go_s<T, 6>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, pf, s); break;
-    case 7: ln_go_s<T, 7>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, pf, s); break;
-    case 8: ln_go_s<T, 8>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, pf, s); break;
+    case 1: ln_go_s<T, 1>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, s); break;
+    case 2: ln_go_s<T, 2>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, s); break;
+    case 3: ln_go_s<T, 3>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, s); break;
+    case 4: ln_go_s<T, 4>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, s); break;
+    case 5: ln_go_s<T, 5>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, s); break;
+    case 6: ln_go_s<T, 6>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, s); break;
+    case 7: ln_go_s<T, 7>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, s); break;
+    case 8: ln_go_s<T, 8>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, s); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
-// blocks [0, nmain) of a launch with a prefetch: nmain = N rounded up to 8
-static Prefetch pf_after(Prefetch pf, int nmain) {
-  if (!pf.Wp || pf.nworkers <= 0 || pf.nworkers % 8) {
-    pf.nworkers = 0;
-    pf.nmain = 1 << 30;
-  } else {
-    pf.nmain = (nmain + 7) / 8 * 8;
-  }
-  return pf;
-}
-
 hipError_t launch_ln(int f32, float* x, int N, int d, const float* part, int S, size_t pstride, const void* bias,
-                     const void* g, const void* b, float eps, void* a, int lda, const Prefetch& pf0, hipStream_t s) {
+                     const void* g, const void* b, float eps, void* a, int lda, unsigned long long* sig,
+                     hipStream_t s) {
   if (S > 0 && !bias) return hipErrorInvalidValue;
-  const Prefetch pf = pf_after(pf0, N);
-  if (f32) return ln_go_e<float>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, pf, s);
-  return ln_go_e<uint16_t>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, pf, s);
+  if (f32) return ln_go_e<float>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, s);
+  return ln_go_e<uint16_t>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, s);
 }
 
 // ------------------------------------------------------------------ GEMM epilogues
@@ -376,25 +350,19 @@ hipError_t launch_pack_bf16(const uint16_t* W, int M, int K, void* out, hipStrea
 //    accumulators per node; the 4 lanes of a row are summed (xor 16, xor 32).
 // Occupancy is traded for registers (1-2 waves per SIMD).
 
-template <int NT, int RB, int KIND, bool VEC, int NV, int U>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) void gemm_kernel(
-    const u32x4* __restrict__ Wp, int KC, int RBtot, int kc_split, const uint16_t* __restrict__ act, Epi ep,
-    Prefetch pf) {
+template <int NT, int RB, int KIND, bool VEC, int NV, int U, int NW = 4>
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(NW / 4, NW / 2))) void gemm_kernel(
+    const u32x4* __restrict__ Wp, int KC, int RBtot, int kc_split, const uint16_t* __restrict__ act, Epi ep) {
   static_assert(!VEC || RB == 1, "vector path: one row block per workgroup");
   constexpr int NB = VEC ? NV : NT;  // activation fragments per k-step
   constexpr int NN = VEC ? NV : 16 * NT;     // output nodes
-  __shared__ float red[4 * RB * NN * 16];
-  __shared__ uint32_t pf_lds[kPrefetchLdsWords];
-  if ((int)blockIdx.x >= pf.nmain) {
-    prefetch_weights(pf, blockIdx.x - pf.nmain, pf_lds);
-    return;
-  }
+  __shared__ float red[NW * RB * NN * 16];
+  pass_signal(ep.sig);
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
   const int rb0 = blockIdx.x * RB;
-  if (rb0 >= RBtot) return;  // padding block of a launch with a prefetch
   const int kc0 = blockIdx.y * kc_split;
   const int kc1 = min(KC, kc0 + kc_split);
-  const int nsteps = kc1 - kc0 > w ? (kc1 - kc0 - w + 3) / 4 : 0;
+  const int nsteps = kc1 - kc0 > w ? (kc1 - kc0 - w + NW - 1) / NW : 0;
   // weight rows past the matrix (last workgroup) read row block rb0 instead
   // and are never stored
   const u32x4* wb[RB];
@@ -408,7 +376,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) voi
   u32x4 bq[U][NB];
   const int klast = kc1 - 1;
   auto load_step = [&](int s, int u) {
-    const int kc = min(kc0 + w + 4 * s, klast);
+    const int kc = min(kc0 + w + NW * s, klast);
 #pragma unroll
     for (int r = 0; r < RB; ++r) wq[u][r] = wb[r][(size_t)kc * 64];
 #pragma unroll
@@ -483,20 +451,27 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) voi
   __syncthreads();
   Epi e2 = ep;
   e2.split = blockIdx.y;
-  for (int idx = tid; idx < RB * NN * 16; idx += 256) {
+  for (int idx = tid; idx < RB * NN * 16; idx += 64 * NW) {
     const int row = idx & 15, node = (idx >> 4) % NN, r = idx / (16 * NN);
     const size_t st = (size_t)RB * NN * 16;
     const size_t base = ((size_t)r * NN + node) * 16 + row;
-    const float s = ((red[base] + red[st + base]) + red[2 * st + base]) + red[3 * st + base];
+    float s = red[base];
+#pragma unroll
+    for (int ww = 1; ww < NW; ++ww) s += red[ww * st + base];
     const int o = (rb0 + r) * 16 + row;
     if (rb0 + r < RBtot && o < ep.M && node < ep.N) epilogue<uint16_t, KIND>(e2, node, o, s);
   }
 }
 
-GemmCfg gemm_cfg(int N, int vec) {
+// Tile shape per node count and GEMM kind (measured on the GPT-2-L shapes:
+// K = 1280 for QKV / MLP up / attention out, 5120 for MLP down).  At 17-32
+// nodes: QKV one row block per workgroup (240 workgroups), the others two;
+// 8 waves, with 1-5 k-steps of loads in flight.
+GemmCfg gemm_cfg(int N, int vec, int kind) {
   GemmCfg c{};
   c.rb = 1;
   c.ck = 1;
+  c.nw = 4;
   if (vec) {
     int nv = 1;
     while (nv < N) nv *= 2;
@@ -509,6 +484,10 @@ GemmCfg gemm_cfg(int N, int vec) {
   c.nt = nt;
   c.nv = 0;
   c.rb = nt <= 4 ? 2 : 1;
+  if (nt == 2) {
+    c.nw = 8;
+    c.rb = kind == EPI_QKV ? 1 : 2;
+  }
   return c;
 }
 
@@ -518,7 +497,8 @@ int gemm_split_kc(int M, int K, int N, int vec, int want_split, int* splits) {
     *splits = 1;
     return KC;
   }
-  const int gx = ((M + 15) / 16 + gemm_cfg(N, vec).rb - 1) / gemm_cfg(N, vec).rb;
+  const int rb = gemm_cfg(N, vec, EPI_PARTIAL).rb;
+  const int gx = ((M + 15) / 16 + rb - 1) / rb;
   int S = 1;  // a power of two with S * gx >= 256 workgroups
   while (S * gx < 256 && S < kMaxSplits) S *= 2;
   const int kcs = (KC + S - 1) / S;
@@ -537,68 +517,161 @@ GemmGeom gemm_geom(int kind, int vec, int M, int K, int N, int kcs) {
   g.RBtot = (M + 15) / 16;
   g.kcs = kcs;
   if (vec) g.RB = 1;
-  else if (kind == EPI_LOGITS) g.RB = head_rb(gemm_cfg(N, 0).nt);
-  else g.RB = gemm_cfg(N, 0).rb;
+  else if (kind == EPI_LOGITS) g.RB = head_rb(gemm_cfg(N, 0, kind).nt);
+  else g.RB = gemm_cfg(N, 0, kind).rb;
   g.gx = (g.RBtot + g.RB - 1) / g.RB;
   g.gy = (g.KC + kcs - 1) / kcs;
   return g;
 }
 
-template <int NT, int RB, int KIND, bool VEC, int NV, int U>
-static void gemm_launch(const GemmGeom& g, const void* Wp, const uint16_t* act, const Epi& ep, const Prefetch& pf,
-                        hipStream_t s) {
-  dim3 grid(pf.nworkers ? pf.nmain + pf.nworkers : g.gx, g.gy);
-  gemm_kernel<NT, RB, KIND, VEC, NV, U><<<grid, 256, 0, s>>>((const u32x4*)Wp, g.KC, g.RBtot, g.kcs, act, ep, pf);
+template <int NT, int RB, int KIND, bool VEC, int NV, int U, int NW = 4>
+static void gemm_launch(const GemmGeom& g, const void* Wp, const uint16_t* act, const Epi& ep, hipStream_t s) {
+  gemm_kernel<NT, RB, KIND, VEC, NV, U, NW>
+      <<<dim3(g.gx, g.gy), 64 * NW, 0, s>>>((const u32x4*)Wp, g.KC, g.RBtot, g.kcs, act, ep);
 }
 
 template <int NT, int RB, bool VEC, int NV, int U>
 static void gemm_go(int kind, const GemmGeom& g, const void* Wp, const uint16_t* act, const Epi& ep,
-                    const Prefetch& pf, hipStream_t s) {
+                    hipStream_t s) {
   switch (kind) {
-    case EPI_QKV: gemm_launch<NT, RB, EPI_QKV, VEC, NV, U>(g, Wp, act, ep, pf, s); break;
-    case EPI_PARTIAL: gemm_launch<NT, RB, EPI_PARTIAL, VEC, NV, U>(g, Wp, act, ep, pf, s); break;
-    case EPI_GELU: gemm_launch<NT, RB, EPI_GELU, VEC, NV, U>(g, Wp, act, ep, pf, s); break;
+    case EPI_QKV: gemm_launch<NT, RB, EPI_QKV, VEC, NV, U>(g, Wp, act, ep, s); break;
+    case EPI_PARTIAL: gemm_launch<NT, RB, EPI_PARTIAL, VEC, NV, U>(g, Wp, act, ep, s); break;
+    case EPI_GELU: gemm_launch<NT, RB, EPI_GELU, VEC, NV, U>(g, Wp, act, ep, s); break;
     default:
-      if constexpr (VEC) gemm_launch<NT, RB, EPI_LOGITS, VEC, NV, U>(g, Wp, act, ep, pf, s);
+      if constexpr (VEC) gemm_launch<NT, RB, EPI_LOGITS, VEC, NV, U>(g, Wp, act, ep, s);
       break;
   }
 }
 
 hipError_t launch_gemm_bf16(int kind, int vec, const void* Wp, int M, int K, const uint16_t* act, int kcs,
-                            const Epi& ep, const Prefetch& pf0, hipStream_t s) {
+                            const Epi& ep, hipStream_t s) {
   if (kcs <= 0) return hipErrorInvalidValue;
   if (ep.N > (vec ? 16 : 256)) return hipErrorInvalidValue;
   const GemmGeom g = gemm_geom(kind, vec, M, K, ep.N, kcs);
-  // a prefetch rides along only on a launch with one k-split (its blocks
-  // are then appended in x and the GEMM's own block ids stay bx)
-  const Prefetch pf = pf_after(g.gy == 1 ? pf0 : Prefetch{}, g.gx);
   if (kind == EPI_LOGITS && !vec) {
-    switch (gemm_cfg(ep.N, 0).nt) {
-      case 1: gemm_launch<1, 8, EPI_LOGITS, false, 0, 3>(g, Wp, act, ep, pf, s); break;
-      case 2: gemm_launch<2, 8, EPI_LOGITS, false, 0, 2>(g, Wp, act, ep, pf, s); break;
-      case 4: gemm_launch<4, 4, EPI_LOGITS, false, 0, 2>(g, Wp, act, ep, pf, s); break;
-      case 8: gemm_launch<8, 2, EPI_LOGITS, false, 0, 1>(g, Wp, act, ep, pf, s); break;
-      default: gemm_launch<16, 1, EPI_LOGITS, false, 0, 1>(g, Wp, act, ep, pf, s); break;
+    switch (gemm_cfg(ep.N, 0, kind).nt) {
+      case 1: gemm_launch<1, 8, EPI_LOGITS, false, 0, 3>(g, Wp, act, ep, s); break;
+      case 2: gemm_launch<2, 8, EPI_LOGITS, false, 0, 2>(g, Wp, act, ep, s); break;
+      case 4: gemm_launch<4, 4, EPI_LOGITS, false, 0, 2>(g, Wp, act, ep, s); break;
+      case 8: gemm_launch<8, 2, EPI_LOGITS, false, 0, 1>(g, Wp, act, ep, s); break;
+      default: gemm_launch<16, 1, EPI_LOGITS, false, 0, 1>(g, Wp, act, ep, s); break;
     }
     return hipGetLastError();
   }
   if (vec) {
-    switch (gemm_cfg(ep.N, 1).nv) {
-      case 1: gemm_go<1, 1, true, 1, 8>(kind, g, Wp, act, ep, pf, s); break;
-      case 2: gemm_go<1, 1, true, 2, 8>(kind, g, Wp, act, ep, pf, s); break;
-      case 4: gemm_go<1, 1, true, 4, 6>(kind, g, Wp, act, ep, pf, s); break;
-      case 8: gemm_go<1, 1, true, 8, 4>(kind, g, Wp, act, ep, pf, s); break;
-      default: gemm_go<1, 1, true, 16, 2>(kind, g, Wp, act, ep, pf, s); break;
+    switch (gemm_cfg(ep.N, 1, kind).nv) {
+      case 1: gemm_go<1, 1, true, 1, 8>(kind, g, Wp, act, ep, s); break;
+      case 2: gemm_go<1, 1, true, 2, 8>(kind, g, Wp, act, ep, s); break;
+      case 4: gemm_go<1, 1, true, 4, 6>(kind, g, Wp, act, ep, s); break;
+      case 8: gemm_go<1, 1, true, 8, 4>(kind, g, Wp, act, ep, s); break;
+      default: gemm_go<1, 1, true, 16, 2>(kind, g, Wp, act, ep, s); break;
     }
   } else {
-    switch (gemm_cfg(ep.N, 0).nt) {
-      case 1: gemm_go<1, 2, false, 0, 6>(kind, g, Wp, act, ep, pf, s); break;
-      case 2: gemm_go<2, 2, false, 0, 4>(kind, g, Wp, act, ep, pf, s); break;
-      case 4: gemm_go<4, 2, false, 0, 3>(kind, g, Wp, act, ep, pf, s); break;
-      case 8: gemm_go<8, 1, false, 0, 2>(kind, g, Wp, act, ep, pf, s); break;
-      default: gemm_go<16, 1, false, 0, 1>(kind, g, Wp, act, ep, pf, s); break;
+    switch (gemm_cfg(ep.N, 0, kind).nt) {
+      case 1: gemm_go<1, 2, false, 0, 6>(kind, g, Wp, act, ep, s); break;
+      case 2:  // must match gemm_cfg
+        if (kind == EPI_QKV) gemm_launch<2, 1, EPI_QKV, false, 0, 5, 8>(g, Wp, act, ep, s);
+        else if (kind == EPI_GELU) gemm_launch<2, 2, EPI_GELU, false, 0, 3, 8>(g, Wp, act, ep, s);
+        else gemm_launch<2, 2, EPI_PARTIAL, false, 0, 1, 8>(g, Wp, act, ep, s);
+        break;
+      case 4: gemm_go<4, 2, false, 0, 3>(kind, g, Wp, act, ep, s); break;
+      case 8: gemm_go<8, 1, false, 0, 2>(kind, g, Wp, act, ep, s); break;
+      default: gemm_go<16, 1, false, 0, 1>(kind, g, Wp, act, ep, s); break;
     }
   }
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ weight prefetcher
+//
+// Runs on its own stream beside one pass (see PrefetchPlan).  Targets in
+// order, per layer l: the QKV weights once MLP down of layer l - 1 (for
+// l = 0: the embedding) has started, attention-out once the attention split
+// has, MLP up once the attention merge has, MLP down once LN2 has; a target
+// whose GEMM has itself started is skipped.  Block b (4 waves) on XCD x has
+// rank b / 8 among the 32 blocks of its XCD and takes the GEMM blocks
+// L = r + 8 j (r = (x - c) mod 8, c the XCD of the pass's block 0) with
+// j = rank, rank + 32, ...; within one, wave w of nw loads k-steps w, w + nw, ... of
+// each of its row blocks, kPfDepth fragments in flight, into registers folded
+// into one value (stored only if it equals `magic`, so the loads are kept).
+// The shallow depth paces the stream: the kernels running beside it are
+// bound by memory latency, which a deeper burst raises by more than the warm
+// weights save.  Thread 0 polls the signal counter with s_sleep between
+// reads; every wait ends by the plan's timeout, after which the prefetcher
+// stops.
+
+constexpr int kPfBlocks = 256;
+constexpr int kPfDepth = 4;
+
+__global__ __launch_bounds__(256) void prefetcher_kernel(PrefetchPlan pp) {
+  __shared__ int go;  // 1 prefetch, 0 skip, -1 stop
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, nwv = blockDim.x >> 6;
+  const int rank = blockIdx.x >> 3, nrank = gridDim.x >> 3;
+  const unsigned x = xcc_id();
+  const unsigned long long t0 = __builtin_amdgcn_s_memrealtime();
+  unsigned acc = 0;
+  for (int l = 0; l < pp.L; ++l) {
+    for (int k = 0; k < 4; ++k) {
+      const int target = k == 0 ? SIG_QKV : k == 1 ? SIG_OUT : k == 2 ? SIG_FC : SIG_PROJ;
+      const int trig_k = k == 1 ? SIG_SPLIT : k == 2 ? SIG_MERGE : SIG_LN2;
+      const unsigned long long trig =
+          pp.base + (k == 0 ? (l == 0 ? 1 : sig_index(l - 1, SIG_PROJ)) : sig_index(l, trig_k));
+      const unsigned long long late = pp.base + sig_index(l, target);
+      if (tid == 0) {
+        int v = -1;
+        for (;;) {
+          const unsigned long long p = __hip_atomic_load(pp.sig, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          if (p >= trig) {
+            v = p >= late ? 0 : 1;
+            break;
+          }
+          if (__builtin_amdgcn_s_memrealtime() - t0 > pp.timeout) break;
+          __builtin_amdgcn_s_sleep(2);
+        }
+        go = v;
+      }
+      __syncthreads();
+      const int g = go;
+      __syncthreads();
+      if (g < 0) {
+        l = pp.L;
+        break;
+      }
+      if (g == 0) continue;
+      const unsigned c = __hip_atomic_load(pp.xcc0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const int r = (int)((x - c) & 7u);
+      const PfGeom G = pp.geo[k];
+      typedef const __attribute__((address_space(1))) u32x4* gptr;  // global, not flat
+      const gptr W = (gptr)pp.W[k * pp.L + l] + lane;
+      const int J = G.nblk > r ? (G.nblk - r + 7) / 8 : 0;
+      for (int j = rank; j < J; j += nrank) {
+        const int L = r + 8 * j;
+        const int bx = L % G.gx, by = L / G.gx;
+        const int kc0 = by * G.kcs, nk = min(G.KC, kc0 + G.kcs) - kc0;
+        for (int rr = 0; rr < G.RB; ++rr) {
+          const gptr src = W + ((size_t)min(bx * G.RB + rr, G.RBtot - 1) * G.KC + kc0) * 64;
+          for (int k0 = w; k0 < nk; k0 += nwv * kPfDepth) {
+            u32x4 q[kPfDepth];
+#pragma unroll
+            for (int u = 0; u < kPfDepth; ++u) q[u] = src[(size_t)min(k0 + nwv * u, nk - 1) * 64];
+#pragma unroll
+            for (int u = 0; u < kPfDepth; ++u) acc ^= q[u][0] ^ q[u][1] ^ q[u][2] ^ q[u][3];
+          }
+        }
+      }
+    }
+  }
+  if (acc == pp.magic) *pp.sink = acc;
+}
+
+hipError_t launch_prefetcher(const PrefetchPlan& pp, hipStream_t s) {
+  if (!pp.W || !pp.sig || !pp.xcc0 || !pp.sink || pp.L <= 0) return hipErrorInvalidValue;
+  for (int k = 0; k < 4; ++k) {
+    const PfGeom& G = pp.geo[k];
+    if (G.KC <= 0 || G.RBtot <= 0 || G.RB <= 0 || G.kcs <= 0 || G.gx <= 0 || G.nblk <= 0 || G.nblk % G.gx)
+      return hipErrorInvalidValue;
+  }
+  prefetcher_kernel<<<kPfBlocks, 256, 0, s>>>(pp);
   return hipGetLastError();
 }
 
@@ -1058,19 +1131,16 @@ __global__ __launch_bounds__(64 * AT_MAXW) void attn_split_kernel(AttnArgs a) {
   constexpr int ROOT = AT_MAXW * 2 * 32 * DH;                     // 32 V rows per half-wave
   __shared__ __align__(16) uint16_t lds[PFX > ROOT ? PFX : ROOT];
   __shared__ __align__(16) float qrow[AT_MAXW][2][DH];
+  pass_signal(a.sig);
   const int npre = a.H * a.nsplit;
   if ((int)blockIdx.x < npre) attn_prefix_chunk<DH>(a, lds, blockIdx.x % a.H, blockIdx.x / a.H);
   else attn_root_path<DH>(a, lds, qrow, (blockIdx.x - npre) % a.H, (blockIdx.x - npre) / a.H);
 }
 
 template <int DH>
-__global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a, Prefetch pf) {
+__global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
   constexpr int REC = DH + 4, PER = 256 / DH, B = 16;
-  __shared__ uint32_t pf_lds[kPrefetchLdsWords];
-  if ((int)blockIdx.x >= pf.nmain) {
-    prefetch_weights(pf, blockIdx.x - pf.nmain, pf_lds);
-    return;
-  }
+  pass_signal(a.sig);
   const int pair = blockIdx.x * PER + threadIdx.x / DH, dd = threadIdx.x % DH;
   if (pair >= a.N * a.H) return;
   const int n = pair / a.H, h = pair - n * a.H, ns = a.nsplit + 1;
@@ -1099,7 +1169,7 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a, Prefetch pf
   st_act((uint16_t*)a.out, n, h * DH + dd, a.ldo, O / L);
 }
 
-hipError_t launch_attn(int f32, int DH, const AttnArgs& a, const Prefetch& pf0, hipStream_t s) {
+hipError_t launch_attn(int f32, int DH, const AttnArgs& a, hipStream_t s) {
   if (!f32) {
     if (a.N <= 0 || a.N > a.max_nodes || (DH != 64 && DH != 32)) return hipErrorInvalidValue;
     if (a.P > 0 && (a.CL <= 0 || a.CL > AT_STAGE || a.CL % 32 || a.nsplit != (a.P + a.CL - 1) / a.CL))
@@ -1107,14 +1177,12 @@ hipError_t launch_attn(int f32, int DH, const AttnArgs& a, const Prefetch& pf0, 
     const int nw = min(AT_MAXW, (a.N + 15) / 16);
     const int blocks = a.H * a.nsplit + a.H * ((a.N + 2 * nw - 1) / (2 * nw));
     const int mblocks = (a.N * a.H * DH + 255) / 256;
-    const Prefetch pf = pf_after(pf0, mblocks);
-    const int mgrid = pf.nworkers ? pf.nmain + pf.nworkers : mblocks;
     if (DH == 64) {
       attn_split_kernel<64><<<blocks, 64 * nw, 0, s>>>(a);
-      attn_merge_kernel<64><<<mgrid, 256, 0, s>>>(a, pf);
+      attn_merge_kernel<64><<<mblocks, 256, 0, s>>>(a);
     } else {
       attn_split_kernel<32><<<blocks, 64 * nw, 0, s>>>(a);
-      attn_merge_kernel<32><<<mgrid, 256, 0, s>>>(a, pf);
+      attn_merge_kernel<32><<<mblocks, 256, 0, s>>>(a);
     }
     return hipGetLastError();
   }

@@ -57,7 +57,18 @@ struct ssd_model {
   bool owns_pack = true;  // false for a prefix view (shares its parent's copies)
   std::vector<const void*> p_qkv, p_o, p_fc, p_pr;
   const void* p_head = nullptr;
+  void* wtab = nullptr;  // device [4][n_layer]: p_qkv, p_o, p_fc, p_pr (for the prefetcher); own copy per view
 };
+
+// the device table of a bf16 model's packed weight pointers, [4][L]
+static hipError_t make_wtab(ssd_model* m) {
+  const int L = m->cfg.n_layer;
+  std::vector<const void*> t;
+  for (auto* v : {&m->p_qkv, &m->p_o, &m->p_fc, &m->p_pr}) t.insert(t.end(), v->begin(), v->begin() + L);
+  hipError_t e = hipMalloc(&m->wtab, t.size() * sizeof(void*));
+  if (e == hipSuccess) e = hipMemcpy(m->wtab, t.data(), t.size() * sizeof(void*), hipMemcpyHostToDevice);
+  return e;
+}
 
 struct ssd_kv {
   const ssd_model* m = nullptr;
@@ -83,12 +94,21 @@ struct ssd_kv {
   int next_slot = 0;
   hipEvent_t slot_ev[kStageSlots] = {};
   bool slot_used[kStageSlots] = {};
+  // pass signals and the weight prefetcher (bf16 models)
+  unsigned long long* d_sig = nullptr;  // bumped by every kernel of a pass as it starts
+  unsigned* d_xcc0 = nullptr;           // XCD of block 0 of the last pass's embedding
+  unsigned* d_sink = nullptr;
+  unsigned long long sig_count = 0;     // signals of every pass enqueued so far
+  hipStream_t pf_stream = nullptr;      // created on first use
 };
 
 struct ssd_graph {
   hipGraph_t graph = nullptr;
   hipGraphExec_t exec = nullptr;
   char* pinned = nullptr;
+  const ssd_model* m = nullptr;  // the pass it replays
+  ssd_kv* kv = nullptr;
+  int n = 0;
 };
 
 // ------------------------------------------------------------------ small host helpers
@@ -225,8 +245,10 @@ extern "C" ssd_status ssd_model_create(const ssd_config* cfg, const ssd_weights*
     }
     m->p_head = pack(m->wte, V, d, b_head);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e == hipSuccess) e = make_wtab(m);
     if (e != hipSuccess) {
       (void)hipFree(m->pack);
+      if (m->wtab) (void)hipFree(m->wtab);
       delete m;
       return fail(SSD_E_DEVICE, std::string("weight packing: ") + hipGetErrorString(e));
     }
@@ -238,6 +260,7 @@ extern "C" ssd_status ssd_model_create(const ssd_config* cfg, const ssd_weights*
 extern "C" void ssd_model_destroy(ssd_model* m) {
   if (!m) return;
   if (m->pack && m->owns_pack) (void)hipFree(m->pack);
+  if (m->wtab) (void)hipFree(m->wtab);
   delete m;
 }
 
@@ -250,11 +273,18 @@ extern "C" ssd_status ssd_model_prefix_view(const ssd_model* m, int32_t n_layer,
   std::vector<const void*>* per[] = {&v->ln1_g, &v->ln1_b, &v->w_qkv, &v->b_qkv, &v->w_o, &v->b_o, &v->ln2_g,
                                      &v->ln2_b, &v->w_fc, &v->b_fc, &v->w_pr, &v->b_pr};
   for (auto a : per) a->resize(n_layer);
+  v->wtab = nullptr;
   if (!v->f32) {
     v->p_qkv.resize(n_layer);
     v->p_o.resize(n_layer);
     v->p_fc.resize(n_layer);
     v->p_pr.resize(n_layer);
+    const hipError_t e = make_wtab(v);
+    if (e != hipSuccess) {
+      if (v->wtab) (void)hipFree(v->wtab);
+      delete v;
+      return fail(SSD_E_DEVICE, std::string("weight table: ") + hipGetErrorString(e));
+    }
   }
   *out = v;
   return SSD_OK;
@@ -332,6 +362,7 @@ extern "C" ssd_status ssd_kv_create(const ssd_model* m, int32_t max_ctx, int32_t
   const size_t o_amw = take(std::max(argmax_work_bytes(max_nodes, V), topk_work_bytes(max_nodes, V)));
   const size_t o_r = take((size_t)V * 8), o_p = take((size_t)V * 8), o_qq = take((size_t)V * 8);
   const size_t o_err = take(256);
+  const size_t o_sig = take(256);  // signal counter, XCD of block 0, sink
   hipError_t e = hipMalloc(&kv->ws, off);
   if (e == hipSuccess) e = hipMemset(kv->ws, 0, off);
   if (e != hipSuccess) {
@@ -355,6 +386,9 @@ extern "C" ssd_status ssd_kv_create(const ssd_model* m, int32_t max_ctx, int32_t
   kv->d_p = (double*)(b + o_p);
   kv->d_qq = (double*)(b + o_qq);
   kv->d_err = (unsigned*)(b + o_err);
+  kv->d_sig = (unsigned long long*)(b + o_sig);
+  kv->d_xcc0 = (unsigned*)(b + o_sig + 8);
+  kv->d_sink = (unsigned*)(b + o_sig + 16);
   kv->slot_bytes = (stage_bytes(max_nodes) + 255) / 256 * 256;
   e = hipHostMalloc((void**)&kv->pinned, kv->slot_bytes * kStageSlots, hipHostMallocDefault);
   for (int i = 0; i < kStageSlots && e == hipSuccess; ++i) e = hipEventCreateWithFlags(&kv->slot_ev[i], hipEventDisableTiming);
@@ -368,6 +402,10 @@ extern "C" ssd_status ssd_kv_create(const ssd_model* m, int32_t max_ctx, int32_t
 
 extern "C" void ssd_kv_destroy(ssd_kv* kv) {
   if (!kv) return;
+  if (kv->pf_stream) {
+    (void)hipStreamSynchronize(kv->pf_stream);
+    (void)hipStreamDestroy(kv->pf_stream);
+  }
   for (int i = 0; i < kStageSlots; ++i)
     if (kv->slot_ev[i]) {
       (void)hipEventSynchronize(kv->slot_ev[i]);
@@ -453,26 +491,46 @@ static int gemm_kcs(int n, int kind, int rows, int K) {
   return gemm_split_kc(rows, K, std::min(n, vec ? 16 : 256), vec, kind == EPI_PARTIAL, &S);
 }
 
-// The weight fragments the first launch of run_gemm(m, n, kind, Wp, rows, K)
-// reads, for the kernel enqueued just before it to warm (bf16 models).
-static Prefetch next_gemm(const ssd_model* m, int n, int kind, const void* Wp, int rows, int K) {
-  Prefetch pf{};
-  if (m->f32 || !g_prefetch || !Wp) return pf;
-  const int vec = gemm_vec(n);
-  const GemmGeom g = gemm_geom(kind, vec, rows, K, std::min(n, vec ? 16 : 256), gemm_kcs(n, kind, rows, K));
-  pf.Wp = Wp;
-  pf.KC = g.KC;
-  pf.RBtot = g.RBtot;
-  pf.RB = g.RB;
-  pf.kcs = g.kcs;
-  pf.gx = g.gx;
-  pf.nblk = g.gx * g.gy;
-  pf.nworkers = std::min((pf.nblk + 7) / 8 * 8, 256);
-  return pf;
+// The prefetcher's plan for a bf16 pass over n nodes: the launch geometry of
+// the first launch of each weight GEMM (see run_gemm), the weight table and
+// the session's signal words; base is filled in when the pass is enqueued.
+static PrefetchPlan prefetch_plan(const ssd_model* m, const ssd_kv* kv, int n) {
+  PrefetchPlan pp{};
+  const int d = m->cfg.d_model, M = m->cfg.d_mlp;
+  const int vec = gemm_vec(n), nn = std::min(n, vec ? 16 : 256);
+  const int kinds[4] = {EPI_QKV, EPI_PARTIAL, EPI_GELU, EPI_PARTIAL};
+  const int rows[4] = {3 * d, d, M, d}, Ks[4] = {d, d, d, M};
+  for (int k = 0; k < 4; ++k) {
+    const GemmGeom g = gemm_geom(kinds[k], vec, rows[k], Ks[k], nn, gemm_kcs(n, kinds[k], rows[k], Ks[k]));
+    pp.geo[k] = PfGeom{g.KC, g.RBtot, g.RB, g.kcs, g.gx, g.gx * g.gy};
+  }
+  pp.W = (const void* const*)m->wtab;
+  pp.L = m->cfg.n_layer;
+  pp.sig = kv->d_sig;
+  pp.xcc0 = kv->d_xcc0;
+  pp.timeout = 5000000ull;  // 50 ms
+  pp.sink = kv->d_sink;
+  pp.magic = 0x5bd1e995u;
+  return pp;
+}
+
+// Accounts for the signals of one bf16 pass about to be enqueued and, when
+// weight prefetch is on, launches its prefetcher on the session's side
+// stream first (the pass never waits for it).
+static ssd_status start_pass_prefetch(const ssd_model* m, ssd_kv* kv, int n) {
+  if (m->f32) return SSD_OK;
+  const unsigned long long base = kv->sig_count;
+  kv->sig_count += (unsigned long long)sigs_per_pass(m->cfg.n_layer);
+  if (!g_prefetch) return SSD_OK;
+  if (!kv->pf_stream) HIP_TRY(hipStreamCreateWithFlags(&kv->pf_stream, hipStreamNonBlocking));
+  PrefetchPlan pp = prefetch_plan(m, kv, n);
+  pp.base = base;
+  HIP_TRY(launch_prefetcher(pp, kv->pf_stream));
+  return SSD_OK;
 }
 
 static hipError_t run_gemm(const ssd_model* m, int n, int kind, const void* Wraw, const void* Wp, int rows, int K,
-                           const void* act, const Epi& ep, hipStream_t s, const Prefetch& pf = Prefetch{}) {
+                           const void* act, const Epi& ep, hipStream_t s) {
   if (m->f32) return launch_gemm_f32(kind, (const float*)Wraw, rows, K, (const float*)act, K, ep, s);
   const int vec = gemm_vec(n);
   const int group = vec ? 16 : 256;
@@ -483,7 +541,8 @@ static hipError_t run_gemm(const ssd_model* m, int n, int kind, const void* Wraw
     e2.N = std::min(group, n - n0);
     // fragment tiles of 16 nodes, each K/32 fragments of 512 elements
     const uint16_t* a = (const uint16_t*)act + (size_t)(n0 / 16) * (K / 32) * 512;
-    hipError_t r = launch_gemm_bf16(kind, vec, Wp, rows, K, a, kcs, e2, n0 == 0 ? pf : Prefetch{}, s);
+    e2.sig = n0 == 0 ? ep.sig : nullptr;  // one signal per GEMM
+    hipError_t r = launch_gemm_bf16(kind, vec, Wp, rows, K, a, kcs, e2, s);
     if (r != hipSuccess) return r;
   }
   return hipSuccess;
@@ -512,7 +571,8 @@ static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int3
   const int* d_off = kv->d_tree + 4 * maxn;
   const int* d_path32 = kv->d_tree + 5 * maxn;
   const int* d_paths = d_path32 + (size_t)n * kPath32;
-  HIP_TRY(launch_embed(f32, m->wte, m->wpe, d_tok, d_pos, n, d, kv->x, s));
+  unsigned long long* sig = f32 ? nullptr : kv->d_sig;  // pass signals (bf16 models)
+  HIP_TRY(launch_embed(f32, m->wte, m->wpe, d_tok, d_pos, n, d, kv->x, sig, kv->d_xcc0, s));
 
   // GEMM-input leading dimensions (fp32: row stride; bf16: k-steps)
   const int ld_d = f32 ? d : d / 32, ld_m = f32 ? M : M / 32;
@@ -527,8 +587,9 @@ static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int3
   const void* pend_bias = nullptr;
   for (int l = 0; l < L; ++l) {
     HIP_TRY(launch_ln(f32, kv->x, n, d, kv->part, pend_S, pstride, pend_bias, m->ln1_g[l], m->ln1_b[l], c.ln_eps,
-                      kv->act_a, ld_d, next_gemm(m, n, EPI_QKV, f32 ? nullptr : m->p_qkv[l], 3 * d, d), s));
+                      kv->act_a, ld_d, sig, s));
     Epi e{};
+    e.sig = sig;
     e.bias = m->b_qkv[l];
     e.N = n;
     e.M = 3 * d;
@@ -564,9 +625,11 @@ static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int3
     a.scale = 1.0f / std::sqrt((float)DH);
     a.CL = attn_chunk(P);
     a.nsplit = attn_nsplit(P);
-    HIP_TRY(launch_attn(f32, DH, a, next_gemm(m, n, kind_res, f32 ? nullptr : m->p_o[l], d, d), s));
+    a.sig = sig;
+    HIP_TRY(launch_attn(f32, DH, a, s));
 
     Epi eo{};
+    eo.sig = sig;
     eo.bias = f32 ? m->b_o[l] : nullptr;
     eo.N = n;
     eo.M = d;
@@ -577,18 +640,19 @@ static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int3
     HIP_TRY(run_gemm(m, n, kind_res, m->w_o[l], f32 ? nullptr : m->p_o[l], d, d, kv->act_o, eo, s));
 
     HIP_TRY(launch_ln(f32, kv->x, n, d, kv->part, f32 ? 0 : s_o, pstride, m->b_o[l], m->ln2_g[l], m->ln2_b[l],
-                      c.ln_eps, kv->act_a, ld_d, next_gemm(m, n, EPI_GELU, f32 ? nullptr : m->p_fc[l], M, d), s));
+                      c.ln_eps, kv->act_a, ld_d, sig, s));
     Epi ef{};
+    ef.sig = sig;
     ef.bias = m->b_fc[l];
     ef.N = n;
     ef.M = M;
     ef.d = d;
     ef.out = kv->act_f;
     ef.ldo = ld_m;
-    HIP_TRY(run_gemm(m, n, EPI_GELU, m->w_fc[l], f32 ? nullptr : m->p_fc[l], M, d, kv->act_a, ef, s,
-                     next_gemm(m, n, kind_res, f32 ? nullptr : m->p_pr[l], d, M)));
+    HIP_TRY(run_gemm(m, n, EPI_GELU, m->w_fc[l], f32 ? nullptr : m->p_fc[l], M, d, kv->act_a, ef, s));
 
     Epi ep{};
+    ep.sig = sig;
     ep.bias = f32 ? m->b_pr[l] : nullptr;
     ep.N = n;
     ep.M = d;
@@ -601,7 +665,7 @@ static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int3
     pend_bias = m->b_pr[l];
   }
   HIP_TRY(launch_ln(f32, kv->x, n, d, kv->part, pend_S, pstride, pend_bias, m->lnf_g, m->lnf_b, c.ln_eps, kv->act_a,
-                    ld_d, Prefetch{}, s));
+                    ld_d, nullptr, s));
   Epi eh{};
   eh.bias = nullptr;
   eh.N = n;
@@ -624,7 +688,8 @@ extern "C" ssd_status ssd_tree_verify(const ssd_model* m, ssd_kv* kv, int32_t pr
   st = acquire_slot(kv, &host, &slot);
   if (st != SSD_OK) return st;
   const size_t used = fill_stage(host, prefix_len, tree_tokens, parent_idx, n_nodes, kv->max_nodes);
-  st = enqueue_verify(m, kv, prefix_len, n_nodes, host, used, logits, s);
+  st = start_pass_prefetch(m, kv, n_nodes);
+  if (st == SSD_OK) st = enqueue_verify(m, kv, prefix_len, n_nodes, host, used, logits, s);
   ssd_status st2 = release_slot(kv, slot, s);
   return st != SSD_OK ? st : st2;
 }
@@ -637,6 +702,9 @@ extern "C" ssd_status ssd_graph_capture_verify(const ssd_model* m, ssd_kv* kv, i
   ssd_status st = check_verify_args(m, kv, prefix_len, tree_tokens, parent_idx, n_nodes, logits, &md);
   if (st != SSD_OK) return st;
   ssd_graph* g = new ssd_graph();
+  g->m = m;
+  g->kv = kv;
+  g->n = n_nodes;
   hipError_t e = hipHostMalloc((void**)&g->pinned, kv->slot_bytes, hipHostMallocDefault);
   if (e != hipSuccess) {
     delete g;
@@ -675,6 +743,8 @@ extern "C" ssd_status ssd_graph_capture_verify(const ssd_model* m, ssd_kv* kv, i
 
 extern "C" ssd_status ssd_graph_launch(ssd_graph* g, void* stream) {
   if (!g || !g->exec) return fail(SSD_E_INVALID_ARG, "null graph");
+  const ssd_status st = start_pass_prefetch(g->m, g->kv, g->n);
+  if (st != SSD_OK) return st;
   HIP_TRY(hipGraphLaunch(g->exec, (hipStream_t)stream));
   return SSD_OK;
 }

@@ -44,12 +44,13 @@ struct Epi {
   float* part;
   long long part_stride;  // elements between splits
   int split;              // set by the kernel from blockIdx.y
+  unsigned long long* sig;  // pass signal counter (nullptr: none)
 };
 
 // tile shape of the bf16 GEMM for a node count: node tiles of 16, row blocks
 // per workgroup, k-steps per staged chunk, nodes of the vector path
 struct GemmCfg {
-  int nt, rb, ck, nv;
+  int nt, rb, ck, nv, nw;  // nw: waves per workgroup
 };
 
 // launch geometry of one bf16 GEMM: block (bx, by) owns weight row blocks
@@ -59,18 +60,33 @@ struct GemmGeom {
   int RB, kcs, gx, gy, KC, RBtot;
 };
 
-// Weight prefetch into the L2 of the XCD that will read it.  Block b of a
-// launch runs on XCD (b + c) mod 8, with the same c for every launch of a
-// queue (whatever the grid), so block B of one launch and block L of the
-// next share an L2 when B = L (mod 8).  A launch carrying a Prefetch runs its
-// own work in blocks [0, nmain) and, in blocks nmain + w (w < nworkers, both
-// multiples of 8), loads the weight fragments of the next GEMM's blocks
-// L = w (mod 8) into LDS that nothing reads: the bytes stay in that L2.
-struct Prefetch {
-  const void* Wp;  // packed weights of the next GEMM (nullptr: no prefetch)
-  int KC, RBtot, RB, kcs, gx, nblk;  // its geometry; its block L = bx + gx by, L < nblk
-  int nmain;       // set by the launcher
-  int nworkers;
+// ---- weight prefetch from a second stream
+//
+// Every kernel of a bfloat16 pass bumps a signal counter when it starts
+// (block 0): the embedding, then per layer LN1, QKV GEMM, attention split,
+// attention merge, attention-out GEMM, LN2, MLP up, MLP down.  A prefetcher
+// kernel launched on another stream beside the pass waits for these signals
+// and loads each weight GEMM's fragments into the L2 of the XCD that will
+// read them a few kernels ahead: block b of every launch of a queue runs on
+// XCD (b + c) mod 8 with one c per queue, which the embedding records.
+enum SigKernel { SIG_LN1 = 0, SIG_QKV, SIG_SPLIT, SIG_MERGE, SIG_OUT, SIG_LN2, SIG_FC, SIG_PROJ, kSigPerLayer };
+// counter value (past a pass's base) once kernel k of layer l has started
+inline __host__ __device__ int sig_index(int l, int k) { return 2 + kSigPerLayer * l + k; }
+inline int sigs_per_pass(int L) { return 1 + kSigPerLayer * L; }
+
+struct PfGeom {
+  int KC, RBtot, RB, kcs, gx, nblk;  // a GEMM launch (see GemmGeom), nblk = gx * gy
+};
+struct PrefetchPlan {
+  const void* const* W;     // device [4][L]: packed QKV, attention-out, MLP-up, MLP-down weights
+  int L;
+  PfGeom geo[4];            // their launches at this pass's node count
+  unsigned long long* sig;  // the session's signal counter
+  const unsigned* xcc0;     // XCD of block 0 of the pass's embedding
+  unsigned long long base;  // counter value before this pass
+  unsigned long long timeout;  // s_memrealtime ticks (100 MHz) before the prefetcher stops waiting
+  unsigned* sink;           // written only when the folded loads equal `magic` (keeps them alive)
+  unsigned magic;
 };
 
 struct AttnArgs {
@@ -94,6 +110,7 @@ struct AttnArgs {
   // bf16 models
   int CL;               // cache rows per prefix chunk (attn_chunk(P))
   int nsplit;           // prefix chunks (attn_nsplit(P))
+  unsigned long long* sig;  // pass signal counter (nullptr: none); both kernels signal
 };
 
 // bf16 attention: cache rows per prefix chunk, a multiple of 32 between 64
@@ -118,24 +135,24 @@ inline int attn_max_nsplit(int max_ctx) {
 
 // ---- launchers (kernels.hip); all enqueue on `s` and return the launch status
 hipError_t launch_embed(int f32, const void* wte, const void* wpe, const int* tokens, const int* pos, int N, int d,
-                        float* x, hipStream_t s);
+                        float* x, unsigned long long* sig, unsigned* xcc0, hipStream_t s);
 // x += bias + part[0..S-1] (if S > 0), then LayerNorm into the GEMM-input
 // buffer a (lda: fp32 row stride, or bf16 k-steps d / 32; see st_act)
 hipError_t launch_ln(int f32, float* x, int N, int d, const float* part, int S, size_t pstride, const void* bias,
-                     const void* g, const void* b, float eps, void* a, int lda, const Prefetch& pf, hipStream_t s);
+                     const void* g, const void* b, float eps, void* a, int lda, unsigned long long* sig, hipStream_t s);
 hipError_t launch_gemm_f32(int kind, const float* W, int M, int K, const float* act, int lda, const Epi& ep,
                            hipStream_t s);
-GemmCfg gemm_cfg(int N, int vec);
+GemmCfg gemm_cfg(int N, int vec, int kind);
 // k-steps per split and number of splits (EPI_PARTIAL only; 1 otherwise)
 int gemm_split_kc(int M, int K, int N, int vec, int want_split, int* splits);
 GemmGeom gemm_geom(int kind, int vec, int M, int K, int N, int kcs);
 // Wp: weights packed in 16x32 float16 fragments (see pack); act: activations
 // of this launch's first node in fragment order (see st_act); kcs k-steps per
-// split (grid.y = ceil(K/32 / kcs)); pf: weights of the next GEMM to warm
-// (only honoured when grid.y = 1)
+// split (grid.y = ceil(K/32 / kcs))
 hipError_t launch_gemm_bf16(int kind, int vec, const void* Wp, int M, int K, const uint16_t* act, int kcs,
-                            const Epi& ep, const Prefetch& pf, hipStream_t s);
-hipError_t launch_attn(int f32, int DH, const AttnArgs& a, const Prefetch& pf, hipStream_t s);
+                            const Epi& ep, hipStream_t s);
+hipError_t launch_attn(int f32, int DH, const AttnArgs& a, hipStream_t s);
+hipError_t launch_prefetcher(const PrefetchPlan& pp, hipStream_t s);
 hipError_t launch_pack_bf16(const uint16_t* W, int M, int K, void* out, hipStream_t s);
 size_t packed_bytes(int M, int K);
 // greedy argmax per node; work: argmax_work_bytes(N, V) bytes of device scratch
