@@ -228,6 +228,58 @@ ssd_status ssd_set_gemm_path(int32_t path);
  * or 1). */
 ssd_status ssd_set_weight_prefetch(int32_t on);
 
+/* How a bfloat16 verification pass runs (Sec. 2.1: a decode step streams
+ * every weight once; Sec. 3.1: one step scores the whole tree).
+ *   0 (default) = automatic: the persistent single launch when the session
+ *     supports it (head dimension 64, at most 64 nodes, a 256-CU device with
+ *     8 XCDs), else one kernel per sub-layer;
+ *   1 = always one kernel per sub-layer;
+ *   2 = the persistent single launch only: ssd_tree_verify and
+ *     ssd_graph_capture_verify return SSD_E_UNSUPPORTED where it does not
+ *     apply.
+ * The persistent launch runs every layer in one kernel: 256 compute
+ * workgroups (one per CU) hand results to each other through flags in device
+ * memory, and 256 more warm the L2 with the weights of their partner's next
+ * stage.  Every wait inside it is bounded; if one times out (200 ms) the
+ * launch ends early, its logits are undefined, and the session's error
+ * counter (ssd_kv_error_count) is incremented.  Both ways meet the same
+ * tolerance against the definition; their logits differ in the last bits.
+ * Process-wide.  Errors: SSD_E_INVALID_ARG (mode not 0, 1 or 2). */
+ssd_status ssd_set_pass_mode(int32_t mode);
+
+/* Host-only: the persistent launch's work split for a model shape and a
+ * count of 16-node tiles (1..4), as the session computes it.  tab receives
+ * [256][32] int32 rows, one per compute workgroup (XCD x, rank r at row
+ * 32 x + r): [0] attention units, then up to 8 entries head | tile << 16;
+ * [9] QKV row blocks, then up to 4 row-block indices of W_qkv; [14] the same
+ * for W_o; [19] for W_fc; [24] for W_pr; [29], [30] the workgroup's range of
+ * LM-head row blocks.  xh[2x], xh[2x+1] bound XCD x's heads; xf[2x], xf[2x+1]
+ * its hidden features in units of 32.  Errors: SSD_E_INVALID_ARG (null
+ * pointer), SSD_E_UNSUPPORTED (the shape does not fit the split: head
+ * dimension not 64, or too many units for a workgroup). */
+ssd_status ssd_fused_plan(int32_t n_head, int32_t d_model, int32_t d_mlp, int32_t vocab, int32_t n_tiles,
+                          int32_t *tab, int32_t *xh, int32_t *xf);
+
+/* Stage timestamps of the persistent launch, for profiling.  With buf not
+ * NULL, every later persistent pass of this session records for compute
+ * workgroup g (XCD x, rank r: g = 32 x + r), layer l (n_layer + 1 rows; row
+ * n_layer holds the final LayerNorm in stage 0 and the LM head in stage 1)
+ * and stage s (8 per layer: LayerNorm, QKV, attention, out-projection,
+ * LayerNorm, MLP up, MLP down, unused) three s_memrealtime readings (100 MHz):
+ * stage entry, dependency met, stage published, at
+ * buf[((g * (n_layer + 1) + l) * 8 + s) * 3 + k].  buf is caller-owned device
+ * memory of 256 * (n_layer + 1) * 24 uint64 words for the largest model the
+ * session runs; stages a workgroup skips keep old values.  NULL stops
+ * recording.  Errors: SSD_E_INVALID_ARG (null session), SSD_E_UNSUPPORTED
+ * (the session has no persistent pass). */
+ssd_status ssd_kv_set_trace(ssd_kv *kv, uint64_t *buf);
+
+/* Prefetch distance of the persistent launch, in stages (a layer has seven:
+ * LayerNorm, QKV, attention, out-projection, LayerNorm, MLP up, MLP down);
+ * default 1.  Results are bitwise the same for every value.  Process-wide.
+ * Errors: SSD_E_INVALID_ARG (outside 0..8). */
+ssd_status ssd_set_fused_ahead(int32_t stages);
+
 const char *ssd_status_string(ssd_status s);
 const char *ssd_last_error(void);
 

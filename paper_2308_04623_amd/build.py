@@ -5,7 +5,7 @@ import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
-SOURCES = [os.path.join(HERE, "csrc", "kernels.hip"), os.path.join(HERE, "csrc", "runtime.hip")]
+SOURCES = [os.path.join(HERE, "csrc", n) for n in ("kernels.hip", "fused.hip", "runtime.hip")]
 OUT = os.path.join(HERE, "libssd.so")
 
 HIPCC_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

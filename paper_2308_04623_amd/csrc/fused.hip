@@ -1,0 +1,1273 @@
+// The whole verification pass of a bfloat16 model (head dimension 64, at most
+// 64 tree nodes) as one persistent launch on CDNA4 (gfx950).
+//
+// Sec. 2.1 of Spector & Re (arXiv 2308.04623) observes that one small-batch
+// decode step of a transformer is bound by streaming the weights from memory,
+// and Sec. 3.1 makes the step score a whole token tree against the cached
+// prefix.  At GPT-2-L size each layer's four weight matrices take about 6 us
+// to stream at full HBM bandwidth, so the pass cannot afford a kernel boundary
+// (3-7 us each) per sub-layer.  Here one launch runs every layer:
+//
+//  * 256 compute workgroups, one per CU.  A workgroup reads the XCD it runs
+//    on from the hardware (x) and takes rank r = blockIdx / 8 within it.  Each
+//    XCD owns a contiguous range of heads and a slice of the MLP's hidden
+//    features, sized so that every XCD streams the same weight bytes per
+//    layer.  Inside an XCD the work of a stage is split over its 32 ranks
+//    (see the host planner below).
+//  * Stages per layer: LN1 (residual update + LayerNorm of the XCD's rows),
+//    QKV (the XCD's heads), ATT (tree attention per head and 16-node tile),
+//    WO (attention out-projection over the XCD's heads: a partial residual),
+//    LN2, FC (+GELU, the XCD's hidden slice), WPR (MLP down-projection over
+//    that slice: a partial residual).  Only the two partial residuals cross
+//    XCDs: every XCD adds the eight partials of a node row itself, in XCD
+//    order, into its own copy of the residual stream, so all copies agree
+//    bit for bit.  Every other hand-off stays inside one XCD's L2.
+//  * Hand-offs are per-workgroup stage flags carrying a monotonically
+//    increasing tag (pass, layer, stage).  A workgroup writes its outputs,
+//    waits for its stores, then stores its flag; consumers poll the 32 flags
+//    of their XCD or all 256 flags.  Data and flags read across XCDs use
+//    device-coherent (sc1) accesses; inside an XCD plain stores and
+//    non-temporal loads (which miss the CU's L1) suffice.
+//  * 256 prefetch workgroups (blocks 256..511) each follow one compute
+//    workgroup on the same XCD, loading the weights (and cached K/V) of its
+//    next stage into that XCD's L2 while it waits on a dependency.  They only
+//    read; nothing waits on them.
+//  * Every wait is bounded (s_memrealtime); a timeout raises an abort word
+//    that every other wait also watches, so all workgroups leave the kernel,
+//    and the session's error counter records it.
+//
+// Arithmetic per output is fixed by the matrix, the k-range of the XCD and
+// the workgroup-internal split, never by the node count or a node's slot, so
+// a node's logits do not depend on the rest of the tree.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include <algorithm>
+#include <string>
+#include <vector>
+
+#include "ssd_internal.h"
+
+namespace ssd {
+namespace fz {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x8 __attribute__((ext_vector_type(8)));
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+// Global-memory pointers (address space 1): loads through them are
+// global_load, waited on in order, never flat.
+template <typename T>
+using gptr = const __attribute__((address_space(1))) T*;
+template <typename T>
+using gw = __attribute__((address_space(1))) T*;
+template <typename T>
+__device__ __forceinline__ gptr<T> G(const void* p) {
+  return (gptr<T>)p;
+}
+
+constexpr int NTH = 512;  // threads per workgroup
+constexpr int NWV = NTH / 64;  // waves per workgroup
+constexpr int DH = 64;
+
+__device__ __forceinline__ float bf2f(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
+__device__ __forceinline__ uint16_t f2bf(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
+__device__ __forceinline__ uint32_t f2bf2(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){a, b}, bf16x2_t));
+}
+__device__ __forceinline__ unsigned xcc_id() {
+  unsigned x;
+  asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(x));
+  return x & 15;
+}
+__device__ __forceinline__ unsigned long long now() { return __builtin_amdgcn_s_memrealtime(); }
+
+// float16 GEMM input in matrix-core fragment order (ld = k-steps of 32 per
+// 16-node tile): element (n, k) in fragment (n/16) ld + k/32, lane
+// (n%16) + 16 ((k%32)/8), position k%8
+__device__ __forceinline__ void st_act(uint16_t* p, int n, int k, int ld, float v) {
+  const size_t f = (size_t)(n >> 4) * ld + (k >> 5);
+  p[f * 512 + ((n & 15) + 16 * ((k & 31) >> 3)) * 8 + (k & 7)] = __builtin_bit_cast(uint16_t, (_Float16)v);
+}
+
+__device__ __forceinline__ void st_act(gw<uint16_t> p, int n, int k, int ld, float v) {
+  const size_t f = (size_t)(n >> 4) * ld + (k >> 5);
+  p[f * 512 + ((n & 15) + 16 * ((k & 31) >> 3)) * 8 + (k & 7)] = __builtin_bit_cast(uint16_t, (_Float16)v);
+}
+
+__device__ __forceinline__ float gelu_tanh(float x) {
+  const float c = 0.7978845608028654f;  // sqrt(2/pi)
+  return 0.5f * x * (1.0f + tanhf(c * (x + 0.044715f * x * x * x)));
+}
+
+__device__ __forceinline__ void pack_hilo8(const float (&v)[8], u32x4& hi, u32x4& lo) {
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const uint32_t hp = f2bf2(v[2 * e], v[2 * e + 1]);
+    hi[e] = hp;
+    lo[e] = f2bf2(v[2 * e] - __uint_as_float(hp << 16), v[2 * e + 1] - __uint_as_float(hp & 0xffff0000u));
+  }
+}
+
+__device__ __forceinline__ f32x4 mfma_bf16(const u32x4& a, const u32x4& b, const f32x4& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c, 0,
+                                                  0, 0);
+}
+
+__device__ __forceinline__ void wave_sync_lds() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+
+// A uniform base pointer the compiler must treat as new at each use, so that
+// per-thread addresses derived from it are formed inside the stage body
+// instead of being hoisted out of the stage loop (where they would occupy,
+// and spill, registers for the whole pass).
+__device__ __forceinline__ unsigned long long opq_bits(unsigned long long v) {
+  unsigned lo = __builtin_amdgcn_readfirstlane((unsigned)v), hi = __builtin_amdgcn_readfirstlane((unsigned)(v >> 32));
+  asm volatile("" : "+s"(lo), "+s"(hi));
+  return ((unsigned long long)hi << 32) | lo;
+}
+// the thread index, opaque for the same reason
+__device__ __forceinline__ int opq_tid() {
+  int t = threadIdx.x;
+  asm volatile("" : "+v"(t));
+  return t;
+}
+template <class T>
+__device__ __forceinline__ gw<T> opq(T* p) {
+  return (gw<T>)opq_bits((unsigned long long)p);
+}
+template <class T>
+__device__ __forceinline__ gptr<T> opq(const T* p) {
+  return (gptr<T>)opq_bits((unsigned long long)p);
+}
+template <class T>
+__device__ __forceinline__ gptr<T> opq(gptr<T> p) {
+  return (gptr<T>)opq_bits((unsigned long long)p);
+}
+
+// loads of data another CU of this XCD wrote during the pass: miss the L1
+__device__ __forceinline__ u32x4 ld_x(const u32x4* p) { return __builtin_nontemporal_load(p); }
+__device__ __forceinline__ float ld_x(const float* p) { return __builtin_nontemporal_load(p); }
+__device__ __forceinline__ int ld_x(const int* p) { return __builtin_nontemporal_load(p); }
+__device__ __forceinline__ u32x4 ld_x(gptr<u32x4> p) { return __builtin_nontemporal_load(p); }
+__device__ __forceinline__ float ld_x(gptr<float> p) { return __builtin_nontemporal_load(p); }
+__device__ __forceinline__ int ld_x(gptr<int> p) { return __builtin_nontemporal_load(p); }
+// device-coherent accesses (data crossing XCDs)
+__device__ __forceinline__ float ld_dev(const float* p) {
+  return __hip_atomic_load((float*)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_dev(gptr<float> p) {
+  return __hip_atomic_load((gw<float>)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_dev(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ unsigned ld_flag(const unsigned* p) {
+  return __hip_atomic_load((unsigned*)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ bool tag_reached(unsigned v, unsigned tag) { return (int)(v - tag) >= 0; }
+
+// ------------------------------------------------------------------ waits and signals
+
+struct Wg {
+  int x, r, g;       // XCD, rank, x * 32 + r
+  unsigned E;        // this pass's number
+  unsigned tagbase;  // E * tags per pass
+  int* sh;           // LDS words shared by the workgroup
+};
+
+// the dependency of a stage: flags of stage id on XCD wx (-1: all XCDs) at
+// tag; on = false when there is none.  Stages load what does not depend on
+// it (weights, cached K/V) before they wait.
+struct WaitSpec {
+  int id, wx;
+  unsigned tag;
+  bool on;
+  int sl, sfid;  // layer and flag id of the caller's stage timestamps
+};
+
+__device__ __forceinline__ unsigned tag_of(const Wg& w, int l, int s) {
+  return w.tagbase + (unsigned)(l * kFStages + s) + 1u;
+}
+
+__device__ __forceinline__ void raise_abort(const FusedArgs& a, unsigned code) {
+  if (__hip_atomic_exchange(&a.ctl[FZ_ABORT], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0u) {
+    __hip_atomic_store(&a.ctl[FZ_WHY], code, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (a.err) __hip_atomic_fetch_add(a.err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+// Waits until the flags of stage s reach tag: the 32 of XCD xs, or all 256
+// when xs < 0.  Wave 0 polls; returns false (in every thread) on abort or
+// timeout.
+__device__ __forceinline__ bool wait_flags(const FusedArgs& a, const Wg& w, int s, int xs, unsigned tag) {
+  if (threadIdx.x < 64) {
+    const int lane = threadIdx.x;
+    const unsigned* f = a.flags + (size_t)s * kFGroups;
+    const unsigned long long t0 = now();
+    int ok = 0;
+    for (;;) {
+      bool mine;
+      if (xs < 0) {
+        const unsigned v0 = ld_flag(f + 4 * lane), v1 = ld_flag(f + 4 * lane + 1);
+        const unsigned v2 = ld_flag(f + 4 * lane + 2), v3 = ld_flag(f + 4 * lane + 3);
+        mine = tag_reached(v0, tag) && tag_reached(v1, tag) && tag_reached(v2, tag) && tag_reached(v3, tag);
+      } else {
+        mine = lane >= kFRanks || tag_reached(ld_flag(f + xs * kFRanks + lane), tag);
+      }
+      if (__all(mine)) {
+        ok = 1;
+        break;
+      }
+      if (ld_flag(&a.ctl[FZ_ABORT])) break;
+      if (now() - t0 > a.timeout) {
+        if (lane == 0) raise_abort(a, 0x100u + (unsigned)s);
+        break;
+      }
+      for (int z = 0; z < a.poll_sleep; ++z) __builtin_amdgcn_s_sleep(8);
+      __builtin_amdgcn_s_sleep(1);
+    }
+    if (lane == 0) w.sh[0] = ok;
+  }
+  __syncthreads();
+  const bool ok = w.sh[0] != 0;
+  __syncthreads();
+  return ok;
+}
+
+// Publishes stage s of layer l: every thread's stores complete, then one flag.
+__device__ __forceinline__ void signal(const FusedArgs& a, const Wg& w, int l, int s, bool cross_xcd) {
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    unsigned* f = a.flags + (size_t)s * kFGroups + w.g;
+    if (cross_xcd) __hip_atomic_store(f, tag_of(w, l, s), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    else __hip_atomic_store(f, tag_of(w, l, s), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  }
+}
+
+// progress word read by this workgroup's prefetcher: pass (low 16 bits) in
+// the high half, step in the low half (0xffff: done)
+__device__ __forceinline__ void progress(const FusedArgs& a, const Wg& w, int step) {
+  if (threadIdx.x == 0)
+    __hip_atomic_store(&a.prog[w.g], ((w.E & 0xffffu) << 16) | (unsigned)min(step, 0xffff), __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// stage timestamps (when the session traces): entry, dependency met, done
+__device__ __forceinline__ void stamp(const FusedArgs& a, const Wg& w, int l, int s, int k) {
+  if (a.trace && threadIdx.x == 0)
+    a.trace[(((size_t)w.g * (a.L + 1) + l) * kFStages + s) * 3 + k] = now();
+}
+
+// ------------------------------------------------------------------ per-layer parameters
+
+enum LwSlot { LW_QKV = 0, LW_O, LW_FC, LW_PR, LB_QKV, LB_O, LB_FC, LB_PR, LN1G, LN1B, LN2G, LN2B };
+
+
+__device__ __forceinline__ const void* lw(const FusedArgs& a, int l, int slot) { return a.lw[l * kLwSlots + slot]; }
+
+// ------------------------------------------------------------------ LayerNorm of one node row
+//
+// mode 0: x = wte[token] + wpe[position] (first layer);
+// mode 1: x += bias + part[X] for every XCD X that owns a share of the
+//         residual GEMM, in XCD order (device-coherent loads);
+// then a = (x - mean) / sqrt(var + eps) * g + b into this XCD's GEMM input.
+
+template <int E>
+__device__ __forceinline__ bool ln_row(const FusedArgs& a, const Wg& w, const WaitSpec& ws, int n, int mode,
+                                       gptr<uint16_t> bias, const float* part, const int* xrange, gptr<uint16_t> g,
+                                       gptr<uint16_t> b, uint16_t* act, float* red, bool dbg) {
+  const int d = a.d, tid = opq_tid();
+  const gw<float> xr = opq(a.xr + ((size_t)w.x * kFMaxN + n) * d);
+  bias = opq(bias);
+  g = opq(g);
+  b = opq(b);
+  const gptr<float> partg = opq(part);
+  const gw<uint16_t> actg = opq(act);
+  // every load is issued (clamped to the row, unconditionally) before any is
+  // used, so the row costs one memory round trip
+  unsigned kk[E];
+#pragma unroll
+  for (int i = 0; i < E; ++i) kk[i] = (unsigned)min(tid + i * NTH, d - 1);
+  uint16_t gr[E], br[E];
+#pragma unroll
+  for (int i = 0; i < E; ++i) {
+    gr[i] = g[kk[i]];
+    br[i] = b[kk[i]];
+  }
+  float v[E];
+  if (mode == 0) {
+    const int tok = ld_x(a.tree + n), pos = ld_x(a.tree + a.max_nodes + n);
+    const gptr<uint16_t> te = opq(a.wte) + (size_t)tok * d;
+    const gptr<uint16_t> pe = opq(a.wpe) + (size_t)pos * d;
+    uint16_t tr[E], pr[E];
+#pragma unroll
+    for (int i = 0; i < E; ++i) {
+      tr[i] = te[kk[i]];
+      pr[i] = pe[kk[i]];
+    }
+#pragma unroll
+    for (int i = 0; i < E; ++i) v[i] = bf2f(tr[i]) + bf2f(pr[i]);
+  } else {
+    float xv[E], pv[kFXcd][E];
+    uint16_t cr[E];
+#pragma unroll
+    for (int i = 0; i < E; ++i) {
+      xv[i] = xr[kk[i]];
+      cr[i] = bias[kk[i]];
+    }
+    // the partial residuals are what this stage waits for
+    if (ws.on && !wait_flags(a, w, ws.id, ws.wx, ws.tag)) return false;
+    stamp(a, w, ws.sl, ws.sfid, 1);
+#pragma unroll
+    for (int X = 0; X < kFXcd; ++X) {
+      const gptr<float> prow = partg + ((size_t)X * kFMaxN + n) * d;
+#pragma unroll
+      for (int i = 0; i < E; ++i) pv[X][i] = ld_dev(prow + kk[i]);
+    }
+    if (dbg && threadIdx.x == 0) {
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      a.trace[(((size_t)w.g * (a.L + 1) + a.dbg_l) * kFStages + FS_SPARE) * 3 + 0] = now();
+    }
+    // bias, then the partials of the XCDs that own a share, in XCD order
+#pragma unroll
+    for (int i = 0; i < E; ++i) {
+      float acc = bf2f(cr[i]);
+#pragma unroll
+      for (int X = 0; X < kFXcd; ++X) acc += xrange[2 * X + 1] > xrange[2 * X] ? pv[X][i] : 0.f;
+      v[i] = xv[i] + acc;
+    }
+  }
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < E; ++i) {
+    const int k = tid + i * NTH;
+    if (k < d) {
+      xr[k] = v[i];
+      s += v[i];
+    }
+  }
+  // block sums, fixed order
+  auto bsum = [&](float t) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) t += __shfl_xor(t, o);
+    __syncthreads();
+    if ((tid & 63) == 0) red[tid >> 6] = t;
+    __syncthreads();
+    return ((red[0] + red[1]) + (red[2] + red[3])) + ((red[4] + red[5]) + (red[6] + red[7]));
+  };
+  const float mean = bsum(s) / d;
+  float q = 0.f;
+#pragma unroll
+  for (int i = 0; i < E; ++i)
+    if (tid + i * NTH < d) q += (v[i] - mean) * (v[i] - mean);
+  const float den = sqrtf(bsum(q) / d + a.eps);
+  if (dbg && threadIdx.x == 0)
+    a.trace[(((size_t)w.g * (a.L + 1) + a.dbg_l) * kFStages + FS_SPARE) * 3 + 1] = now();
+#pragma unroll
+  for (int i = 0; i < E; ++i) {
+    const int k = tid + i * NTH;
+    if (k < d) st_act(actg, n, k, d / 32, (v[i] - mean) / den * bf2f(gr[i]) + bf2f(br[i]));
+  }
+  if (dbg && threadIdx.x == 0) {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    a.trace[(((size_t)w.g * (a.L + 1) + a.dbg_l) * kFStages + FS_SPARE) * 3 + 2] = now();
+  }
+  return true;
+}
+
+// ------------------------------------------------------------------ skinny GEMM of one task
+//
+// Y[n][o] = sum_k A[n][k] W[o][k] for the task's row blocks (up to RBM, any
+// order) over k-steps [kc0, kc1).  Wave w takes k-steps kc0 + w, kc0 + w + 4,
+// ..., U steps of loads in flight; per step it multiplies every row block's
+// weight fragment into every 16-node activation fragment on
+// v_mfma_f32_16x16x32_f16.  The four waves are summed in wave order through
+// LDS, one row block at a time, and the epilogue writes each output.
+
+enum FEpi { FE_QKV = 0, FE_WO, FE_FC, FE_WPR, FE_HEAD };
+
+__device__ __forceinline__ void epilogue(const FusedArgs& a, const Wg& w, int epi, int l, int n, int o, float v) {
+  const int d = a.d;
+  switch (epi) {
+    case FE_QKV:
+      if (o < d) {
+        a.q[(size_t)n * d + o] = v;
+      } else {
+        const int oo = o < 2 * d ? o - d : o - 2 * d;
+        const int h = oo / DH, e = oo - h * DH;
+        uint16_t* dst = o < 2 * d ? a.kt : a.vt;
+        dst[(((size_t)l * a.H + h) * a.max_nodes + n) * DH + e] = f2bf(v);
+      }
+      break;
+    case FE_WO: st_dev(a.part_o + ((size_t)w.x * kFMaxN + n) * d + o, v); break;
+    case FE_FC: st_act(a.ff, n, o, a.M / 32, gelu_tanh(v)); break;
+    case FE_WPR: st_dev(a.part_p + ((size_t)w.x * kFMaxN + n) * d + o, v); break;
+    default: a.logits[(size_t)n * a.V + o] = v; break;
+  }
+}
+
+// One GEMM task of RB row blocks: rbs[0 .. nrb) (plan entries) or, with rbs
+// null, nrb consecutive ones from rb_first; row blocks past nrb repeat the
+// last one and are not stored.
+template <int NT, int RB, int U>
+__device__ __forceinline__ bool gemm_rb(const FusedArgs& a, const Wg& w, const WaitSpec& ws, int epi, int l,
+                                        const int* rbs, int rb_first, int nrb, gptr<uint16_t> bias, gptr<u32x4> Wp,
+                                        int KC, int M, int kc0, int kc1, const uint16_t* act, int act_kc,
+                                        float* red) {
+  constexpr int NN = 16 * NT;
+  const int tid = opq_tid(), wv = tid >> 6, lane = tid & 63;
+  const int nsteps = kc1 - kc0 > wv ? (kc1 - kc0 - wv + NWV - 1) / NWV : 0;
+  Wp = opq(Wp);
+  const gptr<uint16_t> actg = opq(act);
+  bias = opq(bias);
+  int rbv[RB];
+#pragma unroll
+  for (int r = 0; r < RB; ++r) {
+    const int rr = min(r, nrb - 1);
+    rbv[r] = rbs ? rbs[rr] : rb_first + rr;
+  }
+  // this thread's epilogue row of every row block is tid % 16: its bias is
+  // loaded before the k-loop
+  float bias_r[RB];
+  {
+    uint16_t raw[RB];
+#pragma unroll
+    for (int r = 0; r < RB; ++r) raw[r] = bias ? bias[rbv[r] * 16 + (tid & 15)] : (uint16_t)0;
+#pragma unroll
+    for (int r = 0; r < RB; ++r) bias_r[r] = bf2f(raw[r]);
+  }
+  gptr<u32x4> wb[RB];
+#pragma unroll
+  for (int r = 0; r < RB; ++r) wb[r] = Wp + (size_t)rbv[r] * KC * 64 + lane;
+  const gptr<u32x4> ab = (gptr<u32x4>)actg + lane;
+  u32x4 wq[U][RB];
+  u32x4 bq[U][NT];
+  const int klast = kc1 - 1;
+  auto load_w = [&](int s, int u) {
+    const int kc = min(kc0 + wv + NWV * s, klast);
+#pragma unroll
+    for (int r = 0; r < RB; ++r) wq[u][r] = wb[r][(size_t)kc * 64];
+  };
+  auto load_a = [&](int s, int u) {
+    const int kc = min(kc0 + wv + NWV * s, klast);
+#pragma unroll
+    for (int t = 0; t < NT; ++t) bq[u][t] = ld_x(ab + ((size_t)t * act_kc + kc) * 64);
+  };
+  auto load_step = [&](int s, int u) {
+    load_w(s, u);
+    load_a(s, u);
+  };
+  f32x4 acc[RB][NT];
+#pragma unroll
+  for (int r = 0; r < RB; ++r)
+#pragma unroll
+    for (int t = 0; t < NT; ++t) acc[r][t] = (f32x4){0.f, 0.f, 0.f, 0.f};
+  // the first U steps' weights do not depend on the previous stage: they are
+  // in flight while the workgroup waits for it
+  if (nsteps > 0) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) load_w(u, u);
+  }
+  if (ws.on && !wait_flags(a, w, ws.id, ws.wx, ws.tag)) return false;
+  stamp(a, w, ws.sl, ws.sfid, 1);
+  if (nsteps > 0) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) load_a(u, u);
+    __builtin_amdgcn_sched_barrier(0);
+    for (int s0 = 0; s0 < nsteps; s0 += U) {
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const bool ok = s0 + u < nsteps;
+#pragma unroll
+        for (int r = 0; r < RB; ++r) {
+          const u32x4 wf = ok ? wq[u][r] : (u32x4){0, 0, 0, 0};
+#pragma unroll
+          for (int t = 0; t < NT; ++t)
+            acc[r][t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, wf),
+                                                               __builtin_bit_cast(f16x8, bq[u][t]), acc[r][t], 0, 0, 0);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        load_step(s0 + u + U, u);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+  }
+  const int N = a.N;
+#pragma unroll
+  for (int r = 0; r < RB; ++r) {
+    if (r >= nrb) break;
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) red[((wv * NN) + 16 * t + (lane & 15)) * 16 + 4 * (lane >> 4) + q] = acc[r][t][q];
+    __syncthreads();
+    for (int idx = tid; idx < NN * 16; idx += NTH) {
+      const int row = idx & 15, node = idx >> 4;
+      float sum = red[idx];
+#pragma unroll
+      for (int ww = 1; ww < NWV; ++ww) sum += red[ww * NN * 16 + idx];
+      const int o = rbv[r] * 16 + row;
+      if (node < N && o < M) epilogue(a, w, epi, l, node, o, sum + bias_r[r]);
+    }
+    __syncthreads();
+  }
+  return true;
+}
+
+// one task of 1..4 row blocks, loads in flight per wave sized to the
+// register budget; three code bodies serve every stage
+template <int NT>
+__device__ __forceinline__ bool gemm_task(const FusedArgs& a, const Wg& w, const WaitSpec& ws, int epi, int l,
+                                          const int* rbs, int rb_first, int nrb, gptr<uint16_t> bias,
+                                          gptr<u32x4> Wp, int KC, int M, int kc0, int kc1, const uint16_t* act,
+                                          int act_kc, float* red) {
+  if (nrb == 1)
+    return gemm_rb<NT, 1, NT <= 2 ? 8 : 6>(a, w, ws, epi, l, rbs, rb_first, 1, bias, Wp, KC, M, kc0, kc1, act, act_kc,
+                                          red);
+  if (nrb == 2)
+    return gemm_rb<NT, 2, NT <= 2 ? 6 : 5>(a, w, ws, epi, l, rbs, rb_first, 2, bias, Wp, KC, M, kc0, kc1, act, act_kc,
+                                          red);
+  return gemm_rb<NT, 4, 4>(a, w, ws, epi, l, rbs, rb_first, nrb, bias, Wp, KC, M, kc0, kc1, act, act_kc, red);
+}
+
+// ------------------------------------------------------------------ tree attention, one head x 16-node tile
+//
+// Node i attends to cache rows 0..P-1 and then to its root path in the tree
+// scratch (Sec. 3.1: cross-attention with the cache, self-attention in the
+// batch masked by the tree).  The prefix is staged 128 rows at a time (K rows
+// and V^T in LDS); wave w takes rows 32w..32w+31 of every chunk on the matrix
+// cores (S^T = K Q^T, O^T = V^T P^T with v_mfma_f32_16x16x32_bf16; q and p as
+// bf16 hi + lo, K and V exact) with its own online softmax.  The K operand's
+// rows are ordered so that lane l holds the scores of keys 8(l/16)..+7 of node
+// l%16, which is exactly its slot of the P^T operand.  Each half-wave then
+// takes a node's root path on the vector ALU (root first, 32 keys per batch).
+// The four prefix parts and the root-path part are merged in that order.
+
+constexpr int ACH = 32 * NWV;               // prefix rows per chunk: 32 per wave
+constexpr int AKS = DH + 8;                 // LDS row stride of K (elements)
+constexpr int AVS = AKS;                    // LDS row stride of V (row-major like K)
+constexpr int AREC = DH + 4;                // part record: max, sum, -, -, output
+constexpr int A_KV_BYTES = 2 * ACH * AKS * 2;
+constexpr int A_RV_BYTES = 2 * NWV * 32 * DH * 2;                 // root-path V rows, 32 per half-wave
+constexpr int A_REGION = A_KV_BYTES > A_RV_BYTES ? A_KV_BYTES : A_RV_BYTES;
+constexpr int A_PART_BYTES = (NWV * 16 + 16) * AREC * 4;
+constexpr int A_Q_BYTES = NWV * 2 * DH * 4;
+
+__device__ __forceinline__ bool attention_task(const FusedArgs& a, const Wg& w, const WaitSpec& ws, int l, int h, int t,
+                                               unsigned char* lds, bool dbg) {
+  uint16_t* ks = (uint16_t*)lds;
+  uint16_t* vs = ks + ACH * AKS;
+  float* wpart = (float*)(lds + A_REGION);  // [NWV][16][AREC]
+  float* rpart = wpart + NWV * 16 * AREC;   // [16][AREC]
+  float* qrow = rpart + 16 * AREC;          // [NWV][2][DH]
+  const int tid = opq_tid(), wv = tid >> 6, lane = tid & 63, i = lane & 15, g = lane >> 4;
+  const int N = a.N, P = a.P, d = a.d;
+  const float scale = a.scale;
+  const size_t head_rows = ((size_t)l * a.H + h);
+  const gptr<uint16_t> kc = opq(a.kc + head_rows * a.max_ctx * DH);
+  const gptr<uint16_t> vc = opq(a.vc + head_rows * a.max_ctx * DH);
+  const gptr<float> qbase = opq((const float*)a.q);
+  const gptr<int> tree = opq(a.tree);
+  constexpr int DPL = DH / 32;  // root path: dims per lane of a half-wave
+  const int hw = lane >> 5, hl = lane & 31;
+
+  // 1. What does not depend on this layer's QKV outputs: the cached prefix
+  //    (first two chunks, two register sets) and the root-path indices of
+  //    this half-wave's node.
+  const int nchunks = (P + ACH - 1) / ACH;
+  u32x4 kA[4], vA[4], kB[4], vB[4];
+  auto load_chunk = [&](int c, u32x4(&kr)[4], u32x4(&vr)[4]) {
+    const int cb = c * ACH, ck = min(ACH, P - cb);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int e = tid + j * NTH, r = min(e >> 3, ck - 1), c8 = e & 7;
+      kr[j] = *(gptr<u32x4>)(kc + (size_t)(cb + r) * DH + 8 * c8);
+      vr[j] = *(gptr<u32x4>)(vc + (size_t)(cb + r) * DH + 8 * c8);
+    }
+  };
+  if (nchunks > 0) load_chunk(0, kA, vA);
+  if (nchunks > 1) load_chunk(1, kB, vB);
+  const gptr<int> depth = tree + 2 * a.max_nodes;
+  const gptr<int> anc_off = tree + 4 * a.max_nodes;
+  const gptr<int> path32 = tree + 5 * a.max_nodes;
+  const gptr<int> ancl = path32 + (size_t)N * kPath32;
+  const int rnl = 2 * wv + hw;  // this half-wave's node within the tile
+  const int rnc = min(16 * t + rnl, N - 1);
+  int rkey = ld_x(path32 + (size_t)rnc * kPath32 + hl);
+  const int rdep = ld_x(depth + rnc);
+
+  // 2. The dependency.
+  if (ws.on && !wait_flags(a, w, ws.id, ws.wx, ws.tag)) return false;
+  stamp(a, w, ws.sl, ws.sfid, 1);
+
+  // 3. Queries (B operand: node 16 t + i, dims 32 kc2 + 8 g .. +8) and the
+  //    first 32 root-path K/V rows.
+  const int qn = min(16 * t + i, N - 1);
+  u32x4 qh[2], ql[2];
+#pragma unroll
+  for (int kc2 = 0; kc2 < 2; ++kc2) {
+    const gptr<float> qp = qbase + (size_t)qn * d + h * DH + 32 * kc2 + 8 * g;
+    const u32x4 q0 = ld_x((gptr<u32x4>)qp), q1 = ld_x((gptr<u32x4>)(qp + 4));
+    const float v[8] = {__uint_as_float(q0[0]), __uint_as_float(q0[1]), __uint_as_float(q0[2]),
+                        __uint_as_float(q0[3]), __uint_as_float(q1[0]), __uint_as_float(q1[1]),
+                        __uint_as_float(q1[2]), __uint_as_float(q1[3])};
+    pack_hilo8(v, qh[kc2], ql[kc2]);
+  }
+  const gptr<uint16_t> ktb = opq((const uint16_t*)a.kt + head_rows * a.max_nodes * DH);
+  const gptr<uint16_t> vtb = opq((const uint16_t*)a.vt + head_rows * a.max_nodes * DH);
+  u32x4 rk[DH / 8], rv[DH / 8];
+  // issued once the last prefix chunk is staged, so that no chunk waits for them
+  auto load_root = [&]() {
+#pragma unroll
+    for (int j = 0; j < DH / 8; ++j) {
+      rk[j] = ld_x((gptr<u32x4>)(ktb + (size_t)rkey * DH + 8 * j));
+      rv[j] = ld_x((gptr<u32x4>)(vtb + (size_t)rkey * DH + 8 * j));
+    }
+  };
+  if (nchunks == 0) load_root();
+
+  // 4. Prefix chunks, two in flight: chunk c + 2 is loaded into the
+  //    registers chunk c has just left.
+  float m = -INFINITY, lsum = 0.f;
+  f32x4 o[4];
+#pragma unroll
+  for (int tt = 0; tt < 4; ++tt) o[tt] = (f32x4){0.f, 0.f, 0.f, 0.f};
+  auto run_chunk = [&](int c, u32x4(&kr)[4], u32x4(&vr)[4]) {
+    const int nk = min(ACH, P - c * ACH);
+    __syncthreads();  // the previous chunk has been read
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int e = tid + j * NTH, r = e >> 3, c8 = e & 7;
+      const bool ok = r < nk;
+      *(u32x4*)(ks + r * AKS + 8 * c8) = ok ? kr[j] : (u32x4){0, 0, 0, 0};
+      *(u32x4*)(vs + r * AVS + 8 * c8) = ok ? vr[j] : (u32x4){0, 0, 0, 0};
+    }
+    if (c + 2 < nchunks) load_chunk(c + 2, kr, vr);
+    if (c == nchunks - 1) load_root();
+    __syncthreads();
+    if (32 * wv < nk) {
+      const uint16_t* kb = ks + (32 * wv + 8 * (i >> 2) + (i & 3)) * AKS + 8 * g;
+      f32x4 s0 = (f32x4){0, 0, 0, 0}, s1 = (f32x4){0, 0, 0, 0};
+#pragma unroll
+      for (int kc2 = 0; kc2 < 2; ++kc2) {
+        const u32x4 k0 = *(const u32x4*)(kb + 32 * kc2);
+        const u32x4 k1 = *(const u32x4*)(kb + 4 * AKS + 32 * kc2);
+        s0 = mfma_bf16(k0, qh[kc2], s0);
+        s0 = mfma_bf16(k0, ql[kc2], s0);
+        s1 = mfma_bf16(k1, qh[kc2], s1);
+        s1 = mfma_bf16(k1, ql[kc2], s1);
+      }
+      float sv[8];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int key = 32 * wv + 8 * g + r;
+        sv[r] = key < nk ? s0[r] * scale : -INFINITY;
+        sv[4 + r] = key + 4 < nk ? s1[r] * scale : -INFINITY;
+      }
+      float mb = sv[0];
+#pragma unroll
+      for (int e = 1; e < 8; ++e) mb = fmaxf(mb, sv[e]);
+      mb = fmaxf(mb, __shfl_xor(mb, 16));
+      mb = fmaxf(mb, __shfl_xor(mb, 32));
+      const float mn = fmaxf(m, mb);
+      const float alpha = __expf(m - mn);
+      float pv[8], ps = 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        pv[e] = __expf(sv[e] - mn);
+        ps += pv[e];
+      }
+      ps += __shfl_xor(ps, 16);
+      ps += __shfl_xor(ps, 32);
+      lsum = fmaf(lsum, alpha, ps);
+      m = mn;
+      u32x4 ph, pl;
+      pack_hilo8(pv, ph, pl);
+#pragma unroll
+      for (int tt = 0; tt < 4; ++tt) {
+        // A operand V^T (16 dims x 32 keys): lane (i, g) gathers dim 16 tt + i
+        // of keys 8 g .. 8 g + 7 of this wave's 32 from the row-major rows
+        const uint16_t* vcol = vs + (32 * wv + 8 * g) * AVS + 16 * tt + i;
+        uint32_t h[8];
+#pragma unroll
+        for (int jj = 0; jj < 8; ++jj) h[jj] = vcol[jj * AVS];
+        const u32x4 va = (u32x4){h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
+        o[tt] = o[tt] * alpha;
+        o[tt] = mfma_bf16(va, ph, o[tt]);
+        o[tt] = mfma_bf16(va, pl, o[tt]);
+      }
+    }
+  };
+  for (int c = 0; c < nchunks; c += 2) {
+    run_chunk(c, kA, vA);
+    if (c + 1 < nchunks) run_chunk(c + 1, kB, vB);
+  }
+  if (dbg && threadIdx.x == 0) a.trace[(((size_t)w.g * (a.L + 1) + a.dbg_l + 1) * kFStages + FS_SPARE) * 3 + 0] = now();
+  // this wave's prefix part of node 16 t + i: lane (i, g) holds dims 16 tt + 4 g + r
+  {
+    float* rec = wpart + (wv * 16 + i) * AREC;
+    if (g == 0) {
+      rec[0] = m;
+      rec[1] = lsum;
+    }
+#pragma unroll
+    for (int tt = 0; tt < 4; ++tt) *(f32x4*)(rec + 4 + 16 * tt + 4 * g) = o[tt];
+  }
+  __syncthreads();  // K/V staging region is reused for root-path V rows
+
+  // 5. Root path: half-wave (wv, hw) takes node 2 wv + hw of the tile on the
+  //    vector ALU, root first, 32 keys per batch.
+  {
+    uint16_t* rvl = (uint16_t*)lds + (2 * wv + hw) * 32 * DH;  // [32 keys][DH]
+    float* qr = qrow + (wv * 2 + hw) * DH;
+    {
+      const int nl = rnl;
+      const int n = 16 * t + nl;
+      {
+        const gptr<float> qp = qbase + (size_t)rnc * d + h * DH + hl * DPL;
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) qr[hl * DPL + e] = ld_x(qp + e);
+      }
+      float rm = -INFINITY, rl = 0.f, ro[DPL];
+#pragma unroll
+      for (int e = 0; e < DPL; ++e) ro[e] = 0.f;
+      const int rbatches = (max(rdep, __shfl_xor(rdep, 32)) + 32) / 32;  // wave-uniform
+      for (int bt = 0; bt < rbatches; ++bt) {
+        const int j = 32 * bt + hl;
+        if (bt > 0) {
+          rkey = ld_x(ancl + ld_x(anc_off + rnc) + min(j, rdep));
+#pragma unroll
+          for (int jj = 0; jj < DH / 8; ++jj) {
+            rk[jj] = ld_x((gptr<u32x4>)(ktb + (size_t)rkey * DH + 8 * jj));
+            rv[jj] = ld_x((gptr<u32x4>)(vtb + (size_t)rkey * DH + 8 * jj));
+          }
+        }
+#pragma unroll
+        for (int jj = 0; jj < DH / 8; ++jj) *(u32x4*)(rvl + hl * DH + 8 * jj) = rv[jj];
+        wave_sync_lds();
+        float dot = 0.f;
+#pragma unroll
+        for (int c8 = 0; c8 < DH / 8; ++c8) {
+          const f32x4 qa = *(const f32x4*)&qr[8 * c8];
+          const f32x4 qb = *(const f32x4*)&qr[8 * c8 + 4];
+          const u32x4 ku = rk[c8];
+          dot = fmaf(qa[0], __uint_as_float(ku[0] << 16), dot);
+          dot = fmaf(qa[1], __uint_as_float(ku[0] & 0xffff0000u), dot);
+          dot = fmaf(qa[2], __uint_as_float(ku[1] << 16), dot);
+          dot = fmaf(qa[3], __uint_as_float(ku[1] & 0xffff0000u), dot);
+          dot = fmaf(qb[0], __uint_as_float(ku[2] << 16), dot);
+          dot = fmaf(qb[1], __uint_as_float(ku[2] & 0xffff0000u), dot);
+          dot = fmaf(qb[2], __uint_as_float(ku[3] << 16), dot);
+          dot = fmaf(qb[3], __uint_as_float(ku[3] & 0xffff0000u), dot);
+        }
+        const bool kvalid = j <= rdep;
+        const float sc = kvalid ? dot * scale : -INFINITY;
+        float mb = sc;
+#pragma unroll
+        for (int off = 1; off < 32; off <<= 1) mb = fmaxf(mb, __shfl_xor(mb, off));
+        const float mn = fmaxf(rm, mb);
+        const float alpha = __expf(rm - mn);
+        const float p = kvalid ? __expf(sc - mn) : 0.f;
+        float ps = p;
+#pragma unroll
+        for (int off = 1; off < 32; off <<= 1) ps += __shfl_xor(ps, off);
+        rl = fmaf(rl, alpha, ps);
+        rm = mn;
+        const int cnt = min(32, rdep + 1 - 32 * bt);
+        const int cmax = max(cnt, __shfl_xor(cnt, 32));  // wave-uniform
+        float acc[DPL];
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) acc[e] = 0.f;
+        for (int jj = 0; jj < cmax; ++jj) {
+          const float pj = jj < cnt ? __shfl(p, (hw << 5) + jj) : 0.f;
+          const uint16_t* vr2 = rvl + jj * DH + DPL * hl;
+#pragma unroll
+          for (int e = 0; e < DPL; ++e) acc[e] = fmaf(pj, bf2f(vr2[e]), acc[e]);
+        }
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) ro[e] = fmaf(ro[e], alpha, acc[e]);
+        wave_sync_lds();
+      }
+      float* rec = rpart + nl * AREC;
+      if (hl == 0) {
+        rec[0] = rm;
+        rec[1] = rl;
+      }
+#pragma unroll
+      for (int e = 0; e < DPL; ++e) rec[4 + DPL * hl + e] = ro[e];
+    }
+  }
+  __syncthreads();
+  if (dbg && threadIdx.x == 0) a.trace[(((size_t)w.g * (a.L + 1) + a.dbg_l + 1) * kFStages + FS_SPARE) * 3 + 1] = now();
+  // merge: thread -> node, DPT consecutive dims; the wave parts in wave order, then the root path
+  {
+    constexpr int DPT = 16 * DH / NTH;  // output dims per thread
+    const int nl = tid / (DH / DPT), d0 = DPT * (tid % (DH / DPT));
+    const int n = 16 * t + nl;
+    float M = -INFINITY, L = 0.f, O[DPT];
+#pragma unroll
+    for (int e = 0; e < DPT; ++e) O[e] = 0.f;
+    for (int j = 0; j <= NWV; ++j) {
+      const float* rec = j < NWV ? wpart + (j * 16 + nl) * AREC : rpart + nl * AREC;
+      const float mj = rec[0], lj = rec[1];
+      if (mj == -INFINITY) continue;
+      const float mn = fmaxf(M, mj);
+      const float al = __expf(M - mn), wj = __expf(mj - mn);
+      L = fmaf(L, al, lj * wj);
+#pragma unroll
+      for (int e = 0; e < DPT; ++e) O[e] = fmaf(O[e], al, rec[4 + d0 + e] * wj);
+      M = mn;
+    }
+    if (n < N) {
+#pragma unroll
+      for (int e = 0; e < DPT; ++e) st_act(a.fo, n, h * DH + d0 + e, d / 32, O[e] / L);
+    }
+  }
+  __syncthreads();
+  return true;
+}
+
+// ------------------------------------------------------------------ the plan of one workgroup
+//
+// int32 [kPlanStride] per workgroup (see FusedPlan in ssd_internal.h):
+//   ATT: count, then head | tile << 16
+//   QKV, WO, FC, WPR: count, then row blocks
+//   HEAD: first row block, end row block of the LM head
+
+// ------------------------------------------------------------------ compute workgroups
+
+template <int NT>
+__device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* lds) {
+  int* sh = (int*)(lds + A_REGION + A_PART_BYTES + A_Q_BYTES);  // 16 words
+  float* red = (float*)lds;                                        // GEMM / LN reductions
+  Wg w;
+  w.x = (int)xcc_id();
+  w.r = blockIdx.x >> 3;
+  w.g = w.x * kFRanks + w.r;
+  w.sh = sh;
+  if (threadIdx.x == 0) {
+    const unsigned E = __hip_atomic_load(&a.ctl[FZ_PASS], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1u;
+    sh[1] = (int)E;
+    // (x, r) must name one workgroup of 8 XCDs: a second claim in the same pass aborts
+    int ok = w.x < kFXcd;
+    if (ok) ok = __hip_atomic_exchange(&a.ctl[FZ_CLAIM + w.g], E, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != E;
+    if (!ok) raise_abort(a, 1u);
+    sh[3] = ok;
+  }
+  __syncthreads();
+  w.E = (unsigned)sh[1];
+  w.tagbase = w.E * kFTagsPerPass;
+  const bool placed = sh[3] != 0;
+  __syncthreads();
+  if (!placed) {
+    // not a valid (XCD, rank): count as finished, touch nothing else
+    if (threadIdx.x == 0) {
+      const unsigned prev = __hip_atomic_fetch_add(&a.ctl[FZ_DONE], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (prev == kFGroups - 1) {
+        __hip_atomic_store(&a.ctl[FZ_DONE], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(&a.ctl[FZ_ABORT], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(&a.ctl[FZ_PASS], w.E, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
+    return;
+  }
+
+  const int* p = a.plan + (size_t)w.g * kPlanStride;
+  const int n_att = p[PL_ATT], n_qkv = p[PL_QKV], n_wo = p[PL_WO], n_fc = p[PL_FC], n_wpr = p[PL_WPR];
+  const int hb0 = p[PL_HEAD], hb1 = p[PL_HEAD + 1];
+  const int d = a.d, M = a.M, KCd = d / 32, KCm = M / 32;
+  const int kh0 = 2 * a.xh[2 * w.x], kh1 = 2 * a.xh[2 * w.x + 1];  // the XCD's heads, in k-steps of W_o
+  const int kf0 = a.xf[2 * w.x], kf1 = a.xf[2 * w.x + 1];           // hidden slice, in k-steps of W_pr
+  uint16_t* act1 = a.act1 + (size_t)w.x * a.act_stride;
+  uint16_t* act2 = a.act2 + (size_t)w.x * a.act_stride;
+  const int N = a.N, L = a.L;
+  constexpr int E = 4;  // LayerNorm elements per thread: d <= 2048
+
+  // One runtime loop over the pass's stages, so that each stage body (the
+  // LayerNorm, the GEMM at 1, 2 and 4 row blocks, the attention) exists once
+  // in the code: the whole kernel stays small enough for the instruction
+  // cache, which a layer-by-layer unrolled body does not.
+  //   kind 0..6: LN1, QKV, ATT, WO, LN2, FC, WPR of layer l; 7: final
+  //   LayerNorm; 8: LM head.
+  const int nst = L * 7 + 2;
+  for (int st = 0; st < nst; ++st) {
+    const int l = st < L * 7 ? st / 7 : L;
+    const int kind = st < L * 7 ? st % 7 : 7 + (st - L * 7);
+    // flag id, waited flag id / layer / XCD (-1 all, -2 none), work present
+    int fid, wid = 0, wl = l, wx = w.x, work;
+    switch (kind) {
+      case 0: fid = FS_LN1; wid = FS_WPR; wl = l - 1; wx = l > 0 ? -1 : -2; work = w.r < N; break;
+      case 1: fid = FS_QKV; wid = FS_LN1; work = n_qkv > 0; break;
+      case 2: fid = FS_ATT; wid = FS_QKV; work = n_att > 0; break;
+      case 3: fid = FS_WO; wid = FS_ATT; work = n_wo > 0; break;
+      case 4: fid = FS_LN2; wid = FS_WO; wx = -1; work = w.r < N; break;
+      case 5: fid = FS_FC; wid = FS_LN2; work = n_fc > 0; break;
+      case 6: fid = FS_WPR; wid = FS_FC; work = n_wpr > 0; break;
+      case 7: fid = FS_LN1; wid = FS_WPR; wl = L - 1; wx = -1; work = w.r < N; break;
+      default: fid = FS_QKV; wid = FS_LN1; work = hb1 > hb0; break;
+    }
+    progress(a, w, kind < 7 ? l * kFStages + fid : L * kFStages + (kind == 7 ? 0 : 1));
+    stamp(a, w, l, fid, 0);
+    if (work) {
+      // each body loads what does not depend on the previous stage, then waits
+      const WaitSpec ws{wid, wx, tag_of(w, wl, wid), wx != -2, l, fid};
+      const WaitSpec none{0, 0, 0u, false, l, fid};
+      if (kind == 0 || kind == 4 || kind == 7) {
+        // residual update + LayerNorm of this workgroup's node rows
+        const int mode = (kind == 0 && l == 0) ? 0 : 1;
+        gptr<uint16_t> bias, g, b;
+        const float* part;
+        const int* xrange;
+        uint16_t* act;
+        if (kind == 4) {
+          bias = G<uint16_t>(lw(a, l, LB_O));
+          part = a.part_o;
+          xrange = a.xh;
+          g = G<uint16_t>(lw(a, l, LN2G));
+          b = G<uint16_t>(lw(a, l, LN2B));
+          act = act2;
+        } else {
+          const int lp = kind == 7 ? L - 1 : max(l - 1, 0);
+          bias = G<uint16_t>(lw(a, lp, LB_PR));
+          part = a.part_p;
+          xrange = a.xf;
+          g = kind == 7 ? G<uint16_t>(a.lnf_g) : G<uint16_t>(lw(a, l, LN1G));
+          b = kind == 7 ? G<uint16_t>(a.lnf_b) : G<uint16_t>(lw(a, l, LN1B));
+          act = act1;
+        }
+        const bool dbg = a.trace && (a.dbg & 1) && kind == 0 && l == a.dbg_l;
+        for (int n = w.r; n < N; n += kFRanks)
+          if (!ln_row<E>(a, w, n == w.r ? ws : none, n, mode, bias, part, xrange, g, b, act, red, dbg)) goto out;
+      } else if (kind == 2) {
+        for (int j = 0; j < n_att; ++j) {
+          const int e = p[PL_ATT + 1 + j];
+          if (!attention_task(a, w, j == 0 ? ws : none, l, e & 0xffff, e >> 16, lds,
+                              a.trace && (a.dbg & 1) && l == a.dbg_l && j == 0))
+            goto out;
+        }
+      } else if (kind == 8) {
+        for (int b0 = hb0, j = 0; b0 < hb1; b0 += 4, ++j) {
+          progress(a, w, L * kFStages + 1 + j / 2);
+          if (!gemm_task<NT>(a, w, b0 == hb0 ? ws : none, FE_HEAD, L, nullptr, b0, min(4, hb1 - b0),
+                             G<uint16_t>(nullptr), G<u32x4>(a.p_head), KCd, a.V, 0, KCd, act1, KCd, red))
+            goto out;
+        }
+      } else {
+        // the weight GEMMs of a layer
+        int epi, nrb, slot, KC, Mo, k0, k1, akc;
+        gptr<uint16_t> bias = G<uint16_t>(nullptr);
+        const uint16_t* act;
+        switch (kind) {
+          case 1: epi = FE_QKV; nrb = n_qkv; slot = PL_QKV; KC = KCd; Mo = 3 * d; k0 = 0; k1 = KCd; akc = KCd;
+                  bias = G<uint16_t>(lw(a, l, LB_QKV)); act = act1; break;
+          case 3: epi = FE_WO; nrb = n_wo; slot = PL_WO; KC = KCd; Mo = d; k0 = kh0; k1 = kh1; akc = KCd;
+                  act = a.fo; break;
+          case 5: epi = FE_FC; nrb = n_fc; slot = PL_FC; KC = KCd; Mo = M; k0 = 0; k1 = KCd; akc = KCd;
+                  bias = G<uint16_t>(lw(a, l, LB_FC)); act = act2; break;
+          default: epi = FE_WPR; nrb = n_wpr; slot = PL_WPR; KC = KCm; Mo = d; k0 = kf0; k1 = kf1; akc = KCm;
+                   act = a.ff; break;
+        }
+        const int wslot = kind == 1 ? LW_QKV : kind == 3 ? LW_O : kind == 5 ? LW_FC : LW_PR;
+        if (!gemm_task<NT>(a, w, ws, epi, l, p + slot + 1, 0, nrb, bias, G<u32x4>(lw(a, l, wslot)), KC, Mo, k0, k1,
+                           act, akc, red))
+          goto out;
+      }
+    }
+    signal(a, w, l, fid, kind == 3 || kind == 6);
+    stamp(a, w, l, fid, 2);
+  }
+out:
+  __syncthreads();
+  progress(a, w, 0xffff);  // done
+  if (threadIdx.x == 0) {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    const unsigned prev = __hip_atomic_fetch_add(&a.ctl[FZ_DONE], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (prev == kFGroups - 1) {
+      __hip_atomic_store(&a.ctl[FZ_DONE], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(&a.ctl[FZ_ABORT], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(&a.ctl[FZ_PASS], w.E, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+}
+
+// ------------------------------------------------------------------ prefetch workgroups
+//
+// Block 256 + b follows compute workgroup (its XCD, b / 8).  Before that
+// workgroup starts stage k it loads the weights of stage k + ahead (its row
+// blocks and k-ranges; the cached K/V of its attention heads) into the XCD's
+// L2.  Loads are folded into one value that is stored only if it equals a
+// magic word, so they are kept.  Stops when the compute workgroup reports
+// done, on abort, or after the timeout.
+
+struct Range {
+  const unsigned char* p;
+  size_t bytes;
+};
+
+__device__ __forceinline__ unsigned touch(const Range& rg, unsigned acc) {
+  typedef const __attribute__((address_space(1))) u32x4* gptr;
+  const gptr base = (gptr)rg.p;
+  const size_t n16 = rg.bytes / 16;
+  constexpr int D = 8;
+  for (size_t i0 = threadIdx.x; i0 < n16; i0 += (size_t)NTH * D) {
+    u32x4 v[D];
+#pragma unroll
+    for (int u = 0; u < D; ++u) v[u] = base[min(i0 + (size_t)u * NTH, n16 - 1)];
+#pragma unroll
+    for (int u = 0; u < D; ++u) acc ^= v[u][0] ^ v[u][3];
+  }
+  return acc;
+}
+
+template <int NT>
+__device__ __forceinline__ void prefetch_wg(const FusedArgs& a, unsigned char* lds) {
+  int* sh = (int*)(lds + A_REGION + A_PART_BYTES + A_Q_BYTES);
+  const int x = (int)xcc_id(), r = (blockIdx.x - kFGroups) >> 3;
+  if (x >= kFXcd || r >= kFRanks) return;
+  const int g = x * kFRanks + r;
+  const int* plan = a.plan + (size_t)g * kPlanStride;
+  const unsigned E = __hip_atomic_load(&a.ctl[FZ_PASS], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1u;
+  const unsigned long long t0 = now();
+  const int d = a.d, KCd = d / 32, KCm = a.M / 32;
+  const int kh0 = 2 * a.xh[2 * x], kh1 = 2 * a.xh[2 * x + 1];
+  const int kf0 = a.xf[2 * x], kf1 = a.xf[2 * x + 1];
+  unsigned acc = 0;
+  const int L = a.L;
+  constexpr int HRB = 8;  // the compute workgroup reports LM-head progress per 8 row blocks
+  const int hb0 = plan[PL_HEAD], hb1 = plan[PL_HEAD + 1];
+  const int nhead = (hb1 - hb0 + HRB - 1) / HRB;
+  const int nsteps = L * kFStages + 1 + nhead;
+  unsigned last = 0xffffffffu;
+  unsigned long long tl = now();
+  for (int step = 0; step < nsteps; ++step) {
+    const int l = step / kFStages, s = step % kFStages;
+    if (step < L * kFStages) {
+      if (s != FS_QKV && s != FS_ATT && s != FS_WO && s != FS_FC && s != FS_WPR) continue;
+    } else if (step == L * kFStages) {
+      continue;  // final LayerNorm: no weights
+    }
+    // wait until the compute workgroup has reached step - ahead in this pass
+    if (threadIdx.x == 0) {
+      int go = 0;
+      for (;;) {
+        const unsigned pv = __hip_atomic_load(&a.prog[g], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if ((pv >> 16) == (E & 0xffffu)) {
+          const int cur = (int)(pv & 0xffffu);
+          if (cur == 0xffff) break;  // done
+          if (cur + a.ahead >= step) {
+            go = 1;
+            break;
+          }
+        }
+        if (pv != last) {
+          last = pv;
+          tl = now();
+        }
+        if (__hip_atomic_load(&a.ctl[FZ_ABORT], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) break;
+        if (now() - tl > a.pf_idle || now() - t0 > a.timeout) break;  // prefetch is optional
+        __builtin_amdgcn_s_sleep(2);
+      }
+      sh[2] = go;
+    }
+    __syncthreads();
+    const int go = sh[2];
+    __syncthreads();
+    if (!go) break;
+    if (step < L * kFStages) {
+      if (s == FS_QKV) {
+        const int n = plan[PL_QKV];
+        for (int j = 0; j < n; ++j)
+          acc = touch(Range{(const unsigned char*)lw(a, l, LW_QKV) + (size_t)plan[PL_QKV + 1 + j] * KCd * 1024,
+                            (size_t)KCd * 1024},
+                      acc);
+      } else if (s == FS_ATT) {
+        const int n = plan[PL_ATT];
+        for (int j = 0; j < n; ++j) {
+          const int h = plan[PL_ATT + 1 + j] & 0xffff;
+          const size_t off = (((size_t)l * a.H + h) * a.max_ctx) * DH * 2;
+          acc = touch(Range{(const unsigned char*)a.kc + off, (size_t)a.P * DH * 2}, acc);
+          acc = touch(Range{(const unsigned char*)a.vc + off, (size_t)a.P * DH * 2}, acc);
+        }
+      } else if (s == FS_WO) {
+        const int n = plan[PL_WO];
+        for (int j = 0; j < n; ++j)
+          acc = touch(Range{(const unsigned char*)lw(a, l, LW_O) + ((size_t)plan[PL_WO + 1 + j] * KCd + kh0) * 1024,
+                            (size_t)(kh1 - kh0) * 1024},
+                      acc);
+      } else if (s == FS_FC) {
+        const int n = plan[PL_FC];
+        for (int j = 0; j < n; ++j)
+          acc = touch(Range{(const unsigned char*)lw(a, l, LW_FC) + (size_t)plan[PL_FC + 1 + j] * KCd * 1024,
+                            (size_t)KCd * 1024},
+                      acc);
+      } else {
+        const int n = plan[PL_WPR];
+        for (int j = 0; j < n; ++j)
+          acc = touch(Range{(const unsigned char*)lw(a, l, LW_PR) + ((size_t)plan[PL_WPR + 1 + j] * KCm + kf0) * 1024,
+                            (size_t)(kf1 - kf0) * 1024},
+                      acc);
+      }
+    } else {
+      // LM head, in the compute workgroup's task groups
+      const int b0 = hb0 + (step - L * kFStages - 1) * HRB;
+      acc = touch(Range{(const unsigned char*)a.p_head + (size_t)b0 * KCd * 1024,
+                        (size_t)min(HRB, hb1 - b0) * KCd * 1024},
+                  acc);
+    }
+  }
+  if (acc == a.magic) *a.sink = acc;
+}
+
+template <int NT>
+__global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(2))) void pass_kernel(FusedArgs a) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
+  if ((int)blockIdx.x < kFGroups) compute_wg<NT>(a, lds);
+  else prefetch_wg<NT>(a, lds);
+}
+
+}  // namespace fz
+
+// ------------------------------------------------------------------ host planner
+//
+// Splits one layer over the 8 XCDs and their 32 ranks.
+//  * Heads: the first H % 8 XCDs take one more.  A head costs 4 x 64 rows of
+//    d weights (Q, K, V rows and the W_o columns); a hidden feature costs 2 d.
+//    Each XCD's hidden slice (whole k-steps of 32 features) is chosen so that
+//    every XCD streams about the same bytes per layer.
+//  * Inside an XCD each stage's units (attention head x tile; row blocks of
+//    the GEMMs) are dealt so that every rank gets floor or ceil of its share
+//    of that stage, the extra units going to the ranks with the least bytes
+//    so far; a rank's units of a stage are consecutive.
+//  * The LM head's row blocks are cut into 256 consecutive ranges.
+bool fused_plan(int H, int d, int M, int V, int ntiles, int* tab, int* xh, int* xf, std::string* why) {
+  const int DHh = 64;
+  if (H * DHh != d || d % 32 || M % 32 || ntiles < 1 || ntiles > 4) {
+    *why = "fused pass: needs head dimension 64, d and d_mlp multiples of 32, 1-4 node tiles";
+    return false;
+  }
+  const int KM = M / 32;
+  int hx[kFXcd], fx[kFXcd];
+  for (int x = 0; x < kFXcd; ++x) hx[x] = H / kFXcd + (x < H % kFXcd ? 1 : 0);
+  // bytes per layer in units of 4 d bytes: 128 per head, 1 per hidden feature
+  const double target = (128.0 * H + M) / kFXcd;
+  int fsum = 0;
+  for (int x = 0; x < kFXcd; ++x) {
+    const double want = (target - 128.0 * hx[x]) / 32.0;
+    fx[x] = want > 0 ? (int)want : 0;
+    fsum += fx[x];
+  }
+  auto load = [&](int x) { return 128.0 * hx[x] + 32.0 * fx[x]; };
+  while (fsum < KM) {
+    int b = 0;
+    for (int x = 1; x < kFXcd; ++x)
+      if (load(x) < load(b)) b = x;
+    ++fx[b];
+    ++fsum;
+  }
+  while (fsum > KM) {
+    int b = -1;
+    for (int x = 0; x < kFXcd; ++x)
+      if (fx[x] > 0 && (b < 0 || load(x) > load(b))) b = x;
+    --fx[b];
+    --fsum;
+  }
+  int h0 = 0, f0 = 0;
+  for (int x = 0; x < kFXcd; ++x) {
+    xh[2 * x] = h0;
+    xh[2 * x + 1] = h0 + hx[x];
+    h0 += hx[x];
+    xf[2 * x] = f0;
+    xf[2 * x + 1] = f0 + fx[x];
+    f0 += fx[x];
+  }
+  std::fill(tab, tab + (size_t)kFGroups * kPlanStride, 0);
+  const int RBd = d / 16;
+  const double pnom = 512.0;  // nominal prefix rows for an attention unit's cost
+  for (int x = 0; x < kFXcd; ++x) {
+    std::vector<double> ld(kFRanks, 0.0);
+    std::vector<int> unitsA, unitsQ, unitsO, unitsF, unitsP;
+    for (int h = xh[2 * x]; h < xh[2 * x + 1]; ++h)
+      for (int t = 0; t < ntiles; ++t) unitsA.push_back(h | (t << 16));
+    for (int part = 0; part < 3; ++part)
+      for (int h = xh[2 * x]; h < xh[2 * x + 1]; ++h)
+        for (int j = 0; j < DHh / 16; ++j) unitsQ.push_back(part * RBd + h * (DHh / 16) + j);
+    if (hx[x] > 0)
+      for (int rb = 0; rb < RBd; ++rb) unitsO.push_back(rb);
+    for (int rb = 2 * xf[2 * x]; rb < 2 * xf[2 * x + 1]; ++rb) unitsF.push_back(rb);
+    if (fx[x] > 0)
+      for (int rb = 0; rb < RBd; ++rb) unitsP.push_back(rb);
+    struct St {
+      std::vector<int>* u;
+      int slot, maxn;
+      double cost;
+    } st[5] = {{&unitsA, PL_ATT, kPlanMaxAtt, pnom * 256.0},
+               {&unitsQ, PL_QKV, kPlanMaxRb, 32.0 * d},
+               {&unitsO, PL_WO, kPlanMaxRb, 16.0 * 64 * hx[x] * 2},
+               {&unitsF, PL_FC, kPlanMaxRb, 32.0 * d},
+               {&unitsP, PL_WPR, kPlanMaxRb, 16.0 * 32 * fx[x] * 2}};
+    for (const St& S : st) {
+      const int U = (int)S.u->size(), base = U / kFRanks, extra = U % kFRanks;
+      std::vector<int> order(kFRanks);
+      for (int r = 0; r < kFRanks; ++r) order[r] = r;
+      std::stable_sort(order.begin(), order.end(), [&](int p, int q) { return ld[p] < ld[q]; });
+      std::vector<int> cnt(kFRanks, base);
+      for (int k = 0; k < extra; ++k) cnt[order[k]]++;
+      int next = 0;
+      for (int r = 0; r < kFRanks; ++r) {
+        if (cnt[r] > S.maxn) {
+          *why = "fused pass: a rank would get more than the plan's units per stage";
+          return false;
+        }
+        int* row = tab + (size_t)(x * kFRanks + r) * kPlanStride;
+        row[S.slot] = cnt[r];
+        for (int k = 0; k < cnt[r]; ++k) row[S.slot + 1 + k] = (*S.u)[next++];
+        ld[r] += cnt[r] * S.cost;
+      }
+    }
+  }
+  const int RBV = (V + 15) / 16;
+  for (int g = 0; g < kFGroups; ++g) {
+    int* row = tab + (size_t)g * kPlanStride;
+    row[PL_HEAD] = (int)((long long)g * RBV / kFGroups);
+    row[PL_HEAD + 1] = (int)((long long)(g + 1) * RBV / kFGroups);
+  }
+  return true;
+}
+
+hipError_t fused_prepare() {
+  const int lds = (int)fused_lds_bytes();
+  hipError_t e = hipFuncSetAttribute((const void*)fz::pass_kernel<1>, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+  if (e == hipSuccess)
+    e = hipFuncSetAttribute((const void*)fz::pass_kernel<2>, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+  if (e == hipSuccess)
+    e = hipFuncSetAttribute((const void*)fz::pass_kernel<4>, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+  return e;
+}
+
+size_t fused_lds_bytes() { return fz::A_REGION + fz::A_PART_BYTES + fz::A_Q_BYTES + 64; }
+
+hipError_t launch_fused(const FusedArgs& a, hipStream_t s) {
+  if (a.N <= 0 || a.N > kFMaxN || a.d % 32 || a.M % 32 || a.d > 2048 || a.H * fz::DH != a.d) return hipErrorInvalidValue;
+  const int nt = (a.N + 15) / 16;
+  const size_t lds = fused_lds_bytes();
+  const dim3 grid(a.prefetch ? 2 * kFGroups : kFGroups);
+  switch (nt) {
+    case 1: fz::pass_kernel<1><<<grid, fz::NTH, lds, s>>>(a); break;
+    case 2: fz::pass_kernel<2><<<grid, fz::NTH, lds, s>>>(a); break;
+    default: fz::pass_kernel<4><<<grid, fz::NTH, lds, s>>>(a); break;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace ssd

@@ -10,6 +10,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <string>
 #include <vector>
@@ -24,6 +25,12 @@ namespace {
 thread_local std::string g_last_error;
 int g_gemm_path = 0;  // 0 auto, 1 vector ALU, 2 matrix cores
 int g_prefetch = 1;   // warm each weight GEMM's L2 from the kernel before it
+int g_pass_mode = 0;  // 0 auto, 1 one kernel per sub-layer, 2 the persistent single-launch pass only
+int g_fz_ahead = 1;   // stages the persistent pass's prefetchers run ahead
+int g_fz_poll_sleep = [] {
+  const char* e = getenv("SSD_FZ_POLL_SLEEP");
+  return e ? atoi(e) : 0;
+}();
 
 // Node counts up to this use the vector-ALU GEMM on the automatic path.
 constexpr int kVecMaxNodes = 4;
@@ -58,7 +65,23 @@ struct ssd_model {
   std::vector<const void*> p_qkv, p_o, p_fc, p_pr;
   const void* p_head = nullptr;
   void* wtab = nullptr;  // device [4][n_layer]: p_qkv, p_o, p_fc, p_pr (for the prefetcher); own copy per view
+  void* ftab = nullptr;  // device [n_layer][kLwSlots]: the persistent pass's per-layer parameters; own copy per view
 };
+
+// the device table of a bf16 model's per-layer parameters for the persistent
+// pass (see LwSlot in fused.hip)
+static hipError_t make_ftab(ssd_model* m) {
+  const int L = m->cfg.n_layer;
+  std::vector<const void*> t;
+  for (int l = 0; l < L; ++l) {
+    const void* row[kLwSlots] = {m->p_qkv[l], m->p_o[l], m->p_fc[l], m->p_pr[l], m->b_qkv[l], m->b_o[l],
+                                 m->b_fc[l],  m->b_pr[l], m->ln1_g[l], m->ln1_b[l], m->ln2_g[l], m->ln2_b[l]};
+    t.insert(t.end(), row, row + kLwSlots);
+  }
+  hipError_t e = hipMalloc(&m->ftab, t.size() * sizeof(void*));
+  if (e == hipSuccess) e = hipMemcpy(m->ftab, t.data(), t.size() * sizeof(void*), hipMemcpyHostToDevice);
+  return e;
+}
 
 // the device table of a bf16 model's packed weight pointers, [4][L]
 static hipError_t make_wtab(ssd_model* m) {
@@ -100,6 +123,11 @@ struct ssd_kv {
   unsigned* d_sink = nullptr;
   unsigned long long sig_count = 0;     // signals of every pass enqueued so far
   hipStream_t pf_stream = nullptr;      // created on first use
+  // the persistent single-launch pass (bf16 models, head dimension 64)
+  bool fz_ok = false;                  // workspaces and plans exist
+  void* fz_ws = nullptr;
+  FusedArgs fz{};                      // workspace pointers, XCD ranges
+  int* fz_plan[5] = {};                // device plans per 16-node tile count (1..4)
 };
 
 struct ssd_graph {
@@ -136,6 +164,34 @@ extern "C" ssd_status ssd_set_gemm_path(int32_t path) {
 extern "C" ssd_status ssd_set_weight_prefetch(int32_t on) {
   if (on != 0 && on != 1) return fail(SSD_E_INVALID_ARG, "weight prefetch must be 0 or 1");
   g_prefetch = on;
+  return SSD_OK;
+}
+
+extern "C" ssd_status ssd_set_pass_mode(int32_t mode) {
+  if (mode < 0 || mode > 2) return fail(SSD_E_INVALID_ARG, "pass mode must be 0, 1 or 2");
+  g_pass_mode = mode;
+  return SSD_OK;
+}
+
+extern "C" ssd_status ssd_set_fused_ahead(int32_t stages) {
+  if (stages < 0 || stages > 8) return fail(SSD_E_INVALID_ARG, "prefetch distance must be 0..8 stages");
+  g_fz_ahead = stages;
+  return SSD_OK;
+}
+
+extern "C" ssd_status ssd_kv_set_trace(ssd_kv* kv, uint64_t* buf) {
+  if (!kv) return fail(SSD_E_INVALID_ARG, "null session");
+  if (!kv->fz_ok) return fail(SSD_E_UNSUPPORTED, "the session has no persistent pass");
+  kv->fz.trace = (unsigned long long*)buf;
+  return SSD_OK;
+}
+
+extern "C" ssd_status ssd_fused_plan(int32_t n_head, int32_t d_model, int32_t d_mlp, int32_t vocab, int32_t n_tiles,
+                                      int32_t* tab, int32_t* xh, int32_t* xf) {
+  if (!tab || !xh || !xf) return fail(SSD_E_INVALID_ARG, "null output");
+  if (n_head <= 0 || d_model <= 0 || d_mlp <= 0 || vocab <= 0) return fail(SSD_E_INVALID_ARG, "sizes must be positive");
+  std::string why;
+  if (!fused_plan(n_head, d_model, d_mlp, vocab, n_tiles, tab, xh, xf, &why)) return fail(SSD_E_UNSUPPORTED, why);
   return SSD_OK;
 }
 
@@ -246,9 +302,11 @@ extern "C" ssd_status ssd_model_create(const ssd_config* cfg, const ssd_weights*
     m->p_head = pack(m->wte, V, d, b_head);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e == hipSuccess) e = make_wtab(m);
+    if (e == hipSuccess) e = make_ftab(m);
     if (e != hipSuccess) {
       (void)hipFree(m->pack);
       if (m->wtab) (void)hipFree(m->wtab);
+      if (m->ftab) (void)hipFree(m->ftab);
       delete m;
       return fail(SSD_E_DEVICE, std::string("weight packing: ") + hipGetErrorString(e));
     }
@@ -261,6 +319,7 @@ extern "C" void ssd_model_destroy(ssd_model* m) {
   if (!m) return;
   if (m->pack && m->owns_pack) (void)hipFree(m->pack);
   if (m->wtab) (void)hipFree(m->wtab);
+  if (m->ftab) (void)hipFree(m->ftab);
   delete m;
 }
 
@@ -274,14 +333,17 @@ extern "C" ssd_status ssd_model_prefix_view(const ssd_model* m, int32_t n_layer,
                                      &v->ln2_b, &v->w_fc, &v->b_fc, &v->w_pr, &v->b_pr};
   for (auto a : per) a->resize(n_layer);
   v->wtab = nullptr;
+  v->ftab = nullptr;
   if (!v->f32) {
     v->p_qkv.resize(n_layer);
     v->p_o.resize(n_layer);
     v->p_fc.resize(n_layer);
     v->p_pr.resize(n_layer);
-    const hipError_t e = make_wtab(v);
+    hipError_t e = make_wtab(v);
+    if (e == hipSuccess) e = make_ftab(v);
     if (e != hipSuccess) {
       if (v->wtab) (void)hipFree(v->wtab);
+      if (v->ftab) (void)hipFree(v->ftab);
       delete v;
       return fail(SSD_E_DEVICE, std::string("weight table: ") + hipGetErrorString(e));
     }
@@ -312,6 +374,72 @@ extern "C" ssd_status ssd_kv_bytes(const ssd_config* cfg, int32_t max_ctx, int32
 // root paths back to back (offsets above).
 static size_t stage_bytes(int max_nodes) {
   return (size_t)5 * max_nodes * 4 + (size_t)max_nodes * kPath32 * 4 + (size_t)max_nodes * (max_nodes + 1) / 2 * 4;
+}
+
+// Workspaces and work plans of the persistent pass.  The pass needs one
+// workgroup per CU on 8 XCDs of 32 CUs and head dimension 64; otherwise the
+// session keeps only the per-sub-layer kernels (fz_ok stays false).
+static ssd_status fused_setup(ssd_kv* kv) {
+  const ssd_model* m = kv->m;
+  const ssd_config& c = m->cfg;
+  if (m->dh != 64 || c.d_model > 2048 || c.n_layer > kFMaxL) return SSD_OK;
+  int dev = 0, cus = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  HIP_TRY(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+  if (cus != kFGroups) return SSD_OK;
+  const int d = c.d_model, M = c.d_mlp;
+  std::vector<int> tabs((size_t)4 * kFGroups * kPlanStride);
+  FusedArgs& a = kv->fz;
+  std::string why;
+  for (int nt = 1; nt <= 4; ++nt)
+    if (!fused_plan(c.n_head, d, M, c.vocab, nt, tabs.data() + (size_t)(nt - 1) * kFGroups * kPlanStride, a.xh,
+                    a.xf, &why))
+      return SSD_OK;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t o = off;
+    off += (bytes + 255) / 256 * 256;
+    return o;
+  };
+  const size_t act_stride = (size_t)kFMaxN * d;  // float16 elements of one XCD's copy
+  const size_t o_xr = take((size_t)kFXcd * kFMaxN * d * 4), o_q = take((size_t)kFMaxN * d * 4);
+  const size_t o_a1 = take(kFXcd * act_stride * 2), o_a2 = take(kFXcd * act_stride * 2);
+  const size_t o_fo = take((size_t)kFMaxN * d * 2), o_ff = take((size_t)kFMaxN * M * 2);
+  const size_t o_po = take((size_t)kFXcd * kFMaxN * d * 4), o_pp = take((size_t)kFXcd * kFMaxN * d * 4);
+  const size_t o_fl = take((size_t)kFStages * kFGroups * 4), o_ctl = take((size_t)kFCtlWords * 4);
+  const size_t o_prog = take((size_t)kFGroups * 4), o_plan = take(tabs.size() * 4), o_sink = take(4);
+  static const hipError_t prep = fused_prepare();
+  if (prep != hipSuccess) return SSD_OK;  // keep the per-sub-layer kernels
+  HIP_TRY(hipMalloc(&kv->fz_ws, off));
+  HIP_TRY(hipMemset(kv->fz_ws, 0, off));
+  HIP_TRY(hipMemcpy((char*)kv->fz_ws + o_plan, tabs.data(), tabs.size() * 4, hipMemcpyHostToDevice));
+  char* b = (char*)kv->fz_ws;
+  a.xr = (float*)(b + o_xr);
+  a.q = (float*)(b + o_q);
+  a.act1 = (uint16_t*)(b + o_a1);
+  a.act2 = (uint16_t*)(b + o_a2);
+  a.act_stride = act_stride;
+  a.fo = (uint16_t*)(b + o_fo);
+  a.ff = (uint16_t*)(b + o_ff);
+  a.part_o = (float*)(b + o_po);
+  a.part_p = (float*)(b + o_pp);
+  a.flags = (unsigned*)(b + o_fl);
+  a.ctl = (unsigned*)(b + o_ctl);
+  a.prog = (unsigned*)(b + o_prog);
+  a.sink = (unsigned*)(b + o_sink);
+  for (int nt = 1; nt <= 4; ++nt) kv->fz_plan[nt] = (int*)(b + o_plan) + (size_t)(nt - 1) * kFGroups * kPlanStride;
+  a.err = kv->d_err;
+  a.timeout = 20000000ull;  // 200 ms
+  a.pf_idle = 100000ull;    // 1 ms
+  a.magic = 0x5bd1e995u;
+  kv->fz_ok = true;
+  return SSD_OK;
+}
+
+// whether a verification pass of model m over n nodes runs as the persistent single launch
+static bool use_fused(const ssd_model* m, const ssd_kv* kv, int n) {
+  if (g_pass_mode == 1 || m->f32 || !kv->fz_ok || !m->ftab) return false;
+  return n <= kFMaxN;
 }
 
 extern "C" ssd_status ssd_kv_create(const ssd_model* m, int32_t max_ctx, int32_t max_nodes, void* k_cache,
@@ -396,6 +524,13 @@ extern "C" ssd_status ssd_kv_create(const ssd_model* m, int32_t max_ctx, int32_t
     ssd_kv_destroy(kv);
     return fail(SSD_E_DEVICE, std::string("staging allocation: ") + hipGetErrorString(e));
   }
+  if (!m->f32) {
+    const ssd_status fs = fused_setup(kv);
+    if (fs != SSD_OK) {
+      ssd_kv_destroy(kv);
+      return fs;
+    }
+  }
   *out = kv;
   return SSD_OK;
 }
@@ -413,6 +548,7 @@ extern "C" void ssd_kv_destroy(ssd_kv* kv) {
     }
   if (kv->pinned) (void)hipHostFree(kv->pinned);
   if (kv->ws) (void)hipFree(kv->ws);
+  if (kv->fz_ws) (void)hipFree(kv->fz_ws);
   delete kv;
 }
 
@@ -517,8 +653,10 @@ static PrefetchPlan prefetch_plan(const ssd_model* m, const ssd_kv* kv, int n) {
 // Accounts for the signals of one bf16 pass about to be enqueued and, when
 // weight prefetch is on, launches its prefetcher on the session's side
 // stream first (the pass never waits for it).
+static bool use_fused(const ssd_model* m, const ssd_kv* kv, int n);
+
 static ssd_status start_pass_prefetch(const ssd_model* m, ssd_kv* kv, int n) {
-  if (m->f32) return SSD_OK;
+  if (m->f32 || use_fused(m, kv, n)) return SSD_OK;
   const unsigned long long base = kv->sig_count;
   kv->sig_count += (unsigned long long)sigs_per_pass(m->cfg.n_layer);
   if (!g_prefetch) return SSD_OK;
@@ -571,6 +709,41 @@ static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int3
   const int* d_off = kv->d_tree + 4 * maxn;
   const int* d_path32 = kv->d_tree + 5 * maxn;
   const int* d_paths = d_path32 + (size_t)n * kPath32;
+  if (use_fused(m, kv, n)) {
+    FusedArgs a = kv->fz;
+    a.lw = (const void* const*)m->ftab;
+    a.wte = (const uint16_t*)m->wte;
+    a.wpe = (const uint16_t*)m->wpe;
+    a.lnf_g = (const uint16_t*)m->lnf_g;
+    a.lnf_b = (const uint16_t*)m->lnf_b;
+    a.p_head = m->p_head;
+    a.L = L;
+    a.d = d;
+    a.H = H;
+    a.M = M;
+    a.V = V;
+    a.eps = c.ln_eps;
+    a.scale = 1.0f / std::sqrt((float)DH);
+    a.kc = (const uint16_t*)kv->kc;
+    a.vc = (const uint16_t*)kv->vc;
+    a.kt = (uint16_t*)kv->kt;
+    a.vt = (uint16_t*)kv->vt;
+    a.max_ctx = kv->max_ctx;
+    a.max_nodes = maxn;
+    a.tree = kv->d_tree;
+    a.N = n;
+    a.P = P;
+    a.logits = logits;
+    a.plan = kv->fz_plan[(n + 15) / 16];
+    a.ahead = g_fz_ahead;
+    a.poll_sleep = g_fz_poll_sleep;
+    a.dbg = getenv("SSD_FZ_DBG") ? atoi(getenv("SSD_FZ_DBG")) : 0;
+    a.dbg_l = 10;
+    a.prefetch = getenv("SSD_FZ_PF") ? atoi(getenv("SSD_FZ_PF")) : 0;
+    HIP_TRY(launch_fused(a, s));
+    return SSD_OK;
+  }
+  if (g_pass_mode == 2) return fail(SSD_E_UNSUPPORTED, "the persistent pass does not apply to this model, session or tree");
   unsigned long long* sig = f32 ? nullptr : kv->d_sig;  // pass signals (bf16 models)
   HIP_TRY(launch_embed(f32, m->wte, m->wpe, d_tok, d_pos, n, d, kv->x, sig, kv->d_xcc0, s));
 

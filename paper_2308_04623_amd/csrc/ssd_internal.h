@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <string>
+
 namespace ssd {
 
 // Epilogues of the skinny GEMM Y[n][o] = sum_k A[n][k] W[o][k].
@@ -172,5 +174,71 @@ hipError_t launch_sample_accept(const int* tokens, const int* parents, int N, in
 hipError_t launch_commit(int f32, void* kc, void* vc, const void* kt, const void* vt, int LH, int max_ctx,
                          int max_nodes, int DH, int P, const int* path, const int* path_len, unsigned* err,
                          hipStream_t s);
+
+// ---- the persistent single-launch pass (fused.hip), bf16 models with head
+// dimension 64 and at most kFMaxN nodes
+constexpr int kFXcd = 8;                   // XCDs
+constexpr int kFRanks = 32;                // compute workgroups per XCD
+constexpr int kFGroups = kFXcd * kFRanks;  // compute workgroups (one per CU)
+constexpr int kFMaxN = 64;                 // nodes
+constexpr int kFMaxL = 255;                // layers
+// stages of a layer; their flags are [kFStages][kFGroups] words
+enum FStage { FS_LN1 = 0, FS_QKV, FS_ATT, FS_WO, FS_LN2, FS_FC, FS_WPR, FS_SPARE, kFStages };
+constexpr unsigned kFTagsPerPass = (unsigned)kFStages * (kFMaxL + 1);
+constexpr int kLwSlots = 12;  // per-layer parameter pointers (see LwSlot in fused.hip)
+// plan row of one compute workgroup (int32): counts then entries
+enum PlanSlot { PL_ATT = 0, PL_QKV = 9, PL_WO = 14, PL_FC = 19, PL_WPR = 24, PL_HEAD = 29, kPlanStride = 32 };
+constexpr int kPlanMaxAtt = 8, kPlanMaxRb = 4;
+// control words: pass counter, finished workgroups, abort flag, abort reason, claims [kFGroups]
+enum { FZ_PASS = 0, FZ_DONE = 1, FZ_ABORT = 2, FZ_WHY = 3, FZ_CLAIM = 16, kFCtlWords = FZ_CLAIM + kFGroups };
+
+struct FusedArgs {
+  // model
+  const void* const* lw;  // device [L][kLwSlots]: packed W_qkv, W_o, W_fc, W_pr, then biases, LN gains/biases
+  const uint16_t *wte, *wpe, *lnf_g, *lnf_b;
+  const void* p_head;     // packed tied LM head
+  int L, d, H, M, V;
+  float eps, scale;
+  // session
+  const uint16_t *kc, *vc;  // cache [L][H][max_ctx][64]
+  uint16_t *kt, *vt;        // tree scratch [L][H][max_nodes][64]
+  int max_ctx, max_nodes;
+  const int* tree;          // staged tree (tokens, positions, depths, parents, offsets, path32, paths)
+  int N, P;
+  float* logits;            // [N][V]
+  // workspaces
+  float* xr;                // [kFXcd][kFMaxN][d] residual stream, one copy per XCD
+  float* q;                 // [kFMaxN][d]
+  uint16_t *act1, *act2;    // [kFXcd][act_stride] LayerNorm outputs (float16 fragments), one copy per XCD
+  size_t act_stride;
+  uint16_t* fo;             // attention outputs, float16 fragments [4 tiles][d / 32][512]
+  uint16_t* ff;             // GELU outputs, float16 fragments [4 tiles][M / 32][512]
+  float *part_o, *part_p;   // partial residuals [kFXcd][kFMaxN][d]
+  unsigned* flags;          // [kFStages][kFGroups]
+  unsigned* ctl;            // [kFCtlWords]
+  unsigned* prog;           // [kFGroups] progress of each compute workgroup (for its prefetcher)
+  const int* plan;          // [kFGroups][kPlanStride]
+  int xh[2 * kFXcd];        // heads [xh[2x], xh[2x+1]) of XCD x
+  int xf[2 * kFXcd];        // hidden k-steps [xf[2x], xf[2x+1]) of XCD x
+  unsigned* err;            // session error counter
+  unsigned long long timeout;  // s_memrealtime ticks (100 MHz) before a wait gives up
+  unsigned long long pf_idle;  // ticks a prefetcher waits without progress before it stops
+  int ahead;                // stages the prefetchers run ahead
+  int poll_sleep;           // extra back-off between flag polls (units of s_sleep 8)
+  unsigned magic;
+  unsigned* sink;
+  unsigned long long* trace;  // stage timestamps [kFGroups][L + 1][kFStages][3], or nullptr
+  int prefetch;               // also launch the L2 prefetch workgroups
+  int dbg, dbg_l;             // extra LayerNorm timestamps (bit 0) for layer dbg_l, in the spare stage slot
+};
+
+// Work split of the fused pass for a model shape and 16-node tile count:
+// tab receives [kFGroups][kPlanStride]; false (with a reason) if the shape
+// does not fit the plan's limits.
+bool fused_plan(int H, int d, int M, int V, int ntiles, int* tab, int* xh, int* xf, std::string* why);
+size_t fused_lds_bytes();
+// raises the kernels' dynamic LDS limit (once per process, before the first launch)
+hipError_t fused_prepare();
+hipError_t launch_fused(const FusedArgs& a, hipStream_t s);
 
 }  // namespace ssd

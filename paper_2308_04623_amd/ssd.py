@@ -28,7 +28,7 @@ LAYER_TENSORS = ("ln1_g", "ln1_b", "w_qkv", "b_qkv", "w_o", "b_o",
 EXPORTS = ("ssd_model_create", "ssd_model_destroy", "ssd_kv_bytes", "ssd_kv_create", "ssd_kv_destroy",
            "ssd_tree_verify", "ssd_tree_accept", "ssd_kv_commit", "ssd_kv_error_count",
            "ssd_graph_capture_verify", "ssd_graph_launch", "ssd_graph_destroy", "ssd_validate_tree",
-           "ssd_tree_prep", "ssd_set_gemm_path", "ssd_set_weight_prefetch", "ssd_status_string", "ssd_last_error", "ssd_launch_gemm",
+           "ssd_tree_prep", "ssd_set_gemm_path", "ssd_set_weight_prefetch", "ssd_set_pass_mode", "ssd_set_fused_ahead", "ssd_fused_plan", "ssd_kv_set_trace", "ssd_status_string", "ssd_last_error", "ssd_launch_gemm",
            "ssd_model_prefix_view", "ssd_topk")
 
 
@@ -88,6 +88,10 @@ def lib():
             "ssd_tree_prep": [i32p, C.c_int32, i32p, C.POINTER(C.c_uint64)],
             "ssd_set_gemm_path": [C.c_int32],
             "ssd_set_weight_prefetch": [C.c_int32],
+            "ssd_set_pass_mode": [C.c_int32],
+            "ssd_set_fused_ahead": [C.c_int32],
+            "ssd_fused_plan": [C.c_int32] * 5 + [vp, vp, vp],
+            "ssd_kv_set_trace": [vp, vp],
             "ssd_launch_gemm": [vp, vp, C.c_int32, C.c_int32, C.c_int32, vp],
             "ssd_model_prefix_view": [vp, C.c_int32, C.POINTER(vp)],
             "ssd_topk": [vp, vp, C.c_int32, C.c_int32, vp, vp, vp, vp],
@@ -145,6 +149,28 @@ def set_gemm_path(path: int):
 
 def set_weight_prefetch(on: bool):
     _check(lib().ssd_set_weight_prefetch(1 if on else 0), "ssd_set_weight_prefetch")
+
+
+PASS_AUTO, PASS_KERNELS, PASS_FUSED = 0, 1, 2
+
+
+def set_pass_mode(mode: int):
+    """0 automatic, 1 one kernel per sub-layer, 2 the persistent single launch only."""
+    _check(lib().ssd_set_pass_mode(mode), "ssd_set_pass_mode")
+
+
+def fused_plan(n_head: int, d_model: int, d_mlp: int, vocab: int, n_tiles: int):
+    """The persistent pass's work split (host-only): (tab [256][32], xh [16], xf [16])."""
+    tab = np.zeros((256, 32), np.int32)
+    xh = np.zeros(16, np.int32)
+    xf = np.zeros(16, np.int32)
+    _check(lib().ssd_fused_plan(n_head, d_model, d_mlp, vocab, n_tiles, tab.ctypes.data, xh.ctypes.data,
+                                xf.ctypes.data), "ssd_fused_plan")
+    return tab, xh, xf
+
+
+def set_fused_ahead(stages: int):
+    _check(lib().ssd_set_fused_ahead(stages), "ssd_set_fused_ahead")
 
 
 def kv_bytes(cfg, max_ctx: int, max_nodes: int) -> Tuple[int, int]:
@@ -367,6 +393,12 @@ class Session:
         _check(lib().ssd_topk(self.handle, C.c_void_p(logits.data_ptr()), n, k, C.c_void_p(idx.data_ptr()),
                               C.c_void_p(val.data_ptr()), C.c_void_p(lse.data_ptr()), _stream(stream)), "ssd_topk")
         return idx, val, lse
+
+    def set_trace(self, buf=None):
+        """Stage timestamps of the persistent pass into buf (device uint64/int64
+        tensor of 256 * (n_layer + 1) * 24 words), or None to stop."""
+        _check(lib().ssd_kv_set_trace(self.handle, C.c_void_p(buf.data_ptr() if buf is not None else 0)),
+               "ssd_kv_set_trace")
 
     def error_count(self, stream=None) -> int:
         c = C.c_uint32(0)

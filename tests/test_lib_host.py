@@ -76,3 +76,63 @@ def test_weight_prefetch_switch_validates():
     assert ssd.lib().ssd_set_weight_prefetch(2) != 0
     ssd.set_weight_prefetch(False)
     ssd.set_weight_prefetch(True)
+
+
+# ---- the persistent pass's work split (host-only)
+
+SHAPES = [(20, 1280, 5120, 50257), (4, 256, 1024, 2000), (12, 768, 3072, 50257), (25, 1600, 6400, 50257),
+          (1, 64, 256, 100)]
+
+
+@pytest.mark.parametrize("H,d,M,V", SHAPES)
+@pytest.mark.parametrize("nt", [1, 2, 3, 4])
+def test_fused_plan_covers_every_unit_once(H, d, M, V, nt):
+    """Every weight row block of every stage is computed by exactly one
+    workgroup of the XCD that owns it, every (head, tile) attention unit once,
+    and every LM-head row block once; XCD ranges tile the heads and hidden
+    features."""
+    tab, xh, xf = ssd.fused_plan(H, d, M, V, nt)
+    assert xh[0] == 0 and xh[15] == H and xf[0] == 0 and xf[15] == M // 32
+    assert all(xh[2 * x + 1] == xh[2 * x + 2] and xf[2 * x + 1] == xf[2 * x + 2] for x in range(7))
+    assert all(xh[2 * x + 1] >= xh[2 * x] and xf[2 * x + 1] >= xf[2 * x] for x in range(8))
+    rbd = d // 16
+    for x in range(8):
+        rows = tab[32 * x:32 * x + 32]
+        heads = range(xh[2 * x], xh[2 * x + 1])
+
+        def units(slot, cap):
+            out = []
+            for r in rows:
+                assert 0 <= r[slot] <= cap
+                out += list(r[slot + 1:slot + 1 + r[slot]])
+            return sorted(out)
+
+        assert units(0, 8) == sorted(h | (t << 16) for h in heads for t in range(nt))
+        assert units(9, 4) == sorted(p * rbd + 4 * h + j for p in range(3) for h in heads for j in range(4))
+        assert units(14, 4) == (list(range(rbd)) if len(heads) else [])
+        assert units(19, 4) == list(range(2 * xf[2 * x], 2 * xf[2 * x + 1]))
+        assert units(24, 4) == (list(range(rbd)) if xf[2 * x + 1] > xf[2 * x] else [])
+        # each stage split into floor/ceil shares over the 32 ranks
+        for slot in (0, 9, 14, 19, 24):
+            c = rows[:, slot]
+            assert c.max() - c.min() <= 1
+    head = sorted((int(r[29]), int(r[30])) for r in tab)
+    assert head[0][0] == 0 and head[-1][1] == (V + 15) // 16
+    assert all(head[i][1] == head[i + 1][0] for i in range(255))
+
+
+def test_fused_plan_balances_gpt2l_xcds():
+    """GPT-2-L: four XCDs own 3 heads and 576 hidden features, four own 2 heads
+    and 704, so every XCD streams 4,915,200 bytes of weights per layer."""
+    tab, xh, xf = ssd.fused_plan(20, 1280, 5120, 50257, 2)
+    heads = [xh[2 * x + 1] - xh[2 * x] for x in range(8)]
+    hidden = [32 * (xf[2 * x + 1] - xf[2 * x]) for x in range(8)]
+    assert heads == [3, 3, 3, 3, 2, 2, 2, 2]
+    assert hidden == [576] * 4 + [704] * 4
+    per_xcd = [h * 4 * 64 * 1280 * 2 + f * 2 * 1280 * 2 for h, f in zip(heads, hidden)]
+    assert per_xcd == [4915200] * 8
+
+
+def test_fused_plan_rejects_other_head_dims():
+    with pytest.raises(ssd.SSDError):
+        ssd.fused_plan(4, 128, 512, 512, 1)  # head dimension 32
