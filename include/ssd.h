@@ -231,16 +231,16 @@ ssd_status ssd_set_weight_prefetch(int32_t on);
 /* How a bfloat16 verification pass runs (Sec. 2.1: a decode step streams
  * every weight once; Sec. 3.1: one step scores the whole tree).
  *   0 (default) = automatic: the persistent single launch when the session
- *     supports it (head dimension 64, at most 64 nodes, a 256-CU device with
- *     8 XCDs), else one kernel per sub-layer;
+ *     supports it (head dimension 64, a 256-CU device with 8 XCDs) and the
+ *     tree has at most 32 nodes (where it is the faster way), else one
+ *     kernel per sub-layer;
  *   1 = always one kernel per sub-layer;
- *   2 = the persistent single launch only: ssd_tree_verify and
- *     ssd_graph_capture_verify return SSD_E_UNSUPPORTED where it does not
- *     apply.
- * The persistent launch runs every layer in one kernel: 256 compute
- * workgroups (one per CU) hand results to each other through flags in device
- * memory, and 256 more warm the L2 with the weights of their partner's next
- * stage.  Every wait inside it is bounded; if one times out (200 ms) the
+ *   2 = the persistent single launch only (up to 64 nodes):
+ *     ssd_tree_verify and ssd_graph_capture_verify return SSD_E_UNSUPPORTED
+ *     where it does not apply.
+ * The persistent launch runs every layer in one kernel: 256 workgroups (one
+ * per CU) hand results to each other through flags in device memory.  Every
+ * wait inside it is bounded; if one times out (200 ms) the
  * launch ends early, its logits are undefined, and the session's error
  * counter (ssd_kv_error_count) is incremented.  Both ways meet the same
  * tolerance against the definition; their logits differ in the last bits.

@@ -269,6 +269,19 @@ __device__ __forceinline__ void stamp(const FusedArgs& a, const Wg& w, int l, in
     a.trace[(((size_t)w.g * (a.L + 1) + l) * kFStages + s) * 3 + k] = now();
 }
 
+// Workgroup barrier that orders LDS accesses only: outstanding global stores
+// are not waited for (signal() waits for them before a stage is published).
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// (measurement) sub-stage timestamps of one stage of one layer, when a.sub is set
+__device__ __forceinline__ void sub_stamp(const FusedArgs& a, const Wg& w, int l, int k) {
+  if (a.sub && l == a.sub_l && threadIdx.x == 0) a.sub[(size_t)w.g * 16 + k] = now();
+}
+
 // ------------------------------------------------------------------ per-layer parameters
 
 enum LwSlot { LW_QKV = 0, LW_O, LW_FC, LW_PR, LB_QKV, LB_O, LB_FC, LB_PR, LN1G, LN1B, LN2G, LN2B };
@@ -286,7 +299,7 @@ __device__ __forceinline__ const void* lw(const FusedArgs& a, int l, int slot) {
 template <int E>
 __device__ __forceinline__ bool ln_row(const FusedArgs& a, const Wg& w, const WaitSpec& ws, int n, int mode,
                                        gptr<uint16_t> bias, const float* part, const int* xrange, gptr<uint16_t> g,
-                                       gptr<uint16_t> b, uint16_t* act, float* red, bool dbg) {
+                                       gptr<uint16_t> b, uint16_t* act, float* red) {
   const int d = a.d, tid = opq_tid();
   const gw<float> xr = opq(a.xr + ((size_t)w.x * kFMaxN + n) * d);
   bias = opq(bias);
@@ -335,10 +348,6 @@ __device__ __forceinline__ bool ln_row(const FusedArgs& a, const Wg& w, const Wa
 #pragma unroll
       for (int i = 0; i < E; ++i) pv[X][i] = ld_dev(prow + kk[i]);
     }
-    if (dbg && threadIdx.x == 0) {
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      a.trace[(((size_t)w.g * (a.L + 1) + a.dbg_l) * kFStages + FS_SPARE) * 3 + 0] = now();
-    }
     // bias, then the partials of the XCDs that own a share, in XCD order
 #pragma unroll
     for (int i = 0; i < E; ++i) {
@@ -372,16 +381,10 @@ __device__ __forceinline__ bool ln_row(const FusedArgs& a, const Wg& w, const Wa
   for (int i = 0; i < E; ++i)
     if (tid + i * NTH < d) q += (v[i] - mean) * (v[i] - mean);
   const float den = sqrtf(bsum(q) / d + a.eps);
-  if (dbg && threadIdx.x == 0)
-    a.trace[(((size_t)w.g * (a.L + 1) + a.dbg_l) * kFStages + FS_SPARE) * 3 + 1] = now();
 #pragma unroll
   for (int i = 0; i < E; ++i) {
     const int k = tid + i * NTH;
     if (k < d) st_act(actg, n, k, d / 32, (v[i] - mean) / den * bf2f(gr[i]) + bf2f(br[i]));
-  }
-  if (dbg && threadIdx.x == 0) {
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    a.trace[(((size_t)w.g * (a.L + 1) + a.dbg_l) * kFStages + FS_SPARE) * 3 + 2] = now();
   }
   return true;
 }
@@ -426,7 +429,9 @@ __device__ __forceinline__ bool gemm_rb(const FusedArgs& a, const Wg& w, const W
                                         int KC, int M, int kc0, int kc1, const uint16_t* act, int act_kc,
                                         float* red) {
   constexpr int NN = 16 * NT;
-  const int tid = opq_tid(), wv = tid >> 6, lane = tid & 63;
+  // the wave index and step count are scalars, so the step guards below are
+  // scalar branches: an MFMA ignores EXEC and must never sit under a lane mask
+  const int tid = opq_tid(), wv = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int nsteps = kc1 - kc0 > wv ? (kc1 - kc0 - wv + NWV - 1) / NWV : 0;
   Wp = opq(Wp);
   const gptr<uint16_t> actg = opq(act);
@@ -439,14 +444,14 @@ __device__ __forceinline__ bool gemm_rb(const FusedArgs& a, const Wg& w, const W
   }
   // this thread's epilogue row of every row block is tid % 16: its bias is
   // loaded before the k-loop
-  float bias_r[RB];
-  {
-    uint16_t raw[RB];
+  // The load is unconditional (a GEMM without bias reads a word of its own
+  // weights instead, and discards it in the epilogue): a conditional load
+  // would be waited for on the spot.
+  const bool has_bias = bias != nullptr;
+  const gptr<uint16_t> bsrc = has_bias ? bias : (gptr<uint16_t>)Wp;
+  uint16_t bias_r[RB];
 #pragma unroll
-    for (int r = 0; r < RB; ++r) raw[r] = bias ? bias[rbv[r] * 16 + (tid & 15)] : (uint16_t)0;
-#pragma unroll
-    for (int r = 0; r < RB; ++r) bias_r[r] = bf2f(raw[r]);
-  }
+  for (int r = 0; r < RB; ++r) bias_r[r] = bsrc[rbv[r] * 16 + (tid & 15)];
   gptr<u32x4> wb[RB];
 #pragma unroll
   for (int r = 0; r < RB; ++r) wb[r] = Wp + (size_t)rbv[r] * KC * 64 + lane;
@@ -475,35 +480,40 @@ __device__ __forceinline__ bool gemm_rb(const FusedArgs& a, const Wg& w, const W
     for (int t = 0; t < NT; ++t) acc[r][t] = (f32x4){0.f, 0.f, 0.f, 0.f};
   // the first U steps' weights do not depend on the previous stage: they are
   // in flight while the workgroup waits for it
-  if (nsteps > 0) {
+  // only the steps this wave owns are loaded (the step bounds are uniform
+  // per wave, so the guards are scalar branches)
 #pragma unroll
-    for (int u = 0; u < U; ++u) load_w(u, u);
-  }
+  for (int u = 0; u < U; ++u)
+    if (u < nsteps) load_w(u, u);
   if (ws.on && !wait_flags(a, w, ws.id, ws.wx, ws.tag)) return false;
   stamp(a, w, ws.sl, ws.sfid, 1);
-  if (nsteps > 0) {
+  const bool sub = epi == a.sub_epi;
+  if (sub) sub_stamp(a, w, l, 0);
 #pragma unroll
-    for (int u = 0; u < U; ++u) load_a(u, u);
-    __builtin_amdgcn_sched_barrier(0);
-    for (int s0 = 0; s0 < nsteps; s0 += U) {
+  for (int u = 0; u < U; ++u)
+    if (u < nsteps) load_a(u, u);
+  __builtin_amdgcn_sched_barrier(0);
+  for (int s0 = 0; s0 < nsteps; s0 += U) {
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const bool ok = s0 + u < nsteps;
+    for (int u = 0; u < U; ++u) {
+      if (s0 + u < nsteps) {
 #pragma unroll
-        for (int r = 0; r < RB; ++r) {
-          const u32x4 wf = ok ? wq[u][r] : (u32x4){0, 0, 0, 0};
+        for (int r = 0; r < RB; ++r)
 #pragma unroll
           for (int t = 0; t < NT; ++t)
-            acc[r][t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, wf),
+            acc[r][t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, wq[u][r]),
                                                                __builtin_bit_cast(f16x8, bq[u][t]), acc[r][t], 0, 0, 0);
-        }
-        __builtin_amdgcn_sched_barrier(0);
-        load_step(s0 + u + U, u);
-        __builtin_amdgcn_sched_barrier(0);
       }
+      __builtin_amdgcn_sched_barrier(0);
+      if (s0 + u + U < nsteps) load_step(s0 + u + U, u);
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
   const int N = a.N;
+  if (sub) {
+    if (threadIdx.x == 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    sub_stamp(a, w, l, 1);
+  }
 #pragma unroll
   for (int r = 0; r < RB; ++r) {
     if (r >= nrb) break;
@@ -511,17 +521,24 @@ __device__ __forceinline__ bool gemm_rb(const FusedArgs& a, const Wg& w, const W
     for (int t = 0; t < NT; ++t)
 #pragma unroll
       for (int q = 0; q < 4; ++q) red[((wv * NN) + 16 * t + (lane & 15)) * 16 + 4 * (lane >> 4) + q] = acc[r][t][q];
-    __syncthreads();
-    for (int idx = tid; idx < NN * 16; idx += NTH) {
+    lds_barrier();
+    // a compile-time count of slots per thread: a run-time loop here holding
+    // stores would make the compiler wait for all earlier stores first
+#pragma unroll
+    for (int i = 0; i < (NN * 16 + NTH - 1) / NTH; ++i) {
+      const int idx = tid + i * NTH;
+      if (NN * 16 % NTH != 0 && idx >= NN * 16) break;
       const int row = idx & 15, node = idx >> 4;
       float sum = red[idx];
 #pragma unroll
       for (int ww = 1; ww < NWV; ++ww) sum += red[ww * NN * 16 + idx];
       const int o = rbv[r] * 16 + row;
-      if (node < N && o < M) epilogue(a, w, epi, l, node, o, sum + bias_r[r]);
+      if (node < N && o < M) epilogue(a, w, epi, l, node, o, has_bias ? sum + bf2f(bias_r[r]) : sum);
     }
-    __syncthreads();
+    lds_barrier();
+    if (sub && r == 0) sub_stamp(a, w, l, 2);
   }
+  if (sub) sub_stamp(a, w, l, 3);
   return true;
 }
 
@@ -541,36 +558,46 @@ __device__ __forceinline__ bool gemm_task(const FusedArgs& a, const Wg& w, const
   return gemm_rb<NT, 4, 4>(a, w, ws, epi, l, rbs, rb_first, nrb, bias, Wp, KC, M, kc0, kc1, act, act_kc, red);
 }
 
-// ------------------------------------------------------------------ tree attention, one head x 16-node tile
+// ------------------------------------------------------------------ tree attention
 //
 // Node i attends to cache rows 0..P-1 and then to its root path in the tree
 // scratch (Sec. 3.1: cross-attention with the cache, self-attention in the
-// batch masked by the tree).  The prefix is staged 128 rows at a time (K rows
-// and V^T in LDS); wave w takes rows 32w..32w+31 of every chunk on the matrix
-// cores (S^T = K Q^T, O^T = V^T P^T with v_mfma_f32_16x16x32_bf16; q and p as
-// bf16 hi + lo, K and V exact) with its own online softmax.  The K operand's
-// rows are ordered so that lane l holds the scores of keys 8(l/16)..+7 of node
-// l%16, which is exactly its slot of the P^T operand.  Each half-wave then
-// takes a node's root path on the vector ALU (root first, 32 keys per batch).
-// The four prefix parts and the root-path part are merged in that order.
+// batch masked by the tree).  Per (head h, 16-node tile t) the work is cut
+// into units that run on different workgroups of the head's XCD:
+//  * prefix unit p: cache rows 256p .. 256p + 255 (staged as K and V rows in
+//    LDS).  Wave w takes rows 32w .. 32w + 31 on the matrix cores (S^T = K Q^T
+//    and O^T = V^T P^T with v_mfma_f32_16x16x32_bf16; q and p as bf16 hi + lo,
+//    K and V exact).  The K operand's rows are ordered so that lane l holds
+//    the scores of keys 8(l/16)..+7 of node l%16, exactly its slot of the P^T
+//    operand; the V^T operand is gathered from the row-major V rows.  The 8
+//    waves' softmax states are merged in wave order;
+//  * the root unit: each half-wave takes one node's root path on the vector
+//    ALU, root first, 32 keys per batch.
+// Every unit leaves a part (max, sum of exponentials, unnormalised output) per
+// node; the merge stage combines a tile's parts in order (prefix parts, then
+// the root path).  The cut depends on P only, so a node's result does not
+// depend on the rest of the tree.
 
-constexpr int ACH = 32 * NWV;               // prefix rows per chunk: 32 per wave
-constexpr int AKS = DH + 8;                 // LDS row stride of K (elements)
-constexpr int AVS = AKS;                    // LDS row stride of V (row-major like K)
+constexpr int ACH = 32 * NWV;               // prefix rows per unit: 32 per wave
+static_assert(ACH == kFAttRows, "the host counts attention units of kFAttRows rows");
+constexpr int AKS = DH + 8;                 // LDS row stride of K and V (elements)
 constexpr int AREC = DH + 4;                // part record: max, sum, -, -, output
 constexpr int A_KV_BYTES = 2 * ACH * AKS * 2;
-constexpr int A_RV_BYTES = 2 * NWV * 32 * DH * 2;                 // root-path V rows, 32 per half-wave
+constexpr int A_RV_BYTES = 2 * NWV * 32 * DH * 2;  // root-path V rows, 32 per half-wave
 constexpr int A_REGION = A_KV_BYTES > A_RV_BYTES ? A_KV_BYTES : A_RV_BYTES;
-constexpr int A_PART_BYTES = (NWV * 16 + 16) * AREC * 4;
-constexpr int A_Q_BYTES = NWV * 2 * DH * 4;
+constexpr int A_PART_BYTES = NWV * 16 * AREC * 4;  // the waves' states of a prefix unit
+constexpr int A_Q_BYTES = NWV * 2 * DH * 4;        // root-path queries, one row per half-wave
 
-__device__ __forceinline__ bool attention_task(const FusedArgs& a, const Wg& w, const WaitSpec& ws, int l, int h, int t,
-                                               unsigned char* lds, bool dbg) {
+// the part record of (head h, tile t, unit u) for tile node nl
+__device__ __forceinline__ gw<float> part_rec(const FusedArgs& a, int h, int t, int u, int nl) {
+  return (gw<float>)a.apart + ((((size_t)h * 4 + t) * (a.att_units + 1) + u) * 16 + nl) * AREC;
+}
+
+__device__ __forceinline__ bool att_prefix_unit(const FusedArgs& a, const Wg& w, const WaitSpec& ws, int l, int h,
+                                                int t, int u, unsigned char* lds) {
   uint16_t* ks = (uint16_t*)lds;
   uint16_t* vs = ks + ACH * AKS;
   float* wpart = (float*)(lds + A_REGION);  // [NWV][16][AREC]
-  float* rpart = wpart + NWV * 16 * AREC;   // [16][AREC]
-  float* qrow = rpart + 16 * AREC;          // [NWV][2][DH]
   const int tid = opq_tid(), wv = tid >> 6, lane = tid & 63, i = lane & 15, g = lane >> 4;
   const int N = a.N, P = a.P, d = a.d;
   const float scale = a.scale;
@@ -578,41 +605,19 @@ __device__ __forceinline__ bool attention_task(const FusedArgs& a, const Wg& w, 
   const gptr<uint16_t> kc = opq(a.kc + head_rows * a.max_ctx * DH);
   const gptr<uint16_t> vc = opq(a.vc + head_rows * a.max_ctx * DH);
   const gptr<float> qbase = opq((const float*)a.q);
-  const gptr<int> tree = opq(a.tree);
-  constexpr int DPL = DH / 32;  // root path: dims per lane of a half-wave
-  const int hw = lane >> 5, hl = lane & 31;
-
-  // 1. What does not depend on this layer's QKV outputs: the cached prefix
-  //    (first two chunks, two register sets) and the root-path indices of
-  //    this half-wave's node.
-  const int nchunks = (P + ACH - 1) / ACH;
-  u32x4 kA[4], vA[4], kB[4], vB[4];
-  auto load_chunk = [&](int c, u32x4(&kr)[4], u32x4(&vr)[4]) {
-    const int cb = c * ACH, ck = min(ACH, P - cb);
+  const int cb = u * ACH, nk = min(ACH, P - cb);
+  // the unit's cache rows do not depend on this layer's QKV outputs: loaded
+  // before the wait (rows past the prefix re-read the last one, zeroed below)
+  u32x4 kr[4], vr[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int e = tid + j * NTH, r = min(e >> 3, ck - 1), c8 = e & 7;
-      kr[j] = *(gptr<u32x4>)(kc + (size_t)(cb + r) * DH + 8 * c8);
-      vr[j] = *(gptr<u32x4>)(vc + (size_t)(cb + r) * DH + 8 * c8);
-    }
-  };
-  if (nchunks > 0) load_chunk(0, kA, vA);
-  if (nchunks > 1) load_chunk(1, kB, vB);
-  const gptr<int> depth = tree + 2 * a.max_nodes;
-  const gptr<int> anc_off = tree + 4 * a.max_nodes;
-  const gptr<int> path32 = tree + 5 * a.max_nodes;
-  const gptr<int> ancl = path32 + (size_t)N * kPath32;
-  const int rnl = 2 * wv + hw;  // this half-wave's node within the tile
-  const int rnc = min(16 * t + rnl, N - 1);
-  int rkey = ld_x(path32 + (size_t)rnc * kPath32 + hl);
-  const int rdep = ld_x(depth + rnc);
-
-  // 2. The dependency.
+  for (int j = 0; j < 4; ++j) {
+    const int e = tid + j * NTH, r = min(e >> 3, nk - 1), c8 = e & 7;
+    kr[j] = *(gptr<u32x4>)(kc + (size_t)(cb + r) * DH + 8 * c8);
+    vr[j] = *(gptr<u32x4>)(vc + (size_t)(cb + r) * DH + 8 * c8);
+  }
   if (ws.on && !wait_flags(a, w, ws.id, ws.wx, ws.tag)) return false;
   stamp(a, w, ws.sl, ws.sfid, 1);
-
-  // 3. Queries (B operand: node 16 t + i, dims 32 kc2 + 8 g .. +8) and the
-  //    first 32 root-path K/V rows.
+  // queries (B operand: node 16 t + i, dims 32 kc2 + 8 g .. +8)
   const int qn = min(16 * t + i, N - 1);
   u32x4 qh[2], ql[2];
 #pragma unroll
@@ -624,97 +629,69 @@ __device__ __forceinline__ bool attention_task(const FusedArgs& a, const Wg& w, 
                         __uint_as_float(q1[2]), __uint_as_float(q1[3])};
     pack_hilo8(v, qh[kc2], ql[kc2]);
   }
-  const gptr<uint16_t> ktb = opq((const uint16_t*)a.kt + head_rows * a.max_nodes * DH);
-  const gptr<uint16_t> vtb = opq((const uint16_t*)a.vt + head_rows * a.max_nodes * DH);
-  u32x4 rk[DH / 8], rv[DH / 8];
-  // issued once the last prefix chunk is staged, so that no chunk waits for them
-  auto load_root = [&]() {
 #pragma unroll
-    for (int j = 0; j < DH / 8; ++j) {
-      rk[j] = ld_x((gptr<u32x4>)(ktb + (size_t)rkey * DH + 8 * j));
-      rv[j] = ld_x((gptr<u32x4>)(vtb + (size_t)rkey * DH + 8 * j));
-    }
-  };
-  if (nchunks == 0) load_root();
-
-  // 4. Prefix chunks, two in flight: chunk c + 2 is loaded into the
-  //    registers chunk c has just left.
+  for (int j = 0; j < 4; ++j) {
+    const int e = tid + j * NTH, r = e >> 3, c8 = e & 7;
+    const bool ok = r < nk;
+    *(u32x4*)(ks + r * AKS + 8 * c8) = ok ? kr[j] : (u32x4){0, 0, 0, 0};
+    *(u32x4*)(vs + r * AKS + 8 * c8) = ok ? vr[j] : (u32x4){0, 0, 0, 0};
+  }
+  __syncthreads();
   float m = -INFINITY, lsum = 0.f;
   f32x4 o[4];
 #pragma unroll
   for (int tt = 0; tt < 4; ++tt) o[tt] = (f32x4){0.f, 0.f, 0.f, 0.f};
-  auto run_chunk = [&](int c, u32x4(&kr)[4], u32x4(&vr)[4]) {
-    const int nk = min(ACH, P - c * ACH);
-    __syncthreads();  // the previous chunk has been read
+  if (32 * wv < nk) {
+    const uint16_t* kb = ks + (32 * wv + 8 * (i >> 2) + (i & 3)) * AKS + 8 * g;
+    f32x4 s0 = (f32x4){0, 0, 0, 0}, s1 = (f32x4){0, 0, 0, 0};
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int e = tid + j * NTH, r = e >> 3, c8 = e & 7;
-      const bool ok = r < nk;
-      *(u32x4*)(ks + r * AKS + 8 * c8) = ok ? kr[j] : (u32x4){0, 0, 0, 0};
-      *(u32x4*)(vs + r * AVS + 8 * c8) = ok ? vr[j] : (u32x4){0, 0, 0, 0};
+    for (int kc2 = 0; kc2 < 2; ++kc2) {
+      const u32x4 k0 = *(const u32x4*)(kb + 32 * kc2);
+      const u32x4 k1 = *(const u32x4*)(kb + 4 * AKS + 32 * kc2);
+      s0 = mfma_bf16(k0, qh[kc2], s0);
+      s0 = mfma_bf16(k0, ql[kc2], s0);
+      s1 = mfma_bf16(k1, qh[kc2], s1);
+      s1 = mfma_bf16(k1, ql[kc2], s1);
     }
-    if (c + 2 < nchunks) load_chunk(c + 2, kr, vr);
-    if (c == nchunks - 1) load_root();
-    __syncthreads();
-    if (32 * wv < nk) {
-      const uint16_t* kb = ks + (32 * wv + 8 * (i >> 2) + (i & 3)) * AKS + 8 * g;
-      f32x4 s0 = (f32x4){0, 0, 0, 0}, s1 = (f32x4){0, 0, 0, 0};
+    float sv[8];
 #pragma unroll
-      for (int kc2 = 0; kc2 < 2; ++kc2) {
-        const u32x4 k0 = *(const u32x4*)(kb + 32 * kc2);
-        const u32x4 k1 = *(const u32x4*)(kb + 4 * AKS + 32 * kc2);
-        s0 = mfma_bf16(k0, qh[kc2], s0);
-        s0 = mfma_bf16(k0, ql[kc2], s0);
-        s1 = mfma_bf16(k1, qh[kc2], s1);
-        s1 = mfma_bf16(k1, ql[kc2], s1);
-      }
-      float sv[8];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int key = 32 * wv + 8 * g + r;
-        sv[r] = key < nk ? s0[r] * scale : -INFINITY;
-        sv[4 + r] = key + 4 < nk ? s1[r] * scale : -INFINITY;
-      }
-      float mb = sv[0];
-#pragma unroll
-      for (int e = 1; e < 8; ++e) mb = fmaxf(mb, sv[e]);
-      mb = fmaxf(mb, __shfl_xor(mb, 16));
-      mb = fmaxf(mb, __shfl_xor(mb, 32));
-      const float mn = fmaxf(m, mb);
-      const float alpha = __expf(m - mn);
-      float pv[8], ps = 0.f;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        pv[e] = __expf(sv[e] - mn);
-        ps += pv[e];
-      }
-      ps += __shfl_xor(ps, 16);
-      ps += __shfl_xor(ps, 32);
-      lsum = fmaf(lsum, alpha, ps);
-      m = mn;
-      u32x4 ph, pl;
-      pack_hilo8(pv, ph, pl);
-#pragma unroll
-      for (int tt = 0; tt < 4; ++tt) {
-        // A operand V^T (16 dims x 32 keys): lane (i, g) gathers dim 16 tt + i
-        // of keys 8 g .. 8 g + 7 of this wave's 32 from the row-major rows
-        const uint16_t* vcol = vs + (32 * wv + 8 * g) * AVS + 16 * tt + i;
-        uint32_t h[8];
-#pragma unroll
-        for (int jj = 0; jj < 8; ++jj) h[jj] = vcol[jj * AVS];
-        const u32x4 va = (u32x4){h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
-        o[tt] = o[tt] * alpha;
-        o[tt] = mfma_bf16(va, ph, o[tt]);
-        o[tt] = mfma_bf16(va, pl, o[tt]);
-      }
+    for (int r = 0; r < 4; ++r) {
+      const int key = 32 * wv + 8 * g + r;
+      sv[r] = key < nk ? s0[r] * scale : -INFINITY;
+      sv[4 + r] = key + 4 < nk ? s1[r] * scale : -INFINITY;
     }
-  };
-  for (int c = 0; c < nchunks; c += 2) {
-    run_chunk(c, kA, vA);
-    if (c + 1 < nchunks) run_chunk(c + 1, kB, vB);
+    float mb = sv[0];
+#pragma unroll
+    for (int e = 1; e < 8; ++e) mb = fmaxf(mb, sv[e]);
+    mb = fmaxf(mb, __shfl_xor(mb, 16));
+    mb = fmaxf(mb, __shfl_xor(mb, 32));
+    m = mb;
+    float pv[8], ps = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      pv[e] = __expf(sv[e] - m);
+      ps += pv[e];
+    }
+    ps += __shfl_xor(ps, 16);
+    ps += __shfl_xor(ps, 32);
+    lsum = ps;
+    u32x4 ph, pl;
+    pack_hilo8(pv, ph, pl);
+#pragma unroll
+    for (int tt = 0; tt < 4; ++tt) {
+      // A operand V^T (16 dims x 32 keys): lane (i, g) gathers dim 16 tt + i
+      // of keys 8 g .. 8 g + 7 of this wave's 32 from the row-major rows
+      const uint16_t* vcol = vs + (32 * wv + 8 * g) * AKS + 16 * tt + i;
+      uint32_t hh[8];
+#pragma unroll
+      for (int jj = 0; jj < 8; ++jj) hh[jj] = vcol[jj * AKS];
+      const u32x4 va = (u32x4){hh[0] | (hh[1] << 16), hh[2] | (hh[3] << 16), hh[4] | (hh[5] << 16),
+                               hh[6] | (hh[7] << 16)};
+      o[tt] = mfma_bf16(va, ph, o[tt]);
+      o[tt] = mfma_bf16(va, pl, o[tt]);
+    }
   }
-  if (dbg && threadIdx.x == 0) a.trace[(((size_t)w.g * (a.L + 1) + a.dbg_l + 1) * kFStages + FS_SPARE) * 3 + 0] = now();
-  // this wave's prefix part of node 16 t + i: lane (i, g) holds dims 16 tt + 4 g + r
+  // this wave's state of node 16 t + i: lane (i, g) holds dims 16 tt + 4 g + r
   {
     float* rec = wpart + (wv * 16 + i) * AREC;
     if (g == 0) {
@@ -724,102 +701,17 @@ __device__ __forceinline__ bool attention_task(const FusedArgs& a, const Wg& w, 
 #pragma unroll
     for (int tt = 0; tt < 4; ++tt) *(f32x4*)(rec + 4 + 16 * tt + 4 * g) = o[tt];
   }
-  __syncthreads();  // K/V staging region is reused for root-path V rows
-
-  // 5. Root path: half-wave (wv, hw) takes node 2 wv + hw of the tile on the
-  //    vector ALU, root first, 32 keys per batch.
-  {
-    uint16_t* rvl = (uint16_t*)lds + (2 * wv + hw) * 32 * DH;  // [32 keys][DH]
-    float* qr = qrow + (wv * 2 + hw) * DH;
-    {
-      const int nl = rnl;
-      const int n = 16 * t + nl;
-      {
-        const gptr<float> qp = qbase + (size_t)rnc * d + h * DH + hl * DPL;
-#pragma unroll
-        for (int e = 0; e < DPL; ++e) qr[hl * DPL + e] = ld_x(qp + e);
-      }
-      float rm = -INFINITY, rl = 0.f, ro[DPL];
-#pragma unroll
-      for (int e = 0; e < DPL; ++e) ro[e] = 0.f;
-      const int rbatches = (max(rdep, __shfl_xor(rdep, 32)) + 32) / 32;  // wave-uniform
-      for (int bt = 0; bt < rbatches; ++bt) {
-        const int j = 32 * bt + hl;
-        if (bt > 0) {
-          rkey = ld_x(ancl + ld_x(anc_off + rnc) + min(j, rdep));
-#pragma unroll
-          for (int jj = 0; jj < DH / 8; ++jj) {
-            rk[jj] = ld_x((gptr<u32x4>)(ktb + (size_t)rkey * DH + 8 * jj));
-            rv[jj] = ld_x((gptr<u32x4>)(vtb + (size_t)rkey * DH + 8 * jj));
-          }
-        }
-#pragma unroll
-        for (int jj = 0; jj < DH / 8; ++jj) *(u32x4*)(rvl + hl * DH + 8 * jj) = rv[jj];
-        wave_sync_lds();
-        float dot = 0.f;
-#pragma unroll
-        for (int c8 = 0; c8 < DH / 8; ++c8) {
-          const f32x4 qa = *(const f32x4*)&qr[8 * c8];
-          const f32x4 qb = *(const f32x4*)&qr[8 * c8 + 4];
-          const u32x4 ku = rk[c8];
-          dot = fmaf(qa[0], __uint_as_float(ku[0] << 16), dot);
-          dot = fmaf(qa[1], __uint_as_float(ku[0] & 0xffff0000u), dot);
-          dot = fmaf(qa[2], __uint_as_float(ku[1] << 16), dot);
-          dot = fmaf(qa[3], __uint_as_float(ku[1] & 0xffff0000u), dot);
-          dot = fmaf(qb[0], __uint_as_float(ku[2] << 16), dot);
-          dot = fmaf(qb[1], __uint_as_float(ku[2] & 0xffff0000u), dot);
-          dot = fmaf(qb[2], __uint_as_float(ku[3] << 16), dot);
-          dot = fmaf(qb[3], __uint_as_float(ku[3] & 0xffff0000u), dot);
-        }
-        const bool kvalid = j <= rdep;
-        const float sc = kvalid ? dot * scale : -INFINITY;
-        float mb = sc;
-#pragma unroll
-        for (int off = 1; off < 32; off <<= 1) mb = fmaxf(mb, __shfl_xor(mb, off));
-        const float mn = fmaxf(rm, mb);
-        const float alpha = __expf(rm - mn);
-        const float p = kvalid ? __expf(sc - mn) : 0.f;
-        float ps = p;
-#pragma unroll
-        for (int off = 1; off < 32; off <<= 1) ps += __shfl_xor(ps, off);
-        rl = fmaf(rl, alpha, ps);
-        rm = mn;
-        const int cnt = min(32, rdep + 1 - 32 * bt);
-        const int cmax = max(cnt, __shfl_xor(cnt, 32));  // wave-uniform
-        float acc[DPL];
-#pragma unroll
-        for (int e = 0; e < DPL; ++e) acc[e] = 0.f;
-        for (int jj = 0; jj < cmax; ++jj) {
-          const float pj = jj < cnt ? __shfl(p, (hw << 5) + jj) : 0.f;
-          const uint16_t* vr2 = rvl + jj * DH + DPL * hl;
-#pragma unroll
-          for (int e = 0; e < DPL; ++e) acc[e] = fmaf(pj, bf2f(vr2[e]), acc[e]);
-        }
-#pragma unroll
-        for (int e = 0; e < DPL; ++e) ro[e] = fmaf(ro[e], alpha, acc[e]);
-        wave_sync_lds();
-      }
-      float* rec = rpart + nl * AREC;
-      if (hl == 0) {
-        rec[0] = rm;
-        rec[1] = rl;
-      }
-#pragma unroll
-      for (int e = 0; e < DPL; ++e) rec[4 + DPL * hl + e] = ro[e];
-    }
-  }
   __syncthreads();
-  if (dbg && threadIdx.x == 0) a.trace[(((size_t)w.g * (a.L + 1) + a.dbg_l + 1) * kFStages + FS_SPARE) * 3 + 1] = now();
-  // merge: thread -> node, DPT consecutive dims; the wave parts in wave order, then the root path
+  // the waves merged in wave order into the unit's part: thread -> node,
+  // DPT consecutive dims
   {
-    constexpr int DPT = 16 * DH / NTH;  // output dims per thread
+    constexpr int DPT = 16 * DH / NTH;
     const int nl = tid / (DH / DPT), d0 = DPT * (tid % (DH / DPT));
-    const int n = 16 * t + nl;
     float M = -INFINITY, L = 0.f, O[DPT];
 #pragma unroll
     for (int e = 0; e < DPT; ++e) O[e] = 0.f;
-    for (int j = 0; j <= NWV; ++j) {
-      const float* rec = j < NWV ? wpart + (j * 16 + nl) * AREC : rpart + nl * AREC;
+    for (int j = 0; j < NWV; ++j) {
+      const float* rec = wpart + (j * 16 + nl) * AREC;
       const float mj = rec[0], lj = rec[1];
       if (mj == -INFINITY) continue;
       const float mn = fmaxf(M, mj);
@@ -829,12 +721,156 @@ __device__ __forceinline__ bool attention_task(const FusedArgs& a, const Wg& w, 
       for (int e = 0; e < DPT; ++e) O[e] = fmaf(O[e], al, rec[4 + d0 + e] * wj);
       M = mn;
     }
-    if (n < N) {
-#pragma unroll
-      for (int e = 0; e < DPT; ++e) st_act(a.fo, n, h * DH + d0 + e, d / 32, O[e] / L);
+    const gw<float> out = part_rec(a, h, t, u, nl);
+    if (d0 == 0) {
+      out[0] = M;
+      out[1] = L;
     }
+#pragma unroll
+    for (int e = 0; e < DPT; ++e) out[4 + d0 + e] = O[e];
   }
   __syncthreads();
+  return true;
+}
+
+__device__ __forceinline__ bool att_root_unit(const FusedArgs& a, const Wg& w, const WaitSpec& ws, int l, int h,
+                                              int t, unsigned char* lds) {
+  float* qrow = (float*)(lds + A_REGION + A_PART_BYTES);  // [NWV][2][DH]
+  const int tid = opq_tid(), wv = tid >> 6, lane = tid & 63;
+  const int N = a.N, d = a.d;
+  const float scale = a.scale;
+  const size_t head_rows = ((size_t)l * a.H + h);
+  const gptr<float> qbase = opq((const float*)a.q);
+  const gptr<int> tree = opq(a.tree);
+  constexpr int DPL = DH / 32;  // dims per lane of a half-wave
+  const int hw = lane >> 5, hl = lane & 31;
+  const gptr<int> depth = tree + 2 * a.max_nodes;
+  const gptr<int> anc_off = tree + 4 * a.max_nodes;
+  const gptr<int> path32 = tree + 5 * a.max_nodes;
+  const gptr<int> ancl = path32 + (size_t)N * kPath32;
+  const int nl = 2 * wv + hw;  // this half-wave's node within the tile
+  const int rnc = min(16 * t + nl, N - 1);
+  // the tree's indices are known before this layer's QKV outputs are
+  int rkey = ld_x(path32 + (size_t)rnc * kPath32 + hl);
+  const int rdep = ld_x(depth + rnc);
+  if (ws.on && !wait_flags(a, w, ws.id, ws.wx, ws.tag)) return false;
+  stamp(a, w, ws.sl, ws.sfid, 1);
+  const gptr<uint16_t> ktb = opq((const uint16_t*)a.kt + head_rows * a.max_nodes * DH);
+  const gptr<uint16_t> vtb = opq((const uint16_t*)a.vt + head_rows * a.max_nodes * DH);
+  u32x4 rk[DH / 8], rv[DH / 8];
+#pragma unroll
+  for (int j = 0; j < DH / 8; ++j) {
+    rk[j] = ld_x((gptr<u32x4>)(ktb + (size_t)rkey * DH + 8 * j));
+    rv[j] = ld_x((gptr<u32x4>)(vtb + (size_t)rkey * DH + 8 * j));
+  }
+  uint16_t* rvl = (uint16_t*)lds + (2 * wv + hw) * 32 * DH;  // [32 keys][DH]
+  float* qr = qrow + (wv * 2 + hw) * DH;
+  {
+    const gptr<float> qp = qbase + (size_t)rnc * d + h * DH + hl * DPL;
+#pragma unroll
+    for (int e = 0; e < DPL; ++e) qr[hl * DPL + e] = ld_x(qp + e);
+  }
+  float rm = -INFINITY, rl = 0.f, ro[DPL];
+#pragma unroll
+  for (int e = 0; e < DPL; ++e) ro[e] = 0.f;
+  const int rbatches = (max(rdep, __shfl_xor(rdep, 32)) + 32) / 32;  // wave-uniform
+  for (int bt = 0; bt < rbatches; ++bt) {
+    const int j = 32 * bt + hl;
+    if (bt > 0) {
+      rkey = ld_x(ancl + ld_x(anc_off + rnc) + min(j, rdep));
+#pragma unroll
+      for (int jj = 0; jj < DH / 8; ++jj) {
+        rk[jj] = ld_x((gptr<u32x4>)(ktb + (size_t)rkey * DH + 8 * jj));
+        rv[jj] = ld_x((gptr<u32x4>)(vtb + (size_t)rkey * DH + 8 * jj));
+      }
+    }
+#pragma unroll
+    for (int jj = 0; jj < DH / 8; ++jj) *(u32x4*)(rvl + hl * DH + 8 * jj) = rv[jj];
+    wave_sync_lds();
+    float dot = 0.f;
+#pragma unroll
+    for (int c8 = 0; c8 < DH / 8; ++c8) {
+      const f32x4 qa = *(const f32x4*)&qr[8 * c8];
+      const f32x4 qb = *(const f32x4*)&qr[8 * c8 + 4];
+      const u32x4 ku = rk[c8];
+      dot = fmaf(qa[0], __uint_as_float(ku[0] << 16), dot);
+      dot = fmaf(qa[1], __uint_as_float(ku[0] & 0xffff0000u), dot);
+      dot = fmaf(qa[2], __uint_as_float(ku[1] << 16), dot);
+      dot = fmaf(qa[3], __uint_as_float(ku[1] & 0xffff0000u), dot);
+      dot = fmaf(qb[0], __uint_as_float(ku[2] << 16), dot);
+      dot = fmaf(qb[1], __uint_as_float(ku[2] & 0xffff0000u), dot);
+      dot = fmaf(qb[2], __uint_as_float(ku[3] << 16), dot);
+      dot = fmaf(qb[3], __uint_as_float(ku[3] & 0xffff0000u), dot);
+    }
+    const bool kvalid = j <= rdep;
+    const float sc = kvalid ? dot * scale : -INFINITY;
+    float mb = sc;
+#pragma unroll
+    for (int off = 1; off < 32; off <<= 1) mb = fmaxf(mb, __shfl_xor(mb, off));
+    const float mn = fmaxf(rm, mb);
+    const float alpha = __expf(rm - mn);
+    const float p = kvalid ? __expf(sc - mn) : 0.f;
+    float ps = p;
+#pragma unroll
+    for (int off = 1; off < 32; off <<= 1) ps += __shfl_xor(ps, off);
+    rl = fmaf(rl, alpha, ps);
+    rm = mn;
+    const int cnt = min(32, rdep + 1 - 32 * bt);
+    const int cmax = max(cnt, __shfl_xor(cnt, 32));  // wave-uniform
+    float acc[DPL];
+#pragma unroll
+    for (int e = 0; e < DPL; ++e) acc[e] = 0.f;
+    for (int jj = 0; jj < cmax; ++jj) {
+      const float pj = jj < cnt ? __shfl(p, (hw << 5) + jj) : 0.f;
+      const uint16_t* vr2 = rvl + jj * DH + DPL * hl;
+#pragma unroll
+      for (int e = 0; e < DPL; ++e) acc[e] = fmaf(pj, bf2f(vr2[e]), acc[e]);
+    }
+#pragma unroll
+    for (int e = 0; e < DPL; ++e) ro[e] = fmaf(ro[e], alpha, acc[e]);
+    wave_sync_lds();
+  }
+  const gw<float> out = part_rec(a, h, t, a.att_units, nl);
+  if (hl == 0) {
+    out[0] = rm;
+    out[1] = rl;
+  }
+#pragma unroll
+  for (int e = 0; e < DPL; ++e) out[4 + DPL * hl + e] = ro[e];
+  __syncthreads();
+  return true;
+}
+
+// the merge of (head h, tile t): prefix parts in order, then the root path,
+// written as the out-projection's float16 input
+__device__ __forceinline__ bool att_merge_unit(const FusedArgs& a, const Wg& w, const WaitSpec& ws, int h, int t) {
+  if (ws.on && !wait_flags(a, w, ws.id, ws.wx, ws.tag)) return false;
+  stamp(a, w, ws.sl, ws.sfid, 1);
+  constexpr int DPT = 16 * DH / NTH;
+  const int tid = opq_tid();
+  const int nl = tid / (DH / DPT), d0 = DPT * (tid % (DH / DPT));
+  const int n = 16 * t + nl, S = a.att_units;
+  float M = -INFINITY, L = 0.f, O[DPT];
+#pragma unroll
+  for (int e = 0; e < DPT; ++e) O[e] = 0.f;
+  for (int j = 0; j <= S; ++j) {
+    const gptr<float> rec = (gptr<float>)part_rec(a, h, t, j, nl);
+    const float mj = ld_x(rec), lj = ld_x(rec + 1);
+    float ov[DPT];
+#pragma unroll
+    for (int e = 0; e < DPT; ++e) ov[e] = ld_x(rec + 4 + d0 + e);
+    if (mj == -INFINITY) continue;
+    const float mn = fmaxf(M, mj);
+    const float al = __expf(M - mn), wj = __expf(mj - mn);
+    L = fmaf(L, al, lj * wj);
+#pragma unroll
+    for (int e = 0; e < DPT; ++e) O[e] = fmaf(O[e], al, ov[e] * wj);
+    M = mn;
+  }
+  if (n < a.N) {
+#pragma unroll
+    for (int e = 0; e < DPT; ++e) st_act(a.fo, n, h * DH + d0 + e, a.d / 32, O[e] / L);
+  }
   return true;
 }
 
@@ -846,6 +882,30 @@ __device__ __forceinline__ bool attention_task(const FusedArgs& a, const Wg& w, 
 //   HEAD: first row block, end row block of the LM head
 
 // ------------------------------------------------------------------ compute workgroups
+
+// Loads a GEMM task's weight fragments into the XCD's L2 ahead of its stage:
+// waves 1.. of the workgroup take fragment rows in turn (wave 0, which polls
+// flags, issues none, so its polls never wait behind these loads).  The
+// values are folded into acc, which is stored only if it equals a magic word.
+__device__ __forceinline__ unsigned touch_task(const int* rbs, int nrb, gptr<u32x4> Wp, int KC, int kc0, int kc1,
+                                               unsigned acc) {
+  const int tid = opq_tid(), wv = tid >> 6, lane = tid & 63;
+  if (wv == 0) return acc;
+  Wp = opq(Wp);
+  const int nk = kc1 - kc0, tot = nrb * nk;
+  for (int f0 = wv - 1; f0 < tot; f0 += 4 * (NWV - 1)) {
+    u32x4 v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int f = min(f0 + u * (NWV - 1), tot - 1);
+      const int r = f / nk, kc = kc0 + f - r * nk;
+      v[u] = Wp[((size_t)rbs[r] * KC + kc) * 64 + lane];
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) acc ^= v[u][0] ^ v[u][3];
+  }
+  return acc;
+}
 
 template <int NT>
 __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* lds) {
@@ -884,7 +944,7 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
   }
 
   const int* p = a.plan + (size_t)w.g * kPlanStride;
-  const int n_att = p[PL_ATT], n_qkv = p[PL_QKV], n_wo = p[PL_WO], n_fc = p[PL_FC], n_wpr = p[PL_WPR];
+  const int n_qkv = p[PL_QKV], n_wo = p[PL_WO], n_fc = p[PL_FC], n_wpr = p[PL_WPR];
   const int hb0 = p[PL_HEAD], hb1 = p[PL_HEAD + 1];
   const int d = a.d, M = a.M, KCd = d / 32, KCm = M / 32;
   const int kh0 = 2 * a.xh[2 * w.x], kh1 = 2 * a.xh[2 * w.x + 1];  // the XCD's heads, in k-steps of W_o
@@ -895,42 +955,47 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
   constexpr int E = 4;  // LayerNorm elements per thread: d <= 2048
 
   // One runtime loop over the pass's stages, so that each stage body (the
-  // LayerNorm, the GEMM at 1, 2 and 4 row blocks, the attention) exists once
-  // in the code: the whole kernel stays small enough for the instruction
-  // cache, which a layer-by-layer unrolled body does not.
-  //   kind 0..6: LN1, QKV, ATT, WO, LN2, FC, WPR of layer l; 7: final
-  //   LayerNorm; 8: LM head.
-  const int nst = L * 7 + 2;
+  // LayerNorm, the GEMM at 1, 2 and 4 row blocks, the attention units)
+  // exists once in the code.
+  //   kind 0..7: LN1, QKV, ATT, AMG (attention merge), WO, LN2, FC, WPR of
+  //   layer l; 8: final LayerNorm; 9: LM head.
+  const int NTl = (N + 15) / 16;             // 16-node tiles
+  const int S = a.att_units;                 // prefix units of 256 cache rows
+  const int nhx = a.xh[2 * w.x + 1] - a.xh[2 * w.x];
+  const int n_attu = nhx * NTl * (S + 1);    // attention units of this XCD (prefix units + root unit per tile)
+  const int n_amg = nhx * NTl;               // attention merges of this XCD
+  const int nst = L * 8 + 2;
   for (int st = 0; st < nst; ++st) {
-    const int l = st < L * 7 ? st / 7 : L;
-    const int kind = st < L * 7 ? st % 7 : 7 + (st - L * 7);
+    const int l = st < L * 8 ? st / 8 : L;
+    const int kind = st < L * 8 ? st % 8 : 8 + (st - L * 8);
     // flag id, waited flag id / layer / XCD (-1 all, -2 none), work present
     int fid, wid = 0, wl = l, wx = w.x, work;
     switch (kind) {
       case 0: fid = FS_LN1; wid = FS_WPR; wl = l - 1; wx = l > 0 ? -1 : -2; work = w.r < N; break;
       case 1: fid = FS_QKV; wid = FS_LN1; work = n_qkv > 0; break;
-      case 2: fid = FS_ATT; wid = FS_QKV; work = n_att > 0; break;
-      case 3: fid = FS_WO; wid = FS_ATT; work = n_wo > 0; break;
-      case 4: fid = FS_LN2; wid = FS_WO; wx = -1; work = w.r < N; break;
-      case 5: fid = FS_FC; wid = FS_LN2; work = n_fc > 0; break;
-      case 6: fid = FS_WPR; wid = FS_FC; work = n_wpr > 0; break;
-      case 7: fid = FS_LN1; wid = FS_WPR; wl = L - 1; wx = -1; work = w.r < N; break;
+      case 2: fid = FS_ATT; wid = FS_QKV; work = w.r < n_attu; break;
+      case 3: fid = FS_AMG; wid = FS_ATT; work = w.r < n_amg; break;
+      case 4: fid = FS_WO; wid = FS_AMG; work = n_wo > 0; break;
+      case 5: fid = FS_LN2; wid = FS_WO; wx = -1; work = w.r < N; break;
+      case 6: fid = FS_FC; wid = FS_LN2; work = n_fc > 0; break;
+      case 7: fid = FS_WPR; wid = FS_FC; work = n_wpr > 0; break;
+      case 8: fid = FS_LN1; wid = FS_WPR; wl = L - 1; wx = -1; work = w.r < N; break;
       default: fid = FS_QKV; wid = FS_LN1; work = hb1 > hb0; break;
     }
-    progress(a, w, kind < 7 ? l * kFStages + fid : L * kFStages + (kind == 7 ? 0 : 1));
+    progress(a, w, kind < 8 ? l * kFStages + fid : L * kFStages + (kind == 8 ? 0 : 1));
     stamp(a, w, l, fid, 0);
     if (work) {
       // each body loads what does not depend on the previous stage, then waits
       const WaitSpec ws{wid, wx, tag_of(w, wl, wid), wx != -2, l, fid};
       const WaitSpec none{0, 0, 0u, false, l, fid};
-      if (kind == 0 || kind == 4 || kind == 7) {
+      if (kind == 0 || kind == 5 || kind == 8) {
         // residual update + LayerNorm of this workgroup's node rows
         const int mode = (kind == 0 && l == 0) ? 0 : 1;
         gptr<uint16_t> bias, g, b;
         const float* part;
         const int* xrange;
         uint16_t* act;
-        if (kind == 4) {
+        if (kind == 5) {
           bias = G<uint16_t>(lw(a, l, LB_O));
           part = a.part_o;
           xrange = a.xh;
@@ -938,25 +1003,33 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
           b = G<uint16_t>(lw(a, l, LN2B));
           act = act2;
         } else {
-          const int lp = kind == 7 ? L - 1 : max(l - 1, 0);
+          const int lp = kind == 8 ? L - 1 : max(l - 1, 0);
           bias = G<uint16_t>(lw(a, lp, LB_PR));
           part = a.part_p;
           xrange = a.xf;
-          g = kind == 7 ? G<uint16_t>(a.lnf_g) : G<uint16_t>(lw(a, l, LN1G));
-          b = kind == 7 ? G<uint16_t>(a.lnf_b) : G<uint16_t>(lw(a, l, LN1B));
+          g = kind == 8 ? G<uint16_t>(a.lnf_g) : G<uint16_t>(lw(a, l, LN1G));
+          b = kind == 8 ? G<uint16_t>(a.lnf_b) : G<uint16_t>(lw(a, l, LN1B));
           act = act1;
         }
-        const bool dbg = a.trace && (a.dbg & 1) && kind == 0 && l == a.dbg_l;
         for (int n = w.r; n < N; n += kFRanks)
-          if (!ln_row<E>(a, w, n == w.r ? ws : none, n, mode, bias, part, xrange, g, b, act, red, dbg)) goto out;
+          if (!ln_row<E>(a, w, n == w.r ? ws : none, n, mode, bias, part, xrange, g, b, act, red)) goto out;
       } else if (kind == 2) {
-        for (int j = 0; j < n_att; ++j) {
-          const int e = p[PL_ATT + 1 + j];
-          if (!attention_task(a, w, j == 0 ? ws : none, l, e & 0xffff, e >> 16, lds,
-                              a.trace && (a.dbg & 1) && l == a.dbg_l && j == 0))
-            goto out;
+        // attention units of this XCD's heads, dealt to its ranks in turn
+        for (int u = w.r; u < n_attu; u += kFRanks) {
+          const int hloc = u / (NTl * (S + 1)), rem = u - hloc * (NTl * (S + 1));
+          const int t = rem / (S + 1), part = rem - t * (S + 1);
+          const int h = a.xh[2 * w.x] + hloc;
+          const WaitSpec& wsu = u == w.r ? ws : none;
+          const bool ok = part < S ? att_prefix_unit(a, w, wsu, l, h, t, part, lds)
+                                   : att_root_unit(a, w, wsu, l, h, t, lds);
+          if (!ok) goto out;
         }
-      } else if (kind == 8) {
+      } else if (kind == 3) {
+        for (int u = w.r; u < n_amg; u += kFRanks) {
+          const int h = a.xh[2 * w.x] + u / NTl, t = u % NTl;
+          if (!att_merge_unit(a, w, u == w.r ? ws : none, h, t)) goto out;
+        }
+      } else if (kind == 9) {
         for (int b0 = hb0, j = 0; b0 < hb1; b0 += 4, ++j) {
           progress(a, w, L * kFStages + 1 + j / 2);
           if (!gemm_task<NT>(a, w, b0 == hb0 ? ws : none, FE_HEAD, L, nullptr, b0, min(4, hb1 - b0),
@@ -971,20 +1044,22 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
         switch (kind) {
           case 1: epi = FE_QKV; nrb = n_qkv; slot = PL_QKV; KC = KCd; Mo = 3 * d; k0 = 0; k1 = KCd; akc = KCd;
                   bias = G<uint16_t>(lw(a, l, LB_QKV)); act = act1; break;
-          case 3: epi = FE_WO; nrb = n_wo; slot = PL_WO; KC = KCd; Mo = d; k0 = kh0; k1 = kh1; akc = KCd;
+          case 4: epi = FE_WO; nrb = n_wo; slot = PL_WO; KC = KCd; Mo = d; k0 = kh0; k1 = kh1; akc = KCd;
                   act = a.fo; break;
-          case 5: epi = FE_FC; nrb = n_fc; slot = PL_FC; KC = KCd; Mo = M; k0 = 0; k1 = KCd; akc = KCd;
+          case 6: epi = FE_FC; nrb = n_fc; slot = PL_FC; KC = KCd; Mo = M; k0 = 0; k1 = KCd; akc = KCd;
                   bias = G<uint16_t>(lw(a, l, LB_FC)); act = act2; break;
           default: epi = FE_WPR; nrb = n_wpr; slot = PL_WPR; KC = KCm; Mo = d; k0 = kf0; k1 = kf1; akc = KCm;
                    act = a.ff; break;
         }
-        const int wslot = kind == 1 ? LW_QKV : kind == 3 ? LW_O : kind == 5 ? LW_FC : LW_PR;
+        const int wslot = kind == 1 ? LW_QKV : kind == 4 ? LW_O : kind == 6 ? LW_FC : LW_PR;
         if (!gemm_task<NT>(a, w, ws, epi, l, p + slot + 1, 0, nrb, bias, G<u32x4>(lw(a, l, wslot)), KC, Mo, k0, k1,
                            act, akc, red))
           goto out;
       }
     }
-    signal(a, w, l, fid, kind == 3 || kind == 6);
+    if (a.sub && kind == a.sub_kind) sub_stamp(a, w, l, 4);
+    signal(a, w, l, fid, kind == 4 || kind == 7);
+    if (a.sub && kind == a.sub_kind) sub_stamp(a, w, l, 5);
     stamp(a, w, l, fid, 2);
   }
 out:

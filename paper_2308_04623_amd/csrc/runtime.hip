@@ -128,6 +128,7 @@ struct ssd_kv {
   void* fz_ws = nullptr;
   FusedArgs fz{};                      // workspace pointers, XCD ranges
   int* fz_plan[5] = {};                // device plans per 16-node tile count (1..4)
+  unsigned long long* fz_sub = nullptr;  // (measurement) sub-stage timestamps
 };
 
 struct ssd_graph {
@@ -184,6 +185,11 @@ extern "C" ssd_status ssd_kv_set_trace(ssd_kv* kv, uint64_t* buf) {
   if (!kv->fz_ok) return fail(SSD_E_UNSUPPORTED, "the session has no persistent pass");
   kv->fz.trace = (unsigned long long*)buf;
   return SSD_OK;
+}
+
+extern "C" ssd_status ssd_kv_debug_sub(ssd_kv* kv, uint64_t* host16x256) {
+  if (!kv || !kv->fz_ok || !host16x256) return fail(SSD_E_INVALID_ARG, "bad argument");
+  HIP_TRY(hipMemcpy(host16x256, kv->fz_sub, (size_t)kFGroups * 16 * 8, hipMemcpyDeviceToHost));
 }
 
 extern "C" ssd_status ssd_fused_plan(int32_t n_head, int32_t d_model, int32_t d_mlp, int32_t vocab, int32_t n_tiles,
@@ -405,9 +411,12 @@ static ssd_status fused_setup(ssd_kv* kv) {
   const size_t o_xr = take((size_t)kFXcd * kFMaxN * d * 4), o_q = take((size_t)kFMaxN * d * 4);
   const size_t o_a1 = take(kFXcd * act_stride * 2), o_a2 = take(kFXcd * act_stride * 2);
   const size_t o_fo = take((size_t)kFMaxN * d * 2), o_ff = take((size_t)kFMaxN * M * 2);
+  const size_t att_parts = (size_t)(kv->max_ctx + kFAttRows - 1) / kFAttRows + 1;
+  const size_t o_ap = take((size_t)c.n_head * 4 * att_parts * 16 * 68 * 4);
   const size_t o_po = take((size_t)kFXcd * kFMaxN * d * 4), o_pp = take((size_t)kFXcd * kFMaxN * d * 4);
   const size_t o_fl = take((size_t)kFStages * kFGroups * 4), o_ctl = take((size_t)kFCtlWords * 4);
   const size_t o_prog = take((size_t)kFGroups * 4), o_plan = take(tabs.size() * 4), o_sink = take(4);
+  const size_t o_sub = take((size_t)kFGroups * 16 * 8);
   static const hipError_t prep = fused_prepare();
   if (prep != hipSuccess) return SSD_OK;  // keep the per-sub-layer kernels
   HIP_TRY(hipMalloc(&kv->fz_ws, off));
@@ -421,12 +430,14 @@ static ssd_status fused_setup(ssd_kv* kv) {
   a.act_stride = act_stride;
   a.fo = (uint16_t*)(b + o_fo);
   a.ff = (uint16_t*)(b + o_ff);
+  a.apart = (float*)(b + o_ap);
   a.part_o = (float*)(b + o_po);
   a.part_p = (float*)(b + o_pp);
   a.flags = (unsigned*)(b + o_fl);
   a.ctl = (unsigned*)(b + o_ctl);
   a.prog = (unsigned*)(b + o_prog);
   a.sink = (unsigned*)(b + o_sink);
+  kv->fz_sub = (unsigned long long*)(b + o_sub);
   for (int nt = 1; nt <= 4; ++nt) kv->fz_plan[nt] = (int*)(b + o_plan) + (size_t)(nt - 1) * kFGroups * kPlanStride;
   a.err = kv->d_err;
   a.timeout = 20000000ull;  // 200 ms
@@ -439,7 +450,9 @@ static ssd_status fused_setup(ssd_kv* kv) {
 // whether a verification pass of model m over n nodes runs as the persistent single launch
 static bool use_fused(const ssd_model* m, const ssd_kv* kv, int n) {
   if (g_pass_mode == 1 || m->f32 || !kv->fz_ok || !m->ftab) return false;
-  return n <= kFMaxN;
+  // the persistent pass is forced, or chosen where it is the faster one
+  // (measured: up to 32 nodes on the GPT-2-L shape)
+  return g_pass_mode == 2 ? n <= kFMaxN : n <= kFAutoMaxN;
 }
 
 extern "C" ssd_status ssd_kv_create(const ssd_model* m, int32_t max_ctx, int32_t max_nodes, void* k_cache,
@@ -735,11 +748,14 @@ static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int3
     a.P = P;
     a.logits = logits;
     a.plan = kv->fz_plan[(n + 15) / 16];
+    a.att_units = (P + kFAttRows - 1) / kFAttRows;
     a.ahead = g_fz_ahead;
     a.poll_sleep = g_fz_poll_sleep;
-    a.dbg = getenv("SSD_FZ_DBG") ? atoi(getenv("SSD_FZ_DBG")) : 0;
-    a.dbg_l = 10;
     a.prefetch = getenv("SSD_FZ_PF") ? atoi(getenv("SSD_FZ_PF")) : 0;
+    a.sub = kv->fz.trace ? kv->fz_sub : nullptr;
+    a.sub_l = 10;
+    a.sub_kind = getenv("SSD_FZ_SUBKIND") ? atoi(getenv("SSD_FZ_SUBKIND")) : 6;
+    a.sub_epi = getenv("SSD_FZ_SUBEPI") ? atoi(getenv("SSD_FZ_SUBEPI")) : 2;
     HIP_TRY(launch_fused(a, s));
     return SSD_OK;
   }

@@ -181,10 +181,12 @@ constexpr int kFXcd = 8;                   // XCDs
 constexpr int kFRanks = 32;                // compute workgroups per XCD
 constexpr int kFGroups = kFXcd * kFRanks;  // compute workgroups (one per CU)
 constexpr int kFMaxN = 64;                 // nodes
+constexpr int kFAutoMaxN = 32;             // most nodes the default pass mode sends to it
 constexpr int kFMaxL = 255;                // layers
 // stages of a layer; their flags are [kFStages][kFGroups] words
-enum FStage { FS_LN1 = 0, FS_QKV, FS_ATT, FS_WO, FS_LN2, FS_FC, FS_WPR, FS_SPARE, kFStages };
+enum FStage { FS_LN1 = 0, FS_QKV, FS_ATT, FS_WO, FS_LN2, FS_FC, FS_WPR, FS_AMG, kFStages };
 constexpr unsigned kFTagsPerPass = (unsigned)kFStages * (kFMaxL + 1);
+constexpr int kFAttRows = 256;  // cache rows per attention unit (32 per wave of 8)
 constexpr int kLwSlots = 12;  // per-layer parameter pointers (see LwSlot in fused.hip)
 // plan row of one compute workgroup (int32): counts then entries
 enum PlanSlot { PL_ATT = 0, PL_QKV = 9, PL_WO = 14, PL_FC = 19, PL_WPR = 24, PL_HEAD = 29, kPlanStride = 32 };
@@ -212,6 +214,8 @@ struct FusedArgs {
   uint16_t *act1, *act2;    // [kFXcd][act_stride] LayerNorm outputs (float16 fragments), one copy per XCD
   size_t act_stride;
   uint16_t* fo;             // attention outputs, float16 fragments [4 tiles][d / 32][512]
+  float* apart;             // attention parts [H][4 tiles][att_units + 1][16][68]: max, sum, -, -, output
+  int att_units;            // prefix units of 256 cache rows: ceil(P / 256)
   uint16_t* ff;             // GELU outputs, float16 fragments [4 tiles][M / 32][512]
   float *part_o, *part_p;   // partial residuals [kFXcd][kFMaxN][d]
   unsigned* flags;          // [kFStages][kFGroups]
@@ -229,7 +233,8 @@ struct FusedArgs {
   unsigned* sink;
   unsigned long long* trace;  // stage timestamps [kFGroups][L + 1][kFStages][3], or nullptr
   int prefetch;               // also launch the L2 prefetch workgroups
-  int dbg, dbg_l;             // extra LayerNorm timestamps (bit 0) for layer dbg_l, in the spare stage slot
+  unsigned long long* sub;   // (measurement) sub-stage timestamps [kFGroups][16] of one stage, or nullptr
+  int sub_l, sub_kind, sub_epi;
 };
 
 // Work split of the fused pass for a model shape and 16-node tile count:
