@@ -46,8 +46,9 @@ def pass_bytes(cfg, n, P):
 
 def kernel_source_hash():
     h = hashlib.sha256()
-    with open(os.path.join(ROOT, "paper_2308_04623_amd", "csrc", "kernels.hip"), "rb") as f:
-        h.update(f.read())
+    for name in ("kernels.hip", "fused.hip", "ssd_internal.h"):
+        with open(os.path.join(ROOT, "paper_2308_04623_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
     return h.hexdigest()[:16]
 
 
@@ -63,12 +64,14 @@ def cpu_model():
 
 COPY_BYTES = 256 << 20
 FC_KERNEL = "gemm_kernel<2, 2, 2,"  # MLP up-projection + GELU at 17..32 nodes (matrix cores)
+PASS_KERNEL = "pass_kernel"         # the persistent single-launch pass
 
 
-def probe_traffic(sess, cfg, n):
+def probe_traffic(sess, cfg, n, P, toks, par, fused):
     """Kernels for the HBM-traffic counters: a plain device-to-device copy of
-    COPY_BYTES (reads and writes exactly that much), then the MLP
-    up-projection GEMM of every layer twice."""
+    COPY_BYTES (reads and writes exactly that much), then the dominant kernel:
+    three verification passes (persistent pass) or the MLP up-projection GEMM
+    of every layer twice (one kernel per sub-layer)."""
     import torch
     src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device="cuda")
     dst = torch.empty_like(src)
@@ -76,9 +79,13 @@ def probe_traffic(sess, cfg, n):
     for _ in range(3):
         dst.copy_(src)
     torch.cuda.synchronize()
-    for _ in range(2):
-        for l in range(cfg.n_layer):
-            sess.launch_gemm(2, l, n)
+    if fused:
+        for _ in range(3):
+            sess.verify(P, toks, par)
+    else:
+        for _ in range(2):
+            for l in range(cfg.n_layer):
+                sess.launch_gemm(2, l, n)
     torch.cuda.synchronize()
     log("traffic probe done")
 
@@ -111,27 +118,81 @@ def _per_kernel(rows, counter):
     return out
 
 
-def write_traffic(fetch_dir, write_dir, n):
-    out = {"kernel_source": kernel_source_hash(), "nodes": n, "copy_bytes": COPY_BYTES}
+def traffic_path(fused):
+    return os.path.join(ROOT, "profiles", "traffic_pass_kernel.json" if fused else "traffic_fc_gemm.json")
+
+
+def write_traffic(fetch_dir, write_dir, n, fused):
+    kname = PASS_KERNEL if fused else FC_KERNEL
+    out = {"kernel_source": kernel_source_hash(), "kernel": kname, "nodes": n, "copy_bytes": COPY_BYTES}
     for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
         per = _per_kernel(_counter_rows(d), counter)
         # the probe's copy is the largest-grid copy kernel of the run (set-up copies are small)
         grids = [g for (k, g) in per if "copyBuffer" in k]
         copy = [v for (k, g), vs in per.items() if "copyBuffer" in k and grids and g == max(grids) for v in vs]
-        fc = [v for (k, g), vs in per.items() if FC_KERNEL in k for v in vs]
-        if not copy or not fc:
-            raise SystemExit(f"{counter}: copy or GEMM dispatches missing ({sorted(per)})")
+        kern = [v for (k, g), vs in per.items() if kname in k for v in vs]
+        if not copy or not kern:
+            raise SystemExit(f"{counter}: copy or {kname} dispatches missing ({sorted(per)})")
         copy_kib = sorted(copy)[len(copy) // 2]
         scale = COPY_BYTES / (copy_kib * 1024.0)  # bytes per counted KiB unit, from the copy of known size
-        fc_kib = sum(fc) / len(fc)
-        out[counter.lower()] = {"copy_kib_per_dispatch": copy_kib, "gemm_kib_per_dispatch": round(fc_kib, 1),
-                                "scale": round(scale, 4), "gemm_bytes_per_launch": round(fc_kib * 1024 * scale),
-                                "gemm_dispatches": len(fc)}
-    out["bytes_per_launch"] = out["fetch_size"]["gemm_bytes_per_launch"] + out["write_size"]["gemm_bytes_per_launch"]
-    path = os.path.join(ROOT, "profiles", "traffic_fc_gemm.json")
-    with open(path, "w") as fh:
+        k_kib = sum(kern) / len(kern)
+        out[counter.lower()] = {"copy_kib_per_dispatch": copy_kib, "kernel_kib_per_dispatch": round(k_kib, 1),
+                                "scale": round(scale, 4), "kernel_bytes_per_launch": round(k_kib * 1024 * scale),
+                                "kernel_dispatches": len(kern)}
+    out["bytes_per_launch"] = (out["fetch_size"]["kernel_bytes_per_launch"]
+                               + out["write_size"]["kernel_bytes_per_launch"])
+    with open(traffic_path(fused), "w") as fh:
         json.dump(out, fh, indent=1)
     print(json.dumps(out))
+
+
+def stored_traffic(fused, n):
+    """HBM bytes per launch from the committed counter runs, or None when they
+    were taken on other kernel sources or another node count."""
+    path = traffic_path(fused)
+    if not os.path.exists(path):
+        return None
+    t = json.load(open(path))
+    if t.get("kernel_source") == kernel_source_hash() and t.get("nodes") == n:
+        return t.get("bytes_per_launch")
+    return None
+
+
+def fc_gemm_roofline(sess, cfg, N, stream):
+    """Dominant kernel of the one-kernel-per-sub-layer path: the MLP
+    up-projection GEMM (13.1 MB of weights per launch), launched on its own
+    for every layer in turn so its weights stream from HBM, captured in a
+    graph so host launch rate does not limit it; HIP events on the stream it
+    runs on."""
+    import torch
+    fc_graph = torch.cuda.CUDAGraph()
+    cap = torch.cuda.Stream()
+    cap.wait_stream(stream)
+    with torch.cuda.stream(cap):
+        for l in range(cfg.n_layer):  # warm-up outside the graph
+            sess.launch_gemm(2, l, N)
+        cap.synchronize()
+        with torch.cuda.graph(fc_graph, stream=cap):
+            for l in range(cfg.n_layer):
+                sess.launch_gemm(2, l, N)
+    torch.cuda.synchronize()
+    reps = 10
+    for _ in range(3):
+        fc_graph.replay()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    for _ in range(reps):
+        fc_graph.replay()
+    b.record(stream)
+    torch.cuda.synchronize()
+    us_fc = a.elapsed_time(b) * 1e3 / (reps * cfg.n_layer)
+    fc_bytes = cfg.d_mlp * cfg.d_model * 2 + N * cfg.d_model * 2 + N * cfg.d_mlp * 2
+    fc_gbs = fc_bytes / us_fc / 1e3
+    return {"bound": "hbm", "achieved": round(fc_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": round(fc_gbs / PEAK_HBM_GBS, 4), "traffic": stored_traffic(False, N),
+            "kernel": "gemm (MLP up-projection + GELU), 5120x1280 bf16",
+            "bytes_per_launch": fc_bytes, "us_per_launch": round(us_fc, 2)}
 
 
 def end_to_end(ssd, W, cfg, model, N_NEW, PROMPT):
@@ -193,13 +254,16 @@ def main():
     ap.add_argument("--no-e2e", action="store_true", help="skip the staged end-to-end generation")
     ap.add_argument("--traffic-probe", action="store_true",
                     help="only run the kernels the HBM-traffic counters are read on (a 256 MiB device copy, then "
-                         "the MLP up-projection GEMM over every layer); meant to run under rocprofv3 --pmc")
+                         "the dominant kernel); meant to run under rocprofv3 --pmc")
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="read two rocprofv3 --pmc outputs (FETCH_SIZE, WRITE_SIZE) of --traffic-probe and write "
-                         "profiles/traffic_fc_gemm.json; no GPU needed")
+                         "profiles/traffic_pass_kernel.json (or traffic_fc_gemm.json with --kernels-path); "
+                         "no GPU needed")
+    ap.add_argument("--kernels-path", action="store_true",
+                    help="with --traffic-from: the counters are of the one-kernel-per-sub-layer path's GEMM")
     args = ap.parse_args()
     if args.traffic_from:
-        write_traffic(args.traffic_from[0], args.traffic_from[1], args.nodes)
+        write_traffic(args.traffic_from[0], args.traffic_from[1], args.nodes, not args.kernels_path)
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}): this build has no multi-GPU path; "
@@ -225,8 +289,9 @@ def main():
     par = W.branching_tree([4, 2, 2, 1], N)
     toks = W.tree_tokens(par, cfg.vocab, seed=2)
     logits = torch.empty((N, cfg.vocab), dtype=torch.float32, device="cuda")
+    fused = sess.verify_path(N) == ssd.PASS_FUSED
     if args.traffic_probe:
-        probe_traffic(sess, cfg, N)
+        probe_traffic(sess, cfg, N, P, toks, par, fused)
         return
     graph = sess.capture_verify(P, toks, par, logits)
     outs = (torch.zeros(N, dtype=torch.int32, device="cuda"), torch.zeros(1, dtype=torch.int32, device="cuda"),
@@ -267,45 +332,18 @@ def main():
     B = pass_bytes(cfg, N, P)
     log(f"verify pass {us_pass:.1f} us, {B / us_pass / 1e3:.0f} GB/s")
 
-    # dominant kernel: the MLP up-projection GEMM (13.1 MB of weights per
-    # launch), launched on its own for every layer in turn so its weights
-    # stream from HBM; HIP events on the stream it runs on
-    # (captured in a graph so that host launch rate does not limit it; each
-    # replay launches the 36 GEMMs back to back)
-    fc_graph = torch.cuda.CUDAGraph()
-    cap = torch.cuda.Stream()
-    cap.wait_stream(stream)
-    with torch.cuda.stream(cap):
-        for l in range(cfg.n_layer):  # warm-up outside the graph
-            sess.launch_gemm(2, l, N)
-        cap.synchronize()
-        with torch.cuda.graph(fc_graph, stream=cap):
-            for l in range(cfg.n_layer):
-                sess.launch_gemm(2, l, N)
-    torch.cuda.synchronize()
-    reps = 10
-    for _ in range(3):
-        fc_graph.replay()
-    torch.cuda.synchronize()
-    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    a.record(stream)
-    for _ in range(reps):
-        fc_graph.replay()
-    b.record(stream)
-    torch.cuda.synchronize()
-    us_fc = a.elapsed_time(b) * 1e3 / (reps * cfg.n_layer)
-    fc_bytes = cfg.d_mlp * cfg.d_model * 2 + N * cfg.d_model * 2 + N * cfg.d_mlp * 2
-    fc_gbs = fc_bytes / us_fc / 1e3
-    traffic = None
-    tpath = os.path.join(ROOT, "profiles", "traffic_fc_gemm.json")
-    if os.path.exists(tpath):
-        t = json.load(open(tpath))
-        if t.get("kernel_source") == kernel_source_hash() and t.get("nodes") == N:
-            traffic = t.get("bytes_per_launch")
-    roofline = {"bound": "hbm", "achieved": round(fc_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                "frac": round(fc_gbs / PEAK_HBM_GBS, 4), "traffic": traffic,
-                "kernel": "gemm (MLP up-projection + GELU), 5120x1280 bf16",
-                "bytes_per_launch": fc_bytes, "us_per_launch": round(us_fc, 2)}
+    if fused:
+        # dominant kernel: the persistent pass itself (the pass is this one
+        # kernel; the graph adds only the ~2 KB tree upload before it), so its
+        # algorithmic bytes are the pass's and its duration the graph
+        # replays' on the stream they run on
+        roofline = {"bound": "hbm", "achieved": round(B / us_pass / 1e3, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                    "frac": round(B / us_pass / 1e3 / PEAK_HBM_GBS, 4), "traffic": stored_traffic(True, N),
+                    "kernel": f"ssd::fz::pass_kernel<{min((N + 15) // 16, 2) if N <= 32 else 4}> "
+                              "(persistent single-launch verification pass)",
+                    "bytes_per_launch": B, "us_per_launch": round(us_pass, 2)}
+    else:
+        roofline = fc_gemm_roofline(sess, cfg, N, stream)
 
     sweep = []
     if not args.no_sweep:
@@ -351,6 +389,7 @@ def main():
         "config": {"workload": f"GPT-2-L shape tree verification, {N}-node tree (branching 4,2,2,1), "
                                f"{P}-token prefix, greedy accept + commit",
                    "nodes": N, "prefix": P, "layers": cfg.n_layer, "d_model": cfg.d_model, "vocab": cfg.vocab},
+        "verify_path": "persistent single launch" if fused else "one kernel per sub-layer",
         "us_per_verify_pass": round(us_pass, 2),
         "pass_hbm_GBs": round(B / us_pass / 1e3, 1),
         "pass_frac_of_peak": round(B / us_pass / 1e3 / PEAK_HBM_GBS, 4),

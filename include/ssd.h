@@ -247,6 +247,12 @@ ssd_status ssd_set_weight_prefetch(int32_t on);
  * Process-wide.  Errors: SSD_E_INVALID_ARG (mode not 0, 1 or 2). */
 ssd_status ssd_set_pass_mode(int32_t mode);
 
+/* Host-only: which way ssd_tree_verify would run a pass of n nodes of the
+ * model on this session under the current pass mode: *path = 1 (one kernel
+ * per sub-layer) or 2 (the persistent single launch).  Errors:
+ * SSD_E_INVALID_ARG (null pointer, n outside [1, max_nodes]). */
+ssd_status ssd_verify_path(const ssd_model *m, const ssd_kv *kv, int32_t n, int32_t *path);
+
 /* Host-only: the persistent launch's work split for a model shape and a
  * count of 16-node tiles (1..4), as the session computes it.  tab receives
  * [256][32] int32 rows, one per compute workgroup (XCD x, rank r at row

@@ -455,6 +455,12 @@ static bool use_fused(const ssd_model* m, const ssd_kv* kv, int n) {
   return g_pass_mode == 2 ? n <= kFMaxN : n <= kFAutoMaxN;
 }
 
+extern "C" ssd_status ssd_verify_path(const ssd_model* m, const ssd_kv* kv, int32_t n, int32_t* path) {
+  if (!m || !kv || !path || n < 1 || n > kv->max_nodes) return fail(SSD_E_INVALID_ARG, "bad argument");
+  *path = use_fused(m, kv, n) ? 2 : 1;
+  return SSD_OK;
+}
+
 extern "C" ssd_status ssd_kv_create(const ssd_model* m, int32_t max_ctx, int32_t max_nodes, void* k_cache,
                                     void* v_cache, void* k_tree, void* v_tree, ssd_kv** out) {
   if (!m || !out || !k_tree || !v_tree) return fail(SSD_E_INVALID_ARG, "null argument");

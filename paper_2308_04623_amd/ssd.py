@@ -28,7 +28,7 @@ LAYER_TENSORS = ("ln1_g", "ln1_b", "w_qkv", "b_qkv", "w_o", "b_o",
 EXPORTS = ("ssd_model_create", "ssd_model_destroy", "ssd_kv_bytes", "ssd_kv_create", "ssd_kv_destroy",
            "ssd_tree_verify", "ssd_tree_accept", "ssd_kv_commit", "ssd_kv_error_count",
            "ssd_graph_capture_verify", "ssd_graph_launch", "ssd_graph_destroy", "ssd_validate_tree",
-           "ssd_tree_prep", "ssd_set_gemm_path", "ssd_set_weight_prefetch", "ssd_set_pass_mode", "ssd_set_fused_ahead", "ssd_fused_plan", "ssd_kv_set_trace", "ssd_status_string", "ssd_last_error", "ssd_launch_gemm",
+           "ssd_tree_prep", "ssd_set_gemm_path", "ssd_set_weight_prefetch", "ssd_set_pass_mode", "ssd_verify_path", "ssd_set_fused_ahead", "ssd_fused_plan", "ssd_kv_set_trace", "ssd_status_string", "ssd_last_error", "ssd_launch_gemm",
            "ssd_model_prefix_view", "ssd_topk")
 
 
@@ -89,6 +89,7 @@ def lib():
             "ssd_set_gemm_path": [C.c_int32],
             "ssd_set_weight_prefetch": [C.c_int32],
             "ssd_set_pass_mode": [C.c_int32],
+            "ssd_verify_path": [vp, vp, C.c_int32, C.POINTER(C.c_int32)],
             "ssd_set_fused_ahead": [C.c_int32],
             "ssd_fused_plan": [C.c_int32] * 5 + [vp, vp, vp],
             "ssd_kv_set_trace": [vp, vp],
@@ -399,6 +400,12 @@ class Session:
         tensor of 256 * (n_layer + 1) * 24 words), or None to stop."""
         _check(lib().ssd_kv_set_trace(self.handle, C.c_void_p(buf.data_ptr() if buf is not None else 0)),
                "ssd_kv_set_trace")
+
+    def verify_path(self, n: int) -> int:
+        """PASS_KERNELS or PASS_FUSED: how a pass of n nodes would run now."""
+        v = C.c_int32(0)
+        _check(lib().ssd_verify_path(self.model.handle, self.handle, n, C.byref(v)), "ssd_verify_path")
+        return v.value
 
     def error_count(self, stream=None) -> int:
         c = C.c_uint32(0)
