@@ -58,6 +58,10 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x8 __attribute__((ext_vector_type(8)));
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) float lds_f32;
+typedef __attribute__((address_space(3))) f32x4 lds_f32x4;
 typedef float f32x2_t __attribute__((ext_vector_type(2)));
 
 // Global-memory pointers (address space 1): loads through them are
@@ -99,6 +103,18 @@ __device__ __forceinline__ void st_act(gw<uint16_t> p, int n, int k, int ld, flo
   const size_t f = (size_t)(n >> 4) * ld + (k >> 5);
   p[f * 512 + ((n & 15) + 16 * ((k & 31) >> 3)) * 8 + (k & 7)] = __builtin_bit_cast(uint16_t, (_Float16)v);
 }
+
+// four consecutive elements (n, k .. k+3), k % 4 == 0: one 8-byte store
+__device__ __forceinline__ void st_act4(gw<uint16_t> p, int n, int k, int ld, float v0, float v1, float v2, float v3) {
+  const size_t f = (size_t)(n >> 4) * ld + (k >> 5);
+  const uint32_t lo = (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)v0) |
+                      ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)v1) << 16);
+  const uint32_t hi = (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)v2) |
+                      ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)v3) << 16);
+  *(gw<u32x2>)(p + f * 512 + ((n & 15) + 16 * ((k & 31) >> 3)) * 8 + (k & 7)) = (u32x2){lo, hi};
+}
+
+constexpr int CP_SC1 = 16;  // cache policy of a device-coherent load (sc1)
 
 __device__ __forceinline__ float gelu_tanh(float x) {
   const float c = 0.7978845608028654f;  // sqrt(2/pi)
@@ -161,6 +177,8 @@ __device__ __forceinline__ int ld_x(const int* p) { return __builtin_nontemporal
 __device__ __forceinline__ u32x4 ld_x(gptr<u32x4> p) { return __builtin_nontemporal_load(p); }
 __device__ __forceinline__ float ld_x(gptr<float> p) { return __builtin_nontemporal_load(p); }
 __device__ __forceinline__ int ld_x(gptr<int> p) { return __builtin_nontemporal_load(p); }
+__device__ __forceinline__ f32x2_t ld_x(gptr<f32x2_t> p) { return __builtin_nontemporal_load(p); }
+__device__ __forceinline__ f32x4 ld_x(gptr<f32x4> p) { return __builtin_nontemporal_load(p); }
 // device-coherent accesses (data crossing XCDs)
 __device__ __forceinline__ float ld_dev(const float* p) {
   return __hip_atomic_load((float*)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -183,6 +201,7 @@ struct Wg {
   unsigned E;        // this pass's number
   unsigned tagbase;  // E * tags per pass
   int* sh;           // LDS words shared by the workgroup
+  int sub;           // (measurement) the current stage is the one sub-stamped
 };
 
 // the dependency of a stage: flags of stage id on XCD wx (-1: all XCDs) at
@@ -206,41 +225,81 @@ __device__ __forceinline__ void raise_abort(const FusedArgs& a, unsigned code) {
   }
 }
 
-// Waits until the flags of stage s reach tag: the 32 of XCD xs, or all 256
-// when xs < 0.  Wave 0 polls; returns false (in every thread) on abort or
-// timeout.
+// Workgroup barrier that orders LDS accesses only: outstanding global stores
+// are not waited for (signal() waits for them before a stage is published).
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// Barrier of waves 0..3 alone (the other four keep their own loads going):
+// a counter in LDS that every round raises by 4; a wave leaves when the
+// round it joined is complete.  LDS accesses of a wave are performed in
+// order, so its writes before the barrier are visible after it.
+constexpr int QW = 4;  // waves that run the pre-stage rows
+__device__ __forceinline__ void q_barrier(const Wg& w) {
+  __attribute__((address_space(3))) unsigned* cnt = (__attribute__((address_space(3))) unsigned*)(w.sh + 4);
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  unsigned old = 0;
+  if ((threadIdx.x & 63) == 0) old = __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  old = __builtin_amdgcn_readfirstlane(old);
+  const unsigned target = (old / QW + 1) * QW;
+  while ((int)(__hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) - target) < 0)
+    __builtin_amdgcn_s_sleep(1);
+}
+
+// Wave 0 alone polls until the flags of stage s reach tag: the 32 of XCD xs,
+// or all 256 when xs < 0.  No workgroup barrier: the other waves go on with
+// their own work.  Returns false (in every lane) on abort or timeout.  On
+// success the CU's L1 lines are dropped before the wave's own later loads
+// (acquire: a wave's memory operations reach the cache in order, and the
+// flags' values were consumed, so they are complete).  The workgroup-scope
+// invalidate drops the L1 only; the agent-scope one would also drop the
+// XCD's L2.
+__device__ __forceinline__ bool poll_w0(const FusedArgs& a, const Wg& w, int s, int xs, unsigned tag) {
+  const int lane = threadIdx.x & 63;
+  const unsigned* f = a.flags + (size_t)s * kFGroups;
+  const unsigned long long t0 = now();
+  bool ok = false;
+  for (;;) {
+    bool mine;
+    if (xs < 0) {
+      const unsigned v0 = ld_flag(f + 4 * lane), v1 = ld_flag(f + 4 * lane + 1);
+      const unsigned v2 = ld_flag(f + 4 * lane + 2), v3 = ld_flag(f + 4 * lane + 3);
+      mine = tag_reached(v0, tag) && tag_reached(v1, tag) && tag_reached(v2, tag) && tag_reached(v3, tag);
+    } else {
+      mine = lane >= kFRanks || tag_reached(ld_flag(f + xs * kFRanks + lane), tag);
+    }
+    if (w.sub && lane == 0 && a.sub[(size_t)w.g * 16 + 6] == 0) a.sub[(size_t)w.g * 16 + 6] = now();
+    if (__all(mine)) {
+      ok = true;
+      break;
+    }
+    if (ld_flag(&a.ctl[FZ_ABORT])) break;
+    if (now() - t0 > a.timeout) {
+      if (lane == 0) raise_abort(a, 0x100u + (unsigned)s);
+      break;
+    }
+    for (int z = 0; z < a.poll_sleep; ++z) __builtin_amdgcn_s_sleep(8);
+    __builtin_amdgcn_s_sleep(1);
+  }
+  if (ok) asm volatile("buffer_inv sc0" ::: "memory");
+  return ok;
+}
+
+// The same wait for the whole workgroup: wave 0 polls, the others wait at an
+// LDS-only barrier (loads they issued before it, weights or cached K/V, stay
+// in flight), then each wave drops the L1 before its own loads.
 __device__ __forceinline__ bool wait_flags(const FusedArgs& a, const Wg& w, int s, int xs, unsigned tag) {
   if (threadIdx.x < 64) {
-    const int lane = threadIdx.x;
-    const unsigned* f = a.flags + (size_t)s * kFGroups;
-    const unsigned long long t0 = now();
-    int ok = 0;
-    for (;;) {
-      bool mine;
-      if (xs < 0) {
-        const unsigned v0 = ld_flag(f + 4 * lane), v1 = ld_flag(f + 4 * lane + 1);
-        const unsigned v2 = ld_flag(f + 4 * lane + 2), v3 = ld_flag(f + 4 * lane + 3);
-        mine = tag_reached(v0, tag) && tag_reached(v1, tag) && tag_reached(v2, tag) && tag_reached(v3, tag);
-      } else {
-        mine = lane >= kFRanks || tag_reached(ld_flag(f + xs * kFRanks + lane), tag);
-      }
-      if (__all(mine)) {
-        ok = 1;
-        break;
-      }
-      if (ld_flag(&a.ctl[FZ_ABORT])) break;
-      if (now() - t0 > a.timeout) {
-        if (lane == 0) raise_abort(a, 0x100u + (unsigned)s);
-        break;
-      }
-      for (int z = 0; z < a.poll_sleep; ++z) __builtin_amdgcn_s_sleep(8);
-      __builtin_amdgcn_s_sleep(1);
-    }
-    if (lane == 0) w.sh[0] = ok;
+    const bool ok = poll_w0(a, w, s, xs, tag);
+    if (threadIdx.x == 0) w.sh[0] = ok;
   }
-  __syncthreads();
+  lds_barrier();
   const bool ok = w.sh[0] != 0;
-  __syncthreads();
+  lds_barrier();
+  if (threadIdx.x >= 64) asm volatile("buffer_inv sc0" ::: "memory");
   return ok;
 }
 
@@ -253,6 +312,16 @@ __device__ __forceinline__ void signal(const FusedArgs& a, const Wg& w, int l, i
     if (cross_xcd) __hip_atomic_store(f, tag_of(w, l, s), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     else __hip_atomic_store(f, tag_of(w, l, s), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
   }
+}
+
+// Publishes stage s of layer l for work wave 0 did alone (its LayerNorm rows
+// or attention merges, read inside the XCD): its stores complete, then the
+// flag.
+__device__ __forceinline__ void signal_w0(const FusedArgs& a, const Wg& w, int l, int s) {
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  if (threadIdx.x == 0)
+    __hip_atomic_store(a.flags + (size_t)s * kFGroups + w.g, tag_of(w, l, s), __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
 // progress word read by this workgroup's prefetcher: pass (low 16 bits) in
@@ -269,14 +338,6 @@ __device__ __forceinline__ void stamp(const FusedArgs& a, const Wg& w, int l, in
     a.trace[(((size_t)w.g * (a.L + 1) + l) * kFStages + s) * 3 + k] = now();
 }
 
-// Workgroup barrier that orders LDS accesses only: outstanding global stores
-// are not waited for (signal() waits for them before a stage is published).
-__device__ __forceinline__ void lds_barrier() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-  __builtin_amdgcn_s_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-}
-
 // (measurement) sub-stage timestamps of one stage of one layer, when a.sub is set
 __device__ __forceinline__ void sub_stamp(const FusedArgs& a, const Wg& w, int l, int k) {
   if (a.sub && l == a.sub_l && threadIdx.x == 0) a.sub[(size_t)w.g * 16 + k] = now();
@@ -287,105 +348,281 @@ __device__ __forceinline__ void sub_stamp(const FusedArgs& a, const Wg& w, int l
 enum LwSlot { LW_QKV = 0, LW_O, LW_FC, LW_PR, LB_QKV, LB_O, LB_FC, LB_PR, LN1G, LN1B, LN2G, LN2B };
 
 
-__device__ __forceinline__ const void* lw(const FusedArgs& a, int l, int slot) { return a.lw[l * kLwSlots + slot]; }
+__device__ __forceinline__ const void* lw(const FusedArgs& a, int l, int slot) {
+  return ((gptr<const void*>)a.lw)[l * kLwSlots + slot];
+}
 
 // ------------------------------------------------------------------ LayerNorm of one node row
 //
 // mode 0: x = wte[token] + wpe[position] (first layer);
 // mode 1: x += bias + part[X] for every XCD X that owns a share of the
-//         residual GEMM, in XCD order (device-coherent loads);
+//         residual GEMM (bit X of own), in XCD order (device-coherent loads);
 // then a = (x - mean) / sqrt(var + eps) * g + b into this XCD's GEMM input.
+// One wave: lane i takes the float4 chunks i, i + 64, ... (C per lane, so
+// d <= 256 C); sums run over the lane's chunks in order, then across lanes
+// by butterfly.  The other waves of the workgroup are free meanwhile.
 
-template <int E>
-__device__ __forceinline__ bool ln_row(const FusedArgs& a, const Wg& w, const WaitSpec& ws, int n, int mode,
-                                       gptr<uint16_t> bias, const float* part, const int* xrange, gptr<uint16_t> g,
-                                       gptr<uint16_t> b, uint16_t* act, float* red) {
-  const int d = a.d, tid = opq_tid();
-  const gw<float> xr = opq(a.xr + ((size_t)w.x * kFMaxN + n) * d);
-  bias = opq(bias);
-  g = opq(g);
-  b = opq(b);
-  const gptr<float> partg = opq(part);
-  const gw<uint16_t> actg = opq(act);
-  // every load is issued (clamped to the row, unconditionally) before any is
-  // used, so the row costs one memory round trip
-  unsigned kk[E];
+// Sum over the 64 lanes of a wave, the same value in every lane, in a fixed
+// order: DPP exchanges inside each row of 16 lanes (xor 1, xor 2, half-row
+// mirror, row mirror), then the four row sums in lane order.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float x) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), CTRL, 0xf, 0xf, false));
+}
+__device__ __forceinline__ float wave_sum(float x) {
+  x += dpp_f<0xB1>(x);   // quad_perm [1,0,3,2]
+  x += dpp_f<0x4E>(x);   // quad_perm [2,3,0,1]
+  x += dpp_f<0x141>(x);  // row_half_mirror
+  x += dpp_f<0x140>(x);  // row_mirror
+  const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 0));
+  const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 16));
+  const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 32));
+  const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 48));
+  return (r0 + r1) + (r2 + r3);
+}
+
+// bit X set: XCD X owns a share of the range (heads, or MLP features)
+__device__ __forceinline__ unsigned owner_mask(const int* range) {
+  unsigned m = 0;
 #pragma unroll
-  for (int i = 0; i < E; ++i) kk[i] = (unsigned)min(tid + i * NTH, d - 1);
-  uint16_t gr[E], br[E];
-#pragma unroll
-  for (int i = 0; i < E; ++i) {
-    gr[i] = g[kk[i]];
-    br[i] = b[kk[i]];
+  for (int X = 0; X < kFXcd; ++X) m |= (range[2 * X + 1] > range[2 * X] ? 1u : 0u) << X;
+  return m;
+}
+
+// Waves 0..3 (256 threads): thread t takes the float4 chunks t, t + 256, ...
+// (C per thread, d <= 1024 C); sums run over the thread's chunks in order,
+// across its wave by DPP, then over the four waves in wave order.  Wave 0
+// polls with nothing else in flight (a wave's loads complete in order, so
+// anything issued before would delay the poll); the row's loads are issued
+// together right after it.
+template <int C>
+__device__ __forceinline__ bool ln_row_q(const FusedArgs& a, const Wg& w, const WaitSpec& ws, int n, int mode,
+                                         gptr<uint16_t> bias, const float* part, unsigned own, gptr<uint16_t> g,
+                                         gptr<uint16_t> b, uint16_t* act) {
+  const int d = a.d, nc = d / 4, tid = opq_tid(), wv = tid >> 6;
+  float* red = (float*)(w.sh + 8);  // [8]
+  if (mode != 0 && ws.on) {
+    if (wv == 0) {
+      const bool ok = poll_w0(a, w, ws.id, ws.wx, ws.tag);
+      if (tid == 0) w.sh[5] = ok;
+    }
+    q_barrier(w);
+    if (w.sh[5] == 0) return false;
+    if (wv > 0) asm volatile("buffer_inv sc0" ::: "memory");
+    stamp(a, w, ws.sl, ws.sfid, 1);
+    if (w.sub && threadIdx.x == 0) a.sub[(size_t)w.g * 16 + 9] = now();
   }
-  float v[E];
+  const gw<f32x4> xr = (gw<f32x4>)opq(a.xr + ((size_t)w.x * kFMaxN + n) * d);
+  const gptr<u32x2> g4 = (gptr<u32x2>)opq(g), b4 = (gptr<u32x2>)opq(b);
+  const gw<uint16_t> actg = opq(act);
+  int cc[C];
+#pragma unroll
+  for (int i = 0; i < C; ++i) cc[i] = min(tid + QW * 64 * i, nc - 1);
+  auto bf4 = [](u32x2 u) {
+    return (f32x4){__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u), __uint_as_float(u.y << 16),
+                   __uint_as_float(u.y & 0xffff0000u)};
+  };
+  f32x4 v[C];
+  u32x2 gr[C], br[C];
   if (mode == 0) {
     const int tok = ld_x(a.tree + n), pos = ld_x(a.tree + a.max_nodes + n);
-    const gptr<uint16_t> te = opq(a.wte) + (size_t)tok * d;
-    const gptr<uint16_t> pe = opq(a.wpe) + (size_t)pos * d;
-    uint16_t tr[E], pr[E];
+    const gptr<u32x2> te = (gptr<u32x2>)(opq(a.wte) + (size_t)tok * d);
+    const gptr<u32x2> pe = (gptr<u32x2>)(opq(a.wpe) + (size_t)pos * d);
+    u32x2 tr[C], pr[C];
 #pragma unroll
-    for (int i = 0; i < E; ++i) {
-      tr[i] = te[kk[i]];
-      pr[i] = pe[kk[i]];
+    for (int i = 0; i < C; ++i) {
+      tr[i] = te[cc[i]];
+      pr[i] = pe[cc[i]];
+      gr[i] = g4[cc[i]];
+      br[i] = b4[cc[i]];
     }
 #pragma unroll
-    for (int i = 0; i < E; ++i) v[i] = bf2f(tr[i]) + bf2f(pr[i]);
+    for (int i = 0; i < C; ++i) v[i] = bf4(tr[i]) + bf4(pr[i]);
   } else {
-    float xv[E], pv[kFXcd][E];
-    uint16_t cr[E];
+    // every XCD's partials of the row: device-coherent 16-byte loads
+    const __amdgpu_buffer_rsrc_t pr =
+        __builtin_amdgcn_make_buffer_rsrc((void*)part, (short)0, (int)(kFXcd * kFMaxN * d * 4), 0x00020000);
+    f32x4 pv[kFXcd][C];
 #pragma unroll
-    for (int i = 0; i < E; ++i) {
-      xv[i] = xr[kk[i]];
-      cr[i] = bias[kk[i]];
-    }
-    // the partial residuals are what this stage waits for
-    if (ws.on && !wait_flags(a, w, ws.id, ws.wx, ws.tag)) return false;
-    stamp(a, w, ws.sl, ws.sfid, 1);
+    for (int X = 0; X < kFXcd; ++X)
 #pragma unroll
-    for (int X = 0; X < kFXcd; ++X) {
-      const gptr<float> prow = partg + ((size_t)X * kFMaxN + n) * d;
+      for (int i = 0; i < C; ++i)
+        pv[X][i] = __builtin_bit_cast(
+            f32x4, __builtin_amdgcn_raw_buffer_load_b128(pr, (unsigned)(16 * cc[i]),
+                                                         (unsigned)(((size_t)X * kFMaxN + n) * d * 4), CP_SC1));
+    const gptr<u32x2> c4 = (gptr<u32x2>)opq(bias);
+    f32x4 xv[C];
+    u32x2 cr[C];
 #pragma unroll
-      for (int i = 0; i < E; ++i) pv[X][i] = ld_dev(prow + kk[i]);
+    for (int i = 0; i < C; ++i) {
+      xv[i] = xr[cc[i]];
+      cr[i] = c4[cc[i]];
+      gr[i] = g4[cc[i]];
+      br[i] = b4[cc[i]];
     }
     // bias, then the partials of the XCDs that own a share, in XCD order
 #pragma unroll
-    for (int i = 0; i < E; ++i) {
-      float acc = bf2f(cr[i]);
+    for (int i = 0; i < C; ++i) {
+      f32x4 acc = bf4(cr[i]);
+      if (own == (1u << kFXcd) - 1) {
 #pragma unroll
-      for (int X = 0; X < kFXcd; ++X) acc += xrange[2 * X + 1] > xrange[2 * X] ? pv[X][i] : 0.f;
+        for (int X = 0; X < kFXcd; ++X) acc += pv[X][i];
+      } else {
+#pragma unroll
+        for (int X = 0; X < kFXcd; ++X) {
+          const bool o = own >> X & 1u;
+          acc[0] += o ? pv[X][i][0] : 0.f;
+          acc[1] += o ? pv[X][i][1] : 0.f;
+          acc[2] += o ? pv[X][i][2] : 0.f;
+          acc[3] += o ? pv[X][i][3] : 0.f;
+        }
+      }
       v[i] = xv[i] + acc;
     }
+    if (w.sub && threadIdx.x == 0) a.sub[(size_t)w.g * 16 + 10] = now();
   }
   float s = 0.f;
 #pragma unroll
-  for (int i = 0; i < E; ++i) {
-    const int k = tid + i * NTH;
-    if (k < d) {
-      xr[k] = v[i];
-      s += v[i];
+  for (int i = 0; i < C; ++i) {
+    if (tid + QW * 64 * i < nc) {
+      xr[tid + QW * 64 * i] = v[i];
+      s += ((v[i][0] + v[i][1]) + (v[i][2] + v[i][3]));
     }
   }
-  // block sums, fixed order
-  auto bsum = [&](float t) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) t += __shfl_xor(t, o);
-    __syncthreads();
-    if ((tid & 63) == 0) red[tid >> 6] = t;
-    __syncthreads();
-    return ((red[0] + red[1]) + (red[2] + red[3])) + ((red[4] + red[5]) + (red[6] + red[7]));
-  };
-  const float mean = bsum(s) / d;
+  s = wave_sum(s);
+  if ((tid & 63) == 0) red[wv] = s;
+  q_barrier(w);
+  const float mean = ((red[0] + red[1]) + (red[2] + red[3])) / d;
   float q = 0.f;
 #pragma unroll
-  for (int i = 0; i < E; ++i)
-    if (tid + i * NTH < d) q += (v[i] - mean) * (v[i] - mean);
-  const float den = sqrtf(bsum(q) / d + a.eps);
-#pragma unroll
-  for (int i = 0; i < E; ++i) {
-    const int k = tid + i * NTH;
-    if (k < d) st_act(actg, n, k, d / 32, (v[i] - mean) / den * bf2f(gr[i]) + bf2f(br[i]));
+  for (int i = 0; i < C; ++i) {
+    if (tid + QW * 64 * i < nc) {
+      const f32x4 c = v[i] - mean;
+      q += ((c[0] * c[0] + c[1] * c[1]) + (c[2] * c[2] + c[3] * c[3]));
+    }
   }
+  q = wave_sum(q);
+  if ((tid & 63) == 0) red[4 + wv] = q;
+  q_barrier(w);
+  const float rden = 1.0f / sqrtf(((red[4] + red[5]) + (red[6] + red[7])) / d + a.eps);
+#pragma unroll
+  for (int i = 0; i < C; ++i) {
+    const int c = tid + QW * 64 * i;
+    if (c < nc) {
+      const f32x4 gv = bf4(gr[i]), bv = bf4(br[i]);
+      const f32x4 y = (v[i] - mean) * rden * gv + bv;
+      st_act4(actg, n, 4 * c, d / 32, y[0], y[1], y[2], y[3]);
+    }
+  }
+  if (w.sub && threadIdx.x == 0) a.sub[(size_t)w.g * 16 + 11] = now();
+  return true;
+}
+
+// ------------------------------------------------------------------ attention merge and pre-stages
+//
+// An attention unit leaves one record per node of its tile: max, sum, -, -,
+// output[64].
+constexpr int AREC = DH + 4;                // part record: max, sum, -, -, output
+
+__device__ __forceinline__ gw<float> part_rec(const FusedArgs& a, int h, int t, int u, int nl) {
+  return (gw<float>)a.apart + ((((size_t)h * 4 + t) * (a.att_units + 1) + u) * 16 + nl) * AREC;
+}
+
+// One wave merges the parts of (head h, tile t) in part order: lane i takes
+// dims 4 (i % 16) .. +3 of nodes i / 16 + 4 k, k < 4.  Per (node, dim) the
+// arithmetic is the online-softmax merge of the parts, in order.
+__device__ __forceinline__ bool merge_w0(const FusedArgs& a, const Wg& w, const WaitSpec& ws, int h, int t) {
+  if (ws.on && !poll_w0(a, w, ws.id, ws.wx, ws.tag)) return false;
+  stamp(a, w, ws.sl, ws.sfid, 1);
+  constexpr int MJ = 4;  // parts loaded per round trip
+  const int lane = opq_tid() & 63, dg = lane & 15, S = a.att_units;
+  float M[4], Ls[4];
+  f32x4 O[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    M[k] = -INFINITY;
+    Ls[k] = 0.f;
+    O[k] = (f32x4){0.f, 0.f, 0.f, 0.f};
+  }
+  for (int j0 = 0; j0 <= S; j0 += MJ) {
+    f32x2_t ml[MJ][4];
+    f32x4 ov[MJ][4];
+#pragma unroll
+    for (int jj = 0; jj < MJ; ++jj)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const gptr<float> rec = (gptr<float>)part_rec(a, h, t, min(j0 + jj, S), (lane >> 4) + 4 * k);
+        ml[jj][k] = ld_x((gptr<f32x2_t>)rec);
+        ov[jj][k] = ld_x((gptr<f32x4>)(rec + 4) + dg);
+      }
+#pragma unroll
+    for (int jj = 0; jj < MJ; ++jj) {
+      if (j0 + jj > S) break;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const float mj = ml[jj][k][0], lj = ml[jj][k][1];
+        if (mj == -INFINITY) continue;
+        const float mn = fmaxf(M[k], mj);
+        const float al = __expf(M[k] - mn), wj = __expf(mj - mn);
+        Ls[k] = fmaf(Ls[k], al, lj * wj);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) O[k][e] = fmaf(O[k][e], al, ov[jj][k][e] * wj);
+        M[k] = mn;
+      }
+    }
+  }
+  const gw<uint16_t> fo = opq(a.fo);
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int n = 16 * t + (lane >> 4) + 4 * k;
+    if (n < a.N)
+      st_act4(fo, n, h * DH + 4 * dg, a.d / 32, O[k][0] / Ls[k], O[k][1] / Ls[k], O[k][2] / Ls[k], O[k][3] / Ls[k]);
+  }
+  return true;
+}
+
+// What wave 0 does, alone, before a weight GEMM while the other waves' weight
+// loads are in flight: a LayerNorm stage's rows, or an attention-merge
+// stage's units; then it publishes that stage.
+struct PreSpec {
+  int kind;  // 0 nothing, 1 LayerNorm rows, 2 attention merges
+  int l, fid;
+  WaitSpec ws;
+  int mode;
+  gptr<uint16_t> bias, g, b;
+  const float* part;
+  unsigned own;  // XCDs that own a share of the residual GEMM
+  uint16_t* act;
+  int n_amg, NTl;
+};
+
+// Run by waves 0..3 together.  LayerNorm rows use all four; merges use wave
+// 0 (waves 1..3 have nothing to do).  Then the stage is published: the four
+// waves' stores complete, then wave 0 writes the flag.
+__device__ __forceinline__ bool do_pre(const FusedArgs& a, const Wg& w, const PreSpec& ps) {
+  if (ps.kind == 0) return true;
+  const WaitSpec none{0, 0, 0u, false, ps.l, ps.fid};
+  bool ok = true;
+  if (ps.kind == 1) {
+    for (int n = w.r; n < a.N && ok; n += kFRanks)
+      ok = a.d <= 1024 ? ln_row_q<1>(a, w, n == w.r ? ps.ws : none, n, ps.mode, ps.bias, ps.part, ps.own, ps.g,
+                                     ps.b, ps.act)
+                       : ln_row_q<2>(a, w, n == w.r ? ps.ws : none, n, ps.mode, ps.bias, ps.part, ps.own, ps.g,
+                                     ps.b, ps.act);
+  } else if (threadIdx.x < 64) {
+    for (int u = w.r; u < ps.n_amg && ok; u += kFRanks) {
+      const int h = a.xh[2 * w.x] + u / ps.NTl, t = u % ps.NTl;
+      ok = merge_w0(a, w, u == w.r ? ps.ws : none, h, t);
+    }
+  }
+  if (!ok) return false;
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  if (ps.kind == 1) q_barrier(w);
+  if (threadIdx.x == 0)
+    __hip_atomic_store(a.flags + (size_t)ps.fid * kFGroups + w.g, tag_of(w, ps.l, ps.fid), __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_WORKGROUP);
+  if (w.sub && threadIdx.x == 0) a.sub[(size_t)w.g * 16 + 12] = now();
+  stamp(a, w, ps.l, ps.fid, 2);
   return true;
 }
 
@@ -427,12 +664,17 @@ template <int NT, int RB, int U>
 __device__ __forceinline__ bool gemm_rb(const FusedArgs& a, const Wg& w, const WaitSpec& ws, int epi, int l,
                                         const int* rbs, int rb_first, int nrb, gptr<uint16_t> bias, gptr<u32x4> Wp,
                                         int KC, int M, int kc0, int kc1, const uint16_t* act, int act_kc,
-                                        float* red) {
-  constexpr int NN = 16 * NT;
-  // the wave index and step count are scalars, so the step guards below are
-  // scalar branches: an MFMA ignores EXEC and must never sit under a lane mask
+                                        float* red, const PreSpec& ps) {
+  constexpr int NN = 16 * NT, NCW = NWV - QW;
+  // Waves 4..7 compute: wave 4 + c takes k-steps kc0 + c, kc0 + c + 4, ...,
+  // and loads their weights first thing.  Waves 0..3 run the pre-stage
+  // meanwhile; then wave 0, with nothing in flight, waits for this stage's
+  // dependency.  The wave index and step count are scalars, so the step
+  // guards below are scalar branches: an MFMA ignores EXEC and must never
+  // sit under a lane mask.
   const int tid = opq_tid(), wv = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
-  const int nsteps = kc1 - kc0 > wv ? (kc1 - kc0 - wv + NWV - 1) / NWV : 0;
+  const int cw = wv - QW;
+  const int nsteps = wv >= QW && kc1 - kc0 > cw ? (kc1 - kc0 - cw + NCW - 1) / NCW : 0;
   Wp = opq(Wp);
   const gptr<uint16_t> actg = opq(act);
   bias = opq(bias);
@@ -460,12 +702,12 @@ __device__ __forceinline__ bool gemm_rb(const FusedArgs& a, const Wg& w, const W
   u32x4 bq[U][NT];
   const int klast = kc1 - 1;
   auto load_w = [&](int s, int u) {
-    const int kc = min(kc0 + wv + NWV * s, klast);
+    const int kc = min(kc0 + cw + NCW * s, klast);
 #pragma unroll
     for (int r = 0; r < RB; ++r) wq[u][r] = wb[r][(size_t)kc * 64];
   };
   auto load_a = [&](int s, int u) {
-    const int kc = min(kc0 + wv + NWV * s, klast);
+    const int kc = min(kc0 + cw + NCW * s, klast);
 #pragma unroll
     for (int t = 0; t < NT; ++t) bq[u][t] = ld_x(ab + ((size_t)t * act_kc + kc) * 64);
   };
@@ -482,13 +724,32 @@ __device__ __forceinline__ bool gemm_rb(const FusedArgs& a, const Wg& w, const W
   // in flight while the workgroup waits for it
   // only the steps this wave owns are loaded (the step bounds are uniform
   // per wave, so the guards are scalar branches)
+  // (the loads sit in the branch wave 0 does not take, so the weight
+  // registers are not live across the pre-stage's code)
+  if (wv < QW) {
+    bool ok = do_pre(a, w, ps);
+    if (wv == 0) {
+      stamp(a, w, ws.sl, ws.sfid, 0);
+      if (ok && ws.on) ok = poll_w0(a, w, ws.id, ws.wx, ws.tag);
+      if (lane == 0) w.sh[0] = ok;
+    }
+  } else {
 #pragma unroll
-  for (int u = 0; u < U; ++u)
-    if (u < nsteps) load_w(u, u);
-  if (ws.on && !wait_flags(a, w, ws.id, ws.wx, ws.tag)) return false;
+    for (int u = 0; u < U; ++u)
+      if (u < nsteps) load_w(u, u);
+  }
+  lds_barrier();
+  if (w.sh[0] == 0) return false;
+  lds_barrier();
+  if (wv > 0) asm volatile("buffer_inv sc0" ::: "memory");
   stamp(a, w, ws.sl, ws.sfid, 1);
+  if (w.sub && threadIdx.x == 0) a.sub[(size_t)w.g * 16 + 0] = now();
   const bool sub = epi == a.sub_epi;
   if (sub) sub_stamp(a, w, l, 0);
+  if (w.sub && wv == QW) {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    if (lane == 0) a.sub[(size_t)w.g * 16 + 7] = now();
+  }
 #pragma unroll
   for (int u = 0; u < U; ++u)
     if (u < nsteps) load_a(u, u);
@@ -520,7 +781,8 @@ __device__ __forceinline__ bool gemm_rb(const FusedArgs& a, const Wg& w, const W
 #pragma unroll
     for (int t = 0; t < NT; ++t)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) red[((wv * NN) + 16 * t + (lane & 15)) * 16 + 4 * (lane >> 4) + q] = acc[r][t][q];
+      for (int q = 0; q < 4; ++q)
+        if (wv >= QW) red[((cw * NN) + 16 * t + (lane & 15)) * 16 + 4 * (lane >> 4) + q] = acc[r][t][q];
     lds_barrier();
     // a compile-time count of slots per thread: a run-time loop here holding
     // stores would make the compiler wait for all earlier stores first
@@ -531,7 +793,7 @@ __device__ __forceinline__ bool gemm_rb(const FusedArgs& a, const Wg& w, const W
       const int row = idx & 15, node = idx >> 4;
       float sum = red[idx];
 #pragma unroll
-      for (int ww = 1; ww < NWV; ++ww) sum += red[ww * NN * 16 + idx];
+      for (int ww = 1; ww < NCW; ++ww) sum += red[ww * NN * 16 + idx];
       const int o = rbv[r] * 16 + row;
       if (node < N && o < M) epilogue(a, w, epi, l, node, o, has_bias ? sum + bf2f(bias_r[r]) : sum);
     }
@@ -544,18 +806,33 @@ __device__ __forceinline__ bool gemm_rb(const FusedArgs& a, const Wg& w, const W
 
 // one task of 1..4 row blocks, loads in flight per wave sized to the
 // register budget; three code bodies serve every stage
+// Runs the pre-stage (wave 0) when the workgroup has no GEMM task.
+__device__ __forceinline__ bool pre_only(const FusedArgs& a, const Wg& w, const PreSpec& ps) {
+  if (ps.kind == 0) return true;
+  if (threadIdx.x < QW * 64) {
+    const bool ok = do_pre(a, w, ps);
+    if (threadIdx.x == 0) w.sh[0] = ok;
+  }
+  lds_barrier();
+  const bool ok = w.sh[0] != 0;
+  lds_barrier();
+  return ok;
+}
+
 template <int NT>
 __device__ __forceinline__ bool gemm_task(const FusedArgs& a, const Wg& w, const WaitSpec& ws, int epi, int l,
                                           const int* rbs, int rb_first, int nrb, gptr<uint16_t> bias,
                                           gptr<u32x4> Wp, int KC, int M, int kc0, int kc1, const uint16_t* act,
-                                          int act_kc, float* red) {
+                                          int act_kc, float* red, const PreSpec& ps) {
+  if (nrb <= 0) return pre_only(a, w, ps);
   if (nrb == 1)
-    return gemm_rb<NT, 1, NT <= 2 ? 8 : 6>(a, w, ws, epi, l, rbs, rb_first, 1, bias, Wp, KC, M, kc0, kc1, act, act_kc,
-                                          red);
+    return gemm_rb<NT, 1, NT <= 2 ? 10 : 5>(a, w, ws, epi, l, rbs, rb_first, 1, bias, Wp, KC, M, kc0, kc1, act,
+                                           act_kc, red, ps);
   if (nrb == 2)
-    return gemm_rb<NT, 2, NT <= 2 ? 6 : 5>(a, w, ws, epi, l, rbs, rb_first, 2, bias, Wp, KC, M, kc0, kc1, act, act_kc,
-                                          red);
-  return gemm_rb<NT, 4, 4>(a, w, ws, epi, l, rbs, rb_first, nrb, bias, Wp, KC, M, kc0, kc1, act, act_kc, red);
+    return gemm_rb<NT, 2, NT <= 2 ? 10 : 5>(a, w, ws, epi, l, rbs, rb_first, 2, bias, Wp, KC, M, kc0, kc1, act,
+                                           act_kc, red, ps);
+  return gemm_rb<NT, 4, NT <= 2 ? 5 : 3>(a, w, ws, epi, l, rbs, rb_first, nrb, bias, Wp, KC, M, kc0, kc1, act,
+                                         act_kc, red, ps);
 }
 
 // ------------------------------------------------------------------ tree attention
@@ -581,7 +858,6 @@ __device__ __forceinline__ bool gemm_task(const FusedArgs& a, const Wg& w, const
 constexpr int ACH = 32 * NWV;               // prefix rows per unit: 32 per wave
 static_assert(ACH == kFAttRows, "the host counts attention units of kFAttRows rows");
 constexpr int AKS = DH + 8;                 // LDS row stride of K and V (elements)
-constexpr int AREC = DH + 4;                // part record: max, sum, -, -, output
 constexpr int A_KV_BYTES = 2 * ACH * AKS * 2;
 constexpr int A_RV_BYTES = 2 * NWV * 32 * DH * 2;  // root-path V rows, 32 per half-wave
 constexpr int A_REGION = A_KV_BYTES > A_RV_BYTES ? A_KV_BYTES : A_RV_BYTES;
@@ -589,9 +865,6 @@ constexpr int A_PART_BYTES = NWV * 16 * AREC * 4;  // the waves' states of a pre
 constexpr int A_Q_BYTES = NWV * 2 * DH * 4;        // root-path queries, one row per half-wave
 
 // the part record of (head h, tile t, unit u) for tile node nl
-__device__ __forceinline__ gw<float> part_rec(const FusedArgs& a, int h, int t, int u, int nl) {
-  return (gw<float>)a.apart + ((((size_t)h * 4 + t) * (a.att_units + 1) + u) * 16 + nl) * AREC;
-}
 
 __device__ __forceinline__ bool att_prefix_unit(const FusedArgs& a, const Wg& w, const WaitSpec& ws, int l, int h,
                                                 int t, int u, unsigned char* lds) {
@@ -606,14 +879,18 @@ __device__ __forceinline__ bool att_prefix_unit(const FusedArgs& a, const Wg& w,
   const gptr<uint16_t> vc = opq(a.vc + head_rows * a.max_ctx * DH);
   const gptr<float> qbase = opq((const float*)a.q);
   const int cb = u * ACH, nk = min(ACH, P - cb);
-  // the unit's cache rows do not depend on this layer's QKV outputs: loaded
-  // before the wait (rows past the prefix re-read the last one, zeroed below)
-  u32x4 kr[4], vr[4];
+  // The unit's cache rows do not depend on this layer's QKV outputs: waves
+  // 1..7 load them before the wait (wave 0 polls, with nothing in flight).
+  // Rows past the prefix re-read the last one and are zeroed below.
+  constexpr int KVJ = (ACH * 8 + NTH - 64 - 1) / (NTH - 64);  // 16-byte pieces per thread
+  u32x4 kr[KVJ], vr[KVJ];
+  if (wv > 0) {
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int e = tid + j * NTH, r = min(e >> 3, nk - 1), c8 = e & 7;
-    kr[j] = *(gptr<u32x4>)(kc + (size_t)(cb + r) * DH + 8 * c8);
-    vr[j] = *(gptr<u32x4>)(vc + (size_t)(cb + r) * DH + 8 * c8);
+    for (int j = 0; j < KVJ; ++j) {
+      const int e = min(tid - 64 + j * (NTH - 64), ACH * 8 - 1), r = min(e >> 3, nk - 1), c8 = e & 7;
+      kr[j] = *(gptr<u32x4>)(kc + (size_t)(cb + r) * DH + 8 * c8);
+      vr[j] = *(gptr<u32x4>)(vc + (size_t)(cb + r) * DH + 8 * c8);
+    }
   }
   if (ws.on && !wait_flags(a, w, ws.id, ws.wx, ws.tag)) return false;
   stamp(a, w, ws.sl, ws.sfid, 1);
@@ -629,12 +906,16 @@ __device__ __forceinline__ bool att_prefix_unit(const FusedArgs& a, const Wg& w,
                         __uint_as_float(q1[2]), __uint_as_float(q1[3])};
     pack_hilo8(v, qh[kc2], ql[kc2]);
   }
+  if (wv > 0) {
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int e = tid + j * NTH, r = e >> 3, c8 = e & 7;
-    const bool ok = r < nk;
-    *(u32x4*)(ks + r * AKS + 8 * c8) = ok ? kr[j] : (u32x4){0, 0, 0, 0};
-    *(u32x4*)(vs + r * AKS + 8 * c8) = ok ? vr[j] : (u32x4){0, 0, 0, 0};
+    for (int j = 0; j < KVJ; ++j) {
+      const int e = tid - 64 + j * (NTH - 64), r = e >> 3, c8 = e & 7;
+      if (e < ACH * 8) {
+        const bool ok = r < nk;
+        *(u32x4*)(ks + r * AKS + 8 * c8) = ok ? kr[j] : (u32x4){0, 0, 0, 0};
+        *(u32x4*)(vs + r * AKS + 8 * c8) = ok ? vr[j] : (u32x4){0, 0, 0, 0};
+      }
+    }
   }
   __syncthreads();
   float m = -INFINITY, lsum = 0.f;
@@ -843,37 +1124,6 @@ __device__ __forceinline__ bool att_root_unit(const FusedArgs& a, const Wg& w, c
 
 // the merge of (head h, tile t): prefix parts in order, then the root path,
 // written as the out-projection's float16 input
-__device__ __forceinline__ bool att_merge_unit(const FusedArgs& a, const Wg& w, const WaitSpec& ws, int h, int t) {
-  if (ws.on && !wait_flags(a, w, ws.id, ws.wx, ws.tag)) return false;
-  stamp(a, w, ws.sl, ws.sfid, 1);
-  constexpr int DPT = 16 * DH / NTH;
-  const int tid = opq_tid();
-  const int nl = tid / (DH / DPT), d0 = DPT * (tid % (DH / DPT));
-  const int n = 16 * t + nl, S = a.att_units;
-  float M = -INFINITY, L = 0.f, O[DPT];
-#pragma unroll
-  for (int e = 0; e < DPT; ++e) O[e] = 0.f;
-  for (int j = 0; j <= S; ++j) {
-    const gptr<float> rec = (gptr<float>)part_rec(a, h, t, j, nl);
-    const float mj = ld_x(rec), lj = ld_x(rec + 1);
-    float ov[DPT];
-#pragma unroll
-    for (int e = 0; e < DPT; ++e) ov[e] = ld_x(rec + 4 + d0 + e);
-    if (mj == -INFINITY) continue;
-    const float mn = fmaxf(M, mj);
-    const float al = __expf(M - mn), wj = __expf(mj - mn);
-    L = fmaf(L, al, lj * wj);
-#pragma unroll
-    for (int e = 0; e < DPT; ++e) O[e] = fmaf(O[e], al, ov[e] * wj);
-    M = mn;
-  }
-  if (n < a.N) {
-#pragma unroll
-    for (int e = 0; e < DPT; ++e) st_act(a.fo, n, h * DH + d0 + e, a.d / 32, O[e] / L);
-  }
-  return true;
-}
-
 // ------------------------------------------------------------------ the plan of one workgroup
 //
 // int32 [kPlanStride] per workgroup (see FusedPlan in ssd_internal.h):
@@ -912,6 +1162,7 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
   int* sh = (int*)(lds + A_REGION + A_PART_BYTES + A_Q_BYTES);  // 16 words
   float* red = (float*)lds;                                        // GEMM / LN reductions
   Wg w;
+  w.sub = 0;
   w.x = (int)xcc_id();
   w.r = blockIdx.x >> 3;
   w.g = w.x * kFRanks + w.r;
@@ -924,6 +1175,7 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
     if (ok) ok = __hip_atomic_exchange(&a.ctl[FZ_CLAIM + w.g], E, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != E;
     if (!ok) raise_abort(a, 1u);
     sh[3] = ok;
+    sh[4] = 0;  // the counter of q_barrier
   }
   __syncthreads();
   w.E = (unsigned)sh[1];
@@ -952,115 +1204,128 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
   uint16_t* act1 = a.act1 + (size_t)w.x * a.act_stride;
   uint16_t* act2 = a.act2 + (size_t)w.x * a.act_stride;
   const int N = a.N, L = a.L;
-  constexpr int E = 4;  // LayerNorm elements per thread: d <= 2048
 
   // One runtime loop over the pass's stages, so that each stage body (the
   // LayerNorm, the GEMM at 1, 2 and 4 row blocks, the attention units)
   // exists once in the code.
   //   kind 0..7: LN1, QKV, ATT, AMG (attention merge), WO, LN2, FC, WPR of
-  //   layer l; 8: final LayerNorm; 9: LM head.
+  //   layer l; 8: final LayerNorm; 9: LM head.  Kinds 1, 4, 6 and 9 run in
+  //   the same iteration as the stage before them.
   const int NTl = (N + 15) / 16;             // 16-node tiles
   const int S = a.att_units;                 // prefix units of 256 cache rows
   const int nhx = a.xh[2 * w.x + 1] - a.xh[2 * w.x];
   const int n_attu = nhx * NTl * (S + 1);    // attention units of this XCD (prefix units + root unit per tile)
   const int n_amg = nhx * NTl;               // attention merges of this XCD
+  const unsigned own_h = owner_mask(a.xh), own_f = owner_mask(a.xf);
   const int nst = L * 8 + 2;
   for (int st = 0; st < nst; ++st) {
     const int l = st < L * 8 ? st / 8 : L;
     const int kind = st < L * 8 ? st % 8 : 8 + (st - L * 8);
-    // flag id, waited flag id / layer / XCD (-1 all, -2 none), work present
-    int fid, wid = 0, wl = l, wx = w.x, work;
-    switch (kind) {
-      case 0: fid = FS_LN1; wid = FS_WPR; wl = l - 1; wx = l > 0 ? -1 : -2; work = w.r < N; break;
-      case 1: fid = FS_QKV; wid = FS_LN1; work = n_qkv > 0; break;
-      case 2: fid = FS_ATT; wid = FS_QKV; work = w.r < n_attu; break;
-      case 3: fid = FS_AMG; wid = FS_ATT; work = w.r < n_amg; break;
-      case 4: fid = FS_WO; wid = FS_AMG; work = n_wo > 0; break;
-      case 5: fid = FS_LN2; wid = FS_WO; wx = -1; work = w.r < N; break;
-      case 6: fid = FS_FC; wid = FS_LN2; work = n_fc > 0; break;
-      case 7: fid = FS_WPR; wid = FS_FC; work = n_wpr > 0; break;
-      case 8: fid = FS_LN1; wid = FS_WPR; wl = L - 1; wx = -1; work = w.r < N; break;
-      default: fid = FS_QKV; wid = FS_LN1; work = hb1 > hb0; break;
+    if (kind == 1 || kind == 4 || kind == 6 || kind == 9) continue;  // they run with the stage before them
+    if (kind == 2) {
+      // attention units of this XCD's heads, dealt to its ranks in turn
+      progress(a, w, l * kFStages + FS_ATT);
+      stamp(a, w, l, FS_ATT, 0);
+      const WaitSpec ws{FS_QKV, w.x, tag_of(w, l, FS_QKV), true, l, FS_ATT};
+      const WaitSpec none{0, 0, 0u, false, l, FS_ATT};
+      for (int u = w.r; u < n_attu; u += kFRanks) {
+        const int hloc = u / (NTl * (S + 1)), rem = u - hloc * (NTl * (S + 1));
+        const int t = rem / (S + 1), part = rem - t * (S + 1);
+        const int h = a.xh[2 * w.x] + hloc;
+        const WaitSpec& wsu = u == w.r ? ws : none;
+        const bool ok = part < S ? att_prefix_unit(a, w, wsu, l, h, t, part, lds)
+                                 : att_root_unit(a, w, wsu, l, h, t, lds);
+        if (!ok) goto out;
+      }
+      signal(a, w, l, FS_ATT, false);
+      stamp(a, w, l, FS_ATT, 2);
+      continue;
     }
-    progress(a, w, kind < 8 ? l * kFStages + fid : L * kFStages + (kind == 8 ? 0 : 1));
-    stamp(a, w, l, fid, 0);
-    if (work) {
-      // each body loads what does not depend on the previous stage, then waits
-      const WaitSpec ws{wid, wx, tag_of(w, wl, wid), wx != -2, l, fid};
-      const WaitSpec none{0, 0, 0u, false, l, fid};
-      if (kind == 0 || kind == 5 || kind == 8) {
-        // residual update + LayerNorm of this workgroup's node rows
-        const int mode = (kind == 0 && l == 0) ? 0 : 1;
-        gptr<uint16_t> bias, g, b;
-        const float* part;
-        const int* xrange;
-        uint16_t* act;
-        if (kind == 5) {
-          bias = G<uint16_t>(lw(a, l, LB_O));
-          part = a.part_o;
-          xrange = a.xh;
-          g = G<uint16_t>(lw(a, l, LN2G));
-          b = G<uint16_t>(lw(a, l, LN2B));
-          act = act2;
-        } else {
-          const int lp = kind == 8 ? L - 1 : max(l - 1, 0);
-          bias = G<uint16_t>(lw(a, lp, LB_PR));
-          part = a.part_p;
-          xrange = a.xf;
-          g = kind == 8 ? G<uint16_t>(a.lnf_g) : G<uint16_t>(lw(a, l, LN1G));
-          b = kind == 8 ? G<uint16_t>(a.lnf_b) : G<uint16_t>(lw(a, l, LN1B));
-          act = act1;
-        }
-        for (int n = w.r; n < N; n += kFRanks)
-          if (!ln_row<E>(a, w, n == w.r ? ws : none, n, mode, bias, part, xrange, g, b, act, red)) goto out;
-      } else if (kind == 2) {
-        // attention units of this XCD's heads, dealt to its ranks in turn
-        for (int u = w.r; u < n_attu; u += kFRanks) {
-          const int hloc = u / (NTl * (S + 1)), rem = u - hloc * (NTl * (S + 1));
-          const int t = rem / (S + 1), part = rem - t * (S + 1);
-          const int h = a.xh[2 * w.x] + hloc;
-          const WaitSpec& wsu = u == w.r ? ws : none;
-          const bool ok = part < S ? att_prefix_unit(a, w, wsu, l, h, t, part, lds)
-                                   : att_root_unit(a, w, wsu, l, h, t, lds);
-          if (!ok) goto out;
-        }
-      } else if (kind == 3) {
-        for (int u = w.r; u < n_amg; u += kFRanks) {
-          const int h = a.xh[2 * w.x] + u / NTl, t = u % NTl;
-          if (!att_merge_unit(a, w, u == w.r ? ws : none, h, t)) goto out;
-        }
-      } else if (kind == 9) {
-        for (int b0 = hb0, j = 0; b0 < hb1; b0 += 4, ++j) {
-          progress(a, w, L * kFStages + 1 + j / 2);
-          if (!gemm_task<NT>(a, w, b0 == hb0 ? ws : none, FE_HEAD, L, nullptr, b0, min(4, hb1 - b0),
-                             G<uint16_t>(nullptr), G<u32x4>(a.p_head), KCd, a.V, 0, KCd, act1, KCd, red))
-            goto out;
-        }
-      } else {
-        // the weight GEMMs of a layer
-        int epi, nrb, slot, KC, Mo, k0, k1, akc;
-        gptr<uint16_t> bias = G<uint16_t>(nullptr);
-        const uint16_t* act;
-        switch (kind) {
-          case 1: epi = FE_QKV; nrb = n_qkv; slot = PL_QKV; KC = KCd; Mo = 3 * d; k0 = 0; k1 = KCd; akc = KCd;
-                  bias = G<uint16_t>(lw(a, l, LB_QKV)); act = act1; break;
-          case 4: epi = FE_WO; nrb = n_wo; slot = PL_WO; KC = KCd; Mo = d; k0 = kh0; k1 = kh1; akc = KCd;
-                  act = a.fo; break;
-          case 6: epi = FE_FC; nrb = n_fc; slot = PL_FC; KC = KCd; Mo = M; k0 = 0; k1 = KCd; akc = KCd;
-                  bias = G<uint16_t>(lw(a, l, LB_FC)); act = act2; break;
-          default: epi = FE_WPR; nrb = n_wpr; slot = PL_WPR; KC = KCm; Mo = d; k0 = kf0; k1 = kf1; akc = KCm;
-                   act = a.ff; break;
-        }
-        const int wslot = kind == 1 ? LW_QKV : kind == 4 ? LW_O : kind == 6 ? LW_FC : LW_PR;
-        if (!gemm_task<NT>(a, w, ws, epi, l, p + slot + 1, 0, nrb, bias, G<u32x4>(lw(a, l, wslot)), KC, Mo, k0, k1,
-                           act, akc, red))
+    if (kind == 7) {
+      // MLP down-projection over this XCD's hidden slice: partial residuals
+      progress(a, w, l * kFStages + FS_WPR);
+      stamp(a, w, l, FS_WPR, 0);
+      w.sub = a.sub && l == a.sub_l && a.sub_kind == 7;
+      if (w.sub && threadIdx.x == 0) a.sub[(size_t)w.g * 16 + 8] = now();
+      const WaitSpec ws{FS_FC, w.x, tag_of(w, l, FS_FC), true, l, FS_WPR};
+      PreSpec nopre{};
+      if (!gemm_task<NT>(a, w, ws, FE_WPR, l, p + PL_WPR + 1, 0, n_wpr, G<uint16_t>(nullptr),
+                         G<u32x4>(lw(a, l, LW_PR)), KCm, d, kf0, kf1, a.ff, KCm, red, nopre))
+        goto out;
+      signal(a, w, l, FS_WPR, true);
+      stamp(a, w, l, FS_WPR, 2);
+      continue;
+    }
+    // kind 0, 3, 5, 8: wave 0 runs this stage alone (LayerNorm rows, or
+    // attention merges) while waves 1..7 already load the weights of the
+    // GEMM stage that follows it (QKV, out-projection, MLP up-projection, LM
+    // head), which the workgroup then runs.
+    PreSpec ps{};
+    ps.l = l;
+    ps.kind = kind == 3 ? 2 : 1;
+    ps.fid = kind == 3 ? FS_AMG : kind == 5 ? FS_LN2 : FS_LN1;
+    ps.n_amg = n_amg;
+    ps.NTl = NTl;
+    ps.mode = (kind == 0 && l == 0) ? 0 : 1;
+    if (kind == 3) {
+      ps.ws = WaitSpec{FS_ATT, w.x, tag_of(w, l, FS_ATT), true, l, FS_AMG};
+    } else if (kind == 5) {
+      ps.ws = WaitSpec{FS_WO, -1, tag_of(w, l, FS_WO), true, l, FS_LN2};
+      ps.bias = G<uint16_t>(lw(a, l, LB_O));
+      ps.part = a.part_o;
+      ps.own = own_h;
+      ps.g = G<uint16_t>(lw(a, l, LN2G));
+      ps.b = G<uint16_t>(lw(a, l, LN2B));
+      ps.act = act2;
+    } else {
+      const int lp = kind == 8 ? L - 1 : max(l - 1, 0);
+      ps.ws = WaitSpec{FS_WPR, -1, tag_of(w, lp, FS_WPR), kind == 8 || l > 0, l, FS_LN1};
+      ps.bias = G<uint16_t>(lw(a, lp, LB_PR));
+      ps.part = a.part_p;
+      ps.own = own_f;
+      ps.g = kind == 8 ? G<uint16_t>(a.lnf_g) : G<uint16_t>(lw(a, l, LN1G));
+      ps.b = kind == 8 ? G<uint16_t>(a.lnf_b) : G<uint16_t>(lw(a, l, LN1B));
+      ps.act = act1;
+    }
+    progress(a, w, l * kFStages + ps.fid);
+    stamp(a, w, l, ps.fid, 0);
+    int gfid, epi, nrb, Mo, k0 = 0, k1 = KCd, rb_first = 0;
+    const int* rbs = nullptr;
+    gptr<uint16_t> bias = G<uint16_t>(nullptr);
+    gptr<u32x4> Wm;
+    const uint16_t* act = act1;
+    switch (kind) {
+      case 0: gfid = FS_QKV; epi = FE_QKV; nrb = n_qkv; rbs = p + PL_QKV + 1; Wm = G<u32x4>(lw(a, l, LW_QKV));
+              Mo = 3 * d; bias = G<uint16_t>(lw(a, l, LB_QKV)); break;
+      case 3: gfid = FS_WO; epi = FE_WO; nrb = n_wo; rbs = p + PL_WO + 1; Wm = G<u32x4>(lw(a, l, LW_O)); Mo = d;
+              k0 = kh0; k1 = kh1; act = a.fo; break;
+      case 5: gfid = FS_FC; epi = FE_FC; nrb = n_fc; rbs = p + PL_FC + 1; Wm = G<u32x4>(lw(a, l, LW_FC)); Mo = M;
+              bias = G<uint16_t>(lw(a, l, LB_FC)); act = act2; break;
+      default: gfid = FS_QKV; epi = FE_HEAD; nrb = min(4, hb1 - hb0); rb_first = hb0; Wm = G<u32x4>(a.p_head);
+               Mo = a.V; break;
+    }
+    w.sub = a.sub && l == a.sub_l && a.sub_kind == kind + 1;
+    if (w.sub && threadIdx.x == 0) a.sub[(size_t)w.g * 16 + 8] = now();
+    {
+      const WaitSpec gws{ps.fid, w.x, tag_of(w, l, ps.fid), true, l, gfid};
+      if (!gemm_task<NT>(a, w, gws, epi, l, rbs, rb_first, nrb, bias, Wm, KCd, Mo, k0, k1, act, KCd, red, ps))
+        goto out;
+    }
+    if (kind == 8) {
+      // the rest of this workgroup's LM-head row blocks, 4 at a time
+      const WaitSpec none{0, 0, 0u, false, l, gfid};
+      PreSpec nopre{};
+      for (int b0 = hb0 + 4, j = 1; b0 < hb1; b0 += 4, ++j) {
+        progress(a, w, L * kFStages + 1 + j / 2);
+        if (!gemm_task<NT>(a, w, none, FE_HEAD, L, nullptr, b0, min(4, hb1 - b0), G<uint16_t>(nullptr),
+                           G<u32x4>(a.p_head), KCd, a.V, 0, KCd, act1, KCd, red, nopre))
           goto out;
       }
     }
-    if (a.sub && kind == a.sub_kind) sub_stamp(a, w, l, 4);
-    signal(a, w, l, fid, kind == 4 || kind == 7);
-    if (a.sub && kind == a.sub_kind) sub_stamp(a, w, l, 5);
-    stamp(a, w, l, fid, 2);
+    if (a.sub && kind + 1 == a.sub_kind) sub_stamp(a, w, l, 4);
+    signal(a, w, l, gfid, kind == 3);
+    if (a.sub && kind + 1 == a.sub_kind) sub_stamp(a, w, l, 5);
+    stamp(a, w, l, gfid, 2);
   }
 out:
   __syncthreads();

@@ -759,6 +759,7 @@ static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int3
     a.poll_sleep = g_fz_poll_sleep;
     a.prefetch = getenv("SSD_FZ_PF") ? atoi(getenv("SSD_FZ_PF")) : 0;
     a.sub = kv->fz.trace ? kv->fz_sub : nullptr;
+    if (a.sub) HIP_TRY(hipMemsetAsync(a.sub, 0, (size_t)kFGroups * 16 * 8, s));
     a.sub_l = 10;
     a.sub_kind = getenv("SSD_FZ_SUBKIND") ? atoi(getenv("SSD_FZ_SUBKIND")) : 6;
     a.sub_epi = getenv("SSD_FZ_SUBEPI") ? atoi(getenv("SSD_FZ_SUBEPI")) : 2;
