@@ -528,64 +528,73 @@ __device__ __forceinline__ gw<float> part_rec(const FusedArgs& a, int h, int t, 
   return (gw<float>)a.apart + ((((size_t)h * 4 + t) * (a.att_units + 1) + u) * 16 + nl) * AREC;
 }
 
-// One wave merges the parts of (head h, tile t) in part order: lane i takes
-// dims 4 (i % 16) .. +3 of nodes i / 16 + 4 k, k < 4.  Per (node, dim) the
+// The whole workgroup merges the parts of (head h, tile t) in part order:
+// thread i takes dims 2 (i % 32), +1 of node i / 32.  Per (node, dim) the
 // arithmetic is the online-softmax merge of the parts, in order.
-__device__ __forceinline__ bool merge_w0(const FusedArgs& a, const Wg& w, const WaitSpec& ws, int h, int t) {
-  if (ws.on && !poll_w0(a, w, ws.id, ws.wx, ws.tag)) return false;
-  stamp(a, w, ws.sl, ws.sfid, 1);
+__device__ __forceinline__ void merge_tile(const FusedArgs& a, int h, int t) {
+  const int tid = opq_tid(), nl = tid >> 5, d0 = 2 * (tid & 31), S = a.att_units;
+  float M = -INFINITY, Ls = 0.f, O0 = 0.f, O1 = 0.f;
   constexpr int MJ = 4;  // parts loaded per round trip
-  const int lane = opq_tid() & 63, dg = lane & 15, S = a.att_units;
-  float M[4], Ls[4];
-  f32x4 O[4];
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    M[k] = -INFINITY;
-    Ls[k] = 0.f;
-    O[k] = (f32x4){0.f, 0.f, 0.f, 0.f};
-  }
   for (int j0 = 0; j0 <= S; j0 += MJ) {
-    f32x2_t ml[MJ][4];
-    f32x4 ov[MJ][4];
+    f32x2_t ml[MJ], ov[MJ];
 #pragma unroll
-    for (int jj = 0; jj < MJ; ++jj)
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const gptr<float> rec = (gptr<float>)part_rec(a, h, t, min(j0 + jj, S), (lane >> 4) + 4 * k);
-        ml[jj][k] = ld_x((gptr<f32x2_t>)rec);
-        ov[jj][k] = ld_x((gptr<f32x4>)(rec + 4) + dg);
-      }
+    for (int jj = 0; jj < MJ; ++jj) {
+      const gptr<float> rec = (gptr<float>)part_rec(a, h, t, min(j0 + jj, S), nl);
+      ml[jj] = ld_x((gptr<f32x2_t>)rec);
+      ov[jj] = ld_x((gptr<f32x2_t>)(rec + 4 + d0));
+    }
 #pragma unroll
     for (int jj = 0; jj < MJ; ++jj) {
       if (j0 + jj > S) break;
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const float mj = ml[jj][k][0], lj = ml[jj][k][1];
-        if (mj == -INFINITY) continue;
-        const float mn = fmaxf(M[k], mj);
-        const float al = __expf(M[k] - mn), wj = __expf(mj - mn);
-        Ls[k] = fmaf(Ls[k], al, lj * wj);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) O[k][e] = fmaf(O[k][e], al, ov[jj][k][e] * wj);
-        M[k] = mn;
-      }
+      const float mj = ml[jj][0], lj = ml[jj][1];
+      if (mj == -INFINITY) continue;
+      const float mn = fmaxf(M, mj);
+      const float al = __expf(M - mn), wj = __expf(mj - mn);
+      Ls = fmaf(Ls, al, lj * wj);
+      O0 = fmaf(O0, al, ov[jj][0] * wj);
+      O1 = fmaf(O1, al, ov[jj][1] * wj);
+      M = mn;
     }
   }
-  const gw<uint16_t> fo = opq(a.fo);
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    const int n = 16 * t + (lane >> 4) + 4 * k;
-    if (n < a.N)
-      st_act4(fo, n, h * DH + 4 * dg, a.d / 32, O[k][0] / Ls[k], O[k][1] / Ls[k], O[k][2] / Ls[k], O[k][3] / Ls[k]);
+  const int n = 16 * t + nl;
+  if (n < a.N) {
+    const gw<uint16_t> fo = opq(a.fo);
+    st_act(fo, n, h * DH + d0, a.d / 32, O0 / Ls);
+    st_act(fo, n, h * DH + d0 + 1, a.d / 32, O1 / Ls);
   }
-  return true;
 }
 
-// What wave 0 does, alone, before a weight GEMM while the other waves' weight
-// loads are in flight: a LayerNorm stage's rows, or an attention-merge
-// stage's units; then it publishes that stage.
+// After a unit of (head h, tile t) stored its part: its flag (this pass and
+// layer's tag) is published once the part's stores are complete, then the
+// tile's flags are read; if all are set, this workgroup merges the tile.  The
+// unit whose flag completes last sees every flag, so each tile is merged at
+// least once; a tile merged twice gets the same values written twice.
+__device__ __forceinline__ void unit_done(const FusedArgs& a, const Wg& w, int l, int h, int t, int j) {
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  lds_barrier();
+  const unsigned tag = tag_of(w, l, FS_AMG);
+  unsigned* uf = a.uflag + ((size_t)h * 4 + t) * a.uf_stride;
+  if (threadIdx.x < 64) {
+    const int lane = threadIdx.x;
+    if (lane == 0) __hip_atomic_store(uf + j, tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    const unsigned v = ld_flag(uf + min(lane, a.att_units));  // (clamped: the row holds att_units + 1 flags)
+    const bool mine = lane > a.att_units || tag_reached(v, tag);
+    if (lane == 0) w.sh[6] = __all(mine);
+  }
+  lds_barrier();
+  const bool all = w.sh[6] != 0;
+  lds_barrier();
+  if (all) {
+    asm volatile("buffer_inv sc0" ::: "memory");
+    merge_tile(a, h, t);
+  }
+}
+
+// What waves 0..3 do before a weight GEMM while the other waves' weight loads
+// are in flight: a LayerNorm stage's rows; then they publish that stage.
 struct PreSpec {
-  int kind;  // 0 nothing, 1 LayerNorm rows, 2 attention merges
+  int kind;  // 0 nothing, 1 LayerNorm rows
   int l, fid;
   WaitSpec ws;
   int mode;
@@ -593,12 +602,10 @@ struct PreSpec {
   const float* part;
   unsigned own;  // XCDs that own a share of the residual GEMM
   uint16_t* act;
-  int n_amg, NTl;
 };
 
-// Run by waves 0..3 together.  LayerNorm rows use all four; merges use wave
-// 0 (waves 1..3 have nothing to do).  Then the stage is published: the four
-// waves' stores complete, then wave 0 writes the flag.
+// Run by waves 0..3 together: the LayerNorm rows, then the stage is
+// published (the four waves' stores complete, then wave 0 writes the flag).
 __device__ __forceinline__ bool do_pre(const FusedArgs& a, const Wg& w, const PreSpec& ps) {
   if (ps.kind == 0) return true;
   const WaitSpec none{0, 0, 0u, false, ps.l, ps.fid};
@@ -609,15 +616,10 @@ __device__ __forceinline__ bool do_pre(const FusedArgs& a, const Wg& w, const Pr
                                      ps.b, ps.act)
                        : ln_row_q<2>(a, w, n == w.r ? ps.ws : none, n, ps.mode, ps.bias, ps.part, ps.own, ps.g,
                                      ps.b, ps.act);
-  } else if (threadIdx.x < 64) {
-    for (int u = w.r; u < ps.n_amg && ok; u += kFRanks) {
-      const int h = a.xh[2 * w.x] + u / ps.NTl, t = u % ps.NTl;
-      ok = merge_w0(a, w, u == w.r ? ps.ws : none, h, t);
-    }
   }
   if (!ok) return false;
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  if (ps.kind == 1) q_barrier(w);
+  q_barrier(w);
   if (threadIdx.x == 0)
     __hip_atomic_store(a.flags + (size_t)ps.fid * kFGroups + w.g, tag_of(w, ps.l, ps.fid), __ATOMIC_RELAXED,
                        __HIP_MEMORY_SCOPE_WORKGROUP);
@@ -1208,20 +1210,20 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
   // One runtime loop over the pass's stages, so that each stage body (the
   // LayerNorm, the GEMM at 1, 2 and 4 row blocks, the attention units)
   // exists once in the code.
-  //   kind 0..7: LN1, QKV, ATT, AMG (attention merge), WO, LN2, FC, WPR of
-  //   layer l; 8: final LayerNorm; 9: LM head.  Kinds 1, 4, 6 and 9 run in
-  //   the same iteration as the stage before them.
+  //   kind 0..7: LN1, QKV, ATT, (3: none; the last attention unit of a
+  //   tile merges it), WO, LN2, FC, WPR of layer l; 8: final LayerNorm; 9:
+  //   LM head.  Kinds 1, 6 and 9 run in the same iteration as the
+  //   LayerNorm before them.
   const int NTl = (N + 15) / 16;             // 16-node tiles
   const int S = a.att_units;                 // prefix units of 256 cache rows
   const int nhx = a.xh[2 * w.x + 1] - a.xh[2 * w.x];
   const int n_attu = nhx * NTl * (S + 1);    // attention units of this XCD (prefix units + root unit per tile)
-  const int n_amg = nhx * NTl;               // attention merges of this XCD
   const unsigned own_h = owner_mask(a.xh), own_f = owner_mask(a.xf);
   const int nst = L * 8 + 2;
   for (int st = 0; st < nst; ++st) {
     const int l = st < L * 8 ? st / 8 : L;
     const int kind = st < L * 8 ? st % 8 : 8 + (st - L * 8);
-    if (kind == 1 || kind == 4 || kind == 6 || kind == 9) continue;  // they run with the stage before them
+    if (kind == 1 || kind == 3 || kind == 6 || kind == 9) continue;  // run with the stage before them, or none
     if (kind == 2) {
       // attention units of this XCD's heads, dealt to its ranks in turn
       progress(a, w, l * kFStages + FS_ATT);
@@ -1236,40 +1238,42 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
         const bool ok = part < S ? att_prefix_unit(a, w, wsu, l, h, t, part, lds)
                                  : att_root_unit(a, w, wsu, l, h, t, lds);
         if (!ok) goto out;
+        unit_done(a, w, l, h, t, part);
       }
       signal(a, w, l, FS_ATT, false);
       stamp(a, w, l, FS_ATT, 2);
       continue;
     }
-    if (kind == 7) {
-      // MLP down-projection over this XCD's hidden slice: partial residuals
-      progress(a, w, l * kFStages + FS_WPR);
-      stamp(a, w, l, FS_WPR, 0);
-      w.sub = a.sub && l == a.sub_l && a.sub_kind == 7;
+    if (kind == 4 || kind == 7) {
+      // the residual GEMMs: out-projection over this XCD's heads (the merged
+      // attention output), MLP down-projection over its hidden slice; both
+      // leave partial residuals for every XCD's next LayerNorm
+      const bool wo = kind == 4;
+      const int fid = wo ? FS_WO : FS_WPR;
+      progress(a, w, l * kFStages + fid);
+      stamp(a, w, l, fid, 0);
+      w.sub = a.sub && l == a.sub_l && a.sub_kind == kind;
       if (w.sub && threadIdx.x == 0) a.sub[(size_t)w.g * 16 + 8] = now();
-      const WaitSpec ws{FS_FC, w.x, tag_of(w, l, FS_FC), true, l, FS_WPR};
+      const WaitSpec ws{wo ? FS_ATT : FS_FC, w.x, tag_of(w, l, wo ? FS_ATT : FS_FC), true, l, fid};
       PreSpec nopre{};
-      if (!gemm_task<NT>(a, w, ws, FE_WPR, l, p + PL_WPR + 1, 0, n_wpr, G<uint16_t>(nullptr),
-                         G<u32x4>(lw(a, l, LW_PR)), KCm, d, kf0, kf1, a.ff, KCm, red, nopre))
-        goto out;
-      signal(a, w, l, FS_WPR, true);
-      stamp(a, w, l, FS_WPR, 2);
+      const bool ok = wo ? gemm_task<NT>(a, w, ws, FE_WO, l, p + PL_WO + 1, 0, n_wo, G<uint16_t>(nullptr),
+                                         G<u32x4>(lw(a, l, LW_O)), KCd, d, kh0, kh1, a.fo, KCd, red, nopre)
+                         : gemm_task<NT>(a, w, ws, FE_WPR, l, p + PL_WPR + 1, 0, n_wpr, G<uint16_t>(nullptr),
+                                         G<u32x4>(lw(a, l, LW_PR)), KCm, d, kf0, kf1, a.ff, KCm, red, nopre);
+      if (!ok) goto out;
+      signal(a, w, l, fid, true);
+      stamp(a, w, l, fid, 2);
       continue;
     }
-    // kind 0, 3, 5, 8: wave 0 runs this stage alone (LayerNorm rows, or
-    // attention merges) while waves 1..7 already load the weights of the
-    // GEMM stage that follows it (QKV, out-projection, MLP up-projection, LM
-    // head), which the workgroup then runs.
+    // kind 0, 5, 8: waves 0..3 run this LayerNorm stage while waves 4..7
+    // already load the weights of the GEMM stage that follows it (QKV, MLP
+    // up-projection, LM head), which the workgroup then runs.
     PreSpec ps{};
     ps.l = l;
-    ps.kind = kind == 3 ? 2 : 1;
-    ps.fid = kind == 3 ? FS_AMG : kind == 5 ? FS_LN2 : FS_LN1;
-    ps.n_amg = n_amg;
-    ps.NTl = NTl;
+    ps.kind = 1;
+    ps.fid = kind == 5 ? FS_LN2 : FS_LN1;
     ps.mode = (kind == 0 && l == 0) ? 0 : 1;
-    if (kind == 3) {
-      ps.ws = WaitSpec{FS_ATT, w.x, tag_of(w, l, FS_ATT), true, l, FS_AMG};
-    } else if (kind == 5) {
+    if (kind == 5) {
       ps.ws = WaitSpec{FS_WO, -1, tag_of(w, l, FS_WO), true, l, FS_LN2};
       ps.bias = G<uint16_t>(lw(a, l, LB_O));
       ps.part = a.part_o;
@@ -1297,8 +1301,6 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
     switch (kind) {
       case 0: gfid = FS_QKV; epi = FE_QKV; nrb = n_qkv; rbs = p + PL_QKV + 1; Wm = G<u32x4>(lw(a, l, LW_QKV));
               Mo = 3 * d; bias = G<uint16_t>(lw(a, l, LB_QKV)); break;
-      case 3: gfid = FS_WO; epi = FE_WO; nrb = n_wo; rbs = p + PL_WO + 1; Wm = G<u32x4>(lw(a, l, LW_O)); Mo = d;
-              k0 = kh0; k1 = kh1; act = a.fo; break;
       case 5: gfid = FS_FC; epi = FE_FC; nrb = n_fc; rbs = p + PL_FC + 1; Wm = G<u32x4>(lw(a, l, LW_FC)); Mo = M;
               bias = G<uint16_t>(lw(a, l, LB_FC)); act = act2; break;
       default: gfid = FS_QKV; epi = FE_HEAD; nrb = min(4, hb1 - hb0); rb_first = hb0; Wm = G<u32x4>(a.p_head);
@@ -1323,7 +1325,7 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
       }
     }
     if (a.sub && kind + 1 == a.sub_kind) sub_stamp(a, w, l, 4);
-    signal(a, w, l, gfid, kind == 3);
+    signal(a, w, l, gfid, false);
     if (a.sub && kind + 1 == a.sub_kind) sub_stamp(a, w, l, 5);
     stamp(a, w, l, gfid, 2);
   }

@@ -417,6 +417,7 @@ static ssd_status fused_setup(ssd_kv* kv) {
   const size_t o_fl = take((size_t)kFStages * kFGroups * 4), o_ctl = take((size_t)kFCtlWords * 4);
   const size_t o_prog = take((size_t)kFGroups * 4), o_plan = take(tabs.size() * 4), o_sink = take(4);
   const size_t o_sub = take((size_t)kFGroups * 16 * 8);
+  const size_t o_uf = take((size_t)c.n_head * 4 * att_parts * 4);
   static const hipError_t prep = fused_prepare();
   if (prep != hipSuccess) return SSD_OK;  // keep the per-sub-layer kernels
   HIP_TRY(hipMalloc(&kv->fz_ws, off));
@@ -438,6 +439,8 @@ static ssd_status fused_setup(ssd_kv* kv) {
   a.prog = (unsigned*)(b + o_prog);
   a.sink = (unsigned*)(b + o_sink);
   kv->fz_sub = (unsigned long long*)(b + o_sub);
+  a.uflag = (unsigned*)(b + o_uf);
+  a.uf_stride = (int)att_parts;
   for (int nt = 1; nt <= 4; ++nt) kv->fz_plan[nt] = (int*)(b + o_plan) + (size_t)(nt - 1) * kFGroups * kPlanStride;
   a.err = kv->d_err;
   a.timeout = 20000000ull;  // 200 ms

@@ -216,6 +216,8 @@ struct FusedArgs {
   uint16_t* fo;             // attention outputs, float16 fragments [4 tiles][d / 32][512]
   float* apart;             // attention parts [H][4 tiles][att_units + 1][16][68]: max, sum, -, -, output
   int att_units;            // prefix units of 256 cache rows: ceil(P / 256)
+  unsigned* uflag;          // attention unit flags [H][4 tiles][uf_stride]: the tag of the unit's pass and layer
+  int uf_stride;            // >= att_units + 1
   uint16_t* ff;             // GELU outputs, float16 fragments [4 tiles][M / 32][512]
   float *part_o, *part_p;   // partial residuals [kFXcd][kFMaxN][d]
   unsigned* flags;          // [kFStages][kFGroups]
