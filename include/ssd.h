@@ -256,8 +256,9 @@ ssd_status ssd_verify_path(const ssd_model *m, const ssd_kv *kv, int32_t n, int3
 /* Host-only: the persistent launch's work split for a model shape and a
  * count of 16-node tiles (1..4), as the session computes it.  tab receives
  * [256][32] int32 rows, one per compute workgroup (XCD x, rank r at row
- * 32 x + r): [0] attention units, then up to 8 entries head | tile << 16;
- * [9] QKV row blocks, then up to 4 row-block indices of W_qkv; [14] the same
+ * 32 x + r): [0] the rank's position in the order its XCD's attention units
+ * are dealt in (unit u goes to position u mod 32); [9] QKV row blocks, then
+ * up to 4 row-block indices of W_qkv; [14] the same
  * for W_o; [19] for W_fc; [24] for W_pr; [29], [30] the workgroup's range of
  * LM-head row blocks.  xh[2x], xh[2x+1] bound XCD x's heads; xf[2x], xf[2x+1]
  * its hidden features in units of 32.  Errors: SSD_E_INVALID_ARG (null
@@ -279,12 +280,6 @@ ssd_status ssd_fused_plan(int32_t n_head, int32_t d_model, int32_t d_mlp, int32_
  * recording.  Errors: SSD_E_INVALID_ARG (null session), SSD_E_UNSUPPORTED
  * (the session has no persistent pass). */
 ssd_status ssd_kv_set_trace(ssd_kv *kv, uint64_t *buf);
-
-/* Prefetch distance of the persistent launch, in stages (a layer has seven:
- * LayerNorm, QKV, attention, out-projection, LayerNorm, MLP up, MLP down);
- * default 1.  Results are bitwise the same for every value.  Process-wide.
- * Errors: SSD_E_INVALID_ARG (outside 0..8). */
-ssd_status ssd_set_fused_ahead(int32_t stages);
 
 const char *ssd_status_string(ssd_status s);
 const char *ssd_last_error(void);

@@ -26,12 +26,8 @@
 //    increasing tag (pass, layer, stage).  A workgroup writes its outputs,
 //    waits for its stores, then stores its flag; consumers poll the 32 flags
 //    of their XCD or all 256 flags.  Data and flags read across XCDs use
-//    device-coherent (sc1) accesses; inside an XCD plain stores and
-//    non-temporal loads (which miss the CU's L1) suffice.
-//  * 256 prefetch workgroups (blocks 256..511) each follow one compute
-//    workgroup on the same XCD, loading the weights (and cached K/V) of its
-//    next stage into that XCD's L2 while it waits on a dependency.  They only
-//    read; nothing waits on them.
+//    device-coherent (sc1) accesses; inside an XCD plain stores, and loads
+//    after the waiting wave dropped its CU's L1 lines, suffice.
 //  * Every wait is bounded (s_memrealtime); a timeout raises an abort word
 //    that every other wait also watches, so all workgroups leave the kernel,
 //    and the session's error counter records it.
@@ -324,14 +320,6 @@ __device__ __forceinline__ void signal_w0(const FusedArgs& a, const Wg& w, int l
                        __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
-// progress word read by this workgroup's prefetcher: pass (low 16 bits) in
-// the high half, step in the low half (0xffff: done)
-__device__ __forceinline__ void progress(const FusedArgs& a, const Wg& w, int step) {
-  if (threadIdx.x == 0)
-    __hip_atomic_store(&a.prog[w.g], ((w.E & 0xffffu) << 16) | (unsigned)min(step, 0xffff), __ATOMIC_RELAXED,
-                       __HIP_MEMORY_SCOPE_AGENT);
-}
-
 // stage timestamps (when the session traces): entry, dependency met, done
 __device__ __forceinline__ void stamp(const FusedArgs& a, const Wg& w, int l, int s, int k) {
   if (a.trace && threadIdx.x == 0)
@@ -379,6 +367,33 @@ __device__ __forceinline__ float wave_sum(float x) {
   const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 32));
   const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 48));
   return (r0 + r1) + (r2 + r3);
+}
+
+// Max / sum over each half-wave (lanes 0..31, 32..63), the half's value in
+// each of its lanes: DPP inside rows of 16, then the half's two row values
+// in lane order.
+__device__ __forceinline__ float half_pick(float x, float (*op)(float, float)) {
+  const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 0));
+  const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 16));
+  const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 32));
+  const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 48));
+  return (threadIdx.x & 32) ? op(r2, r3) : op(r0, r1);
+}
+__device__ __forceinline__ float fmax_f(float a, float b) { return fmaxf(a, b); }
+__device__ __forceinline__ float fadd_f(float a, float b) { return a + b; }
+__device__ __forceinline__ float half_max(float x) {
+  x = fmaxf(x, dpp_f<0xB1>(x));
+  x = fmaxf(x, dpp_f<0x4E>(x));
+  x = fmaxf(x, dpp_f<0x141>(x));
+  x = fmaxf(x, dpp_f<0x140>(x));
+  return half_pick(x, fmax_f);
+}
+__device__ __forceinline__ float half_sum(float x) {
+  x += dpp_f<0xB1>(x);
+  x += dpp_f<0x4E>(x);
+  x += dpp_f<0x141>(x);
+  x += dpp_f<0x140>(x);
+  return half_pick(x, fadd_f);
 }
 
 // bit X set: XCD X owns a share of the range (heads, or MLP features)
@@ -861,7 +876,7 @@ constexpr int ACH = 32 * NWV;               // prefix rows per unit: 32 per wave
 static_assert(ACH == kFAttRows, "the host counts attention units of kFAttRows rows");
 constexpr int AKS = DH + 8;                 // LDS row stride of K and V (elements)
 constexpr int A_KV_BYTES = 2 * ACH * AKS * 2;
-constexpr int A_RV_BYTES = 2 * NWV * 32 * DH * 2;  // root-path V rows, 32 per half-wave
+constexpr int A_RV_BYTES = 2 * NWV * 32 * AKS * 2;  // root-path V rows, 32 per half-wave (padded rows)
 constexpr int A_REGION = A_KV_BYTES > A_RV_BYTES ? A_KV_BYTES : A_RV_BYTES;
 constexpr int A_PART_BYTES = NWV * 16 * AREC * 4;  // the waves' states of a prefix unit
 constexpr int A_Q_BYTES = NWV * 2 * DH * 4;        // root-path queries, one row per half-wave
@@ -896,6 +911,7 @@ __device__ __forceinline__ bool att_prefix_unit(const FusedArgs& a, const Wg& w,
   }
   if (ws.on && !wait_flags(a, w, ws.id, ws.wx, ws.tag)) return false;
   stamp(a, w, ws.sl, ws.sfid, 1);
+  if (w.sub && ws.on && threadIdx.x == 0) a.sub[(size_t)w.g * 16 + 0] = now();
   // queries (B operand: node 16 t + i, dims 32 kc2 + 8 g .. +8)
   const int qn = min(16 * t + i, N - 1);
   u32x4 qh[2], ql[2];
@@ -908,6 +924,7 @@ __device__ __forceinline__ bool att_prefix_unit(const FusedArgs& a, const Wg& w,
                         __uint_as_float(q1[2]), __uint_as_float(q1[3])};
     pack_hilo8(v, qh[kc2], ql[kc2]);
   }
+  if (w.sub && threadIdx.x == 0) a.sub[(size_t)w.g * 16 + 3] = now();
   if (wv > 0) {
 #pragma unroll
     for (int j = 0; j < KVJ; ++j) {
@@ -920,6 +937,7 @@ __device__ __forceinline__ bool att_prefix_unit(const FusedArgs& a, const Wg& w,
     }
   }
   __syncthreads();
+  if (w.sub && threadIdx.x == 0) a.sub[(size_t)w.g * 16 + 4] = now();
   float m = -INFINITY, lsum = 0.f;
   f32x4 o[4];
 #pragma unroll
@@ -974,6 +992,7 @@ __device__ __forceinline__ bool att_prefix_unit(const FusedArgs& a, const Wg& w,
       o[tt] = mfma_bf16(va, pl, o[tt]);
     }
   }
+  if (w.sub && threadIdx.x == 0) a.sub[(size_t)w.g * 16 + 5] = now();
   // this wave's state of node 16 t + i: lane (i, g) holds dims 16 tt + 4 g + r
   {
     float* rec = wpart + (wv * 16 + i) * AREC;
@@ -984,7 +1003,7 @@ __device__ __forceinline__ bool att_prefix_unit(const FusedArgs& a, const Wg& w,
 #pragma unroll
     for (int tt = 0; tt < 4; ++tt) *(f32x4*)(rec + 4 + 16 * tt + 4 * g) = o[tt];
   }
-  __syncthreads();
+  lds_barrier();
   // the waves merged in wave order into the unit's part: thread -> node,
   // DPT consecutive dims
   {
@@ -993,17 +1012,28 @@ __device__ __forceinline__ bool att_prefix_unit(const FusedArgs& a, const Wg& w,
     float M = -INFINITY, L = 0.f, O[DPT];
 #pragma unroll
     for (int e = 0; e < DPT; ++e) O[e] = 0.f;
+    // every wave's state read at once (one LDS round trip), then merged in
+    // wave order; a wave with no keys (max -inf) is skipped
+    float mv[NWV], lv[NWV], ovv[NWV][DPT];
+#pragma unroll
     for (int j = 0; j < NWV; ++j) {
       const float* rec = wpart + (j * 16 + nl) * AREC;
-      const float mj = rec[0], lj = rec[1];
-      if (mj == -INFINITY) continue;
-      const float mn = fmaxf(M, mj);
-      const float al = __expf(M - mn), wj = __expf(mj - mn);
-      L = fmaf(L, al, lj * wj);
+      mv[j] = rec[0];
+      lv[j] = rec[1];
 #pragma unroll
-      for (int e = 0; e < DPT; ++e) O[e] = fmaf(O[e], al, rec[4 + d0 + e] * wj);
+      for (int e = 0; e < DPT; ++e) ovv[j][e] = rec[4 + d0 + e];
+    }
+#pragma unroll
+    for (int j = 0; j < NWV; ++j) {
+      if (mv[j] == -INFINITY) continue;
+      const float mn = fmaxf(M, mv[j]);
+      const float al = __expf(M - mn), wj = __expf(mv[j] - mn);
+      L = fmaf(L, al, lv[j] * wj);
+#pragma unroll
+      for (int e = 0; e < DPT; ++e) O[e] = fmaf(O[e], al, ovv[j][e] * wj);
       M = mn;
     }
+    if (w.sub && threadIdx.x == 0) a.sub[(size_t)w.g * 16 + 2] = now();
     const gw<float> out = part_rec(a, h, t, u, nl);
     if (d0 == 0) {
       out[0] = M;
@@ -1012,7 +1042,7 @@ __device__ __forceinline__ bool att_prefix_unit(const FusedArgs& a, const Wg& w,
 #pragma unroll
     for (int e = 0; e < DPT; ++e) out[4 + d0 + e] = O[e];
   }
-  __syncthreads();
+  lds_barrier();  // LDS is reused by the next unit; the stores are waited for by unit_done
   return true;
 }
 
@@ -1038,6 +1068,7 @@ __device__ __forceinline__ bool att_root_unit(const FusedArgs& a, const Wg& w, c
   const int rdep = ld_x(depth + rnc);
   if (ws.on && !wait_flags(a, w, ws.id, ws.wx, ws.tag)) return false;
   stamp(a, w, ws.sl, ws.sfid, 1);
+  if (w.sub && ws.on && threadIdx.x == 0) a.sub[(size_t)w.g * 16 + 0] = now();
   const gptr<uint16_t> ktb = opq((const uint16_t*)a.kt + head_rows * a.max_nodes * DH);
   const gptr<uint16_t> vtb = opq((const uint16_t*)a.vt + head_rows * a.max_nodes * DH);
   u32x4 rk[DH / 8], rv[DH / 8];
@@ -1046,12 +1077,16 @@ __device__ __forceinline__ bool att_root_unit(const FusedArgs& a, const Wg& w, c
     rk[j] = ld_x((gptr<u32x4>)(ktb + (size_t)rkey * DH + 8 * j));
     rv[j] = ld_x((gptr<u32x4>)(vtb + (size_t)rkey * DH + 8 * j));
   }
-  uint16_t* rvl = (uint16_t*)lds + (2 * wv + hw) * 32 * DH;  // [32 keys][DH]
+  uint16_t* rvl = (uint16_t*)lds + (2 * wv + hw) * 32 * AKS;  // [32 keys][AKS]: padded, conflict-free
   float* qr = qrow + (wv * 2 + hw) * DH;
   {
     const gptr<float> qp = qbase + (size_t)rnc * d + h * DH + hl * DPL;
 #pragma unroll
     for (int e = 0; e < DPL; ++e) qr[hl * DPL + e] = ld_x(qp + e);
+  }
+  if (w.sub && threadIdx.x == 0) {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    a.sub[(size_t)w.g * 16 + 1] = now();
   }
   float rm = -INFINITY, rl = 0.f, ro[DPL];
 #pragma unroll
@@ -1068,34 +1103,36 @@ __device__ __forceinline__ bool att_root_unit(const FusedArgs& a, const Wg& w, c
       }
     }
 #pragma unroll
-    for (int jj = 0; jj < DH / 8; ++jj) *(u32x4*)(rvl + hl * DH + 8 * jj) = rv[jj];
+    for (int jj = 0; jj < DH / 8; ++jj) *(u32x4*)(rvl + hl * AKS + 8 * jj) = rv[jj];
     wave_sync_lds();
-    float dot = 0.f;
+    if (w.sub && threadIdx.x == 0 && bt == 0) a.sub[(size_t)w.g * 16 + 3] = now();
+    // four independent chains over the dims, combined in a fixed order
+    float dq[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int c8 = 0; c8 < DH / 8; ++c8) {
       const f32x4 qa = *(const f32x4*)&qr[8 * c8];
       const f32x4 qb = *(const f32x4*)&qr[8 * c8 + 4];
       const u32x4 ku = rk[c8];
-      dot = fmaf(qa[0], __uint_as_float(ku[0] << 16), dot);
-      dot = fmaf(qa[1], __uint_as_float(ku[0] & 0xffff0000u), dot);
-      dot = fmaf(qa[2], __uint_as_float(ku[1] << 16), dot);
-      dot = fmaf(qa[3], __uint_as_float(ku[1] & 0xffff0000u), dot);
-      dot = fmaf(qb[0], __uint_as_float(ku[2] << 16), dot);
-      dot = fmaf(qb[1], __uint_as_float(ku[2] & 0xffff0000u), dot);
-      dot = fmaf(qb[2], __uint_as_float(ku[3] << 16), dot);
-      dot = fmaf(qb[3], __uint_as_float(ku[3] & 0xffff0000u), dot);
+      float& d0 = dq[(2 * c8) & 3];
+      float& d1 = dq[(2 * c8 + 1) & 3];
+      d0 = fmaf(qa[0], __uint_as_float(ku[0] << 16), d0);
+      d0 = fmaf(qa[1], __uint_as_float(ku[0] & 0xffff0000u), d0);
+      d0 = fmaf(qa[2], __uint_as_float(ku[1] << 16), d0);
+      d0 = fmaf(qa[3], __uint_as_float(ku[1] & 0xffff0000u), d0);
+      d1 = fmaf(qb[0], __uint_as_float(ku[2] << 16), d1);
+      d1 = fmaf(qb[1], __uint_as_float(ku[2] & 0xffff0000u), d1);
+      d1 = fmaf(qb[2], __uint_as_float(ku[3] << 16), d1);
+      d1 = fmaf(qb[3], __uint_as_float(ku[3] & 0xffff0000u), d1);
     }
+    const float dot = (dq[0] + dq[1]) + (dq[2] + dq[3]);
     const bool kvalid = j <= rdep;
     const float sc = kvalid ? dot * scale : -INFINITY;
-    float mb = sc;
-#pragma unroll
-    for (int off = 1; off < 32; off <<= 1) mb = fmaxf(mb, __shfl_xor(mb, off));
+    const float mb = half_max(sc);
     const float mn = fmaxf(rm, mb);
     const float alpha = __expf(rm - mn);
     const float p = kvalid ? __expf(sc - mn) : 0.f;
-    float ps = p;
-#pragma unroll
-    for (int off = 1; off < 32; off <<= 1) ps += __shfl_xor(ps, off);
+    const float ps = half_sum(p);
+    if (w.sub && threadIdx.x == 0 && bt == 0) a.sub[(size_t)w.g * 16 + 4] = now();
     rl = fmaf(rl, alpha, ps);
     rm = mn;
     const int cnt = min(32, rdep + 1 - 32 * bt);
@@ -1105,7 +1142,7 @@ __device__ __forceinline__ bool att_root_unit(const FusedArgs& a, const Wg& w, c
     for (int e = 0; e < DPL; ++e) acc[e] = 0.f;
     for (int jj = 0; jj < cmax; ++jj) {
       const float pj = jj < cnt ? __shfl(p, (hw << 5) + jj) : 0.f;
-      const uint16_t* vr2 = rvl + jj * DH + DPL * hl;
+      const uint16_t* vr2 = rvl + jj * AKS + DPL * hl;
 #pragma unroll
       for (int e = 0; e < DPL; ++e) acc[e] = fmaf(pj, bf2f(vr2[e]), acc[e]);
     }
@@ -1113,6 +1150,7 @@ __device__ __forceinline__ bool att_root_unit(const FusedArgs& a, const Wg& w, c
     for (int e = 0; e < DPL; ++e) ro[e] = fmaf(ro[e], alpha, acc[e]);
     wave_sync_lds();
   }
+  if (w.sub && threadIdx.x == 0) a.sub[(size_t)w.g * 16 + 2] = now();
   const gw<float> out = part_rec(a, h, t, a.att_units, nl);
   if (hl == 0) {
     out[0] = rm;
@@ -1120,7 +1158,7 @@ __device__ __forceinline__ bool att_root_unit(const FusedArgs& a, const Wg& w, c
   }
 #pragma unroll
   for (int e = 0; e < DPL; ++e) out[4 + DPL * hl + e] = ro[e];
-  __syncthreads();
+  lds_barrier();  // LDS is reused by the next unit; the stores are waited for by unit_done
   return true;
 }
 
@@ -1134,30 +1172,6 @@ __device__ __forceinline__ bool att_root_unit(const FusedArgs& a, const Wg& w, c
 //   HEAD: first row block, end row block of the LM head
 
 // ------------------------------------------------------------------ compute workgroups
-
-// Loads a GEMM task's weight fragments into the XCD's L2 ahead of its stage:
-// waves 1.. of the workgroup take fragment rows in turn (wave 0, which polls
-// flags, issues none, so its polls never wait behind these loads).  The
-// values are folded into acc, which is stored only if it equals a magic word.
-__device__ __forceinline__ unsigned touch_task(const int* rbs, int nrb, gptr<u32x4> Wp, int KC, int kc0, int kc1,
-                                               unsigned acc) {
-  const int tid = opq_tid(), wv = tid >> 6, lane = tid & 63;
-  if (wv == 0) return acc;
-  Wp = opq(Wp);
-  const int nk = kc1 - kc0, tot = nrb * nk;
-  for (int f0 = wv - 1; f0 < tot; f0 += 4 * (NWV - 1)) {
-    u32x4 v[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int f = min(f0 + u * (NWV - 1), tot - 1);
-      const int r = f / nk, kc = kc0 + f - r * nk;
-      v[u] = Wp[((size_t)rbs[r] * KC + kc) * 64 + lane];
-    }
-#pragma unroll
-    for (int u = 0; u < 4; ++u) acc ^= v[u][0] ^ v[u][3];
-  }
-  return acc;
-}
 
 template <int NT>
 __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* lds) {
@@ -1226,19 +1240,28 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
     if (kind == 1 || kind == 3 || kind == 6 || kind == 9) continue;  // run with the stage before them, or none
     if (kind == 2) {
       // attention units of this XCD's heads, dealt to its ranks in turn
-      progress(a, w, l * kFStages + FS_ATT);
       stamp(a, w, l, FS_ATT, 0);
+      w.sub = a.sub && l == a.sub_l && a.sub_kind == 2;
+      if (w.sub && threadIdx.x == 0) a.sub[(size_t)w.g * 16 + 8] = now();
       const WaitSpec ws{FS_QKV, w.x, tag_of(w, l, FS_QKV), true, l, FS_ATT};
       const WaitSpec none{0, 0, 0u, false, l, FS_ATT};
-      for (int u = w.r; u < n_attu; u += kFRanks) {
+      // units go to the ranks in the plan's order (fewest QKV row blocks
+      // first: they are the first to be free)
+      const int apos = p[PL_ATT];
+      for (int u = apos; u < n_attu; u += kFRanks) {
         const int hloc = u / (NTl * (S + 1)), rem = u - hloc * (NTl * (S + 1));
         const int t = rem / (S + 1), part = rem - t * (S + 1);
         const int h = a.xh[2 * w.x] + hloc;
-        const WaitSpec& wsu = u == w.r ? ws : none;
+        const WaitSpec& wsu = u == apos ? ws : none;
         const bool ok = part < S ? att_prefix_unit(a, w, wsu, l, h, t, part, lds)
                                  : att_root_unit(a, w, wsu, l, h, t, lds);
         if (!ok) goto out;
+        if (w.sub && u == apos && threadIdx.x == 0) {
+          a.sub[(size_t)w.g * 16 + 13] = now();
+          a.sub[(size_t)w.g * 16 + 15] = part < S ? 1 : 2;
+        }
         unit_done(a, w, l, h, t, part);
+        if (w.sub && u == apos && threadIdx.x == 0) a.sub[(size_t)w.g * 16 + 14] = now();
       }
       signal(a, w, l, FS_ATT, false);
       stamp(a, w, l, FS_ATT, 2);
@@ -1250,7 +1273,6 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
       // leave partial residuals for every XCD's next LayerNorm
       const bool wo = kind == 4;
       const int fid = wo ? FS_WO : FS_WPR;
-      progress(a, w, l * kFStages + fid);
       stamp(a, w, l, fid, 0);
       w.sub = a.sub && l == a.sub_l && a.sub_kind == kind;
       if (w.sub && threadIdx.x == 0) a.sub[(size_t)w.g * 16 + 8] = now();
@@ -1291,7 +1313,6 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
       ps.b = kind == 8 ? G<uint16_t>(a.lnf_b) : G<uint16_t>(lw(a, l, LN1B));
       ps.act = act1;
     }
-    progress(a, w, l * kFStages + ps.fid);
     stamp(a, w, l, ps.fid, 0);
     int gfid, epi, nrb, Mo, k0 = 0, k1 = KCd, rb_first = 0;
     const int* rbs = nullptr;
@@ -1318,7 +1339,6 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
       const WaitSpec none{0, 0, 0u, false, l, gfid};
       PreSpec nopre{};
       for (int b0 = hb0 + 4, j = 1; b0 < hb1; b0 += 4, ++j) {
-        progress(a, w, L * kFStages + 1 + j / 2);
         if (!gemm_task<NT>(a, w, none, FE_HEAD, L, nullptr, b0, min(4, hb1 - b0), G<uint16_t>(nullptr),
                            G<u32x4>(a.p_head), KCd, a.V, 0, KCd, act1, KCd, red, nopre))
           goto out;
@@ -1331,7 +1351,6 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
   }
 out:
   __syncthreads();
-  progress(a, w, 0xffff);  // done
   if (threadIdx.x == 0) {
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     const unsigned prev = __hip_atomic_fetch_add(&a.ctl[FZ_DONE], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -1343,139 +1362,11 @@ out:
   }
 }
 
-// ------------------------------------------------------------------ prefetch workgroups
-//
-// Block 256 + b follows compute workgroup (its XCD, b / 8).  Before that
-// workgroup starts stage k it loads the weights of stage k + ahead (its row
-// blocks and k-ranges; the cached K/V of its attention heads) into the XCD's
-// L2.  Loads are folded into one value that is stored only if it equals a
-// magic word, so they are kept.  Stops when the compute workgroup reports
-// done, on abort, or after the timeout.
-
-struct Range {
-  const unsigned char* p;
-  size_t bytes;
-};
-
-__device__ __forceinline__ unsigned touch(const Range& rg, unsigned acc) {
-  typedef const __attribute__((address_space(1))) u32x4* gptr;
-  const gptr base = (gptr)rg.p;
-  const size_t n16 = rg.bytes / 16;
-  constexpr int D = 8;
-  for (size_t i0 = threadIdx.x; i0 < n16; i0 += (size_t)NTH * D) {
-    u32x4 v[D];
-#pragma unroll
-    for (int u = 0; u < D; ++u) v[u] = base[min(i0 + (size_t)u * NTH, n16 - 1)];
-#pragma unroll
-    for (int u = 0; u < D; ++u) acc ^= v[u][0] ^ v[u][3];
-  }
-  return acc;
-}
-
-template <int NT>
-__device__ __forceinline__ void prefetch_wg(const FusedArgs& a, unsigned char* lds) {
-  int* sh = (int*)(lds + A_REGION + A_PART_BYTES + A_Q_BYTES);
-  const int x = (int)xcc_id(), r = (blockIdx.x - kFGroups) >> 3;
-  if (x >= kFXcd || r >= kFRanks) return;
-  const int g = x * kFRanks + r;
-  const int* plan = a.plan + (size_t)g * kPlanStride;
-  const unsigned E = __hip_atomic_load(&a.ctl[FZ_PASS], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1u;
-  const unsigned long long t0 = now();
-  const int d = a.d, KCd = d / 32, KCm = a.M / 32;
-  const int kh0 = 2 * a.xh[2 * x], kh1 = 2 * a.xh[2 * x + 1];
-  const int kf0 = a.xf[2 * x], kf1 = a.xf[2 * x + 1];
-  unsigned acc = 0;
-  const int L = a.L;
-  constexpr int HRB = 8;  // the compute workgroup reports LM-head progress per 8 row blocks
-  const int hb0 = plan[PL_HEAD], hb1 = plan[PL_HEAD + 1];
-  const int nhead = (hb1 - hb0 + HRB - 1) / HRB;
-  const int nsteps = L * kFStages + 1 + nhead;
-  unsigned last = 0xffffffffu;
-  unsigned long long tl = now();
-  for (int step = 0; step < nsteps; ++step) {
-    const int l = step / kFStages, s = step % kFStages;
-    if (step < L * kFStages) {
-      if (s != FS_QKV && s != FS_ATT && s != FS_WO && s != FS_FC && s != FS_WPR) continue;
-    } else if (step == L * kFStages) {
-      continue;  // final LayerNorm: no weights
-    }
-    // wait until the compute workgroup has reached step - ahead in this pass
-    if (threadIdx.x == 0) {
-      int go = 0;
-      for (;;) {
-        const unsigned pv = __hip_atomic_load(&a.prog[g], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if ((pv >> 16) == (E & 0xffffu)) {
-          const int cur = (int)(pv & 0xffffu);
-          if (cur == 0xffff) break;  // done
-          if (cur + a.ahead >= step) {
-            go = 1;
-            break;
-          }
-        }
-        if (pv != last) {
-          last = pv;
-          tl = now();
-        }
-        if (__hip_atomic_load(&a.ctl[FZ_ABORT], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) break;
-        if (now() - tl > a.pf_idle || now() - t0 > a.timeout) break;  // prefetch is optional
-        __builtin_amdgcn_s_sleep(2);
-      }
-      sh[2] = go;
-    }
-    __syncthreads();
-    const int go = sh[2];
-    __syncthreads();
-    if (!go) break;
-    if (step < L * kFStages) {
-      if (s == FS_QKV) {
-        const int n = plan[PL_QKV];
-        for (int j = 0; j < n; ++j)
-          acc = touch(Range{(const unsigned char*)lw(a, l, LW_QKV) + (size_t)plan[PL_QKV + 1 + j] * KCd * 1024,
-                            (size_t)KCd * 1024},
-                      acc);
-      } else if (s == FS_ATT) {
-        const int n = plan[PL_ATT];
-        for (int j = 0; j < n; ++j) {
-          const int h = plan[PL_ATT + 1 + j] & 0xffff;
-          const size_t off = (((size_t)l * a.H + h) * a.max_ctx) * DH * 2;
-          acc = touch(Range{(const unsigned char*)a.kc + off, (size_t)a.P * DH * 2}, acc);
-          acc = touch(Range{(const unsigned char*)a.vc + off, (size_t)a.P * DH * 2}, acc);
-        }
-      } else if (s == FS_WO) {
-        const int n = plan[PL_WO];
-        for (int j = 0; j < n; ++j)
-          acc = touch(Range{(const unsigned char*)lw(a, l, LW_O) + ((size_t)plan[PL_WO + 1 + j] * KCd + kh0) * 1024,
-                            (size_t)(kh1 - kh0) * 1024},
-                      acc);
-      } else if (s == FS_FC) {
-        const int n = plan[PL_FC];
-        for (int j = 0; j < n; ++j)
-          acc = touch(Range{(const unsigned char*)lw(a, l, LW_FC) + (size_t)plan[PL_FC + 1 + j] * KCd * 1024,
-                            (size_t)KCd * 1024},
-                      acc);
-      } else {
-        const int n = plan[PL_WPR];
-        for (int j = 0; j < n; ++j)
-          acc = touch(Range{(const unsigned char*)lw(a, l, LW_PR) + ((size_t)plan[PL_WPR + 1 + j] * KCm + kf0) * 1024,
-                            (size_t)(kf1 - kf0) * 1024},
-                      acc);
-      }
-    } else {
-      // LM head, in the compute workgroup's task groups
-      const int b0 = hb0 + (step - L * kFStages - 1) * HRB;
-      acc = touch(Range{(const unsigned char*)a.p_head + (size_t)b0 * KCd * 1024,
-                        (size_t)min(HRB, hb1 - b0) * KCd * 1024},
-                  acc);
-    }
-  }
-  if (acc == a.magic) *a.sink = acc;
-}
 
 template <int NT>
 __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(2))) void pass_kernel(FusedArgs a) {
   extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
-  if ((int)blockIdx.x < kFGroups) compute_wg<NT>(a, lds);
-  else prefetch_wg<NT>(a, lds);
+  compute_wg<NT>(a, lds);
 }
 
 }  // namespace fz
@@ -1535,12 +1426,8 @@ bool fused_plan(int H, int d, int M, int V, int ntiles, int* tab, int* xh, int* 
   }
   std::fill(tab, tab + (size_t)kFGroups * kPlanStride, 0);
   const int RBd = d / 16;
-  const double pnom = 512.0;  // nominal prefix rows for an attention unit's cost
   for (int x = 0; x < kFXcd; ++x) {
-    std::vector<double> ld(kFRanks, 0.0);
-    std::vector<int> unitsA, unitsQ, unitsO, unitsF, unitsP;
-    for (int h = xh[2 * x]; h < xh[2 * x + 1]; ++h)
-      for (int t = 0; t < ntiles; ++t) unitsA.push_back(h | (t << 16));
+    std::vector<int> unitsQ, unitsO, unitsF, unitsP;
     for (int part = 0; part < 3; ++part)
       for (int h = xh[2 * x]; h < xh[2 * x + 1]; ++h)
         for (int j = 0; j < DHh / 16; ++j) unitsQ.push_back(part * RBd + h * (DHh / 16) + j);
@@ -1549,33 +1436,49 @@ bool fused_plan(int H, int d, int M, int V, int ntiles, int* tab, int* xh, int* 
     for (int rb = 2 * xf[2 * x]; rb < 2 * xf[2 * x + 1]; ++rb) unitsF.push_back(rb);
     if (fx[x] > 0)
       for (int rb = 0; rb < RBd; ++rb) unitsP.push_back(rb);
-    struct St {
-      std::vector<int>* u;
-      int slot, maxn;
-      double cost;
-    } st[5] = {{&unitsA, PL_ATT, kPlanMaxAtt, pnom * 256.0},
-               {&unitsQ, PL_QKV, kPlanMaxRb, 32.0 * d},
-               {&unitsO, PL_WO, kPlanMaxRb, 16.0 * 64 * hx[x] * 2},
-               {&unitsF, PL_FC, kPlanMaxRb, 32.0 * d},
-               {&unitsP, PL_WPR, kPlanMaxRb, 16.0 * 32 * fx[x] * 2}};
-    for (const St& S : st) {
-      const int U = (int)S.u->size(), base = U / kFRanks, extra = U % kFRanks;
+    // Ranks finishing a stage early start the next one early, so each
+    // stage's extra units go to the ranks with the least work in the stage
+    // before it (stable: lower ranks first among equals).
+    std::vector<double> prev(kFRanks, 0.0);
+    auto order_by_prev = [&]() {
       std::vector<int> order(kFRanks);
       for (int r = 0; r < kFRanks; ++r) order[r] = r;
-      std::stable_sort(order.begin(), order.end(), [&](int p, int q) { return ld[p] < ld[q]; });
+      std::stable_sort(order.begin(), order.end(), [&](int p, int q) { return prev[p] < prev[q]; });
+      return order;
+    };
+    auto deal = [&](const std::vector<int>& u, int slot, double cost) {
+      const int U = (int)u.size(), base = U / kFRanks, extra = U % kFRanks;
+      const std::vector<int> order = order_by_prev();
       std::vector<int> cnt(kFRanks, base);
       for (int k = 0; k < extra; ++k) cnt[order[k]]++;
       int next = 0;
       for (int r = 0; r < kFRanks; ++r) {
-        if (cnt[r] > S.maxn) {
-          *why = "fused pass: a rank would get more than the plan's units per stage";
-          return false;
-        }
+        if (cnt[r] > kPlanMaxRb) return false;
         int* row = tab + (size_t)(x * kFRanks + r) * kPlanStride;
-        row[S.slot] = cnt[r];
-        for (int k = 0; k < cnt[r]; ++k) row[S.slot + 1 + k] = (*S.u)[next++];
-        ld[r] += cnt[r] * S.cost;
+        row[slot] = cnt[r];
+        for (int k = 0; k < cnt[r]; ++k) row[slot + 1 + k] = u[next++];
+        prev[r] = cnt[r] * cost;
       }
+      return true;
+    };
+    bool ok = deal(unitsQ, PL_QKV, 32.0 * d);
+    // attention: units u = pos, pos + 32, ... go to the rank at position pos
+    // of this order (its cost taken at a nominal 512-row prefix: 3 units per
+    // head and tile)
+    const std::vector<int> aorder = order_by_prev();
+    const int n_att = 3 * hx[x] * ntiles;
+    for (int pos = 0; pos < kFRanks; ++pos) {
+      const int r = aorder[pos];
+      tab[(size_t)(x * kFRanks + r) * kPlanStride + PL_ATT] = pos;
+      prev[r] = (double)((n_att - pos + kFRanks - 1) / kFRanks) * 256.0 * 256.0;
+    }
+    ok = ok && deal(unitsO, PL_WO, 16.0 * 64 * hx[x] * 2);
+    std::fill(prev.begin(), prev.end(), 0.0);  // LN2: one node row per rank, evenly
+    ok = ok && deal(unitsF, PL_FC, 32.0 * d);
+    ok = ok && deal(unitsP, PL_WPR, 16.0 * 32 * fx[x] * 2);
+    if (!ok) {
+      *why = "fused pass: a rank would get more than the plan's units per stage";
+      return false;
     }
   }
   const int RBV = (V + 15) / 16;
@@ -1603,7 +1506,7 @@ hipError_t launch_fused(const FusedArgs& a, hipStream_t s) {
   if (a.N <= 0 || a.N > kFMaxN || a.d % 32 || a.M % 32 || a.d > 2048 || a.H * fz::DH != a.d) return hipErrorInvalidValue;
   const int nt = (a.N + 15) / 16;
   const size_t lds = fused_lds_bytes();
-  const dim3 grid(a.prefetch ? 2 * kFGroups : kFGroups);
+  const dim3 grid(kFGroups);
   switch (nt) {
     case 1: fz::pass_kernel<1><<<grid, fz::NTH, lds, s>>>(a); break;
     case 2: fz::pass_kernel<2><<<grid, fz::NTH, lds, s>>>(a); break;

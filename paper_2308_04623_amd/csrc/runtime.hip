@@ -26,7 +26,6 @@ thread_local std::string g_last_error;
 int g_gemm_path = 0;  // 0 auto, 1 vector ALU, 2 matrix cores
 int g_prefetch = 1;   // warm each weight GEMM's L2 from the kernel before it
 int g_pass_mode = 0;  // 0 auto, 1 one kernel per sub-layer, 2 the persistent single-launch pass only
-int g_fz_ahead = 1;   // stages the persistent pass's prefetchers run ahead
 int g_fz_poll_sleep = [] {
   const char* e = getenv("SSD_FZ_POLL_SLEEP");
   return e ? atoi(e) : 0;
@@ -171,12 +170,6 @@ extern "C" ssd_status ssd_set_weight_prefetch(int32_t on) {
 extern "C" ssd_status ssd_set_pass_mode(int32_t mode) {
   if (mode < 0 || mode > 2) return fail(SSD_E_INVALID_ARG, "pass mode must be 0, 1 or 2");
   g_pass_mode = mode;
-  return SSD_OK;
-}
-
-extern "C" ssd_status ssd_set_fused_ahead(int32_t stages) {
-  if (stages < 0 || stages > 8) return fail(SSD_E_INVALID_ARG, "prefetch distance must be 0..8 stages");
-  g_fz_ahead = stages;
   return SSD_OK;
 }
 
@@ -415,7 +408,7 @@ static ssd_status fused_setup(ssd_kv* kv) {
   const size_t o_ap = take((size_t)c.n_head * 4 * att_parts * 16 * 68 * 4);
   const size_t o_po = take((size_t)kFXcd * kFMaxN * d * 4), o_pp = take((size_t)kFXcd * kFMaxN * d * 4);
   const size_t o_fl = take((size_t)kFStages * kFGroups * 4), o_ctl = take((size_t)kFCtlWords * 4);
-  const size_t o_prog = take((size_t)kFGroups * 4), o_plan = take(tabs.size() * 4), o_sink = take(4);
+  const size_t o_plan = take(tabs.size() * 4);
   const size_t o_sub = take((size_t)kFGroups * 16 * 8);
   const size_t o_uf = take((size_t)c.n_head * 4 * att_parts * 4);
   static const hipError_t prep = fused_prepare();
@@ -436,16 +429,12 @@ static ssd_status fused_setup(ssd_kv* kv) {
   a.part_p = (float*)(b + o_pp);
   a.flags = (unsigned*)(b + o_fl);
   a.ctl = (unsigned*)(b + o_ctl);
-  a.prog = (unsigned*)(b + o_prog);
-  a.sink = (unsigned*)(b + o_sink);
   kv->fz_sub = (unsigned long long*)(b + o_sub);
   a.uflag = (unsigned*)(b + o_uf);
   a.uf_stride = (int)att_parts;
   for (int nt = 1; nt <= 4; ++nt) kv->fz_plan[nt] = (int*)(b + o_plan) + (size_t)(nt - 1) * kFGroups * kPlanStride;
   a.err = kv->d_err;
   a.timeout = 20000000ull;  // 200 ms
-  a.pf_idle = 100000ull;    // 1 ms
-  a.magic = 0x5bd1e995u;
   kv->fz_ok = true;
   return SSD_OK;
 }
@@ -758,9 +747,7 @@ static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int3
     a.logits = logits;
     a.plan = kv->fz_plan[(n + 15) / 16];
     a.att_units = (P + kFAttRows - 1) / kFAttRows;
-    a.ahead = g_fz_ahead;
     a.poll_sleep = g_fz_poll_sleep;
-    a.prefetch = getenv("SSD_FZ_PF") ? atoi(getenv("SSD_FZ_PF")) : 0;
     a.sub = kv->fz.trace ? kv->fz_sub : nullptr;
     if (a.sub) HIP_TRY(hipMemsetAsync(a.sub, 0, (size_t)kFGroups * 16 * 8, s));
     a.sub_l = 10;

@@ -188,9 +188,11 @@ enum FStage { FS_LN1 = 0, FS_QKV, FS_ATT, FS_WO, FS_LN2, FS_FC, FS_WPR, FS_AMG, 
 constexpr unsigned kFTagsPerPass = (unsigned)kFStages * (kFMaxL + 1);
 constexpr int kFAttRows = 256;  // cache rows per attention unit (32 per wave of 8)
 constexpr int kLwSlots = 12;  // per-layer parameter pointers (see LwSlot in fused.hip)
-// plan row of one compute workgroup (int32): counts then entries
+// plan row of one compute workgroup (int32): the rank's position in the
+// order attention units are dealt in; per weight GEMM a count then row blocks;
+// the LM-head row-block range
 enum PlanSlot { PL_ATT = 0, PL_QKV = 9, PL_WO = 14, PL_FC = 19, PL_WPR = 24, PL_HEAD = 29, kPlanStride = 32 };
-constexpr int kPlanMaxAtt = 8, kPlanMaxRb = 4;
+constexpr int kPlanMaxRb = 4;
 // control words: pass counter, finished workgroups, abort flag, abort reason, claims [kFGroups]
 enum { FZ_PASS = 0, FZ_DONE = 1, FZ_ABORT = 2, FZ_WHY = 3, FZ_CLAIM = 16, kFCtlWords = FZ_CLAIM + kFGroups };
 
@@ -222,19 +224,13 @@ struct FusedArgs {
   float *part_o, *part_p;   // partial residuals [kFXcd][kFMaxN][d]
   unsigned* flags;          // [kFStages][kFGroups]
   unsigned* ctl;            // [kFCtlWords]
-  unsigned* prog;           // [kFGroups] progress of each compute workgroup (for its prefetcher)
   const int* plan;          // [kFGroups][kPlanStride]
   int xh[2 * kFXcd];        // heads [xh[2x], xh[2x+1]) of XCD x
   int xf[2 * kFXcd];        // hidden k-steps [xf[2x], xf[2x+1]) of XCD x
   unsigned* err;            // session error counter
   unsigned long long timeout;  // s_memrealtime ticks (100 MHz) before a wait gives up
-  unsigned long long pf_idle;  // ticks a prefetcher waits without progress before it stops
-  int ahead;                // stages the prefetchers run ahead
   int poll_sleep;           // extra back-off between flag polls (units of s_sleep 8)
-  unsigned magic;
-  unsigned* sink;
   unsigned long long* trace;  // stage timestamps [kFGroups][L + 1][kFStages][3], or nullptr
-  int prefetch;               // also launch the L2 prefetch workgroups
   unsigned long long* sub;   // (measurement) sub-stage timestamps [kFGroups][16] of one stage, or nullptr
   int sub_l, sub_kind, sub_epi;
 };

@@ -28,7 +28,7 @@ LAYER_TENSORS = ("ln1_g", "ln1_b", "w_qkv", "b_qkv", "w_o", "b_o",
 EXPORTS = ("ssd_model_create", "ssd_model_destroy", "ssd_kv_bytes", "ssd_kv_create", "ssd_kv_destroy",
            "ssd_tree_verify", "ssd_tree_accept", "ssd_kv_commit", "ssd_kv_error_count",
            "ssd_graph_capture_verify", "ssd_graph_launch", "ssd_graph_destroy", "ssd_validate_tree",
-           "ssd_tree_prep", "ssd_set_gemm_path", "ssd_set_weight_prefetch", "ssd_set_pass_mode", "ssd_verify_path", "ssd_set_fused_ahead", "ssd_fused_plan", "ssd_kv_set_trace", "ssd_status_string", "ssd_last_error", "ssd_launch_gemm",
+           "ssd_tree_prep", "ssd_set_gemm_path", "ssd_set_weight_prefetch", "ssd_set_pass_mode", "ssd_verify_path", "ssd_fused_plan", "ssd_kv_set_trace", "ssd_status_string", "ssd_last_error", "ssd_launch_gemm",
            "ssd_model_prefix_view", "ssd_topk")
 
 
@@ -90,7 +90,6 @@ def lib():
             "ssd_set_weight_prefetch": [C.c_int32],
             "ssd_set_pass_mode": [C.c_int32],
             "ssd_verify_path": [vp, vp, C.c_int32, C.POINTER(C.c_int32)],
-            "ssd_set_fused_ahead": [C.c_int32],
             "ssd_fused_plan": [C.c_int32] * 5 + [vp, vp, vp],
             "ssd_kv_set_trace": [vp, vp],
             "ssd_launch_gemm": [vp, vp, C.c_int32, C.c_int32, C.c_int32, vp],
@@ -168,10 +167,6 @@ def fused_plan(n_head: int, d_model: int, d_mlp: int, vocab: int, n_tiles: int):
     _check(lib().ssd_fused_plan(n_head, d_model, d_mlp, vocab, n_tiles, tab.ctypes.data, xh.ctypes.data,
                                 xf.ctypes.data), "ssd_fused_plan")
     return tab, xh, xf
-
-
-def set_fused_ahead(stages: int):
-    _check(lib().ssd_set_fused_ahead(stages), "ssd_set_fused_ahead")
 
 
 def kv_bytes(cfg, max_ctx: int, max_nodes: int) -> Tuple[int, int]:

@@ -88,9 +88,10 @@ SHAPES = [(20, 1280, 5120, 50257), (4, 256, 1024, 2000), (12, 768, 3072, 50257),
 @pytest.mark.parametrize("nt", [1, 2, 3, 4])
 def test_fused_plan_covers_every_unit_once(H, d, M, V, nt):
     """Every weight row block of every stage is computed by exactly one
-    workgroup of the XCD that owns it, every (head, tile) attention unit once,
-    and every LM-head row block once; XCD ranges tile the heads and hidden
-    features."""
+    workgroup of the XCD that owns it, and every LM-head row block once; XCD
+    ranges tile the heads and hidden features.  The attention order is a
+    permutation of the 32 ranks of an XCD that puts ranks with fewer QKV row
+    blocks first; WPR's extra row blocks go to ranks with fewer FC ones."""
     tab, xh, xf = ssd.fused_plan(H, d, M, V, nt)
     assert xh[0] == 0 and xh[15] == H and xf[0] == 0 and xf[15] == M // 32
     assert all(xh[2 * x + 1] == xh[2 * x + 2] and xf[2 * x + 1] == xf[2 * x + 2] for x in range(7))
@@ -107,13 +108,19 @@ def test_fused_plan_covers_every_unit_once(H, d, M, V, nt):
                 out += list(r[slot + 1:slot + 1 + r[slot]])
             return sorted(out)
 
-        assert units(0, 8) == sorted(h | (t << 16) for h in heads for t in range(nt))
+        pos = rows[:, 0]
+        assert sorted(pos.tolist()) == list(range(32))
+        by_pos = rows[np.argsort(pos)]
+        assert all(by_pos[i, 9] <= by_pos[i + 1, 9] for i in range(31))
+        if rows[:, 24].max() > rows[:, 24].min() and rows[:, 19].max() > rows[:, 19].min():
+            extra_p = rows[:, 24] == rows[:, 24].max()
+            assert rows[extra_p, 19].max() <= rows[~extra_p, 19].min()
         assert units(9, 4) == sorted(p * rbd + 4 * h + j for p in range(3) for h in heads for j in range(4))
         assert units(14, 4) == (list(range(rbd)) if len(heads) else [])
         assert units(19, 4) == list(range(2 * xf[2 * x], 2 * xf[2 * x + 1]))
         assert units(24, 4) == (list(range(rbd)) if xf[2 * x + 1] > xf[2 * x] else [])
         # each stage split into floor/ceil shares over the 32 ranks
-        for slot in (0, 9, 14, 19, 24):
+        for slot in (9, 14, 19, 24):
             c = rows[:, slot]
             assert c.max() - c.min() <= 1
     head = sorted((int(r[29]), int(r[30])) for r in tab)
