@@ -198,6 +198,8 @@ struct Wg {
   unsigned tagbase;  // E * tags per pass
   int* sh;           // LDS words shared by the workgroup
   int sub;           // (measurement) the current stage is the one sub-stamped
+  const int* plan;   // this workgroup's plan row, copied to LDS
+  const unsigned long long* lwt;  // the per-layer parameter pointers, copied to LDS
 };
 
 // the dependency of a stage: flags of stage id on XCD wx (-1: all XCDs) at
@@ -336,8 +338,10 @@ __device__ __forceinline__ void sub_stamp(const FusedArgs& a, const Wg& w, int l
 enum LwSlot { LW_QKV = 0, LW_O, LW_FC, LW_PR, LB_QKV, LB_O, LB_FC, LB_PR, LN1G, LN1B, LN2G, LN2B };
 
 
-__device__ __forceinline__ const void* lw(const FusedArgs& a, int l, int slot) {
-  return ((gptr<const void*>)a.lw)[l * kLwSlots + slot];
+// (read from the workgroup's LDS copy: an LDS read never holds up the wave's
+// flag polls, which a global load issued before them would)
+__device__ __forceinline__ const void* lw(const Wg& w, int l, int slot) {
+  return (const void*)((const __attribute__((address_space(3))) unsigned long long*)w.lwt)[l * kLwSlots + slot];
 }
 
 // ------------------------------------------------------------------ LayerNorm of one node row
@@ -699,7 +703,7 @@ __device__ __forceinline__ bool gemm_rb(const FusedArgs& a, const Wg& w, const W
 #pragma unroll
   for (int r = 0; r < RB; ++r) {
     const int rr = min(r, nrb - 1);
-    rbv[r] = rbs ? rbs[rr] : rb_first + rr;
+    rbv[r] = rbs ? ((const __attribute__((address_space(3))) int*)rbs)[rr] : rb_first + rr;  // (LDS copy)
   }
   // this thread's epilogue row of every row block is tid % 16: its bias is
   // loaded before the k-loop
@@ -709,8 +713,6 @@ __device__ __forceinline__ bool gemm_rb(const FusedArgs& a, const Wg& w, const W
   const bool has_bias = bias != nullptr;
   const gptr<uint16_t> bsrc = has_bias ? bias : (gptr<uint16_t>)Wp;
   uint16_t bias_r[RB];
-#pragma unroll
-  for (int r = 0; r < RB; ++r) bias_r[r] = bsrc[rbv[r] * 16 + (tid & 15)];
   gptr<u32x4> wb[RB];
 #pragma unroll
   for (int r = 0; r < RB; ++r) wb[r] = Wp + (size_t)rbv[r] * KC * 64 + lane;
@@ -761,6 +763,9 @@ __device__ __forceinline__ bool gemm_rb(const FusedArgs& a, const Wg& w, const W
   if (wv > 0) asm volatile("buffer_inv sc0" ::: "memory");
   stamp(a, w, ws.sl, ws.sfid, 1);
   if (w.sub && threadIdx.x == 0) a.sub[(size_t)w.g * 16 + 0] = now();
+  // the bias is loaded only now, so that nothing sits ahead of wave 0's polls
+#pragma unroll
+  for (int r = 0; r < RB; ++r) bias_r[r] = bsrc[rbv[r] * 16 + (tid & 15)];
   const bool sub = epi == a.sub_epi;
   if (sub) sub_stamp(a, w, l, 0);
   if (w.sub && wv == QW) {
@@ -1176,6 +1181,8 @@ __device__ __forceinline__ bool att_root_unit(const FusedArgs& a, const Wg& w, c
 template <int NT>
 __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* lds) {
   int* sh = (int*)(lds + A_REGION + A_PART_BYTES + A_Q_BYTES);  // 16 words
+  int* lplan = sh + 16;                                            // [kPlanStride]
+  unsigned long long* llw = (unsigned long long*)(lplan + kPlanStride);  // [L][kLwSlots]
   float* red = (float*)lds;                                        // GEMM / LN reductions
   Wg w;
   w.sub = 0;
@@ -1183,6 +1190,13 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
   w.r = blockIdx.x >> 3;
   w.g = w.x * kFRanks + w.r;
   w.sh = sh;
+  w.plan = lplan;
+  w.lwt = llw;
+  {
+    const int g = w.x * kFRanks + w.r;
+    if (threadIdx.x < kPlanStride && w.x < kFXcd) lplan[threadIdx.x] = a.plan[(size_t)g * kPlanStride + threadIdx.x];
+    for (int i = threadIdx.x; i < a.L * kLwSlots; i += NTH) llw[i] = (unsigned long long)a.lw[i];
+  }
   if (threadIdx.x == 0) {
     const unsigned E = __hip_atomic_load(&a.ctl[FZ_PASS], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1u;
     sh[1] = (int)E;
@@ -1211,7 +1225,7 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
     return;
   }
 
-  const int* p = a.plan + (size_t)w.g * kPlanStride;
+  const int* p = w.plan;
   const int n_qkv = p[PL_QKV], n_wo = p[PL_WO], n_fc = p[PL_FC], n_wpr = p[PL_WPR];
   const int hb0 = p[PL_HEAD], hb1 = p[PL_HEAD + 1];
   const int d = a.d, M = a.M, KCd = d / 32, KCm = M / 32;
@@ -1279,9 +1293,9 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
       const WaitSpec ws{wo ? FS_ATT : FS_FC, w.x, tag_of(w, l, wo ? FS_ATT : FS_FC), true, l, fid};
       PreSpec nopre{};
       const bool ok = wo ? gemm_task<NT>(a, w, ws, FE_WO, l, p + PL_WO + 1, 0, n_wo, G<uint16_t>(nullptr),
-                                         G<u32x4>(lw(a, l, LW_O)), KCd, d, kh0, kh1, a.fo, KCd, red, nopre)
+                                         G<u32x4>(lw(w, l, LW_O)), KCd, d, kh0, kh1, a.fo, KCd, red, nopre)
                          : gemm_task<NT>(a, w, ws, FE_WPR, l, p + PL_WPR + 1, 0, n_wpr, G<uint16_t>(nullptr),
-                                         G<u32x4>(lw(a, l, LW_PR)), KCm, d, kf0, kf1, a.ff, KCm, red, nopre);
+                                         G<u32x4>(lw(w, l, LW_PR)), KCm, d, kf0, kf1, a.ff, KCm, red, nopre);
       if (!ok) goto out;
       signal(a, w, l, fid, true);
       stamp(a, w, l, fid, 2);
@@ -1297,20 +1311,20 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
     ps.mode = (kind == 0 && l == 0) ? 0 : 1;
     if (kind == 5) {
       ps.ws = WaitSpec{FS_WO, -1, tag_of(w, l, FS_WO), true, l, FS_LN2};
-      ps.bias = G<uint16_t>(lw(a, l, LB_O));
+      ps.bias = G<uint16_t>(lw(w, l, LB_O));
       ps.part = a.part_o;
       ps.own = own_h;
-      ps.g = G<uint16_t>(lw(a, l, LN2G));
-      ps.b = G<uint16_t>(lw(a, l, LN2B));
+      ps.g = G<uint16_t>(lw(w, l, LN2G));
+      ps.b = G<uint16_t>(lw(w, l, LN2B));
       ps.act = act2;
     } else {
       const int lp = kind == 8 ? L - 1 : max(l - 1, 0);
       ps.ws = WaitSpec{FS_WPR, -1, tag_of(w, lp, FS_WPR), kind == 8 || l > 0, l, FS_LN1};
-      ps.bias = G<uint16_t>(lw(a, lp, LB_PR));
+      ps.bias = G<uint16_t>(lw(w, lp, LB_PR));
       ps.part = a.part_p;
       ps.own = own_f;
-      ps.g = kind == 8 ? G<uint16_t>(a.lnf_g) : G<uint16_t>(lw(a, l, LN1G));
-      ps.b = kind == 8 ? G<uint16_t>(a.lnf_b) : G<uint16_t>(lw(a, l, LN1B));
+      ps.g = kind == 8 ? G<uint16_t>(a.lnf_g) : G<uint16_t>(lw(w, l, LN1G));
+      ps.b = kind == 8 ? G<uint16_t>(a.lnf_b) : G<uint16_t>(lw(w, l, LN1B));
       ps.act = act1;
     }
     stamp(a, w, l, ps.fid, 0);
@@ -1320,10 +1334,10 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
     gptr<u32x4> Wm;
     const uint16_t* act = act1;
     switch (kind) {
-      case 0: gfid = FS_QKV; epi = FE_QKV; nrb = n_qkv; rbs = p + PL_QKV + 1; Wm = G<u32x4>(lw(a, l, LW_QKV));
-              Mo = 3 * d; bias = G<uint16_t>(lw(a, l, LB_QKV)); break;
-      case 5: gfid = FS_FC; epi = FE_FC; nrb = n_fc; rbs = p + PL_FC + 1; Wm = G<u32x4>(lw(a, l, LW_FC)); Mo = M;
-              bias = G<uint16_t>(lw(a, l, LB_FC)); act = act2; break;
+      case 0: gfid = FS_QKV; epi = FE_QKV; nrb = n_qkv; rbs = p + PL_QKV + 1; Wm = G<u32x4>(lw(w, l, LW_QKV));
+              Mo = 3 * d; bias = G<uint16_t>(lw(w, l, LB_QKV)); break;
+      case 5: gfid = FS_FC; epi = FE_FC; nrb = n_fc; rbs = p + PL_FC + 1; Wm = G<u32x4>(lw(w, l, LW_FC)); Mo = M;
+              bias = G<uint16_t>(lw(w, l, LB_FC)); act = act2; break;
       default: gfid = FS_QKV; epi = FE_HEAD; nrb = min(4, hb1 - hb0); rb_first = hb0; Wm = G<u32x4>(a.p_head);
                Mo = a.V; break;
     }
@@ -1500,7 +1514,9 @@ hipError_t fused_prepare() {
   return e;
 }
 
-size_t fused_lds_bytes() { return fz::A_REGION + fz::A_PART_BYTES + fz::A_Q_BYTES + 64; }
+size_t fused_lds_bytes() {
+  return fz::A_REGION + fz::A_PART_BYTES + fz::A_Q_BYTES + 64 + kPlanStride * 4 + (size_t)kFMaxL * kLwSlots * 8;
+}
 
 hipError_t launch_fused(const FusedArgs& a, hipStream_t s) {
   if (a.N <= 0 || a.N > kFMaxN || a.d % 32 || a.M % 32 || a.d > 2048 || a.H * fz::DH != a.d) return hipErrorInvalidValue;
