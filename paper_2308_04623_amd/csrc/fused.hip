@@ -197,7 +197,6 @@ struct Wg {
   unsigned E;        // this pass's number
   unsigned tagbase;  // E * tags per pass
   int* sh;           // LDS words shared by the workgroup
-  int sub;           // (measurement) the current stage is the one sub-stamped
   const int* plan;   // this workgroup's plan row, copied to LDS
   const unsigned long long* lwt;  // the per-layer parameter pointers, copied to LDS
 };
@@ -269,7 +268,6 @@ __device__ __forceinline__ bool poll_w0(const FusedArgs& a, const Wg& w, int s, 
     } else {
       mine = lane >= kFRanks || tag_reached(ld_flag(f + xs * kFRanks + lane), tag);
     }
-    if (w.sub && lane == 0 && a.sub[(size_t)w.g * 16 + 6] == 0) a.sub[(size_t)w.g * 16 + 6] = now();
     if (__all(mine)) {
       ok = true;
       break;
@@ -279,7 +277,6 @@ __device__ __forceinline__ bool poll_w0(const FusedArgs& a, const Wg& w, int s, 
       if (lane == 0) raise_abort(a, 0x100u + (unsigned)s);
       break;
     }
-    for (int z = 0; z < a.poll_sleep; ++z) __builtin_amdgcn_s_sleep(8);
     __builtin_amdgcn_s_sleep(1);
   }
   if (ok) asm volatile("buffer_inv sc0" ::: "memory");
@@ -326,11 +323,6 @@ __device__ __forceinline__ void signal_w0(const FusedArgs& a, const Wg& w, int l
 __device__ __forceinline__ void stamp(const FusedArgs& a, const Wg& w, int l, int s, int k) {
   if (a.trace && threadIdx.x == 0)
     a.trace[(((size_t)w.g * (a.L + 1) + l) * kFStages + s) * 3 + k] = now();
-}
-
-// (measurement) sub-stage timestamps of one stage of one layer, when a.sub is set
-__device__ __forceinline__ void sub_stamp(const FusedArgs& a, const Wg& w, int l, int k) {
-  if (a.sub && l == a.sub_l && threadIdx.x == 0) a.sub[(size_t)w.g * 16 + k] = now();
 }
 
 // ------------------------------------------------------------------ per-layer parameters
@@ -429,7 +421,6 @@ __device__ __forceinline__ bool ln_row_q(const FusedArgs& a, const Wg& w, const 
     if (w.sh[5] == 0) return false;
     if (wv > 0) asm volatile("buffer_inv sc0" ::: "memory");
     stamp(a, w, ws.sl, ws.sfid, 1);
-    if (w.sub && threadIdx.x == 0) a.sub[(size_t)w.g * 16 + 9] = now();
   }
   const gw<f32x4> xr = (gw<f32x4>)opq(a.xr + ((size_t)w.x * kFMaxN + n) * d);
   const gptr<u32x2> g4 = (gptr<u32x2>)opq(g), b4 = (gptr<u32x2>)opq(b);
@@ -498,7 +489,6 @@ __device__ __forceinline__ bool ln_row_q(const FusedArgs& a, const Wg& w, const 
       }
       v[i] = xv[i] + acc;
     }
-    if (w.sub && threadIdx.x == 0) a.sub[(size_t)w.g * 16 + 10] = now();
   }
   float s = 0.f;
 #pragma unroll
@@ -533,7 +523,6 @@ __device__ __forceinline__ bool ln_row_q(const FusedArgs& a, const Wg& w, const 
       st_act4(actg, n, 4 * c, d / 32, y[0], y[1], y[2], y[3]);
     }
   }
-  if (w.sub && threadIdx.x == 0) a.sub[(size_t)w.g * 16 + 11] = now();
   return true;
 }
 
@@ -642,7 +631,6 @@ __device__ __forceinline__ bool do_pre(const FusedArgs& a, const Wg& w, const Pr
   if (threadIdx.x == 0)
     __hip_atomic_store(a.flags + (size_t)ps.fid * kFGroups + w.g, tag_of(w, ps.l, ps.fid), __ATOMIC_RELAXED,
                        __HIP_MEMORY_SCOPE_WORKGROUP);
-  if (w.sub && threadIdx.x == 0) a.sub[(size_t)w.g * 16 + 12] = now();
   stamp(a, w, ps.l, ps.fid, 2);
   return true;
 }
@@ -762,16 +750,9 @@ __device__ __forceinline__ bool gemm_rb(const FusedArgs& a, const Wg& w, const W
   lds_barrier();
   if (wv > 0) asm volatile("buffer_inv sc0" ::: "memory");
   stamp(a, w, ws.sl, ws.sfid, 1);
-  if (w.sub && threadIdx.x == 0) a.sub[(size_t)w.g * 16 + 0] = now();
   // the bias is loaded only now, so that nothing sits ahead of wave 0's polls
 #pragma unroll
   for (int r = 0; r < RB; ++r) bias_r[r] = bsrc[rbv[r] * 16 + (tid & 15)];
-  const bool sub = epi == a.sub_epi;
-  if (sub) sub_stamp(a, w, l, 0);
-  if (w.sub && wv == QW) {
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    if (lane == 0) a.sub[(size_t)w.g * 16 + 7] = now();
-  }
 #pragma unroll
   for (int u = 0; u < U; ++u)
     if (u < nsteps) load_a(u, u);
@@ -793,10 +774,6 @@ __device__ __forceinline__ bool gemm_rb(const FusedArgs& a, const Wg& w, const W
     }
   }
   const int N = a.N;
-  if (sub) {
-    if (threadIdx.x == 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    sub_stamp(a, w, l, 1);
-  }
 #pragma unroll
   for (int r = 0; r < RB; ++r) {
     if (r >= nrb) break;
@@ -820,9 +797,7 @@ __device__ __forceinline__ bool gemm_rb(const FusedArgs& a, const Wg& w, const W
       if (node < N && o < M) epilogue(a, w, epi, l, node, o, has_bias ? sum + bf2f(bias_r[r]) : sum);
     }
     lds_barrier();
-    if (sub && r == 0) sub_stamp(a, w, l, 2);
   }
-  if (sub) sub_stamp(a, w, l, 3);
   return true;
 }
 
@@ -916,7 +891,6 @@ __device__ __forceinline__ bool att_prefix_unit(const FusedArgs& a, const Wg& w,
   }
   if (ws.on && !wait_flags(a, w, ws.id, ws.wx, ws.tag)) return false;
   stamp(a, w, ws.sl, ws.sfid, 1);
-  if (w.sub && ws.on && threadIdx.x == 0) a.sub[(size_t)w.g * 16 + 0] = now();
   // queries (B operand: node 16 t + i, dims 32 kc2 + 8 g .. +8)
   const int qn = min(16 * t + i, N - 1);
   u32x4 qh[2], ql[2];
@@ -929,7 +903,6 @@ __device__ __forceinline__ bool att_prefix_unit(const FusedArgs& a, const Wg& w,
                         __uint_as_float(q1[2]), __uint_as_float(q1[3])};
     pack_hilo8(v, qh[kc2], ql[kc2]);
   }
-  if (w.sub && threadIdx.x == 0) a.sub[(size_t)w.g * 16 + 3] = now();
   if (wv > 0) {
 #pragma unroll
     for (int j = 0; j < KVJ; ++j) {
@@ -942,7 +915,6 @@ __device__ __forceinline__ bool att_prefix_unit(const FusedArgs& a, const Wg& w,
     }
   }
   __syncthreads();
-  if (w.sub && threadIdx.x == 0) a.sub[(size_t)w.g * 16 + 4] = now();
   float m = -INFINITY, lsum = 0.f;
   f32x4 o[4];
 #pragma unroll
@@ -997,7 +969,6 @@ __device__ __forceinline__ bool att_prefix_unit(const FusedArgs& a, const Wg& w,
       o[tt] = mfma_bf16(va, pl, o[tt]);
     }
   }
-  if (w.sub && threadIdx.x == 0) a.sub[(size_t)w.g * 16 + 5] = now();
   // this wave's state of node 16 t + i: lane (i, g) holds dims 16 tt + 4 g + r
   {
     float* rec = wpart + (wv * 16 + i) * AREC;
@@ -1038,7 +1009,6 @@ __device__ __forceinline__ bool att_prefix_unit(const FusedArgs& a, const Wg& w,
       for (int e = 0; e < DPT; ++e) O[e] = fmaf(O[e], al, ovv[j][e] * wj);
       M = mn;
     }
-    if (w.sub && threadIdx.x == 0) a.sub[(size_t)w.g * 16 + 2] = now();
     const gw<float> out = part_rec(a, h, t, u, nl);
     if (d0 == 0) {
       out[0] = M;
@@ -1073,7 +1043,6 @@ __device__ __forceinline__ bool att_root_unit(const FusedArgs& a, const Wg& w, c
   const int rdep = ld_x(depth + rnc);
   if (ws.on && !wait_flags(a, w, ws.id, ws.wx, ws.tag)) return false;
   stamp(a, w, ws.sl, ws.sfid, 1);
-  if (w.sub && ws.on && threadIdx.x == 0) a.sub[(size_t)w.g * 16 + 0] = now();
   const gptr<uint16_t> ktb = opq((const uint16_t*)a.kt + head_rows * a.max_nodes * DH);
   const gptr<uint16_t> vtb = opq((const uint16_t*)a.vt + head_rows * a.max_nodes * DH);
   u32x4 rk[DH / 8], rv[DH / 8];
@@ -1088,10 +1057,6 @@ __device__ __forceinline__ bool att_root_unit(const FusedArgs& a, const Wg& w, c
     const gptr<float> qp = qbase + (size_t)rnc * d + h * DH + hl * DPL;
 #pragma unroll
     for (int e = 0; e < DPL; ++e) qr[hl * DPL + e] = ld_x(qp + e);
-  }
-  if (w.sub && threadIdx.x == 0) {
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    a.sub[(size_t)w.g * 16 + 1] = now();
   }
   float rm = -INFINITY, rl = 0.f, ro[DPL];
 #pragma unroll
@@ -1110,7 +1075,6 @@ __device__ __forceinline__ bool att_root_unit(const FusedArgs& a, const Wg& w, c
 #pragma unroll
     for (int jj = 0; jj < DH / 8; ++jj) *(u32x4*)(rvl + hl * AKS + 8 * jj) = rv[jj];
     wave_sync_lds();
-    if (w.sub && threadIdx.x == 0 && bt == 0) a.sub[(size_t)w.g * 16 + 3] = now();
     // four independent chains over the dims, combined in a fixed order
     float dq[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -1137,7 +1101,6 @@ __device__ __forceinline__ bool att_root_unit(const FusedArgs& a, const Wg& w, c
     const float alpha = __expf(rm - mn);
     const float p = kvalid ? __expf(sc - mn) : 0.f;
     const float ps = half_sum(p);
-    if (w.sub && threadIdx.x == 0 && bt == 0) a.sub[(size_t)w.g * 16 + 4] = now();
     rl = fmaf(rl, alpha, ps);
     rm = mn;
     const int cnt = min(32, rdep + 1 - 32 * bt);
@@ -1155,7 +1118,6 @@ __device__ __forceinline__ bool att_root_unit(const FusedArgs& a, const Wg& w, c
     for (int e = 0; e < DPL; ++e) ro[e] = fmaf(ro[e], alpha, acc[e]);
     wave_sync_lds();
   }
-  if (w.sub && threadIdx.x == 0) a.sub[(size_t)w.g * 16 + 2] = now();
   const gw<float> out = part_rec(a, h, t, a.att_units, nl);
   if (hl == 0) {
     out[0] = rm;
@@ -1185,7 +1147,6 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
   unsigned long long* llw = (unsigned long long*)(lplan + kPlanStride);  // [L][kLwSlots]
   float* red = (float*)lds;                                        // GEMM / LN reductions
   Wg w;
-  w.sub = 0;
   w.x = (int)xcc_id();
   w.r = blockIdx.x >> 3;
   w.g = w.x * kFRanks + w.r;
@@ -1255,8 +1216,6 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
     if (kind == 2) {
       // attention units of this XCD's heads, dealt to its ranks in turn
       stamp(a, w, l, FS_ATT, 0);
-      w.sub = a.sub && l == a.sub_l && a.sub_kind == 2;
-      if (w.sub && threadIdx.x == 0) a.sub[(size_t)w.g * 16 + 8] = now();
       const WaitSpec ws{FS_QKV, w.x, tag_of(w, l, FS_QKV), true, l, FS_ATT};
       const WaitSpec none{0, 0, 0u, false, l, FS_ATT};
       // units go to the ranks in the plan's order (fewest QKV row blocks
@@ -1270,12 +1229,7 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
         const bool ok = part < S ? att_prefix_unit(a, w, wsu, l, h, t, part, lds)
                                  : att_root_unit(a, w, wsu, l, h, t, lds);
         if (!ok) goto out;
-        if (w.sub && u == apos && threadIdx.x == 0) {
-          a.sub[(size_t)w.g * 16 + 13] = now();
-          a.sub[(size_t)w.g * 16 + 15] = part < S ? 1 : 2;
-        }
         unit_done(a, w, l, h, t, part);
-        if (w.sub && u == apos && threadIdx.x == 0) a.sub[(size_t)w.g * 16 + 14] = now();
       }
       signal(a, w, l, FS_ATT, false);
       stamp(a, w, l, FS_ATT, 2);
@@ -1288,8 +1242,6 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
       const bool wo = kind == 4;
       const int fid = wo ? FS_WO : FS_WPR;
       stamp(a, w, l, fid, 0);
-      w.sub = a.sub && l == a.sub_l && a.sub_kind == kind;
-      if (w.sub && threadIdx.x == 0) a.sub[(size_t)w.g * 16 + 8] = now();
       const WaitSpec ws{wo ? FS_ATT : FS_FC, w.x, tag_of(w, l, wo ? FS_ATT : FS_FC), true, l, fid};
       PreSpec nopre{};
       const bool ok = wo ? gemm_task<NT>(a, w, ws, FE_WO, l, p + PL_WO + 1, 0, n_wo, G<uint16_t>(nullptr),
@@ -1341,8 +1293,6 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
       default: gfid = FS_QKV; epi = FE_HEAD; nrb = min(4, hb1 - hb0); rb_first = hb0; Wm = G<u32x4>(a.p_head);
                Mo = a.V; break;
     }
-    w.sub = a.sub && l == a.sub_l && a.sub_kind == kind + 1;
-    if (w.sub && threadIdx.x == 0) a.sub[(size_t)w.g * 16 + 8] = now();
     {
       const WaitSpec gws{ps.fid, w.x, tag_of(w, l, ps.fid), true, l, gfid};
       if (!gemm_task<NT>(a, w, gws, epi, l, rbs, rb_first, nrb, bias, Wm, KCd, Mo, k0, k1, act, KCd, red, ps))
@@ -1358,9 +1308,7 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
           goto out;
       }
     }
-    if (a.sub && kind + 1 == a.sub_kind) sub_stamp(a, w, l, 4);
     signal(a, w, l, gfid, false);
-    if (a.sub && kind + 1 == a.sub_kind) sub_stamp(a, w, l, 5);
     stamp(a, w, l, gfid, 2);
   }
 out:

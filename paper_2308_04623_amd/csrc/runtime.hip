@@ -26,10 +26,7 @@ thread_local std::string g_last_error;
 int g_gemm_path = 0;  // 0 auto, 1 vector ALU, 2 matrix cores
 int g_prefetch = 1;   // warm each weight GEMM's L2 from the kernel before it
 int g_pass_mode = 0;  // 0 auto, 1 one kernel per sub-layer, 2 the persistent single-launch pass only
-int g_fz_poll_sleep = [] {
-  const char* e = getenv("SSD_FZ_POLL_SLEEP");
-  return e ? atoi(e) : 0;
-}();
+
 
 // Node counts up to this use the vector-ALU GEMM on the automatic path.
 constexpr int kVecMaxNodes = 4;
@@ -127,7 +124,6 @@ struct ssd_kv {
   void* fz_ws = nullptr;
   FusedArgs fz{};                      // workspace pointers, XCD ranges
   int* fz_plan[5] = {};                // device plans per 16-node tile count (1..4)
-  unsigned long long* fz_sub = nullptr;  // (measurement) sub-stage timestamps
 };
 
 struct ssd_graph {
@@ -178,11 +174,6 @@ extern "C" ssd_status ssd_kv_set_trace(ssd_kv* kv, uint64_t* buf) {
   if (!kv->fz_ok) return fail(SSD_E_UNSUPPORTED, "the session has no persistent pass");
   kv->fz.trace = (unsigned long long*)buf;
   return SSD_OK;
-}
-
-extern "C" ssd_status ssd_kv_debug_sub(ssd_kv* kv, uint64_t* host16x256) {
-  if (!kv || !kv->fz_ok || !host16x256) return fail(SSD_E_INVALID_ARG, "bad argument");
-  HIP_TRY(hipMemcpy(host16x256, kv->fz_sub, (size_t)kFGroups * 16 * 8, hipMemcpyDeviceToHost));
 }
 
 extern "C" ssd_status ssd_fused_plan(int32_t n_head, int32_t d_model, int32_t d_mlp, int32_t vocab, int32_t n_tiles,
@@ -409,7 +400,6 @@ static ssd_status fused_setup(ssd_kv* kv) {
   const size_t o_po = take((size_t)kFXcd * kFMaxN * d * 4), o_pp = take((size_t)kFXcd * kFMaxN * d * 4);
   const size_t o_fl = take((size_t)kFStages * kFGroups * 4), o_ctl = take((size_t)kFCtlWords * 4);
   const size_t o_plan = take(tabs.size() * 4);
-  const size_t o_sub = take((size_t)kFGroups * 16 * 8);
   const size_t o_uf = take((size_t)c.n_head * 4 * att_parts * 4);
   static const hipError_t prep = fused_prepare();
   if (prep != hipSuccess) return SSD_OK;  // keep the per-sub-layer kernels
@@ -429,7 +419,6 @@ static ssd_status fused_setup(ssd_kv* kv) {
   a.part_p = (float*)(b + o_pp);
   a.flags = (unsigned*)(b + o_fl);
   a.ctl = (unsigned*)(b + o_ctl);
-  kv->fz_sub = (unsigned long long*)(b + o_sub);
   a.uflag = (unsigned*)(b + o_uf);
   a.uf_stride = (int)att_parts;
   for (int nt = 1; nt <= 4; ++nt) kv->fz_plan[nt] = (int*)(b + o_plan) + (size_t)(nt - 1) * kFGroups * kPlanStride;
@@ -747,12 +736,6 @@ static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int3
     a.logits = logits;
     a.plan = kv->fz_plan[(n + 15) / 16];
     a.att_units = (P + kFAttRows - 1) / kFAttRows;
-    a.poll_sleep = g_fz_poll_sleep;
-    a.sub = kv->fz.trace ? kv->fz_sub : nullptr;
-    if (a.sub) HIP_TRY(hipMemsetAsync(a.sub, 0, (size_t)kFGroups * 16 * 8, s));
-    a.sub_l = 10;
-    a.sub_kind = getenv("SSD_FZ_SUBKIND") ? atoi(getenv("SSD_FZ_SUBKIND")) : 6;
-    a.sub_epi = getenv("SSD_FZ_SUBEPI") ? atoi(getenv("SSD_FZ_SUBEPI")) : 2;
     HIP_TRY(launch_fused(a, s));
     return SSD_OK;
   }

@@ -229,10 +229,7 @@ struct FusedArgs {
   int xf[2 * kFXcd];        // hidden k-steps [xf[2x], xf[2x+1]) of XCD x
   unsigned* err;            // session error counter
   unsigned long long timeout;  // s_memrealtime ticks (100 MHz) before a wait gives up
-  int poll_sleep;           // extra back-off between flag polls (units of s_sleep 8)
   unsigned long long* trace;  // stage timestamps [kFGroups][L + 1][kFStages][3], or nullptr
-  unsigned long long* sub;   // (measurement) sub-stage timestamps [kFGroups][16] of one stage, or nullptr
-  int sub_l, sub_kind, sub_epi;
 };
 
 // Work split of the fused pass for a model shape and 16-node tile count:

@@ -161,3 +161,26 @@ def test_weight_prefetch_is_bitwise_neutral(big, torch, n):
     assert torch.equal(off_eager, on_eager)
     assert np.array_equal(off_graph, on_graph)
     assert np.array_equal(off_graph, on_eager.numpy())
+
+
+@pytest.mark.parametrize("n,P", [(17, 512), (64, 512), (48, 1500)])
+def test_persistent_pass_sampled_paths(big, torch, n, P):
+    """The persistent single-launch pass forced on the full shape: 2 and 4
+    node tiles, and a 1500-token prefix (6 prefix units per tile, so the
+    tile merges read their parts in two rounds); the root path of the last
+    node against the oracle, in the captured graph."""
+    cfg, w, om, m, ssd = big
+    s, kc, vc = _session(big, torch, P, P + 128, 64, seed=7)
+    toks, par = W.best_first_tree(n, seed=5, vocab=cfg.vocab)
+    toks[0] = 23  # the root (the last emitted token)
+    ssd.set_pass_mode(ssd.PASS_FUSED)
+    try:
+        assert s.verify_path(n) == ssd.PASS_FUSED
+        got = _graph_logits(s, torch, P, toks, par)
+    finally:
+        ssd.set_pass_mode(ssd.PASS_AUTO)
+    assert s.error_count() == 0
+    path, ref = _oracle_path_rows(om, kc, vc, P, toks, par, n - 1)
+    err = np.abs(got[path] - ref).max()
+    print(f"persistent n={n} P={P} path {path} max|d| {err:.3e}", flush=True)
+    assert err < TOL
