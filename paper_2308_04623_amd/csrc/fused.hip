@@ -400,18 +400,19 @@ __device__ __forceinline__ unsigned owner_mask(const int* range) {
   return m;
 }
 
-// Waves 0..3 (256 threads): thread t takes the float4 chunks t, t + 256, ...
-// (C per thread, d <= 1024 C); sums run over the thread's chunks in order,
-// across its wave by DPP, then over the four waves in wave order.  Wave 0
-// polls with nothing else in flight (a wave's loads complete in order, so
-// anything issued before would delay the poll); the row's loads are issued
-// together right after it.
-template <int C>
-__device__ __forceinline__ bool ln_row_q(const FusedArgs& a, const Wg& w, const WaitSpec& ws, int n, int mode,
-                                         gptr<uint16_t> bias, const float* part, unsigned own, gptr<uint16_t> g,
-                                         gptr<uint16_t> b, uint16_t* act) {
+// Waves 0..3 (256 threads) normalise R node rows n0, n0 + 32, ... (those
+// below N) together: thread t takes the float4 chunks t, t + 256, ... of
+// each row (C per thread, d <= 1024 C); sums run over the thread's chunks in
+// order, across its wave by DPP, then over the four waves in wave order.
+// Wave 0 polls with nothing else in flight (a wave's loads complete in
+// order, so anything issued before would delay the poll); every load of
+// every row is issued together right after it.
+template <int C, int R>
+__device__ __forceinline__ bool ln_rows_q(const FusedArgs& a, const Wg& w, const WaitSpec& ws, int n0, int mode,
+                                          gptr<uint16_t> bias, const float* part, unsigned own, gptr<uint16_t> g,
+                                          gptr<uint16_t> b, uint16_t* act) {
   const int d = a.d, nc = d / 4, tid = opq_tid(), wv = tid >> 6;
-  float* red = (float*)(w.sh + 8);  // [8]
+  float* red = (float*)(w.sh + 16);  // [R][8]
   if (mode != 0 && ws.on) {
     if (wv == 0) {
       const bool ok = poll_w0(a, w, ws.id, ws.wx, ws.tag);
@@ -422,7 +423,9 @@ __device__ __forceinline__ bool ln_row_q(const FusedArgs& a, const Wg& w, const 
     if (wv > 0) asm volatile("buffer_inv sc0" ::: "memory");
     stamp(a, w, ws.sl, ws.sfid, 1);
   }
-  const gw<f32x4> xr = (gw<f32x4>)opq(a.xr + ((size_t)w.x * kFMaxN + n) * d);
+  int nr[R];
+#pragma unroll
+  for (int j = 0; j < R; ++j) nr[j] = min(n0 + j * kFRanks, a.N - 1);  // (rows past N repeat the last; not stored)
   const gptr<u32x2> g4 = (gptr<u32x2>)opq(g), b4 = (gptr<u32x2>)opq(b);
   const gw<uint16_t> actg = opq(act);
   int cc[C];
@@ -432,95 +435,122 @@ __device__ __forceinline__ bool ln_row_q(const FusedArgs& a, const Wg& w, const 
     return (f32x4){__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u), __uint_as_float(u.y << 16),
                    __uint_as_float(u.y & 0xffff0000u)};
   };
-  f32x4 v[C];
+  f32x4 v[R][C];
   u32x2 gr[C], br[C];
-  if (mode == 0) {
-    const int tok = ld_x(a.tree + n), pos = ld_x(a.tree + a.max_nodes + n);
-    const gptr<u32x2> te = (gptr<u32x2>)(opq(a.wte) + (size_t)tok * d);
-    const gptr<u32x2> pe = (gptr<u32x2>)(opq(a.wpe) + (size_t)pos * d);
-    u32x2 tr[C], pr[C];
 #pragma unroll
-    for (int i = 0; i < C; ++i) {
-      tr[i] = te[cc[i]];
-      pr[i] = pe[cc[i]];
-      gr[i] = g4[cc[i]];
-      br[i] = b4[cc[i]];
+  for (int i = 0; i < C; ++i) {
+    gr[i] = g4[cc[i]];
+    br[i] = b4[cc[i]];
+  }
+  if (mode == 0) {
+    u32x2 tr[R][C], pr[R][C];
+#pragma unroll
+    for (int j = 0; j < R; ++j) {
+      const int tok = ld_x(a.tree + nr[j]), pos = ld_x(a.tree + a.max_nodes + nr[j]);
+      const gptr<u32x2> te = (gptr<u32x2>)(opq(a.wte) + (size_t)tok * d);
+      const gptr<u32x2> pe = (gptr<u32x2>)(opq(a.wpe) + (size_t)pos * d);
+#pragma unroll
+      for (int i = 0; i < C; ++i) {
+        tr[j][i] = te[cc[i]];
+        pr[j][i] = pe[cc[i]];
+      }
     }
 #pragma unroll
-    for (int i = 0; i < C; ++i) v[i] = bf4(tr[i]) + bf4(pr[i]);
+    for (int j = 0; j < R; ++j)
+#pragma unroll
+      for (int i = 0; i < C; ++i) v[j][i] = bf4(tr[j][i]) + bf4(pr[j][i]);
   } else {
-    // every XCD's partials of the row: device-coherent 16-byte loads
-    const __amdgpu_buffer_rsrc_t pr =
+    // every XCD's partials of the rows: device-coherent 16-byte loads
+    const __amdgpu_buffer_rsrc_t prs =
         __builtin_amdgcn_make_buffer_rsrc((void*)part, (short)0, (int)(kFXcd * kFMaxN * d * 4), 0x00020000);
-    f32x4 pv[kFXcd][C];
+    f32x4 pv[R][kFXcd][C];
 #pragma unroll
-    for (int X = 0; X < kFXcd; ++X)
+    for (int j = 0; j < R; ++j)
 #pragma unroll
-      for (int i = 0; i < C; ++i)
-        pv[X][i] = __builtin_bit_cast(
-            f32x4, __builtin_amdgcn_raw_buffer_load_b128(pr, (unsigned)(16 * cc[i]),
-                                                         (unsigned)(((size_t)X * kFMaxN + n) * d * 4), CP_SC1));
+      for (int X = 0; X < kFXcd; ++X)
+#pragma unroll
+        for (int i = 0; i < C; ++i)
+          pv[j][X][i] = __builtin_bit_cast(
+              f32x4, __builtin_amdgcn_raw_buffer_load_b128(prs, (unsigned)(16 * cc[i]),
+                                                           (unsigned)(((size_t)X * kFMaxN + nr[j]) * d * 4), CP_SC1));
     const gptr<u32x2> c4 = (gptr<u32x2>)opq(bias);
-    f32x4 xv[C];
+    f32x4 xv[R][C];
     u32x2 cr[C];
 #pragma unroll
-    for (int i = 0; i < C; ++i) {
-      xv[i] = xr[cc[i]];
-      cr[i] = c4[cc[i]];
-      gr[i] = g4[cc[i]];
-      br[i] = b4[cc[i]];
+    for (int i = 0; i < C; ++i) cr[i] = c4[cc[i]];
+#pragma unroll
+    for (int j = 0; j < R; ++j) {
+      const gptr<f32x4> xr = (gptr<f32x4>)opq(a.xr + ((size_t)w.x * kFMaxN + nr[j]) * d);
+#pragma unroll
+      for (int i = 0; i < C; ++i) xv[j][i] = xr[cc[i]];
     }
     // bias, then the partials of the XCDs that own a share, in XCD order
 #pragma unroll
-    for (int i = 0; i < C; ++i) {
-      f32x4 acc = bf4(cr[i]);
-      if (own == (1u << kFXcd) - 1) {
+    for (int j = 0; j < R; ++j)
 #pragma unroll
-        for (int X = 0; X < kFXcd; ++X) acc += pv[X][i];
-      } else {
+      for (int i = 0; i < C; ++i) {
+        f32x4 acc = bf4(cr[i]);
+        if (own == (1u << kFXcd) - 1) {
 #pragma unroll
-        for (int X = 0; X < kFXcd; ++X) {
-          const bool o = own >> X & 1u;
-          acc[0] += o ? pv[X][i][0] : 0.f;
-          acc[1] += o ? pv[X][i][1] : 0.f;
-          acc[2] += o ? pv[X][i][2] : 0.f;
-          acc[3] += o ? pv[X][i][3] : 0.f;
+          for (int X = 0; X < kFXcd; ++X) acc += pv[j][X][i];
+        } else {
+#pragma unroll
+          for (int X = 0; X < kFXcd; ++X) {
+            const bool o = own >> X & 1u;
+            acc[0] += o ? pv[j][X][i][0] : 0.f;
+            acc[1] += o ? pv[j][X][i][1] : 0.f;
+            acc[2] += o ? pv[j][X][i][2] : 0.f;
+            acc[3] += o ? pv[j][X][i][3] : 0.f;
+          }
         }
+        v[j][i] = xv[j][i] + acc;
       }
-      v[i] = xv[i] + acc;
-    }
   }
-  float s = 0.f;
+  float sm[R];
 #pragma unroll
-  for (int i = 0; i < C; ++i) {
-    if (tid + QW * 64 * i < nc) {
-      xr[tid + QW * 64 * i] = v[i];
-      s += ((v[i][0] + v[i][1]) + (v[i][2] + v[i][3]));
+  for (int j = 0; j < R; ++j) {
+    const gw<f32x4> xr = (gw<f32x4>)opq(a.xr + ((size_t)w.x * kFMaxN + nr[j]) * d);
+    float sj = 0.f;
+#pragma unroll
+    for (int i = 0; i < C; ++i) {
+      if (tid + QW * 64 * i < nc) {
+        if (n0 + j * kFRanks < a.N) xr[tid + QW * 64 * i] = v[j][i];
+        sj += ((v[j][i][0] + v[j][i][1]) + (v[j][i][2] + v[j][i][3]));
+      }
     }
+    sm[j] = wave_sum(sj);
+    if ((tid & 63) == 0) red[8 * j + wv] = sm[j];
   }
-  s = wave_sum(s);
-  if ((tid & 63) == 0) red[wv] = s;
   q_barrier(w);
-  const float mean = ((red[0] + red[1]) + (red[2] + red[3])) / d;
-  float q = 0.f;
+  float mean[R], qs[R];
 #pragma unroll
-  for (int i = 0; i < C; ++i) {
-    if (tid + QW * 64 * i < nc) {
-      const f32x4 c = v[i] - mean;
-      q += ((c[0] * c[0] + c[1] * c[1]) + (c[2] * c[2] + c[3] * c[3]));
+  for (int j = 0; j < R; ++j) {
+    mean[j] = ((red[8 * j] + red[8 * j + 1]) + (red[8 * j + 2] + red[8 * j + 3])) / d;
+    float q = 0.f;
+#pragma unroll
+    for (int i = 0; i < C; ++i) {
+      if (tid + QW * 64 * i < nc) {
+        const f32x4 c = v[j][i] - mean[j];
+        q += ((c[0] * c[0] + c[1] * c[1]) + (c[2] * c[2] + c[3] * c[3]));
+      }
     }
+    qs[j] = wave_sum(q);
+    if ((tid & 63) == 0) red[8 * j + 4 + wv] = qs[j];
   }
-  q = wave_sum(q);
-  if ((tid & 63) == 0) red[4 + wv] = q;
   q_barrier(w);
-  const float rden = 1.0f / sqrtf(((red[4] + red[5]) + (red[6] + red[7])) / d + a.eps);
 #pragma unroll
-  for (int i = 0; i < C; ++i) {
-    const int c = tid + QW * 64 * i;
-    if (c < nc) {
-      const f32x4 gv = bf4(gr[i]), bv = bf4(br[i]);
-      const f32x4 y = (v[i] - mean) * rden * gv + bv;
-      st_act4(actg, n, 4 * c, d / 32, y[0], y[1], y[2], y[3]);
+  for (int j = 0; j < R; ++j) {
+    if (n0 + j * kFRanks >= a.N) break;
+    const float rden =
+        1.0f / sqrtf(((red[8 * j + 4] + red[8 * j + 5]) + (red[8 * j + 6] + red[8 * j + 7])) / d + a.eps);
+#pragma unroll
+    for (int i = 0; i < C; ++i) {
+      const int c = tid + QW * 64 * i;
+      if (c < nc) {
+        const f32x4 gv = bf4(gr[i]), bv = bf4(br[i]);
+        const f32x4 y = (v[j][i] - mean[j]) * rden * gv + bv;
+        st_act4(actg, nr[j], 4 * c, d / 32, y[0], y[1], y[2], y[3]);
+      }
     }
   }
   return true;
@@ -616,14 +646,16 @@ struct PreSpec {
 // published (the four waves' stores complete, then wave 0 writes the flag).
 __device__ __forceinline__ bool do_pre(const FusedArgs& a, const Wg& w, const PreSpec& ps) {
   if (ps.kind == 0) return true;
-  const WaitSpec none{0, 0, 0u, false, ps.l, ps.fid};
   bool ok = true;
-  if (ps.kind == 1) {
-    for (int n = w.r; n < a.N && ok; n += kFRanks)
-      ok = a.d <= 1024 ? ln_row_q<1>(a, w, n == w.r ? ps.ws : none, n, ps.mode, ps.bias, ps.part, ps.own, ps.g,
-                                     ps.b, ps.act)
-                       : ln_row_q<2>(a, w, n == w.r ? ps.ws : none, n, ps.mode, ps.bias, ps.part, ps.own, ps.g,
-                                     ps.b, ps.act);
+  if (ps.kind == 1 && w.r < a.N) {
+    // this rank's rows: w.r and (at more than 32 nodes) w.r + 32, together
+    const bool two = w.r + kFRanks < a.N;
+    if (a.d <= 1024)
+      ok = two ? ln_rows_q<1, 2>(a, w, ps.ws, w.r, ps.mode, ps.bias, ps.part, ps.own, ps.g, ps.b, ps.act)
+               : ln_rows_q<1, 1>(a, w, ps.ws, w.r, ps.mode, ps.bias, ps.part, ps.own, ps.g, ps.b, ps.act);
+    else
+      ok = two ? ln_rows_q<2, 2>(a, w, ps.ws, w.r, ps.mode, ps.bias, ps.part, ps.own, ps.g, ps.b, ps.act)
+               : ln_rows_q<2, 1>(a, w, ps.ws, w.r, ps.mode, ps.bias, ps.part, ps.own, ps.g, ps.b, ps.act);
   }
   if (!ok) return false;
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -1142,8 +1174,8 @@ __device__ __forceinline__ bool att_root_unit(const FusedArgs& a, const Wg& w, c
 
 template <int NT>
 __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* lds) {
-  int* sh = (int*)(lds + A_REGION + A_PART_BYTES + A_Q_BYTES);  // 16 words
-  int* lplan = sh + 16;                                            // [kPlanStride]
+  int* sh = (int*)(lds + A_REGION + A_PART_BYTES + A_Q_BYTES);  // 32 words
+  int* lplan = sh + 32;                                            // [kPlanStride]
   unsigned long long* llw = (unsigned long long*)(lplan + kPlanStride);  // [L][kLwSlots]
   float* red = (float*)lds;                                        // GEMM / LN reductions
   Wg w;
@@ -1463,7 +1495,7 @@ hipError_t fused_prepare() {
 }
 
 size_t fused_lds_bytes() {
-  return fz::A_REGION + fz::A_PART_BYTES + fz::A_Q_BYTES + 64 + kPlanStride * 4 + (size_t)kFMaxL * kLwSlots * 8;
+  return fz::A_REGION + fz::A_PART_BYTES + fz::A_Q_BYTES + 128 + kPlanStride * 4 + (size_t)kFMaxL * kLwSlots * 8;
 }
 
 hipError_t launch_fused(const FusedArgs& a, hipStream_t s) {

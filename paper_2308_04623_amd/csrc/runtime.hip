@@ -432,7 +432,7 @@ static ssd_status fused_setup(ssd_kv* kv) {
 static bool use_fused(const ssd_model* m, const ssd_kv* kv, int n) {
   if (g_pass_mode == 1 || m->f32 || !kv->fz_ok || !m->ftab) return false;
   // the persistent pass is forced, or chosen where it is the faster one
-  // (measured: up to 32 nodes on the GPT-2-L shape)
+  // (measured on the GPT-2-L shape: at every node count it supports)
   return g_pass_mode == 2 ? n <= kFMaxN : n <= kFAutoMaxN;
 }
 

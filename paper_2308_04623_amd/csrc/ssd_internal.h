@@ -181,7 +181,7 @@ constexpr int kFXcd = 8;                   // XCDs
 constexpr int kFRanks = 32;                // compute workgroups per XCD
 constexpr int kFGroups = kFXcd * kFRanks;  // compute workgroups (one per CU)
 constexpr int kFMaxN = 64;                 // nodes
-constexpr int kFAutoMaxN = 32;             // most nodes the default pass mode sends to it
+constexpr int kFAutoMaxN = 64;             // most nodes the default pass mode sends to it
 constexpr int kFMaxL = 255;                // layers
 // stages of a layer; their flags are [kFStages][kFGroups] words
 enum FStage { FS_LN1 = 0, FS_QKV, FS_ATT, FS_WO, FS_LN2, FS_FC, FS_WPR, FS_AMG, kFStages };
