@@ -197,6 +197,7 @@ struct Wg {
   unsigned E;        // this pass's number
   unsigned tagbase;  // E * tags per pass
   int* sh;           // LDS words shared by the workgroup
+  unsigned char* lds;  // the workgroup's dynamic LDS
   const int* plan;   // this workgroup's plan row, copied to LDS
   const unsigned long long* lwt;  // the per-layer parameter pointers, copied to LDS
 };
@@ -640,7 +641,16 @@ struct PreSpec {
   const float* part;
   unsigned own;  // XCDs that own a share of the residual GEMM
   uint16_t* act;
+  // after the rows, waves 1..3 copy these weight fragments (row blocks
+  // wrbs[0 .. wn) of W, k-steps [wk0, wk1) of KC) into LDS at WST, in
+  // (row block, k-step) order, for a GEMM two stages on (wn = 0: none)
+  int wn, wk0, wk1, wKC;
+  const int* wrbs;
+  gptr<u32x4> wW;
 };
+
+constexpr int WST = 16 * 1024;                              // LDS offset of staged weights
+constexpr int WST_FRAGS = (73728 + 34816 + 4096 - WST) / 1024;  // 1 KB fragments that fit below sh
 
 // Run by waves 0..3 together: the LayerNorm rows, then the stage is
 // published (the four waves' stores complete, then wave 0 writes the flag).
@@ -664,6 +674,19 @@ __device__ __forceinline__ bool do_pre(const FusedArgs& a, const Wg& w, const Pr
     __hip_atomic_store(a.flags + (size_t)ps.fid * kFGroups + w.g, tag_of(w, ps.l, ps.fid), __ATOMIC_RELAXED,
                        __HIP_MEMORY_SCOPE_WORKGROUP);
   stamp(a, w, ps.l, ps.fid, 2);
+  if (ps.wn > 0 && threadIdx.x >= 64) {
+    // (not wave 0: its polls must not wait behind these loads; the stage's
+    // closing vmcnt(0) and barrier complete them before the GEMM reads them)
+    const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63, nk = ps.wk1 - ps.wk0, tot = ps.wn * nk;
+    unsigned char* lds_base = w.lds;
+    const gptr<u32x4> Wv = opq(ps.wW) + lane;
+    for (int f = wv - 1; f < tot; f += QW - 1) {
+      const int r = f / nk, k = ps.wk0 + f - r * nk;
+      const int rb = ((const __attribute__((address_space(3))) int*)ps.wrbs)[r];
+      __builtin_amdgcn_global_load_lds((const void*)(Wv + ((size_t)rb * ps.wKC + k) * 64),
+                                       (lds_void*)(lds_base + WST + (size_t)f * 1024), 16, 0, 0);
+    }
+  }
   return true;
 }
 
@@ -705,7 +728,7 @@ template <int NT, int RB, int U>
 __device__ __forceinline__ bool gemm_rb(const FusedArgs& a, const Wg& w, const WaitSpec& ws, int epi, int l,
                                         const int* rbs, int rb_first, int nrb, gptr<uint16_t> bias, gptr<u32x4> Wp,
                                         int KC, int M, int kc0, int kc1, const uint16_t* act, int act_kc,
-                                        float* red, const PreSpec& ps) {
+                                        float* red, const PreSpec& ps, bool wlds) {
   constexpr int NN = 16 * NT, NCW = NWV - QW;
   // Waves 4..7 compute: wave 4 + c takes k-steps kc0 + c, kc0 + c + 4, ...,
   // and loads their weights first thing.  Waves 0..3 run the pre-stage
@@ -740,10 +763,19 @@ __device__ __forceinline__ bool gemm_rb(const FusedArgs& a, const Wg& w, const W
   u32x4 wq[U][RB];
   u32x4 bq[U][NT];
   const int klast = kc1 - 1;
+  const int nk = kc1 - kc0;
+  const __attribute__((address_space(3))) u32x4* wl =
+      (const __attribute__((address_space(3))) u32x4*)((unsigned char*)red + WST) + lane;
   auto load_w = [&](int s, int u) {
     const int kc = min(kc0 + cw + NCW * s, klast);
+    if (wlds) {
+      // staged in LDS by the stage before the last ((row block, k-step) order)
 #pragma unroll
-    for (int r = 0; r < RB; ++r) wq[u][r] = wb[r][(size_t)kc * 64];
+      for (int r = 0; r < RB; ++r) wq[u][r] = wl[(min(r, nrb - 1) * nk + (kc - kc0)) * 64];
+    } else {
+#pragma unroll
+      for (int r = 0; r < RB; ++r) wq[u][r] = wb[r][(size_t)kc * 64];
+    }
   };
   auto load_a = [&](int s, int u) {
     const int kc = min(kc0 + cw + NCW * s, klast);
@@ -852,16 +884,16 @@ template <int NT>
 __device__ __forceinline__ bool gemm_task(const FusedArgs& a, const Wg& w, const WaitSpec& ws, int epi, int l,
                                           const int* rbs, int rb_first, int nrb, gptr<uint16_t> bias,
                                           gptr<u32x4> Wp, int KC, int M, int kc0, int kc1, const uint16_t* act,
-                                          int act_kc, float* red, const PreSpec& ps) {
+                                          int act_kc, float* red, const PreSpec& ps, bool wlds = false) {
   if (nrb <= 0) return pre_only(a, w, ps);
   if (nrb == 1)
     return gemm_rb<NT, 1, NT <= 2 ? 10 : 5>(a, w, ws, epi, l, rbs, rb_first, 1, bias, Wp, KC, M, kc0, kc1, act,
-                                           act_kc, red, ps);
+                                           act_kc, red, ps, wlds);
   if (nrb == 2)
     return gemm_rb<NT, 2, NT <= 2 ? 10 : 5>(a, w, ws, epi, l, rbs, rb_first, 2, bias, Wp, KC, M, kc0, kc1, act,
-                                           act_kc, red, ps);
+                                           act_kc, red, ps, wlds);
   return gemm_rb<NT, 4, NT <= 2 ? 5 : 3>(a, w, ws, epi, l, rbs, rb_first, nrb, bias, Wp, KC, M, kc0, kc1, act,
-                                         act_kc, red, ps);
+                                         act_kc, red, ps, wlds);
 }
 
 // ------------------------------------------------------------------ tree attention
@@ -890,6 +922,9 @@ constexpr int AKS = DH + 8;                 // LDS row stride of K and V (elemen
 constexpr int A_KV_BYTES = 2 * ACH * AKS * 2;
 constexpr int A_RV_BYTES = 2 * NWV * 32 * AKS * 2;  // root-path V rows, 32 per half-wave (padded rows)
 constexpr int A_REGION = A_KV_BYTES > A_RV_BYTES ? A_KV_BYTES : A_RV_BYTES;
+static_assert(WST + WST_FRAGS * 1024 <= A_REGION + NWV * 16 * AREC * 4 + NWV * 2 * DH * 4,
+              "staged weights must stay below the workgroup's shared words");
+static_assert(WST >= (NWV - QW) * 64 * 16 * 4, "the GEMM reduction must stay below the staged weights");
 constexpr int A_PART_BYTES = NWV * 16 * AREC * 4;  // the waves' states of a prefix unit
 constexpr int A_Q_BYTES = NWV * 2 * DH * 4;        // root-path queries, one row per half-wave
 
@@ -1183,6 +1218,7 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
   w.r = blockIdx.x >> 3;
   w.g = w.x * kFRanks + w.r;
   w.sh = sh;
+  w.lds = lds;
   w.plan = lplan;
   w.lwt = llw;
   {
@@ -1240,6 +1276,11 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
   const int nhx = a.xh[2 * w.x + 1] - a.xh[2 * w.x];
   const int n_attu = nhx * NTl * (S + 1);    // attention units of this XCD (prefix units + root unit per tile)
   const unsigned own_h = owner_mask(a.xh), own_f = owner_mask(a.xf);
+  // With two or more node tiles, the MLP down-projection's weights are
+  // copied into LDS during the up-projection (by waves 1..3, which ran the
+  // LayerNorm) when they fit.  The up-projection's closing wait covers the
+  // copy; with one tile that stage is too short to hide it.
+  const bool wpr_staged = NT >= 2 && n_wpr > 0 && n_wpr * (kf1 - kf0) <= WST_FRAGS;
   const int nst = L * 8 + 2;
   for (int st = 0; st < nst; ++st) {
     const int l = st < L * 8 ? st / 8 : L;
@@ -1279,7 +1320,8 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
       const bool ok = wo ? gemm_task<NT>(a, w, ws, FE_WO, l, p + PL_WO + 1, 0, n_wo, G<uint16_t>(nullptr),
                                          G<u32x4>(lw(w, l, LW_O)), KCd, d, kh0, kh1, a.fo, KCd, red, nopre)
                          : gemm_task<NT>(a, w, ws, FE_WPR, l, p + PL_WPR + 1, 0, n_wpr, G<uint16_t>(nullptr),
-                                         G<u32x4>(lw(w, l, LW_PR)), KCm, d, kf0, kf1, a.ff, KCm, red, nopre);
+                                         G<u32x4>(lw(w, l, LW_PR)), KCm, d, kf0, kf1, a.ff, KCm, red, nopre,
+                                         wpr_staged);
       if (!ok) goto out;
       signal(a, w, l, fid, true);
       stamp(a, w, l, fid, 2);
@@ -1294,6 +1336,14 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
     ps.fid = kind == 5 ? FS_LN2 : FS_LN1;
     ps.mode = (kind == 0 && l == 0) ? 0 : 1;
     if (kind == 5) {
+      if (wpr_staged) {
+        ps.wn = n_wpr;
+        ps.wk0 = kf0;
+        ps.wk1 = kf1;
+        ps.wKC = KCm;
+        ps.wrbs = p + PL_WPR + 1;
+        ps.wW = G<u32x4>(lw(w, l, LW_PR));
+      }
       ps.ws = WaitSpec{FS_WO, -1, tag_of(w, l, FS_WO), true, l, FS_LN2};
       ps.bias = G<uint16_t>(lw(w, l, LB_O));
       ps.part = a.part_o;
