@@ -642,15 +642,16 @@ struct PreSpec {
   unsigned own;  // XCDs that own a share of the residual GEMM
   uint16_t* act;
   // after the rows, waves 1..3 copy these weight fragments (row blocks
-  // wrbs[0 .. wn) of W, k-steps [wk0, wk1) of KC) into LDS at WST, in
+  // wrbs[0 .. wn) of W, k-steps [wk0, wk1) of KC) into LDS at wdst, in
   // (row block, k-step) order, for a GEMM two stages on (wn = 0: none)
-  int wn, wk0, wk1, wKC;
+  int wn, wk0, wk1, wKC, wdst;  // (wdst: byte offset in LDS)
   const int* wrbs;
   gptr<u32x4> wW;
 };
 
-constexpr int WST = 16 * 1024;                              // LDS offset of staged weights
+constexpr int WST = 16 * 1024;                              // LDS offset of the down-projection's staged weights
 constexpr int WST_FRAGS = (73728 + 34816 + 4096 - WST) / 1024;  // 1 KB fragments that fit below sh
+constexpr int WO_FRAGS = 24;  // the out-projection's staged fragments, above the parameter table
 
 // Run by waves 0..3 together: the LayerNorm rows, then the stage is
 // published (the four waves' stores complete, then wave 0 writes the flag).
@@ -684,7 +685,7 @@ __device__ __forceinline__ bool do_pre(const FusedArgs& a, const Wg& w, const Pr
       const int r = f / nk, k = ps.wk0 + f - r * nk;
       const int rb = ((const __attribute__((address_space(3))) int*)ps.wrbs)[r];
       __builtin_amdgcn_global_load_lds((const void*)(Wv + ((size_t)rb * ps.wKC + k) * 64),
-                                       (lds_void*)(lds_base + WST + (size_t)f * 1024), 16, 0, 0);
+                                       (lds_void*)(lds_base + ps.wdst + (size_t)f * 1024), 16, 0, 0);
     }
   }
   return true;
@@ -728,7 +729,7 @@ template <int NT, int RB, int U>
 __device__ __forceinline__ bool gemm_rb(const FusedArgs& a, const Wg& w, const WaitSpec& ws, int epi, int l,
                                         const int* rbs, int rb_first, int nrb, gptr<uint16_t> bias, gptr<u32x4> Wp,
                                         int KC, int M, int kc0, int kc1, const uint16_t* act, int act_kc,
-                                        float* red, const PreSpec& ps, bool wlds) {
+                                        float* red, const PreSpec& ps, int wofs) {
   constexpr int NN = 16 * NT, NCW = NWV - QW;
   // Waves 4..7 compute: wave 4 + c takes k-steps kc0 + c, kc0 + c + 4, ...,
   // and loads their weights first thing.  Waves 0..3 run the pre-stage
@@ -765,10 +766,10 @@ __device__ __forceinline__ bool gemm_rb(const FusedArgs& a, const Wg& w, const W
   const int klast = kc1 - 1;
   const int nk = kc1 - kc0;
   const __attribute__((address_space(3))) u32x4* wl =
-      (const __attribute__((address_space(3))) u32x4*)((unsigned char*)red + WST) + lane;
+      (const __attribute__((address_space(3))) u32x4*)((unsigned char*)red + wofs) + lane;
   auto load_w = [&](int s, int u) {
     const int kc = min(kc0 + cw + NCW * s, klast);
-    if (wlds) {
+    if (wofs) {
       // staged in LDS by the stage before the last ((row block, k-step) order)
 #pragma unroll
       for (int r = 0; r < RB; ++r) wq[u][r] = wl[(min(r, nrb - 1) * nk + (kc - kc0)) * 64];
@@ -884,16 +885,16 @@ template <int NT>
 __device__ __forceinline__ bool gemm_task(const FusedArgs& a, const Wg& w, const WaitSpec& ws, int epi, int l,
                                           const int* rbs, int rb_first, int nrb, gptr<uint16_t> bias,
                                           gptr<u32x4> Wp, int KC, int M, int kc0, int kc1, const uint16_t* act,
-                                          int act_kc, float* red, const PreSpec& ps, bool wlds = false) {
+                                          int act_kc, float* red, const PreSpec& ps, int wofs = 0) {
   if (nrb <= 0) return pre_only(a, w, ps);
   if (nrb == 1)
     return gemm_rb<NT, 1, NT <= 2 ? 10 : 5>(a, w, ws, epi, l, rbs, rb_first, 1, bias, Wp, KC, M, kc0, kc1, act,
-                                           act_kc, red, ps, wlds);
+                                           act_kc, red, ps, wofs);
   if (nrb == 2)
     return gemm_rb<NT, 2, NT <= 2 ? 10 : 5>(a, w, ws, epi, l, rbs, rb_first, 2, bias, Wp, KC, M, kc0, kc1, act,
-                                           act_kc, red, ps, wlds);
+                                           act_kc, red, ps, wofs);
   return gemm_rb<NT, 4, NT <= 2 ? 5 : 3>(a, w, ws, epi, l, rbs, rb_first, nrb, bias, Wp, KC, M, kc0, kc1, act,
-                                         act_kc, red, ps, wlds);
+                                         act_kc, red, ps, wofs);
 }
 
 // ------------------------------------------------------------------ tree attention
@@ -1281,6 +1282,10 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
   // LayerNorm) when they fit.  The up-projection's closing wait covers the
   // copy; with one tile that stage is too short to hide it.
   const bool wpr_staged = NT >= 2 && n_wpr > 0 && n_wpr * (kf1 - kf0) <= WST_FRAGS;
+  // likewise the out-projection's weights during LN1 + QKV, above the
+  // parameter table (the attention stage between uses the LDS below it)
+  const int wo_ofs = A_REGION + A_PART_BYTES + A_Q_BYTES + 256 + L * kLwSlots * 8;
+  const bool wo_staged = NT >= 2 && n_wo > 0 && n_wo * (kh1 - kh0) <= WO_FRAGS;
   const int nst = L * 8 + 2;
   for (int st = 0; st < nst; ++st) {
     const int l = st < L * 8 ? st / 8 : L;
@@ -1318,10 +1323,11 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
       const WaitSpec ws{wo ? FS_ATT : FS_FC, w.x, tag_of(w, l, wo ? FS_ATT : FS_FC), true, l, fid};
       PreSpec nopre{};
       const bool ok = wo ? gemm_task<NT>(a, w, ws, FE_WO, l, p + PL_WO + 1, 0, n_wo, G<uint16_t>(nullptr),
-                                         G<u32x4>(lw(w, l, LW_O)), KCd, d, kh0, kh1, a.fo, KCd, red, nopre)
+                                         G<u32x4>(lw(w, l, LW_O)), KCd, d, kh0, kh1, a.fo, KCd, red, nopre,
+                                         wo_staged ? wo_ofs : 0)
                          : gemm_task<NT>(a, w, ws, FE_WPR, l, p + PL_WPR + 1, 0, n_wpr, G<uint16_t>(nullptr),
                                          G<u32x4>(lw(w, l, LW_PR)), KCm, d, kf0, kf1, a.ff, KCm, red, nopre,
-                                         wpr_staged);
+                                         wpr_staged ? WST : 0);
       if (!ok) goto out;
       signal(a, w, l, fid, true);
       stamp(a, w, l, fid, 2);
@@ -1341,6 +1347,7 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
         ps.wk0 = kf0;
         ps.wk1 = kf1;
         ps.wKC = KCm;
+        ps.wdst = WST;
         ps.wrbs = p + PL_WPR + 1;
         ps.wW = G<u32x4>(lw(w, l, LW_PR));
       }
@@ -1352,6 +1359,15 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
       ps.b = G<uint16_t>(lw(w, l, LN2B));
       ps.act = act2;
     } else {
+      if (kind == 0 && wo_staged) {
+        ps.wn = n_wo;
+        ps.wk0 = kh0;
+        ps.wk1 = kh1;
+        ps.wKC = KCd;
+        ps.wdst = wo_ofs;
+        ps.wrbs = p + PL_WO + 1;
+        ps.wW = G<u32x4>(lw(w, l, LW_O));
+      }
       const int lp = kind == 8 ? L - 1 : max(l - 1, 0);
       ps.ws = WaitSpec{FS_WPR, -1, tag_of(w, lp, FS_WPR), kind == 8 || l > 0, l, FS_LN1};
       ps.bias = G<uint16_t>(lw(w, lp, LB_PR));
@@ -1535,7 +1551,7 @@ bool fused_plan(int H, int d, int M, int V, int ntiles, int* tab, int* xh, int* 
 }
 
 hipError_t fused_prepare() {
-  const int lds = (int)fused_lds_bytes();
+  const int lds = (int)fused_lds_bytes(kFMaxL);
   hipError_t e = hipFuncSetAttribute((const void*)fz::pass_kernel<1>, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
   if (e == hipSuccess)
     e = hipFuncSetAttribute((const void*)fz::pass_kernel<2>, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
@@ -1544,14 +1560,20 @@ hipError_t fused_prepare() {
   return e;
 }
 
-size_t fused_lds_bytes() {
-  return fz::A_REGION + fz::A_PART_BYTES + fz::A_Q_BYTES + 128 + kPlanStride * 4 + (size_t)kFMaxL * kLwSlots * 8;
+// attention / GEMM regions, shared words, plan row, the layers' parameter
+// pointers, the out-projection's staged weights
+size_t fused_lds_bytes(int L) {
+  return fz::A_REGION + fz::A_PART_BYTES + fz::A_Q_BYTES + 128 + kPlanStride * 4 + (size_t)L * kLwSlots * 8 +
+         fz::WO_FRAGS * 1024;
 }
+static_assert(fz::A_REGION + fz::A_PART_BYTES + fz::A_Q_BYTES + 128 + kPlanStride * 4 + kFMaxL * kLwSlots * 8 +
+                      fz::WO_FRAGS * 1024 <= 160 * 1024,
+              "the persistent pass's LDS must fit a gfx950 workgroup (160 KB)");
 
 hipError_t launch_fused(const FusedArgs& a, hipStream_t s) {
   if (a.N <= 0 || a.N > kFMaxN || a.d % 32 || a.M % 32 || a.d > 2048 || a.H * fz::DH != a.d) return hipErrorInvalidValue;
   const int nt = (a.N + 15) / 16;
-  const size_t lds = fused_lds_bytes();
+  const size_t lds = fused_lds_bytes(a.L);
   const dim3 grid(kFGroups);
   switch (nt) {
     case 1: fz::pass_kernel<1><<<grid, fz::NTH, lds, s>>>(a); break;

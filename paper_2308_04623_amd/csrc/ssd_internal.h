@@ -236,7 +236,7 @@ struct FusedArgs {
 // tab receives [kFGroups][kPlanStride]; false (with a reason) if the shape
 // does not fit the plan's limits.
 bool fused_plan(int H, int d, int M, int V, int ntiles, int* tab, int* xh, int* xf, std::string* why);
-size_t fused_lds_bytes();
+size_t fused_lds_bytes(int L);
 // raises the kernels' dynamic LDS limit (once per process, before the first launch)
 hipError_t fused_prepare();
 hipError_t launch_fused(const FusedArgs& a, hipStream_t s);
