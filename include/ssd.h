@@ -231,8 +231,9 @@ ssd_status ssd_set_weight_prefetch(int32_t on);
 /* How a bfloat16 verification pass runs (Sec. 2.1: a decode step streams
  * every weight once; Sec. 3.1: one step scores the whole tree).
  *   0 (default) = automatic: the persistent single launch when the session
- *     supports it (head dimension 64, a 256-CU device with 8 XCDs) and the
- *     tree has at most 64 nodes, else one kernel per sub-layer;
+ *     supports it (head dimension 64, a 256-CU device with 8 XCDs, a cache
+ *     of at most 16128 positions) and the tree has at most 64 nodes, else
+ *     one kernel per sub-layer;
  *   1 = always one kernel per sub-layer;
  *   2 = the persistent single launch only (up to 64 nodes):
  *     ssd_tree_verify and ssd_graph_capture_verify return SSD_E_UNSUPPORTED

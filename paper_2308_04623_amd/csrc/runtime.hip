@@ -396,6 +396,8 @@ static ssd_status fused_setup(ssd_kv* kv) {
   const size_t o_a1 = take(kFXcd * act_stride * 2), o_a2 = take(kFXcd * act_stride * 2);
   const size_t o_fo = take((size_t)kFMaxN * d * 2), o_ff = take((size_t)kFMaxN * M * 2);
   const size_t att_parts = (size_t)(kv->max_ctx + kFAttRows - 1) / kFAttRows + 1;
+  // (one wave reads a tile's unit flags: at most 64 parts)
+  if (att_parts > 64) return SSD_OK;
   const size_t o_ap = take((size_t)c.n_head * 4 * att_parts * 16 * 68 * 4);
   const size_t o_po = take((size_t)kFXcd * kFMaxN * d * 4), o_pp = take((size_t)kFXcd * kFMaxN * d * 4);
   const size_t o_fl = take((size_t)kFStages * kFGroups * 4), o_ctl = take((size_t)kFCtlWords * 4);

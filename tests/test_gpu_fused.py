@@ -227,3 +227,18 @@ def test_fused_only_mode_rejects_unsupported(small, ssd, torch):
     finally:
         ssd.set_pass_mode(ssd.PASS_AUTO)
     s.close()
+
+
+@pytest.mark.gpu
+def test_fused_cache_length_limit(small, ssd, torch):
+    # A tile's unit flags are read by one 64-lane wave: the persistent pass
+    # takes caches of at most 63 prefix units of 256 rows (plus the root
+    # unit); a longer cache keeps the per-sub-layer kernels.
+    t = small
+    paths = []
+    for max_ctx in (63 * 256, 63 * 256 + 1):
+        kc, vc = W.random_kv_cache(t.cfg, max_ctx, 8, seed=5)
+        s = ssd.Session(t.m, max_ctx, 4, ssd.to_device(kc, t.cfg), ssd.to_device(vc, t.cfg))
+        paths.append(s.verify_path(1))
+        s.close()
+    assert paths == [ssd.PASS_FUSED, ssd.PASS_KERNELS]
