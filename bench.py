@@ -266,8 +266,8 @@ def main():
         write_traffic(args.traffic_from[0], args.traffic_from[1], args.nodes, not args.kernels_path)
         return
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for {args.gpus}): this build has no multi-GPU path; "
-              "the pass would shard by tensor parallelism, see DESIGN.md", file=sys.stderr)
+        print(f"bench.py runs on one GPU only (asked for {args.gpus}): the library has no multi-GPU path "
+              "(a pass would shard its heads and MLP slices over GPUs by tensor parallelism)", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
