@@ -22,6 +22,15 @@
 //    XCDs: every XCD adds the eight partials of a node row itself, in XCD
 //    order, into its own copy of the residual stream, so all copies agree
 //    bit for bit.  Every other hand-off stays inside one XCD's L2.
+//  * Inside a workgroup (8 waves): waves 4..7 run a stage's GEMM and issue
+//    their first weight loads before its dependency is met; waves 0..3 run
+//    the LayerNorm rows of the stage before it, and then wave 0 alone polls
+//    for the dependency.  A CU returns vector loads in issue order, across
+//    its waves, so the polling wave keeps nothing of its own in flight; a
+//    poll still waits behind the other waves' loads.  With two or more node
+//    tiles, waves 1..3 also copy into LDS the weights of a GEMM two stages
+//    on: the out-projection's during LN1 + QKV, and the down-projection's
+//    during the up-projection.
 //  * Hand-offs are per-workgroup stage flags carrying a monotonically
 //    increasing tag (pass, layer, stage).  A workgroup writes its outputs,
 //    waits for its stores, then stores its flag; consumers poll the 32 flags
