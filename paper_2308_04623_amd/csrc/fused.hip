@@ -877,7 +877,8 @@ __device__ __forceinline__ bool gemm_rb(const FusedArgs& a, const Wg& w, const W
 
 // one task of 1..4 row blocks, loads in flight per wave sized to the
 // register budget (at four tiles one row block keeps 8 steps in flight and
-// two keep 6: deeper would spill); three code bodies serve every stage
+// two keep 6; four row blocks keep 8 at one tile, 5 at two, 3 at four: deeper
+// would spill); three code bodies serve every stage
 // Runs the pre-stage (wave 0) when the workgroup has no GEMM task.
 __device__ __forceinline__ bool pre_only(const FusedArgs& a, const Wg& w, const PreSpec& ps) {
   if (ps.kind == 0) return true;
@@ -903,7 +904,7 @@ __device__ __forceinline__ bool gemm_task(const FusedArgs& a, const Wg& w, const
   if (nrb == 2)
     return gemm_rb<NT, 2, NT <= 2 ? 10 : 6>(a, w, ws, epi, l, rbs, rb_first, 2, bias, Wp, KC, M, kc0, kc1, act,
                                            act_kc, red, ps, wofs);
-  return gemm_rb<NT, 4, NT <= 2 ? 5 : 3>(a, w, ws, epi, l, rbs, rb_first, nrb, bias, Wp, KC, M, kc0, kc1, act,
+  return gemm_rb<NT, 4, NT == 1 ? 8 : NT == 2 ? 5 : 3>(a, w, ws, epi, l, rbs, rb_first, nrb, bias, Wp, KC, M, kc0, kc1, act,
                                          act_kc, red, ps, wofs);
 }
 
