@@ -315,6 +315,11 @@ def main():
     torch.cuda.synchronize()
     ms_step = e0.elapsed_time(e1) / args.steps
     log(f"step {ms_step * 1e3:.1f} us")
+    # a persistent pass that ended early (its logits undefined) or a float16
+    # overflow counts here: the timing is only valid if none happened
+    errs = sess.error_count()
+    if errs:
+        raise SystemExit(f"the session's error counter is {errs} after the timed steps: results invalid")
 
     def time_graph(g, reps):
         for _ in range(5):

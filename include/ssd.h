@@ -163,12 +163,16 @@ ssd_status ssd_tree_accept(ssd_kv *kv, const ssd_tree *tree, const float *draft_
  * written by ssd_tree_accept) to cache rows prefix_len.. (Sec. 3.1).  Reads
  * the path on the device, so no host sync is needed between accept and
  * commit.  Rows that would fall past max_ctx, or path entries outside
- * [0, max_nodes), are skipped and counted; ssd_kv_error_count reports them. */
+ * [0, max_nodes), are skipped and counted in the session's error counter. */
 ssd_status ssd_kv_commit(ssd_kv *kv, int32_t prefix_len, const int32_t *accepted_path, const int32_t *path_len,
                          void *stream);
 
-/* Number of commit rows skipped as out of range since the session began
- * (synchronises the stream). */
+/* The session's error counter since it began (synchronises the stream): it
+ * counts commit rows skipped as out of range, persistent verification passes
+ * that ended early (a bounded wait timed out, or the launch did not get one
+ * workgroup per CU; that pass's logits are undefined) and GEMM inputs that
+ * overflowed float16 (see ssd_tree_verify).  A caller that needs a valid
+ * result checks that it did not grow. */
 ssd_status ssd_kv_error_count(ssd_kv *kv, void *stream, uint32_t *count);
 
 /* Top-k of every row of logits[n_rows][vocab] (vocab of kv's model), for
@@ -194,14 +198,6 @@ ssd_status ssd_graph_capture_verify(const ssd_model *m, ssd_kv *kv, int32_t pref
 ssd_status ssd_graph_launch(ssd_graph *g, void *stream);
 void ssd_graph_destroy(ssd_graph *g);
 
-/* Launches one weight GEMM of the verification pass on its own, exactly as
- * the pass launches it, for measurement: which = 0 QKV, 1 attention output,
- * 2 MLP up (FC + GELU), 3 MLP down; layer in [0, n_layer).  Reads and writes
- * only the session's workspaces and tree scratch (never the cache or caller
- * buffers), so results are meaningless outside a pass. */
-ssd_status ssd_launch_gemm(const ssd_model *m, ssd_kv *kv, int32_t which, int32_t layer, int32_t n_nodes,
-                           void *stream);
-
 /* Host-only tree checks (no GPU needed).  Validates topology and token ids;
  * writes the maximum depth. */
 ssd_status ssd_validate_tree(const int32_t *tokens, const int32_t *parent_idx, int32_t n, int32_t vocab,
@@ -212,74 +208,44 @@ ssd_status ssd_validate_tree(const int32_t *tokens, const int32_t *parent_idx, i
  * is set iff node j is node i or one of its ancestors). */
 ssd_status ssd_tree_prep(const int32_t *parent_idx, int32_t n, int32_t *depth, uint64_t *anc);
 
-/* Verification-pass GEMM path: 0 = automatic (by node count), 1 = vector
- * ALU, 2 = matrix cores.  Process-wide; bfloat16 models only. */
-ssd_status ssd_set_gemm_path(int32_t path);
+/* Per-session switches (each session has its own; the defaults are 0, 0, 1).
+ *   pass_mode: how a bfloat16 verification pass runs (Sec. 2.1: a decode
+ *     step streams every weight once; Sec. 3.1: one step scores the whole
+ *     tree).
+ *     0 = automatic: the persistent single launch when the session supports
+ *       it (head dimension 64, a 256-CU device with 8 XCDs, a cache of at
+ *       most 16128 positions) and the tree has at most 64 nodes, else one
+ *       kernel per sub-layer;
+ *     1 = always one kernel per sub-layer;
+ *     2 = the persistent single launch only (up to 64 nodes):
+ *       ssd_tree_verify and ssd_graph_capture_verify return SSD_E_UNSUPPORTED
+ *       where it does not apply.
+ *     The persistent launch runs every layer in one kernel: 256 workgroups
+ *     (one per CU) hand results to each other through flags in device
+ *     memory.  Every wait inside it is bounded; if one times out (200 ms) the
+ *     launch ends early, its logits are undefined, and the session's error
+ *     counter (ssd_kv_error_count) is incremented.  Both ways meet the same
+ *     tolerance against the definition; their logits differ in the last bits.
+ *   gemm_path: the per-sub-layer kernels' weight GEMMs, bfloat16 models
+ *     only: 0 = automatic (by node count), 1 = vector ALU, 2 = matrix cores.
+ *   weight_prefetch: 1 = every per-sub-layer bfloat16 pass the session
+ *     enqueues (or a graph of it replays) gets a prefetcher kernel on a
+ *     stream of the session's own; it follows progress signals the pass's
+ *     kernels raise and loads each weight GEMM's fragments into the L2 of the
+ *     XCD whose workgroups will read them, a few kernels ahead.  The pass
+ *     never waits for it; it stops waiting for signals 50 ms after it starts.
+ *     0 = off.  Results are bitwise the same either way.  ssd_kv_destroy
+ *     waits for the session's prefetchers.
+ * A captured graph keeps the pass mode and GEMM path in force when it was
+ * captured.  Errors: SSD_E_INVALID_ARG (null, or a value out of range). */
+typedef struct {
+  int32_t pass_mode;
+  int32_t gemm_path;
+  int32_t weight_prefetch;
+} ssd_options;
 
-/* Weight prefetch beside each pass: 1 (default) = every bfloat16 pass that
- * ssd_tree_verify enqueues, or that ssd_graph_launch replays, gets a
- * prefetcher kernel on a stream of the session's own; it follows progress
- * signals the pass's kernels raise and loads each weight GEMM's fragments
- * into the L2 of the XCD whose workgroups will read them, a few kernels
- * ahead.  The pass never waits for it; it stops waiting for signals 50 ms
- * after it starts.  0 = off.  Results are bitwise the same either way; process-wide.
- * ssd_kv_destroy waits for the session's prefetchers; the model must outlive
- * its sessions' pending passes as always.  Errors: SSD_E_INVALID_ARG (not 0
- * or 1). */
-ssd_status ssd_set_weight_prefetch(int32_t on);
-
-/* How a bfloat16 verification pass runs (Sec. 2.1: a decode step streams
- * every weight once; Sec. 3.1: one step scores the whole tree).
- *   0 (default) = automatic: the persistent single launch when the session
- *     supports it (head dimension 64, a 256-CU device with 8 XCDs, a cache
- *     of at most 16128 positions) and the tree has at most 64 nodes, else
- *     one kernel per sub-layer;
- *   1 = always one kernel per sub-layer;
- *   2 = the persistent single launch only (up to 64 nodes):
- *     ssd_tree_verify and ssd_graph_capture_verify return SSD_E_UNSUPPORTED
- *     where it does not apply.
- * The persistent launch runs every layer in one kernel: 256 workgroups (one
- * per CU) hand results to each other through flags in device memory.  Every
- * wait inside it is bounded; if one times out (200 ms) the
- * launch ends early, its logits are undefined, and the session's error
- * counter (ssd_kv_error_count) is incremented.  Both ways meet the same
- * tolerance against the definition; their logits differ in the last bits.
- * Process-wide.  Errors: SSD_E_INVALID_ARG (mode not 0, 1 or 2). */
-ssd_status ssd_set_pass_mode(int32_t mode);
-
-/* Host-only: which way ssd_tree_verify would run a pass of n nodes of the
- * model on this session under the current pass mode: *path = 1 (one kernel
- * per sub-layer) or 2 (the persistent single launch).  Errors:
- * SSD_E_INVALID_ARG (null pointer, n outside [1, max_nodes]). */
-ssd_status ssd_verify_path(const ssd_model *m, const ssd_kv *kv, int32_t n, int32_t *path);
-
-/* Host-only: the persistent launch's work split for a model shape and a
- * count of 16-node tiles (1..4), as the session computes it.  tab receives
- * [256][32] int32 rows, one per compute workgroup (XCD x, rank r at row
- * 32 x + r): [0] the rank's position in the order its XCD's attention units
- * are dealt in (unit u goes to position u mod 32); [9] QKV row blocks, then
- * up to 4 row-block indices of W_qkv; [14] the same
- * for W_o; [19] for W_fc; [24] for W_pr; [29], [30] the workgroup's range of
- * LM-head row blocks.  xh[2x], xh[2x+1] bound XCD x's heads; xf[2x], xf[2x+1]
- * its hidden features in units of 32.  Errors: SSD_E_INVALID_ARG (null
- * pointer), SSD_E_UNSUPPORTED (the shape does not fit the split: head
- * dimension not 64, or too many units for a workgroup). */
-ssd_status ssd_fused_plan(int32_t n_head, int32_t d_model, int32_t d_mlp, int32_t vocab, int32_t n_tiles,
-                          int32_t *tab, int32_t *xh, int32_t *xf);
-
-/* Stage timestamps of the persistent launch, for profiling.  With buf not
- * NULL, every later persistent pass of this session records for compute
- * workgroup g (XCD x, rank r: g = 32 x + r), layer l (n_layer + 1 rows; row
- * n_layer holds the final LayerNorm in stage 0 and the LM head in stage 1)
- * and stage s (8 per layer: LayerNorm, QKV, attention, out-projection,
- * LayerNorm, MLP up, MLP down, unused) three s_memrealtime readings (100 MHz):
- * stage entry, dependency met, stage published, at
- * buf[((g * (n_layer + 1) + l) * 8 + s) * 3 + k].  buf is caller-owned device
- * memory of 256 * (n_layer + 1) * 24 uint64 words for the largest model the
- * session runs; stages a workgroup skips keep old values.  NULL stops
- * recording.  Errors: SSD_E_INVALID_ARG (null session), SSD_E_UNSUPPORTED
- * (the session has no persistent pass). */
-ssd_status ssd_kv_set_trace(ssd_kv *kv, uint64_t *buf);
+ssd_status ssd_kv_set_options(ssd_kv *kv, const ssd_options *opt);
+ssd_status ssd_kv_get_options(const ssd_kv *kv, ssd_options *opt);
 
 const char *ssd_status_string(ssd_status s);
 const char *ssd_last_error(void);

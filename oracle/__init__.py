@@ -8,6 +8,7 @@ All arrays are numpy host arrays.  Parameters and K/V are float32 or uint16
 """
 from __future__ import annotations
 
+import contextlib
 import ctypes as C
 import os
 import subprocess
@@ -59,29 +60,66 @@ class _Weights(C.Structure):
 _lib = None
 
 
+def _bind(L):
+    i32p = C.POINTER(C.c_int32)
+    L.ssdref_tree_info.argtypes = [i32p, C.c_int32, i32p, C.POINTER(C.c_uint8)]
+    L.ssdref_tree_verify.argtypes = [C.POINTER(_Config), C.POINTER(_Weights), C.c_void_p, C.c_void_p,
+                                     C.c_int32, C.c_int32, i32p, i32p, C.c_int32, C.c_void_p, C.c_void_p,
+                                     C.c_int32, C.POINTER(C.c_float), C.c_int32]
+    L.ssdref_kv_commit.argtypes = [C.POINTER(_Config), C.c_void_p, C.c_void_p, C.c_int32, C.c_int32,
+                                   C.c_void_p, C.c_void_p, C.c_int32, i32p, C.c_int32]
+    L.ssdref_tree_accept.argtypes = [C.c_int32, i32p, i32p, C.c_int32, C.c_int32, C.POINTER(C.c_float),
+                                     C.POINTER(C.c_float), C.c_double, C.c_uint64, i32p, i32p, i32p]
+    L.ssdref_philox4x64_10.argtypes = [C.POINTER(C.c_uint64), C.POINTER(C.c_uint64), C.POINTER(C.c_uint64)]
+    L.ssdref_philox4x64_10.restype = None
+    L.ssdref_uniform.argtypes = [C.c_uint64, C.c_uint64, C.c_uint64]
+    L.ssdref_uniform.restype = C.c_double
+    L.ssdref_round_bf16.argtypes = [C.c_double]
+    L.ssdref_round_bf16.restype = C.c_uint16
+    return L
+
+
 def lib():
     global _lib
     if _lib is None:
         if not os.path.exists(_SO):
             build()
-        L = C.CDLL(_SO)
-        i32p = C.POINTER(C.c_int32)
-        L.ssdref_tree_info.argtypes = [i32p, C.c_int32, i32p, C.POINTER(C.c_uint8)]
-        L.ssdref_tree_verify.argtypes = [C.POINTER(_Config), C.POINTER(_Weights), C.c_void_p, C.c_void_p,
-                                         C.c_int32, C.c_int32, i32p, i32p, C.c_int32, C.c_void_p, C.c_void_p,
-                                         C.c_int32, C.POINTER(C.c_float), C.c_int32]
-        L.ssdref_kv_commit.argtypes = [C.POINTER(_Config), C.c_void_p, C.c_void_p, C.c_int32, C.c_int32,
-                                       C.c_void_p, C.c_void_p, C.c_int32, i32p, C.c_int32]
-        L.ssdref_tree_accept.argtypes = [C.c_int32, i32p, i32p, C.c_int32, C.c_int32, C.POINTER(C.c_float),
-                                         C.POINTER(C.c_float), C.c_double, C.c_uint64, i32p, i32p, i32p]
-        L.ssdref_philox4x64_10.argtypes = [C.POINTER(C.c_uint64), C.POINTER(C.c_uint64), C.POINTER(C.c_uint64)]
-        L.ssdref_philox4x64_10.restype = None
-        L.ssdref_uniform.argtypes = [C.c_uint64, C.c_uint64, C.c_uint64]
-        L.ssdref_uniform.restype = C.c_double
-        L.ssdref_round_bf16.argtypes = [C.c_double]
-        L.ssdref_round_bf16.restype = C.c_uint16
-        _lib = L
+        _lib = _bind(C.CDLL(_SO))
     return _lib
+
+
+def build_variant(replacements: Sequence[Tuple[str, str]], out_dir: str) -> str:
+    """Compiles a copy of ssdref.c with textual replacements (each must occur
+    exactly once) into out_dir; returns the library path.  Used by the power
+    checks of the pins, which plant a mistake in a copy and expect the pin to
+    fail on it."""
+    src = open(_SRC).read()
+    for old, new in replacements:
+        if src.count(old) != 1:
+            raise ValueError(f"replacement target occurs {src.count(old)} times: {old!r}")
+        src = src.replace(old, new)
+    os.makedirs(out_dir, exist_ok=True)
+    c_path = os.path.join(out_dir, "ssdref_variant.c")
+    so_path = os.path.join(out_dir, "libssdref_variant.so")
+    with open(c_path, "w") as f:
+        f.write(src)
+    cmd = [a for a in GCC_CMD]
+    cmd[cmd.index(_SO)] = so_path
+    cmd[cmd.index(_SRC)] = c_path
+    subprocess.run(cmd + ["-I", _HERE], check=True)
+    return so_path
+
+
+@contextlib.contextmanager
+def variant(so_path: str):
+    """Oracle calls inside the block run on another build of ssdref.c."""
+    global _lib
+    prev = lib()
+    _lib = _bind(C.CDLL(so_path))
+    try:
+        yield
+    finally:
+        _lib = prev
 
 
 def _i32(a) -> np.ndarray:

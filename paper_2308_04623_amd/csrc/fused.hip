@@ -98,20 +98,28 @@ __device__ __forceinline__ unsigned long long now() { return __builtin_amdgcn_s_
 
 // float16 GEMM input in matrix-core fragment order (ld = k-steps of 32 per
 // 16-node tile): element (n, k) in fragment (n/16) ld + k/32, lane
-// (n%16) + 16 ((k%32)/8), position k%8
-__device__ __forceinline__ void st_act(uint16_t* p, int n, int k, int ld, float v) {
-  const size_t f = (size_t)(n >> 4) * ld + (k >> 5);
-  p[f * 512 + ((n & 15) + 16 * ((k & 31) >> 3)) * 8 + (k & 7)] = __builtin_bit_cast(uint16_t, (_Float16)v);
+// (n%16) + 16 ((k%32)/8), position k%8.  A value past float16's range
+// (|v| > 65504, or NaN) would enter the matrix cores as inf or NaN: it is
+// counted in err (the session's error counter) and stored as converted.
+// (one count per wave and call: the lowest lane out of range adds 1)
+__device__ __forceinline__ void f16_range(float v, unsigned* err) {
+  const bool over = !(fabsf(v) <= 65504.f);
+  const unsigned long long m = __builtin_amdgcn_ballot_w64(over);
+  if (m && (int)__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u)) == __builtin_ctzll(m))
+    __hip_atomic_fetch_add(err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-__device__ __forceinline__ void st_act(gw<uint16_t> p, int n, int k, int ld, float v) {
+__device__ __forceinline__ void st_act(gw<uint16_t> p, int n, int k, int ld, float v, unsigned* err) {
   const size_t f = (size_t)(n >> 4) * ld + (k >> 5);
+  f16_range(v, err);
   p[f * 512 + ((n & 15) + 16 * ((k & 31) >> 3)) * 8 + (k & 7)] = __builtin_bit_cast(uint16_t, (_Float16)v);
 }
 
 // four consecutive elements (n, k .. k+3), k % 4 == 0: one 8-byte store
-__device__ __forceinline__ void st_act4(gw<uint16_t> p, int n, int k, int ld, float v0, float v1, float v2, float v3) {
+__device__ __forceinline__ void st_act4(gw<uint16_t> p, int n, int k, int ld, float v0, float v1, float v2, float v3,
+                                        unsigned* err) {
   const size_t f = (size_t)(n >> 4) * ld + (k >> 5);
+  f16_range(fmaxf(fmaxf(fabsf(v0), fabsf(v1)), fmaxf(fabsf(v2), fabsf(v3))) + (v0 + v1 + v2 + v3) * 0.f, err);
   const uint32_t lo = (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)v0) |
                       ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)v1) << 16);
   const uint32_t hi = (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)v2) |
@@ -559,7 +567,7 @@ __device__ __forceinline__ bool ln_rows_q(const FusedArgs& a, const Wg& w, const
       if (c < nc) {
         const f32x4 gv = bf4(gr[i]), bv = bf4(br[i]);
         const f32x4 y = (v[j][i] - mean[j]) * rden * gv + bv;
-        st_act4(actg, nr[j], 4 * c, d / 32, y[0], y[1], y[2], y[3]);
+        st_act4(actg, nr[j], 4 * c, d / 32, y[0], y[1], y[2], y[3], a.err);
       }
     }
   }
@@ -607,8 +615,8 @@ __device__ __forceinline__ void merge_tile(const FusedArgs& a, int h, int t) {
   const int n = 16 * t + nl;
   if (n < a.N) {
     const gw<uint16_t> fo = opq(a.fo);
-    st_act(fo, n, h * DH + d0, a.d / 32, O0 / Ls);
-    st_act(fo, n, h * DH + d0 + 1, a.d / 32, O1 / Ls);
+    st_act(fo, n, h * DH + d0, a.d / 32, O0 / Ls, a.err);
+    st_act(fo, n, h * DH + d0 + 1, a.d / 32, O1 / Ls, a.err);
   }
 }
 
@@ -627,7 +635,11 @@ __device__ __forceinline__ void unit_done(const FusedArgs& a, const Wg& w, int l
     if (lane == 0) __hip_atomic_store(uf + j, tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     const unsigned v = ld_flag(uf + min(lane, a.att_units));  // (clamped: the row holds att_units + 1 flags)
-    const bool mine = lane > a.att_units || tag_reached(v, tag);
+    // equality, not "reached": a unit flag is written only when its unit
+    // exists, so a flag unused for a long time may hold any older tag, and
+    // tags wrap; when this check runs no unit of the tile can hold a later
+    // tag, so equality is exact
+    const bool mine = lane > a.att_units || v == tag;
     if (lane == 0) w.sh[6] = __all(mine);
   }
   lds_barrier();
@@ -725,7 +737,7 @@ __device__ __forceinline__ void epilogue(const FusedArgs& a, const Wg& w, int ep
       }
       break;
     case FE_WO: st_dev(a.part_o + ((size_t)w.x * kFMaxN + n) * d + o, v); break;
-    case FE_FC: st_act(a.ff, n, o, a.M / 32, gelu_tanh(v)); break;
+    case FE_FC: st_act(opq(a.ff), n, o, a.M / 32, gelu_tanh(v), a.err); break;
     case FE_WPR: st_dev(a.part_p + ((size_t)w.x * kFMaxN + n) * d + o, v); break;
     default: a.logits[(size_t)n * a.V + o] = v; break;
   }

@@ -56,12 +56,19 @@ template <> __device__ __forceinline__ void stT<uint16_t>(uint16_t* p, size_t i,
 // f = (n/16) * ld + k/32 (ld = K/32), lane (n%16) + 16 ((k%32)/8), position
 // k%8.  The weights are multiplied as float16 too: their packed copies are
 // the bf16 values converted exactly (see pack_kernel).
-template <typename T> __device__ __forceinline__ void st_act(T* p, int n, int k, int ld, float v);
-template <> __device__ __forceinline__ void st_act<float>(float* p, int n, int k, int ld, float v) {
+// A float16 operand past the type's range (|v| > 65504, or NaN) would enter
+// the matrix cores as inf or NaN: such an element is counted in err (the
+// session's error counter) and stored as converted.
+template <typename T> __device__ __forceinline__ void st_act(T* p, int n, int k, int ld, float v, unsigned* err);
+template <> __device__ __forceinline__ void st_act<float>(float* p, int n, int k, int ld, float v, unsigned*) {
   p[(size_t)n * ld + k] = v;
 }
-template <> __device__ __forceinline__ void st_act<uint16_t>(uint16_t* p, int n, int k, int ld, float v) {
+template <>
+__device__ __forceinline__ void st_act<uint16_t>(uint16_t* p, int n, int k, int ld, float v, unsigned* err) {
   const size_t f = (size_t)(n >> 4) * ld + (k >> 5);
+  // (one count per wave and call: the lowest lane out of range adds 1)
+  const unsigned long long m = __builtin_amdgcn_ballot_w64(!(fabsf(v) <= 65504.f));
+  if (m && err && (int)__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u)) == __builtin_ctzll(m)) atomicAdd(err, 1u);
   p[f * 512 + ((n & 15) + 16 * ((k & 31) >> 3)) * 8 + (k & 7)] = __builtin_bit_cast(uint16_t, (_Float16)v);
 }
 __device__ __forceinline__ float h2f(uint16_t h) { return (float)__builtin_bit_cast(_Float16, h); }
@@ -149,7 +156,8 @@ template <typename T, typename OUT, int E, int SPL>
 __global__ __launch_bounds__(256) void ln_resid_kernel(float* __restrict__ x, int d, const float* __restrict__ part,
                                                        int S, size_t pstride, const T* __restrict__ bias,
                                                        const T* __restrict__ g, const T* __restrict__ b, float eps,
-                                                       OUT* __restrict__ a, int lda, unsigned long long* sig) {
+                                                       OUT* __restrict__ a, int lda, unsigned long long* sig,
+                                                       unsigned* err) {
   constexpr int PS = SPL > 0 ? SPL : 1;
   __shared__ float red[4];
   pass_signal(sig);
@@ -199,40 +207,40 @@ __global__ __launch_bounds__(256) void ln_resid_kernel(float* __restrict__ x, in
 #pragma unroll
   for (int i = 0; i < E; ++i) {
     const int k = tid + i * 256;
-    if (k < d) st_act(a, n, k, lda, (v[i] - mean) / den * ldT(gw, i) + ldT(bw, i));
+    if (k < d) st_act(a, n, k, lda, (v[i] - mean) / den * ldT(gw, i) + ldT(bw, i), err);
   }
 }
 
 template <typename T, int E, int SPL>
 static void ln_go(float* x, int N, int d, const float* part, int S, size_t pstride, const void* bias, const void* g,
-                  const void* b, float eps, void* a, int lda, unsigned long long* sig, hipStream_t s) {
+                  const void* b, float eps, void* a, int lda, unsigned long long* sig, unsigned* err, hipStream_t s) {
   ln_resid_kernel<T, T, E, SPL><<<N, 256, 0, s>>>(x, d, part, S, pstride, (const T*)bias, (const T*)g, (const T*)b,
-                                                  eps, (T*)a, lda, sig);
+                                                  eps, (T*)a, lda, sig, err);
 }
 
 template <typename T, int E>
 static void ln_go_s(float* x, int N, int d, const float* part, int S, size_t pstride, const void* bias,
                     const void* g, const void* b, float eps, void* a, int lda, unsigned long long* sig,
-                    hipStream_t s) {
-  if (S == 0) ln_go<T, E, 0>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, s);
-  else if (S == 4) ln_go<T, E, 4>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, s);
-  else if (S == 8) ln_go<T, E, 8>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, s);
-  else ln_go<T, E, -1>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, s);
+                    unsigned* err, hipStream_t s) {
+  if (S == 0) ln_go<T, E, 0>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, err, s);
+  else if (S == 4) ln_go<T, E, 4>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, err, s);
+  else if (S == 8) ln_go<T, E, 8>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, err, s);
+  else ln_go<T, E, -1>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, err, s);
 }
 
 template <typename T>
 static hipError_t ln_go_e(float* x, int N, int d, const float* part, int S, size_t pstride, const void* bias,
                           const void* g, const void* b, float eps, void* a, int lda, unsigned long long* sig,
-                          hipStream_t s) {
+                          unsigned* err, hipStream_t s) {
   switch ((d + 255) / 256) {
-    case 1: ln_go_s<T, 1>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, s); break;
-    case 2: ln_go_s<T, 2>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, s); break;
-    case 3: ln_go_s<T, 3>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, s); break;
-    case 4: ln_go_s<T, 4>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, s); break;
-    case 5: ln_go_s<T, 5>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, s); break;
-    case 6: ln_go_s<T, 6>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, s); break;
-    case 7: ln_go_s<T, 7>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, s); break;
-    case 8: ln_go_s<T, 8>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, s); break;
+    case 1: ln_go_s<T, 1>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, err, s); break;
+    case 2: ln_go_s<T, 2>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, err, s); break;
+    case 3: ln_go_s<T, 3>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, err, s); break;
+    case 4: ln_go_s<T, 4>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, err, s); break;
+    case 5: ln_go_s<T, 5>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, err, s); break;
+    case 6: ln_go_s<T, 6>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, err, s); break;
+    case 7: ln_go_s<T, 7>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, err, s); break;
+    case 8: ln_go_s<T, 8>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, err, s); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -240,10 +248,10 @@ static hipError_t ln_go_e(float* x, int N, int d, const float* part, int S, size
 
 hipError_t launch_ln(int f32, float* x, int N, int d, const float* part, int S, size_t pstride, const void* bias,
                      const void* g, const void* b, float eps, void* a, int lda, unsigned long long* sig,
-                     hipStream_t s) {
+                     unsigned* err, hipStream_t s) {
   if (S > 0 && !bias) return hipErrorInvalidValue;
-  if (f32) return ln_go_e<float>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, s);
-  return ln_go_e<uint16_t>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, s);
+  if (f32) return ln_go_e<float>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, err, s);
+  return ln_go_e<uint16_t>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, err, s);
 }
 
 // ------------------------------------------------------------------ GEMM epilogues
@@ -268,7 +276,7 @@ __device__ __forceinline__ void epilogue(const Epi& e, int n, int o, float acc) 
   } else if (KIND == EPI_RESID) {
     e.x[(size_t)nn * e.d + o] += y;
   } else if (KIND == EPI_GELU) {
-    st_act((T*)e.out, nn, o, e.ldo, gelu_tanh(y));
+    st_act((T*)e.out, nn, o, e.ldo, gelu_tanh(y), e.err);
   } else {
     e.logits[(size_t)nn * e.ldl + o] = acc;
   }
@@ -306,7 +314,7 @@ hipError_t launch_gemm_f32(int kind, const float* W, int M, int K, const float* 
 size_t packed_bytes(int M, int K) { return (size_t)((M + 15) / 16) * (K / 32) * 1024; }
 
 __global__ __launch_bounds__(256) void pack_kernel(const uint16_t* __restrict__ W, int M, int K, int KC,
-                                                   size_t total, uint4* __restrict__ out) {
+                                                   size_t total, uint4* __restrict__ out, unsigned* __restrict__ bad) {
   const size_t idx = (size_t)blockIdx.x * 256 + threadIdx.x;
   if (idx >= total) return;
   const int lane = (int)(idx & 63);
@@ -317,15 +325,24 @@ __global__ __launch_bounds__(256) void pack_kernel(const uint16_t* __restrict__ 
   const int k = kc * 32 + 8 * (lane >> 4);
   u32x4 v = (u32x4){0, 0, 0, 0};
   if (row < M) v = *(const u32x4*)(W + (size_t)row * K + k);
-  // bf16 -> float16: exact for every weight of magnitude in [2^-24, 65504]
+  // bf16 -> float16, round to nearest even.  bf16 keeps 8 significant bits:
+  // the conversion is exact for 0 and every magnitude in [2^-17, 65504]
+  // (float16's subnormal spacing is 2^-24, so 8 significant bits need
+  // |w| >= 2^-17); below 2^-17 the error is at most 2^-25 per weight.
+  // Magnitudes past 65504 (or NaN) cannot be represented: they are counted
+  // in bad and the model is refused.
   const f32x8 f = __builtin_convertvector(__builtin_bit_cast(bf16x8, v), f32x8);
+  bool over = false;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) over |= !(fabsf(f[e]) <= 65504.f);
+  if (over) atomicAdd(bad, 1u);
   out[idx] = __builtin_bit_cast(uint4, __builtin_convertvector(f, f16x8));
 }
 
-hipError_t launch_pack_bf16(const uint16_t* W, int M, int K, void* out, hipStream_t s) {
+hipError_t launch_pack_bf16(const uint16_t* W, int M, int K, void* out, unsigned* bad, hipStream_t s) {
   const int KC = K / 32;
   const size_t total = (size_t)((M + 15) / 16) * KC * 64;
-  pack_kernel<<<(unsigned)((total + 255) / 256), 256, 0, s>>>(W, M, K, KC, total, (uint4*)out);
+  pack_kernel<<<(unsigned)((total + 255) / 256), 256, 0, s>>>(W, M, K, KC, total, (uint4*)out, bad);
   return hipGetLastError();
 }
 
@@ -856,7 +873,7 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnArgs a) {
     o = o * alpha + acc;
     m = mn;
   }
-  if (lane < DH) st_act((T*)a.out, n, h * DH + lane, a.ldo, o / l);
+  if (lane < DH) st_act((T*)a.out, n, h * DH + lane, a.ldo, o / l, a.err);
 }
 
 // ---- bf16 models: two kernels, the first on the matrix cores
@@ -1166,7 +1183,7 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
       M = mn;
     }
   }
-  st_act((uint16_t*)a.out, n, h * DH + dd, a.ldo, O / L);
+  st_act((uint16_t*)a.out, n, h * DH + dd, a.ldo, O / L, a.err);
 }
 
 hipError_t launch_attn(int f32, int DH, const AttnArgs& a, hipStream_t s) {

@@ -23,9 +23,6 @@ using namespace ssd;
 namespace {
 
 thread_local std::string g_last_error;
-int g_gemm_path = 0;  // 0 auto, 1 vector ALU, 2 matrix cores
-int g_prefetch = 1;   // warm each weight GEMM's L2 from the kernel before it
-int g_pass_mode = 0;  // 0 auto, 1 one kernel per sub-layer, 2 the persistent single-launch pass only
 
 
 // Node counts up to this use the vector-ALU GEMM on the automatic path.
@@ -91,6 +88,10 @@ static hipError_t make_wtab(ssd_model* m) {
 
 struct ssd_kv {
   const ssd_model* m = nullptr;
+  // per-session switches (ssd_kv_set_options)
+  int gemm_path = 0;  // 0 auto, 1 vector ALU, 2 matrix cores
+  int prefetch = 1;   // warm each weight GEMM's L2 from the kernel before it
+  int pass_mode = 0;  // 0 auto, 1 one kernel per sub-layer, 2 the persistent single-launch pass only
   int max_ctx = 0, max_nodes = 0, npad = 0;
   void *kc = nullptr, *vc = nullptr, *kt = nullptr, *vt = nullptr;
   void* ws = nullptr;  // one device allocation for every workspace below
@@ -133,6 +134,8 @@ struct ssd_graph {
   const ssd_model* m = nullptr;  // the pass it replays
   ssd_kv* kv = nullptr;
   int n = 0;
+  bool fused = false;   // captured as the persistent single launch
+  int gemm_path = 0;    // the session's GEMM path at capture (fixes the prefetcher's plan)
 };
 
 // ------------------------------------------------------------------ small host helpers
@@ -151,21 +154,23 @@ extern "C" const char* ssd_status_string(ssd_status s) {
 
 extern "C" const char* ssd_last_error(void) { return g_last_error.c_str(); }
 
-extern "C" ssd_status ssd_set_gemm_path(int32_t path) {
-  if (path < 0 || path > 2) return fail(SSD_E_INVALID_ARG, "gemm path must be 0, 1 or 2");
-  g_gemm_path = path;
+extern "C" ssd_status ssd_kv_set_options(ssd_kv* kv, const ssd_options* opt) {
+  if (!kv || !opt) return fail(SSD_E_INVALID_ARG, "null argument");
+  if (opt->pass_mode < 0 || opt->pass_mode > 2) return fail(SSD_E_INVALID_ARG, "pass mode must be 0, 1 or 2");
+  if (opt->gemm_path < 0 || opt->gemm_path > 2) return fail(SSD_E_INVALID_ARG, "gemm path must be 0, 1 or 2");
+  if (opt->weight_prefetch != 0 && opt->weight_prefetch != 1)
+    return fail(SSD_E_INVALID_ARG, "weight prefetch must be 0 or 1");
+  kv->pass_mode = opt->pass_mode;
+  kv->gemm_path = opt->gemm_path;
+  kv->prefetch = opt->weight_prefetch;
   return SSD_OK;
 }
 
-extern "C" ssd_status ssd_set_weight_prefetch(int32_t on) {
-  if (on != 0 && on != 1) return fail(SSD_E_INVALID_ARG, "weight prefetch must be 0 or 1");
-  g_prefetch = on;
-  return SSD_OK;
-}
-
-extern "C" ssd_status ssd_set_pass_mode(int32_t mode) {
-  if (mode < 0 || mode > 2) return fail(SSD_E_INVALID_ARG, "pass mode must be 0, 1 or 2");
-  g_pass_mode = mode;
+extern "C" ssd_status ssd_kv_get_options(const ssd_kv* kv, ssd_options* opt) {
+  if (!kv || !opt) return fail(SSD_E_INVALID_ARG, "null argument");
+  opt->pass_mode = kv->pass_mode;
+  opt->gemm_path = kv->gemm_path;
+  opt->weight_prefetch = kv->prefetch;
   return SSD_OK;
 }
 
@@ -270,15 +275,18 @@ extern "C" ssd_status ssd_model_create(const ssd_config* cfg, const ssd_weights*
     const size_t b_qkv = packed_bytes(3 * d, d), b_o = packed_bytes(d, d), b_fc = packed_bytes(M, d),
                  b_pr = packed_bytes(d, M), b_head = packed_bytes(V, d);
     const size_t total = (b_qkv + b_o + b_fc + b_pr) * L + b_head;
-    hipError_t e = hipMalloc(&m->pack, total);
+    // the packed copies, then one counter of weights past float16's range
+    hipError_t e = hipMalloc(&m->pack, total + 256);
     if (e != hipSuccess) {
       delete m;
       return fail(SSD_E_DEVICE, std::string("hipMalloc(packed weights): ") + hipGetErrorString(e));
     }
     hipStream_t s = (hipStream_t)stream;
+    unsigned* bad = (unsigned*)((char*)m->pack + total);
+    e = hipMemsetAsync(bad, 0, 4, s);
     char* p = (char*)m->pack;
     auto pack = [&](const void* src, int rows, int cols, size_t bytes) -> const void* {
-      if (e == hipSuccess) e = launch_pack_bf16((const uint16_t*)src, rows, cols, p, s);
+      if (e == hipSuccess) e = launch_pack_bf16((const uint16_t*)src, rows, cols, p, bad, s);
       const void* r = p;
       p += bytes;
       return r;
@@ -290,7 +298,15 @@ extern "C" ssd_status ssd_model_create(const ssd_config* cfg, const ssd_weights*
       m->p_pr.push_back(pack(m->w_pr[l], d, M, b_pr));
     }
     m->p_head = pack(m->wte, V, d, b_head);
+    unsigned n_bad = 0;
+    if (e == hipSuccess) e = hipMemcpyAsync(&n_bad, bad, 4, hipMemcpyDeviceToHost, s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e == hipSuccess && n_bad) {
+      (void)hipFree(m->pack);
+      delete m;
+      return fail(SSD_E_UNSUPPORTED, "a weight's magnitude exceeds 65504 (or is NaN): the matrix cores take "
+                                     "float16 copies of the weights");
+    }
     if (e == hipSuccess) e = make_wtab(m);
     if (e == hipSuccess) e = make_ftab(m);
     if (e != hipSuccess) {
@@ -432,10 +448,10 @@ static ssd_status fused_setup(ssd_kv* kv) {
 
 // whether a verification pass of model m over n nodes runs as the persistent single launch
 static bool use_fused(const ssd_model* m, const ssd_kv* kv, int n) {
-  if (g_pass_mode == 1 || m->f32 || !kv->fz_ok || !m->ftab) return false;
+  if (kv->pass_mode == 1 || m->f32 || !kv->fz_ok || !m->ftab) return false;
   // the persistent pass is forced, or chosen where it is the faster one
   // (measured on the GPT-2-L shape: at every node count it supports)
-  return g_pass_mode == 2 ? n <= kFMaxN : n <= kFAutoMaxN;
+  return kv->pass_mode == 2 ? n <= kFMaxN : n <= kFAutoMaxN;
 }
 
 extern "C" ssd_status ssd_verify_path(const ssd_model* m, const ssd_kv* kv, int32_t n, int32_t* path) {
@@ -574,10 +590,19 @@ static ssd_status release_slot(ssd_kv* kv, int slot, hipStream_t s) {
 
 // ------------------------------------------------------------------ verification pass
 
+// A session's workspaces and cache are sized for its model; another model may
+// use it only if every shape equals the session model's, except that it may
+// have fewer layers (a draft view).
+static bool same_shape_prefix(const ssd_config& a, const ssd_config& b) {
+  return a.d_model == b.d_model && a.n_head == b.n_head && a.d_mlp == b.d_mlp && a.vocab == b.vocab &&
+         a.dtype == b.dtype && a.n_layer <= b.n_layer;
+}
+
 static ssd_status check_verify_args(const ssd_model* m, const ssd_kv* kv, int32_t P, const int32_t* tokens,
                                     const int32_t* parents, int32_t n, const float* logits, int32_t* max_depth) {
   if (!m || !kv || !tokens || !parents || !logits) return fail(SSD_E_INVALID_ARG, "null argument");
-  if (kv->m != m && kv->m->cfg.n_layer < m->cfg.n_layer) return fail(SSD_E_INVALID_ARG, "session/model mismatch");
+  if (kv->m != m && !same_shape_prefix(m->cfg, kv->m->cfg))
+    return fail(SSD_E_INVALID_ARG, "the model's shape differs from the session's (only a layer prefix may be used)");
   if (n <= 0) return fail(SSD_E_INVALID_ARG, "n_nodes must be positive");
   if (P < 0) return fail(SSD_E_INVALID_ARG, "negative prefix_len");
   if (n > kv->max_nodes) return fail(SSD_E_CAPACITY, "n_nodes above the session's max_nodes");
@@ -619,12 +644,12 @@ static size_t fill_stage(char* host, int P, const int32_t* tokens, const int32_t
 // One weight GEMM of the pass over n nodes: fp32 models use the plain
 // kernel; bf16 models the vector-ALU kernel for few nodes (or when pinned)
 // and the matrix-core kernel otherwise, in node groups of 16 / 256.
-static int gemm_vec(int n) { return (g_gemm_path == 0 ? (n <= kVecMaxNodes ? 1 : 2) : g_gemm_path) == 1; }
+static int gemm_vec(int path, int n) { return (path == 0 ? (n <= kVecMaxNodes ? 1 : 2) : path) == 1; }
 
 // k-steps per split of a weight GEMM over n nodes (one k-split for every
 // node group, so all nodes leave the same partials)
-static int gemm_kcs(int n, int kind, int rows, int K) {
-  const int vec = gemm_vec(n);
+static int gemm_kcs(int path, int n, int kind, int rows, int K) {
+  const int vec = gemm_vec(path, n);
   int S = 1;
   return gemm_split_kc(rows, K, std::min(n, vec ? 16 : 256), vec, kind == EPI_PARTIAL, &S);
 }
@@ -632,14 +657,14 @@ static int gemm_kcs(int n, int kind, int rows, int K) {
 // The prefetcher's plan for a bf16 pass over n nodes: the launch geometry of
 // the first launch of each weight GEMM (see run_gemm), the weight table and
 // the session's signal words; base is filled in when the pass is enqueued.
-static PrefetchPlan prefetch_plan(const ssd_model* m, const ssd_kv* kv, int n) {
+static PrefetchPlan prefetch_plan(const ssd_model* m, const ssd_kv* kv, int path, int n) {
   PrefetchPlan pp{};
   const int d = m->cfg.d_model, M = m->cfg.d_mlp;
-  const int vec = gemm_vec(n), nn = std::min(n, vec ? 16 : 256);
+  const int vec = gemm_vec(path, n), nn = std::min(n, vec ? 16 : 256);
   const int kinds[4] = {EPI_QKV, EPI_PARTIAL, EPI_GELU, EPI_PARTIAL};
   const int rows[4] = {3 * d, d, M, d}, Ks[4] = {d, d, d, M};
   for (int k = 0; k < 4; ++k) {
-    const GemmGeom g = gemm_geom(kinds[k], vec, rows[k], Ks[k], nn, gemm_kcs(n, kinds[k], rows[k], Ks[k]));
+    const GemmGeom g = gemm_geom(kinds[k], vec, rows[k], Ks[k], nn, gemm_kcs(path, n, kinds[k], rows[k], Ks[k]));
     pp.geo[k] = PfGeom{g.KC, g.RBtot, g.RB, g.kcs, g.gx, g.gx * g.gy};
   }
   pp.W = (const void* const*)m->wtab;
@@ -657,24 +682,24 @@ static PrefetchPlan prefetch_plan(const ssd_model* m, const ssd_kv* kv, int n) {
 // stream first (the pass never waits for it).
 static bool use_fused(const ssd_model* m, const ssd_kv* kv, int n);
 
-static ssd_status start_pass_prefetch(const ssd_model* m, ssd_kv* kv, int n) {
-  if (m->f32 || use_fused(m, kv, n)) return SSD_OK;
+static ssd_status start_pass_prefetch(const ssd_model* m, ssd_kv* kv, int n, bool fused, int path) {
+  if (m->f32 || fused) return SSD_OK;
   const unsigned long long base = kv->sig_count;
   kv->sig_count += (unsigned long long)sigs_per_pass(m->cfg.n_layer);
-  if (!g_prefetch) return SSD_OK;
+  if (!kv->prefetch) return SSD_OK;
   if (!kv->pf_stream) HIP_TRY(hipStreamCreateWithFlags(&kv->pf_stream, hipStreamNonBlocking));
-  PrefetchPlan pp = prefetch_plan(m, kv, n);
+  PrefetchPlan pp = prefetch_plan(m, kv, path, n);
   pp.base = base;
   HIP_TRY(launch_prefetcher(pp, kv->pf_stream));
   return SSD_OK;
 }
 
-static hipError_t run_gemm(const ssd_model* m, int n, int kind, const void* Wraw, const void* Wp, int rows, int K,
-                           const void* act, const Epi& ep, hipStream_t s) {
+static hipError_t run_gemm(const ssd_model* m, int path, int n, int kind, const void* Wraw, const void* Wp, int rows,
+                           int K, const void* act, const Epi& ep, hipStream_t s) {
   if (m->f32) return launch_gemm_f32(kind, (const float*)Wraw, rows, K, (const float*)act, K, ep, s);
-  const int vec = gemm_vec(n);
+  const int vec = gemm_vec(path, n);
   const int group = vec ? 16 : 256;
-  const int kcs = gemm_kcs(n, kind, rows, K);
+  const int kcs = gemm_kcs(path, n, kind, rows, K);
   for (int n0 = 0; n0 < n; n0 += group) {
     Epi e2 = ep;
     e2.node0 = n0;
@@ -689,9 +714,9 @@ static hipError_t run_gemm(const ssd_model* m, int n, int kind, const void* Wraw
 }
 
 // number of split-K partials a residual GEMM leaves for the next LayerNorm
-static int resid_splits(const ssd_model* m, int n, int rows, int K) {
+static int resid_splits(const ssd_model* m, int path, int n, int rows, int K) {
   if (m->f32) return 0;
-  const int vec = gemm_vec(n);
+  const int vec = gemm_vec(path, n);
   int S = 1;
   gemm_split_kc(rows, K, std::min(n, vec ? 16 : 256), vec, 1, &S);
   return S;
@@ -741,7 +766,8 @@ static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int3
     HIP_TRY(launch_fused(a, s));
     return SSD_OK;
   }
-  if (g_pass_mode == 2) return fail(SSD_E_UNSUPPORTED, "the persistent pass does not apply to this model, session or tree");
+  if (kv->pass_mode == 2) return fail(SSD_E_UNSUPPORTED, "the persistent pass does not apply to this model, session or tree");
+  const int gp = kv->gemm_path;
   unsigned long long* sig = f32 ? nullptr : kv->d_sig;  // pass signals (bf16 models)
   HIP_TRY(launch_embed(f32, m->wte, m->wpe, d_tok, d_pos, n, d, kv->x, sig, kv->d_xcc0, s));
 
@@ -751,14 +777,14 @@ static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int3
   // fp32 models add residuals inside the GEMM; bf16 models leave split-K
   // partials that the next LayerNorm adds (with the bias)
   const int kind_res = f32 ? EPI_RESID : EPI_PARTIAL;
-  const int s_o = resid_splits(m, n, d, d), s_pr = resid_splits(m, n, d, M);
+  const int s_o = resid_splits(m, gp, n, d, d), s_pr = resid_splits(m, gp, n, d, M);
   const size_t kv_layer = (size_t)H * DH;  // elements per K/V row across heads
 
   int pend_S = 0;               // partials waiting to be added to x
   const void* pend_bias = nullptr;
   for (int l = 0; l < L; ++l) {
     HIP_TRY(launch_ln(f32, kv->x, n, d, kv->part, pend_S, pstride, pend_bias, m->ln1_g[l], m->ln1_b[l], c.ln_eps,
-                      kv->act_a, ld_d, sig, s));
+                      kv->act_a, ld_d, sig, kv->d_err, s));
     Epi e{};
     e.sig = sig;
     e.bias = m->b_qkv[l];
@@ -771,7 +797,7 @@ static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int3
     e.H = H;
     e.DH = DH;
     e.max_nodes = maxn;
-    HIP_TRY(run_gemm(m, n, EPI_QKV, m->w_qkv[l], f32 ? nullptr : m->p_qkv[l], 3 * d, d, kv->act_a, e, s));
+    HIP_TRY(run_gemm(m, gp, n, EPI_QKV, m->w_qkv[l], f32 ? nullptr : m->p_qkv[l], 3 * d, d, kv->act_a, e, s));
 
     AttnArgs a{};
     a.q = kv->q;
@@ -797,6 +823,7 @@ static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int3
     a.CL = attn_chunk(P);
     a.nsplit = attn_nsplit(P);
     a.sig = sig;
+    a.err = kv->d_err;
     HIP_TRY(launch_attn(f32, DH, a, s));
 
     Epi eo{};
@@ -808,19 +835,20 @@ static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int3
     eo.x = kv->x;
     eo.part = kv->part;
     eo.part_stride = (long long)pstride;
-    HIP_TRY(run_gemm(m, n, kind_res, m->w_o[l], f32 ? nullptr : m->p_o[l], d, d, kv->act_o, eo, s));
+    HIP_TRY(run_gemm(m, gp, n, kind_res, m->w_o[l], f32 ? nullptr : m->p_o[l], d, d, kv->act_o, eo, s));
 
     HIP_TRY(launch_ln(f32, kv->x, n, d, kv->part, f32 ? 0 : s_o, pstride, m->b_o[l], m->ln2_g[l], m->ln2_b[l],
-                      c.ln_eps, kv->act_a, ld_d, sig, s));
+                      c.ln_eps, kv->act_a, ld_d, sig, kv->d_err, s));
     Epi ef{};
     ef.sig = sig;
+    ef.err = kv->d_err;
     ef.bias = m->b_fc[l];
     ef.N = n;
     ef.M = M;
     ef.d = d;
     ef.out = kv->act_f;
     ef.ldo = ld_m;
-    HIP_TRY(run_gemm(m, n, EPI_GELU, m->w_fc[l], f32 ? nullptr : m->p_fc[l], M, d, kv->act_a, ef, s));
+    HIP_TRY(run_gemm(m, gp, n, EPI_GELU, m->w_fc[l], f32 ? nullptr : m->p_fc[l], M, d, kv->act_a, ef, s));
 
     Epi ep{};
     ep.sig = sig;
@@ -831,12 +859,12 @@ static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int3
     ep.x = kv->x;
     ep.part = kv->part;
     ep.part_stride = (long long)pstride;
-    HIP_TRY(run_gemm(m, n, kind_res, m->w_pr[l], f32 ? nullptr : m->p_pr[l], d, M, kv->act_f, ep, s));
+    HIP_TRY(run_gemm(m, gp, n, kind_res, m->w_pr[l], f32 ? nullptr : m->p_pr[l], d, M, kv->act_f, ep, s));
     pend_S = f32 ? 0 : s_pr;
     pend_bias = m->b_pr[l];
   }
   HIP_TRY(launch_ln(f32, kv->x, n, d, kv->part, pend_S, pstride, pend_bias, m->lnf_g, m->lnf_b, c.ln_eps, kv->act_a,
-                    ld_d, nullptr, s));
+                    ld_d, nullptr, kv->d_err, s));
   Epi eh{};
   eh.bias = nullptr;
   eh.N = n;
@@ -844,7 +872,7 @@ static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int3
   eh.d = d;
   eh.logits = logits;
   eh.ldl = V;
-  HIP_TRY(run_gemm(m, n, EPI_LOGITS, m->wte, f32 ? nullptr : m->p_head, V, d, kv->act_a, eh, s));
+  HIP_TRY(run_gemm(m, gp, n, EPI_LOGITS, m->wte, f32 ? nullptr : m->p_head, V, d, kv->act_a, eh, s));
   return SSD_OK;
 }
 
@@ -859,7 +887,7 @@ extern "C" ssd_status ssd_tree_verify(const ssd_model* m, ssd_kv* kv, int32_t pr
   st = acquire_slot(kv, &host, &slot);
   if (st != SSD_OK) return st;
   const size_t used = fill_stage(host, prefix_len, tree_tokens, parent_idx, n_nodes, kv->max_nodes);
-  st = start_pass_prefetch(m, kv, n_nodes);
+  st = start_pass_prefetch(m, kv, n_nodes, use_fused(m, kv, n_nodes), kv->gemm_path);
   if (st == SSD_OK) st = enqueue_verify(m, kv, prefix_len, n_nodes, host, used, logits, s);
   ssd_status st2 = release_slot(kv, slot, s);
   return st != SSD_OK ? st : st2;
@@ -876,6 +904,8 @@ extern "C" ssd_status ssd_graph_capture_verify(const ssd_model* m, ssd_kv* kv, i
   g->m = m;
   g->kv = kv;
   g->n = n_nodes;
+  g->fused = use_fused(m, kv, n_nodes);
+  g->gemm_path = kv->gemm_path;
   hipError_t e = hipHostMalloc((void**)&g->pinned, kv->slot_bytes, hipHostMallocDefault);
   if (e != hipSuccess) {
     delete g;
@@ -914,7 +944,7 @@ extern "C" ssd_status ssd_graph_capture_verify(const ssd_model* m, ssd_kv* kv, i
 
 extern "C" ssd_status ssd_graph_launch(ssd_graph* g, void* stream) {
   if (!g || !g->exec) return fail(SSD_E_INVALID_ARG, "null graph");
-  const ssd_status st = start_pass_prefetch(g->m, g->kv, g->n);
+  const ssd_status st = start_pass_prefetch(g->m, g->kv, g->n, g->fused, g->gemm_path);
   if (st != SSD_OK) return st;
   HIP_TRY(hipGraphLaunch(g->exec, (hipStream_t)stream));
   return SSD_OK;
@@ -931,6 +961,8 @@ extern "C" void ssd_graph_destroy(ssd_graph* g) {
 extern "C" ssd_status ssd_launch_gemm(const ssd_model* m, ssd_kv* kv, int32_t which, int32_t layer, int32_t n_nodes,
                                       void* stream) {
   if (!m || !kv) return fail(SSD_E_INVALID_ARG, "null argument");
+  if (kv->m != m && !same_shape_prefix(m->cfg, kv->m->cfg))
+    return fail(SSD_E_INVALID_ARG, "the model's shape differs from the session's");
   const ssd_config& c = m->cfg;
   if (which < 0 || which > 3 || layer < 0 || layer >= c.n_layer) return fail(SSD_E_INVALID_ARG, "bad matrix id");
   if (n_nodes <= 0 || n_nodes > kv->max_nodes) return fail(SSD_E_CAPACITY, "n_nodes outside the session");
@@ -972,7 +1004,7 @@ extern "C" ssd_status ssd_launch_gemm(const ssd_model* m, ssd_kv* kv, int32_t wh
   }
   e.M = rows;
   (void)lda;
-  HIP_TRY(run_gemm(m, n_nodes, kind, Wraw, Wp, rows, K, act, e, (hipStream_t)stream));
+  HIP_TRY(run_gemm(m, kv->gemm_path, n_nodes, kind, Wraw, Wp, rows, K, act, e, (hipStream_t)stream));
   return SSD_OK;
 }
 

@@ -47,6 +47,7 @@ struct Epi {
   long long part_stride;  // elements between splits
   int split;              // set by the kernel from blockIdx.y
   unsigned long long* sig;  // pass signal counter (nullptr: none)
+  unsigned* err;            // session error counter: float16 GEMM inputs out of range (nullptr: none)
 };
 
 // tile shape of the bf16 GEMM for a node count: node tiles of 16, row blocks
@@ -113,6 +114,7 @@ struct AttnArgs {
   int CL;               // cache rows per prefix chunk (attn_chunk(P))
   int nsplit;           // prefix chunks (attn_nsplit(P))
   unsigned long long* sig;  // pass signal counter (nullptr: none); both kernels signal
+  unsigned* err;            // session error counter: float16 outputs out of range (nullptr: none)
 };
 
 // bf16 attention: cache rows per prefix chunk, a multiple of 32 between 64
@@ -141,7 +143,8 @@ hipError_t launch_embed(int f32, const void* wte, const void* wpe, const int* to
 // x += bias + part[0..S-1] (if S > 0), then LayerNorm into the GEMM-input
 // buffer a (lda: fp32 row stride, or bf16 k-steps d / 32; see st_act)
 hipError_t launch_ln(int f32, float* x, int N, int d, const float* part, int S, size_t pstride, const void* bias,
-                     const void* g, const void* b, float eps, void* a, int lda, unsigned long long* sig, hipStream_t s);
+                     const void* g, const void* b, float eps, void* a, int lda, unsigned long long* sig,
+                     unsigned* err, hipStream_t s);
 hipError_t launch_gemm_f32(int kind, const float* W, int M, int K, const float* act, int lda, const Epi& ep,
                            hipStream_t s);
 GemmCfg gemm_cfg(int N, int vec, int kind);
@@ -155,7 +158,8 @@ hipError_t launch_gemm_bf16(int kind, int vec, const void* Wp, int M, int K, con
                             const Epi& ep, hipStream_t s);
 hipError_t launch_attn(int f32, int DH, const AttnArgs& a, hipStream_t s);
 hipError_t launch_prefetcher(const PrefetchPlan& pp, hipStream_t s);
-hipError_t launch_pack_bf16(const uint16_t* W, int M, int K, void* out, hipStream_t s);
+// bad: device counter of packed 16-byte groups holding a weight past float16's range
+hipError_t launch_pack_bf16(const uint16_t* W, int M, int K, void* out, unsigned* bad, hipStream_t s);
 size_t packed_bytes(int M, int K);
 // greedy argmax per node; work: argmax_work_bytes(N, V) bytes of device scratch
 size_t argmax_work_bytes(int N, int V);

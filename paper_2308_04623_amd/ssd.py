@@ -7,6 +7,7 @@ CPU fallback.
 """
 from __future__ import annotations
 
+import contextlib
 import ctypes as C
 import os
 from typing import Dict, Optional, Sequence, Tuple
@@ -28,8 +29,10 @@ LAYER_TENSORS = ("ln1_g", "ln1_b", "w_qkv", "b_qkv", "w_o", "b_o",
 EXPORTS = ("ssd_model_create", "ssd_model_destroy", "ssd_kv_bytes", "ssd_kv_create", "ssd_kv_destroy",
            "ssd_tree_verify", "ssd_tree_accept", "ssd_kv_commit", "ssd_kv_error_count",
            "ssd_graph_capture_verify", "ssd_graph_launch", "ssd_graph_destroy", "ssd_validate_tree",
-           "ssd_tree_prep", "ssd_set_gemm_path", "ssd_set_weight_prefetch", "ssd_set_pass_mode", "ssd_verify_path", "ssd_fused_plan", "ssd_kv_set_trace", "ssd_status_string", "ssd_last_error", "ssd_launch_gemm",
+           "ssd_tree_prep", "ssd_kv_set_options", "ssd_kv_get_options", "ssd_status_string", "ssd_last_error",
            "ssd_model_prefix_view", "ssd_topk")
+# and every function include/ssd_diag.h declares (measurement and diagnostics)
+DIAG_EXPORTS = ("ssd_launch_gemm", "ssd_verify_path", "ssd_fused_plan", "ssd_kv_set_trace")
 
 
 class SSDError(RuntimeError):
@@ -49,6 +52,10 @@ _PP = C.POINTER(C.c_void_p)
 class _Weights(C.Structure):
     _fields_ = [("wte", C.c_void_p), ("wpe", C.c_void_p), ("lnf_g", C.c_void_p), ("lnf_b", C.c_void_p)] + \
                [(n, _PP) for n in LAYER_TENSORS]
+
+
+class _Options(C.Structure):
+    _fields_ = [("pass_mode", C.c_int32), ("gemm_path", C.c_int32), ("weight_prefetch", C.c_int32)]
 
 
 class _Tree(C.Structure):
@@ -86,9 +93,8 @@ def lib():
             "ssd_graph_destroy": [vp],
             "ssd_validate_tree": [i32p, i32p, C.c_int32, C.c_int32, i32p],
             "ssd_tree_prep": [i32p, C.c_int32, i32p, C.POINTER(C.c_uint64)],
-            "ssd_set_gemm_path": [C.c_int32],
-            "ssd_set_weight_prefetch": [C.c_int32],
-            "ssd_set_pass_mode": [C.c_int32],
+            "ssd_kv_set_options": [vp, C.POINTER(_Options)],
+            "ssd_kv_get_options": [vp, C.POINTER(_Options)],
             "ssd_verify_path": [vp, vp, C.c_int32, C.POINTER(C.c_int32)],
             "ssd_fused_plan": [C.c_int32] * 5 + [vp, vp, vp],
             "ssd_kv_set_trace": [vp, vp],
@@ -143,20 +149,7 @@ def tree_prep(parent_idx) -> Tuple[np.ndarray, np.ndarray]:
     return depth, anc
 
 
-def set_gemm_path(path: int):
-    _check(lib().ssd_set_gemm_path(path), "ssd_set_gemm_path")
-
-
-def set_weight_prefetch(on: bool):
-    _check(lib().ssd_set_weight_prefetch(1 if on else 0), "ssd_set_weight_prefetch")
-
-
 PASS_AUTO, PASS_KERNELS, PASS_FUSED = 0, 1, 2
-
-
-def set_pass_mode(mode: int):
-    """0 automatic, 1 one kernel per sub-layer, 2 the persistent single launch only."""
-    _check(lib().ssd_set_pass_mode(mode), "ssd_set_pass_mode")
 
 
 def fused_plan(n_head: int, d_model: int, d_mlp: int, vocab: int, n_tiles: int):
@@ -401,6 +394,33 @@ class Session:
         v = C.c_int32(0)
         _check(lib().ssd_verify_path(self.model.handle, self.handle, n, C.byref(v)), "ssd_verify_path")
         return v.value
+
+    def get_options(self) -> Dict[str, int]:
+        o = _Options()
+        _check(lib().ssd_kv_get_options(self.handle, C.byref(o)), "ssd_kv_get_options")
+        return {"pass_mode": o.pass_mode, "gemm_path": o.gemm_path, "weight_prefetch": o.weight_prefetch}
+
+    def set_options(self, pass_mode: Optional[int] = None, gemm_path: Optional[int] = None,
+                    weight_prefetch: Optional[int] = None):
+        """This session's switches (ssd_kv_set_options); None keeps a value.
+        pass_mode: PASS_AUTO / PASS_KERNELS / PASS_FUSED; gemm_path: GEMM_AUTO
+        / GEMM_VEC / GEMM_MFMA; weight_prefetch: 0 or 1."""
+        cur = self.get_options()
+        for k, v in (("pass_mode", pass_mode), ("gemm_path", gemm_path), ("weight_prefetch", weight_prefetch)):
+            if v is not None:
+                cur[k] = int(v)
+        o = _Options(cur["pass_mode"], cur["gemm_path"], cur["weight_prefetch"])
+        _check(lib().ssd_kv_set_options(self.handle, C.byref(o)), "ssd_kv_set_options")
+
+    @contextlib.contextmanager
+    def options(self, **kw):
+        """Switches set for the block, restored afterwards."""
+        prev = self.get_options()
+        self.set_options(**kw)
+        try:
+            yield self
+        finally:
+            self.set_options(**prev)
 
     def error_count(self, stream=None) -> int:
         c = C.c_uint32(0)

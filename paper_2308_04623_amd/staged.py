@@ -206,6 +206,14 @@ class GpuBackend:
         # per oracle step, the top-2 logit gap at the node whose argmax became
         # the next token (to tell precision ties from real divergences)
         self.gaps = [] if record_gaps else None
+        self._errors = {id(s): s.error_count() for s in (self.o, self.d)}
+
+    def _check_errors(self, session):
+        """A pass that ended early, a float16 overflow or a skipped commit row
+        leaves results undefined: stop rather than emit tokens from them."""
+        n = session.error_count()
+        if n != self._errors[id(session)]:
+            raise RuntimeError(f"libssd session error counter grew from {self._errors[id(session)]} to {n}")
 
     def prefill(self, tokens: np.ndarray, P: int = 0) -> int:
         """Cache `tokens` after P cached ones, in chains of at most max_nodes
@@ -222,17 +230,20 @@ class GpuBackend:
             plen = torch.tensor([n], dtype=torch.int32, device=self.o.model.device)
             self.o.commit(P, path, plen)
             P += n
+        self._check_errors(self.o)
         return P
 
     def draft_top(self, P: int, toks: np.ndarray, par: np.ndarray, k: int):
         lg = self.d.verify(P, toks, par)
         idx, val, lse = self.d.topk(lg, k)
+        self._check_errors(self.d)
         return idx.cpu().numpy(), val.cpu().numpy(), lse.cpu().numpy()
 
     def oracle_step(self, P: int, toks: np.ndarray, par: np.ndarray):
         lg = self.o.verify(P, toks, par)
         path, plen, nxt = self.o.accept(toks, par, lg)
         self.o.commit(P, path, plen)
+        self._check_errors(self.o)
         n = int(plen.item())
         p = path[:n].cpu().numpy().astype(np.int32)
         if self.gaps is not None:
@@ -248,6 +259,7 @@ class GpuBackend:
         par = np.arange(-1, n - 1, dtype=np.int32)
         lg = self.d.verify(0, window_tokens, par)
         idx, _, _ = self.d.topk(lg, 1)
+        self._check_errors(self.d)
         return idx[:, 0].cpu().numpy()
 
 

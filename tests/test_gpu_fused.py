@@ -35,7 +35,6 @@ def ssd(torch):
     from paper_2308_04623_amd import ssd as s
     s.lib()
     yield s
-    s.set_pass_mode(s.PASS_AUTO)
 
 
 class Small:
@@ -69,8 +68,14 @@ TREES = {"single": np.array([-1], np.int32), "binary15": W.complete_binary_tree(
          "random48": _rand_tree(2, 48), "chain64": W.chain_tree(64), "random64": _rand_tree(3, 64)}
 
 
-def _fused(ssd):
-    ssd.set_pass_mode(ssd.PASS_FUSED)
+def _fused(ssd, *sessions):
+    for s in sessions:
+        s.set_options(pass_mode=ssd.PASS_FUSED)
+
+
+def _auto(ssd, *sessions):
+    for s in sessions:
+        s.set_options(pass_mode=ssd.PASS_AUTO)
 
 
 @pytest.mark.parametrize("name", list(TREES))
@@ -82,12 +87,12 @@ def test_fused_verify_matches_oracle(small, ssd, torch, name, P):
     print(f"fused verify {name} P={P}", flush=True)
     ref, kt, vt = t.oracle_verify(toks, par, P)
     before = t.s.error_count()
-    _fused(ssd)
+    _fused(ssd, t.s)
     try:
         lg = t.s.verify(P, toks, par)
         torch.cuda.synchronize()
     finally:
-        ssd.set_pass_mode(ssd.PASS_AUTO)
+        _auto(ssd, t.s)
     assert t.s.error_count() == before
     got = lg.cpu().numpy()
     err = np.abs(got - ref).max()
@@ -108,11 +113,8 @@ def test_fused_and_kernel_paths_agree(small, ssd, torch):
     ref, _, _ = t.oracle_verify(toks, par, t.P)
     out = {}
     for mode in (ssd.PASS_KERNELS, ssd.PASS_FUSED):
-        ssd.set_pass_mode(mode)
-        try:
+        with t.s.options(pass_mode=mode):
             out[mode] = t.s.verify(t.P, toks, par).cpu().numpy()
-        finally:
-            ssd.set_pass_mode(ssd.PASS_AUTO)
     assert np.abs(out[ssd.PASS_FUSED] - ref).max() < TOL
     assert np.abs(out[ssd.PASS_KERNELS] - ref).max() < TOL
     assert np.abs(out[ssd.PASS_FUSED] - out[ssd.PASS_KERNELS]).max() < TOL
@@ -122,7 +124,7 @@ def test_fused_determinism_and_graph_replay(small, ssd, torch):
     t = small
     par = TREES["random64"]
     toks = W.tree_tokens(par, t.cfg.vocab, seed=9)
-    _fused(ssd)
+    _fused(ssd, t.s)
     try:
         a = t.s.verify(t.P, toks, par).clone()
         b = t.s.verify(t.P, toks, par).clone()
@@ -140,7 +142,7 @@ def test_fused_determinism_and_graph_replay(small, ssd, torch):
             torch.cuda.synchronize()
         g.close()
     finally:
-        ssd.set_pass_mode(ssd.PASS_AUTO)
+        _auto(ssd, t.s)
     assert t.s.error_count() == 0
 
 
@@ -149,7 +151,7 @@ def test_fused_node_independent_of_tree_slot_and_tiles(small, ssd, torch):
     alone (1 tile), at other slots among decoys (1 tile), and spread over a
     3-tile tree."""
     t = small
-    _fused(ssd)
+    _fused(ssd, t.s)
     try:
         toks_a = np.array([5, 6, 7, 8], np.int32)
         lg_a = t.s.verify(t.P, toks_a, W.chain_tree(4)).clone()
@@ -174,7 +176,7 @@ def test_fused_node_independent_of_tree_slot_and_tiles(small, ssd, torch):
         lg_c = t.s.verify(t.P, toks_c, par_c).clone()
         torch.cuda.synchronize()
     finally:
-        ssd.set_pass_mode(ssd.PASS_AUTO)
+        _auto(ssd, t.s)
     for i, j in zip(range(4), [0, 2, 5, 9]):
         assert torch.equal(lg_a[i], lg_b[j]), (i, j)
     for i, j in zip(range(4), slots):
@@ -194,7 +196,7 @@ def test_fused_prefix_view_equals_truncated_model(small, ssd, torch):
     view = t.m.prefix_view(2)
     par = TREES["branch32"]
     toks = W.tree_tokens(par, t.cfg.vocab, seed=4)
-    _fused(ssd)
+    _fused(ssd, t.s, s2)
     try:
         a = s2.verify(t.P, toks, par).clone()
         lg = torch.empty((len(par), t.cfg.vocab), dtype=torch.float32, device="cuda")
@@ -205,7 +207,7 @@ def test_fused_prefix_view_equals_truncated_model(small, ssd, torch):
                                      C.c_void_p(lg.data_ptr()), _stream(None)), "ssd_tree_verify")
         torch.cuda.synchronize()
     finally:
-        ssd.set_pass_mode(ssd.PASS_AUTO)
+        _auto(ssd, t.s, s2)
     assert torch.equal(a, lg)
     om2 = oracle.Model(cfg2, w2)
     ref = oracle.tree_verify(om2, t.kc[:2], t.vc[:2], t.P, toks, par, om2.kv(t.max_nodes), om2.kv(t.max_nodes))
@@ -219,13 +221,10 @@ def test_fused_only_mode_rejects_unsupported(small, ssd, torch):
     t = small
     par = W.chain_tree(65)
     s = ssd.Session(t.m, t.max_ctx, 65, ssd.to_device(t.kc, t.cfg), ssd.to_device(t.vc, t.cfg))
-    _fused(ssd)
-    try:
-        with pytest.raises(ssd.SSDError) as e:
-            s.verify(t.P, W.tree_tokens(par, t.cfg.vocab, seed=1), par)
-        assert e.value.status == ssd.E_UNSUPPORTED
-    finally:
-        ssd.set_pass_mode(ssd.PASS_AUTO)
+    _fused(ssd, s)
+    with pytest.raises(ssd.SSDError) as e:
+        s.verify(t.P, W.tree_tokens(par, t.cfg.vocab, seed=1), par)
+    assert e.value.status == ssd.E_UNSUPPORTED
     s.close()
 
 
@@ -242,3 +241,19 @@ def test_fused_cache_length_limit(small, ssd, torch):
         paths.append(s.verify_path(1))
         s.close()
     assert paths == [ssd.PASS_FUSED, ssd.PASS_KERNELS]
+
+
+def test_fused_float16_overflow_is_counted(small, ssd, torch):
+    """A LayerNorm output past float16's range (gain 1e5) is counted in the
+    session's error counter by the persistent pass too."""
+    t = small
+    w = dict(t.w)
+    w["ln1_g"] = [W.f32_to_bf16_bits(np.full(t.cfg.d_model, 1e5, np.float32))] + list(t.w["ln1_g"][1:])
+    m = ssd.Model(t.cfg, w)
+    s = ssd.Session(m, t.max_ctx, 16, ssd.to_device(t.kc, t.cfg), ssd.to_device(t.vc, t.cfg))
+    _fused(ssd, s)
+    assert s.verify_path(3) == ssd.PASS_FUSED
+    s.verify(t.P, [1, 2, 3], [-1, 0, 0])
+    assert s.error_count() > 0
+    s.close()
+    m.close()

@@ -28,7 +28,6 @@ def ssd(torch):
     from paper_2308_04623_amd import ssd as s
     s.lib()
     yield s
-    s.set_gemm_path(s.GEMM_AUTO)
 
 
 class Tiny:
@@ -98,14 +97,14 @@ def test_tiny_bf16_verify(tiny16, ssd, torch, gemm, name):
     par = TREES[name]
     if gemm == "vec" and len(par) > 16:
         par = par[:16]
-    ssd.set_gemm_path(ssd.GEMM_VEC if gemm == "vec" else ssd.GEMM_MFMA)
+    t.s.set_options(gemm_path=ssd.GEMM_VEC if gemm == "vec" else ssd.GEMM_MFMA)
     try:
         toks = W.tree_tokens(par, t.cfg.vocab, seed=7)
         ref, kt, vt = t.oracle_verify(toks, par)
         lg = t.s.verify(t.P, toks, par)
         torch.cuda.synchronize()
     finally:
-        ssd.set_gemm_path(ssd.GEMM_AUTO)
+        t.s.set_options(gemm_path=ssd.GEMM_AUTO)
     assert np.abs(lg.cpu().numpy() - ref).max() < TOL_BF16
     n = len(par)
     kg = W.bf16_bits_to_f32(ssd.to_host_bits(t.s.k_tree)[:, :, :n])
@@ -138,7 +137,7 @@ def test_node_result_independent_of_tree_and_slot(tiny16, ssd, torch, gemm):
     """A node's logits depend only on its root path, bitwise, whatever the
     other nodes and its index (one GEMM path pinned)."""
     t = tiny16
-    ssd.set_gemm_path(ssd.GEMM_VEC if gemm == "vec" else ssd.GEMM_MFMA)
+    t.s.set_options(gemm_path=ssd.GEMM_VEC if gemm == "vec" else ssd.GEMM_MFMA)
     try:
         toks_a = np.array([5, 6, 7, 8], np.int32)
         lg_a = t.s.verify(t.P, toks_a, W.chain_tree(4)).clone()
@@ -148,7 +147,7 @@ def test_node_result_independent_of_tree_and_slot(tiny16, ssd, torch, gemm):
         lg_b = t.s.verify(t.P, toks_b, par_b).clone()
         torch.cuda.synchronize()
     finally:
-        ssd.set_gemm_path(ssd.GEMM_AUTO)
+        t.s.set_options(gemm_path=ssd.GEMM_AUTO)
     for i, j in zip([0, 1, 2, 3], [0, 2, 5, 9]):
         assert torch.equal(lg_a[i], lg_b[j]), (i, j)
 
@@ -263,3 +262,103 @@ def test_greedy_accept_full_vocab_ties(wide, ssd, torch):
     path, plen, nxt = s.accept(toks, par, torch.from_numpy(lg).cuda())
     op, on = oracle.tree_accept(oracle.GREEDY, toks, par, lg)
     assert path[:int(plen.item())].cpu().numpy().tolist() == op.tolist() and int(nxt.item()) == on
+
+
+@pytest.mark.parametrize("T", [0.7, 1.5])
+@pytest.mark.parametrize("mode", ["wor", "iid"])
+def test_sampling_accept_temperature_and_zero_draft_entries(wide, ssd, torch, T, mode):
+    """Temperatures other than 1, and draft rows that are exactly zero at
+    tested tokens: such a child is accepted iff the residual target mass at
+    its token is positive (tested both ways: tokens whose target probability
+    underflows to 0 are rejected)."""
+    cfg, s = wide
+    V = 4096
+    g = np.random.default_rng(int(T * 10) + len(mode))
+    md = ssd.SAMPLE_WOR if mode == "wor" else ssd.SAMPLE_IID
+    zero_hits = 0
+    for trial in range(10):
+        toks, par = _draft_tree(g, V, [3, 2, 2, 1], 40)
+        n = len(par)
+        lg = (g.standard_normal((n, V)) * 2.0).astype(np.float32)
+        q = g.dirichlet(np.ones(V) * 0.3, size=n).astype(np.float32)
+        for c in range(1, n):
+            u = par[c]
+            kind = g.random()
+            if kind < 0.35:
+                q[u, toks[c]] = 0.0                       # zero draft mass, positive target mass
+                zero_hits += 1
+            elif kind < 0.5:
+                q[u, toks[c]] = 0.0                       # zero draft mass and zero target mass
+                lg[u, toks[c]] = -1e30
+                zero_hits += 1
+        dlg, dq = torch.from_numpy(lg).cuda(), torch.from_numpy(q).cuda()
+        path, plen, nxt = s.accept(toks, par, dlg, mode=md, draft_probs=dq, temperature=T, seed=100 + trial)
+        op, on = oracle.tree_accept(oracle.SAMPLE_WOR if mode == "wor" else oracle.SAMPLE_IID, toks, par, lg, q,
+                                    T, 100 + trial)
+        assert path[:int(plen.item())].cpu().numpy().tolist() == op.tolist(), trial
+        assert int(nxt.item()) == on, trial
+    assert zero_hits > 20
+
+
+@pytest.mark.parametrize("mode", ["wor", "iid"])
+def test_sampling_accept_residual_mass_zero(wide, ssd, torch, mode):
+    """A root whose target and draft are the same point mass: every child
+    (a different token) is rejected, the residual becomes all zeros (Z = 0),
+    and the extra token is drawn from the target itself (the point)."""
+    cfg, s = wide
+    V = 1000
+    par = np.array([-1, 0, 0, 0, 1], np.int32)
+    toks = np.array([5, 11, 12, 13, 14], np.int32)
+    n = len(par)
+    lg = np.full((n, V), -1e30, np.float32)
+    lg[:, 7] = 0.0
+    q = np.zeros((n, V), np.float32)
+    q[:, 7] = 1.0
+    md = ssd.SAMPLE_WOR if mode == "wor" else ssd.SAMPLE_IID
+    for seed in range(3):
+        path, plen, nxt = s.accept(toks, par, torch.from_numpy(lg).cuda(), mode=md,
+                                   draft_probs=torch.from_numpy(q).cuda(), temperature=1.0, seed=seed)
+        op, on = oracle.tree_accept(oracle.SAMPLE_WOR if mode == "wor" else oracle.SAMPLE_IID, toks, par, lg, q,
+                                    1.0, seed)
+        assert op.tolist() == [0] and on == 7
+        assert path[:int(plen.item())].cpu().numpy().tolist() == [0] and int(nxt.item()) == 7
+
+
+def test_session_options_validate_and_stay_per_session(tiny16, ssd, torch):
+    t = tiny16
+    default = {"pass_mode": ssd.PASS_AUTO, "gemm_path": ssd.GEMM_AUTO, "weight_prefetch": 1}
+    assert t.s.get_options() == default
+    for bad in (dict(pass_mode=3), dict(gemm_path=-1), dict(weight_prefetch=2)):
+        with pytest.raises(ssd.SSDError) as e:
+            t.s.set_options(**bad)
+        assert e.value.status == ssd.E_INVALID_ARG
+    assert t.s.get_options() == default
+    other = ssd.Session(t.m, 16, 4)
+    with t.s.options(pass_mode=ssd.PASS_KERNELS, gemm_path=ssd.GEMM_VEC, weight_prefetch=0):
+        assert t.s.get_options() == {"pass_mode": 1, "gemm_path": 1, "weight_prefetch": 0}
+        assert other.get_options() == default
+    assert t.s.get_options() == default
+    other.close()
+
+
+def test_float16_range_is_checked(ssd, torch):
+    """The matrix cores take float16 copies of bf16 weights and float16 GEMM
+    inputs: a weight past 65504 is refused at model creation, and a GEMM
+    input past it is counted in the session's error counter."""
+    cfg = W.TINY.with_(dtype="bf16", n_layer=1)
+    w = W.make_weights(cfg, 0)
+    big = W.f32_to_bf16_bits(np.array([1e5], np.float32))[0]
+    w2 = dict(w)
+    w2["w_fc"] = [w["w_fc"][0].copy()]
+    w2["w_fc"][0][3, 5] = big
+    with pytest.raises(ssd.SSDError) as e:
+        ssd.Model(cfg, w2)
+    assert e.value.status == ssd.E_UNSUPPORTED
+    w3 = dict(w)
+    w3["ln1_g"] = [W.f32_to_bf16_bits(np.full(cfg.d_model, 1e5, np.float32))]
+    m = ssd.Model(cfg, w3)
+    s = ssd.Session(m, 16, 4)
+    assert s.error_count() == 0
+    s.verify(0, [1, 2], [-1, 0])
+    assert s.error_count() > 0
+    s.close()

@@ -35,7 +35,6 @@ def ssd(torch):
     from paper_2308_04623_amd import ssd as s
     s.lib()
     yield s
-    s.set_gemm_path(s.GEMM_AUTO)
 
 
 def _compare(staged, plain, gaps):
@@ -136,3 +135,45 @@ def test_staged_equals_plain_gpt2l(ssd, torch):
     w = W.make_weights(cfg, 0)
     st, plain, agree = _staged_vs_plain(ssd, torch, cfg, w, 4, 128, 64, 4096, 256)
     assert agree >= 1
+
+
+def test_staged_equals_oracle_plain_greedy_tiny_f32(ssd, torch):
+    """On the float32 model the GPU's staged loop emits exactly the oracle's
+    plain greedy sequence (no tie escape: the oracle's smallest top-2 gap
+    over the sequence is far above the 1e-4 logit tolerance)."""
+    from tests.helpers import oracle_prefill
+    cfg = W.TINY
+    w = W.make_weights(cfg, 0, perturb_affine=True)
+    prompt_len, n_new = 40, 48
+    prompt = W.prefix_tokens(prompt_len, cfg.vocab, seed=5)
+    om = oracle.Model(cfg, w)
+    kc, vc, _ = oracle_prefill(om, prompt[:-1], prompt_len + n_new + 8)
+    P, root = prompt_len - 1, int(prompt[-1])
+    kt, vt = om.kv(1), om.kv(1)
+    ref, gaps = [], []
+    while len(ref) < n_new:
+        lg = oracle.tree_verify(om, kc, vc, P, [root], [-1], kt, vt)
+        top = np.sort(lg[0])
+        gaps.append(float(top[-1] - top[-2]))
+        path, nxt = oracle.tree_accept(oracle.GREEDY, [root], [-1], lg)
+        oracle.kv_commit(om, kc, vc, P, kt, vt, path)
+        P += len(path)
+        ref.append(nxt)
+        root = nxt
+    assert min(gaps) > 1e-3, min(gaps)
+
+    m = ssd.Model(cfg, w)
+    draft = m.prefix_view(1)
+    max_ctx = prompt_len + n_new + 80
+    o = ssd.Session(m, max_ctx, 64)
+    d = ssd.Session(draft, max_ctx, 64, o.k_cache, o.v_cache)
+    b = S.GpuBackend(o, d)
+    P2 = b.prefill(prompt[:-1])
+    stream = S.bigram_stream(cfg.vocab, 2048, seed=4)
+    preds = np.concatenate([b.greedy_predictions(stream[i:i + 64]) for i in range(0, 2048, 64)])
+    succ = S.bigram_table(stream, preds, cfg.vocab)
+    st = S.staged_greedy(b, P2, int(prompt[-1]), n_new, succ)
+    assert o.error_count() == 0 and d.error_count() == 0
+    print(f"staged {st.steps} steps, accepted {sum(st.accepted)}, min oracle gap {min(gaps):.3g}")
+    assert st.tokens == ref
+    assert sum(st.accepted) > 0
