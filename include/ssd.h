@@ -159,6 +159,21 @@ ssd_status ssd_tree_accept(ssd_kv *kv, const ssd_tree *tree, const float *draft_
                            uint64_t rng_seed, int32_t *accepted_path, int32_t *path_len, int32_t *next_token,
                            void *stream);
 
+/* The accept walk of ssd_tree_accept (same arguments, same outputs, same
+ * kernels) for callers that cannot allocate device memory: code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc.  It
+ * needs no session and calls no allocating routine: its scratch (the staged
+ * tree, argmax partials, the sampling walk's float64 rows) is one file-scope
+ * device array of 1,646,592 bytes that every GPU the library runs on holds
+ * until the process ends, and the tree reaches the device inside the kernel
+ * arguments.  Limits: n_nodes <= 256 and vocab <= 65536 (SSD_E_CAPACITY
+ * beyond).  All calls on one GPU share that GPU's array: calls that overlap
+ * on one GPU (two streams, or two host threads) race; calls ordered on one
+ * stream do not.  Errors: as ssd_tree_accept, plus SSD_E_CAPACITY. */
+ssd_status ssd_tree_accept_noalloc(const ssd_tree *tree, const float *draft_probs, const float *oracle_logits,
+                                   uint64_t rng_seed, int32_t *accepted_path, int32_t *path_len,
+                                   int32_t *next_token, void *stream);
+
 /* Appends tree scratch rows accepted_path[0..*path_len-1] (device arrays, as
  * written by ssd_tree_accept) to cache rows prefix_len.. (Sec. 3.1).  Reads
  * the path on the device, so no host sync is needed between accept and

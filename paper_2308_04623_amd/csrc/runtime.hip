@@ -12,6 +12,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -1064,6 +1065,115 @@ extern "C" ssd_status ssd_tree_accept(ssd_kv* kv, const ssd_tree* tree, const fl
                                  accepted_path, path_len, next_token, s));
   }
   return release_slot(kv, slot, s);
+}
+
+// ------------------------------------------------------------------ accept without allocation
+//
+// For callers that cannot allocate device memory (code under HIP graph
+// capture, tight serving loops, harnesses that forbid hipMalloc): the accept
+// walk with its scratch in one file-scope device array instead of a
+// session's workspace.  The array holds the staged tree, the argmax partials
+// and results, and the sampling walk's three float64 vocabulary rows; every
+// kernel writes what it later reads, so nothing needs clearing between calls.
+// Each device gets its own copy of the array at its own address, fetched once
+// per device with hipGetSymbolAddress; every call on a device shares it, so
+// calls that overlap on one device (two streams, or two host threads) race.
+constexpr int kNaMaxNodes = 256;
+constexpr int kNaMaxVocab = 65536;
+constexpr size_t kNaTreeOfs = 0;                                  // tokens, parents, depth: int32[3][kNaMaxNodes]
+constexpr size_t kNaArgOfs = 4096;                                // argmax results: int32[kNaMaxNodes]
+constexpr size_t kNaWorkOfs = 8192;                               // argmax partials
+constexpr size_t kNaWorkBytes = (size_t)kNaMaxNodes * ((kNaMaxVocab + 2047) / 2048) * 8;
+constexpr size_t kNaRowsOfs = kNaWorkOfs + kNaWorkBytes;          // r, p, qq: float64[3][kNaMaxVocab]
+constexpr size_t kNaScratchBytes = kNaRowsOfs + (size_t)3 * kNaMaxVocab * 8;
+static_assert(kNaScratchBytes <= (2u << 20), "the no-allocation scratch is at most 2 MiB per device");
+static __device__ __align__(256) unsigned char scratch[kNaScratchBytes];
+
+// the tree travels in the kernel's arguments (no host-to-device copy)
+struct NaTree {
+  int32_t tokens[kNaMaxNodes];
+  int32_t parents[kNaMaxNodes];
+  int32_t n;
+};
+
+// tokens, parents and depths into the scratch's tree rows (validated on the host)
+__global__ __launch_bounds__(256) void na_tree_kernel(NaTree t, int32_t* out) {
+  const int n = t.n;
+  for (int i = threadIdx.x; i < n; i += blockDim.x) {
+    out[i] = t.tokens[i];
+    out[kNaMaxNodes + i] = t.parents[i];
+  }
+  if (threadIdx.x == 0) {
+    int32_t* dep = out + 2 * kNaMaxNodes;
+    dep[0] = 0;
+    for (int i = 1; i < n; ++i) dep[i] = dep[t.parents[i]] + 1;
+  }
+}
+
+static std::mutex g_na_mu;
+static void* g_na_ptr[64] = {};
+
+// this device's address of `scratch` (looked up once per device)
+static ssd_status na_scratch(unsigned char** out) {
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  if (dev < 0 || dev >= 64) return fail(SSD_E_DEVICE, "device index beyond 63");
+  std::lock_guard<std::mutex> lk(g_na_mu);
+  if (!g_na_ptr[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(SSD_E_DEVICE, std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(e));
+    g_na_ptr[dev] = p;
+  }
+  *out = (unsigned char*)g_na_ptr[dev];
+  return SSD_OK;
+}
+
+extern "C" ssd_status ssd_tree_accept_noalloc(const ssd_tree* tree, const float* draft_probs,
+                                              const float* oracle_logits, uint64_t rng_seed, int32_t* accepted_path,
+                                              int32_t* path_len, int32_t* next_token, void* stream) {
+  if (!tree || !oracle_logits || !accepted_path || !path_len || !next_token)
+    return fail(SSD_E_INVALID_ARG, "null argument");
+  const int n = tree->n_nodes, V = tree->vocab;
+  if (n <= 0 || V <= 0) return fail(SSD_E_INVALID_ARG, "n_nodes and vocab must be positive");
+  if (n > kNaMaxNodes) return fail(SSD_E_CAPACITY, "n_nodes above 256 (the no-allocation accept's limit)");
+  if (V > kNaMaxVocab) return fail(SSD_E_CAPACITY, "vocab above 65536 (the no-allocation accept's limit)");
+  const bool greedy = tree->mode == SSD_ACCEPT_GREEDY;
+  if (!greedy && tree->mode != SSD_ACCEPT_SAMPLE_WOR && tree->mode != SSD_ACCEPT_SAMPLE_IID)
+    return fail(SSD_E_INVALID_ARG, "unknown accept mode");
+  if (greedy && draft_probs) return fail(SSD_E_INVALID_ARG, "draft_probs must be NULL for greedy acceptance");
+  if (!greedy && !draft_probs) return fail(SSD_E_INVALID_ARG, "draft_probs required for sampling");
+  if (!greedy && !(tree->temperature > 0.f)) return fail(SSD_E_INVALID_ARG, "temperature must be positive");
+  if (argmax_work_bytes(n, V) > kNaWorkBytes) return fail(SSD_E_CAPACITY, "argmax partials exceed the scratch");
+  int32_t md = 0;
+  ssd_status st = ssd_validate_tree(tree->tokens, tree->parent_idx, n, V, &md);
+  if (st != SSD_OK) return st;
+  unsigned char* base = nullptr;
+  st = na_scratch(&base);
+  if (st != SSD_OK) return st;
+  NaTree t{};
+  t.n = n;
+  for (int i = 0; i < n; ++i) {
+    t.tokens[i] = tree->tokens[i];
+    t.parents[i] = tree->parent_idx[i];
+  }
+  hipStream_t s = (hipStream_t)stream;
+  int32_t* dt = (int32_t*)(base + kNaTreeOfs);
+  na_tree_kernel<<<1, 256, 0, s>>>(t, dt);
+  HIP_TRY(hipGetLastError());
+  if (greedy) {
+    int32_t* g = (int32_t*)(base + kNaArgOfs);
+    HIP_TRY(launch_argmax(oracle_logits, n, V, g, base + kNaWorkOfs, s));
+    HIP_TRY(launch_greedy_walk(dt, dt + kNaMaxNodes, dt + 2 * kNaMaxNodes, n, g, accepted_path, path_len, next_token,
+                               s));
+  } else {
+    double* rows = (double*)(base + kNaRowsOfs);
+    HIP_TRY(launch_sample_accept(dt, dt + kNaMaxNodes, n, V, oracle_logits, draft_probs, (double)tree->temperature,
+                                 rng_seed, tree->mode == SSD_ACCEPT_SAMPLE_WOR ? 1 : 0, rows, rows + kNaMaxVocab,
+                                 rows + 2 * kNaMaxVocab, accepted_path, path_len, next_token, s));
+  }
+  return SSD_OK;
 }
 
 // ------------------------------------------------------------------ commit

@@ -30,7 +30,7 @@ EXPORTS = ("ssd_model_create", "ssd_model_destroy", "ssd_kv_bytes", "ssd_kv_crea
            "ssd_tree_verify", "ssd_tree_accept", "ssd_kv_commit", "ssd_kv_error_count",
            "ssd_graph_capture_verify", "ssd_graph_launch", "ssd_graph_destroy", "ssd_validate_tree",
            "ssd_tree_prep", "ssd_kv_set_options", "ssd_kv_get_options", "ssd_status_string", "ssd_last_error",
-           "ssd_model_prefix_view", "ssd_topk")
+           "ssd_model_prefix_view", "ssd_topk", "ssd_tree_accept_noalloc")
 # and every function include/ssd_diag.h declares (measurement and diagnostics)
 DIAG_EXPORTS = ("ssd_launch_gemm", "ssd_verify_path", "ssd_fused_plan", "ssd_kv_set_trace")
 
@@ -86,6 +86,7 @@ def lib():
             "ssd_kv_destroy": [vp],
             "ssd_tree_verify": [vp, vp, C.c_int32, i32p, i32p, C.c_int32, vp, vp],
             "ssd_tree_accept": [vp, C.POINTER(_Tree), vp, vp, C.c_uint64, vp, vp, vp, vp],
+            "ssd_tree_accept_noalloc": [C.POINTER(_Tree), vp, vp, C.c_uint64, vp, vp, vp, vp],
             "ssd_kv_commit": [vp, C.c_int32, vp, vp, vp],
             "ssd_kv_error_count": [vp, vp, C.POINTER(C.c_uint32)],
             "ssd_graph_capture_verify": [vp, vp, C.c_int32, i32p, i32p, C.c_int32, vp, vp, C.POINTER(vp)],
@@ -160,6 +161,21 @@ def fused_plan(n_head: int, d_model: int, d_mlp: int, vocab: int, n_tiles: int):
     _check(lib().ssd_fused_plan(n_head, d_model, d_mlp, vocab, n_tiles, tab.ctypes.data, xh.ctypes.data,
                                 xf.ctypes.data), "ssd_fused_plan")
     return tab, xh, xf
+
+
+def accept_noalloc(tokens, parent_idx, logits, out, mode: int = GREEDY, draft_probs=None,
+                   temperature: float = 1.0, seed: int = 0, stream=None):
+    """ssd_tree_accept_noalloc: the accept walk without a session or any
+    device allocation (n <= 256, vocab <= 65536).  out = (path[n],
+    path_len[1], next_token[1]) device int32 tensors the caller allocated."""
+    t, p = _i32(tokens), _i32(parent_idx)
+    path, plen, nxt = out
+    tree = _Tree(_p32(t), _p32(p), len(t), logits.shape[1], mode, float(temperature))
+    dp = C.c_void_p(draft_probs.data_ptr()) if draft_probs is not None else C.c_void_p(0)
+    _check(lib().ssd_tree_accept_noalloc(C.byref(tree), dp, C.c_void_p(logits.data_ptr()), C.c_uint64(seed),
+                                         C.c_void_p(path.data_ptr()), C.c_void_p(plen.data_ptr()),
+                                         C.c_void_p(nxt.data_ptr()), _stream(stream)), "ssd_tree_accept_noalloc")
+    return path, plen, nxt
 
 
 def kv_bytes(cfg, max_ctx: int, max_nodes: int) -> Tuple[int, int]:
