@@ -57,7 +57,9 @@ typedef enum { SSD_F32 = 0, SSD_BF16 = 1 } ssd_dtype;
 typedef enum {
   SSD_ACCEPT_GREEDY = 0,     /* argmax walk                                          */
   SSD_ACCEPT_SAMPLE_WOR = 1, /* rejection sampling; siblings were drawn without replacement */
-  SSD_ACCEPT_SAMPLE_IID = 2  /* rejection sampling; siblings were drawn independently       */
+  SSD_ACCEPT_SAMPLE_IID = 2, /* rejection sampling; siblings were drawn independently       */
+  SSD_ACCEPT_SAMPLE_DET = 3  /* rejection sampling; siblings were chosen (e.g. the draft's top
+                                tokens), each proposed with certainty: no draft rows      */
 } ssd_accept_mode;
 
 typedef struct {
@@ -96,6 +98,9 @@ typedef struct {
   int32_t vocab;
   ssd_accept_mode mode;
   float temperature; /* sampling modes: target = softmax(logits / temperature) */
+  int32_t top_k;     /* sampling modes: > 0 restricts the target to the row's top_k
+                        largest logits (ties at the cut to the lower token id,
+                        renormalised; Sec. 4 uses k = 50, T = 1); 0 = whole vocabulary */
 } ssd_tree;
 
 /* Loads a model.  Supported shapes: d_model % 32 == 0, d_mlp % 32 == 0,
@@ -147,14 +152,23 @@ ssd_status ssd_tree_verify(const ssd_model *m, ssd_kv *kv, int32_t prefix_len, c
  *  greedy: a node is kept when its parent is kept and its token is the
  *    parent's argmax (lowest token id on ties); the deepest kept node (lowest
  *    index on ties) ends the path and its argmax is the extra token.
- *  sampling: recursive rejection sampling down the tree.  draft_probs
- *    ([n_nodes][vocab], device) row u is the distribution node u's children
- *    were drawn from.  Uniforms come from Philox4x64-10 keyed by
- *    (rng_seed, 0) with counter (child index, 0, 0, 0) for the test of that
- *    child, and (rng_seed, 1) with counter (last node) for the extra token.
+ *  sampling: recursive rejection sampling down the tree.  For the two
+ *    drawn modes draft_probs ([n_nodes][vocab], device) row u is the
+ *    distribution node u's children were drawn from: child x is accepted
+ *    with probability min(1, r(x) / q(x)) (r the residual target, q the
+ *    draft row, in the without-replacement mode with the rejected tokens'
+ *    draft mass removed); on rejection r becomes max(r - q, 0).  In the
+ *    chosen mode (SSD_ACCEPT_SAMPLE_DET, draft_probs NULL) child x is
+ *    accepted with probability r(x) and on rejection x's mass leaves r.  If
+ *    no child of the last accepted node is accepted, the extra token is
+ *    drawn from the residual (the full target at a leaf).  Uniforms come
+ *    from Philox4x64-10 keyed by (rng_seed, 0) with counter
+ *    (child index, 0, 0, 0) for the test of that child, and (rng_seed, 1)
+ *    with counter (last node) for the extra token.
  * Outputs (device): accepted_path[0..*path_len-1] root first (path[0] = 0),
  * *next_token.  Emitted tokens are tokens[path[1..]] then next_token.
- * draft_probs must be NULL for greedy and non-NULL for sampling. */
+ * draft_probs must be non-NULL exactly for the two drawn modes; top_k < 0 is
+ * SSD_E_INVALID_ARG. */
 ssd_status ssd_tree_accept(ssd_kv *kv, const ssd_tree *tree, const float *draft_probs, const float *oracle_logits,
                            uint64_t rng_seed, int32_t *accepted_path, int32_t *path_len, int32_t *next_token,
                            void *stream);

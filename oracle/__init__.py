@@ -24,7 +24,7 @@ GCC_CMD = ["gcc", "-O3", "-std=c11", "-D_GNU_SOURCE", "-fopenmp", "-fPIC", "-sha
            "-ffp-contract=off", "-fno-fast-math", "-Wall", "-Wextra", "-o", _SO, _SRC, "-lm"]
 
 F32, BF16 = 0, 1
-GREEDY, SAMPLE_WOR, SAMPLE_IID = 0, 1, 2
+GREEDY, SAMPLE_WOR, SAMPLE_IID, SAMPLE_DET = 0, 1, 2, 3
 _ERR = {-1: "invalid argument", -2: "invalid tree", -3: "capacity exceeded"}
 
 LAYER_TENSORS = ("ln1_g", "ln1_b", "w_qkv", "b_qkv", "w_o", "b_o",
@@ -70,6 +70,8 @@ def _bind(L):
                                    C.c_void_p, C.c_void_p, C.c_int32, i32p, C.c_int32]
     L.ssdref_tree_accept.argtypes = [C.c_int32, i32p, i32p, C.c_int32, C.c_int32, C.POINTER(C.c_float),
                                      C.POINTER(C.c_float), C.c_double, C.c_uint64, i32p, i32p, i32p]
+    L.ssdref_tree_accept_k.argtypes = [C.c_int32, i32p, i32p, C.c_int32, C.c_int32, C.POINTER(C.c_float),
+                                       C.POINTER(C.c_float), C.c_double, C.c_int32, C.c_uint64, i32p, i32p, i32p]
     L.ssdref_philox4x64_10.argtypes = [C.POINTER(C.c_uint64), C.POINTER(C.c_uint64), C.POINTER(C.c_uint64)]
     L.ssdref_philox4x64_10.restype = None
     L.ssdref_uniform.argtypes = [C.c_uint64, C.c_uint64, C.c_uint64]
@@ -212,8 +214,10 @@ def kv_commit(model: Model, k_cache: np.ndarray, v_cache: np.ndarray, prefix_len
 
 def tree_accept(mode: int, tokens: Sequence[int], parent_idx: Sequence[int], logits: np.ndarray,
                 draft_probs: Optional[np.ndarray] = None, temperature: float = 1.0,
-                seed: int = 0) -> Tuple[np.ndarray, int]:
-    """Returns (path root-first, next_token)."""
+                seed: int = 0, top_k: int = 0) -> Tuple[np.ndarray, int]:
+    """Returns (path root-first, next_token).  top_k > 0 restricts every
+    sampling target to the row's top_k logits; mode SAMPLE_DET takes no
+    draft_probs (children chosen, not drawn)."""
     t, p = _i32(tokens), _i32(parent_idx)
     n = len(t)
     lg = np.ascontiguousarray(logits, dtype=np.float32)
@@ -223,10 +227,10 @@ def tree_accept(mode: int, tokens: Sequence[int], parent_idx: Sequence[int], log
     plen = np.zeros(1, dtype=np.int32)
     nxt = np.zeros(1, dtype=np.int32)
     fp = C.POINTER(C.c_float)
-    rc = lib().ssdref_tree_accept(mode, _ptr(t, C.POINTER(C.c_int32)), _ptr(p, C.POINTER(C.c_int32)), n, vocab,
-                                  None if dp is None else _ptr(dp, fp), _ptr(lg, fp), float(temperature),
-                                  C.c_uint64(seed), _ptr(path, C.POINTER(C.c_int32)),
-                                  _ptr(plen, C.POINTER(C.c_int32)), _ptr(nxt, C.POINTER(C.c_int32)))
+    rc = lib().ssdref_tree_accept_k(mode, _ptr(t, C.POINTER(C.c_int32)), _ptr(p, C.POINTER(C.c_int32)), n, vocab,
+                                    None if dp is None else _ptr(dp, fp), _ptr(lg, fp), float(temperature),
+                                    int(top_k), C.c_uint64(seed), _ptr(path, C.POINTER(C.c_int32)),
+                                    _ptr(plen, C.POINTER(C.c_int32)), _ptr(nxt, C.POINTER(C.c_int32)))
     _check(rc, "tree_accept")
     return path[:plen[0]].copy(), int(nxt[0])
 

@@ -376,19 +376,47 @@ static int32_t argmax_lowest(const float *row, int32_t V) {
   return best;
 }
 
-/* p = softmax(logits / T) in fp64 */
-static void softmax_t(const float *row, int32_t V, double T, double *p) {
-  double mx = (double)row[0] / T;
-  for (int32_t v = 1; v < V; ++v) {
+/* keep[v] = token v is among the k largest logits of the row, ties at the
+ * cut to the lower id (k = 0 or k >= V: every token): the row's ids sorted
+ * by (logit descending, id ascending), the first k kept */
+static const float *g_sort_row; /* the row qsort compares (calls are not concurrent) */
+static int by_logit_then_id(const void *a, const void *b) {
+  const int32_t i = *(const int32_t *)a, j = *(const int32_t *)b;
+  if (g_sort_row[i] > g_sort_row[j]) return -1;
+  if (g_sort_row[i] < g_sort_row[j]) return 1;
+  return (i > j) - (i < j);
+}
+
+static void top_k_mask(const float *row, int32_t V, int32_t k, uint8_t *keep) {
+  if (k <= 0 || k >= V) {
+    memset(keep, 1, (size_t)V);
+    return;
+  }
+  int32_t *ids = (int32_t *)malloc(sizeof(int32_t) * V);
+  for (int32_t v = 0; v < V; ++v) ids[v] = v;
+  g_sort_row = row;
+  qsort(ids, (size_t)V, sizeof(int32_t), by_logit_then_id);
+  memset(keep, 0, (size_t)V);
+  for (int32_t i = 0; i < k; ++i) keep[ids[i]] = 1;
+  free(ids);
+}
+
+/* p = softmax(logits / T) in fp64, over the top-k tokens only (k = 0: all) */
+static void softmax_t(const float *row, int32_t V, double T, int32_t k, double *p) {
+  uint8_t *keep = (uint8_t *)malloc((size_t)V);
+  top_k_mask(row, V, k, keep);
+  double mx = -INFINITY;
+  for (int32_t v = 0; v < V; ++v) {
     double z = (double)row[v] / T;
-    if (z > mx) mx = z;
+    if (keep[v] && z > mx) mx = z;
   }
   double s = 0.0;
   for (int32_t v = 0; v < V; ++v) {
-    p[v] = exp((double)row[v] / T - mx);
+    p[v] = keep[v] ? exp((double)row[v] / T - mx) : 0.0;
     s += p[v];
   }
   for (int32_t v = 0; v < V; ++v) p[v] /= s;
+  free(keep);
 }
 
 /* smallest v with r[0] + ... + r[v] > U * Z (ascending fp64 sum); if rounding
@@ -408,11 +436,23 @@ static int32_t sample_cdf(const double *r, int32_t V, double Z, double U) {
 int ssdref_tree_accept(int32_t mode, const int32_t *tokens, const int32_t *parent_idx, int32_t n_nodes,
                        int32_t vocab, const float *draft_probs, const float *logits, double temperature,
                        uint64_t seed, int32_t *path, int32_t *path_len, int32_t *next_token) {
+  if (mode == SSDREF_ACCEPT_SAMPLE_DET) return SSDREF_E_ARG;
+  return ssdref_tree_accept_k(mode, tokens, parent_idx, n_nodes, vocab, draft_probs, logits, temperature, 0, seed,
+                              path, path_len, next_token);
+}
+
+int ssdref_tree_accept_k(int32_t mode, const int32_t *tokens, const int32_t *parent_idx, int32_t n_nodes,
+                         int32_t vocab, const float *draft_probs, const float *logits, double temperature,
+                         int32_t top_k, uint64_t seed, int32_t *path, int32_t *path_len, int32_t *next_token) {
   if (!tokens || !parent_idx || !logits || !path || !path_len || !next_token) return SSDREF_E_ARG;
-  if (n_nodes <= 0 || vocab <= 0) return SSDREF_E_ARG;
-  if (mode != SSDREF_ACCEPT_GREEDY && mode != SSDREF_ACCEPT_SAMPLE_WOR && mode != SSDREF_ACCEPT_SAMPLE_IID)
+  if (n_nodes <= 0 || vocab <= 0 || top_k < 0) return SSDREF_E_ARG;
+  if (mode != SSDREF_ACCEPT_GREEDY && mode != SSDREF_ACCEPT_SAMPLE_WOR && mode != SSDREF_ACCEPT_SAMPLE_IID &&
+      mode != SSDREF_ACCEPT_SAMPLE_DET)
     return SSDREF_E_ARG;
-  if (mode != SSDREF_ACCEPT_GREEDY && (!draft_probs || !(temperature > 0.0))) return SSDREF_E_ARG;
+  const int det = mode == SSDREF_ACCEPT_SAMPLE_DET;
+  if (mode != SSDREF_ACCEPT_GREEDY && !(temperature > 0.0)) return SSDREF_E_ARG;
+  if (mode != SSDREF_ACCEPT_GREEDY && !det && !draft_probs) return SSDREF_E_ARG;
+  if (det && draft_probs) return SSDREF_E_ARG;
   const int32_t n = n_nodes, V = vocab;
   int32_t *depth = (int32_t *)malloc(sizeof(int32_t) * n);
   int rc = ssdref_tree_info(parent_idx, n, depth, NULL);
@@ -454,14 +494,16 @@ int ssdref_tree_accept(int32_t mode, const int32_t *tokens, const int32_t *paren
   double Z = 1.0;
   path[len++] = 0;
   for (;;) {
-    softmax_t(logits + (size_t)u * V, V, temperature, p);
+    softmax_t(logits + (size_t)u * V, V, temperature, top_k, p);
     memcpy(r, p, sizeof(double) * V);
     Z = 1.0;
-    const float *q = draft_probs + (size_t)u * V;
     double Zq = 0.0;
-    for (int32_t v = 0; v < V; ++v) {
-      qq[v] = (double)q[v];
-      Zq += qq[v];
+    if (!det) {
+      const float *q = draft_probs + (size_t)u * V;
+      for (int32_t v = 0; v < V; ++v) {
+        qq[v] = (double)q[v];
+        Zq += qq[v];
+      }
     }
     int32_t accepted = -1;
     for (int32_t c = u + 1; c < n; ++c) {
@@ -469,7 +511,9 @@ int ssdref_tree_accept(int32_t mode, const int32_t *tokens, const int32_t *paren
       const int32_t xt = tokens[c];
       const double U = ssdref_uniform(seed, 0, (uint64_t)c);
       int acc;
-      if (qq[xt] == 0.0)
+      if (det) /* the candidate was proposed with certainty */
+        acc = Z > 0.0 && U < r[xt] / Z;
+      else if (qq[xt] == 0.0)
         acc = r[xt] > 0.0;
       else
         acc = U < (r[xt] / Z) / (qq[xt] / Zq);
@@ -478,6 +522,13 @@ int ssdref_tree_accept(int32_t mode, const int32_t *tokens, const int32_t *paren
         break;
       }
       double nz = 0.0;
+      if (det) {
+        /* rejected: the candidate's token leaves the residual */
+        r[xt] = 0.0;
+        for (int32_t v = 0; v < V; ++v) nz += r[v];
+        Z = nz;
+        continue;
+      }
       for (int32_t v = 0; v < V; ++v) {
         double t = r[v] / Z - qq[v] / Zq;
         r[v] = t > 0.0 ? t : 0.0;

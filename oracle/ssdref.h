@@ -57,6 +57,7 @@ extern "C" {
 #define SSDREF_ACCEPT_GREEDY 0
 #define SSDREF_ACCEPT_SAMPLE_WOR 1 /* siblings were drawn without replacement */
 #define SSDREF_ACCEPT_SAMPLE_IID 2 /* siblings were drawn independently      */
+#define SSDREF_ACCEPT_SAMPLE_DET 3 /* siblings were chosen, not drawn (e.g. the draft's top tokens) */
 
 typedef struct {
   int32_t n_layer, d_model, n_head, d_mlp, vocab, n_pos;
@@ -115,6 +116,21 @@ int ssdref_kv_commit(const ssdref_config *cfg, void *k_cache, void *v_cache, int
 int ssdref_tree_accept(int32_t mode, const int32_t *tokens, const int32_t *parent_idx, int32_t n_nodes,
                        int32_t vocab, const float *draft_probs, const float *logits, double temperature,
                        uint64_t seed, int32_t *path, int32_t *path_len, int32_t *next_token);
+
+/* The same walk with two sampling variants (Sec. 4 evaluates top-k sampling
+ * with k = 50, T = 1):
+ *  top_k > 0: the target at node u is softmax(logits[u] / temperature) over
+ *    the top_k largest logits of the row only (ties at the cut go to the
+ *    lower token id), zero elsewhere; top_k = 0 keeps the whole vocabulary.
+ *    Greedy acceptance ignores it.
+ *  mode SAMPLE_DET: the children of a node were chosen deterministically
+ *    (draft_probs must be NULL): each child in turn is accepted with
+ *    probability r(x) / Z (the residual target mass at its token); on
+ *    rejection that token's mass is removed.  The extra token is drawn from
+ *    the residual, as in the other sampling modes. */
+int ssdref_tree_accept_k(int32_t mode, const int32_t *tokens, const int32_t *parent_idx, int32_t n_nodes,
+                         int32_t vocab, const float *draft_probs, const float *logits, double temperature,
+                         int32_t top_k, uint64_t seed, int32_t *path, int32_t *path_len, int32_t *next_token);
 
 /* Philox4x64-10 (Salmon, Moraes, Dror, Shaw, SC'11): out = bijection(ctr; key). */
 void ssdref_philox4x64_10(const uint64_t key[2], const uint64_t ctr[4], uint64_t out[4]);

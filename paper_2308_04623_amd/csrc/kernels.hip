@@ -1545,37 +1545,123 @@ __device__ double block_max_d(double v, double* red) {
   return r;
 }
 
+// order-preserving key of a logit: a larger key is a larger value (-0 and
+// +0 map to the same key, as they compare equal)
+__device__ __forceinline__ unsigned mono_key(float f) {
+  const unsigned u = __float_as_uint(f == 0.f ? 0.f : f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// The top-k cut of one row (every thread takes its contiguous chunk
+// [v0, v1)): the k-th largest key thr (radix select, 8 bits per pass from the
+// top), how many of the tokens whose key equals thr are kept (take; lowest ids
+// first) and how many such ties lie in lower threads' chunks (tie_base).  A
+// token is kept iff its key exceeds thr, or equals it with tie rank < take.
+__device__ void topk_cut(const float* row, int v0, int v1, int k, unsigned* hist, int* scan, int* sh2,
+                         unsigned& thr, int& take, int& tie_base) {
+  const int tid = threadIdx.x;
+  unsigned prefix = 0, mask = 0;
+  int need = k;
+  for (int pass = 0; pass < 4; ++pass) {
+    const int shift = 24 - 8 * pass;
+    for (int i = tid; i < 256; i += SA_THREADS) hist[i] = 0;
+    __syncthreads();
+    for (int v = v0; v < v1; ++v) {
+      const unsigned key = mono_key(row[v]);
+      if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    if (tid == 0) {
+      int cum = 0, d = 255;
+      for (; d > 0; --d) {
+        if (cum + (int)hist[d] >= need) break;
+        cum += (int)hist[d];
+      }
+      sh2[0] = d;
+      sh2[1] = need - cum;
+    }
+    __syncthreads();
+    prefix |= (unsigned)sh2[0] << shift;
+    mask |= 255u << shift;
+    need = sh2[1];
+    __syncthreads();
+  }
+  thr = prefix;
+  take = need;
+  int cnt = 0;
+  for (int v = v0; v < v1; ++v) cnt += mono_key(row[v]) == thr;
+  scan[tid] = cnt;
+  __syncthreads();
+  for (int off = 1; off < SA_THREADS; off <<= 1) {
+    const int t = tid >= off ? scan[tid - off] : 0;
+    __syncthreads();
+    scan[tid] += t;
+    __syncthreads();
+  }
+  tie_base = scan[tid] - cnt;
+  __syncthreads();
+}
+
+// Recursive rejection sampling down the tree (Sec. 2.3 over the tree batch
+// of Sec. 3.1), one workgroup.  mode: 1 siblings drawn without replacement
+// from draft row u, 2 drawn independently, 3 chosen (each child proposed with
+// certainty; no draft rows).  topk > 0 restricts every target to the row's
+// topk largest logits (ties at the cut to the lower id).
 __global__ __launch_bounds__(SA_THREADS) void sample_accept_kernel(
     const int* __restrict__ tokens, const int* __restrict__ parents, int N, int V, const float* __restrict__ logits,
-    const float* __restrict__ draft, double T, uint64_t seed, int wor, double* __restrict__ r, double* __restrict__ p,
-    double* __restrict__ qq, int* __restrict__ path, int* __restrict__ path_len, int* __restrict__ next) {
+    const float* __restrict__ draft, double T, uint64_t seed, int mode, int topk, double* __restrict__ r,
+    double* __restrict__ p, double* __restrict__ qq, int* __restrict__ path, int* __restrict__ path_len,
+    int* __restrict__ next) {
   __shared__ double red[SA_THREADS];
-  __shared__ int sh_choice;
+  __shared__ int scan[SA_THREADS];
+  __shared__ unsigned hist[256];
+  __shared__ int sh2[2];
   const int tid = threadIdx.x;
   const int C = (V + SA_THREADS - 1) / SA_THREADS;
-  const int v0 = tid * C, v1 = min(V, v0 + C);
+  const int v0 = min(V, tid * C), v1 = min(V, v0 + C);
+  const bool wor = mode == 1, det = mode == 3;
+  const bool cut = topk > 0 && topk < V;
   int u = 0, len = 1;
   if (tid == 0) path[0] = 0;
   double Z = 1.0;
   for (;;) {
     const float* row = logits + (size_t)u * V;
+    unsigned thr = 0;
+    int take = 0, tie_rank = 0;
+    if (cut) topk_cut(row, v0, v1, topk, hist, scan, sh2, thr, take, tie_rank);
+    // p = softmax(row / T) over the kept tokens
     double mx = -INFINITY;
-    for (int v = v0; v < v1; ++v) mx = fmax(mx, (double)row[v] / T);
+    int tr = tie_rank;
+    for (int v = v0; v < v1; ++v) {
+      bool keep = true;
+      if (cut) {
+        const unsigned key = mono_key(row[v]);
+        keep = key > thr || (key == thr && tr++ < take);
+      }
+      if (keep) mx = fmax(mx, (double)row[v] / T);
+    }
     mx = block_max_d(mx, red);
     double s = 0.0;
+    tr = tie_rank;
     for (int v = v0; v < v1; ++v) {
-      const double e = exp((double)row[v] / T - mx);
+      bool keep = true;
+      if (cut) {
+        const unsigned key = mono_key(row[v]);
+        keep = key > thr || (key == thr && tr++ < take);
+      }
+      const double e = keep ? exp((double)row[v] / T - mx) : 0.0;
       p[v] = e;
       s += e;
     }
     const double S = block_sum_chunks(s, red);
-    const float* q = draft + (size_t)u * V;
     double sq = 0.0;
     for (int v = v0; v < v1; ++v) {
       p[v] = p[v] / S;
       r[v] = p[v];
-      qq[v] = (double)q[v];
-      sq += qq[v];
+      if (!det) {
+        qq[v] = (double)draft[(size_t)u * V + v];
+        sq += qq[v];
+      }
     }
     double Zq = block_sum_chunks(sq, red);  // includes the barrier that publishes r, qq
     Z = 1.0;
@@ -1584,14 +1670,28 @@ __global__ __launch_bounds__(SA_THREADS) void sample_accept_kernel(
       if (parents[c] != u) continue;
       const int x = tokens[c];
       const double U = philox_uniform(seed, 0, (uint64_t)c);
-      const double rx = r[x], qx = qq[x];
-      const bool acc = (qx == 0.0) ? (rx > 0.0) : (U < (rx / Z) / (qx / Zq));
+      const double rx = r[x];
+      bool acc;
+      if (det) {
+        acc = Z > 0.0 && U < rx / Z;
+      } else {
+        const double qx = qq[x];
+        acc = (qx == 0.0) ? (rx > 0.0) : (U < (rx / Z) / (qx / Zq));
+      }
       if (acc) {
         accepted = c;
         break;
       }
       __syncthreads();  // everyone has read r[x], qq[x]
       double nz = 0.0;
+      if (det) {
+        // the rejected candidate's token leaves the residual
+        if (tid == 0) r[x] = 0.0;
+        __syncthreads();
+        for (int v = v0; v < v1; ++v) nz += r[v];
+        Z = block_sum_chunks(nz, red);
+        continue;
+      }
       for (int v = v0; v < v1; ++v) {
         const double t = r[v] / Z - qq[v] / Zq;
         r[v] = t > 0.0 ? t : 0.0;
@@ -1624,16 +1724,14 @@ __global__ __launch_bounds__(SA_THREADS) void sample_accept_kernel(
     if (w[v] > 0.0) lastpos = v;
   }
   red[tid] = cs;
-  __shared__ int last_sh[SA_THREADS];
-  last_sh[tid] = lastpos;
+  scan[tid] = lastpos;
   __syncthreads();
   if (tid == 0) {
     double run = 0.0;
-    int choice = -1, last = 0;
+    int choice = -1;
     for (int t = 0; t < SA_THREADS && choice < 0; ++t) {
-      if (last_sh[t] >= 0) last = last_sh[t];
       if (run + red[t] > target) {
-        const int a = t * C, b = min(V, a + C);
+        const int a = min(V, t * C), b = min(V, a + C);
         double c2 = run;
         for (int v = a; v < b; ++v) {
           c2 += w[v];
@@ -1646,24 +1744,25 @@ __global__ __launch_bounds__(SA_THREADS) void sample_accept_kernel(
       run += red[t];
     }
     if (choice < 0) {
+      // rounding left no crossing: the last token with positive weight
+      choice = 0;
       for (int t = SA_THREADS - 1; t >= 0; --t)
-        if (last_sh[t] >= 0) {
-          last = last_sh[t];
+        if (scan[t] >= 0) {
+          choice = scan[t];
           break;
         }
-      choice = last;
     }
-    sh_choice = choice;
     *path_len = len;
     *next = choice;
   }
 }
 
 hipError_t launch_sample_accept(const int* tokens, const int* parents, int N, int V, const float* logits,
-                                const float* draft, double temperature, uint64_t seed, int wor, double* r, double* p,
-                                double* qq, int* path, int* path_len, int* next, hipStream_t s) {
-  sample_accept_kernel<<<1, SA_THREADS, 0, s>>>(tokens, parents, N, V, logits, draft, temperature, seed, wor, r, p,
-                                                qq, path, path_len, next);
+                                const float* draft, double temperature, uint64_t seed, int mode, int topk, double* r,
+                                double* p, double* qq, int* path, int* path_len, int* next, hipStream_t s) {
+  if (mode < 1 || mode > 3 || (mode == 3) != (draft == nullptr)) return hipErrorInvalidValue;
+  sample_accept_kernel<<<1, SA_THREADS, 0, s>>>(tokens, parents, N, V, logits, draft, temperature, seed, mode, topk,
+                                                r, p, qq, path, path_len, next);
   return hipGetLastError();
 }
 

@@ -1023,6 +1023,21 @@ extern "C" ssd_status ssd_topk(ssd_kv* kv, const float* logits, int32_t n_rows, 
 
 // ------------------------------------------------------------------ accept
 
+// accept-mode rules shared by both accept entry points
+static ssd_status check_accept_mode(const ssd_tree* tree, const float* draft_probs) {
+  const int mode = tree->mode;
+  if (mode != SSD_ACCEPT_GREEDY && mode != SSD_ACCEPT_SAMPLE_WOR && mode != SSD_ACCEPT_SAMPLE_IID &&
+      mode != SSD_ACCEPT_SAMPLE_DET)
+    return fail(SSD_E_INVALID_ARG, "unknown accept mode");
+  const bool drawn = mode == SSD_ACCEPT_SAMPLE_WOR || mode == SSD_ACCEPT_SAMPLE_IID;
+  if (drawn && !draft_probs) return fail(SSD_E_INVALID_ARG, "draft_probs required when siblings were drawn");
+  if (!drawn && draft_probs) return fail(SSD_E_INVALID_ARG, "draft_probs must be NULL for this accept mode");
+  if (mode != SSD_ACCEPT_GREEDY && !(tree->temperature > 0.f))
+    return fail(SSD_E_INVALID_ARG, "temperature must be positive");
+  if (tree->top_k < 0) return fail(SSD_E_INVALID_ARG, "top_k must be >= 0");
+  return SSD_OK;
+}
+
 extern "C" ssd_status ssd_tree_accept(ssd_kv* kv, const ssd_tree* tree, const float* draft_probs,
                                       const float* oracle_logits, uint64_t rng_seed, int32_t* accepted_path,
                                       int32_t* path_len, int32_t* next_token, void* stream) {
@@ -1032,14 +1047,11 @@ extern "C" ssd_status ssd_tree_accept(ssd_kv* kv, const ssd_tree* tree, const fl
   if (n <= 0 || V <= 0) return fail(SSD_E_INVALID_ARG, "n_nodes and vocab must be positive");
   if (n > kv->max_nodes) return fail(SSD_E_CAPACITY, "n_nodes above the session's max_nodes");
   if (V > kv->m->cfg.vocab) return fail(SSD_E_CAPACITY, "vocab above the model's vocab");
+  ssd_status st = check_accept_mode(tree, draft_probs);
+  if (st != SSD_OK) return st;
   const bool greedy = tree->mode == SSD_ACCEPT_GREEDY;
-  if (!greedy && tree->mode != SSD_ACCEPT_SAMPLE_WOR && tree->mode != SSD_ACCEPT_SAMPLE_IID)
-    return fail(SSD_E_INVALID_ARG, "unknown accept mode");
-  if (greedy && draft_probs) return fail(SSD_E_INVALID_ARG, "draft_probs must be NULL for greedy acceptance");
-  if (!greedy && !draft_probs) return fail(SSD_E_INVALID_ARG, "draft_probs required for sampling");
-  if (!greedy && !(tree->temperature > 0.f)) return fail(SSD_E_INVALID_ARG, "temperature must be positive");
   int32_t md = 0;
-  ssd_status st = ssd_validate_tree(tree->tokens, tree->parent_idx, n, V, &md);
+  st = ssd_validate_tree(tree->tokens, tree->parent_idx, n, V, &md);
   if (st != SSD_OK) return st;
   hipStream_t s = (hipStream_t)stream;
   char* host = nullptr;
@@ -1061,8 +1073,8 @@ extern "C" ssd_status ssd_tree_accept(ssd_kv* kv, const ssd_tree* tree, const fl
     HIP_TRY(launch_greedy_walk(dt, dt + n, dt + 2 * n, n, kv->d_argmax, accepted_path, path_len, next_token, s));
   } else {
     HIP_TRY(launch_sample_accept(dt, dt + n, n, V, oracle_logits, draft_probs, (double)tree->temperature, rng_seed,
-                                 tree->mode == SSD_ACCEPT_SAMPLE_WOR ? 1 : 0, kv->d_r, kv->d_p, kv->d_qq,
-                                 accepted_path, path_len, next_token, s));
+                                 (int)tree->mode, tree->top_k, kv->d_r, kv->d_p, kv->d_qq, accepted_path, path_len,
+                                 next_token, s));
   }
   return release_slot(kv, slot, s);
 }
@@ -1139,15 +1151,12 @@ extern "C" ssd_status ssd_tree_accept_noalloc(const ssd_tree* tree, const float*
   if (n <= 0 || V <= 0) return fail(SSD_E_INVALID_ARG, "n_nodes and vocab must be positive");
   if (n > kNaMaxNodes) return fail(SSD_E_CAPACITY, "n_nodes above 256 (the no-allocation accept's limit)");
   if (V > kNaMaxVocab) return fail(SSD_E_CAPACITY, "vocab above 65536 (the no-allocation accept's limit)");
+  ssd_status st = check_accept_mode(tree, draft_probs);
+  if (st != SSD_OK) return st;
   const bool greedy = tree->mode == SSD_ACCEPT_GREEDY;
-  if (!greedy && tree->mode != SSD_ACCEPT_SAMPLE_WOR && tree->mode != SSD_ACCEPT_SAMPLE_IID)
-    return fail(SSD_E_INVALID_ARG, "unknown accept mode");
-  if (greedy && draft_probs) return fail(SSD_E_INVALID_ARG, "draft_probs must be NULL for greedy acceptance");
-  if (!greedy && !draft_probs) return fail(SSD_E_INVALID_ARG, "draft_probs required for sampling");
-  if (!greedy && !(tree->temperature > 0.f)) return fail(SSD_E_INVALID_ARG, "temperature must be positive");
   if (argmax_work_bytes(n, V) > kNaWorkBytes) return fail(SSD_E_CAPACITY, "argmax partials exceed the scratch");
   int32_t md = 0;
-  ssd_status st = ssd_validate_tree(tree->tokens, tree->parent_idx, n, V, &md);
+  st = ssd_validate_tree(tree->tokens, tree->parent_idx, n, V, &md);
   if (st != SSD_OK) return st;
   unsigned char* base = nullptr;
   st = na_scratch(&base);
@@ -1170,7 +1179,7 @@ extern "C" ssd_status ssd_tree_accept_noalloc(const ssd_tree* tree, const float*
   } else {
     double* rows = (double*)(base + kNaRowsOfs);
     HIP_TRY(launch_sample_accept(dt, dt + kNaMaxNodes, n, V, oracle_logits, draft_probs, (double)tree->temperature,
-                                 rng_seed, tree->mode == SSD_ACCEPT_SAMPLE_WOR ? 1 : 0, rows, rows + kNaMaxVocab,
+                                 rng_seed, (int)tree->mode, tree->top_k, rows, rows + kNaMaxVocab,
                                  rows + 2 * kNaMaxVocab, accepted_path, path_len, next_token, s));
   }
   return SSD_OK;

@@ -172,9 +172,11 @@ hipError_t launch_topk(const float* logits, int N, int V, int k, int* idx, float
                        hipStream_t s);
 hipError_t launch_greedy_walk(const int* tokens, const int* parents, const int* depth, int N, const int* g,
                               int* path, int* path_len, int* next, hipStream_t s);
+// mode: 1 without replacement, 2 independent, 3 chosen (draft == nullptr);
+// topk > 0 restricts the targets to each row's topk largest logits
 hipError_t launch_sample_accept(const int* tokens, const int* parents, int N, int V, const float* logits,
-                                const float* draft, double temperature, uint64_t seed, int wor, double* r, double* p,
-                                double* qq, int* path, int* path_len, int* next, hipStream_t s);
+                                const float* draft, double temperature, uint64_t seed, int mode, int topk, double* r,
+                                double* p, double* qq, int* path, int* path_len, int* next, hipStream_t s);
 hipError_t launch_commit(int f32, void* kc, void* vc, const void* kt, const void* vt, int LH, int max_ctx,
                          int max_nodes, int DH, int P, const int* path, const int* path_len, unsigned* err,
                          hipStream_t s);

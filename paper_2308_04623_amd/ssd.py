@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(_HERE, "libssd.so")
 
 OK, E_INVALID_ARG, E_INVALID_TREE, E_CAPACITY, E_DEVICE, E_UNSUPPORTED = 0, -1, -2, -3, -4, -5
 F32, BF16 = 0, 1
-GREEDY, SAMPLE_WOR, SAMPLE_IID = 0, 1, 2
+GREEDY, SAMPLE_WOR, SAMPLE_IID, SAMPLE_DET = 0, 1, 2, 3
 GEMM_AUTO, GEMM_VEC, GEMM_MFMA = 0, 1, 2
 
 LAYER_TENSORS = ("ln1_g", "ln1_b", "w_qkv", "b_qkv", "w_o", "b_o",
@@ -60,7 +60,7 @@ class _Options(C.Structure):
 
 class _Tree(C.Structure):
     _fields_ = [("tokens", C.POINTER(C.c_int32)), ("parent_idx", C.POINTER(C.c_int32)), ("n_nodes", C.c_int32),
-                ("vocab", C.c_int32), ("mode", C.c_int32), ("temperature", C.c_float)]
+                ("vocab", C.c_int32), ("mode", C.c_int32), ("temperature", C.c_float), ("top_k", C.c_int32)]
 
 
 _lib = None
@@ -164,13 +164,13 @@ def fused_plan(n_head: int, d_model: int, d_mlp: int, vocab: int, n_tiles: int):
 
 
 def accept_noalloc(tokens, parent_idx, logits, out, mode: int = GREEDY, draft_probs=None,
-                   temperature: float = 1.0, seed: int = 0, stream=None):
+                   temperature: float = 1.0, seed: int = 0, top_k: int = 0, stream=None):
     """ssd_tree_accept_noalloc: the accept walk without a session or any
     device allocation (n <= 256, vocab <= 65536).  out = (path[n],
     path_len[1], next_token[1]) device int32 tensors the caller allocated."""
     t, p = _i32(tokens), _i32(parent_idx)
     path, plen, nxt = out
-    tree = _Tree(_p32(t), _p32(p), len(t), logits.shape[1], mode, float(temperature))
+    tree = _Tree(_p32(t), _p32(p), len(t), logits.shape[1], mode, float(temperature), int(top_k))
     dp = C.c_void_p(draft_probs.data_ptr()) if draft_probs is not None else C.c_void_p(0)
     _check(lib().ssd_tree_accept_noalloc(C.byref(tree), dp, C.c_void_p(logits.data_ptr()), C.c_uint64(seed),
                                          C.c_void_p(path.data_ptr()), C.c_void_p(plen.data_ptr()),
@@ -361,7 +361,7 @@ class Session:
         return Graph(h, (t, p, logits))
 
     def accept(self, tokens, parent_idx, logits, mode: int = GREEDY, draft_probs=None, temperature: float = 1.0,
-               seed: int = 0, out=None, stream=None):
+               seed: int = 0, out=None, stream=None, top_k: int = 0):
         """Returns device int32 tensors (path[n], path_len[1], next_token[1])."""
         torch = _torch()
         t, p = _i32(tokens), _i32(parent_idx)
@@ -371,7 +371,7 @@ class Session:
                    torch.zeros(1, dtype=torch.int32, device=self.model.device),
                    torch.zeros(1, dtype=torch.int32, device=self.model.device))
         path, plen, nxt = out
-        tree = _Tree(_p32(t), _p32(p), n, logits.shape[1], mode, float(temperature))
+        tree = _Tree(_p32(t), _p32(p), n, logits.shape[1], mode, float(temperature), int(top_k))
         dp = C.c_void_p(draft_probs.data_ptr()) if draft_probs is not None else C.c_void_p(0)
         _check(lib().ssd_tree_accept(self.handle, C.byref(tree), dp, C.c_void_p(logits.data_ptr()), C.c_uint64(seed),
                                      C.c_void_p(path.data_ptr()), C.c_void_p(plen.data_ptr()),

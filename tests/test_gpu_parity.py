@@ -362,3 +362,33 @@ def test_float16_range_is_checked(ssd, torch):
     s.verify(0, [1, 2], [-1, 0])
     assert s.error_count() > 0
     s.close()
+
+
+@pytest.mark.parametrize("V", [512, 50257])
+@pytest.mark.parametrize("mode", ["wor", "iid", "det"])
+@pytest.mark.parametrize("k", [1, 50])
+def test_sampling_accept_topk_and_chosen_siblings_bit_exact(wide, ssd, torch, V, mode, k):
+    """Top-k targets (Sec. 4's k = 50, T = 1; ties at the cut to the lower id,
+    here made likely by rounding the logits) and siblings chosen rather than
+    drawn (the draft's top tokens; no draft rows): path and extra token
+    bit-exact against the oracle on identical logits."""
+    cfg, s = wide
+    g = np.random.default_rng(V + k + len(mode))
+    md = {"wor": ssd.SAMPLE_WOR, "iid": ssd.SAMPLE_IID, "det": ssd.SAMPLE_DET}[mode]
+    omd = {"wor": oracle.SAMPLE_WOR, "iid": oracle.SAMPLE_IID, "det": oracle.SAMPLE_DET}[mode]
+    for trial in range(8):
+        toks, par = _draft_tree(g, V, [4, 2, 2, 1], 32 if trial % 2 else 120)
+        n = len(par)
+        lg = np.round(g.standard_normal((n, V)) * 2.0, 1).astype(np.float32)
+        q = g.dirichlet(np.ones(V) * 0.3, size=n).astype(np.float32)
+        for c in range(1, n):
+            if g.random() < 0.7:     # the target's top tokens, so paths get long
+                toks[c] = int(np.lexsort((np.arange(V), -lg[par[c]]))[int(g.integers(0, min(k, 4)))])
+        dlg = torch.from_numpy(lg).cuda()
+        dq = None if mode == "det" else torch.from_numpy(q).cuda()
+        path, plen, nxt = s.accept(toks, par, dlg, mode=md, draft_probs=dq, temperature=1.0, seed=trial, top_k=k)
+        op, on = oracle.tree_accept(omd, toks, par, lg, None if mode == "det" else q, 1.0, trial, top_k=k)
+        assert path[:int(plen.item())].cpu().numpy().tolist() == op.tolist(), trial
+        assert int(nxt.item()) == on, trial
+        if k == 1:   # the target is the argmax: every emitted token is one
+            assert on == int(np.lexsort((np.arange(V), -lg[op[-1]]))[0])

@@ -40,18 +40,20 @@ def _case(g, n, V, greedy_hint):
     return toks, par, lg, q
 
 
-@pytest.mark.parametrize("mode", ["greedy", "wor", "iid"])
+@pytest.mark.parametrize("mode", ["greedy", "wor", "iid", "det"])
 def test_noalloc_accept_equals_session_accept(env, mode):
     torch, ssd, s = env
-    md = {"greedy": ssd.GREEDY, "wor": ssd.SAMPLE_WOR, "iid": ssd.SAMPLE_IID}[mode]
+    md = {"greedy": ssd.GREEDY, "wor": ssd.SAMPLE_WOR, "iid": ssd.SAMPLE_IID, "det": ssd.SAMPLE_DET}[mode]
+    top_k = 50 if mode == "det" else 0
     g = np.random.default_rng(len(mode))
     for call, (n, V) in enumerate([(256, 50257), (24, 3000)]):
         print(f"noalloc {mode} call {call}: n={n} V={V}", flush=True)
         toks, par, lg, q = _case(g, n, V, mode == "greedy")
         dlg = torch.from_numpy(lg).cuda()
-        dq = None if mode == "greedy" else torch.from_numpy(q).cuda()
-        a = s.accept(toks, par, dlg, mode=md, draft_probs=dq, temperature=1.0, seed=call)
-        b = ssd.accept_noalloc(toks, par, dlg, _outs(torch, n), mode=md, draft_probs=dq, temperature=1.0, seed=call)
+        dq = None if mode in ("greedy", "det") else torch.from_numpy(q).cuda()
+        a = s.accept(toks, par, dlg, mode=md, draft_probs=dq, temperature=1.0, seed=call, top_k=top_k)
+        b = ssd.accept_noalloc(toks, par, dlg, _outs(torch, n), mode=md, draft_probs=dq, temperature=1.0, seed=call,
+                               top_k=top_k)
         torch.cuda.synchronize()
         la, lb = int(a[1].item()), int(b[1].item())
         assert la == lb, (call, la, lb)
