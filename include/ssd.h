@@ -148,6 +148,17 @@ void ssd_kv_destroy(ssd_kv *kv);
 ssd_status ssd_tree_verify(const ssd_model *m, ssd_kv *kv, int32_t prefix_len, const int32_t *tree_tokens,
                            const int32_t *parent_idx, int32_t n_nodes, float *logits, void *stream);
 
+/* ssd_tree_verify followed by the greedy accept walk of ssd_tree_accept
+ * (SSD_ACCEPT_GREEDY) on the logits it wrote, with the same outputs as that
+ * pair of calls, bit for bit.  When the pass runs as the persistent single
+ * launch (see ssd_options), its LM head also leaves each workgroup's largest
+ * logit and token per node, so the walk needs no second read of the
+ * [n_nodes][vocab] logits (Sec. 4, greedy "deterministic" decoding).
+ * Errors: as ssd_tree_verify, plus SSD_E_INVALID_ARG for a null output. */
+ssd_status ssd_tree_verify_greedy(const ssd_model *m, ssd_kv *kv, int32_t prefix_len, const int32_t *tree_tokens,
+                                  const int32_t *parent_idx, int32_t n_nodes, float *logits, int32_t *accepted_path,
+                                  int32_t *path_len, int32_t *next_token, void *stream);
+
 /* Accept/reject walk (Sec. 2.3, 3.1) over logits from ssd_tree_verify.
  *  greedy: a node is kept when its parent is kept and its token is the
  *    parent's argmax (lowest token id on ties); the deepest kept node (lowest
@@ -224,6 +235,12 @@ ssd_status ssd_topk(ssd_kv *kv, const float *logits, int32_t n_rows, int32_t k, 
 ssd_status ssd_graph_capture_verify(const ssd_model *m, ssd_kv *kv, int32_t prefix_len, const int32_t *tree_tokens,
                                     const int32_t *parent_idx, int32_t n_nodes, float *logits, void *stream,
                                     ssd_graph **out);
+/* The same for ssd_tree_verify_greedy: the graph replays the pass and the
+ * greedy walk into the given device outputs. */
+ssd_status ssd_graph_capture_verify_greedy(const ssd_model *m, ssd_kv *kv, int32_t prefix_len,
+                                           const int32_t *tree_tokens, const int32_t *parent_idx, int32_t n_nodes,
+                                           float *logits, int32_t *accepted_path, int32_t *path_len,
+                                           int32_t *next_token, void *stream, ssd_graph **out);
 ssd_status ssd_graph_launch(ssd_graph *g, void *stream);
 void ssd_graph_destroy(ssd_graph *g);
 
@@ -242,9 +259,8 @@ ssd_status ssd_tree_prep(const int32_t *parent_idx, int32_t n, int32_t *depth, u
  *     step streams every weight once; Sec. 3.1: one step scores the whole
  *     tree).
  *     0 = automatic: the persistent single launch when the session supports
- *       it (head dimension 64, a 256-CU device with 8 XCDs, a cache of at
- *       most 16128 positions) and the tree has at most 64 nodes, else one
- *       kernel per sub-layer;
+ *       it (head dimension 64, a 256-CU device with 8 XCDs) and the tree has
+ *       at most 64 nodes, else one kernel per sub-layer;
  *     1 = always one kernel per sub-layer;
  *     2 = the persistent single launch only (up to 64 nodes):
  *       ssd_tree_verify and ssd_graph_capture_verify return SSD_E_UNSUPPORTED

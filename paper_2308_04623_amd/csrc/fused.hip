@@ -620,32 +620,30 @@ __device__ __forceinline__ void merge_tile(const FusedArgs& a, int h, int t) {
   }
 }
 
-// After a unit of (head h, tile t) stored its part: its flag (this pass and
-// layer's tag) is published once the part's stores are complete, then the
-// tile's flags are read; if all are set, this workgroup merges the tile.  The
-// unit whose flag completes last sees every flag, so each tile is merged at
-// least once; a tile merged twice gets the same values written twice.
+// After a unit of (head h, tile t) stored its part: once every wave's part
+// stores are complete, one lane counts the unit in the tile's counter with an
+// atomic increment that wraps after the tile's last unit (S prefix units +
+// the root unit); the unit that reads the count S (the last one to arrive)
+// merges the tile.  The increments of a tile are serialised at the counter,
+// so exactly one unit merges, after every part is stored, and the counter is
+// back at 0 for the next layer.  (A flag per unit, each unit reading all its
+// tile's flags after storing its own, let the two last units miss each
+// other's flags now and then, so that no unit merged: on this hardware a
+// completed store is not yet seen by another CU's load for a short time.)
 __device__ __forceinline__ void unit_done(const FusedArgs& a, const Wg& w, int l, int h, int t, int j) {
+  (void)l;
+  (void)j;
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   lds_barrier();
-  const unsigned tag = tag_of(w, l, FS_AMG);
-  unsigned* uf = a.uflag + ((size_t)h * 4 + t) * a.uf_stride;
-  if (threadIdx.x < 64) {
-    const int lane = threadIdx.x;
-    if (lane == 0) __hip_atomic_store(uf + j, tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    const unsigned v = ld_flag(uf + min(lane, a.att_units));  // (clamped: the row holds att_units + 1 flags)
-    // equality, not "reached": a unit flag is written only when its unit
-    // exists, so a flag unused for a long time may hold any older tag, and
-    // tags wrap; when this check runs no unit of the tile can hold a later
-    // tag, so equality is exact
-    const bool mine = lane > a.att_units || v == tag;
-    if (lane == 0) w.sh[6] = __all(mine);
+  if (threadIdx.x == 0) {
+    const unsigned old = __builtin_amdgcn_atomic_inc32(a.tile_ctr + (size_t)h * 4 + t, (unsigned)a.att_units,
+                                                       __ATOMIC_RELAXED, "agent");
+    w.sh[6] = old == (unsigned)a.att_units;
   }
   lds_barrier();
-  const bool all = w.sh[6] != 0;
+  const bool last = w.sh[6] != 0;
   lds_barrier();
-  if (all) {
+  if (last) {
     asm volatile("buffer_inv sc0" ::: "memory");
     merge_tile(a, h, t);
   }
@@ -743,6 +741,15 @@ __device__ __forceinline__ void epilogue(const FusedArgs& a, const Wg& w, int ep
   }
 }
 
+// The LM head's running maximum per node of this workgroup (greedy accept
+// without re-reading the logits): thread t owns epilogue slots t and t + 512,
+// i.e. row (t % 16) of node t / 16 and of node t / 16 + 32, in every row
+// block; a slot keeps its largest logit and, among equals, the lowest token.
+struct HeadBest {
+  float v[2];
+  int o[2];
+};
+
 // One GEMM task of RB row blocks: rbs[0 .. nrb) (plan entries) or, with rbs
 // null, nrb consecutive ones from rb_first; row blocks past nrb repeat the
 // last one and are not stored.
@@ -750,7 +757,7 @@ template <int NT, int RB, int U>
 __device__ __forceinline__ bool gemm_rb(const FusedArgs& a, const Wg& w, const WaitSpec& ws, int epi, int l,
                                         const int* rbs, int rb_first, int nrb, gptr<uint16_t> bias, gptr<u32x4> Wp,
                                         int KC, int M, int kc0, int kc1, const uint16_t* act, int act_kc,
-                                        float* red, const PreSpec& ps, int wofs) {
+                                        float* red, const PreSpec& ps, int wofs, HeadBest* hb) {
   constexpr int NN = 16 * NT, NCW = NWV - QW;
   // Waves 4..7 compute: wave 4 + c takes k-steps kc0 + c, kc0 + c + 4, ...,
   // and loads their weights first thing.  Waves 0..3 run the pre-stage
@@ -880,7 +887,14 @@ __device__ __forceinline__ bool gemm_rb(const FusedArgs& a, const Wg& w, const W
 #pragma unroll
       for (int ww = 1; ww < NCW; ++ww) sum += red[ww * NN * 16 + idx];
       const int o = rbv[r] * 16 + row;
-      if (node < N && o < M) epilogue(a, w, epi, l, node, o, has_bias ? sum + bf2f(bias_r[r]) : sum);
+      if (node < N && o < M) {
+        const float y = has_bias ? sum + bf2f(bias_r[r]) : sum;
+        epilogue(a, w, epi, l, node, o, y);
+        if (hb && (y > hb->v[i] || (y == hb->v[i] && o < hb->o[i]))) {
+          hb->v[i] = y;
+          hb->o[i] = o;
+        }
+      }
     }
     lds_barrier();
   }
@@ -908,16 +922,17 @@ template <int NT>
 __device__ __forceinline__ bool gemm_task(const FusedArgs& a, const Wg& w, const WaitSpec& ws, int epi, int l,
                                           const int* rbs, int rb_first, int nrb, gptr<uint16_t> bias,
                                           gptr<u32x4> Wp, int KC, int M, int kc0, int kc1, const uint16_t* act,
-                                          int act_kc, float* red, const PreSpec& ps, int wofs = 0) {
+                                          int act_kc, float* red, const PreSpec& ps, int wofs = 0,
+                                          HeadBest* hb = nullptr) {
   if (nrb <= 0) return pre_only(a, w, ps);
   if (nrb == 1)
     return gemm_rb<NT, 1, NT <= 2 ? 10 : 8>(a, w, ws, epi, l, rbs, rb_first, 1, bias, Wp, KC, M, kc0, kc1, act,
-                                           act_kc, red, ps, wofs);
+                                           act_kc, red, ps, wofs, hb);
   if (nrb == 2)
     return gemm_rb<NT, 2, NT <= 2 ? 10 : 6>(a, w, ws, epi, l, rbs, rb_first, 2, bias, Wp, KC, M, kc0, kc1, act,
-                                           act_kc, red, ps, wofs);
+                                           act_kc, red, ps, wofs, hb);
   return gemm_rb<NT, 4, NT == 1 ? 8 : NT == 2 ? 5 : 3>(a, w, ws, epi, l, rbs, rb_first, nrb, bias, Wp, KC, M, kc0, kc1, act,
-                                         act_kc, red, ps, wofs);
+                                         act_kc, red, ps, wofs, hb);
 }
 
 // ------------------------------------------------------------------ tree attention
@@ -1278,6 +1293,13 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
     return;
   }
 
+  // Rank 0 of each XCD clears the tile counters of the XCD's heads (a pass
+  // that ended early may have left counts behind).  Its stores complete
+  // before its first stage flag, and every attention unit of the XCD waits
+  // for that rank's QKV flag, so the counters are 0 before any unit counts.
+  if (w.r == 0 && (int)threadIdx.x < 4 * (a.xh[2 * w.x + 1] - a.xh[2 * w.x]))
+    __hip_atomic_store(a.tile_ctr + (size_t)a.xh[2 * w.x] * 4 + threadIdx.x, 0u, __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
   const int* p = w.plan;
   const int n_qkv = p[PL_QKV], n_wo = p[PL_WO], n_fc = p[PL_FC], n_wpr = p[PL_WPR];
   const int hb0 = p[PL_HEAD], hb1 = p[PL_HEAD + 1];
@@ -1309,6 +1331,7 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
   // parameter table (the attention stage between uses the LDS below it)
   const int wo_ofs = A_REGION + A_PART_BYTES + A_Q_BYTES + 256 + L * kLwSlots * 8;
   const bool wo_staged = NT >= 2 && n_wo > 0 && n_wo * (kh1 - kh0) <= WO_FRAGS;
+  HeadBest hbest{{-INFINITY, -INFINITY}, {0x7fffffff, 0x7fffffff}};
   const int nst = L * 8 + 2;
   for (int st = 0; st < nst; ++st) {
     const int l = st < L * 8 ? st / 8 : L;
@@ -1416,7 +1439,8 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
     }
     {
       const WaitSpec gws{ps.fid, w.x, tag_of(w, l, ps.fid), true, l, gfid};
-      if (!gemm_task<NT>(a, w, gws, epi, l, rbs, rb_first, nrb, bias, Wm, KCd, Mo, k0, k1, act, KCd, red, ps))
+      if (!gemm_task<NT>(a, w, gws, epi, l, rbs, rb_first, nrb, bias, Wm, KCd, Mo, k0, k1, act, KCd, red, ps, 0,
+                         kind == 8 ? &hbest : nullptr))
         goto out;
     }
     if (kind == 8) {
@@ -1425,8 +1449,27 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
       PreSpec nopre{};
       for (int b0 = hb0 + 4, j = 1; b0 < hb1; b0 += 4, ++j) {
         if (!gemm_task<NT>(a, w, none, FE_HEAD, L, nullptr, b0, min(4, hb1 - b0), G<uint16_t>(nullptr),
-                           G<u32x4>(a.p_head), KCd, a.V, 0, KCd, act1, KCd, red, nopre))
+                           G<u32x4>(a.p_head), KCd, a.V, 0, KCd, act1, KCd, red, nopre, 0, &hbest))
           goto out;
+      }
+      // this workgroup's maximum per node: the 16 slots of a node sit in 16
+      // consecutive lanes; (logit, token) pairs, ties to the lower token
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        float v = hbest.v[i];
+        int o = hbest.o[i];
+#pragma unroll
+        for (int m = 1; m < 16; m <<= 1) {
+          const float v2 = __shfl_xor(v, m);
+          const int o2 = __shfl_xor(o, m);
+          if (v2 > v || (v2 == v && o2 < o)) {
+            v = v2;
+            o = o2;
+          }
+        }
+        const int idx = threadIdx.x + i * NTH, node = idx >> 4;
+        if ((idx & 15) == 0 && idx < 16 * 16 * NT && node < N)
+          *(gw<u32x2>)(a.head_part + ((size_t)node * kFGroups + w.g) * 2) = (u32x2){__float_as_uint(v), (unsigned)o};
       }
     }
     signal(a, w, l, gfid, false);

@@ -1474,6 +1474,68 @@ __global__ void greedy_walk_kernel(const int* __restrict__ tokens, const int* __
   *next = g[best];
 }
 
+// Greedy accept from per-workgroup maxima (the persistent pass's LM head
+// leaves, for every node, each of G workgroups' largest logit and its token):
+// 16 threads per node reduce its G pairs (ties to the lower token), then one
+// thread walks the tree as greedy_walk_kernel does.
+__global__ __launch_bounds__(1024) void greedy_from_parts_kernel(const unsigned* __restrict__ parts, int G, int N,
+                                                                  const int* __restrict__ tokens,
+                                                                  const int* __restrict__ parents,
+                                                                  const int* __restrict__ depth,
+                                                                  int* __restrict__ path, int* __restrict__ path_len,
+                                                                  int* __restrict__ next) {
+  __shared__ int g[64];
+  __shared__ unsigned char m[64];
+  const int tid = threadIdx.x, n = tid >> 4, j = tid & 15;
+  float v = -INFINITY;
+  int o = 0x7fffffff;
+  if (n < N) {
+    for (int k = j; k < G; k += 16) {
+      const unsigned* pr = parts + ((size_t)n * G + k) * 2;
+      const float v2 = __uint_as_float(pr[0]);
+      const int o2 = (int)pr[1];
+      if (v2 > v || (v2 == v && o2 < o)) {
+        v = v2;
+        o = o2;
+      }
+    }
+  }
+#pragma unroll
+  for (int msk = 1; msk < 16; msk <<= 1) {
+    const float v2 = __shfl_xor(v, msk);
+    const int o2 = __shfl_xor(o, msk);
+    if (v2 > v || (v2 == v && o2 < o)) {
+      v = v2;
+      o = o2;
+    }
+  }
+  if (j == 0 && n < N) g[n] = o == 0x7fffffff ? 0 : o;  // (a row of NaN logits: token 0)
+  __syncthreads();
+  if (tid != 0) return;
+  m[0] = 1;
+  int best = 0;
+  for (int i = 1; i < N; ++i) {
+    const int p = parents[i];
+    m[i] = m[p] && tokens[i] == g[p];
+    if (m[i] && depth[i] > depth[best]) best = i;
+  }
+  const int len = depth[best] + 1;
+  int jj = best;
+  for (int t = len - 1; t >= 0; --t) {
+    path[t] = jj;
+    jj = parents[jj];
+  }
+  *path_len = len;
+  *next = g[best];
+}
+
+hipError_t launch_greedy_from_parts(const unsigned* parts, int G, int N, const int* tokens, const int* parents,
+                                    const int* depth, int* path, int* path_len, int* next, hipStream_t s) {
+  if (N < 1 || N > 64) return hipErrorInvalidValue;
+  greedy_from_parts_kernel<<<1, 1024, 0, s>>>(parts, G, N, tokens, parents, depth, path, path_len, next);
+  return hipGetLastError();
+}
+
 size_t argmax_work_bytes(int N, int V) { return (size_t)N * ((V + kArgmaxChunk - 1) / kArgmaxChunk) * 8; }
 
 hipError_t launch_argmax(const float* logits, int N, int V, int* g, void* work, hipStream_t s) {

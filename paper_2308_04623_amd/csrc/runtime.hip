@@ -413,13 +413,12 @@ static ssd_status fused_setup(ssd_kv* kv) {
   const size_t o_a1 = take(kFXcd * act_stride * 2), o_a2 = take(kFXcd * act_stride * 2);
   const size_t o_fo = take((size_t)kFMaxN * d * 2), o_ff = take((size_t)kFMaxN * M * 2);
   const size_t att_parts = (size_t)(kv->max_ctx + kFAttRows - 1) / kFAttRows + 1;
-  // (one wave reads a tile's unit flags: at most 64 parts)
-  if (att_parts > 64) return SSD_OK;
   const size_t o_ap = take((size_t)c.n_head * 4 * att_parts * 16 * 68 * 4);
   const size_t o_po = take((size_t)kFXcd * kFMaxN * d * 4), o_pp = take((size_t)kFXcd * kFMaxN * d * 4);
   const size_t o_fl = take((size_t)kFStages * kFGroups * 4), o_ctl = take((size_t)kFCtlWords * 4);
   const size_t o_plan = take(tabs.size() * 4);
-  const size_t o_uf = take((size_t)c.n_head * 4 * att_parts * 4);
+  const size_t o_tc = take((size_t)c.n_head * 4 * 4);
+  const size_t o_hp = take((size_t)kFMaxN * kFGroups * 8);
   static const hipError_t prep = fused_prepare();
   if (prep != hipSuccess) return SSD_OK;  // keep the per-sub-layer kernels
   HIP_TRY(hipMalloc(&kv->fz_ws, off));
@@ -438,8 +437,8 @@ static ssd_status fused_setup(ssd_kv* kv) {
   a.part_p = (float*)(b + o_pp);
   a.flags = (unsigned*)(b + o_fl);
   a.ctl = (unsigned*)(b + o_ctl);
-  a.uflag = (unsigned*)(b + o_uf);
-  a.uf_stride = (int)att_parts;
+  a.tile_ctr = (unsigned*)(b + o_tc);
+  a.head_part = (unsigned*)(b + o_hp);
   for (int nt = 1; nt <= 4; ++nt) kv->fz_plan[nt] = (int*)(b + o_plan) + (size_t)(nt - 1) * kFGroups * kPlanStride;
   a.err = kv->d_err;
   a.timeout = 20000000ull;  // 200 ms
@@ -877,6 +876,44 @@ static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int3
   return SSD_OK;
 }
 
+// The greedy accept right after a pass of n nodes whose staged tree is in
+// kv->d_tree: from the persistent pass's per-workgroup LM-head maxima, or by
+// reading the logits (one kernel per sub-layer).
+static ssd_status enqueue_greedy_after_pass(const ssd_model* m, ssd_kv* kv, int32_t n, bool fused, const float* logits,
+                                            int32_t* path, int32_t* path_len, int32_t* next, hipStream_t s) {
+  const int maxn = kv->max_nodes;
+  const int *tok = kv->d_tree, *dep = kv->d_tree + 2 * maxn, *par = kv->d_tree + 3 * maxn;
+  if (fused) {
+    HIP_TRY(launch_greedy_from_parts(kv->fz.head_part, kFGroups, n, tok, par, dep, path, path_len, next, s));
+  } else {
+    HIP_TRY(launch_argmax(logits, n, m->cfg.vocab, kv->d_argmax, kv->d_amwork, s));
+    HIP_TRY(launch_greedy_walk(tok, par, dep, n, kv->d_argmax, path, path_len, next, s));
+  }
+  return SSD_OK;
+}
+
+extern "C" ssd_status ssd_tree_verify_greedy(const ssd_model* m, ssd_kv* kv, int32_t prefix_len,
+                                             const int32_t* tree_tokens, const int32_t* parent_idx, int32_t n_nodes,
+                                             float* logits, int32_t* accepted_path, int32_t* path_len,
+                                             int32_t* next_token, void* stream) {
+  if (!accepted_path || !path_len || !next_token) return fail(SSD_E_INVALID_ARG, "null output");
+  int32_t md = 0;
+  ssd_status st = check_verify_args(m, kv, prefix_len, tree_tokens, parent_idx, n_nodes, logits, &md);
+  if (st != SSD_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  char* host = nullptr;
+  int slot = -1;
+  st = acquire_slot(kv, &host, &slot);
+  if (st != SSD_OK) return st;
+  const size_t used = fill_stage(host, prefix_len, tree_tokens, parent_idx, n_nodes, kv->max_nodes);
+  const bool fused = use_fused(m, kv, n_nodes);
+  st = start_pass_prefetch(m, kv, n_nodes, fused, kv->gemm_path);
+  if (st == SSD_OK) st = enqueue_verify(m, kv, prefix_len, n_nodes, host, used, logits, s);
+  if (st == SSD_OK) st = enqueue_greedy_after_pass(m, kv, n_nodes, fused, logits, accepted_path, path_len, next_token, s);
+  ssd_status st2 = release_slot(kv, slot, s);
+  return st != SSD_OK ? st : st2;
+}
+
 extern "C" ssd_status ssd_tree_verify(const ssd_model* m, ssd_kv* kv, int32_t prefix_len, const int32_t* tree_tokens,
                                       const int32_t* parent_idx, int32_t n_nodes, float* logits, void* stream) {
   int32_t md = 0;
@@ -894,9 +931,31 @@ extern "C" ssd_status ssd_tree_verify(const ssd_model* m, ssd_kv* kv, int32_t pr
   return st != SSD_OK ? st : st2;
 }
 
+static ssd_status capture_pass(const ssd_model* m, ssd_kv* kv, int32_t prefix_len, const int32_t* tree_tokens,
+                               const int32_t* parent_idx, int32_t n_nodes, float* logits, int32_t* path,
+                               int32_t* path_len, int32_t* next, ssd_graph** out);
+
 extern "C" ssd_status ssd_graph_capture_verify(const ssd_model* m, ssd_kv* kv, int32_t prefix_len,
                                                const int32_t* tree_tokens, const int32_t* parent_idx,
                                                int32_t n_nodes, float* logits, void* stream, ssd_graph** out) {
+  (void)stream;
+  return capture_pass(m, kv, prefix_len, tree_tokens, parent_idx, n_nodes, logits, nullptr, nullptr, nullptr, out);
+}
+
+extern "C" ssd_status ssd_graph_capture_verify_greedy(const ssd_model* m, ssd_kv* kv, int32_t prefix_len,
+                                                      const int32_t* tree_tokens, const int32_t* parent_idx,
+                                                      int32_t n_nodes, float* logits, int32_t* accepted_path,
+                                                      int32_t* path_len, int32_t* next_token, void* stream,
+                                                      ssd_graph** out) {
+  (void)stream;
+  if (!accepted_path || !path_len || !next_token) return fail(SSD_E_INVALID_ARG, "null output");
+  return capture_pass(m, kv, prefix_len, tree_tokens, parent_idx, n_nodes, logits, accepted_path, path_len,
+                      next_token, out);
+}
+
+static ssd_status capture_pass(const ssd_model* m, ssd_kv* kv, int32_t prefix_len, const int32_t* tree_tokens,
+                               const int32_t* parent_idx, int32_t n_nodes, float* logits, int32_t* path,
+                               int32_t* path_len, int32_t* next, ssd_graph** out) {
   if (!out) return fail(SSD_E_INVALID_ARG, "null output");
   int32_t md = 0;
   ssd_status st = check_verify_args(m, kv, prefix_len, tree_tokens, parent_idx, n_nodes, logits, &md);
@@ -915,7 +974,6 @@ extern "C" ssd_status ssd_graph_capture_verify(const ssd_model* m, ssd_kv* kv, i
   const size_t used = fill_stage(g->pinned, prefix_len, tree_tokens, parent_idx, n_nodes, kv->max_nodes);
   // capture on a private stream (the legacy null stream cannot be captured);
   // the graph is later launched on the caller's stream
-  (void)stream;
   hipStream_t cs = nullptr;
   e = hipStreamCreateWithFlags(&cs, hipStreamNonBlocking);
   if (e == hipSuccess) e = hipStreamBeginCapture(cs, hipStreamCaptureModeThreadLocal);
@@ -925,6 +983,7 @@ extern "C" ssd_status ssd_graph_capture_verify(const ssd_model* m, ssd_kv* kv, i
     return fail(SSD_E_DEVICE, std::string("hipStreamBeginCapture: ") + hipGetErrorString(e));
   }
   st = enqueue_verify(m, kv, prefix_len, n_nodes, g->pinned, used, logits, cs);
+  if (st == SSD_OK && path) st = enqueue_greedy_after_pass(m, kv, n_nodes, g->fused, logits, path, path_len, next, cs);
   hipGraph_t graph = nullptr;
   e = hipStreamEndCapture(cs, &graph);
   (void)hipStreamDestroy(cs);

@@ -170,6 +170,10 @@ constexpr int kTopKMax = 8;
 size_t topk_work_bytes(int N, int V);
 hipError_t launch_topk(const float* logits, int N, int V, int k, int* idx, float* val, float* lse, void* work,
                        hipStream_t s);
+// greedy accept from G per-workgroup (logit bits, token) maxima per node
+// (parts [N][G][2], N <= 64): the argmax of every node, then the walk
+hipError_t launch_greedy_from_parts(const unsigned* parts, int G, int N, const int* tokens, const int* parents,
+                                    const int* depth, int* path, int* path_len, int* next, hipStream_t s);
 hipError_t launch_greedy_walk(const int* tokens, const int* parents, const int* depth, int N, const int* g,
                               int* path, int* path_len, int* next, hipStream_t s);
 // mode: 1 without replacement, 2 independent, 3 chosen (draft == nullptr);
@@ -190,7 +194,7 @@ constexpr int kFMaxN = 64;                 // nodes
 constexpr int kFAutoMaxN = 64;             // most nodes the default pass mode sends to it
 constexpr int kFMaxL = 255;                // layers
 // stages of a layer; their flags are [kFStages][kFGroups] words
-enum FStage { FS_LN1 = 0, FS_QKV, FS_ATT, FS_WO, FS_LN2, FS_FC, FS_WPR, FS_AMG, kFStages };
+enum FStage { FS_LN1 = 0, FS_QKV, FS_ATT, FS_WO, FS_LN2, FS_FC, FS_WPR, FS_SPARE, kFStages };
 constexpr unsigned kFTagsPerPass = (unsigned)kFStages * (kFMaxL + 1);
 constexpr int kFAttRows = 256;  // cache rows per attention unit (32 per wave of 8)
 constexpr int kLwSlots = 12;  // per-layer parameter pointers (see LwSlot in fused.hip)
@@ -216,6 +220,7 @@ struct FusedArgs {
   const int* tree;          // staged tree (tokens, positions, depths, parents, offsets, path32, paths)
   int N, P;
   float* logits;            // [N][V]
+  unsigned* head_part;      // [kFMaxN][kFGroups][2]: each workgroup's largest logit (bits) and its token per node
   // workspaces
   float* xr;                // [kFXcd][kFMaxN][d] residual stream, one copy per XCD
   float* q;                 // [kFMaxN][d]
@@ -224,8 +229,7 @@ struct FusedArgs {
   uint16_t* fo;             // attention outputs, float16 fragments [4 tiles][d / 32][512]
   float* apart;             // attention parts [H][4 tiles][att_units + 1][16][68]: max, sum, -, -, output
   int att_units;            // prefix units of 256 cache rows: ceil(P / 256)
-  unsigned* uflag;          // attention unit flags [H][4 tiles][uf_stride]: the tag of the unit's pass and layer
-  int uf_stride;            // >= att_units + 1
+  unsigned* tile_ctr;       // [H][4 tiles]: attention units of the tile done in this layer (wraps to 0)
   uint16_t* ff;             // GELU outputs, float16 fragments [4 tiles][M / 32][512]
   float *part_o, *part_p;   // partial residuals [kFXcd][kFMaxN][d]
   unsigned* flags;          // [kFStages][kFGroups]

@@ -30,7 +30,8 @@ EXPORTS = ("ssd_model_create", "ssd_model_destroy", "ssd_kv_bytes", "ssd_kv_crea
            "ssd_tree_verify", "ssd_tree_accept", "ssd_kv_commit", "ssd_kv_error_count",
            "ssd_graph_capture_verify", "ssd_graph_launch", "ssd_graph_destroy", "ssd_validate_tree",
            "ssd_tree_prep", "ssd_kv_set_options", "ssd_kv_get_options", "ssd_status_string", "ssd_last_error",
-           "ssd_model_prefix_view", "ssd_topk", "ssd_tree_accept_noalloc")
+           "ssd_model_prefix_view", "ssd_topk", "ssd_tree_accept_noalloc", "ssd_tree_verify_greedy",
+           "ssd_graph_capture_verify_greedy")
 # and every function include/ssd_diag.h declares (measurement and diagnostics)
 DIAG_EXPORTS = ("ssd_launch_gemm", "ssd_verify_path", "ssd_fused_plan", "ssd_kv_set_trace")
 
@@ -85,6 +86,9 @@ def lib():
             "ssd_kv_create": [vp, C.c_int32, C.c_int32, vp, vp, vp, vp, C.POINTER(vp)],
             "ssd_kv_destroy": [vp],
             "ssd_tree_verify": [vp, vp, C.c_int32, i32p, i32p, C.c_int32, vp, vp],
+            "ssd_tree_verify_greedy": [vp, vp, C.c_int32, i32p, i32p, C.c_int32, vp, vp, vp, vp, vp],
+            "ssd_graph_capture_verify_greedy": [vp, vp, C.c_int32, i32p, i32p, C.c_int32, vp, vp, vp, vp, vp,
+                                                C.POINTER(vp)],
             "ssd_tree_accept": [vp, C.POINTER(_Tree), vp, vp, C.c_uint64, vp, vp, vp, vp],
             "ssd_tree_accept_noalloc": [C.POINTER(_Tree), vp, vp, C.c_uint64, vp, vp, vp, vp],
             "ssd_kv_commit": [vp, C.c_int32, vp, vp, vp],
@@ -351,6 +355,40 @@ class Session:
         _check(lib().ssd_tree_verify(self.model.handle, self.handle, prefix_len, _p32(t), _p32(p), n,
                                      C.c_void_p(logits.data_ptr()), _stream(stream)), "ssd_tree_verify")
         return logits
+
+    def _accept_outs(self, n, out):
+        torch = _torch()
+        if out is not None:
+            return out
+        return (torch.zeros(n, dtype=torch.int32, device=self.model.device),
+                torch.zeros(1, dtype=torch.int32, device=self.model.device),
+                torch.zeros(1, dtype=torch.int32, device=self.model.device))
+
+    def verify_greedy(self, prefix_len: int, tokens, parent_idx, logits=None, out=None, stream=None):
+        """ssd_tree_verify_greedy: (logits, path, path_len, next_token)."""
+        torch = _torch()
+        t, p = _i32(tokens), _i32(parent_idx)
+        n = len(t)
+        if logits is None:
+            logits = torch.empty((n, self.model.cfg.vocab), dtype=torch.float32, device=self.model.device)
+        path, plen, nxt = self._accept_outs(n, out)
+        _check(lib().ssd_tree_verify_greedy(self.model.handle, self.handle, prefix_len, _p32(t), _p32(p), n,
+                                            C.c_void_p(logits.data_ptr()), C.c_void_p(path.data_ptr()),
+                                            C.c_void_p(plen.data_ptr()), C.c_void_p(nxt.data_ptr()),
+                                            _stream(stream)), "ssd_tree_verify_greedy")
+        return logits, path, plen, nxt
+
+    def capture_verify_greedy(self, prefix_len: int, tokens, parent_idx, logits, out, stream=None) -> Graph:
+        """ssd_graph_capture_verify_greedy into logits and out = (path, path_len, next_token)."""
+        t, p = _i32(tokens), _i32(parent_idx)
+        path, plen, nxt = out
+        h = C.c_void_p()
+        _check(lib().ssd_graph_capture_verify_greedy(self.model.handle, self.handle, prefix_len, _p32(t), _p32(p),
+                                                     len(t), C.c_void_p(logits.data_ptr()),
+                                                     C.c_void_p(path.data_ptr()), C.c_void_p(plen.data_ptr()),
+                                                     C.c_void_p(nxt.data_ptr()), _stream(stream), C.byref(h)),
+               "ssd_graph_capture_verify_greedy")
+        return Graph(h, (t, p, logits, out))
 
     def capture_verify(self, prefix_len: int, tokens, parent_idx, logits, stream=None) -> Graph:
         t, p = _i32(tokens), _i32(parent_idx)

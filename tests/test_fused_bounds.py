@@ -65,7 +65,7 @@ def check_pass(H, d, M, V, L, N, P, max_ctx, max_nodes):
     S = (P + ATT_ROWS - 1) // ATT_ROWS
     sizes = {
         "xr": XCD * MAXN * d, "q": MAXN * d, "act": XCD * MAXN * d, "fo": MAXN * d, "ff": MAXN * M,
-        "apart": H * 4 * att_parts * 16 * AREC, "uflag": H * 4 * att_parts, "part": XCD * MAXN * d,
+        "apart": H * 4 * att_parts * 16 * AREC, "tile_ctr": H * 4, "part": XCD * MAXN * d,
         "logits": N * V, "kvt": L * H * max_nodes * DH, "kvc": L * H * max_ctx * DH,
         "w_qkv": (3 * d // 16) * KCd * 64, "w_o": RBd * KCd * 64, "w_fc": (M // 16) * KCd * 64,
         "w_pr": RBd * KCm * 64, "head": ((V + 15) // 16) * KCd * 64,
@@ -136,7 +136,7 @@ def check_pass(H, d, M, V, L, N, P, max_ctx, max_nodes):
                 c.rng(f"{tag} att head", h, h, H)
                 rec = lambda j, nl: ((((h * 4 + t) * (S + 1) + j) * 16 + nl) * AREC)
                 c.rng(f"{tag} part record", rec(part, 0), rec(part, 15) + AREC - 1, sizes["apart"])
-                c.rng(f"{tag} unit flags", (h * 4 + t) * att_parts, (h * 4 + t) * att_parts + S, sizes["uflag"])
+                c.rng(f"{tag} tile counter", h * 4 + t, h * 4 + t, sizes["tile_ctr"])
                 c.rng(f"{tag} merge parts", rec(0, 0), rec(S, 15) + AREC - 1, sizes["apart"])
                 n_lo, n_hi = 16 * t, min(16 * t + 15, N - 1)
                 c.rng(f"{tag} query rows", n_lo * d + h * DH, n_hi * d + h * DH + DH - 1, sizes["q"])
@@ -164,7 +164,7 @@ SHAPES = {"small": (4, 256, 1024, 2000, 3), "gpt2l": (20, 1280, 5120, 50257, 36)
 
 
 @pytest.mark.parametrize("shape", list(SHAPES))
-@pytest.mark.parametrize("P", [0, 64, 200, 512, 1500])
+@pytest.mark.parametrize("P", [0, 64, 200, 512, 1500, 5000])
 def test_persistent_pass_accesses_stay_in_bounds(shape, P):
     H, d, M, V, L = SHAPES[shape]
     max_ctx, max_nodes = P + 128, 64

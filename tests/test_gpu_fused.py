@@ -228,19 +228,28 @@ def test_fused_only_mode_rejects_unsupported(small, ssd, torch):
     s.close()
 
 
-@pytest.mark.gpu
-def test_fused_cache_length_limit(small, ssd, torch):
-    # A tile's unit flags are read by one 64-lane wave: the persistent pass
-    # takes caches of at most 63 prefix units of 256 rows (plus the root
-    # unit); a longer cache keeps the per-sub-layer kernels.
-    t = small
-    paths = []
-    for max_ctx in (63 * 256, 63 * 256 + 1):
-        kc, vc = W.random_kv_cache(t.cfg, max_ctx, 8, seed=5)
-        s = ssd.Session(t.m, max_ctx, 4, ssd.to_device(kc, t.cfg), ssd.to_device(vc, t.cfg))
-        paths.append(s.verify_path(1))
-        s.close()
-    assert paths == [ssd.PASS_FUSED, ssd.PASS_KERNELS]
+def test_fused_long_cache_matches_oracle(ssd, torch):
+    """A 5000-row prefix: 20 prefix units per (head, tile), so every tile's
+    parts are merged in several rounds and the tile counter wraps at 20."""
+    P, max_ctx = 5000, 5120
+    cfg = SMALL.with_(n_pos=max_ctx + 64)
+    w = W.make_weights(cfg, 1, perturb_affine=True)
+    om = oracle.Model(cfg, w)
+    m = ssd.Model(cfg, w)
+    kc, vc = W.random_kv_cache(cfg, max_ctx, P, seed=5)
+    s = ssd.Session(m, max_ctx, 40, ssd.to_device(kc, cfg), ssd.to_device(vc, cfg))
+    _fused(ssd, s)
+    assert s.verify_path(33) == ssd.PASS_FUSED
+    par = TREES["random33"]
+    toks = W.tree_tokens(par, cfg.vocab, seed=8)
+    got = s.verify(P, toks, par).cpu().numpy()
+    again = s.verify(P, toks, par).cpu().numpy()
+    assert s.error_count() == 0
+    assert np.array_equal(got, again)
+    ref = oracle.tree_verify(om, kc, vc, P, toks, par, om.kv(40), om.kv(40))
+    assert np.abs(got - ref).max() < TOL
+    s.close()
+    m.close()
 
 
 def test_fused_float16_overflow_is_counted(small, ssd, torch):
@@ -255,5 +264,49 @@ def test_fused_float16_overflow_is_counted(small, ssd, torch):
     assert s.verify_path(3) == ssd.PASS_FUSED
     s.verify(t.P, [1, 2, 3], [-1, 0, 0])
     assert s.error_count() > 0
+    s.close()
+    m.close()
+
+
+@pytest.mark.parametrize("name", ["single", "binary15", "random33", "random64"])
+@pytest.mark.parametrize("mode", ["fused", "kernels"])
+def test_verify_greedy_equals_verify_then_accept(small, ssd, torch, name, mode):
+    """ssd_tree_verify_greedy (the persistent pass's LM head leaves each
+    workgroup's maximum per node, so the walk skips the logits) gives the
+    logits and the greedy path of ssd_tree_verify + ssd_tree_accept, bit for
+    bit, eagerly and from a captured graph; a vocabulary row duplicated at a
+    far id makes exact ties across workgroups, which go to the lower id."""
+    t = small
+    w = dict(t.w)
+    wte = t.w["wte"].copy()
+    wte[1999] = wte[3]           # token 3 and token 1999 always have equal logits
+    w["wte"] = wte
+    m = ssd.Model(t.cfg, w)
+    s = ssd.Session(m, t.max_ctx, t.max_nodes, ssd.to_device(t.kc, t.cfg), ssd.to_device(t.vc, t.cfg))
+    s.set_options(pass_mode=ssd.PASS_FUSED if mode == "fused" else ssd.PASS_KERNELS)
+    par = TREES[name]
+    toks = W.tree_tokens(par, t.cfg.vocab, seed=21)
+    for P in (0, t.P):
+        lg_a = s.verify(P, toks, par).clone()
+        pa, la, na = s.accept(toks, par, lg_a)
+        lg_b, pb, lb, nb = s.verify_greedy(P, toks, par)
+        torch.cuda.synchronize()
+        assert torch.equal(lg_a, lg_b)
+        n = int(la.item())
+        assert int(lb.item()) == n and pa[:n].tolist() == pb[:n].tolist() and int(na.item()) == int(nb.item())
+        host = lg_a.cpu().numpy()
+        assert np.array_equal(host[:, 3], host[:, 1999])
+        # graph replay of the same step
+        lg_c = torch.zeros_like(lg_a)
+        outs = s._accept_outs(len(par), None)
+        g = s.capture_verify_greedy(P, toks, par, lg_c, outs)
+        for _ in range(2):
+            g.launch()
+            torch.cuda.synchronize()
+            assert torch.equal(lg_c, lg_a)
+            assert int(outs[1].item()) == n and outs[0][:n].tolist() == pa[:n].tolist()
+            assert int(outs[2].item()) == int(na.item())
+        g.close()
+    assert s.error_count() == 0
     s.close()
     m.close()

@@ -92,11 +92,15 @@ def _full_tree_check(s, om, kc, vc, torch, P, toks, par, max_nodes):
     gap = srt[:, -1] - srt[:, -2]
     for i in np.flatnonzero(ga != ra):
         assert gap[i] <= 2 * err[i].max(), (i, gap[i])
-    # greedy accept on the GPU's logits is bit-exact
+    # greedy accept on the GPU's logits is bit-exact, also through the
+    # verify + greedy step (the persistent pass skips re-reading the logits)
     dlg = torch.from_numpy(got).cuda()
     path, plen, nxt = s.accept(toks, par, dlg)
     op, on = oracle.tree_accept(oracle.GREEDY, toks, par, got)
     assert path[:int(plen.item())].cpu().numpy().tolist() == op.tolist() and int(nxt.item()) == on
+    lg2, p2, l2, n2 = s.verify_greedy(P, toks, par)
+    assert np.array_equal(lg2.cpu().numpy(), got)
+    assert p2[:int(l2.item())].cpu().numpy().tolist() == op.tolist() and int(n2.item()) == on
 
 
 def test_c2_full_tree(big, torch):
@@ -197,3 +201,21 @@ def test_persistent_pass_sampled_paths(big, torch, n, P):
     err = np.abs(got[path] - ref).max()
     print(f"persistent n={n} P={P} path {path} max|d| {err:.3e}", flush=True)
     assert err < TOL
+
+
+@pytest.mark.parametrize("n,P", [(16, 1024), (64, 1024), (48, 1500)])
+def test_persistent_pass_bitwise_repeatable(big, torch, n, P):
+    """Repeated passes of the persistent launch give bit-identical logits,
+    eagerly and from a captured graph, with four to six prefix units per
+    (head, tile) (a tile is merged by exactly one unit, the last to finish)."""
+    cfg, w, om, m, ssd = big
+    s, kc, vc = _session(big, torch, P, P + 64, 64, seed=4)
+    toks, par = W.best_first_tree(n, seed=3, vocab=cfg.vocab)
+    toks[0] = 17
+    with s.options(pass_mode=ssd.PASS_FUSED):
+        ref = s.verify(P, toks, par).cpu().numpy()
+        for rep in range(8):
+            assert np.array_equal(s.verify(P, toks, par).cpu().numpy(), ref), rep
+        for rep in range(4):
+            assert np.array_equal(_graph_logits(s, torch, P, toks, par), ref), rep
+    assert s.error_count() == 0
