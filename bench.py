@@ -4,10 +4,19 @@
 Workload: GPT-2-L shape (36 x 1280, 20 heads of 64, MLP 5120, vocab 50257),
 random N(0, 0.02) bf16 weights, a synthetic 512-token prefix cache and a
 32-node tree (branching 4,2,2,1 breadth-first, truncated), greedy acceptance.
-One step = the whole hot path on that input: the captured verification pass,
-the accept walk and the KV commit (commit rewrites the same rows past the
-prefix every step, and verification never reads them, so steps repeat
-exactly).  Inputs are resident in HBM before timing starts.
+One step = the whole hot path on that input: the captured verification pass
+with its greedy accept (the argmax of every node taken from the LM head's
+per-workgroup maxima, then the walk down the tree), and the KV commit of the
+accepted path (commit rewrites the same rows past the prefix every step, and
+verification never reads them, so steps repeat exactly).  `value` is the
+tree tokens verified per second of timed steps.  Inputs are resident in HBM
+before timing starts.
+
+Also reported: the pass alone and its HBM roofline fraction, the tree-size x
+prefix sweep (with both GEMM paths of the one-kernel-per-sub-layer pass and
+their crossover), the 256-node / 2048-token stress point with its sampling
+accepts timed, staged end-to-end generation (greedy and top-50 sampling),
+and the CPU oracle's time on this host.
 
 Prints one JSON line on stdout; progress goes to stderr.
 """
@@ -228,6 +237,15 @@ def end_to_end(ssd, W, cfg, model, N_NEW, PROMPT):
         b_gap, P3 = backend(record_gaps=True)
         S.plain_greedy(b_gap, P3, int(prompt[-1]), agree + 1)
         gap = b_gap.gaps[agree]
+    # the same with top-k sampling (k = 50, T = 1): plain steps draw from the
+    # oracle's top-k target; staged steps accept the draft's chosen children
+    # by rejection sampling against it, so both emit that law (Sec. 2.3)
+    b_ps, P4 = backend()
+    plain_s = S.plain_sample(b_ps, P4, int(prompt[-1]), N_NEW, top_k=50, seed0=11)
+    b_ss, P5 = backend()
+    st_s = S.staged_sample(b_ss, P5, int(prompt[-1]), N_NEW, succ, top_k=50, seed0=11)
+    log(f"end to end, top-50 sampling: plain {N_NEW / plain_s.seconds:.1f} tok/s, staged "
+        f"{N_NEW / st_s.seconds:.1f} tok/s, accepted {sum(st_s.accepted)} in {st_s.steps} steps")
     log(f"end to end: plain {N_NEW / plain.seconds:.1f} tok/s, staged {N_NEW / st.seconds:.1f} tok/s, "
         f"accepted {sum(st.accepted)} in {st.steps} steps, agree {agree}/{N_NEW}"
         + ("" if gap is None else f", plain top-2 gap at the divergence {gap:.3g}"))
@@ -239,7 +257,11 @@ def end_to_end(ssd, W, cfg, model, N_NEW, PROMPT):
             "mean_endorsed_nodes": round(float(np.mean(st.endorsed)), 2),
             "tokens_equal_to_plain": agree,
             "plain_top2_gap_at_divergence": None if gap is None else round(gap, 6),
-            "bigram_build_s": round(t_bigram, 2)}
+            "bigram_build_s": round(t_bigram, 2),
+            "top50_sampling": {"plain_tokens_per_s": round(N_NEW / plain_s.seconds, 1),
+                               "staged_tokens_per_s": round(N_NEW / st_s.seconds, 1), "staged_steps": st_s.steps,
+                               "accepted_tree_tokens": int(sum(st_s.accepted)),
+                               "mean_oracle_tree_nodes": round(float(np.mean(st_s.oracle_nodes)), 1)}}
 
 
 def main():
@@ -278,7 +300,10 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
-    cfg = W.GPT2L
+    # GPT-2-L shape with the position table extended to 2048 + 256 rows (the
+    # 2048-token stress point needs them; positions are gathered, not
+    # streamed, so no byte count changes)
+    cfg = W.GPT2L_LONG
     N, P = args.nodes, args.prefix
     max_ctx, max_nodes = 1024 + 64, 128
     log("generating GPT-2-L weights")
@@ -293,15 +318,16 @@ def main():
     if args.traffic_probe:
         probe_traffic(sess, cfg, N, P, toks, par, fused)
         return
-    graph = sess.capture_verify(P, toks, par, logits)
+    stream = torch.cuda.current_stream()
     outs = (torch.zeros(N, dtype=torch.int32, device="cuda"), torch.zeros(1, dtype=torch.int32, device="cuda"),
             torch.zeros(1, dtype=torch.int32, device="cuda"))
-    stream = torch.cuda.current_stream()
+    # one step: the captured pass with its greedy accept (ssd_tree_verify_greedy),
+    # then the KV commit of the accepted path
+    graph_step = sess.capture_verify_greedy(P, toks, par, logits, outs)
 
     def step():
-        graph.launch()
-        path, plen, _ = sess.accept(toks, par, logits, out=outs)
-        sess.commit(P, path, plen)
+        graph_step.launch()
+        sess.commit(P, outs[0], outs[1])
 
     log(f"warmup {args.warmup}")
     for _ in range(args.warmup):
@@ -333,9 +359,27 @@ def main():
         torch.cuda.synchronize()
         return a.elapsed_time(b) / reps * 1e3  # us
 
+    def time_calls(fn, reps):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(reps):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps * 1e3  # us
+
+    graph = sess.capture_verify(P, toks, par, logits)
     us_pass = time_graph(graph, max(args.steps, 50))
+    us_step_graph = time_graph(graph_step, 50)
+    us_accept_logits = time_calls(lambda: sess.accept(toks, par, logits, out=outs), 50)
     B = pass_bytes(cfg, N, P)
-    log(f"verify pass {us_pass:.1f} us, {B / us_pass / 1e3:.0f} GB/s")
+    log(f"verify pass {us_pass:.1f} us, {B / us_pass / 1e3:.0f} GB/s; pass + greedy accept {us_step_graph:.1f} us; "
+        f"accept from the logits {us_accept_logits:.1f} us")
+    if sess.error_count():
+        raise SystemExit("the session's error counter grew during the timed passes")
 
     if fused:
         # dominant kernel: the persistent pass itself (the pass is this one
@@ -350,19 +394,84 @@ def main():
     else:
         roofline = fc_gemm_roofline(sess, cfg, N, stream)
 
-    sweep = []
-    if not args.no_sweep:
-        for n_s, p_s in [(1, 512), (8, 512), (16, 512), (64, 512), (128, 512), (64, 128), (64, 1024)]:
-            tt, pp = W.best_first_tree(n_s, seed=3, vocab=cfg.vocab)
-            tt[0] = int(toks[0])
-            lg = torch.empty((n_s, cfg.vocab), dtype=torch.float32, device="cuda")
-            g = sess.capture_verify(p_s, tt, pp, lg)
-            us = time_graph(g, 50)
+    def pass_point(n_s, p_s, s_=None, **opts):
+        s_ = s_ or sess
+        tt, pp = W.best_first_tree(n_s, seed=3, vocab=cfg.vocab)
+        tt[0] = int(toks[0])
+        lg = torch.empty((n_s, cfg.vocab), dtype=torch.float32, device="cuda")
+        with s_.options(**opts):
+            path = s_.verify_path(n_s)
+            g = s_.capture_verify(p_s, tt, pp, lg)
+            us = time_graph(g, 30)
             g.close()
-            bb = pass_bytes(cfg, n_s, p_s)
-            sweep.append({"nodes": n_s, "prefix": p_s, "us": round(us, 1), "GB/s": round(bb / us / 1e3, 1),
-                          "frac": round(bb / us / 1e3 / PEAK_HBM_GBS, 4)})
-            log(f"sweep N={n_s} P={p_s}: {us:.1f} us")
+        bb = pass_bytes(cfg, n_s, p_s)
+        return {"nodes": n_s, "prefix": p_s, "us": round(us, 1), "GB/s": round(bb / us / 1e3, 1),
+                "frac": round(bb / us / 1e3 / PEAK_HBM_GBS, 4),
+                "path": "persistent" if path == ssd.PASS_FUSED else "per-sub-layer"}
+
+    sweep, crossover = [], None
+    if not args.no_sweep:
+        # the size x prefix grid; each point in the default mode, and on the
+        # one-kernel-per-sub-layer path with each GEMM path pinned (vector ALU
+        # vs matrix cores) to locate their crossover
+        grid = [(n_s, p_s) for p_s in (128, 512, 1024) for n_s in (1, 8, 16, 64, 128)]
+        per_p = {}
+        for n_s, p_s in grid:
+            pt = pass_point(n_s, p_s)
+            vec = pass_point(n_s, p_s, pass_mode=ssd.PASS_KERNELS, gemm_path=ssd.GEMM_VEC)
+            mma = pass_point(n_s, p_s, pass_mode=ssd.PASS_KERNELS, gemm_path=ssd.GEMM_MFMA)
+            pt["kernels_vec_us"], pt["kernels_mfma_us"] = vec["us"], mma["us"]
+            sweep.append(pt)
+            per_p.setdefault(p_s, []).append((n_s, vec["us"], mma["us"]))
+            log(f"sweep N={n_s} P={p_s}: {pt['us']:.1f} us ({pt['path']}); per-sub-layer vec {vec['us']:.1f}, "
+                f"mfma {mma['us']:.1f}")
+        # smallest node count at which the matrix-core GEMMs beat the vector ALU
+        crossover = {str(p_s): next((n for n, v, m in pts if m < v), None) for p_s, pts in per_p.items()}
+        # latency growth with tree size at the 512-token prefix (log-log slope per step)
+        row = sorted((p["nodes"], p["us"]) for p in sweep if p["prefix"] == 512)
+        slopes = [round(float(np.log(b[1] / a[1]) / np.log(b[0] / a[0])), 3) for a, b in zip(row, row[1:])]
+        crossover = {"smallest_nodes_mfma_faster_by_prefix": crossover, "loglog_slopes_P512": slopes,
+                     "T128_over_T1_P512": round(row[-1][1] / row[0][1], 3)}
+        if sess.error_count():
+            raise SystemExit("the session's error counter grew during the sweep")
+
+    stress = None
+    if not args.no_sweep:
+        # 256-node tree (branching 8,4,2,2,1 cut at 256) over a 2048-token
+        # prefix, temperature-1 rejection sampling over the full vocabulary
+        # with draft rows 0.5 x oracle softmax + 0.5 x Dirichlet(0.1) noise
+        n5, p5 = 256, 2048
+        kc5, vc5 = W.random_kv_cache(cfg, p5 + 8, p5, seed=5)
+        s5 = ssd.Session(model, p5 + 8, n5, ssd.to_device(kc5, cfg), ssd.to_device(vc5, cfg))
+        par5 = W.branching_tree([8, 4, 2, 2, 1], n5)
+        tok5 = W.tree_tokens(par5, cfg.vocab, seed=6)
+        lg5 = torch.empty((n5, cfg.vocab), dtype=torch.float32, device="cuda")
+        g5 = s5.capture_verify(p5, tok5, par5, lg5)
+        us5 = time_graph(g5, 20)
+        g5.launch()
+        torch.cuda.synchronize()
+        gen = torch.Generator(device="cuda").manual_seed(7)
+        noise = torch._standard_gamma(torch.full((n5, cfg.vocab), 0.1, device="cuda"), generator=gen)
+        q5 = (0.5 * torch.softmax(lg5, 1) + 0.5 * noise / noise.sum(1, keepdim=True)).float().contiguous()
+        out5 = (torch.zeros(n5, dtype=torch.int32, device="cuda"), torch.zeros(1, dtype=torch.int32, device="cuda"),
+                torch.zeros(1, dtype=torch.int32, device="cuda"))
+        acc = {}
+        for name, kw in (("wor", dict(mode=ssd.SAMPLE_WOR, draft_probs=q5)),
+                         ("wor_top50", dict(mode=ssd.SAMPLE_WOR, draft_probs=q5, top_k=50)),
+                         ("chosen_top50", dict(mode=ssd.SAMPLE_DET, top_k=50)),
+                         ("greedy", dict())):
+            acc[name] = round(time_calls(lambda: s5.accept(tok5, par5, lg5, out=out5, seed=3, **kw), 10), 1)
+        b5 = pass_bytes(cfg, n5, p5)
+        stress = {"workload": "256-node tree (branching 8,4,2,2,1 cut at 256), 2048-token prefix, T=1 rejection "
+                              "sampling over 50257 tokens, draft = 0.5 softmax + 0.5 Dirichlet(0.1)",
+                  "verify_us": round(us5, 1), "GB/s": round(b5 / us5 / 1e3, 1),
+                  "frac": round(b5 / us5 / 1e3 / PEAK_HBM_GBS, 4), "accept_us": acc,
+                  "path": "persistent" if s5.verify_path(n5) == ssd.PASS_FUSED else "per-sub-layer"}
+        log(f"stress: verify {us5:.1f} us, accept {acc}")
+        if s5.error_count():
+            raise SystemExit("the stress session's error counter grew")
+        g5.close()
+        s5.close()
 
     e2e = None
     if not args.no_e2e:
@@ -374,19 +483,41 @@ def main():
         threads = int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or (os.cpu_count() or 1)
         om = oracle.Model(cfg, w)
         okt, ovt = om.kv(max_nodes), om.kv(max_nodes)
-        times = []
-        t_start = time.time()
-        while len(times) < 30 and (time.time() - t_start) < 12.0:
-            t0 = time.time()
-            oracle.tree_verify(om, kc, vc, P, toks, par, okt, ovt, threads)
-            times.append(time.time() - t0)
-        tpass = sorted(times)[len(times) // 2]
-        cpu = {"value": round(N / tpass, 3), "unit": "verified tree tokens/s", "cores": threads, "kind": "oracle",
-               "sample": f"{len(times)} full oracle verification passes of this workload (fp64, {N} nodes, "
-                         f"prefix {P}), median {tpass:.2f} s each; host {cpu_model()}"}
-        log(f"oracle pass {tpass:.2f} s on {threads} threads")
 
-    value = N / (us_pass * 1e-6)
+        def oracle_time(n_s, p_s, tt, pp, budget, reps):
+            ts = []
+            t_start = time.time()
+            while len(ts) < reps and (time.time() - t_start) < budget:
+                t0 = time.time()
+                oracle.tree_verify(om, kc, vc, p_s, tt, pp, okt, ovt, threads)
+                ts.append(time.time() - t0)
+            return sorted(ts)[len(ts) // 2], len(ts)
+
+        tpass, nrun = oracle_time(N, P, toks, par, 10.0, 30)
+        t64, _ = oracle_time(64, 512, *W.best_first_tree(64, seed=3, vocab=cfg.vocab), 6.0, 3)
+        t1, n1 = oracle_time(1, 512, np.array([int(toks[0])], np.int32), np.array([-1], np.int32), 4.0, 20)
+        # the tiny fp32 model (2 x 128, vocab 512): a 15-node binary tree over 64 cached tokens
+        tcfg = W.TINY
+        tw = W.make_weights(tcfg, 0)
+        tom = oracle.Model(tcfg, tw)
+        tkc, tvc = W.random_kv_cache(tcfg, 128, 64, seed=1)
+        tpar = W.complete_binary_tree(15)
+        ttok = W.tree_tokens(tpar, tcfg.vocab, seed=2)
+        tt0 = time.time()
+        for _ in range(20):
+            oracle.tree_verify(tom, tkc, tvc, 64, ttok, tpar, tom.kv(16), tom.kv(16), threads)
+        t_tiny = (time.time() - tt0) / 20
+        cpu = {"value": round(N / tpass, 3), "unit": "verified tree tokens/s", "cores": threads, "kind": "oracle",
+               "sample": f"{nrun} full oracle verification passes of this workload (fp64, {N} nodes, "
+                         f"prefix {P}), median {tpass:.2f} s each; host {cpu_model()}",
+               "also": {"nodes64_prefix512_pass_s": round(t64, 3),
+                        "plain_decode_tokens_per_s": round(1.0 / t1, 3),
+                        "tiny_fp32_15_nodes_pass_ms": round(t_tiny * 1e3, 3)}}
+        log(f"oracle pass {tpass:.2f} s on {threads} threads; 64 nodes {t64:.2f} s; plain decode {1 / t1:.2f} tok/s")
+
+    # whole-step throughput: tree tokens verified per second of timed steps
+    # (pass, greedy accept, commit)
+    value = N / (ms_step * 1e-3)
     line = {
         "metric": METRIC, "value": round(value, 1), "unit": "verified tree tokens/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True,
@@ -396,6 +527,8 @@ def main():
                    "nodes": N, "prefix": P, "layers": cfg.n_layer, "d_model": cfg.d_model, "vocab": cfg.vocab},
         "verify_path": "persistent single launch" if fused else "one kernel per sub-layer",
         "us_per_verify_pass": round(us_pass, 2),
+        "us_pass_plus_greedy_accept": round(us_step_graph, 2),
+        "us_accept_from_logits": round(us_accept_logits, 2),
         "pass_hbm_GBs": round(B / us_pass / 1e3, 1),
         "pass_frac_of_peak": round(B / us_pass / 1e3 / PEAK_HBM_GBS, 4),
         "pass_algorithmic_bytes": B,
@@ -403,6 +536,8 @@ def main():
         "cpu_baseline": cpu,
         "end_to_end": e2e,
         "sweep": sweep,
+        "sweep_summary": crossover,
+        "stress": stress,
     }
     print(json.dumps(line), flush=True)
 

@@ -193,6 +193,48 @@ def staged_greedy(backend, P: int, root: int, n_new: int, succ: np.ndarray) -> D
     return st
 
 
+def plain_sample(backend, P: int, root: int, n_new: int, top_k: int, temperature: float = 1.0,
+                 seed0: int = 0) -> DecodeStats:
+    """One-token steps with sampling: the next token drawn from the oracle's
+    top-k target (Sec. 4: top-k sampling with k = 50, T = 1)."""
+    st = DecodeStats()
+    t0 = time.perf_counter()
+    while len(st.tokens) < n_new:
+        path, nxt = backend.oracle_step(P, np.array([root], np.int32), np.array([-1], np.int32),
+                                        sample=(top_k, temperature, seed0 + st.steps))
+        P += len(path)
+        st.tokens.append(nxt)
+        st.steps += 1
+        root = nxt
+    st.seconds = time.perf_counter() - t0
+    return st
+
+
+def staged_sample(backend, P: int, root: int, n_new: int, succ: np.ndarray, top_k: int,
+                  temperature: float = 1.0, seed0: int = 0) -> DecodeStats:
+    """Staged speculation with sampling: the same trees as staged_greedy (the
+    draft's top tokens, chosen rather than drawn), accepted by rejection
+    sampling against the oracle's top-k target, so the emitted tokens follow
+    that target exactly (Sec. 2.3)."""
+    st = DecodeStats()
+    t0 = time.perf_counter()
+    while len(st.tokens) < n_new:
+        bt, bp = bigram_tree(root, succ)
+        top_idx, top_val, lse = backend.draft_top(P, bt, bp, DRAFT_TOP)
+        ot, op, n_end = oracle_tree(bt, bp, top_idx, top_val, lse)
+        path, nxt = backend.oracle_step(P, ot, op, sample=(top_k, temperature, seed0 + st.steps))
+        P += len(path)
+        st.tokens += [int(ot[i]) for i in path[1:]] + [int(nxt)]
+        st.steps += 1
+        st.accepted.append(len(path) - 1)
+        st.oracle_nodes.append(len(ot))
+        st.endorsed.append(n_end)
+        root = int(nxt)
+    st.tokens = st.tokens[:n_new]
+    st.seconds = time.perf_counter() - t0
+    return st
+
+
 # ---------------------------------------------------------------- GPU backend (libssd)
 
 class GpuBackend:
@@ -239,9 +281,18 @@ class GpuBackend:
         self._check_errors(self.d)
         return idx.cpu().numpy(), val.cpu().numpy(), lse.cpu().numpy()
 
-    def oracle_step(self, P: int, toks: np.ndarray, par: np.ndarray):
-        lg = self.o.verify(P, toks, par)
-        path, plen, nxt = self.o.accept(toks, par, lg)
+    def oracle_step(self, P: int, toks: np.ndarray, par: np.ndarray, sample=None):
+        """Verify, accept and commit; greedy, or with sample = (top_k,
+        temperature, seed) rejection sampling of children chosen by the
+        draft (SSD_ACCEPT_SAMPLE_DET)."""
+        from . import ssd
+        if sample is None:
+            lg, path, plen, nxt = self.o.verify_greedy(P, toks, par)
+        else:
+            top_k, temperature, seed = sample
+            lg = self.o.verify(P, toks, par)
+            path, plen, nxt = self.o.accept(toks, par, lg, mode=ssd.SAMPLE_DET, temperature=temperature, seed=seed,
+                                            top_k=top_k)
         self.o.commit(P, path, plen)
         self._check_errors(self.o)
         n = int(plen.item())

@@ -177,3 +177,41 @@ def test_staged_equals_oracle_plain_greedy_tiny_f32(ssd, torch):
     print(f"staged {st.steps} steps, accepted {sum(st.accepted)}, min oracle gap {min(gaps):.3g}")
     assert st.tokens == ref
     assert sum(st.accepted) > 0
+
+
+def test_staged_sampling_top1_is_greedy_and_top50_runs(ssd, torch):
+    """With k = 1 the top-k target is a point mass on the argmax, so the
+    sampling loops (children chosen by the draft, accepted by rejection
+    sampling, SSD_ACCEPT_SAMPLE_DET) must emit the greedy sequence of the
+    same verification shapes; with k = 50 they must run without error."""
+    cfg = W.TINY.with_(dtype="bf16")
+    w = W.make_weights(cfg, 0, perturb_affine=True)
+    m = ssd.Model(cfg, w)
+    draft = m.prefix_view(1)
+    prompt_len, n_new = 40, 32
+    prompt = W.prefix_tokens(prompt_len, cfg.vocab, seed=5)
+    max_ctx = prompt_len + n_new + 80
+
+    def backend():
+        o = ssd.Session(m, max_ctx, 64)
+        d = ssd.Session(draft, max_ctx, 64, o.k_cache, o.v_cache)
+        b = S.GpuBackend(o, d)
+        return b, b.prefill(prompt[:-1])
+
+    b, P = backend()
+    stream = S.bigram_stream(cfg.vocab, 2048, seed=4)
+    preds = np.concatenate([b.greedy_predictions(stream[i:i + 64]) for i in range(0, 2048, 64)])
+    succ = S.bigram_table(stream, preds, cfg.vocab)
+    greedy = S.staged_greedy(b, P, int(prompt[-1]), n_new, succ)
+    b1, P1 = backend()
+    top1 = S.staged_sample(b1, P1, int(prompt[-1]), n_new, succ, top_k=1, seed0=3)
+    assert top1.tokens == greedy.tokens
+    assert top1.accepted == greedy.accepted
+    b2, P2 = backend()
+    plain1 = S.plain_sample(b2, P2, int(prompt[-1]), 8, top_k=1)
+    b3, P3 = backend()
+    assert plain1.tokens == S.plain_greedy(b3, P3, int(prompt[-1]), 8).tokens
+    b4, P4 = backend()
+    s50 = S.staged_sample(b4, P4, int(prompt[-1]), n_new, succ, top_k=50, seed0=3)
+    assert len(s50.tokens) == n_new and all(0 <= t < cfg.vocab for t in s50.tokens)
+    assert b4.o.error_count() == 0 and b4.d.error_count() == 0
