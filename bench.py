@@ -264,6 +264,76 @@ def end_to_end(ssd, W, cfg, model, N_NEW, PROMPT):
                                "mean_oracle_tree_nodes": round(float(np.mean(st_s.oracle_nodes)), 1)}}
 
 
+STAGES = ["LN1", "QKV", "ATT", "WO", "LN2", "FC", "WPR"]
+CROSS_XCD = {0, 4}  # stages whose inputs come from all 8 XCDs
+
+
+def stage_trace(sess, cfg, N, P, toks, par, us_pass):
+    """Record one persistent pass's stage timestamps (ssd_kv_set_trace) and
+    write a summary per stage to profiles/stage_trace_n{N}_p{P}.md: per XCD
+    and layer (layers 2..L-2), the hand-off (last producer published -> first
+    consumer's dependency met), the met skew inside the XCD, the span (first
+    met -> last published) and their total; medians, with the max of the
+    total."""
+    import numpy as np
+    import torch
+    L = cfg.n_layer
+    buf = torch.zeros(256 * (L + 1) * 24, dtype=torch.int64, device="cuda")
+    sess.set_trace(buf)
+    sess.verify(P, toks, par)
+    torch.cuda.synchronize()
+    sess.set_trace(None)
+    t = buf.cpu().numpy().reshape(256, L + 1, 8, 3).astype(np.int64)
+    x_of = np.arange(256) // 32   # trace rows are x * 32 + rank
+    res = {s_: [] for s_ in range(7)}
+    for l in range(2, L - 1):
+        for s_ in range(7):
+            pl, ps = (l, s_ - 1) if s_ else (l - 1, 6)
+            for x in range(8):
+                cons = x_of == x
+                prod = np.ones(256, bool) if s_ in CROSS_XCD else cons
+                pdone = t[prod, pl, ps, 2].max()
+                met = t[cons, l, s_, 1]
+                met = met[met > 0]
+                if len(met) == 0:
+                    continue
+                done = t[cons, l, s_, 2].max()
+                res[s_].append((met.min() - pdone, met.max() - met.min(), done - met.min(), done - pdone))
+    period = np.median([(t[:, l + 1, 0, 0].min() - t[:, l, 0, 0].min()) * 0.01 for l in range(1, L - 1)])
+    head = (t[:, L, 1, 2].max() - t[:, L, 0, 0].min()) * 0.01
+    rows = []
+    tot = 0.0
+    for s_ in range(7):
+        a = np.array(res[s_], dtype=np.float64) * 0.01
+        med = np.median(a, 0)
+        tot += med[3]
+        rows.append(f"| {STAGES[s_]} | {'all 8 XCDs' if s_ in CROSS_XCD else 'own XCD'} | {med[0]:.2f} | "
+                    f"{med[1]:.2f} | {med[2]:.2f} | {med[3]:.2f} | {a[:, 3].max():.2f} |")
+    cmd = f"python bench.py --stage-trace --nodes {N} --prefix {P}"
+    text = "\n".join([
+        f"# Stage trace of the persistent pass: GPT-2-L shape, {N} nodes, {P}-token prefix",
+        "",
+        f"Command: `{cmd}` (MI355X; kernel sources {kernel_source_hash()}).",
+        "",
+        "One traced pass (s_memrealtime, 100 MHz, per workgroup: stage entry, dependency met, "
+        "stage published). Per XCD and layer (layers 2..L-2), medians in us:",
+        "hand-off = last producer published -> first consumer met; skew = first -> last consumer "
+        "met inside the XCD; span = first met -> last published; total = last producer "
+        "published -> last published (the stage's share of the critical path).",
+        "",
+        "| stage | inputs from | hand-off | met skew | span | total | max total |",
+        "|---|---|---|---|---|---|---|",
+        *rows,
+        "",
+        f"Sum of the median totals: {tot:.2f} us per layer; median layer period {period:.2f} us; "
+        f"final LayerNorm + LM head {head:.1f} us; untraced pass {us_pass:.1f} us.",
+        ""])
+    path = os.path.join(ROOT, "profiles", f"stage_trace_n{N}_p{P}.md")
+    with open(path, "w") as f:
+        f.write(text)
+    log(text)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -281,6 +351,9 @@ def main():
                     help="read two rocprofv3 --pmc outputs (FETCH_SIZE, WRITE_SIZE) of --traffic-probe and write "
                          "profiles/traffic_pass_kernel.json (or traffic_fc_gemm.json with --kernels-path); "
                          "no GPU needed")
+    ap.add_argument("--stage-trace", action="store_true",
+                    help="time the pass, record one traced persistent pass and write "
+                         "profiles/stage_trace_n{nodes}_p{prefix}.md")
     ap.add_argument("--kernels-path", action="store_true",
                     help="with --traffic-from: the counters are of the one-kernel-per-sub-layer path's GEMM")
     args = ap.parse_args()
@@ -305,11 +378,12 @@ def main():
     # streamed, so no byte count changes)
     cfg = W.GPT2L_LONG
     N, P = args.nodes, args.prefix
-    max_ctx, max_nodes = 1024 + 64, 128
+    cached = max(1024, P)
+    max_ctx, max_nodes = cached + 64, max(128, N)
     log("generating GPT-2-L weights")
     w = W.make_weights(cfg, 0)
     model = ssd.Model(cfg, w)
-    kc, vc = W.random_kv_cache(cfg, max_ctx, 1024, seed=3)
+    kc, vc = W.random_kv_cache(cfg, max_ctx, cached, seed=3)
     sess = ssd.Session(model, max_ctx, max_nodes, ssd.to_device(kc, cfg), ssd.to_device(vc, cfg))
     par = W.branching_tree([4, 2, 2, 1], N)
     toks = W.tree_tokens(par, cfg.vocab, seed=2)
@@ -317,6 +391,21 @@ def main():
     fused = sess.verify_path(N) == ssd.PASS_FUSED
     if args.traffic_probe:
         probe_traffic(sess, cfg, N, P, toks, par, fused)
+        return
+    if args.stage_trace:
+        if not fused:
+            raise SystemExit(f"a {N}-node pass does not run as the persistent kernel: nothing to trace")
+        g = sess.capture_verify(P, toks, par, logits)
+        for _ in range(5):
+            g.launch()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(50):
+            g.launch()
+        b.record()
+        torch.cuda.synchronize()
+        stage_trace(sess, cfg, N, P, toks, par, a.elapsed_time(b) / 50 * 1e3)
         return
     stream = torch.cuda.current_stream()
     outs = (torch.zeros(N, dtype=torch.int32, device="cuda"), torch.zeros(1, dtype=torch.int32, device="cuda"),
@@ -494,7 +583,9 @@ def main():
             return sorted(ts)[len(ts) // 2], len(ts)
 
         tpass, nrun = oracle_time(N, P, toks, par, 10.0, 30)
-        t64, _ = oracle_time(64, 512, *W.best_first_tree(64, seed=3, vocab=cfg.vocab), 6.0, 3)
+        tok64, par64 = W.best_first_tree(64, seed=3, vocab=cfg.vocab)
+        tok64[0] = int(toks[0])
+        t64, _ = oracle_time(64, 512, tok64, par64, 6.0, 3)
         t1, n1 = oracle_time(1, 512, np.array([int(toks[0])], np.int32), np.array([-1], np.int32), 4.0, 20)
         # the tiny fp32 model (2 x 128, vocab 512): a 15-node binary tree over 64 cached tokens
         tcfg = W.TINY

@@ -30,8 +30,11 @@
  * Model: GPT-2, pre-LayerNorm blocks, tanh GELU, learned absolute positions,
  * LM head tied to the token embedding.  All parameters and the K/V cache use
  * one storage type (float32 or bfloat16); accumulation is float32.  For
- * bfloat16 models the weight GEMMs multiply float16 operands (exact copies
- * of the weights, activations rounded to float16).
+ * bfloat16 models the weight GEMMs multiply float16 operands: the weights
+ * converted to float16 (exact for 0 and magnitudes in [2^-17, 65504], within
+ * 2^-25 below; a weight past 65504 makes ssd_model_create fail) and the
+ * activations rounded to float16 (an activation past 65504 is counted in the
+ * session's error counter, see ssd_kv_error_count).
  */
 #ifndef SSD_H
 #define SSD_H
@@ -107,7 +110,9 @@ typedef struct {
  * head_dim (= d_model / n_head) of 32 or 64.  For bfloat16 the library
  * repacks every matrix (and the LM head) once into a private copy laid out in
  * matrix-core tile order (freed by ssd_model_destroy); this call waits for it.
- * Errors: SSD_E_INVALID_ARG, SSD_E_UNSUPPORTED, SSD_E_DEVICE. */
+ * Errors: SSD_E_INVALID_ARG, SSD_E_UNSUPPORTED (also: a bfloat16 matrix or
+ * LM-head weight of magnitude above 65504, or NaN, which its float16 copy
+ * cannot hold), SSD_E_DEVICE. */
 ssd_status ssd_model_create(const ssd_config *cfg, const ssd_weights *w, void *stream, ssd_model **out);
 void ssd_model_destroy(ssd_model *m);
 

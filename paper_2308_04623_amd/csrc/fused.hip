@@ -19,9 +19,12 @@
 //    WO (attention out-projection over the XCD's heads: a partial residual),
 //    LN2, FC (+GELU, the XCD's hidden slice), WPR (MLP down-projection over
 //    that slice: a partial residual).  Only the two partial residuals cross
-//    XCDs: every XCD adds the eight partials of a node row itself, in XCD
-//    order, into its own copy of the residual stream, so all copies agree
-//    bit for bit.  Every other hand-off stays inside one XCD's L2.
+//    XCDs: every XCD adds its partial of each output, in fixed point (units
+//    of 2^-32, 64-bit integers), into one device-wide sum with an atomic add;
+//    integer addition does not depend on the order the XCDs arrive in, so
+//    every XCD reads the same sum, adds it to its own copy of the residual
+//    stream, and all copies agree bit for bit.  Every other hand-off stays
+//    inside one XCD's L2.
 //  * Inside a workgroup (8 waves): waves 4..7 run a stage's GEMM and issue
 //    their first weight loads before its dependency is met; waves 0..3 run
 //    the LayerNorm rows of the stage before it, and then wave 0 alone polls
@@ -199,9 +202,6 @@ __device__ __forceinline__ float ld_dev(const float* p) {
 __device__ __forceinline__ float ld_dev(gptr<float> p) {
   return __hip_atomic_load((gw<float>)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ void st_dev(float* p, float v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
 __device__ __forceinline__ unsigned ld_flag(const unsigned* p) {
   return __hip_atomic_load((unsigned*)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -357,9 +357,11 @@ __device__ __forceinline__ const void* lw(const Wg& w, int l, int slot) {
 // ------------------------------------------------------------------ LayerNorm of one node row
 //
 // mode 0: x = wte[token] + wpe[position] (first layer);
-// mode 1: x += bias + part[X] for every XCD X that owns a share of the
-//         residual GEMM (bit X of own), in XCD order (device-coherent loads);
+// mode 1: x += float((S + bias) * 2^-32), S the fixed-point sum of every
+//         XCD's partial of the residual GEMM (device-coherent loads), the
+//         bias rounded to the same units: one rounding per element;
 // then a = (x - mean) / sqrt(var + eps) * g + b into this XCD's GEMM input.
+// The sums of sub-layer k live in buffer k % 3 (see xs_zero).
 // One wave: lane i takes the float4 chunks i, i + 64, ... (C per lane, so
 // d <= 256 C); sums run over the lane's chunks in order, then across lanes
 // by butterfly.  The other waves of the workgroup are free meanwhile.
@@ -410,12 +412,42 @@ __device__ __forceinline__ float half_sum(float x) {
   return half_pick(x, fadd_f);
 }
 
-// bit X set: XCD X owns a share of the range (heads, or MLP features)
-__device__ __forceinline__ unsigned owner_mask(const int* range) {
-  unsigned m = 0;
-#pragma unroll
-  for (int X = 0; X < kFXcd; ++X) m |= (range[2 * X + 1] > range[2 * X] ? 1u : 0u) << X;
-  return m;
+// Fixed-point residual sums.  Sub-layer k (2l: out-projection of layer l,
+// 2l + 1: its down-projection) is summed in buffer k % 3 of xacc.  A buffer
+// is cleared (each XCD its eighth of the columns of the rows below N) by the
+// LayerNorm that consumes the sum after it: the LayerNorm of sub-layer k
+// clears buffer (k - 1) % 3, which every XCD has read by then (that
+// LayerNorm waits for every XCD's sub-layer k, which each XCD runs after
+// its own LayerNorm of k - 1), and which is next added to by sub-layer
+// k + 2, which every XCD runs after the LayerNorm of k + 1, itself waiting
+// for every XCD's sub-layer k + 1 and so for every XCD's clearing.  The
+// first layer's LayerNorm clears buffers 0 and 1, and the first QKV stage
+// waits for all 256 workgroups' first LayerNorm, so a pass starts from clear
+// sums whatever the pass before it left (one that ended early included).
+constexpr double kFixScale = 4294967296.0;     // 2^32 units per 1.0
+constexpr float kFixMax = 134217728.f;         // 2^27: nine terms stay below 2^63
+__device__ __forceinline__ gw<long long> xs_row(const FusedArgs& a, int k, int n) {
+  return (gw<long long>)a.xacc + ((size_t)(k % 3) * kFMaxN + n) * a.d;
+}
+// this XCD's eighth of the columns of row n of buffer b, stored as zeros
+// (device-coherent stores, as the atomics that follow are performed beyond
+// the XCD's L2); run by waves 0..3
+__device__ __forceinline__ void xs_zero(const FusedArgs& a, const Wg& w, int b, int n) {
+  const int c8 = a.d / kFXcd, tid = opq_tid();
+  for (int c = tid; c < c8; c += QW * 64)
+    __hip_atomic_store(xs_row(a, b, n) + w.x * c8 + c, 0ll, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// adds this XCD's partial v of output o of node n to sub-layer k's sum; a
+// magnitude past 2^27 (or NaN) is counted in err (one count per wave) and
+// clamped, so the nine terms of a sum cannot overflow
+__device__ __forceinline__ void xs_add(const FusedArgs& a, int k, int n, int o, float v) {
+  const bool over = !(fabsf(v) <= kFixMax);
+  const unsigned long long m = __builtin_amdgcn_ballot_w64(over);
+  if (m && (int)__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u)) == __builtin_ctzll(m))
+    __hip_atomic_fetch_add(a.err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  const float vc = over ? (v > 0.f ? kFixMax : -kFixMax) : v;
+  __hip_atomic_fetch_add(xs_row(a, k, n) + o, (long long)llrint((double)vc * kFixScale), __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Waves 0..3 (256 threads) normalise R node rows n0, n0 + 32, ... (those
@@ -427,7 +459,7 @@ __device__ __forceinline__ unsigned owner_mask(const int* range) {
 // every row is issued together right after it.
 template <int C, int R>
 __device__ __forceinline__ bool ln_rows_q(const FusedArgs& a, const Wg& w, const WaitSpec& ws, int n0, int mode,
-                                          gptr<uint16_t> bias, const float* part, unsigned own, gptr<uint16_t> g,
+                                          gptr<uint16_t> bias, int kin, unsigned zmask, gptr<uint16_t> g,
                                           gptr<uint16_t> b, uint16_t* act) {
   const int d = a.d, nc = d / 4, tid = opq_tid(), wv = tid >> 6;
   float* red = (float*)(w.sh + 16);  // [R][8]
@@ -478,19 +510,20 @@ __device__ __forceinline__ bool ln_rows_q(const FusedArgs& a, const Wg& w, const
 #pragma unroll
       for (int i = 0; i < C; ++i) v[j][i] = bf4(tr[j][i]) + bf4(pr[j][i]);
   } else {
-    // every XCD's partials of the rows: device-coherent 16-byte loads
-    const __amdgpu_buffer_rsrc_t prs =
-        __builtin_amdgcn_make_buffer_rsrc((void*)part, (short)0, (int)(kFXcd * kFMaxN * d * 4), 0x00020000);
-    f32x4 pv[R][kFXcd][C];
+    // the rows' fixed-point sums: device-coherent 16-byte loads (two per
+    // float4 chunk)
+    const __amdgpu_buffer_rsrc_t srs = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(a.xacc + (size_t)(kin % 3) * kFMaxN * d), (short)0, (int)(kFMaxN * d * 8), 0x00020000);
+    u32x4 sv[R][C][2];
 #pragma unroll
     for (int j = 0; j < R; ++j)
 #pragma unroll
-      for (int X = 0; X < kFXcd; ++X)
+      for (int i = 0; i < C; ++i)
 #pragma unroll
-        for (int i = 0; i < C; ++i)
-          pv[j][X][i] = __builtin_bit_cast(
-              f32x4, __builtin_amdgcn_raw_buffer_load_b128(prs, (unsigned)(16 * cc[i]),
-                                                           (unsigned)(((size_t)X * kFMaxN + nr[j]) * d * 4), CP_SC1));
+        for (int hf = 0; hf < 2; ++hf)
+          sv[j][i][hf] = __builtin_bit_cast(
+              u32x4, __builtin_amdgcn_raw_buffer_load_b128(srs, (unsigned)(32 * cc[i] + 16 * hf),
+                                                           (unsigned)((size_t)nr[j] * d * 8), CP_SC1));
     const gptr<u32x2> c4 = (gptr<u32x2>)opq(bias);
     f32x4 xv[R][C];
     u32x2 cr[C];
@@ -502,28 +535,29 @@ __device__ __forceinline__ bool ln_rows_q(const FusedArgs& a, const Wg& w, const
 #pragma unroll
       for (int i = 0; i < C; ++i) xv[j][i] = xr[cc[i]];
     }
-    // bias, then the partials of the XCDs that own a share, in XCD order
+    // the sum plus the bias in the same units, rounded once to float
+    auto fx = [](unsigned lo, unsigned hi, float bv) {
+      const long long s = (long long)(((unsigned long long)hi << 32) | lo) + (long long)llrint((double)bv * kFixScale);
+      return (float)((double)s * (1.0 / kFixScale));
+    };
 #pragma unroll
     for (int j = 0; j < R; ++j)
 #pragma unroll
       for (int i = 0; i < C; ++i) {
-        f32x4 acc = bf4(cr[i]);
-        if (own == (1u << kFXcd) - 1) {
-#pragma unroll
-          for (int X = 0; X < kFXcd; ++X) acc += pv[j][X][i];
-        } else {
-#pragma unroll
-          for (int X = 0; X < kFXcd; ++X) {
-            const bool o = own >> X & 1u;
-            acc[0] += o ? pv[j][X][i][0] : 0.f;
-            acc[1] += o ? pv[j][X][i][1] : 0.f;
-            acc[2] += o ? pv[j][X][i][2] : 0.f;
-            acc[3] += o ? pv[j][X][i][3] : 0.f;
-          }
-        }
+        const f32x4 bb = bf4(cr[i]);
+        const f32x4 acc = {fx(sv[j][i][0].x, sv[j][i][0].y, bb[0]), fx(sv[j][i][0].z, sv[j][i][0].w, bb[1]),
+                           fx(sv[j][i][1].x, sv[j][i][1].y, bb[2]), fx(sv[j][i][1].z, sv[j][i][1].w, bb[3])};
         v[j][i] = xv[j][i] + acc;
       }
   }
+  // clear the buffers this stage is due to clear (its rows, this XCD's
+  // columns); issued after every load above
+#pragma unroll
+  for (int zb = 0; zb < 3; ++zb)
+    if (zmask >> zb & 1u)
+#pragma unroll
+      for (int j = 0; j < R; ++j)
+        if (n0 + j * kFRanks < a.N) xs_zero(a, w, zb, n0 + j * kFRanks);
   float sm[R];
 #pragma unroll
   for (int j = 0; j < R; ++j) {
@@ -657,8 +691,8 @@ struct PreSpec {
   WaitSpec ws;
   int mode;
   gptr<uint16_t> bias, g, b;
-  const float* part;
-  unsigned own;  // XCDs that own a share of the residual GEMM
+  int kin;          // the sub-layer whose fixed-point sums the rows add (mode 1)
+  unsigned zmask;   // sum buffers this stage clears (bit b: buffer b)
   uint16_t* act;
   // after the rows, waves 1..3 copy these weight fragments (row blocks
   // wrbs[0 .. wn) of W, k-steps [wk0, wk1) of KC) into LDS at wdst, in
@@ -681,18 +715,22 @@ __device__ __forceinline__ bool do_pre(const FusedArgs& a, const Wg& w, const Pr
     // this rank's rows: w.r and (at more than 32 nodes) w.r + 32, together
     const bool two = w.r + kFRanks < a.N;
     if (a.d <= 1024)
-      ok = two ? ln_rows_q<1, 2>(a, w, ps.ws, w.r, ps.mode, ps.bias, ps.part, ps.own, ps.g, ps.b, ps.act)
-               : ln_rows_q<1, 1>(a, w, ps.ws, w.r, ps.mode, ps.bias, ps.part, ps.own, ps.g, ps.b, ps.act);
+      ok = two ? ln_rows_q<1, 2>(a, w, ps.ws, w.r, ps.mode, ps.bias, ps.kin, ps.zmask, ps.g, ps.b, ps.act)
+               : ln_rows_q<1, 1>(a, w, ps.ws, w.r, ps.mode, ps.bias, ps.kin, ps.zmask, ps.g, ps.b, ps.act);
     else
-      ok = two ? ln_rows_q<2, 2>(a, w, ps.ws, w.r, ps.mode, ps.bias, ps.part, ps.own, ps.g, ps.b, ps.act)
-               : ln_rows_q<2, 1>(a, w, ps.ws, w.r, ps.mode, ps.bias, ps.part, ps.own, ps.g, ps.b, ps.act);
+      ok = two ? ln_rows_q<2, 2>(a, w, ps.ws, w.r, ps.mode, ps.bias, ps.kin, ps.zmask, ps.g, ps.b, ps.act)
+               : ln_rows_q<2, 1>(a, w, ps.ws, w.r, ps.mode, ps.bias, ps.kin, ps.zmask, ps.g, ps.b, ps.act);
   }
   if (!ok) return false;
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   q_barrier(w);
-  if (threadIdx.x == 0)
-    __hip_atomic_store(a.flags + (size_t)ps.fid * kFGroups + w.g, tag_of(w, ps.l, ps.fid), __ATOMIC_RELAXED,
-                       __HIP_MEMORY_SCOPE_WORKGROUP);
+  if (threadIdx.x == 0) {
+    // (the first layer's LayerNorm is waited for by every XCD: a
+    // device-coherent flag; the others are read inside the XCD)
+    unsigned* f = a.flags + (size_t)ps.fid * kFGroups + w.g;
+    if (ps.mode == 0) __hip_atomic_store(f, tag_of(w, ps.l, ps.fid), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    else __hip_atomic_store(f, tag_of(w, ps.l, ps.fid), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  }
   stamp(a, w, ps.l, ps.fid, 2);
   if (ps.wn > 0 && threadIdx.x >= 64) {
     // (not wave 0: its polls must not wait behind these loads; the stage's
@@ -734,9 +772,9 @@ __device__ __forceinline__ void epilogue(const FusedArgs& a, const Wg& w, int ep
         dst[(((size_t)l * a.H + h) * a.max_nodes + n) * DH + e] = f2bf(v);
       }
       break;
-    case FE_WO: st_dev(a.part_o + ((size_t)w.x * kFMaxN + n) * d + o, v); break;
+    case FE_WO: xs_add(a, 2 * l, n, o, v); break;
     case FE_FC: st_act(opq(a.ff), n, o, a.M / 32, gelu_tanh(v), a.err); break;
-    case FE_WPR: st_dev(a.part_p + ((size_t)w.x * kFMaxN + n) * d + o, v); break;
+    case FE_WPR: xs_add(a, 2 * l + 1, n, o, v); break;
     default: a.logits[(size_t)n * a.V + o] = v; break;
   }
 }
@@ -1321,7 +1359,6 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
   const int S = a.att_units;                 // prefix units of 256 cache rows
   const int nhx = a.xh[2 * w.x + 1] - a.xh[2 * w.x];
   const int n_attu = nhx * NTl * (S + 1);    // attention units of this XCD (prefix units + root unit per tile)
-  const unsigned own_h = owner_mask(a.xh), own_f = owner_mask(a.xf);
   // With two or more node tiles, the MLP down-projection's weights are
   // copied into LDS during the up-projection (by waves 1..3, which ran the
   // LayerNorm) when they fit.  The up-projection's closing wait covers the
@@ -1399,8 +1436,8 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
       }
       ps.ws = WaitSpec{FS_WO, -1, tag_of(w, l, FS_WO), true, l, FS_LN2};
       ps.bias = G<uint16_t>(lw(w, l, LB_O));
-      ps.part = a.part_o;
-      ps.own = own_h;
+      ps.kin = 2 * l;
+      ps.zmask = 1u << ((2 * l + 2) % 3);  // sub-layer 2l - 1's buffer
       ps.g = G<uint16_t>(lw(w, l, LN2G));
       ps.b = G<uint16_t>(lw(w, l, LN2B));
       ps.act = act2;
@@ -1417,8 +1454,9 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
       const int lp = kind == 8 ? L - 1 : max(l - 1, 0);
       ps.ws = WaitSpec{FS_WPR, -1, tag_of(w, lp, FS_WPR), kind == 8 || l > 0, l, FS_LN1};
       ps.bias = G<uint16_t>(lw(w, lp, LB_PR));
-      ps.part = a.part_p;
-      ps.own = own_f;
+      ps.kin = 2 * lp + 1;
+      // sub-layer 2lp's buffer; the first layer clears the first two
+      ps.zmask = ps.mode == 0 ? 3u : 1u << ((2 * lp) % 3);
       ps.g = kind == 8 ? G<uint16_t>(a.lnf_g) : G<uint16_t>(lw(w, l, LN1G));
       ps.b = kind == 8 ? G<uint16_t>(a.lnf_b) : G<uint16_t>(lw(w, l, LN1B));
       ps.act = act1;
@@ -1438,7 +1476,9 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
                Mo = a.V; break;
     }
     {
-      const WaitSpec gws{ps.fid, w.x, tag_of(w, l, ps.fid), true, l, gfid};
+      // (the first QKV stage waits for every XCD's first LayerNorm, which
+      // clears the first two sum buffers: see xs_zero)
+      const WaitSpec gws{ps.fid, (kind == 0 && l == 0) ? -1 : w.x, tag_of(w, l, ps.fid), true, l, gfid};
       if (!gemm_task<NT>(a, w, gws, epi, l, rbs, rb_first, nrb, bias, Wm, KCd, Mo, k0, k1, act, KCd, red, ps, 0,
                          kind == 8 ? &hbest : nullptr))
         goto out;

@@ -9,7 +9,8 @@
 //            in matrix-core fragment order for bf16 models (see st_act)
 //   part     fp32 [S][N][d]      split-K partial sums of the residual GEMMs
 //   K/V      storage type [L][H][rows][DH] (cache rows: positions; scratch rows: nodes)
-//   packed W 16x32 float16 fragments (exact copies of the bf16 weights);
+//   packed W 16x32 float16 fragments (the bf16 weights converted: exact for 0
+//            and magnitudes in [2^-17, 65504], within 2^-25 below);
 //            fragment (rb, kc) holds rows 16rb.., k 32kc..,
 //            lane l's 16 bytes = W[16rb + l%16][32kc + 8(l/16) .. +8], fragments
 //            ordered rb-major so one wave streams 1 KB contiguous per load.
@@ -55,7 +56,8 @@ template <> __device__ __forceinline__ void stT<uint16_t>(uint16_t* p, size_t i,
 // operand fragment is 1 KB contiguous: element (n, k) lives in fragment
 // f = (n/16) * ld + k/32 (ld = K/32), lane (n%16) + 16 ((k%32)/8), position
 // k%8.  The weights are multiplied as float16 too: their packed copies are
-// the bf16 values converted exactly (see pack_kernel).
+// the bf16 values converted to float16 (exact for 0 and magnitudes in
+// [2^-17, 65504]; see pack_kernel).
 // A float16 operand past the type's range (|v| > 65504, or NaN) would enter
 // the matrix cores as inf or NaN: such an element is counted in err (the
 // session's error counter) and stored as converted.

@@ -414,7 +414,7 @@ static ssd_status fused_setup(ssd_kv* kv) {
   const size_t o_fo = take((size_t)kFMaxN * d * 2), o_ff = take((size_t)kFMaxN * M * 2);
   const size_t att_parts = (size_t)(kv->max_ctx + kFAttRows - 1) / kFAttRows + 1;
   const size_t o_ap = take((size_t)c.n_head * 4 * att_parts * 16 * 68 * 4);
-  const size_t o_po = take((size_t)kFXcd * kFMaxN * d * 4), o_pp = take((size_t)kFXcd * kFMaxN * d * 4);
+  const size_t o_xs = take((size_t)3 * kFMaxN * d * 8);
   const size_t o_fl = take((size_t)kFStages * kFGroups * 4), o_ctl = take((size_t)kFCtlWords * 4);
   const size_t o_plan = take(tabs.size() * 4);
   const size_t o_tc = take((size_t)c.n_head * 4 * 4);
@@ -433,8 +433,7 @@ static ssd_status fused_setup(ssd_kv* kv) {
   a.fo = (uint16_t*)(b + o_fo);
   a.ff = (uint16_t*)(b + o_ff);
   a.apart = (float*)(b + o_ap);
-  a.part_o = (float*)(b + o_po);
-  a.part_p = (float*)(b + o_pp);
+  a.xacc = (long long*)(b + o_xs);
   a.flags = (unsigned*)(b + o_fl);
   a.ctl = (unsigned*)(b + o_ctl);
   a.tile_ctr = (unsigned*)(b + o_tc);

@@ -231,7 +231,7 @@ struct FusedArgs {
   int att_units;            // prefix units of 256 cache rows: ceil(P / 256)
   unsigned* tile_ctr;       // [H][4 tiles]: attention units of the tile done in this layer (wraps to 0)
   uint16_t* ff;             // GELU outputs, float16 fragments [4 tiles][M / 32][512]
-  float *part_o, *part_p;   // partial residuals [kFXcd][kFMaxN][d]
+  long long* xacc;          // [3][kFMaxN][d] fixed-point (2^-32) sums of the residual GEMMs' partials
   unsigned* flags;          // [kFStages][kFGroups]
   unsigned* ctl;            // [kFCtlWords]
   const int* plan;          // [kFGroups][kPlanStride]

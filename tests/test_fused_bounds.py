@@ -65,7 +65,7 @@ def check_pass(H, d, M, V, L, N, P, max_ctx, max_nodes):
     S = (P + ATT_ROWS - 1) // ATT_ROWS
     sizes = {
         "xr": XCD * MAXN * d, "q": MAXN * d, "act": XCD * MAXN * d, "fo": MAXN * d, "ff": MAXN * M,
-        "apart": H * 4 * att_parts * 16 * AREC, "tile_ctr": H * 4, "part": XCD * MAXN * d,
+        "apart": H * 4 * att_parts * 16 * AREC, "tile_ctr": H * 4, "xacc": 3 * MAXN * d,
         "logits": N * V, "kvt": L * H * max_nodes * DH, "kvc": L * H * max_ctx * DH,
         "w_qkv": (3 * d // 16) * KCd * 64, "w_o": RBd * KCd * 64, "w_fc": (M // 16) * KCd * 64,
         "w_pr": RBd * KCm * 64, "head": ((V + 15) // 16) * KCd * 64,
@@ -82,13 +82,16 @@ def check_pass(H, d, M, V, L, N, P, max_ctx, max_nodes):
         for r in range(RANKS):
             row = tab[x * RANKS + r]
             tag = f"x{x} r{r}"
-            # LayerNorm rows r, r + 32 below N: x row, partials, act row
+            # LayerNorm rows r, r + 32 below N: x row, fixed-point sum row of
+            # each buffer, this XCD's eighth of the columns cleared, act row
             for n in (r, r + RANKS):
                 if n >= N:
                     continue
                 c.rng(f"{tag} xr row", (x * MAXN + n) * d, (x * MAXN + n) * d + d - 1, sizes["xr"])
-                for X in range(XCD):
-                    c.rng(f"{tag} partial row", (X * MAXN + n) * d, (X * MAXN + n) * d + d - 1, sizes["part"])
+                for b in range(3):
+                    c.rng(f"{tag} sum row", (b * MAXN + n) * d, (b * MAXN + n) * d + d - 1, sizes["xacc"])
+                    c.rng(f"{tag} cleared columns", (b * MAXN + n) * d + x * (d // 8),
+                          (b * MAXN + n) * d + (x + 1) * (d // 8) - 1, sizes["xacc"])
                 c.rng(f"{tag} act row", act_base + act_index(n, 0, KCd), act_base + act_index(n, d - 4, KCd) + 3,
                       sizes["act"])
             # GEMM tasks: weights of each row block, activation fragments of every tile
@@ -117,7 +120,8 @@ def check_pass(H, d, M, V, L, N, P, max_ctx, max_nodes):
                             c.rng(f"{tag} k/v tree row", ((L - 1) * H + h) * max_nodes * DH,
                                   (((L - 1) * H + h) * max_nodes + N - 1) * DH + DH - 1, sizes["kvt"])
                 elif slot in (PL_WO, PL_WPR):
-                    c.rng(f"{tag} partial out", (x * MAXN) * d + o_lo, (x * MAXN + N - 1) * d + o_hi, sizes["part"])
+                    for b in range(3):
+                        c.rng(f"{tag} sum out", (b * MAXN) * d + o_lo, (b * MAXN + N - 1) * d + o_hi, sizes["xacc"])
                 elif slot == PL_FC:
                     c.rng(f"{tag} ff out", act_index(0, o_lo, KCm), act_index(N - 1, o_hi, KCm), sizes["ff"])
             # staged weights in LDS
