@@ -184,7 +184,12 @@ ssd_status ssd_tree_verify_greedy(const ssd_model *m, ssd_kv *kv, int32_t prefix
  * Outputs (device): accepted_path[0..*path_len-1] root first (path[0] = 0),
  * *next_token.  Emitted tokens are tokens[path[1..]] then next_token.
  * draft_probs must be non-NULL exactly for the two drawn modes; top_k < 0 is
- * SSD_E_INVALID_ARG. */
+ * SSD_E_INVALID_ARG; a sampling mode with vocab above 131072 is
+ * SSD_E_CAPACITY.  The sampling walk runs on ceil(vocab / 2048)
+ * workgroups that wait for each other; if they cannot all run at once
+ * within 0.5 s (the GPU held by other work), the walk gives up: *path_len
+ * is set to 0 (never a valid length) and the session's error counter counts
+ * it. */
 ssd_status ssd_tree_accept(ssd_kv *kv, const ssd_tree *tree, const float *draft_probs, const float *oracle_logits,
                            uint64_t rng_seed, int32_t *accepted_path, int32_t *path_len, int32_t *next_token,
                            void *stream);
@@ -193,13 +198,15 @@ ssd_status ssd_tree_accept(ssd_kv *kv, const ssd_tree *tree, const float *draft_
  * kernels) for callers that cannot allocate device memory: code under HIP
  * graph capture, tight serving loops, harnesses that forbid hipMalloc.  It
  * needs no session and calls no allocating routine: its scratch (the staged
- * tree, argmax partials, the sampling walk's float64 rows) is one file-scope
- * device array of 1,646,592 bytes that every GPU the library runs on holds
+ * tree, argmax partials, the sampling walk's exchange area) is one
+ * file-scope device array of 209,408 bytes that every GPU the library runs on holds
  * until the process ends, and the tree reaches the device inside the kernel
  * arguments.  Limits: n_nodes <= 256 and vocab <= 65536 (SSD_E_CAPACITY
  * beyond).  All calls on one GPU share that GPU's array: calls that overlap
  * on one GPU (two streams, or two host threads) race; calls ordered on one
- * stream do not.  Errors: as ssd_tree_accept, plus SSD_E_CAPACITY. */
+ * stream do not.  A sampling walk that gives up sets *path_len = 0 (there
+ * is no session to count it).  Errors: as ssd_tree_accept, plus
+ * SSD_E_CAPACITY. */
 ssd_status ssd_tree_accept_noalloc(const ssd_tree *tree, const float *draft_probs, const float *oracle_logits,
                                    uint64_t rng_seed, int32_t *accepted_path, int32_t *path_len,
                                    int32_t *next_token, void *stream);

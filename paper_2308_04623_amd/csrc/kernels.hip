@@ -225,6 +225,8 @@ static void ln_go_s(float* x, int N, int d, const float* part, int S, size_t pst
                     const void* g, const void* b, float eps, void* a, int lda, unsigned long long* sig,
                     unsigned* err, hipStream_t s) {
   if (S == 0) ln_go<T, E, 0>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, err, s);
+  else if (S == 1) ln_go<T, E, 1>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, err, s);
+  else if (S == 2) ln_go<T, E, 2>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, err, s);
   else if (S == 4) ln_go<T, E, 4>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, err, s);
   else if (S == 8) ln_go<T, E, 8>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, err, s);
   else ln_go<T, E, -1>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, err, s);
@@ -482,6 +484,118 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(NW / 4,
   }
 }
 
+// ------------------------------------------------------------------ weight GEMM for wide trees
+//
+// Above 64 nodes a workgroup of gemm_kernel reads every node's activations
+// (N x K float16) for one or two row blocks of weights, so activation bytes
+// dominate what each CU pulls in.  Here a workgroup owns RBT row blocks x
+// kG2TT node tiles of the output over one k-range and reads RBT + kG2TT
+// fragments per k-step.  Its four waves split the k-steps (wave w: kc0 + w,
+// + 4, ...), each multiplying every weight fragment of a step into every
+// activation fragment of it on v_mfma_f32_16x16x32_f16, and the waves'
+// tiles are summed through LDS in wave order, one row block at a time.  The
+// workgroups of one row-block group are placed on one XCD (workgroup b runs
+// on XCD b % 8), so the weights they share come from HBM once and then from
+// that XCD's L2.  Block b: XCD x = b % 8; q = b / 8 names (group i = x + 8
+// (q / (gt gy)), node-tile group j, k-split sk); groups past gx exit.
+constexpr int kG2TT = 4;  // node tiles per workgroup
+
+template <int RBT, int KIND, int U>
+__global__ __launch_bounds__(256) void gemm2d_kernel(const u32x4* __restrict__ Wp, int KC, int RBtot, int NT,
+                                                     int kcs, int gx, int gt, int gy,
+                                                     const uint16_t* __restrict__ act, Epi ep) {
+  constexpr int TT = kG2TT;
+  __shared__ float red[4 * TT * 16 * 16];
+  pass_signal(ep.sig);
+  const int b = blockIdx.x, x = b & 7, q = b >> 3, per = gt * gy;
+  const int i = x + 8 * (q / per), rem = q % per;
+  const int j = rem / gy, sk = rem % gy;
+  if (i >= gx) return;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+  const int rb0 = i * RBT, t0 = j * TT;
+  const int kc0 = sk * kcs, kc1 = min(KC, kc0 + kcs);
+  const int nsteps = kc1 - kc0 > w ? (kc1 - kc0 - w + 3) / 4 : 0;
+  // row blocks past the matrix and node tiles past the tree read the last
+  // one instead and are never stored
+  const u32x4* wb[RBT];
+  const u32x4* ab[TT];
+#pragma unroll
+  for (int r = 0; r < RBT; ++r) wb[r] = Wp + (size_t)min(rb0 + r, RBtot - 1) * KC * 64 + lane;
+#pragma unroll
+  for (int t = 0; t < TT; ++t) ab[t] = (const u32x4*)act + (size_t)min(t0 + t, NT - 1) * KC * 64 + lane;
+  u32x4 wq[U][RBT], bq[U][TT];
+  const int klast = kc1 - 1;
+  auto load_step = [&](int s, int u) {
+    const int kc = min(kc0 + w + 4 * s, klast);
+#pragma unroll
+    for (int r = 0; r < RBT; ++r) wq[u][r] = wb[r][(size_t)kc * 64];
+#pragma unroll
+    for (int t = 0; t < TT; ++t) bq[u][t] = ab[t][(size_t)kc * 64];
+  };
+  f32x4 acc[RBT][TT];
+#pragma unroll
+  for (int r = 0; r < RBT; ++r)
+#pragma unroll
+    for (int t = 0; t < TT; ++t) acc[r][t] = (f32x4){0.f, 0.f, 0.f, 0.f};
+  if (nsteps > 0) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) load_step(u, u);
+    __builtin_amdgcn_sched_barrier(0);
+    for (int s0 = 0; s0 < nsteps; s0 += U) {
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        // (the step guard is uniform per wave: a select, never a branch
+        // around an MFMA)
+        const bool ok = s0 + u < nsteps;
+#pragma unroll
+        for (int r = 0; r < RBT; ++r) {
+          const u32x4 wf = ok ? wq[u][r] : (u32x4){0, 0, 0, 0};
+#pragma unroll
+          for (int t = 0; t < TT; ++t)
+            acc[r][t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, wf),
+                                                               __builtin_bit_cast(f16x8, bq[u][t]), acc[r][t], 0, 0, 0);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        load_step(s0 + u + U, u);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+  }
+  Epi e2 = ep;
+  e2.split = sk;
+#pragma unroll
+  for (int r = 0; r < RBT; ++r) {
+    if (rb0 + r >= RBtot) break;
+    // lane l of a tile holds rows 4 (l / 16) + c, node l % 16
+#pragma unroll
+    for (int t = 0; t < TT; ++t)
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+        red[((w * TT + t) * 16 + (lane & 15)) * 16 + 4 * (lane >> 4) + c] = acc[r][t][c];
+    __syncthreads();
+    for (int idx = tid; idx < TT * 256; idx += 256) {
+      const int row = idx & 15, node = t0 * 16 + (idx >> 4);
+      float sum = red[idx];
+#pragma unroll
+      for (int ww = 1; ww < 4; ++ww) sum += red[ww * TT * 256 + idx];
+      const int o = (rb0 + r) * 16 + row;
+      if (o < ep.M && node < ep.N) epilogue<uint16_t, KIND>(e2, node, o, sum);
+    }
+    __syncthreads();
+  }
+}
+
+// row blocks per workgroup of the wide-tree GEMM for a kind and node-tile
+// group count: enough workgroups to cover the 256 CUs, as few activation
+// re-reads as that allows (the LM head, with thousands of row blocks, takes 8)
+static int g2_rbt(int kind, int gt) {
+  if (kind == EPI_LOGITS) return 8;
+  if (kind == EPI_PARTIAL) return gt <= 2 ? 1 : 2;
+  return gt <= 2 ? 2 : 4;
+}
+
+bool gemm_wide(int vec, int N) { return !vec && N > 64; }
+
 // Tile shape per node count and GEMM kind (measured on the GPT-2-L shapes:
 // K = 1280 for QKV / MLP up / attention out, 5120 for MLP down).  At 17-32
 // nodes: QKV one row block per workgroup (240 workgroups), the others two;
@@ -516,6 +630,15 @@ int gemm_split_kc(int M, int K, int N, int vec, int want_split, int* splits) {
     *splits = 1;
     return KC;
   }
+  if (gemm_wide(vec, N)) {
+    const int gt = ((N + 15) / 16 + kG2TT - 1) / kG2TT;
+    const int gx = ((M + 15) / 16 + g2_rbt(EPI_PARTIAL, gt) - 1) / g2_rbt(EPI_PARTIAL, gt);
+    int S = 1;
+    while (S * gx * gt < 256 && S < kMaxSplits) S *= 2;
+    const int kcs = (KC + S - 1) / S;
+    *splits = (KC + kcs - 1) / kcs;
+    return kcs;
+  }
   const int rb = gemm_cfg(N, vec, EPI_PARTIAL).rb;
   const int gx = ((M + 15) / 16 + rb - 1) / rb;
   int S = 1;  // a power of two with S * gx >= 256 workgroups
@@ -535,6 +658,16 @@ GemmGeom gemm_geom(int kind, int vec, int M, int K, int N, int kcs) {
   g.KC = K / 32;
   g.RBtot = (M + 15) / 16;
   g.kcs = kcs;
+  if (gemm_wide(vec, N)) {
+    // the wide-tree kernel as the prefetcher sees it: row-block groups
+    // padded to a multiple of 8, so that group bx runs on XCD bx % 8 (plus
+    // the launch's offset) like block bx of the plain kernel
+    const int gt = ((N + 15) / 16 + kG2TT - 1) / kG2TT;
+    g.RB = g2_rbt(kind, gt);
+    g.gx = 8 * (((g.RBtot + g.RB - 1) / g.RB + 7) / 8);
+    g.gy = (g.KC + kcs - 1) / kcs;
+    return g;
+  }
   if (vec) g.RB = 1;
   else if (kind == EPI_LOGITS) g.RB = head_rb(gemm_cfg(N, 0, kind).nt);
   else g.RB = gemm_cfg(N, 0, kind).rb;
@@ -562,10 +695,43 @@ static void gemm_go(int kind, const GemmGeom& g, const void* Wp, const uint16_t*
   }
 }
 
+template <int RBT, int U>
+static void gemm2d_go(int kind, const u32x4* Wp, int KC, int RBtot, int NT, int kcs, int gx, int gt, int gy,
+                      const uint16_t* act, const Epi& ep, hipStream_t s) {
+  const dim3 grid(8 * ((gx + 7) / 8) * gt * gy);
+  switch (kind) {
+    case EPI_QKV: gemm2d_kernel<RBT, EPI_QKV, U><<<grid, 256, 0, s>>>(Wp, KC, RBtot, NT, kcs, gx, gt, gy, act, ep); break;
+    case EPI_PARTIAL:
+      gemm2d_kernel<RBT, EPI_PARTIAL, U><<<grid, 256, 0, s>>>(Wp, KC, RBtot, NT, kcs, gx, gt, gy, act, ep);
+      break;
+    case EPI_GELU: gemm2d_kernel<RBT, EPI_GELU, U><<<grid, 256, 0, s>>>(Wp, KC, RBtot, NT, kcs, gx, gt, gy, act, ep); break;
+    default:
+      gemm2d_kernel<RBT, EPI_LOGITS, U><<<grid, 256, 0, s>>>(Wp, KC, RBtot, NT, kcs, gx, gt, gy, act, ep);
+      break;
+  }
+}
+
+static hipError_t launch_gemm_wide(int kind, const void* Wp, int M, int K, const uint16_t* act, int kcs,
+                                   const Epi& ep, hipStream_t s) {
+  const int KC = K / 32, RBtot = (M + 15) / 16, NT = (ep.N + 15) / 16;
+  const int gt = (NT + kG2TT - 1) / kG2TT, rbt = g2_rbt(kind, gt);
+  const int gx = (RBtot + rbt - 1) / rbt, gy = (KC + kcs - 1) / kcs;
+  if (kind != EPI_PARTIAL && gy != 1) return hipErrorInvalidValue;
+  const u32x4* W = (const u32x4*)Wp;
+  switch (rbt) {
+    case 1: gemm2d_go<1, 2>(kind, W, KC, RBtot, NT, kcs, gx, gt, gy, act, ep, s); break;
+    case 2: gemm2d_go<2, 2>(kind, W, KC, RBtot, NT, kcs, gx, gt, gy, act, ep, s); break;
+    case 4: gemm2d_go<4, 2>(kind, W, KC, RBtot, NT, kcs, gx, gt, gy, act, ep, s); break;
+    default: gemm2d_go<8, 1>(kind, W, KC, RBtot, NT, kcs, gx, gt, gy, act, ep, s); break;
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_gemm_bf16(int kind, int vec, const void* Wp, int M, int K, const uint16_t* act, int kcs,
                             const Epi& ep, hipStream_t s) {
   if (kcs <= 0) return hipErrorInvalidValue;
   if (ep.N > (vec ? 16 : 256)) return hipErrorInvalidValue;
+  if (gemm_wide(vec, ep.N)) return launch_gemm_wide(kind, Wp, M, K, act, kcs, ep, s);
   const GemmGeom g = gemm_geom(kind, vec, M, K, ep.N, kcs);
   if (kind == EPI_LOGITS && !vec) {
     switch (gemm_cfg(ep.N, 0, kind).nt) {
@@ -1581,34 +1747,6 @@ __device__ double philox_uniform(uint64_t seed, uint64_t stream, uint64_t ctr0) 
   return (double)(c0 >> 11) * 0x1.0p-53;
 }
 
-#define SA_THREADS 1024
-
-// every thread sums its contiguous chunk of the vocabulary in index order;
-// chunk sums are then added pairwise in a fixed tree
-__device__ double block_sum_chunks(double v, double* red) {
-  red[threadIdx.x] = v;
-  __syncthreads();
-  for (int off = SA_THREADS / 2; off > 0; off >>= 1) {
-    if (threadIdx.x < off) red[threadIdx.x] = red[threadIdx.x] + red[threadIdx.x + off];
-    __syncthreads();
-  }
-  const double r = red[0];
-  __syncthreads();
-  return r;
-}
-
-__device__ double block_max_d(double v, double* red) {
-  red[threadIdx.x] = v;
-  __syncthreads();
-  for (int off = SA_THREADS / 2; off > 0; off >>= 1) {
-    if (threadIdx.x < off) red[threadIdx.x] = fmax(red[threadIdx.x], red[threadIdx.x + off]);
-    __syncthreads();
-  }
-  const double r = red[0];
-  __syncthreads();
-  return r;
-}
-
 // order-preserving key of a logit: a larger key is a larger value (-0 and
 // +0 map to the same key, as they compare equal)
 __device__ __forceinline__ unsigned mono_key(float f) {
@@ -1616,217 +1754,538 @@ __device__ __forceinline__ unsigned mono_key(float f) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-// The top-k cut of one row (every thread takes its contiguous chunk
-// [v0, v1)): the k-th largest key thr (radix select, 8 bits per pass from the
-// top), how many of the tokens whose key equals thr are kept (take; lowest ids
-// first) and how many such ties lie in lower threads' chunks (tie_base).  A
-// token is kept iff its key exceeds thr, or equals it with tie rank < take.
-__device__ void topk_cut(const float* row, int v0, int v1, int k, unsigned* hist, int* scan, int* sh2,
-                         unsigned& thr, int& take, int& tie_base) {
-  const int tid = threadIdx.x;
-  unsigned prefix = 0, mask = 0;
-  int need = k;
-  for (int pass = 0; pass < 4; ++pass) {
-    const int shift = 24 - 8 * pass;
-    for (int i = tid; i < 256; i += SA_THREADS) hist[i] = 0;
-    __syncthreads();
-    for (int v = v0; v < v1; ++v) {
-      const unsigned key = mono_key(row[v]);
-      if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
-    }
-    __syncthreads();
-    if (tid == 0) {
-      int cum = 0, d = 255;
-      for (; d > 0; --d) {
-        if (cum + (int)hist[d] >= need) break;
-        cum += (int)hist[d];
-      }
-      sh2[0] = d;
-      sh2[1] = need - cum;
-    }
-    __syncthreads();
-    prefix |= (unsigned)sh2[0] << shift;
-    mask |= 255u << shift;
-    need = sh2[1];
-    __syncthreads();
+// Recursive rejection sampling down the tree (Sec. 2.3 over the tree batch
+// of Sec. 3.1), spread over G = ceil(V / 2048) workgroups: workgroup g holds
+// the vocabulary slice [2048 g, 2048 g + 2048) of the current node's target
+// p, residual r and draft row q in LDS (float64), thread t the 8 entries
+// 8t .. 8t + 7 of the slice.  Every decision needs a few sums over the whole
+// vocabulary; the workgroups exchange their slices' values in rounds: each
+// stores a record, waits for its stores, raises its round flag, and waits
+// for all G flags of the round, then reads every record and combines them
+// in slice order, so all workgroups hold the same sums and take the same
+// branches.  Records alternate between two buffers by round parity: a
+// workgroup writes round k + 2 only after every workgroup has raised round
+// k + 1, which each does after reading round k.
+//
+// Placement: 8 G workgroups are launched and those of index 8 g take slice
+// g (the others leave at once), so that with the usual round-robin dispatch
+// all G share one XCD.  The first round exchanges each workgroup's XCD; if
+// they agree, later rounds keep records and flags in that XCD's L2 (plain
+// stores; readers drop their CU's L1 first), otherwise every access is
+// device-coherent (sc1) throughout.
+//
+// Rounds per node: the radix select of the top-k cut (4, plus 1 for the
+// tie ranks), the softmax statistics (max, rescaled sum, draft sum: 1), then
+// one per tested child: the owner of the child's token decides, and every
+// workgroup adds up its slice's residual as it would be after a rejection;
+// on rejection every workgroup applies it.  The extra token takes one more
+// round (slice sums, then a scan of the crossing slice).
+//
+// Round flags carry epoch * 65536 + round, the epoch read from ctl[0] at
+// start (the last workgroup to finish raises it), so nothing is cleared
+// between calls.  Every wait is bounded; a wait that times out (the
+// workgroups could not all run at once) raises ctl[2], every workgroup
+// leaves, *path_len is set to 0 and err (when given) counts it.
+// mode: 1 siblings drawn without replacement from draft row u, 2 drawn
+// independently, 3 chosen (each child proposed with certainty; no draft
+// rows).  topk > 0 restricts every target to the row's topk largest logits
+// (ties at the cut to the lower id).
+
+constexpr int SW_THREADS = 256, SW_SLICE = 2048, SW_PER = SW_SLICE / SW_THREADS, SW_MAXG = 64, SW_REC = 4;
+constexpr int SW_MAXN = 1024;  // nodes (the tree's parents sit in LDS)
+enum { SWC_EPOCH = 0, SWC_DONE = 1, SWC_ABORT = 2, SWC_FLAGS = 64 };
+// work layout (bytes): ctl + flags (u32[SWC_FLAGS + SW_MAXG]), records
+// double[2][SW_MAXG][SW_REC], histograms u32[2][SW_MAXG][256]
+constexpr size_t kSwRecOfs = (SWC_FLAGS + SW_MAXG) * 4;
+constexpr size_t kSwHistOfs = kSwRecOfs + (size_t)2 * SW_MAXG * SW_REC * 8;
+constexpr size_t kSwBytes = kSwHistOfs + (size_t)2 * SW_MAXG * 256 * 4;
+
+struct SwArgs {
+  const int* tokens;
+  const int* parents;
+  int N, V, G;
+  const float* logits;
+  const float* draft;
+  double T;
+  uint64_t seed;
+  int mode, topk;
+  int* path;
+  int* path_len;
+  int* next;
+  unsigned char* work;
+  unsigned* err;
+  unsigned long long timeout;
+};
+
+struct SwState {
+  unsigned* ctl;
+  unsigned* flags;
+  double* rec;     // [2][SW_MAXG][SW_REC]
+  unsigned* hist;  // [2][SW_MAXG][256]
+  unsigned tagbase;
+  int k;           // rounds done
+  bool local;      // every workgroup on one XCD: records and flags through its L2
+};
+
+__device__ __forceinline__ unsigned sw_xcc() {
+  unsigned x;
+  asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(x));
+  return x & 15;
+}
+__device__ __forceinline__ double* sw_rec(SwState& st, int par, int g) {
+  return st.rec + ((size_t)par * SW_MAXG + g) * SW_REC;
+}
+__device__ __forceinline__ unsigned* sw_hist(SwState& st, int par, int g) {
+  return st.hist + ((size_t)par * SW_MAXG + g) * 256;
+}
+// local: plain stores into the XCD's L2, read with non-temporal loads
+// (which do not hit lines the reader's L1 kept from an earlier round);
+// otherwise device-coherent (sc1) accesses
+template <typename T>
+__device__ __forceinline__ void sw_st(const SwState& st, T* p, T v) {
+  if (st.local) *(__attribute__((address_space(1))) T*)p = v;
+  else __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+template <typename T>
+__device__ __forceinline__ T sw_ld(const SwState& st, const T* p) {
+  if (st.local) return __builtin_nontemporal_load((const __attribute__((address_space(1))) T*)p);
+  return __hip_atomic_load((T*)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Fixed-order sums and maxima over the workgroup: each wave's value by a
+// butterfly, lane 0's result taken (every lane then holds the same value),
+// then the four waves in order; every thread returns the same value.
+__device__ __forceinline__ double sw_wave_sum(double v) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return __shfl(v, 0);
+}
+__device__ __forceinline__ double sw_wave_max(double v) {
+  for (int o = 32; o > 0; o >>= 1) v = fmax(v, __shfl_xor(v, o));
+  return __shfl(v, 0);
+}
+__device__ void sw_sum2(double& a, double& b, double* red) {
+  const double wa = sw_wave_sum(a), wb = sw_wave_sum(b);
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+    red[w] = wa;
+    red[4 + w] = wb;
   }
-  thr = prefix;
-  take = need;
-  int cnt = 0;
-  for (int v = v0; v < v1; ++v) cnt += mono_key(row[v]) == thr;
-  scan[tid] = cnt;
   __syncthreads();
-  for (int off = 1; off < SA_THREADS; off <<= 1) {
-    const int t = tid >= off ? scan[tid - off] : 0;
-    __syncthreads();
-    scan[tid] += t;
-    __syncthreads();
+  a = (red[0] + red[1]) + (red[2] + red[3]);
+  b = (red[4] + red[5]) + (red[6] + red[7]);
+  __syncthreads();
+}
+__device__ double sw_max(double v, double* red) {
+  const double wv = sw_wave_max(v);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = wv;
+  __syncthreads();
+  const double r = fmax(fmax(red[0], red[1]), fmax(red[2], red[3]));
+  __syncthreads();
+  return r;
+}
+
+// Publishes this workgroup's round (its record stores issued before) and
+// waits for every workgroup's; false on abort or timeout (in every thread).
+__device__ bool sw_round(const SwArgs& a, SwState& st, int g, int* shok) {
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  const unsigned tag = st.tagbase + (unsigned)st.k + 1u;
+  if (threadIdx.x == 0) sw_st(st, st.flags + g, tag);
+  if (threadIdx.x < 64) {
+    const unsigned long long t0 = __builtin_amdgcn_s_memrealtime();
+    bool ok = false;
+    for (;;) {
+      bool mine = true;
+      for (int i = threadIdx.x; i < a.G; i += 64)
+        mine = mine && (int)(__hip_atomic_load(st.flags + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) - tag) >= 0;
+      if (__all(mine)) {
+        ok = true;
+        break;
+      }
+      if (__hip_atomic_load(st.ctl + SWC_ABORT, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) break;
+      if (__builtin_amdgcn_s_memrealtime() - t0 > a.timeout) {
+        if (threadIdx.x == 0 && __hip_atomic_exchange(st.ctl + SWC_ABORT, 1u, __ATOMIC_RELAXED,
+                                                      __HIP_MEMORY_SCOPE_AGENT) == 0u && a.err)
+          __hip_atomic_fetch_add(a.err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
+    if (threadIdx.x == 0) *shok = ok;
   }
-  tie_base = scan[tid] - cnt;
+  __syncthreads();
+  const bool ok = *shok != 0;
+  if (ok && st.local) asm volatile("buffer_inv sc0" ::: "memory");
+  __syncthreads();
+  ++st.k;
+  return ok;
+}
+
+// every workgroup's record of round parity par into LDS (thread i loads
+// workgroup i's), for the combining thread to read in slice order
+__device__ __forceinline__ void sw_gather(SwState& st, int par, int G, double (*gb)[SW_REC]) {
+  for (int i = threadIdx.x; i < G; i += SW_THREADS)
+#pragma unroll
+    for (int j = 0; j < SW_REC; ++j) gb[i][j] = sw_ld(st, sw_rec(st, par, i) + j);
   __syncthreads();
 }
 
-// Recursive rejection sampling down the tree (Sec. 2.3 over the tree batch
-// of Sec. 3.1), one workgroup.  mode: 1 siblings drawn without replacement
-// from draft row u, 2 drawn independently, 3 chosen (each child proposed with
-// certainty; no draft rows).  topk > 0 restricts every target to the row's
-// topk largest logits (ties at the cut to the lower id).
-__global__ __launch_bounds__(SA_THREADS) void sample_accept_kernel(
-    const int* __restrict__ tokens, const int* __restrict__ parents, int N, int V, const float* __restrict__ logits,
-    const float* __restrict__ draft, double T, uint64_t seed, int mode, int topk, double* __restrict__ r,
-    double* __restrict__ p, double* __restrict__ qq, int* __restrict__ path, int* __restrict__ path_len,
-    int* __restrict__ next) {
-  __shared__ double red[SA_THREADS];
-  __shared__ int scan[SA_THREADS];
-  __shared__ unsigned hist[256];
-  __shared__ int sh2[2];
-  const int tid = threadIdx.x;
-  const int C = (V + SA_THREADS - 1) / SA_THREADS;
-  const int v0 = min(V, tid * C), v1 = min(V, v0 + C);
-  const bool wor = mode == 1, det = mode == 3;
-  const bool cut = topk > 0 && topk < V;
+// the first child of u above index c0 (N if none): every thread tests its
+// share of the candidates, then the smallest hit over the workgroup
+__device__ __forceinline__ int sw_next_child(const int* par_l, int N, int u, int c0, int* shmin) {
+  int best = N;
+  for (int c = c0 + 1 + (int)threadIdx.x; c < N; c += SW_THREADS)
+    if (par_l[c] == u) {
+      best = c;
+      break;
+    }
+  for (int o = 32; o > 0; o >>= 1) best = min(best, __shfl_xor(best, o));
+  if ((threadIdx.x & 63) == 0) shmin[threadIdx.x >> 6] = best;
+  __syncthreads();
+  const int r = min(min(shmin[0], shmin[1]), min(shmin[2], shmin[3]));
+  __syncthreads();
+  return r;
+}
+
+__global__ __launch_bounds__(SW_THREADS) void sample_accept_kernel(SwArgs a) {
+  if (blockIdx.x & 7) return;  // (see Placement above)
+  __shared__ double r[SW_SLICE], p[SW_SLICE], q[SW_SLICE];
+  __shared__ double red[8], cs[SW_THREADS];
+  __shared__ unsigned hl[256];
+  __shared__ int shi[8];
+  __shared__ double shd[8];
+  __shared__ double gb[SW_MAXG][SW_REC];
+  __shared__ int par_l[SW_MAXN], shmin[4];
+  const int tid = threadIdx.x, g = blockIdx.x >> 3, G = a.G, V = a.V;
+  for (int i = tid; i < a.N; i += SW_THREADS) par_l[i] = a.parents[i];
+  const int b0 = g * SW_SLICE + tid * SW_PER;  // this thread's first vocabulary index
+  const bool wor = a.mode == 1, det = a.mode == 3;
+  const bool cut = a.topk > 0 && a.topk < V;
+  SwState st;
+  st.ctl = (unsigned*)a.work;
+  st.flags = st.ctl + SWC_FLAGS;
+  st.rec = (double*)(a.work + kSwRecOfs);
+  st.hist = (unsigned*)(a.work + kSwHistOfs);
+  st.k = 0;
+  st.local = false;
+  if (tid == 0) shi[0] = (int)__hip_atomic_load(st.ctl + SWC_EPOCH, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __syncthreads();
+  st.tagbase = ((unsigned)shi[0] + 1u) * 65536u;
+  // round 0: where every workgroup runs
+  if (tid == 0) sw_st(st, sw_rec(st, 0, g), (double)sw_xcc());
+  bool ok = sw_round(a, st, g, shi + 1);
+  if (ok) {
+    sw_gather(st, 0, G, gb);
+    bool same = true;
+    for (int i = 0; i < G; ++i) same = same && gb[i][0] == gb[0][0];
+    st.local = same;
+    __syncthreads();
+  }
   int u = 0, len = 1;
-  if (tid == 0) path[0] = 0;
-  double Z = 1.0;
-  for (;;) {
-    const float* row = logits + (size_t)u * V;
-    unsigned thr = 0;
-    int take = 0, tie_rank = 0;
-    if (cut) topk_cut(row, v0, v1, topk, hist, scan, sh2, thr, take, tie_rank);
-    // p = softmax(row / T) over the kept tokens
-    double mx = -INFINITY;
-    int tr = tie_rank;
-    for (int v = v0; v < v1; ++v) {
-      bool keep = true;
-      if (cut) {
-        const unsigned key = mono_key(row[v]);
-        keep = key > thr || (key == thr && tr++ < take);
-      }
-      if (keep) mx = fmax(mx, (double)row[v] / T);
+  if (ok && g == 0 && tid == 0) a.path[0] = 0;
+  double Z = 1.0, Zq = 0.0;
+  while (ok) {
+    // ---- the target at node u: the thread's logits (and draft entries)
+    float lg[SW_PER];
+    unsigned key[SW_PER];
+    bool keep[SW_PER];
+#pragma unroll
+    for (int i = 0; i < SW_PER; ++i) {
+      const int v = b0 + i;
+      lg[i] = v < V ? a.logits[(size_t)u * V + v] : 0.f;
+      keep[i] = v < V;
+      key[i] = mono_key(lg[i]);
+      q[tid * SW_PER + i] = (!det && v < V) ? (double)a.draft[(size_t)u * V + v] : 0.0;
     }
-    mx = block_max_d(mx, red);
-    double s = 0.0;
-    tr = tie_rank;
-    for (int v = v0; v < v1; ++v) {
-      bool keep = true;
-      if (cut) {
-        const unsigned key = mono_key(row[v]);
-        keep = key > thr || (key == thr && tr++ < take);
+    if (cut) {
+      // radix select of the topk-th largest key over all slices, 8 bits a pass
+      unsigned prefix = 0, mask = 0;
+      int need = a.topk;
+      for (int pass = 0; pass < 4; ++pass) {
+        const int shift = 24 - 8 * pass;
+        hl[tid] = 0;
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < SW_PER; ++i)
+          if (keep[i] && (key[i] & mask) == prefix) atomicAdd(&hl[(key[i] >> shift) & 255u], 1u);
+        __syncthreads();
+        const int par = st.k & 1;
+        sw_st(st, sw_hist(st, par, g) + tid, hl[tid]);
+        ok = sw_round(a, st, g, shi + 1);
+        if (!ok) break;
+        unsigned tot = 0;
+        for (int gg = 0; gg < G; ++gg) tot += sw_ld(st, sw_hist(st, par, gg) + tid);
+        hl[tid] = tot;
+        __syncthreads();
+        if (tid == 0) {
+          int cum = 0, dgt = 255;
+          for (; dgt > 0; --dgt) {
+            if (cum + (int)hl[dgt] >= need) break;
+            cum += (int)hl[dgt];
+          }
+          shi[2] = dgt;
+          shi[3] = need - cum;
+        }
+        __syncthreads();
+        prefix |= (unsigned)shi[2] << shift;
+        mask |= 255u << shift;
+        need = shi[3];
+        __syncthreads();
       }
-      const double e = keep ? exp((double)row[v] / T - mx) : 0.0;
-      p[v] = e;
-      s += e;
-    }
-    const double S = block_sum_chunks(s, red);
-    double sq = 0.0;
-    for (int v = v0; v < v1; ++v) {
-      p[v] = p[v] / S;
-      r[v] = p[v];
-      if (!det) {
-        qq[v] = (double)draft[(size_t)u * V + v];
-        sq += qq[v];
+      if (!ok) break;
+      // tie ranks at the cut: ties in lower slices, lower threads, then in order
+      int cnt = 0;
+#pragma unroll
+      for (int i = 0; i < SW_PER; ++i) cnt += keep[i] && key[i] == prefix;
+      cs[tid] = (double)cnt;
+      __syncthreads();
+      if (tid == 0) {
+        double run = 0.0;
+        for (int t = 0; t < SW_THREADS; ++t) {
+          const double c = cs[t];
+          cs[t] = run;
+          run += c;
+        }
+        shd[0] = run;
+      }
+      __syncthreads();
+      int rank = (int)cs[tid];
+      const int par = st.k & 1;
+      if (tid == 0) sw_st(st, sw_rec(st, par, g), shd[0]);
+      ok = sw_round(a, st, g, shi + 1);
+      if (!ok) break;
+      sw_gather(st, par, G, gb);
+      double base = 0.0;
+      for (int gg = 0; gg < g; ++gg) base += gb[gg][0];
+      rank += (int)base;
+#pragma unroll
+      for (int i = 0; i < SW_PER; ++i) {
+        if (!keep[i] || key[i] > prefix) continue;
+        keep[i] = key[i] == prefix && rank++ < need;
       }
     }
-    double Zq = block_sum_chunks(sq, red);  // includes the barrier that publishes r, qq
+    // ---- softmax statistics over the kept entries, and the draft row's sum
+    double mloc = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < SW_PER; ++i)
+      if (keep[i]) mloc = fmax(mloc, (double)lg[i] / a.T);
+    const double m_g = sw_max(mloc, red);
+    double sl = 0.0, ql = 0.0;
+#pragma unroll
+    for (int i = 0; i < SW_PER; ++i) {
+      if (keep[i]) sl += exp((double)lg[i] / a.T - m_g);
+      ql += q[tid * SW_PER + i];
+    }
+    sw_sum2(sl, ql, red);
+    {
+      const int par = st.k & 1;
+      if (tid == 0) {
+        double* rc = sw_rec(st, par, g);
+        sw_st(st, rc, m_g);
+        sw_st(st, rc + 1, sl);
+        sw_st(st, rc + 2, ql);
+      }
+      ok = sw_round(a, st, g, shi + 1);
+      if (!ok) break;
+      sw_gather(st, par, G, gb);
+      if (tid == 0) {
+        double M = -INFINITY;
+        for (int gg = 0; gg < G; ++gg) M = fmax(M, gb[gg][0]);
+        double S = 0.0, Sq = 0.0;
+        for (int gg = 0; gg < G; ++gg) {
+          const double mg = gb[gg][0];
+          if (mg != -INFINITY) S += gb[gg][1] * exp(mg - M);
+          Sq += gb[gg][2];
+        }
+        shd[1] = M;
+        shd[2] = S;
+        shd[3] = Sq;
+      }
+      __syncthreads();
+    }
+    const double M = shd[1], S = shd[2];
+    Zq = shd[3];
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < SW_PER; ++i) {
+      const double pv = keep[i] ? exp((double)lg[i] / a.T - M) / S : 0.0;
+      p[tid * SW_PER + i] = pv;
+      r[tid * SW_PER + i] = pv;
+    }
+    __syncthreads();
     Z = 1.0;
     int accepted = -1;
-    for (int c = u + 1; c < N; ++c) {
-      if (parents[c] != u) continue;
-      const int x = tokens[c];
-      const double U = philox_uniform(seed, 0, (uint64_t)c);
-      const double rx = r[x];
-      bool acc;
-      if (det) {
-        acc = Z > 0.0 && U < rx / Z;
-      } else {
-        const double qx = qq[x];
-        acc = (qx == 0.0) ? (rx > 0.0) : (U < (rx / Z) / (qx / Zq));
+    // ---- the children of u, in index order
+    for (int c = sw_next_child(par_l, a.N, u, u, shmin); c < a.N; c = sw_next_child(par_l, a.N, u, c, shmin)) {
+      const int x = a.tokens[c];
+      const int owner = x / SW_SLICE, xl = x - owner * SW_SLICE;
+      // this slice's residual as it would be after rejecting x
+      double zl = 0.0, zql = 0.0;
+#pragma unroll
+      for (int i = 0; i < SW_PER; ++i) {
+        const int l = tid * SW_PER + i, v = b0 + i;
+        double t;
+        if (det) t = v == x ? 0.0 : r[l];
+        else {
+          const double dd = r[l] / Z - q[l] / Zq;
+          t = dd > 0.0 ? dd : 0.0;
+        }
+        zl += t;
+        zql += v == x ? 0.0 : q[l];
       }
-      if (acc) {
+      sw_sum2(zl, zql, red);
+      const int par = st.k & 1;
+      if (tid == 0) {
+        double acc = 0.0;
+        if (g == owner) {
+          const double U = philox_uniform(a.seed, 0, (uint64_t)c);
+          const double rx = r[xl];
+          bool yes;
+          if (det) {
+            yes = Z > 0.0 && U < rx / Z;
+          } else {
+            const double qx = q[xl];
+            yes = (qx == 0.0) ? (rx > 0.0) : (U < (rx / Z) / (qx / Zq));
+          }
+          acc = yes ? 1.0 : 0.0;
+        }
+        double* rc = sw_rec(st, par, g);
+        sw_st(st, rc, zl);
+        sw_st(st, rc + 1, zql);
+        sw_st(st, rc + 2, acc);
+      }
+      ok = sw_round(a, st, g, shi + 1);
+      if (!ok) break;
+      sw_gather(st, par, G, gb);
+      double zs = 0.0, zqs = 0.0;
+      for (int gg = 0; gg < G; ++gg) {
+        zs += gb[gg][0];
+        zqs += gb[gg][1];
+      }
+      const bool yes = gb[owner][2] != 0.0;
+      __syncthreads();  // (gb is rewritten by the next round's gather)
+      if (yes) {
         accepted = c;
         break;
       }
-      __syncthreads();  // everyone has read r[x], qq[x]
-      double nz = 0.0;
-      if (det) {
-        // the rejected candidate's token leaves the residual
-        if (tid == 0) r[x] = 0.0;
-        __syncthreads();
-        for (int v = v0; v < v1; ++v) nz += r[v];
-        Z = block_sum_chunks(nz, red);
-        continue;
+      // rejected: apply the residual every workgroup summed
+#pragma unroll
+      for (int i = 0; i < SW_PER; ++i) {
+        const int l = tid * SW_PER + i, v = b0 + i;
+        if (det) {
+          if (v == x) r[l] = 0.0;
+        } else {
+          const double dd = r[l] / Z - q[l] / Zq;
+          r[l] = dd > 0.0 ? dd : 0.0;
+          if (wor && v == x) q[l] = 0.0;
+        }
       }
-      for (int v = v0; v < v1; ++v) {
-        const double t = r[v] / Z - qq[v] / Zq;
-        r[v] = t > 0.0 ? t : 0.0;
-        nz += r[v];
-      }
-      Z = block_sum_chunks(nz, red);
-      if (wor) {
-        if (tid == 0) qq[x] = 0.0;
-        __syncthreads();
-        double s2 = 0.0;
-        for (int v = v0; v < v1; ++v) s2 += qq[v];
-        Zq = block_sum_chunks(s2, red);
-      }
+      Z = zs;
+      if (wor) Zq = zqs;
+      __syncthreads();
     }
-    if (accepted < 0) break;
-    if (tid == 0) path[len] = accepted;
+    if (!ok || accepted < 0) break;
+    if (g == 0 && tid == 0) a.path[len] = accepted;
     ++len;
     u = accepted;
     __syncthreads();
   }
-  // extra token: smallest v whose running sum exceeds U * Z
-  const double U2 = philox_uniform(seed, 1, (uint64_t)u);
-  const bool use_r = Z > 0.0;
-  const double* w = use_r ? r : p;
-  const double target = U2 * (use_r ? Z : 1.0);
-  double cs = 0.0;
-  int lastpos = -1;
-  for (int v = v0; v < v1; ++v) {
-    cs += w[v];
-    if (w[v] > 0.0) lastpos = v;
-  }
-  red[tid] = cs;
-  scan[tid] = lastpos;
-  __syncthreads();
-  if (tid == 0) {
-    double run = 0.0;
-    int choice = -1;
-    for (int t = 0; t < SA_THREADS && choice < 0; ++t) {
-      if (run + red[t] > target) {
-        const int a = min(V, t * C), b = min(V, a + C);
-        double c2 = run;
-        for (int v = a; v < b; ++v) {
-          c2 += w[v];
-          if (c2 > target) {
-            choice = v;
-            break;
-          }
-        }
-      }
-      run += red[t];
+  if (ok) {
+    // ---- extra token: the smallest v whose running sum of w exceeds U2 * Z
+    // (w = r, or p when rounding left no residual mass), summed per thread in
+    // index order, per slice over threads in order, then over slices in order
+    const double U2 = philox_uniform(a.seed, 1, (uint64_t)u);
+    const bool use_r = Z > 0.0;
+    const double* w = use_r ? r : p;
+    const double target = U2 * (use_r ? Z : 1.0);
+    double c1 = 0.0;
+    int lastpos = -1;
+#pragma unroll
+    for (int i = 0; i < SW_PER; ++i) {
+      const double wv = w[tid * SW_PER + i];
+      c1 += wv;
+      if (wv > 0.0) lastpos = b0 + i;
     }
-    if (choice < 0) {
-      // rounding left no crossing: the last token with positive weight
-      choice = 0;
-      for (int t = SA_THREADS - 1; t >= 0; --t)
-        if (scan[t] >= 0) {
-          choice = scan[t];
+    cs[tid] = c1;
+    const int lp = (int)sw_max((double)lastpos, red);
+    const int par = st.k & 1;
+    if (tid == 0) {
+      double Wg = 0.0;
+      for (int t = 0; t < SW_THREADS; ++t) Wg += cs[t];
+      double* rc = sw_rec(st, par, g);
+      sw_st(st, rc, Wg);
+      sw_st(st, rc + 1, (double)lp);
+    }
+    ok = sw_round(a, st, g, shi + 1);
+    if (ok) sw_gather(st, par, G, gb);
+    if (ok && tid == 0) {
+      // the slice where the running sum crosses the target
+      double run = 0.0;
+      int gx = -1;
+      for (int gg = 0; gg < G; ++gg) {
+        if (run + gb[gg][0] > target) {
+          gx = gg;
           break;
         }
+        run += gb[gg][0];
+      }
+      int choice = -1;
+      if (gx == g) {
+        // in it, the thread chunk, then the entry
+        double c2 = run;
+        for (int t = 0; t < SW_THREADS && choice < 0; ++t) {
+          if (c2 + cs[t] > target) {
+            double c3 = c2;
+            for (int i = 0; i < SW_PER; ++i) {
+              c3 += w[t * SW_PER + i];
+              if (c3 > target) {
+                choice = g * SW_SLICE + t * SW_PER + i;
+                break;
+              }
+            }
+          }
+          c2 += cs[t];
+        }
+        if (choice < 0) choice = lp >= 0 ? lp : g * SW_SLICE;  // rounding left no crossing in the slice
+      } else if (gx < 0 && g == 0) {
+        // rounding left no crossing: the last token with positive weight
+        choice = 0;
+        for (int gg = G - 1; gg >= 0; --gg)
+          if (gb[gg][1] >= 0.0) {
+            choice = (int)gb[gg][1];
+            break;
+          }
+      }
+      if (choice >= 0) *a.next = choice;
+      if (g == 0) *a.path_len = len;
     }
-    *path_len = len;
-    *next = choice;
+  }
+  // the last workgroup out raises the epoch (and clears an abort)
+  __syncthreads();
+  if (tid == 0) {
+    if (!ok && g == 0) *a.path_len = 0;
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    const unsigned prev = __hip_atomic_fetch_add(st.ctl + SWC_DONE, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (prev == (unsigned)G - 1) {
+      __hip_atomic_store(st.ctl + SWC_DONE, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(st.ctl + SWC_ABORT, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(st.ctl + SWC_EPOCH, (st.tagbase >> 16), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
   }
 }
 
+static_assert(kSwBytes == kSampleWorkBytes, "the exchange area's size is declared in ssd_internal.h");
+size_t sample_work_bytes() { return kSwBytes; }
+
 hipError_t launch_sample_accept(const int* tokens, const int* parents, int N, int V, const float* logits,
-                                const float* draft, double temperature, uint64_t seed, int mode, int topk, double* r,
-                                double* p, double* qq, int* path, int* path_len, int* next, hipStream_t s) {
+                                const float* draft, double temperature, uint64_t seed, int mode, int topk, void* work,
+                                unsigned* err, int* path, int* path_len, int* next, hipStream_t s) {
   if (mode < 1 || mode > 3 || (mode == 3) != (draft == nullptr)) return hipErrorInvalidValue;
-  sample_accept_kernel<<<1, SA_THREADS, 0, s>>>(tokens, parents, N, V, logits, draft, temperature, seed, mode, topk,
-                                                r, p, qq, path, path_len, next);
+  const int G = (V + SW_SLICE - 1) / SW_SLICE;
+  if (V <= 0 || G > SW_MAXG || N <= 0 || N > SW_MAXN || !work) return hipErrorInvalidValue;
+  SwArgs a{tokens, parents, N, V, G, logits, draft, temperature, seed, mode, topk, path, path_len, next,
+           (unsigned char*)work, err, 50000000ull /* 0.5 s at 100 MHz */};
+  sample_accept_kernel<<<8 * G, SW_THREADS, 0, s>>>(a);
   return hipGetLastError();
 }
 

@@ -107,7 +107,7 @@ struct ssd_kv {
   int* d_accept_tree = nullptr;  // tokens[N] parents[N] depth[N] for accept
   int* d_argmax = nullptr;
   void* d_amwork = nullptr;  // argmax / top-k partials
-  double *d_r = nullptr, *d_p = nullptr, *d_qq = nullptr;
+  void* d_sw = nullptr;   // the sampling walk's exchange area (sample_work_bytes, zeroed at creation)
   unsigned* d_err = nullptr;
   // pinned staging ring
   char* pinned = nullptr;
@@ -505,7 +505,7 @@ extern "C" ssd_status ssd_kv_create(const ssd_model* m, int32_t max_ctx, int32_t
   const size_t o_tree = take(stage_bytes(max_nodes));
   const size_t o_at = take((size_t)3 * max_nodes * 4), o_am = take((size_t)max_nodes * 4);
   const size_t o_amw = take(std::max(argmax_work_bytes(max_nodes, V), topk_work_bytes(max_nodes, V)));
-  const size_t o_r = take((size_t)V * 8), o_p = take((size_t)V * 8), o_qq = take((size_t)V * 8);
+  const size_t o_sw = take(sample_work_bytes());
   const size_t o_err = take(256);
   const size_t o_sig = take(256);  // signal counter, XCD of block 0, sink
   hipError_t e = hipMalloc(&kv->ws, off);
@@ -527,9 +527,7 @@ extern "C" ssd_status ssd_kv_create(const ssd_model* m, int32_t max_ctx, int32_t
   kv->d_accept_tree = (int*)(b + o_at);
   kv->d_argmax = (int*)(b + o_am);
   kv->d_amwork = b + o_amw;
-  kv->d_r = (double*)(b + o_r);
-  kv->d_p = (double*)(b + o_p);
-  kv->d_qq = (double*)(b + o_qq);
+  kv->d_sw = b + o_sw;
   kv->d_err = (unsigned*)(b + o_err);
   kv->d_sig = (unsigned long long*)(b + o_sig);
   kv->d_xcc0 = (unsigned*)(b + o_sig + 8);
@@ -1093,6 +1091,8 @@ static ssd_status check_accept_mode(const ssd_tree* tree, const float* draft_pro
   if (mode != SSD_ACCEPT_GREEDY && !(tree->temperature > 0.f))
     return fail(SSD_E_INVALID_ARG, "temperature must be positive");
   if (tree->top_k < 0) return fail(SSD_E_INVALID_ARG, "top_k must be >= 0");
+  if (mode != SSD_ACCEPT_GREEDY && tree->vocab > kSampleMaxVocab)
+    return fail(SSD_E_CAPACITY, "vocab above 131072 (the sampling walk's limit)");
   return SSD_OK;
 }
 
@@ -1131,7 +1131,7 @@ extern "C" ssd_status ssd_tree_accept(ssd_kv* kv, const ssd_tree* tree, const fl
     HIP_TRY(launch_greedy_walk(dt, dt + n, dt + 2 * n, n, kv->d_argmax, accepted_path, path_len, next_token, s));
   } else {
     HIP_TRY(launch_sample_accept(dt, dt + n, n, V, oracle_logits, draft_probs, (double)tree->temperature, rng_seed,
-                                 (int)tree->mode, tree->top_k, kv->d_r, kv->d_p, kv->d_qq, accepted_path, path_len,
+                                 (int)tree->mode, tree->top_k, kv->d_sw, kv->d_err, accepted_path, path_len,
                                  next_token, s));
   }
   return release_slot(kv, slot, s);
@@ -1143,8 +1143,10 @@ extern "C" ssd_status ssd_tree_accept(ssd_kv* kv, const ssd_tree* tree, const fl
 // capture, tight serving loops, harnesses that forbid hipMalloc): the accept
 // walk with its scratch in one file-scope device array instead of a
 // session's workspace.  The array holds the staged tree, the argmax partials
-// and results, and the sampling walk's three float64 vocabulary rows; every
-// kernel writes what it later reads, so nothing needs clearing between calls.
+// and results, and the sampling walk's exchange area.  The argmax kernels
+// write what they later read; the exchange area starts zeroed (as the array
+// does when the module loads) and the sampler keeps it consistent itself
+// (an epoch raised by every call), so nothing needs clearing between calls.
 // Each device gets its own copy of the array at its own address, fetched once
 // per device with hipGetSymbolAddress; every call on a device shares it, so
 // calls that overlap on one device (two streams, or two host threads) race.
@@ -1154,8 +1156,8 @@ constexpr size_t kNaTreeOfs = 0;                                  // tokens, par
 constexpr size_t kNaArgOfs = 4096;                                // argmax results: int32[kNaMaxNodes]
 constexpr size_t kNaWorkOfs = 8192;                               // argmax partials
 constexpr size_t kNaWorkBytes = (size_t)kNaMaxNodes * ((kNaMaxVocab + 2047) / 2048) * 8;
-constexpr size_t kNaRowsOfs = kNaWorkOfs + kNaWorkBytes;          // r, p, qq: float64[3][kNaMaxVocab]
-constexpr size_t kNaScratchBytes = kNaRowsOfs + (size_t)3 * kNaMaxVocab * 8;
+constexpr size_t kNaSwOfs = kNaWorkOfs + kNaWorkBytes;            // the sampling walk's exchange area
+constexpr size_t kNaScratchBytes = kNaSwOfs + kSampleWorkBytes;
 static_assert(kNaScratchBytes <= (2u << 20), "the no-allocation scratch is at most 2 MiB per device");
 static __device__ __align__(256) unsigned char scratch[kNaScratchBytes];
 
@@ -1235,10 +1237,9 @@ extern "C" ssd_status ssd_tree_accept_noalloc(const ssd_tree* tree, const float*
     HIP_TRY(launch_greedy_walk(dt, dt + kNaMaxNodes, dt + 2 * kNaMaxNodes, n, g, accepted_path, path_len, next_token,
                                s));
   } else {
-    double* rows = (double*)(base + kNaRowsOfs);
     HIP_TRY(launch_sample_accept(dt, dt + kNaMaxNodes, n, V, oracle_logits, draft_probs, (double)tree->temperature,
-                                 rng_seed, (int)tree->mode, tree->top_k, rows, rows + kNaMaxVocab,
-                                 rows + 2 * kNaMaxVocab, accepted_path, path_len, next_token, s));
+                                 rng_seed, (int)tree->mode, tree->top_k, base + kNaSwOfs, nullptr, accepted_path,
+                                 path_len, next_token, s));
   }
   return SSD_OK;
 }

@@ -150,6 +150,9 @@ hipError_t launch_gemm_f32(int kind, const float* W, int M, int K, const float* 
 GemmCfg gemm_cfg(int N, int vec, int kind);
 // k-steps per split and number of splits (EPI_PARTIAL only; 1 otherwise)
 int gemm_split_kc(int M, int K, int N, int vec, int want_split, int* splits);
+// whether a matrix-core GEMM over N nodes (of one launch) takes the
+// wide-tree kernel (row blocks x node tiles per workgroup)
+bool gemm_wide(int vec, int N);
 GemmGeom gemm_geom(int kind, int vec, int M, int K, int N, int kcs);
 // Wp: weights packed in 16x32 float16 fragments (see pack); act: activations
 // of this launch's first node in fragment order (see st_act); kcs k-steps per
@@ -178,9 +181,16 @@ hipError_t launch_greedy_walk(const int* tokens, const int* parents, const int* 
                               int* path, int* path_len, int* next, hipStream_t s);
 // mode: 1 without replacement, 2 independent, 3 chosen (draft == nullptr);
 // topk > 0 restricts the targets to each row's topk largest logits
+// rejection sampling down the tree on ceil(V / 2048) workgroups that trade
+// slice sums through work (sample_work_bytes(), zeroed once before the first
+// use and then owned by the sampler: one call at a time per work area); on a
+// wait that times out *path_len = 0 and err (if given) counts it
+constexpr size_t kSampleWorkBytes = (64 + 64) * 4 + (size_t)2 * 64 * 4 * 8 + (size_t)2 * 64 * 256 * 4;
+constexpr int kSampleMaxVocab = 64 * 2048;  // the sampling walk's vocabulary limit
+size_t sample_work_bytes();
 hipError_t launch_sample_accept(const int* tokens, const int* parents, int N, int V, const float* logits,
-                                const float* draft, double temperature, uint64_t seed, int mode, int topk, double* r,
-                                double* p, double* qq, int* path, int* path_len, int* next, hipStream_t s);
+                                const float* draft, double temperature, uint64_t seed, int mode, int topk, void* work,
+                                unsigned* err, int* path, int* path_len, int* next, hipStream_t s);
 hipError_t launch_commit(int f32, void* kc, void* vc, const void* kt, const void* vt, int LH, int max_ctx,
                          int max_nodes, int DH, int P, const int* path, const int* path_len, unsigned* err,
                          hipStream_t s);
