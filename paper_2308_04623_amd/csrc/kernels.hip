@@ -500,12 +500,12 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(NW / 4,
 // (q / (gt gy)), node-tile group j, k-split sk); groups past gx exit.
 constexpr int kG2TT = 4;  // node tiles per workgroup
 
-template <int RBT, int KIND, int U>
-__global__ __launch_bounds__(256) void gemm2d_kernel(const u32x4* __restrict__ Wp, int KC, int RBtot, int NT,
-                                                     int kcs, int gx, int gt, int gy,
-                                                     const uint16_t* __restrict__ act, Epi ep) {
+template <int RBT, int KIND, int U, int NW>
+__global__ __launch_bounds__(64 * NW) void gemm2d_kernel(const u32x4* __restrict__ Wp, int KC, int RBtot, int NT,
+                                                         int kcs, int gx, int gt, int gy,
+                                                         const uint16_t* __restrict__ act, Epi ep) {
   constexpr int TT = kG2TT;
-  __shared__ float red[4 * TT * 16 * 16];
+  __shared__ float red[NW * TT * 16 * 16];
   pass_signal(ep.sig);
   const int b = blockIdx.x, x = b & 7, q = b >> 3, per = gt * gy;
   const int i = x + 8 * (q / per), rem = q % per;
@@ -514,7 +514,7 @@ __global__ __launch_bounds__(256) void gemm2d_kernel(const u32x4* __restrict__ W
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
   const int rb0 = i * RBT, t0 = j * TT;
   const int kc0 = sk * kcs, kc1 = min(KC, kc0 + kcs);
-  const int nsteps = kc1 - kc0 > w ? (kc1 - kc0 - w + 3) / 4 : 0;
+  const int nsteps = kc1 - kc0 > w ? (kc1 - kc0 - w + NW - 1) / NW : 0;
   // row blocks past the matrix and node tiles past the tree read the last
   // one instead and are never stored
   const u32x4* wb[RBT];
@@ -526,7 +526,7 @@ __global__ __launch_bounds__(256) void gemm2d_kernel(const u32x4* __restrict__ W
   u32x4 wq[U][RBT], bq[U][TT];
   const int klast = kc1 - 1;
   auto load_step = [&](int s, int u) {
-    const int kc = min(kc0 + w + 4 * s, klast);
+    const int kc = min(kc0 + w + NW * s, klast);
 #pragma unroll
     for (int r = 0; r < RBT; ++r) wq[u][r] = wb[r][(size_t)kc * 64];
 #pragma unroll
@@ -573,11 +573,11 @@ __global__ __launch_bounds__(256) void gemm2d_kernel(const u32x4* __restrict__ W
       for (int c = 0; c < 4; ++c)
         red[((w * TT + t) * 16 + (lane & 15)) * 16 + 4 * (lane >> 4) + c] = acc[r][t][c];
     __syncthreads();
-    for (int idx = tid; idx < TT * 256; idx += 256) {
+    for (int idx = tid; idx < TT * 256; idx += 64 * NW) {
       const int row = idx & 15, node = t0 * 16 + (idx >> 4);
       float sum = red[idx];
 #pragma unroll
-      for (int ww = 1; ww < 4; ++ww) sum += red[ww * TT * 256 + idx];
+      for (int ww = 1; ww < NW; ++ww) sum += red[ww * TT * 256 + idx];
       const int o = (rb0 + r) * 16 + row;
       if (o < ep.M && node < ep.N) epilogue<uint16_t, KIND>(e2, node, o, sum);
     }
@@ -695,18 +695,22 @@ static void gemm_go(int kind, const GemmGeom& g, const void* Wp, const uint16_t*
   }
 }
 
-template <int RBT, int U>
+template <int RBT, int U, int NW>
 static void gemm2d_go(int kind, const u32x4* Wp, int KC, int RBtot, int NT, int kcs, int gx, int gt, int gy,
                       const uint16_t* act, const Epi& ep, hipStream_t s) {
   const dim3 grid(8 * ((gx + 7) / 8) * gt * gy);
   switch (kind) {
-    case EPI_QKV: gemm2d_kernel<RBT, EPI_QKV, U><<<grid, 256, 0, s>>>(Wp, KC, RBtot, NT, kcs, gx, gt, gy, act, ep); break;
-    case EPI_PARTIAL:
-      gemm2d_kernel<RBT, EPI_PARTIAL, U><<<grid, 256, 0, s>>>(Wp, KC, RBtot, NT, kcs, gx, gt, gy, act, ep);
+    case EPI_QKV:
+      gemm2d_kernel<RBT, EPI_QKV, U, NW><<<grid, 64 * NW, 0, s>>>(Wp, KC, RBtot, NT, kcs, gx, gt, gy, act, ep);
       break;
-    case EPI_GELU: gemm2d_kernel<RBT, EPI_GELU, U><<<grid, 256, 0, s>>>(Wp, KC, RBtot, NT, kcs, gx, gt, gy, act, ep); break;
+    case EPI_PARTIAL:
+      gemm2d_kernel<RBT, EPI_PARTIAL, U, NW><<<grid, 64 * NW, 0, s>>>(Wp, KC, RBtot, NT, kcs, gx, gt, gy, act, ep);
+      break;
+    case EPI_GELU:
+      gemm2d_kernel<RBT, EPI_GELU, U, NW><<<grid, 64 * NW, 0, s>>>(Wp, KC, RBtot, NT, kcs, gx, gt, gy, act, ep);
+      break;
     default:
-      gemm2d_kernel<RBT, EPI_LOGITS, U><<<grid, 256, 0, s>>>(Wp, KC, RBtot, NT, kcs, gx, gt, gy, act, ep);
+      gemm2d_kernel<RBT, EPI_LOGITS, U, NW><<<grid, 64 * NW, 0, s>>>(Wp, KC, RBtot, NT, kcs, gx, gt, gy, act, ep);
       break;
   }
 }
@@ -719,10 +723,10 @@ static hipError_t launch_gemm_wide(int kind, const void* Wp, int M, int K, const
   if (kind != EPI_PARTIAL && gy != 1) return hipErrorInvalidValue;
   const u32x4* W = (const u32x4*)Wp;
   switch (rbt) {
-    case 1: gemm2d_go<1, 2>(kind, W, KC, RBtot, NT, kcs, gx, gt, gy, act, ep, s); break;
-    case 2: gemm2d_go<2, 2>(kind, W, KC, RBtot, NT, kcs, gx, gt, gy, act, ep, s); break;
-    case 4: gemm2d_go<4, 2>(kind, W, KC, RBtot, NT, kcs, gx, gt, gy, act, ep, s); break;
-    default: gemm2d_go<8, 1>(kind, W, KC, RBtot, NT, kcs, gx, gt, gy, act, ep, s); break;
+    case 1: gemm2d_go<1, 2, 4>(kind, W, KC, RBtot, NT, kcs, gx, gt, gy, act, ep, s); break;
+    case 2: gemm2d_go<2, 2, 4>(kind, W, KC, RBtot, NT, kcs, gx, gt, gy, act, ep, s); break;
+    case 4: gemm2d_go<4, 2, 4>(kind, W, KC, RBtot, NT, kcs, gx, gt, gy, act, ep, s); break;
+    default: gemm2d_go<8, 1, 4>(kind, W, KC, RBtot, NT, kcs, gx, gt, gy, act, ep, s); break;
   }
   return hipGetLastError();
 }
