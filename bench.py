@@ -167,6 +167,42 @@ def stored_traffic(fused, n):
     return None
 
 
+def write_mfma(counter_dir, trace_dir, n, P, cmd_pmc, cmd_trace):
+    """Matrix-core use of the weight GEMMs from a rocprofv3 --pmc run
+    (MfmaUtil, MfmaFlopsF16 per dispatch) and a --kernel-trace --stats run of
+    the same command (average durations): profiles/mfma_gemm_n{n}_p{P}.md."""
+    import csv
+    import glob
+    rows = _counter_rows(counter_dir)
+    util = _per_kernel(rows, "MfmaUtil")
+    flops = _per_kernel(rows, "MfmaFlopsF16")
+    avg = {}
+    for f in glob.glob(os.path.join(trace_dir, "**", "*kernel_stats.csv"), recursive=True):
+        for r in csv.DictReader(open(f, newline="")):
+            avg[r["Name"]] = float(r["AverageNs"]) * 1e-3
+    lines = [f"# Matrix-core use of the weight GEMMs: GPT-2-L shape, {n} nodes, {P}-token prefix", "",
+             "Commands (repo root, one MI355X; `TMPDIR=/tmp`):", "", f"    {cmd_pmc}", f"    {cmd_trace}",
+             f"    python bench.py --mfma-from {counter_dir} {trace_dir} --nodes {n} --prefix {P}", "",
+             "MfmaUtil = matrix-core busy cycles / (GPU active cycles x 1024 SIMDs); FLOPs are rocprofv3's "
+             "MfmaFlopsF16 (512 per MOPS count). TFLOP/s = FLOPs per dispatch / the kernel's average duration "
+             "in the trace run; the dense float16 peak is 2500 TFLOP/s.", "",
+             "| kernel | dispatches | MfmaUtil % | GFLOP per dispatch | avg us | TFLOP/s | of peak |",
+             "|---|---|---|---|---|---|---|"]
+    for (name, grid), us in sorted(util.items(), key=lambda kv: -sum(kv[1])):
+        fl = flops.get((name, grid), [0.0])
+        f_avg = sum(fl) / len(fl)
+        t = next((v for k, v in avg.items() if k.split("(")[0] == name.split("(")[0]), None)
+        tf = f_avg / (t * 1e-6) / 1e12 if t else None
+        short = name.split("(")[0]
+        lines.append(f"| `{short}` (grid {grid}) | {len(us)} | {sum(us) / len(us):.2f} | {f_avg / 1e9:.3f} | "
+                     f"{t if t is None else round(t, 2)} | {'' if tf is None else round(tf, 1)} | "
+                     f"{'' if tf is None else f'{tf / 2500 * 100:.2f}%'} |")
+    text = "\n".join(lines) + "\n"
+    with open(os.path.join(ROOT, "profiles", f"mfma_gemm_n{n}_p{P}.md"), "w") as fh:
+        fh.write(text)
+    print(text)
+
+
 def fc_gemm_roofline(sess, cfg, N, stream):
     """Dominant kernel of the one-kernel-per-sub-layer path: the MLP
     up-projection GEMM (13.1 MB of weights per launch), launched on its own
@@ -354,9 +390,21 @@ def main():
     ap.add_argument("--stage-trace", action="store_true",
                     help="time the pass, record one traced persistent pass and write "
                          "profiles/stage_trace_n{nodes}_p{prefix}.md")
+    ap.add_argument("--mfma-probe", action="store_true",
+                    help="only run three eager verification passes (for rocprofv3 --pmc MfmaUtil MfmaFlopsF16)")
+    ap.add_argument("--mfma-from", nargs=2, metavar=("COUNTER_DIR", "TRACE_DIR"),
+                    help="summarise a rocprofv3 --pmc MfmaUtil MfmaFlopsF16 run and a --kernel-trace --stats -f csv "
+                         "run of the same command into profiles/mfma_gemm_n{nodes}_p{prefix}.md; no GPU needed")
     ap.add_argument("--kernels-path", action="store_true",
                     help="with --traffic-from: the counters are of the one-kernel-per-sub-layer path's GEMM")
     args = ap.parse_args()
+    if args.mfma_from:
+        base = f"python -u bench.py --nodes {args.nodes} --prefix {args.prefix} --mfma-probe"
+        write_mfma(args.mfma_from[0], args.mfma_from[1], args.nodes, args.prefix,
+                   f"rocprofv3 --pmc MfmaUtil MfmaFlopsF16 --kernel-include-regex gemm -f csv -d {args.mfma_from[0]} "
+                   f"-o pmc -- {base}",
+                   f"rocprofv3 --kernel-trace --stats -f csv -d {args.mfma_from[1]} -o trace -- {base}")
+        return
     if args.traffic_from:
         write_traffic(args.traffic_from[0], args.traffic_from[1], args.nodes, not args.kernels_path)
         return
@@ -391,6 +439,13 @@ def main():
     fused = sess.verify_path(N) == ssd.PASS_FUSED
     if args.traffic_probe:
         probe_traffic(sess, cfg, N, P, toks, par, fused)
+        return
+    if args.mfma_probe:
+        # a few eager passes (no graph replays) for the matrix-core counters
+        for _ in range(3):
+            sess.verify(P, toks, par)
+        torch.cuda.synchronize()
+        log("mfma probe done")
         return
     if args.stage_trace:
         if not fused:

@@ -795,7 +795,7 @@ template <int NT, int RB, int U>
 __device__ __forceinline__ bool gemm_rb(const FusedArgs& a, const Wg& w, const WaitSpec& ws, int epi, int l,
                                         const int* rbs, int rb_first, int nrb, gptr<uint16_t> bias, gptr<u32x4> Wp,
                                         int KC, int M, int kc0, int kc1, const uint16_t* act, int act_kc,
-                                        float* red, const PreSpec& ps, int wofs, HeadBest* hb) {
+                                        float* red, const PreSpec& ps, int wofs, HeadBest& hb, bool track) {
   constexpr int NN = 16 * NT, NCW = NWV - QW;
   // Waves 4..7 compute: wave 4 + c takes k-steps kc0 + c, kc0 + c + 4, ...,
   // and loads their weights first thing.  Waves 0..3 run the pre-stage
@@ -928,9 +928,9 @@ __device__ __forceinline__ bool gemm_rb(const FusedArgs& a, const Wg& w, const W
       if (node < N && o < M) {
         const float y = has_bias ? sum + bf2f(bias_r[r]) : sum;
         epilogue(a, w, epi, l, node, o, y);
-        if (hb && (y > hb->v[i] || (y == hb->v[i] && o < hb->o[i]))) {
-          hb->v[i] = y;
-          hb->o[i] = o;
+        if (track && (y > hb.v[i] || (y == hb.v[i] && o < hb.o[i]))) {
+          hb.v[i] = y;
+          hb.o[i] = o;
         }
       }
     }
@@ -960,17 +960,17 @@ template <int NT>
 __device__ __forceinline__ bool gemm_task(const FusedArgs& a, const Wg& w, const WaitSpec& ws, int epi, int l,
                                           const int* rbs, int rb_first, int nrb, gptr<uint16_t> bias,
                                           gptr<u32x4> Wp, int KC, int M, int kc0, int kc1, const uint16_t* act,
-                                          int act_kc, float* red, const PreSpec& ps, int wofs = 0,
-                                          HeadBest* hb = nullptr) {
+                                          int act_kc, float* red, const PreSpec& ps, int wofs,
+                                          HeadBest& hb, bool track) {
   if (nrb <= 0) return pre_only(a, w, ps);
   if (nrb == 1)
     return gemm_rb<NT, 1, NT <= 2 ? 10 : 8>(a, w, ws, epi, l, rbs, rb_first, 1, bias, Wp, KC, M, kc0, kc1, act,
-                                           act_kc, red, ps, wofs, hb);
+                                           act_kc, red, ps, wofs, hb, track);
   if (nrb == 2)
     return gemm_rb<NT, 2, NT <= 2 ? 10 : 6>(a, w, ws, epi, l, rbs, rb_first, 2, bias, Wp, KC, M, kc0, kc1, act,
-                                           act_kc, red, ps, wofs, hb);
+                                           act_kc, red, ps, wofs, hb, track);
   return gemm_rb<NT, 4, NT == 1 ? 8 : NT == 2 ? 5 : 3>(a, w, ws, epi, l, rbs, rb_first, nrb, bias, Wp, KC, M, kc0, kc1, act,
-                                         act_kc, red, ps, wofs, hb);
+                                         act_kc, red, ps, wofs, hb, track);
 }
 
 // ------------------------------------------------------------------ tree attention
@@ -1407,10 +1407,10 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
       PreSpec nopre{};
       const bool ok = wo ? gemm_task<NT>(a, w, ws, FE_WO, l, p + PL_WO + 1, 0, n_wo, G<uint16_t>(nullptr),
                                          G<u32x4>(lw(w, l, LW_O)), KCd, d, kh0, kh1, a.fo, KCd, red, nopre,
-                                         wo_staged ? wo_ofs : 0)
+                                         wo_staged ? wo_ofs : 0, hbest, false)
                          : gemm_task<NT>(a, w, ws, FE_WPR, l, p + PL_WPR + 1, 0, n_wpr, G<uint16_t>(nullptr),
                                          G<u32x4>(lw(w, l, LW_PR)), KCm, d, kf0, kf1, a.ff, KCm, red, nopre,
-                                         wpr_staged ? WST : 0);
+                                         wpr_staged ? WST : 0, hbest, false);
       if (!ok) goto out;
       signal(a, w, l, fid, true);
       stamp(a, w, l, fid, 2);
@@ -1480,7 +1480,7 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
       // clears the first two sum buffers: see xs_zero)
       const WaitSpec gws{ps.fid, (kind == 0 && l == 0) ? -1 : w.x, tag_of(w, l, ps.fid), true, l, gfid};
       if (!gemm_task<NT>(a, w, gws, epi, l, rbs, rb_first, nrb, bias, Wm, KCd, Mo, k0, k1, act, KCd, red, ps, 0,
-                         kind == 8 ? &hbest : nullptr))
+                         hbest, kind == 8))
         goto out;
     }
     if (kind == 8) {
@@ -1489,7 +1489,7 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
       PreSpec nopre{};
       for (int b0 = hb0 + 4, j = 1; b0 < hb1; b0 += 4, ++j) {
         if (!gemm_task<NT>(a, w, none, FE_HEAD, L, nullptr, b0, min(4, hb1 - b0), G<uint16_t>(nullptr),
-                           G<u32x4>(a.p_head), KCd, a.V, 0, KCd, act1, KCd, red, nopre, 0, &hbest))
+                           G<u32x4>(a.p_head), KCd, a.V, 0, KCd, act1, KCd, red, nopre, 0, hbest, true))
           goto out;
       }
       // this workgroup's maximum per node: the 16 slots of a node sit in 16

@@ -1624,48 +1624,105 @@ hipError_t launch_topk(const float* logits, int N, int V, int k, int* idx, float
 
 // one thread: matched = parent matched and token == parent's argmax; keep the
 // deepest matched node (lowest index among equals)
-__global__ void greedy_walk_kernel(const int* __restrict__ tokens, const int* __restrict__ parents,
-                                   const int* __restrict__ depth, int N, const int* __restrict__ g,
-                                   int* __restrict__ path, int* __restrict__ path_len, int* __restrict__ next) {
-  __shared__ unsigned char m[1024];
-  if (threadIdx.x != 0) return;
-  m[0] = 1;
+// The greedy walk over LDS copies of the tree (tok, par, dep) and the
+// per-node argmax gl, by the whole block: node i is kept iff every edge on
+// its root path has the child's token equal to its parent's argmax (pointer
+// jumping: after round r, keep[i] covers the 2^r edges above i); the deepest
+// kept node, the lowest index among equals, ends the path, and its argmax is
+// the extra token.
+__device__ void greedy_walk_lds(int N, const int* tok, const int* par, const int* dep, const int* gl, int* anc,
+                                unsigned char* keep, int* redv, int* path, int* path_len, int* next) {
+  const int tid = threadIdx.x, nt = blockDim.x;
+  for (int i = tid; i < N; i += nt) {
+    keep[i] = i == 0 || tok[i] == gl[par[i]];
+    anc[i] = i == 0 ? -1 : par[i];
+  }
+  __syncthreads();
+  for (int span = 1; span < N; span *= 2) {
+    // (reads of the round complete before any write: two passes per round)
+    unsigned char kv[4];
+    int av[4];
+    int c = 0;
+    for (int i = tid; i < N && c < 4; i += nt, ++c) {
+      const int a0 = anc[i];
+      kv[c] = keep[i] && (a0 < 0 || keep[a0]);
+      av[c] = a0 < 0 ? -1 : anc[a0];
+    }
+    __syncthreads();
+    c = 0;
+    for (int i = tid; i < N && c < 4; i += nt, ++c) {
+      keep[i] = kv[c];
+      anc[i] = av[c];
+    }
+    __syncthreads();
+  }
+  // deepest kept node, lowest index on ties: key = depth * 2^16 + (65535 - i)
   int best = 0;
-  for (int i = 1; i < N; ++i) {
-    const int p = parents[i];
-    m[i] = m[p] && tokens[i] == g[p];
-    if (m[i] && depth[i] > depth[best]) best = i;
+  for (int i = tid; i < N; i += nt)
+    if (keep[i]) best = max(best, (dep[i] << 16) | (65535 - i));
+  for (int o = 32; o > 0; o >>= 1) best = max(best, __shfl_xor(best, o));
+  if ((tid & 63) == 0) redv[tid >> 6] = best;
+  __syncthreads();
+  if (tid == 0) {
+    int b = 0;
+    for (int w = 0; w < nt / 64; ++w) b = max(b, redv[w]);
+    const int bi = 65535 - (b & 65535);
+    const int len = dep[bi] + 1;
+    int j = bi;
+    for (int t = len - 1; t >= 0; --t) {
+      path[t] = j;
+      j = par[j];
+    }
+    *path_len = len;
+    *next = gl[bi];
   }
-  const int len = depth[best] + 1;
-  int j = best;
-  for (int t = len - 1; t >= 0; --t) {
-    path[t] = j;
-    j = parents[j];
+}
+
+// greedy walk of up to 1024 nodes on the per-node argmax g (one block of
+// 256 threads: each thread walks at most 4 nodes per pass)
+__global__ __launch_bounds__(256) void greedy_walk_kernel(const int* __restrict__ tokens,
+                                                          const int* __restrict__ parents,
+                                                          const int* __restrict__ depth, int N,
+                                                          const int* __restrict__ g, int* __restrict__ path,
+                                                          int* __restrict__ path_len, int* __restrict__ next) {
+  __shared__ int tok[1024], par[1024], dep[1024], gl[1024], anc[1024], redv[4];
+  __shared__ unsigned char keep[1024];
+  for (int i = threadIdx.x; i < N; i += blockDim.x) {
+    tok[i] = tokens[i];
+    par[i] = parents[i];
+    dep[i] = depth[i];
+    gl[i] = g[i];
   }
-  *path_len = len;
-  *next = g[best];
+  __syncthreads();
+  greedy_walk_lds(N, tok, par, dep, gl, anc, keep, redv, path, path_len, next);
 }
 
 // Greedy accept from per-workgroup maxima (the persistent pass's LM head
 // leaves, for every node, each of G workgroups' largest logit and its token):
-// 16 threads per node reduce its G pairs (ties to the lower token), then one
-// thread walks the tree as greedy_walk_kernel does.
+// 16 threads per node reduce its G pairs (ties to the lower token), then the
+// block walks the tree as greedy_walk_kernel does.
 __global__ __launch_bounds__(1024) void greedy_from_parts_kernel(const unsigned* __restrict__ parts, int G, int N,
                                                                   const int* __restrict__ tokens,
                                                                   const int* __restrict__ parents,
                                                                   const int* __restrict__ depth,
                                                                   int* __restrict__ path, int* __restrict__ path_len,
                                                                   int* __restrict__ next) {
-  __shared__ int g[64];
-  __shared__ unsigned char m[64];
+  __shared__ int tok[64], par[64], dep[64], gl[64], anc[64], redv[16];
+  __shared__ unsigned char keep[64];
   const int tid = threadIdx.x, n = tid >> 4, j = tid & 15;
+  if (tid < N) {
+    tok[tid] = tokens[tid];
+    par[tid] = parents[tid];
+    dep[tid] = depth[tid];
+  }
   float v = -INFINITY;
   int o = 0x7fffffff;
   if (n < N) {
+    typedef unsigned u2v __attribute__((ext_vector_type(2)));
     for (int k = j; k < G; k += 16) {
-      const unsigned* pr = parts + ((size_t)n * G + k) * 2;
-      const float v2 = __uint_as_float(pr[0]);
-      const int o2 = (int)pr[1];
+      const u2v pr = *(const u2v*)(parts + ((size_t)n * G + k) * 2);
+      const float v2 = __uint_as_float(pr.x);
+      const int o2 = (int)pr.y;
       if (v2 > v || (v2 == v && o2 < o)) {
         v = v2;
         o = o2;
@@ -1681,24 +1738,9 @@ __global__ __launch_bounds__(1024) void greedy_from_parts_kernel(const unsigned*
       o = o2;
     }
   }
-  if (j == 0 && n < N) g[n] = o == 0x7fffffff ? 0 : o;  // (a row of NaN logits: token 0)
+  if (j == 0 && n < N) gl[n] = o == 0x7fffffff ? 0 : o;  // (a row of NaN logits: token 0)
   __syncthreads();
-  if (tid != 0) return;
-  m[0] = 1;
-  int best = 0;
-  for (int i = 1; i < N; ++i) {
-    const int p = parents[i];
-    m[i] = m[p] && tokens[i] == g[p];
-    if (m[i] && depth[i] > depth[best]) best = i;
-  }
-  const int len = depth[best] + 1;
-  int jj = best;
-  for (int t = len - 1; t >= 0; --t) {
-    path[t] = jj;
-    jj = parents[jj];
-  }
-  *path_len = len;
-  *next = g[best];
+  greedy_walk_lds(N, tok, par, dep, gl, anc, keep, redv, path, path_len, next);
 }
 
 hipError_t launch_greedy_from_parts(const unsigned* parts, int G, int N, const int* tokens, const int* parents,
@@ -1721,7 +1763,8 @@ hipError_t launch_argmax(const float* logits, int N, int V, int* g, void* work, 
 
 hipError_t launch_greedy_walk(const int* tokens, const int* parents, const int* depth, int N, const int* g,
                               int* path, int* path_len, int* next, hipStream_t s) {
-  greedy_walk_kernel<<<1, 64, 0, s>>>(tokens, parents, depth, N, g, path, path_len, next);
+  if (N < 1 || N > 1024) return hipErrorInvalidValue;
+  greedy_walk_kernel<<<1, 256, 0, s>>>(tokens, parents, depth, N, g, path, path_len, next);
   return hipGetLastError();
 }
 
