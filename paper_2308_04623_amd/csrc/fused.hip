@@ -33,7 +33,7 @@
 //    poll still waits behind the other waves' loads.  With two or more node
 //    tiles, waves 1..3 also copy into LDS the weights of a GEMM two stages
 //    on: the out-projection's during LN1 + QKV, and the down-projection's
-//    during the up-projection.
+//    during the up-projection (at four tiles already during LN2's wait).
 //  * Hand-offs are per-workgroup stage flags carrying a monotonically
 //    increasing tag (pass, layer, stage).  A workgroup writes its outputs,
 //    waits for its stores, then stores its flag; consumers poll the 32 flags
@@ -1364,6 +1364,7 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
   // LayerNorm) when they fit.  The up-projection's closing wait covers the
   // copy; with one tile that stage is too short to hide it.
   const bool wpr_staged = NT >= 2 && n_wpr > 0 && n_wpr * (kf1 - kf0) <= WST_FRAGS;
+  const bool wpr_early = wpr_staged && NT == 4;  // (see the out-projection stage)
   // likewise the out-projection's weights during LN1 + QKV, above the
   // parameter table (the attention stage between uses the LDS below it)
   const int wo_ofs = A_REGION + A_PART_BYTES + A_Q_BYTES + 256 + L * kLwSlots * 8;
@@ -1414,6 +1415,20 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
       if (!ok) goto out;
       signal(a, w, l, fid, true);
       stamp(a, w, l, fid, 2);
+      if (wo && wpr_early && threadIdx.x >= 64) {
+        // at four node tiles the down-projection's weights are copied into
+        // LDS from here (waves 1..7), inside the LayerNorm's cross-XCD wait,
+        // rather than after the LayerNorm's rows (measured: 3 % faster at
+        // 64 nodes, neutral or slower at 32)
+        const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63, nk = kf1 - kf0, tot = n_wpr * nk;
+        const gptr<u32x4> Wv = opq(G<u32x4>(lw(w, l, LW_PR))) + lane;
+        for (int f = wv - 1; f < tot; f += NWV - 1) {
+          const int r = f / nk, k = kf0 + f - r * nk;
+          const int rb = ((const __attribute__((address_space(3))) int*)(p + PL_WPR + 1))[r];
+          __builtin_amdgcn_global_load_lds((const void*)(Wv + ((size_t)rb * KCm + k) * 64),
+                                           (lds_void*)(lds + WST + (size_t)f * 1024), 16, 0, 0);
+        }
+      }
       continue;
     }
     // kind 0, 5, 8: waves 0..3 run this LayerNorm stage while waves 4..7
@@ -1425,7 +1440,7 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
     ps.fid = kind == 5 ? FS_LN2 : FS_LN1;
     ps.mode = (kind == 0 && l == 0) ? 0 : 1;
     if (kind == 5) {
-      if (wpr_staged) {
+      if (wpr_staged && !wpr_early) {
         ps.wn = n_wpr;
         ps.wk0 = kf0;
         ps.wk1 = kf1;
