@@ -1384,8 +1384,27 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
       // first: they are the first to be free)
       const int apos = p[PL_ATT];
       for (int u = apos; u < n_attu; u += kFRanks) {
-        const int hloc = u / (NTl * (S + 1)), rem = u - hloc * (NTl * (S + 1));
-        const int t = rem / (S + 1), part = rem - t * (S + 1);
+        // units in (head, tile, part) order; when they outnumber the ranks,
+        // the root units of every (head, tile) first, so that the ranks that
+        // take a second unit took a (shorter) root unit first (measured: 1.5 %
+        // faster at 64 nodes; at 16 and 32 nodes the plain order is faster)
+        int hloc, t, part;
+        if (n_attu <= kFRanks) {
+          hloc = u / (NTl * (S + 1));
+          const int rem = u - hloc * (NTl * (S + 1));
+          t = rem / (S + 1);
+          part = rem - t * (S + 1);
+        } else if (u < nhx * NTl) {
+          hloc = u / NTl;
+          t = u - hloc * NTl;
+          part = S;
+        } else {
+          const int v = u - nhx * NTl;
+          hloc = v / (NTl * S);
+          const int rem = v - hloc * (NTl * S);
+          t = rem / S;
+          part = rem - t * S;
+        }
         const int h = a.xh[2 * w.x] + hloc;
         const WaitSpec& wsu = u == apos ? ws : none;
         const bool ok = part < S ? att_prefix_unit(a, w, wsu, l, h, t, part, lds)

@@ -8,9 +8,10 @@ stage, the largest and smallest index each access can form (the same
 expressions as the kernel's, written out per access) on the real plan
 tables, and checks them against the sizes of the buffers the session
 allocates, for the small test model, the GPT-2-L shape and GPT-2-sized
-variants, N = 1..64 and prefixes 0, 64, 200, 512 and 1500.  A plan or layout
-change that lets any access leave its allocation fails here, on the CPU,
-before a kernel runs.
+variants, N = 1..64 and prefixes 0 to 5000; it also checks that the ranks of
+every XCD are dealt each of its attention units exactly once.  A plan or
+layout change that lets any access leave its allocation fails here, on the
+CPU, before a kernel runs.
 """
 import numpy as np
 import pytest
@@ -79,6 +80,7 @@ def check_pass(H, d, M, V, L, N, P, max_ctx, max_nodes):
         kf0, kf1 = xf[2 * x], xf[2 * x + 1]
         nhx = xh[2 * x + 1] - xh[2 * x]
         n_attu = nhx * nt * (S + 1)
+        dealt = []
         for r in range(RANKS):
             row = tab[x * RANKS + r]
             tag = f"x{x} r{r}"
@@ -134,9 +136,16 @@ def check_pass(H, d, M, V, L, N, P, max_ctx, max_nodes):
                       A_REGION + A_PART + A_Q)
             # attention units dealt to this rank
             for u in range(row[PL_ATT], n_attu, RANKS):
-                hloc, rem = divmod(u, nt * (S + 1))
-                t, part = divmod(rem, S + 1)
+                if n_attu <= RANKS:
+                    hloc, rem = divmod(u, nt * (S + 1))
+                    t, part = divmod(rem, S + 1)
+                elif u < nhx * nt:
+                    (hloc, t), part = divmod(u, nt), S
+                else:
+                    hloc, rem = divmod(u - nhx * nt, nt * S)
+                    t, part = divmod(rem, S)
                 h = xh[2 * x] + hloc
+                dealt.append((hloc, t, part))
                 c.rng(f"{tag} att head", h, h, H)
                 rec = lambda j, nl: ((((h * 4 + t) * (S + 1) + j) * 16 + nl) * AREC)
                 c.rng(f"{tag} part record", rec(part, 0), rec(part, 15) + AREC - 1, sizes["apart"])
@@ -160,6 +169,9 @@ def check_pass(H, d, M, V, L, N, P, max_ctx, max_nodes):
             if hb1 > hb0:
                 c.rng(f"{tag} head fragments", hb0 * KCd * 64, (hb1 - 1) * KCd * 64 + KCd * 64 - 1, sizes["head"])
                 c.rng(f"{tag} logits", hb0 * 16, (N - 1) * V + min(hb1 * 16, V) - 1, sizes["logits"])
+        want = sorted((hl, tt, pp) for hl in range(nhx) for tt in range(nt) for pp in range(S + 1))
+        if sorted(dealt) != want:
+            c.bad.append(f"x{x}: attention units dealt {len(dealt)}, not each of {len(want)} once")
     return c.bad
 
 
