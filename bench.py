@@ -53,9 +53,12 @@ def pass_bytes(cfg, n, P):
     return mats + head + vecs + kv_row * P + (kv_row + V * 4) * n
 
 
-def kernel_source_hash():
+def kernel_source_hash(fused=True):
+    """Hash of the sources of the dominant kernel: the persistent pass
+    (fused.hip) or the per-sub-layer kernels (kernels.hip), with their shared
+    header."""
     h = hashlib.sha256()
-    for name in ("kernels.hip", "fused.hip", "ssd_internal.h"):
+    for name in ("fused.hip" if fused else "kernels.hip", "ssd_internal.h"):
         with open(os.path.join(ROOT, "paper_2308_04623_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
@@ -133,7 +136,7 @@ def traffic_path(fused):
 
 def write_traffic(fetch_dir, write_dir, n, fused):
     kname = PASS_KERNEL if fused else FC_KERNEL
-    out = {"kernel_source": kernel_source_hash(), "kernel": kname, "nodes": n, "copy_bytes": COPY_BYTES}
+    out = {"kernel_source": kernel_source_hash(fused), "kernel": kname, "nodes": n, "copy_bytes": COPY_BYTES}
     for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
         per = _per_kernel(_counter_rows(d), counter)
         # the probe's copy is the largest-grid copy kernel of the run (set-up copies are small)
@@ -162,7 +165,7 @@ def stored_traffic(fused, n):
     if not os.path.exists(path):
         return None
     t = json.load(open(path))
-    if t.get("kernel_source") == kernel_source_hash() and t.get("nodes") == n:
+    if t.get("kernel_source") == kernel_source_hash(fused) and t.get("nodes") == n:
         return t.get("bytes_per_launch")
     return None
 

@@ -1718,11 +1718,19 @@ __global__ __launch_bounds__(1024) void greedy_from_parts_kernel(const unsigned*
   float v = -INFINITY;
   int o = 0x7fffffff;
   if (n < N) {
+    // all of the thread's (up to 16) pairs loaded first, then compared
     typedef unsigned u2v __attribute__((ext_vector_type(2)));
-    for (int k = j; k < G; k += 16) {
-      const u2v pr = *(const u2v*)(parts + ((size_t)n * G + k) * 2);
-      const float v2 = __uint_as_float(pr.x);
-      const int o2 = (int)pr.y;
+    u2v pr[16];
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      const int k = min(j + 16 * q, G - 1);
+      pr[q] = *(const u2v*)(parts + ((size_t)n * G + k) * 2);
+    }
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      if (j + 16 * q >= G) break;
+      const float v2 = __uint_as_float(pr[q].x);
+      const int o2 = (int)pr[q].y;
       if (v2 > v || (v2 == v && o2 < o)) {
         v = v2;
         o = o2;
@@ -1745,7 +1753,7 @@ __global__ __launch_bounds__(1024) void greedy_from_parts_kernel(const unsigned*
 
 hipError_t launch_greedy_from_parts(const unsigned* parts, int G, int N, const int* tokens, const int* parents,
                                     const int* depth, int* path, int* path_len, int* next, hipStream_t s) {
-  if (N < 1 || N > 64) return hipErrorInvalidValue;
+  if (N < 1 || N > 64 || G < 1 || G > 256) return hipErrorInvalidValue;
   greedy_from_parts_kernel<<<1, 1024, 0, s>>>(parts, G, N, tokens, parents, depth, path, path_len, next);
   return hipGetLastError();
 }
