@@ -36,6 +36,7 @@ __device__ __forceinline__ float bf2f(uint16_t h) { return __uint_as_float((uint
 __device__ __forceinline__ uint16_t f2bf(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
 // two floats -> packed bfloat16 pair (first in the low half), one instruction
 __device__ __forceinline__ uint32_t f2bf2(float a, float b) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){a, b}, bf16x2_t));
@@ -1091,11 +1092,18 @@ __device__ __forceinline__ void wave_sync_lds() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// a part record of the bf16 attention: max and sum of exponentials (float32),
+// 8 bytes of padding, then the unnormalised output in float16 (it is rounded
+// to float16 again as the next GEMM's input)
+template <int DH> constexpr int part_bytes() { return 16 + 2 * DH; }
+__device__ __forceinline__ uint32_t f16pair(float a, float b) {
+  return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)a) | ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)b) << 16);
+}
+
 template <int DH>
 __device__ __forceinline__ void attn_prefix_chunk(const AttnArgs& a, uint16_t* lds, int h, int c) {
   constexpr int KS = DH + 8;        // LDS row stride of K (elements)
   constexpr int VS = AT_STAGE + 8;  // LDS row stride of V^T (elements)
-  constexpr int REC = DH + 4;
   constexpr int MAXU = AT_STAGE * DH / 8 / 64;  // 16-byte units per thread, one wave
   uint16_t* ks = lds;
   uint16_t* vts = lds + AT_STAGE * KS;
@@ -1212,10 +1220,12 @@ __device__ __forceinline__ void attn_prefix_chunk(const AttnArgs& a, uint16_t* l
     // part of node 16 t + i: lane (i, g) holds dims 16 tt + 4 g + r
     const int n = 16 * t + i;
     if (n < a.N) {
-      float* rec = a.part + (((size_t)h * ns + c) * a.N + n) * REC;
-      if (g == 0) *(f32x4*)rec = (f32x4){m, l, 0.f, 0.f};
+      unsigned char* rec = (unsigned char*)a.part + (((size_t)h * ns + c) * a.N + n) * part_bytes<DH>();
+      if (g == 0) *(f32x2_t*)rec = (f32x2_t){m, l};
 #pragma unroll
-      for (int tt = 0; tt < DH / 16; ++tt) *(f32x4*)(rec + 4 + 16 * tt + 4 * g) = o[tt];
+      for (int tt = 0; tt < DH / 16; ++tt)
+        *(u32x2*)(rec + 16 + 2 * (16 * tt + 4 * g)) =
+            (u32x2){f16pair(o[tt][0], o[tt][1]), f16pair(o[tt][2], o[tt][3])};
     }
   }
 }
@@ -1223,7 +1233,6 @@ __device__ __forceinline__ void attn_prefix_chunk(const AttnArgs& a, uint16_t* l
 template <int DH>
 __device__ __forceinline__ void attn_root_path(const AttnArgs& a, uint16_t* lds, float (*qrow)[2][DH], int h, int grp) {
   constexpr int DPL = DH / 32;  // output dims per lane of a half-wave
-  constexpr int REC = DH + 4;
   const int tid = threadIdx.x, nw = blockDim.x >> 6, w = tid >> 6, lane = tid & 63;
   const int hw = lane >> 5, hl = lane & 31;
   const int n = grp * 2 * nw + 2 * w + hw;  // this half-wave's node
@@ -1307,10 +1316,11 @@ __device__ __forceinline__ void attn_root_path(const AttnArgs& a, uint16_t* lds,
     wave_sync_lds();  // the batch's V rows are read before the next batch overwrites them
   }
   if (n < a.N) {
-    float* rec = a.part + (((size_t)h * (a.nsplit + 1) + a.nsplit) * a.N + n) * REC;
-    if (hl == 0) *(f32x4*)rec = (f32x4){rm, rl, 0.f, 0.f};
-#pragma unroll
-    for (int e = 0; e < DPL; ++e) rec[4 + DPL * hl + e] = ro[e];
+    unsigned char* rec =
+        (unsigned char*)a.part + (((size_t)h * (a.nsplit + 1) + a.nsplit) * a.N + n) * part_bytes<DH>();
+    if (hl == 0) *(f32x2_t*)rec = (f32x2_t){rm, rl};
+    if constexpr (DPL == 2) *(uint32_t*)(rec + 16 + 4 * hl) = f16pair(ro[0], ro[1]);
+    else *(uint16_t*)(rec + 16 + 2 * hl) = __builtin_bit_cast(uint16_t, (_Float16)ro[0]);
   }
 }
 
@@ -1328,13 +1338,13 @@ __global__ __launch_bounds__(64 * AT_MAXW) void attn_split_kernel(AttnArgs a) {
 
 template <int DH>
 __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
-  constexpr int REC = DH + 4, PER = 256 / DH, B = 16;
+  constexpr int RB = part_bytes<DH>(), PER = 256 / DH, B = 16;
   pass_signal(a.sig);
   const int pair = blockIdx.x * PER + threadIdx.x / DH, dd = threadIdx.x % DH;
   if (pair >= a.N * a.H) return;
   const int n = pair / a.H, h = pair - n * a.H, ns = a.nsplit + 1;
-  const size_t cs = (size_t)a.N * REC;
-  const float* rec = a.part + ((size_t)h * ns * a.N + n) * REC;
+  const size_t cs = (size_t)a.N * RB;
+  const unsigned char* rec = (const unsigned char*)a.part + ((size_t)h * ns * a.N + n) * RB;
   float M = -INFINITY, L = 0.f, O = 0.f;
   for (int c0 = 0; c0 < ns; c0 += B) {
     f32x2_t ml[B];
@@ -1343,7 +1353,7 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
     for (int j = 0; j < B; ++j) {
       const int cc = min(c0 + j, ns - 1);
       ml[j] = *(const f32x2_t*)(rec + cc * cs);
-      ov[j] = rec[cc * cs + 4 + dd];
+      ov[j] = (float)__builtin_bit_cast(_Float16, *(const uint16_t*)(rec + cc * cs + 16 + 2 * dd));
     }
 #pragma unroll
     for (int j = 0; j < B; ++j) {

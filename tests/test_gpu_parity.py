@@ -198,6 +198,17 @@ def test_error_paths_enqueue_nothing(tiny32, ssd, torch):
         with pytest.raises(ssd.SSDError) as e:
             t.s.verify(c["P"], c["toks"], c["par"])
         assert e.value.status == st
+    # a model of another shape on this session's buffers: refused on the host
+    own = t.s.model
+    for other_cfg in (t.cfg.with_(d_mlp=t.cfg.d_mlp // 2), t.cfg.with_(vocab=t.cfg.vocab + 32),
+                      t.cfg.with_(n_layer=t.cfg.n_layer + 1)):
+        t.s.model = ssd.Model(other_cfg, W.make_weights(other_cfg, 2))
+        try:
+            with pytest.raises(ssd.SSDError) as e:
+                t.s.verify(0, [1, 2], [-1, 0])
+            assert e.value.status == ssd.E_INVALID_ARG, other_cfg
+        finally:
+            t.s.model = own
     lg = torch.zeros((2, t.cfg.vocab), device="cuda")
     with pytest.raises(ssd.SSDError):
         t.s.accept([0, 1], [-1, 0], lg, mode=ssd.SAMPLE_WOR)             # no draft probs
