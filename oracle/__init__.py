@@ -52,9 +52,19 @@ class _Config(C.Structure):
 _PP = C.POINTER(C.c_void_p)
 
 
+_I8P, _F32P = C.POINTER(C.c_int8), C.POINTER(C.c_float)
+Q8_MATRICES = ("w_qkv", "w_o", "w_fc", "w_pr")
+
+
+class _Q8(C.Structure):
+    _fields_ = [(f"{n}_code", C.POINTER(_I8P)) for n in ("qkv", "o", "fc", "pr")] + \
+               [(f"{n}_scale", C.POINTER(_F32P)) for n in ("qkv", "o", "fc", "pr")] + \
+               [("head_code", _I8P), ("head_scale", _F32P)]
+
+
 class _Weights(C.Structure):
     _fields_ = [("wte", C.c_void_p), ("wpe", C.c_void_p), ("lnf_g", C.c_void_p), ("lnf_b", C.c_void_p)] + \
-               [(n, _PP) for n in LAYER_TENSORS]
+               [(n, _PP) for n in LAYER_TENSORS] + [("q8", C.POINTER(_Q8))]
 
 
 _lib = None
@@ -76,6 +86,7 @@ def _bind(L):
     L.ssdref_philox4x64_10.restype = None
     L.ssdref_uniform.argtypes = [C.c_uint64, C.c_uint64, C.c_uint64]
     L.ssdref_uniform.restype = C.c_double
+    L.ssdref_quantize_q8.argtypes = [C.POINTER(C.c_uint16), C.c_int32, C.c_int32, _I8P, _F32P]
     L.ssdref_round_bf16.argtypes = [C.c_double]
     L.ssdref_round_bf16.restype = C.c_uint16
     return L
@@ -137,10 +148,25 @@ def _check(rc: int, what: str):
         raise OracleError(rc, what)
 
 
-class Model:
-    """A GPT-2 model for the oracle: config fields plus host parameter arrays."""
+def quantize_q8(w_bits: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
+    """8-bit codes (int8 [rows][cols]) and per-row scales (float32 [rows]) of
+    a bfloat16 matrix, by ssdref_quantize_q8 (format in ssdref.h)."""
+    w = np.ascontiguousarray(w_bits, dtype=np.uint16)
+    rows, cols = w.shape
+    codes = np.zeros((rows, cols), dtype=np.int8)
+    scales = np.zeros(rows, dtype=np.float32)
+    _check(lib().ssdref_quantize_q8(w.ctypes.data_as(C.POINTER(C.c_uint16)), rows, cols,
+                                    codes.ctypes.data_as(_I8P), scales.ctypes.data_as(_F32P)), "quantize_q8")
+    return codes, scales
 
-    def __init__(self, cfg, weights: Dict[str, object]):
+
+class Model:
+    """A GPT-2 model for the oracle: config fields plus host parameter arrays.
+    q8=True (bfloat16 models): the four weight matrices of every layer and
+    the LM head are used as their 8-bit copies (quantize_q8); the embedding
+    keeps wte."""
+
+    def __init__(self, cfg, weights: Dict[str, object], q8: bool = False):
         self.cfg = cfg
         self.dtype = F32 if cfg.dtype == "f32" else BF16
         self.np_dtype = np.float32 if self.dtype == F32 else np.uint16
@@ -159,6 +185,22 @@ class Model:
             ptrs = (C.c_void_p * cfg.n_layer)(*[arr(a) for a in weights[n]])
             self._keep.append(ptrs)
             fields[n] = C.cast(ptrs, _PP)
+        self.q8 = None
+        if q8:
+            if self.dtype != BF16:
+                raise ValueError("8-bit weights are made from a bfloat16 model")
+            self.q8 = {n: [quantize_q8(a) for a in weights[n]] for n in Q8_MATRICES}
+            self.q8["head"] = quantize_q8(weights["wte"])
+            qf = {}
+            for n, short in zip(Q8_MATRICES, ("qkv", "o", "fc", "pr")):
+                codes = (_I8P * cfg.n_layer)(*[c.ctypes.data_as(_I8P) for c, _ in self.q8[n]])
+                scales = (_F32P * cfg.n_layer)(*[sc.ctypes.data_as(_F32P) for _, sc in self.q8[n]])
+                self._keep += [codes, scales]
+                qf[f"{short}_code"] = C.cast(codes, C.POINTER(_I8P))
+                qf[f"{short}_scale"] = C.cast(scales, C.POINTER(_F32P))
+            hc, hs = self.q8["head"]
+            self._q8 = _Q8(head_code=hc.ctypes.data_as(_I8P), head_scale=hs.ctypes.data_as(_F32P), **qf)
+            fields["q8"] = C.pointer(self._q8)
         self._w = _Weights(**fields)
 
     def kv(self, rows: int) -> np.ndarray:

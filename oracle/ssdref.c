@@ -116,9 +116,11 @@ static void layer_norm(const double *x, int32_t n, int32_t d, const void *g, con
 }
 
 /* out[i][o] = (sum_k a[i][k] * W[o][k]) + bias[o]   (bias may be NULL)
- * W is [out_dim][in_dim] in storage type dt.  k ascends for every element. */
-static void linear(const void *W, const void *bias, int dt, int32_t out_dim, int32_t in_dim,
-                   const double *a, int32_t n, double *out, int nt) {
+ * W is [out_dim][in_dim] in storage type dt, or, when qc is not NULL, the
+ * 8-bit weights W[o][k] = qs[o] * qc[o][k] (exact in fp64).  k ascends for
+ * every element. */
+static void linear(const void *W, const int8_t *qc, const float *qs, const void *bias, int dt, int32_t out_dim,
+                   int32_t in_dim, const double *a, int32_t n, double *out, int nt) {
   /* node-minor copy of the input so that one k step touches all nodes */
   double *aT = (double *)malloc(sizeof(double) * (size_t)in_dim * n);
   for (int32_t i = 0; i < n; ++i)
@@ -129,7 +131,8 @@ static void linear(const void *W, const void *bias, int dt, int32_t out_dim, int
     double *acc = (double *)malloc(sizeof(double) * (size_t)n);
 #pragma omp for schedule(static)
     for (int32_t o = 0; o < out_dim; ++o) {
-      for (int32_t k = 0; k < in_dim; ++k) wrow[k] = ld(W, (size_t)o * in_dim + k, dt);
+      for (int32_t k = 0; k < in_dim; ++k)
+        wrow[k] = qc ? (double)qs[o] * (double)qc[(size_t)o * in_dim + k] : ld(W, (size_t)o * in_dim + k, dt);
       for (int32_t i = 0; i < n; ++i) acc[i] = 0.0;
       for (int32_t k = 0; k < in_dim; ++k) {
         const double wk = wrow[k];
@@ -161,6 +164,40 @@ static int check_cfg(const ssdref_config *c) {
 }
 
 /* ------------------------------------------------------------------ */
+/* 8-bit weights (Sec. 4, further speed-ups; format in ssdref.h)       */
+/* ------------------------------------------------------------------ */
+
+int ssdref_quantize_q8(const uint16_t *w, int32_t rows, int32_t cols, int8_t *codes, float *scales) {
+  if (!w || !codes || !scales || rows <= 0 || cols <= 0) return SSDREF_E_ARG;
+  for (size_t e = 0; e < (size_t)rows * cols; ++e)
+    if (!isfinite(bf16_bits_to_double(w[e]))) return SSDREF_E_ARG;
+  for (int32_t o = 0; o < rows; ++o) {
+    const uint16_t *row = w + (size_t)o * cols;
+    int8_t *out = codes + (size_t)o * cols;
+    float a = 0.0f;
+    for (int32_t k = 0; k < cols; ++k) {
+      const float v = fabsf((float)bf16_bits_to_double(row[k]));
+      if (v > a) a = v;
+    }
+    if (!(a >= 0x1p-100f)) {
+      scales[o] = 0.0f;
+      memset(out, 0, (size_t)cols);
+      continue;
+    }
+    const float r = 127.0f / a;
+    for (int32_t k = 0; k < cols; ++k) {
+      const float p = (float)bf16_bits_to_double(row[k]) * r;
+      float c = rintf(p);
+      if (c > 127.0f) c = 127.0f;
+      if (c < -127.0f) c = -127.0f;
+      out[k] = (int8_t)c;
+    }
+    scales[o] = a / 127.0f;
+  }
+  return SSDREF_OK;
+}
+
+/* ------------------------------------------------------------------ */
 /* tree verification pass                                              */
 /* ------------------------------------------------------------------ */
 
@@ -175,6 +212,8 @@ int ssdref_tree_verify(const ssdref_config *cfg, const ssdref_weights *w, const 
   const int32_t L = cfg->n_layer, d = cfg->d_model, H = cfg->n_head, dh = d / H, M = cfg->d_mlp;
   const int32_t V = cfg->vocab, n = n_nodes;
   const int dt = cfg->dtype;
+  const ssdref_q8 *q8 = w->q8;
+  if (q8 && dt != SSDREF_BF16) return SSDREF_E_ARG;
 #ifdef _OPENMP
   const int ntu = n_threads > 0 ? n_threads : omp_get_max_threads();
 #else
@@ -216,7 +255,8 @@ int ssdref_tree_verify(const ssdref_config *cfg, const ssdref_weights *w, const 
   const double scale = 1.0 / sqrt((double)dh);
   for (int32_t l = 0; l < L; ++l) {
     layer_norm(x, n, d, w->ln1_g[l], w->ln1_b[l], dt, cfg->ln_eps, a);
-    linear(w->w_qkv[l], w->b_qkv[l], dt, 3 * d, d, a, n, qkv, ntu);
+    linear(w->w_qkv[l], q8 ? q8->qkv_code[l] : NULL, q8 ? q8->qkv_scale[l] : NULL, w->b_qkv[l], dt, 3 * d, d, a,
+           n, qkv, ntu);
 
     /* the batch's own K/V go to the tree scratch, rounded to the storage type */
     for (int32_t i = 0; i < n; ++i)
@@ -269,25 +309,30 @@ int ssdref_tree_verify(const ssdref_config *cfg, const ssdref_weights *w, const 
       free(path);
     }
 
-    linear(w->w_o[l], w->b_o[l], dt, d, d, att, n, tmp, ntu);
+    linear(w->w_o[l], q8 ? q8->o_code[l] : NULL, q8 ? q8->o_scale[l] : NULL, w->b_o[l], dt, d, d, att, n, tmp,
+           ntu);
     for (size_t e = 0; e < (size_t)n * d; ++e) x[e] += tmp[e];
 
     layer_norm(x, n, d, w->ln2_g[l], w->ln2_b[l], dt, cfg->ln_eps, a);
-    linear(w->w_fc[l], w->b_fc[l], dt, M, d, a, n, f, ntu);
+    linear(w->w_fc[l], q8 ? q8->fc_code[l] : NULL, q8 ? q8->fc_scale[l] : NULL, w->b_fc[l], dt, M, d, a, n, f,
+           ntu);
     for (size_t e = 0; e < (size_t)n * M; ++e) f[e] = gelu(f[e]);
-    linear(w->w_pr[l], w->b_pr[l], dt, d, M, f, n, tmp, ntu);
+    linear(w->w_pr[l], q8 ? q8->pr_code[l] : NULL, q8 ? q8->pr_scale[l] : NULL, w->b_pr[l], dt, d, M, f, n, tmp,
+           ntu);
     for (size_t e = 0; e < (size_t)n * d; ++e) x[e] += tmp[e];
   }
 
   layer_norm(x, n, d, w->lnf_g, w->lnf_b, dt, cfg->ln_eps, a);
-  /* tied LM head: logits = ln_f(x) . wte^T, computed in blocks of rows */
+  /* tied LM head: logits = ln_f(x) . wte^T (or its 8-bit copy), computed in
+   * blocks of rows */
   {
     const int32_t blk = 4096;
     double *lg = (double *)malloc(sizeof(double) * (size_t)n * blk);
     for (int32_t v0 = 0; v0 < V; v0 += blk) {
       const int32_t nv = V - v0 < blk ? V - v0 : blk;
       const void *Wv = (const char *)w->wte + (size_t)v0 * d * elem_size(dt);
-      linear(Wv, NULL, dt, nv, d, a, n, lg, ntu);
+      linear(Wv, q8 ? q8->head_code + (size_t)v0 * d : NULL, q8 ? q8->head_scale + v0 : NULL, NULL, dt, nv, d, a,
+             n, lg, ntu);
       for (int32_t i = 0; i < n; ++i)
         for (int32_t v = 0; v < nv; ++v) logits[(size_t)i * V + v0 + v] = (float)lg[(size_t)i * nv + v];
     }

@@ -65,9 +65,33 @@ typedef struct {
   double ln_eps;
 } ssdref_config;
 
+/* 8-bit weights (Sec. 4 lists 8-bit weights among the further speed-ups
+ * and fixes no format; this is the reading taken here): symmetric, one
+ * float32 scale per output row.  For row o of a bfloat16 matrix let
+ * a = max_k |w[o][k]| (exact in float32).  The codes are decided in float32,
+ * each operation rounded once to nearest even:
+ *   r = 127 / a,   code[o][k] = clamp(rint(w[o][k] * r), -127, 127),
+ *   scale[o] = a / 127;
+ * a row with a < 2^-100 (zeros included) gets scale 0 and codes 0.  The model
+ * then uses the weight scale[o] * code[o][k], read exactly in fp64.
+ * Returns SSDREF_E_ARG (writing nothing) on a NaN or infinite weight. */
+int ssdref_quantize_q8(const uint16_t *w, int32_t rows, int32_t cols, int8_t *codes, float *scales);
+
+/* The 8-bit matrices of a bfloat16 model, from ssdref_quantize_q8: the four
+ * per-layer weight matrices (arrays of n_layer pointers) and the LM head's
+ * own copy of wte (wte itself stays the embedding table). */
+typedef struct {
+  const int8_t *const *qkv_code, *const *o_code, *const *fc_code, *const *pr_code; /* [out][in] */
+  const float *const *qkv_scale, *const *o_scale, *const *fc_scale, *const *pr_scale; /* [out] */
+  const int8_t *head_code;  /* [vocab][d] */
+  const float *head_scale;  /* [vocab]    */
+} ssdref_q8;
+
 /* GPT-2 parameters.  Matrices are [out][in] row-major; element type per
  * config.dtype (bf16 = uint16 bit pattern).  Per-layer entries are arrays of
- * n_layer pointers.  The LM head is tied to wte. */
+ * n_layer pointers.  The LM head is tied to wte.  q8 is NULL, or (bf16
+ * models only) the 8-bit copies the weight matrices and the LM head are read
+ * from instead of w_qkv, w_o, w_fc, w_pr and wte. */
 typedef struct {
   const void *wte;   /* [vocab][d]  */
   const void *wpe;   /* [n_pos][d]  */
@@ -79,6 +103,7 @@ typedef struct {
   const void *const *ln2_g, *const *ln2_b; /* [d]              */
   const void *const *w_fc, *const *b_fc;   /* [d_mlp][d], [d_mlp] */
   const void *const *w_pr, *const *b_pr;   /* [d][d_mlp], [d]  */
+  const ssdref_q8 *q8;
 } ssdref_weights;
 
 /* Tree bookkeeping (Sec. 3.1).  parent_idx[0] must be -1 and
