@@ -114,6 +114,22 @@ typedef struct {
  * LM-head weight of magnitude above 65504, or NaN, which its float16 copy
  * cannot hold), SSD_E_DEVICE. */
 ssd_status ssd_model_create(const ssd_config *cfg, const ssd_weights *w, void *stream, ssd_model **out);
+
+/* Loads a bfloat16 model with 8-bit weights (Sec. 4 names 8-bit weights
+ * among the further speed-ups; the format is this library's reading): the
+ * four weight matrices of every layer and the tied LM head are replaced by
+ * symmetric 8-bit codes with one float32 scale per output row, made once
+ * here from the bfloat16 weights in w.  Per row, with a the largest weight
+ * magnitude, the codes are decided in float32 with every operation rounded
+ * to nearest even: r = 127 / a, code = clamp(rint(w * r), -127, 127),
+ * scale = a / 127 (rows with a < 2^-100: scale 0, codes 0).  The model then
+ * multiplies scale * code, half the weight bytes of ssd_model_create's
+ * float16 copies; the embedding lookups, biases and LayerNorm parameters
+ * stay bfloat16.  This is a different model from the bfloat16 one: its
+ * logits follow the 8-bit weights.  The K/V cache stays bfloat16.  Extra
+ * requirements: dtype SSD_BF16, d_model and d_mlp multiples of 64.  Errors:
+ * as ssd_model_create; SSD_E_UNSUPPORTED also for a NaN or infinite weight. */
+ssd_status ssd_model_create_q8(const ssd_config *cfg, const ssd_weights *w, void *stream, ssd_model **out);
 void ssd_model_destroy(ssd_model *m);
 
 /* Draft view for staged speculation (Sec. 3.2: a cheaper model proposes the

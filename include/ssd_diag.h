@@ -57,6 +57,14 @@ ssd_status ssd_fused_plan(int32_t n_head, int32_t d_model, int32_t d_mlp, int32_
  * (the session has no persistent pass). */
 ssd_status ssd_kv_set_trace(ssd_kv *kv, uint64_t *buf);
 
+/* The 8-bit copy of one weight matrix of a model from ssd_model_create_q8,
+ * for checking: which = 0 W_qkv, 1 W_o, 2 W_fc, 3 W_pr (of `layer`), 4 the
+ * LM head (layer ignored).  Writes codes[rows][cols] (int8, row-major as the
+ * bfloat16 matrix) and scales[rows] (float32) to HOST memory; synchronises
+ * the device.  Errors: SSD_E_INVALID_ARG (null pointer, bad id or layer, a
+ * model without 8-bit weights), SSD_E_DEVICE. */
+ssd_status ssd_model_q8_matrix(const ssd_model *m, int32_t which, int32_t layer, int8_t *codes, float *scales);
+
 #ifdef __cplusplus
 }
 #endif

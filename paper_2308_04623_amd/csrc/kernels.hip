@@ -14,9 +14,14 @@
 //            fragment (rb, kc) holds rows 16rb.., k 32kc..,
 //            lane l's 16 bytes = W[16rb + l%16][32kc + 8(l/16) .. +8], fragments
 //            ordered rb-major so one wave streams 1 KB contiguous per load.
+//            8-bit models: the same fragments at half size (512 B), lane l's
+//            8 bytes = the codes of the same 8 weights plus 128, and a float32
+//            scale per row; the weight is scale * code.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
+
+#include <type_traits>
 
 #include "ssd_internal.h"
 
@@ -27,6 +32,7 @@ typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
 
 // ------------------------------------------------------------------ helpers
 
@@ -351,6 +357,79 @@ hipError_t launch_pack_bf16(const uint16_t* W, int M, int K, void* out, unsigned
   return hipGetLastError();
 }
 
+// 8-bit weights (symmetric, one float32 scale per row).  Per row, with a the
+// largest magnitude (exact in float32), the codes are decided in float32,
+// every operation rounded once to nearest even: r = 127 / a,
+// code = clamp(rint(w r), -127, 127), scale = a / 127; a row with
+// a < 2^-100 gets scale 0 and codes 0.  One workgroup per 16-row block: 16
+// threads per row find a, then every thread writes 8-byte lane slots of the
+// block's fragments (codes stored plus 128).  Rows past M get scale 0 and
+// code 0; NaN or infinite weights are counted in bad.
+__global__ __launch_bounds__(256) void pack_q8_kernel(const uint16_t* __restrict__ W, int M, int K, int KC,
+                                                      u32x2* __restrict__ out, float* __restrict__ scales,
+                                                      unsigned* __restrict__ bad) {
+  __shared__ float rr[16];
+  const int rb = blockIdx.x, tid = threadIdx.x, rl = tid >> 4, sub = tid & 15, row = rb * 16 + rl;
+  float a = 0.f;
+  int nf = 0;
+  if (row < M)
+    for (int k = sub; k < K; k += 16) {
+      const float v = bf2f(W[(size_t)row * K + k]);
+      nf |= !isfinite(v);
+      a = fmaxf(a, fabsf(v));
+    }
+#pragma unroll
+  for (int m = 1; m < 16; m <<= 1) {
+    a = fmaxf(a, __shfl_xor(a, m));
+    nf |= __shfl_xor(nf, m);
+  }
+  if (sub == 0) {
+    if (nf) atomicAdd(bad, 1u);
+    const bool live = row < M && a >= 0x1p-100f;
+    rr[rl] = live ? 127.0f / a : 0.f;
+    scales[row] = live ? a / 127.0f : 0.f;
+  }
+  __syncthreads();
+  for (int idx = tid; idx < KC * 64; idx += 256) {
+    const int kc = idx >> 6, lane = idx & 63, r = lane & 15, k = kc * 32 + 8 * (lane >> 4);
+    u32x2 b = (u32x2){0x80808080u, 0x80808080u};
+    if (rb * 16 + r < M) {
+      const u32x4 v = *(const u32x4*)(W + (size_t)(rb * 16 + r) * K + k);
+      const f32x8 f = __builtin_convertvector(__builtin_bit_cast(bf16x8, v), f32x8);
+      const float rv = rr[r];
+      b = (u32x2){0u, 0u};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float c = fminf(fmaxf(rintf(f[e] * rv), -127.f), 127.f);
+        b[e >> 2] |= (unsigned)((int)c + 128) << (8 * (e & 3));
+      }
+    }
+    out[((size_t)rb * KC + kc) * 64 + lane] = b;
+  }
+}
+
+size_t packed_q8_bytes(int M, int K) { return (size_t)((M + 15) / 16) * (K / 32) * 512; }
+
+hipError_t launch_pack_q8(const uint16_t* W, int M, int K, void* out, float* scales, unsigned* bad, hipStream_t s) {
+  if (K % 32) return hipErrorInvalidValue;
+  pack_q8_kernel<<<(unsigned)((M + 15) / 16), 256, 0, s>>>(W, M, K, K / 32, (u32x2*)out, scales, bad);
+  return hipGetLastError();
+}
+
+// A weight fragment slot as the A operand of v_mfma_f32_16x16x32_f16: the
+// float16 copy as it is, or 8 codes plus 128 widened to float16.  Byte u is
+// put under the exponent bits 0x64 (the float16 1024 + u, exact) and 1152 is
+// subtracted (exact: u - 128 lies in [-128, 127]).
+__device__ __forceinline__ f16x8 wfrag(const u32x4& w) { return __builtin_bit_cast(f16x8, w); }
+__device__ __forceinline__ f16x8 wfrag(const u32x2& w) {
+  u32x4 h;
+  h[0] = __builtin_amdgcn_perm(0x64646464u, w[0], 0x04010400u);
+  h[1] = __builtin_amdgcn_perm(0x64646464u, w[0], 0x04030402u);
+  h[2] = __builtin_amdgcn_perm(0x64646464u, w[1], 0x04010400u);
+  h[3] = __builtin_amdgcn_perm(0x64646464u, w[1], 0x04030402u);
+  return __builtin_bit_cast(f16x8, h) - (f16x8)(_Float16)1152.0f;
+}
+
 // ------------------------------------------------------------------ GEMM, bf16 models (float16 operands)
 //
 // Y[n][o] = sum_k A[n][k] W[o][k] over packed weight fragments.
@@ -371,11 +450,15 @@ hipError_t launch_pack_bf16(const uint16_t* W, int M, int K, void* out, unsigned
 //  vector ALU (few nodes): each lane multiplies its 8 weights into fp32
 //    accumulators per node; the 4 lanes of a row are summed (xor 16, xor 32).
 // Occupancy is traded for registers (1-2 waves per SIMD).
+// Q8: 8-bit weight fragments (512 B), widened to float16 in registers before
+// the product; each output is scaled by its row's scale before the epilogue.
 
-template <int NT, int RB, int KIND, bool VEC, int NV, int U, int NW = 4>
+template <int NT, int RB, int KIND, bool VEC, int NV, int U, int NW = 4, bool Q8 = false>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(NW / 4, NW / 2))) void gemm_kernel(
-    const u32x4* __restrict__ Wp, int KC, int RBtot, int kc_split, const uint16_t* __restrict__ act, Epi ep) {
+    const void* __restrict__ Wv, int KC, int RBtot, int kc_split, const uint16_t* __restrict__ act, Epi ep) {
   static_assert(!VEC || RB == 1, "vector path: one row block per workgroup");
+  using WT = typename std::conditional<Q8, u32x2, u32x4>::type;
+  const WT* Wp = (const WT*)Wv;
   constexpr int NB = VEC ? NV : NT;  // activation fragments per k-step
   constexpr int NN = VEC ? NV : 16 * NT;     // output nodes
   __shared__ float red[NW * RB * NN * 16];
@@ -387,14 +470,14 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(NW / 4,
   const int nsteps = kc1 - kc0 > w ? (kc1 - kc0 - w + NW - 1) / NW : 0;
   // weight rows past the matrix (last workgroup) read row block rb0 instead
   // and are never stored
-  const u32x4* wb[RB];
+  const WT* wb[RB];
 #pragma unroll
   for (int r = 0; r < RB; ++r) wb[r] = Wp + (size_t)min(rb0 + r, RBtot - 1) * KC * 64 + lane;
   // activation fragments (see st_act): MFMA lanes read their own slot; in the
   // vector path lane l reads node n's slot in its 8-k group, 16 (l/16) + n
   const u32x4* abase = (const u32x4*)act + (VEC ? 16 * (lane >> 4) : lane);
 
-  u32x4 wq[U][RB];
+  WT wq[U][RB];
   u32x4 bq[U][NB];
   const int klast = kc1 - 1;
   auto load_step = [&](int s, int u) {
@@ -429,15 +512,15 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(NW / 4,
         if constexpr (!VEC) {
 #pragma unroll
           for (int r = 0; r < RB; ++r) {
-            const u32x4 wf = ok ? wq[u][r] : (u32x4){0, 0, 0, 0};
+            const f16x8 wf = ok ? wfrag(wq[u][r]) : (f16x8)(_Float16)0.0f;
 #pragma unroll
             for (int t = 0; t < NT; ++t)
-              acc[r][t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
-                  __builtin_bit_cast(f16x8, wf), __builtin_bit_cast(f16x8, bq[u][t]), acc[r][t], 0, 0, 0);
+              acc[r][t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(wf, __builtin_bit_cast(f16x8, bq[u][t]),
+                                                                 acc[r][t], 0, 0, 0);
           }
         } else {
-          const u32x4 wf = ok ? wq[u][0] : (u32x4){0, 0, 0, 0};
-          const f32x8 wv = __builtin_convertvector(__builtin_bit_cast(f16x8, wf), f32x8);
+          const f16x8 wf = ok ? wfrag(wq[u][0]) : (f16x8)(_Float16)0.0f;
+          const f32x8 wv = __builtin_convertvector(wf, f32x8);
 #pragma unroll
           for (int n = 0; n < NV; ++n) {
             const f32x8 av = __builtin_convertvector(__builtin_bit_cast(f16x8, bq[u][n]), f32x8);
@@ -481,7 +564,10 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(NW / 4,
 #pragma unroll
     for (int ww = 1; ww < NW; ++ww) s += red[ww * st + base];
     const int o = (rb0 + r) * 16 + row;
-    if (rb0 + r < RBtot && o < ep.M && node < ep.N) epilogue<uint16_t, KIND>(e2, node, o, s);
+    if (rb0 + r < RBtot && o < ep.M && node < ep.N) {
+      if constexpr (Q8) s *= ep.wscale[o];
+      epilogue<uint16_t, KIND>(e2, node, o, s);
+    }
   }
 }
 
@@ -501,11 +587,13 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(NW / 4,
 // (q / (gt gy)), node-tile group j, k-split sk); groups past gx exit.
 constexpr int kG2TT = 4;  // node tiles per workgroup
 
-template <int RBT, int KIND, int U, int NW>
-__global__ __launch_bounds__(64 * NW) void gemm2d_kernel(const u32x4* __restrict__ Wp, int KC, int RBtot, int NT,
+template <int RBT, int KIND, int U, int NW, bool Q8>
+__global__ __launch_bounds__(64 * NW) void gemm2d_kernel(const void* __restrict__ Wv, int KC, int RBtot, int NT,
                                                          int kcs, int gx, int gt, int gy,
                                                          const uint16_t* __restrict__ act, Epi ep) {
   constexpr int TT = kG2TT;
+  using WT = typename std::conditional<Q8, u32x2, u32x4>::type;
+  const WT* Wp = (const WT*)Wv;
   __shared__ float red[NW * TT * 16 * 16];
   pass_signal(ep.sig);
   const int b = blockIdx.x, x = b & 7, q = b >> 3, per = gt * gy;
@@ -518,13 +606,14 @@ __global__ __launch_bounds__(64 * NW) void gemm2d_kernel(const u32x4* __restrict
   const int nsteps = kc1 - kc0 > w ? (kc1 - kc0 - w + NW - 1) / NW : 0;
   // row blocks past the matrix and node tiles past the tree read the last
   // one instead and are never stored
-  const u32x4* wb[RBT];
+  const WT* wb[RBT];
   const u32x4* ab[TT];
 #pragma unroll
   for (int r = 0; r < RBT; ++r) wb[r] = Wp + (size_t)min(rb0 + r, RBtot - 1) * KC * 64 + lane;
 #pragma unroll
   for (int t = 0; t < TT; ++t) ab[t] = (const u32x4*)act + (size_t)min(t0 + t, NT - 1) * KC * 64 + lane;
-  u32x4 wq[U][RBT], bq[U][TT];
+  WT wq[U][RBT];
+  u32x4 bq[U][TT];
   const int klast = kc1 - 1;
   auto load_step = [&](int s, int u) {
     const int kc = min(kc0 + w + NW * s, klast);
@@ -550,11 +639,11 @@ __global__ __launch_bounds__(64 * NW) void gemm2d_kernel(const u32x4* __restrict
         const bool ok = s0 + u < nsteps;
 #pragma unroll
         for (int r = 0; r < RBT; ++r) {
-          const u32x4 wf = ok ? wq[u][r] : (u32x4){0, 0, 0, 0};
+          const f16x8 wf = ok ? wfrag(wq[u][r]) : (f16x8)(_Float16)0.0f;
 #pragma unroll
           for (int t = 0; t < TT; ++t)
-            acc[r][t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, wf),
-                                                               __builtin_bit_cast(f16x8, bq[u][t]), acc[r][t], 0, 0, 0);
+            acc[r][t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(wf, __builtin_bit_cast(f16x8, bq[u][t]), acc[r][t],
+                                                               0, 0, 0);
         }
         __builtin_amdgcn_sched_barrier(0);
         load_step(s0 + u + U, u);
@@ -580,7 +669,10 @@ __global__ __launch_bounds__(64 * NW) void gemm2d_kernel(const u32x4* __restrict
 #pragma unroll
       for (int ww = 1; ww < NW; ++ww) sum += red[ww * TT * 256 + idx];
       const int o = (rb0 + r) * 16 + row;
-      if (o < ep.M && node < ep.N) epilogue<uint16_t, KIND>(e2, node, o, sum);
+      if (o < ep.M && node < ep.N) {
+        if constexpr (Q8) sum *= ep.wscale[o];
+        epilogue<uint16_t, KIND>(e2, node, o, sum);
+      }
     }
     __syncthreads();
   }
@@ -679,8 +771,12 @@ GemmGeom gemm_geom(int kind, int vec, int M, int K, int N, int kcs) {
 
 template <int NT, int RB, int KIND, bool VEC, int NV, int U, int NW = 4>
 static void gemm_launch(const GemmGeom& g, const void* Wp, const uint16_t* act, const Epi& ep, hipStream_t s) {
-  gemm_kernel<NT, RB, KIND, VEC, NV, U, NW>
-      <<<dim3(g.gx, g.gy), 64 * NW, 0, s>>>((const u32x4*)Wp, g.KC, g.RBtot, g.kcs, act, ep);
+  if (ep.wscale)
+    gemm_kernel<NT, RB, KIND, VEC, NV, U, NW, true>
+        <<<dim3(g.gx, g.gy), 64 * NW, 0, s>>>(Wp, g.KC, g.RBtot, g.kcs, act, ep);
+  else
+    gemm_kernel<NT, RB, KIND, VEC, NV, U, NW, false>
+        <<<dim3(g.gx, g.gy), 64 * NW, 0, s>>>(Wp, g.KC, g.RBtot, g.kcs, act, ep);
 }
 
 template <int NT, int RB, bool VEC, int NV, int U>
@@ -696,23 +792,26 @@ static void gemm_go(int kind, const GemmGeom& g, const void* Wp, const uint16_t*
   }
 }
 
+template <int RBT, int KIND, int U, int NW>
+static void gemm2d_launch(const dim3& grid, const void* Wp, int KC, int RBtot, int NT, int kcs, int gx, int gt,
+                          int gy, const uint16_t* act, const Epi& ep, hipStream_t s) {
+  if (ep.wscale)
+    gemm2d_kernel<RBT, KIND, U, NW, true><<<grid, 64 * NW, 0, s>>>(Wp, KC, RBtot, NT, kcs, gx, gt, gy, act, ep);
+  else
+    gemm2d_kernel<RBT, KIND, U, NW, false><<<grid, 64 * NW, 0, s>>>(Wp, KC, RBtot, NT, kcs, gx, gt, gy, act, ep);
+}
+
 template <int RBT, int U, int NW>
-static void gemm2d_go(int kind, const u32x4* Wp, int KC, int RBtot, int NT, int kcs, int gx, int gt, int gy,
+static void gemm2d_go(int kind, const void* Wp, int KC, int RBtot, int NT, int kcs, int gx, int gt, int gy,
                       const uint16_t* act, const Epi& ep, hipStream_t s) {
   const dim3 grid(8 * ((gx + 7) / 8) * gt * gy);
   switch (kind) {
-    case EPI_QKV:
-      gemm2d_kernel<RBT, EPI_QKV, U, NW><<<grid, 64 * NW, 0, s>>>(Wp, KC, RBtot, NT, kcs, gx, gt, gy, act, ep);
-      break;
+    case EPI_QKV: gemm2d_launch<RBT, EPI_QKV, U, NW>(grid, Wp, KC, RBtot, NT, kcs, gx, gt, gy, act, ep, s); break;
     case EPI_PARTIAL:
-      gemm2d_kernel<RBT, EPI_PARTIAL, U, NW><<<grid, 64 * NW, 0, s>>>(Wp, KC, RBtot, NT, kcs, gx, gt, gy, act, ep);
+      gemm2d_launch<RBT, EPI_PARTIAL, U, NW>(grid, Wp, KC, RBtot, NT, kcs, gx, gt, gy, act, ep, s);
       break;
-    case EPI_GELU:
-      gemm2d_kernel<RBT, EPI_GELU, U, NW><<<grid, 64 * NW, 0, s>>>(Wp, KC, RBtot, NT, kcs, gx, gt, gy, act, ep);
-      break;
-    default:
-      gemm2d_kernel<RBT, EPI_LOGITS, U, NW><<<grid, 64 * NW, 0, s>>>(Wp, KC, RBtot, NT, kcs, gx, gt, gy, act, ep);
-      break;
+    case EPI_GELU: gemm2d_launch<RBT, EPI_GELU, U, NW>(grid, Wp, KC, RBtot, NT, kcs, gx, gt, gy, act, ep, s); break;
+    default: gemm2d_launch<RBT, EPI_LOGITS, U, NW>(grid, Wp, KC, RBtot, NT, kcs, gx, gt, gy, act, ep, s); break;
   }
 }
 
@@ -722,7 +821,7 @@ static hipError_t launch_gemm_wide(int kind, const void* Wp, int M, int K, const
   const int gt = (NT + kG2TT - 1) / kG2TT, rbt = g2_rbt(kind, gt);
   const int gx = (RBtot + rbt - 1) / rbt, gy = (KC + kcs - 1) / kcs;
   if (kind != EPI_PARTIAL && gy != 1) return hipErrorInvalidValue;
-  const u32x4* W = (const u32x4*)Wp;
+  const void* W = Wp;
   switch (rbt) {
     case 1: gemm2d_go<1, 2, 4>(kind, W, KC, RBtot, NT, kcs, gx, gt, gy, act, ep, s); break;
     case 2: gemm2d_go<2, 2, 4>(kind, W, KC, RBtot, NT, kcs, gx, gt, gy, act, ep, s); break;

@@ -58,6 +58,10 @@ struct ssd_model {
   bool owns_pack = true;  // false for a prefix view (shares its parent's copies)
   std::vector<const void*> p_qkv, p_o, p_fc, p_pr;
   const void* p_head = nullptr;
+  // 8-bit models: the packed copies hold 8-bit fragments, with these per-row scales
+  bool q8 = false;
+  std::vector<const float*> s_qkv, s_o, s_fc, s_pr;
+  const float* s_head = nullptr;
   void* wtab = nullptr;  // device [4][n_layer]: p_qkv, p_o, p_fc, p_pr (for the prefetcher); own copy per view
   void* ftab = nullptr;  // device [n_layer][kLwSlots]: the persistent pass's per-layer parameters; own copy per view
 };
@@ -245,13 +249,15 @@ static bool cfg_ok(const ssd_config* c, std::string* why) {
   return true;
 }
 
-extern "C" ssd_status ssd_model_create(const ssd_config* cfg, const ssd_weights* w, void* stream, ssd_model** out) {
+static ssd_status model_create(const ssd_config* cfg, const ssd_weights* w, void* stream, ssd_model** out, bool q8) {
   std::string why;
   if (!out || !w) return fail(SSD_E_INVALID_ARG, "null argument");
   if (!cfg_ok(cfg, &why)) return fail(SSD_E_INVALID_ARG, why);
   const int d = cfg->d_model, dh = d / cfg->n_head, L = cfg->n_layer;
   if (d % 32 || cfg->d_mlp % 32 || (dh != 32 && dh != 64))
     return fail(SSD_E_UNSUPPORTED, "need d_model % 32 == 0, d_mlp % 32 == 0, head_dim 32 or 64");
+  if (q8 && cfg->dtype != SSD_BF16) return fail(SSD_E_UNSUPPORTED, "8-bit weights are made from a bfloat16 model");
+  if (q8 && (d % 64 || cfg->d_mlp % 64)) return fail(SSD_E_UNSUPPORTED, "8-bit weights need d_model, d_mlp % 64 == 0");
   if (!w->wte || !w->wpe || !w->lnf_g || !w->lnf_b) return fail(SSD_E_INVALID_ARG, "null embedding / ln_f pointer");
   const void* const* per[12] = {w->ln1_g, w->ln1_b, w->w_qkv, w->b_qkv, w->w_o, w->b_o,
                                 w->ln2_g, w->ln2_b, w->w_fc, w->b_fc, w->w_pr, w->b_pr};
@@ -273,10 +279,16 @@ extern "C" ssd_status ssd_model_create(const ssd_config* cfg, const ssd_weights*
   for (int i = 0; i < 12; ++i) dst[i]->assign(per[i], per[i] + L);
   if (!m->f32) {
     const int M = cfg->d_mlp, V = cfg->vocab;
-    const size_t b_qkv = packed_bytes(3 * d, d), b_o = packed_bytes(d, d), b_fc = packed_bytes(M, d),
-                 b_pr = packed_bytes(d, M), b_head = packed_bytes(V, d);
-    const size_t total = (b_qkv + b_o + b_fc + b_pr) * L + b_head;
-    // the packed copies, then one counter of weights past float16's range
+    m->q8 = q8;
+    auto pbytes = [&](int rows, int K) { return q8 ? packed_q8_bytes(rows, K) : packed_bytes(rows, K); };
+    // per-row scales of the 8-bit copies: [ceil(rows/16) 16] float32, 256-byte aligned
+    auto sbytes = [&](int rows) { return q8 ? (size_t)round_up(round_up(rows, 16) * 4, 256) : (size_t)0; };
+    const size_t b_qkv = pbytes(3 * d, d), b_o = pbytes(d, d), b_fc = pbytes(M, d), b_pr = pbytes(d, M),
+                 b_head = pbytes(V, d);
+    const size_t total = (b_qkv + b_o + b_fc + b_pr + sbytes(3 * d) + 2 * sbytes(d) + sbytes(M)) * L + b_head +
+                         sbytes(V);
+    // the packed copies (and scales), then one counter of weights past
+    // float16's range (8-bit copies: of rows holding a NaN or infinity)
     hipError_t e = hipMalloc(&m->pack, total + 256);
     if (e != hipSuccess) {
       delete m;
@@ -286,27 +298,38 @@ extern "C" ssd_status ssd_model_create(const ssd_config* cfg, const ssd_weights*
     unsigned* bad = (unsigned*)((char*)m->pack + total);
     e = hipMemsetAsync(bad, 0, 4, s);
     char* p = (char*)m->pack;
-    auto pack = [&](const void* src, int rows, int cols, size_t bytes) -> const void* {
-      if (e == hipSuccess) e = launch_pack_bf16((const uint16_t*)src, rows, cols, p, bad, s);
+    // (8-bit: the fragments first, then the row scales)
+    auto pack = [&](const void* src, int rows, int cols, size_t bytes, std::vector<const float*>* sc) -> const void* {
       const void* r = p;
-      p += bytes;
+      if (!q8) {
+        if (e == hipSuccess) e = launch_pack_bf16((const uint16_t*)src, rows, cols, p, bad, s);
+        p += bytes;
+        return r;
+      }
+      float* scales = (float*)(p + bytes);
+      if (e == hipSuccess) e = launch_pack_q8((const uint16_t*)src, rows, cols, p, scales, bad, s);
+      sc->push_back(scales);
+      p += bytes + sbytes(rows);
       return r;
     };
+    std::vector<const float*> s_head;
     for (int l = 0; l < L; ++l) {
-      m->p_qkv.push_back(pack(m->w_qkv[l], 3 * d, d, b_qkv));
-      m->p_o.push_back(pack(m->w_o[l], d, d, b_o));
-      m->p_fc.push_back(pack(m->w_fc[l], M, d, b_fc));
-      m->p_pr.push_back(pack(m->w_pr[l], d, M, b_pr));
+      m->p_qkv.push_back(pack(m->w_qkv[l], 3 * d, d, b_qkv, &m->s_qkv));
+      m->p_o.push_back(pack(m->w_o[l], d, d, b_o, &m->s_o));
+      m->p_fc.push_back(pack(m->w_fc[l], M, d, b_fc, &m->s_fc));
+      m->p_pr.push_back(pack(m->w_pr[l], d, M, b_pr, &m->s_pr));
     }
-    m->p_head = pack(m->wte, V, d, b_head);
+    m->p_head = pack(m->wte, V, d, b_head, &s_head);
+    if (q8) m->s_head = s_head[0];
     unsigned n_bad = 0;
     if (e == hipSuccess) e = hipMemcpyAsync(&n_bad, bad, 4, hipMemcpyDeviceToHost, s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e == hipSuccess && n_bad) {
       (void)hipFree(m->pack);
       delete m;
-      return fail(SSD_E_UNSUPPORTED, "a weight's magnitude exceeds 65504 (or is NaN): the matrix cores take "
-                                     "float16 copies of the weights");
+      return fail(SSD_E_UNSUPPORTED, q8 ? "a weight is NaN or infinite: it has no 8-bit code"
+                                        : "a weight's magnitude exceeds 65504 (or is NaN): the matrix cores take "
+                                          "float16 copies of the weights");
     }
     if (e == hipSuccess) e = make_wtab(m);
     if (e == hipSuccess) e = make_ftab(m);
@@ -320,6 +343,15 @@ extern "C" ssd_status ssd_model_create(const ssd_config* cfg, const ssd_weights*
   }
   *out = m;
   return SSD_OK;
+}
+
+extern "C" ssd_status ssd_model_create(const ssd_config* cfg, const ssd_weights* w, void* stream, ssd_model** out) {
+  return model_create(cfg, w, stream, out, false);
+}
+
+extern "C" ssd_status ssd_model_create_q8(const ssd_config* cfg, const ssd_weights* w, void* stream,
+                                          ssd_model** out) {
+  return model_create(cfg, w, stream, out, true);
 }
 
 extern "C" void ssd_model_destroy(ssd_model* m) {
@@ -346,6 +378,12 @@ extern "C" ssd_status ssd_model_prefix_view(const ssd_model* m, int32_t n_layer,
     v->p_o.resize(n_layer);
     v->p_fc.resize(n_layer);
     v->p_pr.resize(n_layer);
+    if (v->q8) {
+      v->s_qkv.resize(n_layer);
+      v->s_o.resize(n_layer);
+      v->s_fc.resize(n_layer);
+      v->s_pr.resize(n_layer);
+    }
     hipError_t e = make_wtab(v);
     if (e == hipSuccess) e = make_ftab(v);
     if (e != hipSuccess) {
@@ -447,7 +485,7 @@ static ssd_status fused_setup(ssd_kv* kv) {
 
 // whether a verification pass of model m over n nodes runs as the persistent single launch
 static bool use_fused(const ssd_model* m, const ssd_kv* kv, int n) {
-  if (kv->pass_mode == 1 || m->f32 || !kv->fz_ok || !m->ftab) return false;
+  if (kv->pass_mode == 1 || m->f32 || m->q8 || !kv->fz_ok || !m->ftab) return false;
   // the persistent pass is forced, or chosen where it is the faster one
   // (measured on the GPT-2-L shape: at every node count it supports)
   return kv->pass_mode == 2 ? n <= kFMaxN : n <= kFAutoMaxN;
@@ -662,7 +700,10 @@ static PrefetchPlan prefetch_plan(const ssd_model* m, const ssd_kv* kv, int path
   const int rows[4] = {3 * d, d, M, d}, Ks[4] = {d, d, d, M};
   for (int k = 0; k < 4; ++k) {
     const GemmGeom g = gemm_geom(kinds[k], vec, rows[k], Ks[k], nn, gemm_kcs(path, n, kinds[k], rows[k], Ks[k]));
-    pp.geo[k] = PfGeom{g.KC, g.RBtot, g.RB, g.kcs, g.gx, g.gx * g.gy};
+    // (the prefetcher reads 1 KB fragments: an 8-bit row block is KC / 2 of
+    // them, K being a multiple of 64; a split's range rounds to whole ones)
+    if (m->q8) pp.geo[k] = PfGeom{g.KC / 2, g.RBtot, g.RB, (g.kcs + 1) / 2, g.gx, g.gx * g.gy};
+    else pp.geo[k] = PfGeom{g.KC, g.RBtot, g.RB, g.kcs, g.gx, g.gx * g.gy};
   }
   pp.W = (const void* const*)m->wtab;
   pp.L = m->cfg.n_layer;
@@ -691,8 +732,8 @@ static ssd_status start_pass_prefetch(const ssd_model* m, ssd_kv* kv, int n, boo
   return SSD_OK;
 }
 
-static hipError_t run_gemm(const ssd_model* m, int path, int n, int kind, const void* Wraw, const void* Wp, int rows,
-                           int K, const void* act, const Epi& ep, hipStream_t s) {
+static hipError_t run_gemm(const ssd_model* m, int path, int n, int kind, const void* Wraw, const void* Wp,
+                           const float* wscale, int rows, int K, const void* act, const Epi& ep, hipStream_t s) {
   if (m->f32) return launch_gemm_f32(kind, (const float*)Wraw, rows, K, (const float*)act, K, ep, s);
   const int vec = gemm_vec(path, n);
   const int group = vec ? 16 : 256;
@@ -704,6 +745,7 @@ static hipError_t run_gemm(const ssd_model* m, int path, int n, int kind, const 
     // fragment tiles of 16 nodes, each K/32 fragments of 512 elements
     const uint16_t* a = (const uint16_t*)act + (size_t)(n0 / 16) * (K / 32) * 512;
     e2.sig = n0 == 0 ? ep.sig : nullptr;  // one signal per GEMM
+    e2.wscale = m->q8 ? wscale : nullptr;
     hipError_t r = launch_gemm_bf16(kind, vec, Wp, rows, K, a, kcs, e2, s);
     if (r != hipSuccess) return r;
   }
@@ -765,6 +807,7 @@ static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int3
   }
   if (kv->pass_mode == 2) return fail(SSD_E_UNSUPPORTED, "the persistent pass does not apply to this model, session or tree");
   const int gp = kv->gemm_path;
+  const bool q8 = m->q8;
   unsigned long long* sig = f32 ? nullptr : kv->d_sig;  // pass signals (bf16 models)
   HIP_TRY(launch_embed(f32, m->wte, m->wpe, d_tok, d_pos, n, d, kv->x, sig, kv->d_xcc0, s));
 
@@ -794,7 +837,8 @@ static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int3
     e.H = H;
     e.DH = DH;
     e.max_nodes = maxn;
-    HIP_TRY(run_gemm(m, gp, n, EPI_QKV, m->w_qkv[l], f32 ? nullptr : m->p_qkv[l], 3 * d, d, kv->act_a, e, s));
+    HIP_TRY(run_gemm(m, gp, n, EPI_QKV, m->w_qkv[l], f32 ? nullptr : m->p_qkv[l], q8 ? m->s_qkv[l] : nullptr,
+                     3 * d, d, kv->act_a, e, s));
 
     AttnArgs a{};
     a.q = kv->q;
@@ -832,7 +876,8 @@ static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int3
     eo.x = kv->x;
     eo.part = kv->part;
     eo.part_stride = (long long)pstride;
-    HIP_TRY(run_gemm(m, gp, n, kind_res, m->w_o[l], f32 ? nullptr : m->p_o[l], d, d, kv->act_o, eo, s));
+    HIP_TRY(run_gemm(m, gp, n, kind_res, m->w_o[l], f32 ? nullptr : m->p_o[l], q8 ? m->s_o[l] : nullptr, d, d,
+                     kv->act_o, eo, s));
 
     HIP_TRY(launch_ln(f32, kv->x, n, d, kv->part, f32 ? 0 : s_o, pstride, m->b_o[l], m->ln2_g[l], m->ln2_b[l],
                       c.ln_eps, kv->act_a, ld_d, sig, kv->d_err, s));
@@ -845,7 +890,8 @@ static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int3
     ef.d = d;
     ef.out = kv->act_f;
     ef.ldo = ld_m;
-    HIP_TRY(run_gemm(m, gp, n, EPI_GELU, m->w_fc[l], f32 ? nullptr : m->p_fc[l], M, d, kv->act_a, ef, s));
+    HIP_TRY(run_gemm(m, gp, n, EPI_GELU, m->w_fc[l], f32 ? nullptr : m->p_fc[l], q8 ? m->s_fc[l] : nullptr, M, d,
+                     kv->act_a, ef, s));
 
     Epi ep{};
     ep.sig = sig;
@@ -856,7 +902,8 @@ static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int3
     ep.x = kv->x;
     ep.part = kv->part;
     ep.part_stride = (long long)pstride;
-    HIP_TRY(run_gemm(m, gp, n, kind_res, m->w_pr[l], f32 ? nullptr : m->p_pr[l], d, M, kv->act_f, ep, s));
+    HIP_TRY(run_gemm(m, gp, n, kind_res, m->w_pr[l], f32 ? nullptr : m->p_pr[l], q8 ? m->s_pr[l] : nullptr, d, M,
+                     kv->act_f, ep, s));
     pend_S = f32 ? 0 : s_pr;
     pend_bias = m->b_pr[l];
   }
@@ -869,7 +916,7 @@ static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int3
   eh.d = d;
   eh.logits = logits;
   eh.ldl = V;
-  HIP_TRY(run_gemm(m, gp, n, EPI_LOGITS, m->wte, f32 ? nullptr : m->p_head, V, d, kv->act_a, eh, s));
+  HIP_TRY(run_gemm(m, gp, n, EPI_LOGITS, m->wte, f32 ? nullptr : m->p_head, m->s_head, V, d, kv->act_a, eh, s));
   return SSD_OK;
 }
 
@@ -1037,6 +1084,7 @@ extern "C" ssd_status ssd_launch_gemm(const ssd_model* m, ssd_kv* kv, int32_t wh
   e.part_stride = (long long)kv->max_nodes * d;
   const int kind_res = m->f32 ? EPI_RESID : EPI_PARTIAL;
   const void *Wraw = nullptr, *Wp = nullptr, *act = kv->act_a;
+  const float* wscale = nullptr;
   int rows = d, K = d, lda = d, kind = kind_res;
   switch (which) {
     case 0:
@@ -1044,24 +1092,28 @@ extern "C" ssd_status ssd_launch_gemm(const ssd_model* m, ssd_kv* kv, int32_t wh
       e.kt = (char*)kv->kt + (size_t)layer * c.n_head * m->dh * kv->max_nodes * es;
       e.vt = (char*)kv->vt + (size_t)layer * c.n_head * m->dh * kv->max_nodes * es;
       if (!m->f32) Wp = m->p_qkv[layer];
+      if (m->q8) wscale = m->s_qkv[layer];
       break;
     case 1:
       Wraw = m->w_o[layer]; act = kv->act_o; if (m->f32) e.bias = m->b_o[layer];
       if (!m->f32) Wp = m->p_o[layer];
+      if (m->q8) wscale = m->s_o[layer];
       break;
     case 2:
       kind = EPI_GELU; rows = M; Wraw = m->w_fc[layer]; e.bias = m->b_fc[layer]; e.out = kv->act_f;
       e.ldo = m->f32 ? M : M / 32;
       if (!m->f32) Wp = m->p_fc[layer];
+      if (m->q8) wscale = m->s_fc[layer];
       break;
     default:
       K = M; lda = M; Wraw = m->w_pr[layer]; act = kv->act_f; if (m->f32) e.bias = m->b_pr[layer];
       if (!m->f32) Wp = m->p_pr[layer];
+      if (m->q8) wscale = m->s_pr[layer];
       break;
   }
   e.M = rows;
   (void)lda;
-  HIP_TRY(run_gemm(m, kv->gemm_path, n_nodes, kind, Wraw, Wp, rows, K, act, e, (hipStream_t)stream));
+  HIP_TRY(run_gemm(m, kv->gemm_path, n_nodes, kind, Wraw, Wp, wscale, rows, K, act, e, (hipStream_t)stream));
   return SSD_OK;
 }
 
@@ -1263,5 +1315,36 @@ extern "C" ssd_status ssd_kv_error_count(ssd_kv* kv, void* stream, uint32_t* cou
   HIP_TRY(hipMemcpyAsync(&h, kv->d_err, 4, hipMemcpyDeviceToHost, (hipStream_t)stream));
   HIP_TRY(hipStreamSynchronize((hipStream_t)stream));
   *count = h;
+  return SSD_OK;
+}
+
+// ------------------------------------------------------------------ 8-bit weights, read back
+
+extern "C" ssd_status ssd_model_q8_matrix(const ssd_model* m, int32_t which, int32_t layer, int8_t* codes,
+                                          float* scales) {
+  if (!m || !codes || !scales) return fail(SSD_E_INVALID_ARG, "null argument");
+  if (!m->q8) return fail(SSD_E_INVALID_ARG, "the model has no 8-bit weights");
+  const ssd_config& c = m->cfg;
+  if (which < 0 || which > 4 || (which < 4 && (layer < 0 || layer >= c.n_layer)))
+    return fail(SSD_E_INVALID_ARG, "bad matrix id or layer");
+  const int d = c.d_model, M = c.d_mlp;
+  const int rows[5] = {3 * d, d, M, d, c.vocab}, Ks[5] = {d, d, d, M, d};
+  const void* frag[5] = {nullptr, nullptr, nullptr, nullptr, m->p_head};
+  const float* sc[5] = {nullptr, nullptr, nullptr, nullptr, m->s_head};
+  if (which < 4) {
+    frag[which] = (which == 0 ? m->p_qkv : which == 1 ? m->p_o : which == 2 ? m->p_fc : m->p_pr)[layer];
+    sc[which] = (which == 0 ? m->s_qkv : which == 1 ? m->s_o : which == 2 ? m->s_fc : m->s_pr)[layer];
+  }
+  const int R = rows[which], K = Ks[which], KC = K / 32;
+  std::vector<uint8_t> f(packed_q8_bytes(R, K));
+  HIP_TRY(hipDeviceSynchronize());
+  HIP_TRY(hipMemcpy(f.data(), frag[which], f.size(), hipMemcpyDeviceToHost));
+  HIP_TRY(hipMemcpy(scales, sc[which], (size_t)R * 4, hipMemcpyDeviceToHost));
+  // fragment (rb, kc), lane l, byte j: row 16 rb + l % 16, k = 32 kc + 8 (l / 16) + j
+  for (int r = 0; r < R; ++r)
+    for (int k = 0; k < K; ++k) {
+      const int rb = r / 16, kc = k / 32, lane = (r % 16) + 16 * ((k % 32) / 8);
+      codes[(size_t)r * K + k] = (int8_t)((int)f[(((size_t)rb * KC + kc) * 64 + lane) * 8 + k % 8] - 128);
+    }
   return SSD_OK;
 }

@@ -48,6 +48,7 @@ struct Epi {
   int split;              // set by the kernel from blockIdx.y
   unsigned long long* sig;  // pass signal counter (nullptr: none)
   unsigned* err;            // session error counter: float16 GEMM inputs out of range (nullptr: none)
+  const float* wscale;      // 8-bit weights: the rows' scales (nullptr: float16 weight fragments)
 };
 
 // tile shape of the bf16 GEMM for a node count: node tiles of 16, row blocks
@@ -155,8 +156,9 @@ int gemm_split_kc(int M, int K, int N, int vec, int want_split, int* splits);
 // wide-tree kernel (row blocks x node tiles per workgroup)
 bool gemm_wide(int vec, int N);
 GemmGeom gemm_geom(int kind, int vec, int M, int K, int N, int kcs);
-// Wp: weights packed in 16x32 float16 fragments (see pack); act: activations
-// of this launch's first node in fragment order (see st_act); kcs k-steps per
+// Wp: weights packed in 16x32 float16 fragments (see pack), or, with
+// ep.wscale set, in 16x32 8-bit fragments (see pack_q8); act: activations of
+// this launch's first node in fragment order (see st_act); kcs k-steps per
 // split (grid.y = ceil(K/32 / kcs))
 hipError_t launch_gemm_bf16(int kind, int vec, const void* Wp, int M, int K, const uint16_t* act, int kcs,
                             const Epi& ep, hipStream_t s);
@@ -165,6 +167,10 @@ hipError_t launch_prefetcher(const PrefetchPlan& pp, hipStream_t s);
 // bad: device counter of packed 16-byte groups holding a weight past float16's range
 hipError_t launch_pack_bf16(const uint16_t* W, int M, int K, void* out, unsigned* bad, hipStream_t s);
 size_t packed_bytes(int M, int K);
+// 8-bit copy of a bf16 matrix: fragments (packed_q8_bytes) and scales
+// [ceil(M/16) 16] float32; bad counts rows holding a NaN or infinite weight
+hipError_t launch_pack_q8(const uint16_t* W, int M, int K, void* out, float* scales, unsigned* bad, hipStream_t s);
+size_t packed_q8_bytes(int M, int K);
 // greedy argmax per node; work: argmax_work_bytes(N, V) bytes of device scratch
 size_t argmax_work_bytes(int N, int V);
 hipError_t launch_argmax(const float* logits, int N, int V, int* g, void* work, hipStream_t s);

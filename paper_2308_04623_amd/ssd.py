@@ -26,14 +26,14 @@ LAYER_TENSORS = ("ln1_g", "ln1_b", "w_qkv", "b_qkv", "w_o", "b_o",
                  "ln2_g", "ln2_b", "w_fc", "b_fc", "w_pr", "b_pr")
 
 # every function include/ssd.h declares
-EXPORTS = ("ssd_model_create", "ssd_model_destroy", "ssd_kv_bytes", "ssd_kv_create", "ssd_kv_destroy",
+EXPORTS = ("ssd_model_create", "ssd_model_create_q8", "ssd_model_destroy", "ssd_kv_bytes", "ssd_kv_create", "ssd_kv_destroy",
            "ssd_tree_verify", "ssd_tree_accept", "ssd_kv_commit", "ssd_kv_error_count",
            "ssd_graph_capture_verify", "ssd_graph_launch", "ssd_graph_destroy", "ssd_validate_tree",
            "ssd_tree_prep", "ssd_kv_set_options", "ssd_kv_get_options", "ssd_status_string", "ssd_last_error",
            "ssd_model_prefix_view", "ssd_topk", "ssd_tree_accept_noalloc", "ssd_tree_verify_greedy",
            "ssd_graph_capture_verify_greedy")
 # and every function include/ssd_diag.h declares (measurement and diagnostics)
-DIAG_EXPORTS = ("ssd_launch_gemm", "ssd_verify_path", "ssd_fused_plan", "ssd_kv_set_trace")
+DIAG_EXPORTS = ("ssd_launch_gemm", "ssd_verify_path", "ssd_fused_plan", "ssd_kv_set_trace", "ssd_model_q8_matrix")
 
 
 class SSDError(RuntimeError):
@@ -80,6 +80,8 @@ def lib():
         i32p, vp = C.POINTER(C.c_int32), C.c_void_p
         sig = {
             "ssd_model_create": [C.POINTER(_Config), C.POINTER(_Weights), vp, C.POINTER(vp)],
+            "ssd_model_create_q8": [C.POINTER(_Config), C.POINTER(_Weights), vp, C.POINTER(vp)],
+            "ssd_model_q8_matrix": [vp, C.c_int32, C.c_int32, vp, vp],
             "ssd_model_destroy": [vp],
             "ssd_kv_bytes": [C.POINTER(_Config), C.c_int32, C.c_int32, C.POINTER(C.c_size_t),
                              C.POINTER(C.c_size_t)],
@@ -231,10 +233,13 @@ def to_host_bits(t) -> np.ndarray:
 
 class Model:
     """A GPT-2 model resident on the GPU.  `weights` is the dict produced by
-    workloads.make_weights (host arrays); they are uploaded once."""
+    workloads.make_weights (host arrays); they are uploaded once.  q8=True
+    (bfloat16 models): ssd_model_create_q8, 8-bit weight matrices and LM
+    head."""
 
-    def __init__(self, cfg, weights: Dict[str, object], device="cuda", stream=None):
+    def __init__(self, cfg, weights: Dict[str, object], device="cuda", stream=None, q8: bool = False):
         self.cfg = cfg
+        self.q8 = q8
         self.device = device
         self.tensors = {}
         ptr = lambda t: C.c_void_p(t.data_ptr())
@@ -251,9 +256,23 @@ class Model:
         self._cfg = _config(cfg)
         self._w = _Weights(**fields)
         h = C.c_void_p()
-        _check(lib().ssd_model_create(C.byref(self._cfg), C.byref(self._w), _stream(stream), C.byref(h)),
-               "ssd_model_create")
+        create = lib().ssd_model_create_q8 if q8 else lib().ssd_model_create
+        _check(create(C.byref(self._cfg), C.byref(self._w), _stream(stream), C.byref(h)),
+               "ssd_model_create_q8" if q8 else "ssd_model_create")
         self.handle = h
+
+    def q8_matrix(self, which: int, layer: int = 0):
+        """(codes int8 [rows][cols], scales float32 [rows]) of one 8-bit
+        matrix: which 0 W_qkv, 1 W_o, 2 W_fc, 3 W_pr, 4 the LM head."""
+        c = self.cfg
+        ok = 0 <= which <= 4   # (other ids go to the library, which refuses them)
+        rows = [3 * c.d_model, c.d_model, c.d_mlp, c.d_model, c.vocab][which] if ok else 1
+        cols = [c.d_model, c.d_model, c.d_model, c.d_mlp, c.d_model][which] if ok else 1
+        codes = np.zeros((rows, cols), dtype=np.int8)
+        scales = np.zeros(rows, dtype=np.float32)
+        _check(lib().ssd_model_q8_matrix(self.handle, which, layer, C.c_void_p(codes.ctypes.data),
+                                         C.c_void_p(scales.ctypes.data)), "ssd_model_q8_matrix")
+        return codes, scales
 
     def prefix_view(self, n_layer: int) -> "ModelView":
         """Draft view: the first n_layer blocks with this model's final

@@ -1,0 +1,88 @@
+"""Full-size parity of the 8-bit weight model on the GPT-2-L shape (36 x
+1280, 20 heads, MLP 5120, vocab 50257) against the oracle's 8-bit mode, in
+the launch configuration the benchmark times (the captured graph of the
+pass, default pass mode).
+
+- Codes and scales of the LM head and of the first and last layers' MLP
+  matrices bit-exact.
+- Every row and every logit (2e-2 max-abs) at 32 nodes ([4,2,2,1]) over a
+  512-token prefix and at 128 nodes (a best-first tree), the session's error
+  counter at 0, greedy accept bit-exact on the GPU's logits.
+The prefix caches are synthetic N(0, 0.7) K/V."""
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2308_04623_amd import workloads as W
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+TOL = 2e-2
+THREADS = int(os.environ.get("OMP_NUM_THREADS", "0") or 0)
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as t
+    assert t.cuda.is_available()
+    return t
+
+
+@pytest.fixture(scope="module")
+def big(torch):
+    from paper_2308_04623_amd import ssd
+    cfg = W.GPT2L
+    print("generating GPT-2-L weights", flush=True)
+    w = W.make_weights(cfg, 0)
+    om = oracle.Model(cfg, w, q8=True)
+    m = ssd.Model(cfg, w, q8=True)
+    return cfg, om, m, ssd
+
+
+def test_gpt2l_q8_codes_bit_exact(big):
+    cfg, om, m, ssd = big
+    for which, name, l in ((2, "w_fc", 0), (3, "w_pr", cfg.n_layer - 1), (0, "w_qkv", 17)):
+        codes, scales = m.q8_matrix(which, l)
+        rc, rs = om.q8[name][l]
+        assert np.array_equal(codes, rc), (name, l)
+        assert np.array_equal(scales.view(np.uint32), rs.view(np.uint32)), (name, l)
+    codes, scales = m.q8_matrix(4)
+    rc, rs = om.q8["head"]
+    assert np.array_equal(codes, rc) and np.array_equal(scales.view(np.uint32), rs.view(np.uint32))
+
+
+def _check_tree(big, torch, P, toks, par, max_nodes, seed):
+    cfg, om, m, ssd = big
+    kc, vc = W.random_kv_cache(cfg, P + 64, P, seed=seed)
+    s = ssd.Session(m, P + 64, max_nodes, ssd.to_device(kc, cfg), ssd.to_device(vc, cfg))
+    lg = torch.zeros((len(par), cfg.vocab), dtype=torch.float32, device="cuda")
+    g = s.capture_verify(P, toks, par, lg)
+    g.launch()
+    torch.cuda.synchronize()
+    got = lg.cpu().numpy()
+    g.close()
+    assert s.error_count() == 0
+    print(f"oracle verify ({len(par)} nodes, P={P}, 8-bit)", flush=True)
+    ref = oracle.tree_verify(om, kc, vc, P, toks, par, om.kv(max_nodes), om.kv(max_nodes), THREADS)
+    err = np.abs(got - ref)
+    print(f"n={len(par)} P={P} max|d| {err.max():.3e} mean {err.mean():.3e}", flush=True)
+    assert err.max() < TOL
+    path, plen, nxt = s.accept(toks, par, lg)
+    op, on = oracle.tree_accept(oracle.GREEDY, toks, par, got)
+    assert path[:int(plen.item())].cpu().numpy().tolist() == op.tolist() and int(nxt.item()) == on
+    s.close()
+
+
+def test_gpt2l_q8_c2_full_tree(big, torch):
+    cfg = big[0]
+    par = W.branching_tree([4, 2, 2, 1], 32)
+    toks = W.tree_tokens(par, cfg.vocab, seed=2)
+    _check_tree(big, torch, 512, toks, par, 64, seed=3)
+
+
+def test_gpt2l_q8_128_nodes_full_tree(big, torch):
+    cfg = big[0]
+    toks, par = W.best_first_tree(128, seed=3, vocab=cfg.vocab)
+    toks[0] = 17
+    _check_tree(big, torch, 512, toks, par, 128, seed=4)
