@@ -53,6 +53,7 @@
 
 #include <algorithm>
 #include <string>
+#include <type_traits>
 #include <vector>
 
 #include "ssd_internal.h"
@@ -71,6 +72,20 @@ typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) float lds_f32;
 typedef __attribute__((address_space(3))) f32x4 lds_f32x4;
 typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+// A weight fragment slot as the A operand of v_mfma_f32_16x16x32_f16: the
+// float16 copy as it is, or (8-bit models) 8 codes plus 128 widened to
+// float16: byte u goes under the exponent bits 0x64 (the float16 1024 + u,
+// exact) and 1152 is subtracted (exact: u - 128 lies in [-128, 127]).
+__device__ __forceinline__ f16x8 wfrag(const u32x4& w) { return __builtin_bit_cast(f16x8, w); }
+__device__ __forceinline__ f16x8 wfrag(const u32x2& w) {
+  u32x4 h;
+  h[0] = __builtin_amdgcn_perm(0x64646464u, w[0], 0x04010400u);
+  h[1] = __builtin_amdgcn_perm(0x64646464u, w[0], 0x04030402u);
+  h[2] = __builtin_amdgcn_perm(0x64646464u, w[1], 0x04010400u);
+  h[3] = __builtin_amdgcn_perm(0x64646464u, w[1], 0x04030402u);
+  return __builtin_bit_cast(f16x8, h) - (f16x8)(_Float16)1152.0f;
+}
 
 // Global-memory pointers (address space 1): loads through them are
 // global_load, waited on in order, never flat.
@@ -706,8 +721,39 @@ constexpr int WST = 16 * 1024;                              // LDS offset of the
 constexpr int WST_FRAGS = (73728 + 34816 + 4096 - WST) / 1024;  // 1 KB fragments that fit below sh
 constexpr int WO_FRAGS = 24;  // the out-projection's staged fragments, above the parameter table
 
+// Copies weight fragments f = wv - 1, wv - 1 + nw, ... < n * nk (row block
+// rbs[f / nk] (an LDS list), k-step k0 + f % nk of a matrix of KC k-steps)
+// into LDS at dst + f * fragment bytes, by waves 1.. of a stage (nw of them).
+// float16 fragments (1 KB) take one 16-byte copy per lane; 8-bit fragments
+// (512 B) two 4-byte copies, of their first and second 256 bytes, so the LDS
+// image equals the fragment either way.
+template <bool Q8>
+__device__ __forceinline__ void stage_frags(gptr<u32x4> W, const int* rbs, int n, int k0, int nk, int KC,
+                                            unsigned char* dst, int wv, int nw) {
+  const int lane = threadIdx.x & 63, tot = n * nk;
+  if constexpr (!Q8) {
+    const gptr<u32x4> Wv = opq(W) + lane;
+    for (int f = wv - 1; f < tot; f += nw) {
+      const int r = f / nk, k = k0 + f - r * nk;
+      const int rb = ((const __attribute__((address_space(3))) int*)rbs)[r];
+      __builtin_amdgcn_global_load_lds((const void*)(Wv + ((size_t)rb * KC + k) * 64),
+                                       (lds_void*)(dst + (size_t)f * 1024), 16, 0, 0);
+    }
+  } else {
+    const gptr<unsigned> Wv = (gptr<unsigned>)opq(W) + lane;
+    for (int f = wv - 1; f < tot; f += nw) {
+      const int r = f / nk, k = k0 + f - r * nk;
+      const int rb = ((const __attribute__((address_space(3))) int*)rbs)[r];
+      const gptr<unsigned> src = Wv + ((size_t)rb * KC + k) * 128;
+      __builtin_amdgcn_global_load_lds((const void*)src, (lds_void*)(dst + (size_t)f * 512), 4, 0, 0);
+      __builtin_amdgcn_global_load_lds((const void*)(src + 64), (lds_void*)(dst + (size_t)f * 512 + 256), 4, 0, 0);
+    }
+  }
+}
+
 // Run by waves 0..3 together: the LayerNorm rows, then the stage is
 // published (the four waves' stores complete, then wave 0 writes the flag).
+template <bool Q8>
 __device__ __forceinline__ bool do_pre(const FusedArgs& a, const Wg& w, const PreSpec& ps) {
   if (ps.kind == 0) return true;
   bool ok = true;
@@ -735,15 +781,8 @@ __device__ __forceinline__ bool do_pre(const FusedArgs& a, const Wg& w, const Pr
   if (ps.wn > 0 && threadIdx.x >= 64) {
     // (not wave 0: its polls must not wait behind these loads; the stage's
     // closing vmcnt(0) and barrier complete them before the GEMM reads them)
-    const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63, nk = ps.wk1 - ps.wk0, tot = ps.wn * nk;
-    unsigned char* lds_base = w.lds;
-    const gptr<u32x4> Wv = opq(ps.wW) + lane;
-    for (int f = wv - 1; f < tot; f += QW - 1) {
-      const int r = f / nk, k = ps.wk0 + f - r * nk;
-      const int rb = ((const __attribute__((address_space(3))) int*)ps.wrbs)[r];
-      __builtin_amdgcn_global_load_lds((const void*)(Wv + ((size_t)rb * ps.wKC + k) * 64),
-                                       (lds_void*)(lds_base + ps.wdst + (size_t)f * 1024), 16, 0, 0);
-    }
+    stage_frags<Q8>(ps.wW, ps.wrbs, ps.wn, ps.wk0, ps.wk1 - ps.wk0, ps.wKC, w.lds + ps.wdst, threadIdx.x >> 6,
+                    QW - 1);
   }
   return true;
 }
@@ -790,13 +829,16 @@ struct HeadBest {
 
 // One GEMM task of RB row blocks: rbs[0 .. nrb) (plan entries) or, with rbs
 // null, nrb consecutive ones from rb_first; row blocks past nrb repeat the
-// last one and are not stored.
-template <int NT, int RB, int U>
+// last one and are not stored.  Q8: the matrix is in 8-bit fragments (512 B,
+// widened to float16 in registers) followed by its rows' float32 scales
+// ([ceil(M / 16) 16]); each output is scaled by its row's before the bias.
+template <int NT, int RB, int U, bool Q8>
 __device__ __forceinline__ bool gemm_rb(const FusedArgs& a, const Wg& w, const WaitSpec& ws, int epi, int l,
                                         const int* rbs, int rb_first, int nrb, gptr<uint16_t> bias, gptr<u32x4> Wp,
                                         int KC, int M, int kc0, int kc1, const uint16_t* act, int act_kc,
                                         float* red, const PreSpec& ps, int wofs, HeadBest& hb, bool track) {
   constexpr int NN = 16 * NT, NCW = NWV - QW;
+  using WT = typename std::conditional<Q8, u32x2, u32x4>::type;
   // Waves 4..7 compute: wave 4 + c takes k-steps kc0 + c, kc0 + c + 4, ...,
   // and loads their weights first thing.  Waves 0..3 run the pre-stage
   // meanwhile; then wave 0, with nothing in flight, waits for this stage's
@@ -807,6 +849,7 @@ __device__ __forceinline__ bool gemm_rb(const FusedArgs& a, const Wg& w, const W
   const int cw = wv - QW;
   const int nsteps = wv >= QW && kc1 - kc0 > cw ? (kc1 - kc0 - cw + NCW - 1) / NCW : 0;
   Wp = opq(Wp);
+  const gptr<WT> Wq = (gptr<WT>)Wp;
   const gptr<uint16_t> actg = opq(act);
   bias = opq(bias);
   int rbv[RB];
@@ -823,16 +866,17 @@ __device__ __forceinline__ bool gemm_rb(const FusedArgs& a, const Wg& w, const W
   const bool has_bias = bias != nullptr;
   const gptr<uint16_t> bsrc = has_bias ? bias : (gptr<uint16_t>)Wp;
   uint16_t bias_r[RB];
-  gptr<u32x4> wb[RB];
+  float scale_r[RB];
+  gptr<WT> wb[RB];
 #pragma unroll
-  for (int r = 0; r < RB; ++r) wb[r] = Wp + (size_t)rbv[r] * KC * 64 + lane;
+  for (int r = 0; r < RB; ++r) wb[r] = Wq + (size_t)rbv[r] * KC * 64 + lane;
   const gptr<u32x4> ab = (gptr<u32x4>)actg + lane;
-  u32x4 wq[U][RB];
+  WT wq[U][RB];
   u32x4 bq[U][NT];
   const int klast = kc1 - 1;
   const int nk = kc1 - kc0;
-  const __attribute__((address_space(3))) u32x4* wl =
-      (const __attribute__((address_space(3))) u32x4*)((unsigned char*)red + wofs) + lane;
+  const __attribute__((address_space(3))) WT* wl =
+      (const __attribute__((address_space(3))) WT*)((unsigned char*)red + wofs) + lane;
   auto load_w = [&](int s, int u) {
     const int kc = min(kc0 + cw + NCW * s, klast);
     if (wofs) {
@@ -865,7 +909,7 @@ __device__ __forceinline__ bool gemm_rb(const FusedArgs& a, const Wg& w, const W
   // (the loads sit in the branch wave 0 does not take, so the weight
   // registers are not live across the pre-stage's code)
   if (wv < QW) {
-    bool ok = do_pre(a, w, ps);
+    bool ok = do_pre<Q8>(a, w, ps);
     if (wv == 0) {
       stamp(a, w, ws.sl, ws.sfid, 0);
       if (ok && ws.on) ok = poll_w0(a, w, ws.id, ws.wx, ws.tag);
@@ -884,6 +928,11 @@ __device__ __forceinline__ bool gemm_rb(const FusedArgs& a, const Wg& w, const W
   // the bias is loaded only now, so that nothing sits ahead of wave 0's polls
 #pragma unroll
   for (int r = 0; r < RB; ++r) bias_r[r] = bsrc[rbv[r] * 16 + (tid & 15)];
+  if constexpr (Q8) {
+    const gptr<float> sc = (gptr<float>)(Wq + (size_t)((M + 15) / 16) * KC * 64);
+#pragma unroll
+    for (int r = 0; r < RB; ++r) scale_r[r] = sc[rbv[r] * 16 + (tid & 15)];
+  }
 #pragma unroll
   for (int u = 0; u < U; ++u)
     if (u < nsteps) load_a(u, u);
@@ -896,8 +945,8 @@ __device__ __forceinline__ bool gemm_rb(const FusedArgs& a, const Wg& w, const W
         for (int r = 0; r < RB; ++r)
 #pragma unroll
           for (int t = 0; t < NT; ++t)
-            acc[r][t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, wq[u][r]),
-                                                               __builtin_bit_cast(f16x8, bq[u][t]), acc[r][t], 0, 0, 0);
+            acc[r][t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(wfrag(wq[u][r]), __builtin_bit_cast(f16x8, bq[u][t]),
+                                                               acc[r][t], 0, 0, 0);
       }
       __builtin_amdgcn_sched_barrier(0);
       if (s0 + u + U < nsteps) load_step(s0 + u + U, u);
@@ -926,6 +975,7 @@ __device__ __forceinline__ bool gemm_rb(const FusedArgs& a, const Wg& w, const W
       for (int ww = 1; ww < NCW; ++ww) sum += red[ww * NN * 16 + idx];
       const int o = rbv[r] * 16 + row;
       if (node < N && o < M) {
+        if constexpr (Q8) sum *= scale_r[r];
         const float y = has_bias ? sum + bf2f(bias_r[r]) : sum;
         epilogue(a, w, epi, l, node, o, y);
         if (track && (y > hb.v[i] || (y == hb.v[i] && o < hb.o[i]))) {
@@ -944,10 +994,11 @@ __device__ __forceinline__ bool gemm_rb(const FusedArgs& a, const Wg& w, const W
 // two keep 6; four row blocks keep 8 at one tile, 5 at two, 3 at four: deeper
 // would spill); three code bodies serve every stage
 // Runs the pre-stage (wave 0) when the workgroup has no GEMM task.
+template <bool Q8>
 __device__ __forceinline__ bool pre_only(const FusedArgs& a, const Wg& w, const PreSpec& ps) {
   if (ps.kind == 0) return true;
   if (threadIdx.x < QW * 64) {
-    const bool ok = do_pre(a, w, ps);
+    const bool ok = do_pre<Q8>(a, w, ps);
     if (threadIdx.x == 0) w.sh[0] = ok;
   }
   lds_barrier();
@@ -956,21 +1007,21 @@ __device__ __forceinline__ bool pre_only(const FusedArgs& a, const Wg& w, const 
   return ok;
 }
 
-template <int NT>
+template <int NT, bool Q8>
 __device__ __forceinline__ bool gemm_task(const FusedArgs& a, const Wg& w, const WaitSpec& ws, int epi, int l,
                                           const int* rbs, int rb_first, int nrb, gptr<uint16_t> bias,
                                           gptr<u32x4> Wp, int KC, int M, int kc0, int kc1, const uint16_t* act,
                                           int act_kc, float* red, const PreSpec& ps, int wofs,
                                           HeadBest& hb, bool track) {
-  if (nrb <= 0) return pre_only(a, w, ps);
+  if (nrb <= 0) return pre_only<Q8>(a, w, ps);
   if (nrb == 1)
-    return gemm_rb<NT, 1, NT <= 2 ? 10 : 8>(a, w, ws, epi, l, rbs, rb_first, 1, bias, Wp, KC, M, kc0, kc1, act,
+    return gemm_rb<NT, 1, NT <= 2 ? 10 : 8, Q8>(a, w, ws, epi, l, rbs, rb_first, 1, bias, Wp, KC, M, kc0, kc1, act,
                                            act_kc, red, ps, wofs, hb, track);
   if (nrb == 2)
-    return gemm_rb<NT, 2, NT <= 2 ? 10 : 6>(a, w, ws, epi, l, rbs, rb_first, 2, bias, Wp, KC, M, kc0, kc1, act,
+    return gemm_rb<NT, 2, NT <= 2 ? 10 : 6, Q8>(a, w, ws, epi, l, rbs, rb_first, 2, bias, Wp, KC, M, kc0, kc1, act,
                                            act_kc, red, ps, wofs, hb, track);
-  return gemm_rb<NT, 4, NT == 1 ? 8 : NT == 2 ? 5 : 3>(a, w, ws, epi, l, rbs, rb_first, nrb, bias, Wp, KC, M, kc0, kc1, act,
-                                         act_kc, red, ps, wofs, hb, track);
+  return gemm_rb<NT, 4, NT == 1 ? 8 : NT == 2 ? 5 : 3, Q8>(a, w, ws, epi, l, rbs, rb_first, nrb, bias, Wp, KC, M, kc0,
+                                                            kc1, act, act_kc, red, ps, wofs, hb, track);
 }
 
 // ------------------------------------------------------------------ tree attention
@@ -1284,7 +1335,7 @@ __device__ __forceinline__ bool att_root_unit(const FusedArgs& a, const Wg& w, c
 
 // ------------------------------------------------------------------ compute workgroups
 
-template <int NT>
+template <int NT, bool Q8>
 __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* lds) {
   int* sh = (int*)(lds + A_REGION + A_PART_BYTES + A_Q_BYTES);  // 32 words
   int* lplan = sh + 32;                                            // [kPlanStride]
@@ -1425,10 +1476,10 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
       stamp(a, w, l, fid, 0);
       const WaitSpec ws{wo ? FS_ATT : FS_FC, w.x, tag_of(w, l, wo ? FS_ATT : FS_FC), true, l, fid};
       PreSpec nopre{};
-      const bool ok = wo ? gemm_task<NT>(a, w, ws, FE_WO, l, p + PL_WO + 1, 0, n_wo, G<uint16_t>(nullptr),
+      const bool ok = wo ? gemm_task<NT, Q8>(a, w, ws, FE_WO, l, p + PL_WO + 1, 0, n_wo, G<uint16_t>(nullptr),
                                          G<u32x4>(lw(w, l, LW_O)), KCd, d, kh0, kh1, a.fo, KCd, red, nopre,
                                          wo_staged ? wo_ofs : 0, hbest, false)
-                         : gemm_task<NT>(a, w, ws, FE_WPR, l, p + PL_WPR + 1, 0, n_wpr, G<uint16_t>(nullptr),
+                         : gemm_task<NT, Q8>(a, w, ws, FE_WPR, l, p + PL_WPR + 1, 0, n_wpr, G<uint16_t>(nullptr),
                                          G<u32x4>(lw(w, l, LW_PR)), KCm, d, kf0, kf1, a.ff, KCm, red, nopre,
                                          wpr_staged ? WST : 0, hbest, false);
       if (!ok) goto out;
@@ -1439,14 +1490,8 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
         // LDS from here (waves 1..7), inside the LayerNorm's cross-XCD wait,
         // rather than after the LayerNorm's rows (measured: 3 % faster at
         // 64 nodes, neutral or slower at 32)
-        const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63, nk = kf1 - kf0, tot = n_wpr * nk;
-        const gptr<u32x4> Wv = opq(G<u32x4>(lw(w, l, LW_PR))) + lane;
-        for (int f = wv - 1; f < tot; f += NWV - 1) {
-          const int r = f / nk, k = kf0 + f - r * nk;
-          const int rb = ((const __attribute__((address_space(3))) int*)(p + PL_WPR + 1))[r];
-          __builtin_amdgcn_global_load_lds((const void*)(Wv + ((size_t)rb * KCm + k) * 64),
-                                           (lds_void*)(lds + WST + (size_t)f * 1024), 16, 0, 0);
-        }
+        stage_frags<Q8>(G<u32x4>(lw(w, l, LW_PR)), p + PL_WPR + 1, n_wpr, kf0, kf1 - kf0, KCm, lds + WST,
+                        threadIdx.x >> 6, NWV - 1);
       }
       continue;
     }
@@ -1513,7 +1558,7 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
       // (the first QKV stage waits for every XCD's first LayerNorm, which
       // clears the first two sum buffers: see xs_zero)
       const WaitSpec gws{ps.fid, (kind == 0 && l == 0) ? -1 : w.x, tag_of(w, l, ps.fid), true, l, gfid};
-      if (!gemm_task<NT>(a, w, gws, epi, l, rbs, rb_first, nrb, bias, Wm, KCd, Mo, k0, k1, act, KCd, red, ps, 0,
+      if (!gemm_task<NT, Q8>(a, w, gws, epi, l, rbs, rb_first, nrb, bias, Wm, KCd, Mo, k0, k1, act, KCd, red, ps, 0,
                          hbest, kind == 8))
         goto out;
     }
@@ -1522,7 +1567,7 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
       const WaitSpec none{0, 0, 0u, false, l, gfid};
       PreSpec nopre{};
       for (int b0 = hb0 + 4, j = 1; b0 < hb1; b0 += 4, ++j) {
-        if (!gemm_task<NT>(a, w, none, FE_HEAD, L, nullptr, b0, min(4, hb1 - b0), G<uint16_t>(nullptr),
+        if (!gemm_task<NT, Q8>(a, w, none, FE_HEAD, L, nullptr, b0, min(4, hb1 - b0), G<uint16_t>(nullptr),
                            G<u32x4>(a.p_head), KCd, a.V, 0, KCd, act1, KCd, red, nopre, 0, hbest, true))
           goto out;
       }
@@ -1563,10 +1608,10 @@ out:
 }
 
 
-template <int NT>
+template <int NT, bool Q8>
 __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(2))) void pass_kernel(FusedArgs a) {
   extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
-  compute_wg<NT>(a, lds);
+  compute_wg<NT, Q8>(a, lds);
 }
 
 }  // namespace fz
@@ -1692,11 +1737,12 @@ bool fused_plan(int H, int d, int M, int V, int ntiles, int* tab, int* xh, int* 
 
 hipError_t fused_prepare() {
   const int lds = (int)fused_lds_bytes(kFMaxL);
-  hipError_t e = hipFuncSetAttribute((const void*)fz::pass_kernel<1>, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
-  if (e == hipSuccess)
-    e = hipFuncSetAttribute((const void*)fz::pass_kernel<2>, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
-  if (e == hipSuccess)
-    e = hipFuncSetAttribute((const void*)fz::pass_kernel<4>, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+  const void* fns[6] = {(const void*)fz::pass_kernel<1, false>, (const void*)fz::pass_kernel<2, false>,
+                        (const void*)fz::pass_kernel<4, false>, (const void*)fz::pass_kernel<1, true>,
+                        (const void*)fz::pass_kernel<2, true>,  (const void*)fz::pass_kernel<4, true>};
+  hipError_t e = hipSuccess;
+  for (int i = 0; i < 6 && e == hipSuccess; ++i)
+    e = hipFuncSetAttribute(fns[i], hipFuncAttributeMaxDynamicSharedMemorySize, lds);
   return e;
 }
 
@@ -1715,10 +1761,18 @@ hipError_t launch_fused(const FusedArgs& a, hipStream_t s) {
   const int nt = (a.N + 15) / 16;
   const size_t lds = fused_lds_bytes(a.L);
   const dim3 grid(kFGroups);
-  switch (nt) {
-    case 1: fz::pass_kernel<1><<<grid, fz::NTH, lds, s>>>(a); break;
-    case 2: fz::pass_kernel<2><<<grid, fz::NTH, lds, s>>>(a); break;
-    default: fz::pass_kernel<4><<<grid, fz::NTH, lds, s>>>(a); break;
+  if (a.q8) {
+    switch (nt) {
+      case 1: fz::pass_kernel<1, true><<<grid, fz::NTH, lds, s>>>(a); break;
+      case 2: fz::pass_kernel<2, true><<<grid, fz::NTH, lds, s>>>(a); break;
+      default: fz::pass_kernel<4, true><<<grid, fz::NTH, lds, s>>>(a); break;
+    }
+  } else {
+    switch (nt) {
+      case 1: fz::pass_kernel<1, false><<<grid, fz::NTH, lds, s>>>(a); break;
+      case 2: fz::pass_kernel<2, false><<<grid, fz::NTH, lds, s>>>(a); break;
+      default: fz::pass_kernel<4, false><<<grid, fz::NTH, lds, s>>>(a); break;
+    }
   }
   return hipGetLastError();
 }

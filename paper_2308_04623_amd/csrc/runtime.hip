@@ -485,7 +485,7 @@ static ssd_status fused_setup(ssd_kv* kv) {
 
 // whether a verification pass of model m over n nodes runs as the persistent single launch
 static bool use_fused(const ssd_model* m, const ssd_kv* kv, int n) {
-  if (kv->pass_mode == 1 || m->f32 || m->q8 || !kv->fz_ok || !m->ftab) return false;
+  if (kv->pass_mode == 1 || m->f32 || !kv->fz_ok || !m->ftab) return false;
   // the persistent pass is forced, or chosen where it is the faster one
   // (measured on the GPT-2-L shape: at every node count it supports)
   return kv->pass_mode == 2 ? n <= kFMaxN : n <= kFAutoMaxN;
@@ -783,6 +783,7 @@ static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int3
     a.lnf_g = (const uint16_t*)m->lnf_g;
     a.lnf_b = (const uint16_t*)m->lnf_b;
     a.p_head = m->p_head;
+    a.q8 = m->q8 ? 1 : 0;
     a.L = L;
     a.d = d;
     a.H = H;

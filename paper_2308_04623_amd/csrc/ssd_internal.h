@@ -257,6 +257,7 @@ struct FusedArgs {
   unsigned* err;            // session error counter
   unsigned long long timeout;  // s_memrealtime ticks (100 MHz) before a wait gives up
   unsigned long long* trace;  // stage timestamps [kFGroups][L + 1][kFStages][3], or nullptr
+  int q8;                   // 8-bit weights: each packed matrix is 8-bit fragments followed by its row scales
 };
 
 // Work split of the fused pass for a model shape and 16-node tile count:

@@ -56,8 +56,12 @@ def lds_bytes(L):
     return A_REGION + A_PART + A_Q + 128 + PLAN_STRIDE * 4 + L * LW_SLOTS * 8 + WO_FRAGS * 1024
 
 
-def check_pass(H, d, M, V, L, N, P, max_ctx, max_nodes):
+def check_pass(H, d, M, V, L, N, P, max_ctx, max_nodes, q8=False):
+    """q8: 8-bit weights (fragments of 512 B, indexed in 8-byte lane slots
+    like the float16 ones in 16-byte slots, followed by one float32 scale per
+    row of the 16-row blocks; staged into LDS by two 4-byte copies each)."""
     c = Check()
+    FB = 512 if q8 else 1024                        # fragment bytes
     nt = (N + 15) // 16
     NT = 1 if nt == 1 else 2 if nt == 2 else 4          # the kernel template serving nt tiles
     tab, xh, xf = ssd.fused_plan(H, d, M, V, nt)
@@ -96,7 +100,8 @@ def check_pass(H, d, M, V, L, N, P, max_ctx, max_nodes):
                           (b * MAXN + n) * d + (x + 1) * (d // 8) - 1, sizes["xacc"])
                 c.rng(f"{tag} act row", act_base + act_index(n, 0, KCd), act_base + act_index(n, d - 4, KCd) + 3,
                       sizes["act"])
-            # GEMM tasks: weights of each row block, activation fragments of every tile
+            # GEMM tasks: weights of each row block, activation fragments of
+            # every tile (and the 8-bit copies' row scales)
             for slot, wname, kc0, kc1, KC, actn, rows_out in (
                     (PL_QKV, "w_qkv", 0, KCd, KCd, "act", 3 * d), (PL_WO, "w_o", kh0, kh1, KCd, "fo", d),
                     (PL_FC, "w_fc", 0, KCd, KCd, "act", M), (PL_WPR, "w_pr", kf0, kf1, KCm, "ff", d)):
@@ -105,6 +110,9 @@ def check_pass(H, d, M, V, L, N, P, max_ctx, max_nodes):
                     continue
                 rbs = row[slot + 1:slot + 1 + nrb]
                 c.rng(f"{tag} {wname} row blocks", int(rbs.min()) * 16, int(rbs.max()) * 16 + 15, rows_out)
+                if q8:
+                    c.rng(f"{tag} {wname} scales", int(rbs.min()) * 16, int(rbs.max()) * 16 + 15,
+                          sizes[wname] // (KC * 64) * 16)
                 if kc1 > kc0:
                     c.rng(f"{tag} {wname} fragments", (int(rbs.min()) * KC + kc0) * 64,
                           (int(rbs.max()) * KC + kc1 - 1) * 64 + 63, sizes[wname])
@@ -128,12 +136,20 @@ def check_pass(H, d, M, V, L, N, P, max_ctx, max_nodes):
                     c.rng(f"{tag} ff out", act_index(0, o_lo, KCm), act_index(N - 1, o_hi, KCm), sizes["ff"])
             # staged weights in LDS
             n_wo, n_wpr = row[PL_WO], row[PL_WPR]
+            # (the copies' sources, in 4-byte words: (rb KC + k) FB / 4 + lane
+            # (+ 64 for the second half of an 8-bit fragment))
             if NT >= 2 and n_wo > 0 and n_wo * (kh1 - kh0) <= WO_FRAGS:
                 ofs = A_REGION + A_PART + A_Q + 256 + L * LW_SLOTS * 8
-                c.rng(f"{tag} staged W_o (LDS)", ofs, ofs + n_wo * (kh1 - kh0) * 1024 - 1, lds_bytes(L))
+                c.rng(f"{tag} staged W_o (LDS)", ofs, ofs + n_wo * (kh1 - kh0) * FB - 1, lds_bytes(L))
+                rbs = row[PL_WO + 1:PL_WO + 1 + n_wo]
+                c.rng(f"{tag} staged W_o sources", (int(rbs.min()) * KCd + kh0) * FB // 4,
+                      (int(rbs.max()) * KCd + kh1 - 1) * FB // 4 + FB // 4 - 1, sizes["w_o"] * FB // 4 // 64)
             if NT >= 2 and n_wpr > 0 and n_wpr * (kf1 - kf0) <= WST_FRAGS:
-                c.rng(f"{tag} staged W_pr (LDS)", WST, WST + n_wpr * (kf1 - kf0) * 1024 - 1,
+                c.rng(f"{tag} staged W_pr (LDS)", WST, WST + n_wpr * (kf1 - kf0) * FB - 1,
                       A_REGION + A_PART + A_Q)
+                rbs = row[PL_WPR + 1:PL_WPR + 1 + n_wpr]
+                c.rng(f"{tag} staged W_pr sources", (int(rbs.min()) * KCm + kf0) * FB // 4,
+                      (int(rbs.max()) * KCm + kf1 - 1) * FB // 4 + FB // 4 - 1, sizes["w_pr"] * FB // 4 // 64)
             # attention units dealt to this rank
             for u in range(row[PL_ATT], n_attu, RANKS):
                 if n_attu <= RANKS:
@@ -168,6 +184,8 @@ def check_pass(H, d, M, V, L, N, P, max_ctx, max_nodes):
             hb0, hb1 = row[PL_HEAD], row[PL_HEAD + 1]
             if hb1 > hb0:
                 c.rng(f"{tag} head fragments", hb0 * KCd * 64, (hb1 - 1) * KCd * 64 + KCd * 64 - 1, sizes["head"])
+                if q8:
+                    c.rng(f"{tag} head scales", hb0 * 16, (hb1 - 1) * 16 + 15, ((V + 15) // 16) * 16)
                 c.rng(f"{tag} logits", hb0 * 16, (N - 1) * V + min(hb1 * 16, V) - 1, sizes["logits"])
         want = sorted((hl, tt, pp) for hl in range(nhx) for tt in range(nt) for pp in range(S + 1))
         if sorted(dealt) != want:
@@ -179,14 +197,15 @@ SHAPES = {"small": (4, 256, 1024, 2000, 3), "gpt2l": (20, 1280, 5120, 50257, 36)
           "gpt2m": (16, 1024, 4096, 50257, 24), "gpt2xl": (25, 1600, 6400, 50257, 48)}
 
 
+@pytest.mark.parametrize("q8", [False, True])
 @pytest.mark.parametrize("shape", list(SHAPES))
 @pytest.mark.parametrize("P", [0, 64, 200, 512, 1500, 5000])
-def test_persistent_pass_accesses_stay_in_bounds(shape, P):
+def test_persistent_pass_accesses_stay_in_bounds(shape, P, q8):
     H, d, M, V, L = SHAPES[shape]
     max_ctx, max_nodes = P + 128, 64
     bad = []
     for N in list(range(1, 18)) + [31, 32, 33, 47, 48, 49, 63, 64]:
-        bad += [f"N={N}: {b}" for b in check_pass(H, d, M, V, L, N, P, max_ctx, max_nodes)]
+        bad += [f"N={N}: {b}" for b in check_pass(H, d, M, V, L, N, P, max_ctx, max_nodes, q8)]
     assert not bad, bad[:10]
 
 

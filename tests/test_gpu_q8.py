@@ -199,3 +199,97 @@ def test_q8_error_paths(ssd, torch):
         assert e.value.status == ssd.E_INVALID_ARG
     m16.close()
     m8.close()
+
+
+# ---- the persistent single-launch pass (head dimension 64, <= 64 nodes)
+
+SMALL = W.GPT2Config(n_layer=3, d_model=256, n_head=4, d_mlp=1024, vocab=2000, n_pos=512, dtype="bf16")
+
+
+class Q8Small:
+    def __init__(self, ssd, P=200, max_ctx=320, max_nodes=64):
+        self.cfg = cfg = SMALL
+        self.w = W.make_weights(cfg, 0, perturb_affine=True)
+        self.om = oracle.Model(cfg, self.w, q8=True)
+        self.P, self.max_ctx, self.max_nodes = P, max_ctx, max_nodes
+        self.kc, self.vc = W.random_kv_cache(cfg, max_ctx, P, seed=3)
+        self.m = ssd.Model(cfg, self.w, q8=True)
+        self.s = ssd.Session(self.m, max_ctx, max_nodes, ssd.to_device(self.kc, cfg), ssd.to_device(self.vc, cfg))
+
+    def oracle_verify(self, toks, parents, P):
+        kt, vt = self.om.kv(self.max_nodes), self.om.kv(self.max_nodes)
+        return oracle.tree_verify(self.om, self.kc, self.vc, P, toks, parents, kt, vt), kt, vt
+
+
+@pytest.fixture(scope="module")
+def sq(ssd):
+    return Q8Small(ssd)
+
+
+def _rand_tree(seed, n):
+    g = np.random.default_rng(seed)
+    return np.array([-1] + [int(g.integers(max(0, i - 8), i)) for i in range(1, n)], np.int32)
+
+
+FTREES = {"single": np.array([-1], np.int32), "binary15": W.complete_binary_tree(15), "chain17": W.chain_tree(17),
+          "branch32": W.branching_tree([4, 2, 2, 1], 32), "random33": _rand_tree(1, 33),
+          "random48": _rand_tree(2, 48), "random64": _rand_tree(3, 64)}
+
+
+@pytest.mark.parametrize("name", list(FTREES))
+@pytest.mark.parametrize("P", [0, 64, 200])
+def test_q8_fused_verify_matches_oracle(sq, ssd, torch, name, P):
+    par = FTREES[name]
+    toks = W.tree_tokens(par, sq.cfg.vocab, seed=len(par) + P)
+    print(f"8-bit fused verify {name} P={P}", flush=True)
+    ref, kt, vt = sq.oracle_verify(toks, par, P)
+    with sq.s.options(pass_mode=ssd.PASS_FUSED):
+        assert sq.s.verify_path(len(par)) == ssd.PASS_FUSED
+        lg = sq.s.verify(P, toks, par)
+        torch.cuda.synchronize()
+    assert sq.s.error_count() == 0
+    got = lg.cpu().numpy()
+    assert np.abs(got - ref).max() < TOL
+    n = len(par)
+    for a, b in ((sq.s.k_tree, kt), (sq.s.v_tree, vt)):
+        g = W.bf16_bits_to_f32(ssd.to_host_bits(a)[:, :, :n])
+        assert np.abs(g - W.bf16_bits_to_f32(b[:, :, :n])).max() < TOL
+    path, plen, nxt = sq.s.accept(toks, par, lg)
+    op, on = oracle.tree_accept(oracle.GREEDY, toks, par, got)
+    assert path[:int(plen.item())].cpu().numpy().tolist() == op.tolist() and int(nxt.item()) == on
+
+
+def test_q8_fused_replay_greedy_and_kernel_path(sq, ssd, torch):
+    """The 8-bit persistent pass: bitwise repeatable eagerly and from a
+    captured graph; its verify + greedy step equals verify then accept bit
+    for bit; the per-sub-layer path agrees with it within the bar."""
+    par = FTREES["random64"]
+    toks = W.tree_tokens(par, sq.cfg.vocab, seed=9)
+    ref, _, _ = sq.oracle_verify(toks, par, sq.P)
+    with sq.s.options(pass_mode=ssd.PASS_FUSED):
+        a = sq.s.verify(sq.P, toks, par).clone()
+        b = sq.s.verify(sq.P, toks, par).clone()
+        torch.cuda.synchronize()
+        assert torch.equal(a, b)
+        out = torch.zeros_like(a)
+        g = sq.s.capture_verify(sq.P, toks, par, out)
+        other = W.tree_tokens(FTREES["binary15"], sq.cfg.vocab, seed=1)
+        for _ in range(3):
+            out.zero_()
+            g.launch()
+            torch.cuda.synchronize()
+            assert torch.equal(out, a)
+            sq.s.verify(sq.P, other, FTREES["binary15"])
+            torch.cuda.synchronize()
+        g.close()
+        pa, la, na = sq.s.accept(toks, par, a)
+        lg_b, pb, lb, nb = sq.s.verify_greedy(sq.P, toks, par)
+        torch.cuda.synchronize()
+        assert torch.equal(a, lg_b)
+        n = int(la.item())
+        assert int(lb.item()) == n and pa[:n].tolist() == pb[:n].tolist() and int(na.item()) == int(nb.item())
+    with sq.s.options(pass_mode=ssd.PASS_KERNELS):
+        k = sq.s.verify(sq.P, toks, par).cpu().numpy()
+    assert np.abs(k - ref).max() < TOL
+    assert np.abs(a.cpu().numpy() - ref).max() < TOL
+    assert sq.s.error_count() == 0

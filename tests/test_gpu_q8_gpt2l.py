@@ -6,8 +6,9 @@ pass, default pass mode).
 - Codes and scales of the LM head and of the first and last layers' MLP
   matrices bit-exact.
 - Every row and every logit (2e-2 max-abs) at 32 nodes ([4,2,2,1]) over a
-  512-token prefix and at 128 nodes (a best-first tree), the session's error
-  counter at 0, greedy accept bit-exact on the GPU's logits.
+  512-token prefix, 64 nodes over 1024 (both the persistent pass) and 128
+  nodes over 512 (one kernel per sub-layer), best-first trees; the
+  session's error counter at 0; greedy accept bit-exact on the GPU's logits.
 The prefix caches are synthetic N(0, 0.7) K/V."""
 import os
 
@@ -56,6 +57,8 @@ def _check_tree(big, torch, P, toks, par, max_nodes, seed):
     cfg, om, m, ssd = big
     kc, vc = W.random_kv_cache(cfg, P + 64, P, seed=seed)
     s = ssd.Session(m, P + 64, max_nodes, ssd.to_device(kc, cfg), ssd.to_device(vc, cfg))
+    # (the persistent pass up to 64 nodes, one kernel per sub-layer above)
+    assert s.verify_path(len(par)) == (ssd.PASS_FUSED if len(par) <= 64 else ssd.PASS_KERNELS)
     lg = torch.zeros((len(par), cfg.vocab), dtype=torch.float32, device="cuda")
     g = s.capture_verify(P, toks, par, lg)
     g.launch()
@@ -79,6 +82,13 @@ def test_gpt2l_q8_c2_full_tree(big, torch):
     par = W.branching_tree([4, 2, 2, 1], 32)
     toks = W.tree_tokens(par, cfg.vocab, seed=2)
     _check_tree(big, torch, 512, toks, par, 64, seed=3)
+
+
+def test_gpt2l_q8_64_nodes_full_tree(big, torch):
+    cfg = big[0]
+    toks, par = W.best_first_tree(64, seed=5, vocab=cfg.vocab)
+    toks[0] = 23
+    _check_tree(big, torch, 1024, toks, par, 64, seed=6)
 
 
 def test_gpt2l_q8_128_nodes_full_tree(big, torch):
