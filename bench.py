@@ -39,15 +39,20 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def pass_bytes(cfg, n, P):
+def pass_bytes(cfg, n, P, q8=False):
     """Algorithmic HBM bytes of one verification pass: every parameter once
     (matrices, tied LM head, vectors; the embedding rows gathered are
     negligible), the prefix K/V once, the tree K/V written once and the
-    float32 logits written once."""
+    float32 logits written once.  q8: the matrices and the LM head as 8-bit
+    codes plus one float32 scale per row (rows padded to 16)."""
     d, m, L, V = cfg.d_model, cfg.d_mlp, cfg.n_layer, cfg.vocab
     es = 2 if cfg.dtype == "bf16" else 4
     mats = L * (3 * d * d + d * d + m * d + d * m) * es
     head = V * d * es
+    if q8:
+        pad = lambda r: (r + 15) // 16 * 16
+        mats = L * (3 * d * d + d * d + m * d + d * m) + L * 4 * (pad(3 * d) + pad(d) + pad(m) + pad(d))
+        head = V * d + 4 * pad(V)
     vecs = (L * (2 * d + 3 * d + d + 2 * d + m + d) + 2 * d) * es
     kv_row = L * 2 * d * es
     return mats + head + vecs + kv_row * P + (kv_row + V * 4) * n
@@ -398,6 +403,8 @@ def main():
     ap.add_argument("--mfma-from", nargs=2, metavar=("COUNTER_DIR", "TRACE_DIR"),
                     help="summarise a rocprofv3 --pmc MfmaUtil MfmaFlopsF16 run and a --kernel-trace --stats -f csv "
                          "run of the same command into profiles/mfma_gemm_n{nodes}_p{prefix}.md; no GPU needed")
+    ap.add_argument("--q8", action="store_true",
+                    help="run the timed step (and the probe modes) on the 8-bit weight model of the same weights")
     ap.add_argument("--kernels-path", action="store_true",
                     help="with --traffic-from: the counters are of the one-kernel-per-sub-layer path's GEMM")
     args = ap.parse_args()
@@ -433,7 +440,7 @@ def main():
     max_ctx, max_nodes = cached + 64, max(128, N)
     log("generating GPT-2-L weights")
     w = W.make_weights(cfg, 0)
-    model = ssd.Model(cfg, w)
+    model = ssd.Model(cfg, w, q8=args.q8)
     kc, vc = W.random_kv_cache(cfg, max_ctx, cached, seed=3)
     sess = ssd.Session(model, max_ctx, max_nodes, ssd.to_device(kc, cfg), ssd.to_device(vc, cfg))
     par = W.branching_tree([4, 2, 2, 1], N)
@@ -522,7 +529,7 @@ def main():
     us_pass = time_graph(graph, max(args.steps, 50))
     us_step_graph = time_graph(graph_step, 50)
     us_accept_logits = time_calls(lambda: sess.accept(toks, par, logits, out=outs), 50)
-    B = pass_bytes(cfg, N, P)
+    B = pass_bytes(cfg, N, P, args.q8)
     log(f"verify pass {us_pass:.1f} us, {B / us_pass / 1e3:.0f} GB/s; pass + greedy accept {us_step_graph:.1f} us; "
         f"accept from the logits {us_accept_logits:.1f} us")
     if sess.error_count():
@@ -534,15 +541,17 @@ def main():
         # algorithmic bytes are the pass's and its duration the graph
         # replays' on the stream they run on
         roofline = {"bound": "hbm", "achieved": round(B / us_pass / 1e3, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                    "frac": round(B / us_pass / 1e3 / PEAK_HBM_GBS, 4), "traffic": stored_traffic(True, N),
+                    "frac": round(B / us_pass / 1e3 / PEAK_HBM_GBS, 4),
+                    "traffic": None if args.q8 else stored_traffic(True, N),
                     "kernel": f"ssd::fz::pass_kernel<{min((N + 15) // 16, 2) if N <= 32 else 4}> "
                               "(persistent single-launch verification pass)",
                     "bytes_per_launch": B, "us_per_launch": round(us_pass, 2)}
     else:
         roofline = fc_gemm_roofline(sess, cfg, N, stream)
 
-    def pass_point(n_s, p_s, s_=None, **opts):
+    def pass_point(n_s, p_s, s_=None, q8=None, **opts):
         s_ = s_ or sess
+        q8 = args.q8 if q8 is None else q8
         tt, pp = W.best_first_tree(n_s, seed=3, vocab=cfg.vocab)
         tt[0] = int(toks[0])
         lg = torch.empty((n_s, cfg.vocab), dtype=torch.float32, device="cuda")
@@ -551,7 +560,7 @@ def main():
             g = s_.capture_verify(p_s, tt, pp, lg)
             us = time_graph(g, 30)
             g.close()
-        bb = pass_bytes(cfg, n_s, p_s)
+        bb = pass_bytes(cfg, n_s, p_s, q8)
         return {"nodes": n_s, "prefix": p_s, "us": round(us, 1), "GB/s": round(bb / us / 1e3, 1),
                 "frac": round(bb / us / 1e3 / PEAK_HBM_GBS, 4),
                 "path": "persistent" if path == ssd.PASS_FUSED else "per-sub-layer"}
@@ -608,7 +617,7 @@ def main():
                          ("chosen_top50", dict(mode=ssd.SAMPLE_DET, top_k=50)),
                          ("greedy", dict())):
             acc[name] = round(time_calls(lambda: s5.accept(tok5, par5, lg5, out=out5, seed=3, **kw), 10), 1)
-        b5 = pass_bytes(cfg, n5, p5)
+        b5 = pass_bytes(cfg, n5, p5, args.q8)
         stress = {"workload": "256-node tree (branching 8,4,2,2,1 cut at 256), 2048-token prefix, T=1 rejection "
                               "sampling over 50257 tokens, draft = 0.5 softmax + 0.5 Dirichlet(0.1)",
                   "verify_us": round(us5, 1), "GB/s": round(b5 / us5 / 1e3, 1),
@@ -620,6 +629,62 @@ def main():
         g5.close()
         s5.close()
 
+    w8 = None
+    if not args.no_sweep and not args.q8:
+        # the same weights as 8-bit codes (ssd_model_create_q8): the pass at
+        # five points on both models, the timed step at this workload, and
+        # how far the 8-bit model's logits sit from the bfloat16 model's
+        m8 = ssd.Model(cfg, w, q8=True)
+        s8 = ssd.Session(m8, max_ctx, max_nodes, ssd.to_device(kc, cfg), ssd.to_device(vc, cfg))
+        pts8 = []
+        for n_s, p_s in ((1, 512), (32, 512), (64, 512), (128, 512)):
+            a16, a8 = pass_point(n_s, p_s), pass_point(n_s, p_s, s_=s8, q8=True)
+            pts8.append({"nodes": n_s, "prefix": p_s, "us_16bit": a16["us"], "us_8bit": a8["us"],
+                         "GB/s_8bit": a8["GB/s"], "frac_8bit": a8["frac"], "path": a8["path"]})
+        kc6, vc6 = W.random_kv_cache(cfg, 2048 + 8, 2048, seed=5)
+        s86 = ssd.Session(m8, 2048 + 8, 256, ssd.to_device(kc6, cfg), ssd.to_device(vc6, cfg))
+        s16 = ssd.Session(model, 2048 + 8, 256, ssd.to_device(kc6, cfg), ssd.to_device(vc6, cfg))
+        a16, a8 = pass_point(256, 2048, s_=s16), pass_point(256, 2048, s_=s86, q8=True)
+        pts8.append({"nodes": 256, "prefix": 2048, "us_16bit": a16["us"], "us_8bit": a8["us"],
+                     "GB/s_8bit": a8["GB/s"], "frac_8bit": a8["frac"], "path": a8["path"]})
+        s86.close()
+        s16.close()
+        lg8 = torch.empty_like(logits)
+        outs8 = tuple(torch.zeros_like(o) for o in outs)
+        g8 = s8.capture_verify_greedy(P, toks, par, lg8, outs8)
+
+        def step8():
+            g8.launch()
+            s8.commit(P, outs8[0], outs8[1])
+
+        for _ in range(args.warmup):
+            step8()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(args.steps):
+            step8()
+        b.record(stream)
+        torch.cuda.synchronize()
+        ms8 = a.elapsed_time(b) / args.steps
+        g8.close()
+        lg16 = sess.verify(P, toks, par).cpu().numpy()
+        lq = s8.verify(P, toks, par).cpu().numpy()
+        srt = np.sort(lg16, 1)
+        if s8.error_count():
+            raise SystemExit("the 8-bit session's error counter grew")
+        w8 = {"workload": "the same GPT-2-L weights as symmetric 8-bit codes with a float32 scale per row "
+                          "(matrices and LM head; float16 activations, float32 accumulation as in the "
+                          "16-bit model)",
+              "value": round(N / (ms8 * 1e-3), 1), "ms_per_step": round(ms8, 4),
+              "pass_bytes_8bit": pass_bytes(cfg, N, P, True), "points": pts8,
+              "max_abs_logit_change_vs_16bit": round(float(np.abs(lq - lg16).max()), 4),
+              "greedy_tokens_equal_vs_16bit": int((lq.argmax(1) == lg16.argmax(1)).sum()),
+              "greedy_tokens_compared": int(N), "top2_gap_median_16bit": round(float(np.median(srt[:, -1] - srt[:, -2])), 4)}
+        log(f"8-bit weights: step {ms8 * 1e3:.1f} us; points {pts8}")
+        s8.close()
+        m8.close()
+
     e2e = None
     if not args.no_e2e:
         e2e = end_to_end(ssd, W, cfg, model, N_NEW=256, PROMPT=128)
@@ -628,7 +693,7 @@ def main():
     if not args.no_cpu_baseline:
         import oracle
         threads = int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or (os.cpu_count() or 1)
-        om = oracle.Model(cfg, w)
+        om = oracle.Model(cfg, w, q8=args.q8)
         okt, ovt = om.kv(max_nodes), om.kv(max_nodes)
 
         def oracle_time(n_s, p_s, tt, pp, budget, reps):
@@ -670,9 +735,10 @@ def main():
     line = {
         "metric": METRIC, "value": round(value, 1), "unit": "verified tree tokens/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "scaling": "weak", "vs_baseline": None, "dtype": "int8" if args.q8 else "bf16", "data": "synthetic",
         "config": {"workload": f"GPT-2-L shape tree verification, {N}-node tree (branching 4,2,2,1), "
-                               f"{P}-token prefix, greedy accept + commit",
+                               f"{P}-token prefix, greedy accept + commit"
+                               + (", 8-bit weights (symmetric codes, float32 row scales)" if args.q8 else ""),
                    "nodes": N, "prefix": P, "layers": cfg.n_layer, "d_model": cfg.d_model, "vocab": cfg.vocab},
         "verify_path": "persistent single launch" if fused else "one kernel per sub-layer",
         "us_per_verify_pass": round(us_pass, 2),
@@ -687,6 +753,7 @@ def main():
         "sweep": sweep,
         "sweep_summary": crossover,
         "stress": stress,
+        "weights_8bit": w8,
     }
     print(json.dumps(line), flush=True)
 

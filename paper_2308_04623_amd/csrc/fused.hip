@@ -725,8 +725,8 @@ constexpr int WO_FRAGS = 24;  // the out-projection's staged fragments, above th
 // rbs[f / nk] (an LDS list), k-step k0 + f % nk of a matrix of KC k-steps)
 // into LDS at dst + f * fragment bytes, by waves 1.. of a stage (nw of them).
 // float16 fragments (1 KB) take one 16-byte copy per lane; 8-bit fragments
-// (512 B) two 4-byte copies, of their first and second 256 bytes, so the LDS
-// image equals the fragment either way.
+// (512 B) go two at a time (see below), so the LDS image equals the
+// fragments either way.
 template <bool Q8>
 __device__ __forceinline__ void stage_frags(gptr<u32x4> W, const int* rbs, int n, int k0, int nk, int KC,
                                             unsigned char* dst, int wv, int nw) {
@@ -740,13 +740,24 @@ __device__ __forceinline__ void stage_frags(gptr<u32x4> W, const int* rbs, int n
                                        (lds_void*)(dst + (size_t)f * 1024), 16, 0, 0);
     }
   } else {
-    const gptr<unsigned> Wv = (gptr<unsigned>)opq(W) + lane;
-    for (int f = wv - 1; f < tot; f += nw) {
-      const int r = f / nk, k = k0 + f - r * nk;
+    // two consecutive k-steps of a row block are 1 KB contiguous in memory
+    // and in LDS: one 16-byte copy per lane; an odd last k-step of a row
+    // block goes as two 4-byte copies
+    const int np = nk >> 1, per = np + (nk & 1);
+    const gptr<u32x4> W16 = opq(W) + lane;
+    const gptr<unsigned> W4 = (gptr<unsigned>)opq(W) + lane;
+    (void)tot;
+    for (int c = wv - 1; c < n * per; c += nw) {
+      const int r = c / per, j = c - r * per, k = k0 + 2 * j;
       const int rb = ((const __attribute__((address_space(3))) int*)rbs)[r];
-      const gptr<unsigned> src = Wv + ((size_t)rb * KC + k) * 128;
-      __builtin_amdgcn_global_load_lds((const void*)src, (lds_void*)(dst + (size_t)f * 512), 4, 0, 0);
-      __builtin_amdgcn_global_load_lds((const void*)(src + 64), (lds_void*)(dst + (size_t)f * 512 + 256), 4, 0, 0);
+      unsigned char* d = dst + (size_t)(r * nk + 2 * j) * 512;
+      if (j < np) {
+        __builtin_amdgcn_global_load_lds((const void*)(W16 + ((size_t)rb * KC + k) * 32), (lds_void*)d, 16, 0, 0);
+      } else {
+        const gptr<unsigned> src = W4 + ((size_t)rb * KC + k) * 128;
+        __builtin_amdgcn_global_load_lds((const void*)src, (lds_void*)d, 4, 0, 0);
+        __builtin_amdgcn_global_load_lds((const void*)(src + 64), (lds_void*)(d + 256), 4, 0, 0);
+      }
     }
   }
 }
