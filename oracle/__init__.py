@@ -24,7 +24,7 @@ GCC_CMD = ["gcc", "-O3", "-std=c11", "-D_GNU_SOURCE", "-fopenmp", "-fPIC", "-sha
            "-ffp-contract=off", "-fno-fast-math", "-Wall", "-Wextra", "-o", _SO, _SRC, "-lm"]
 
 F32, BF16 = 0, 1
-GREEDY, SAMPLE_WOR, SAMPLE_IID, SAMPLE_DET = 0, 1, 2, 3
+GREEDY, SAMPLE_WOR, SAMPLE_IID, SAMPLE_DET, SAMPLE_CDF = 0, 1, 2, 3, 4
 _ERR = {-1: "invalid argument", -2: "invalid tree", -3: "capacity exceeded"}
 
 LAYER_TENSORS = ("ln1_g", "ln1_b", "w_qkv", "b_qkv", "w_o", "b_o",

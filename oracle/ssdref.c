@@ -492,9 +492,9 @@ int ssdref_tree_accept_k(int32_t mode, const int32_t *tokens, const int32_t *par
   if (!tokens || !parent_idx || !logits || !path || !path_len || !next_token) return SSDREF_E_ARG;
   if (n_nodes <= 0 || vocab <= 0 || top_k < 0) return SSDREF_E_ARG;
   if (mode != SSDREF_ACCEPT_GREEDY && mode != SSDREF_ACCEPT_SAMPLE_WOR && mode != SSDREF_ACCEPT_SAMPLE_IID &&
-      mode != SSDREF_ACCEPT_SAMPLE_DET)
+      mode != SSDREF_ACCEPT_SAMPLE_DET && mode != SSDREF_ACCEPT_SAMPLE_CDF)
     return SSDREF_E_ARG;
-  const int det = mode == SSDREF_ACCEPT_SAMPLE_DET;
+  const int det = mode == SSDREF_ACCEPT_SAMPLE_DET || mode == SSDREF_ACCEPT_SAMPLE_CDF;
   if (mode != SSDREF_ACCEPT_GREEDY && !(temperature > 0.0)) return SSDREF_E_ARG;
   if (mode != SSDREF_ACCEPT_GREEDY && !det && !draft_probs) return SSDREF_E_ARG;
   if (det && draft_probs) return SSDREF_E_ARG;
@@ -527,6 +527,29 @@ int ssdref_tree_accept_k(int32_t mode, const int32_t *tokens, const int32_t *par
     *next_token = g[best];
     free(g);
     free(m);
+    free(depth);
+    return SSDREF_OK;
+  }
+
+  if (mode == SSDREF_ACCEPT_SAMPLE_CDF) {
+    /* inverse-CDF coupling: the oracle's token at each node from the node's
+     * own uniform, followed down the tree while a child carries it */
+    double *pc = (double *)malloc(sizeof(double) * V);
+    int32_t u = 0, len = 0, x = 0;
+    path[len++] = 0;
+    for (;;) {
+      softmax_t(logits + (size_t)u * V, V, temperature, top_k, pc);
+      x = sample_cdf(pc, V, 1.0, ssdref_uniform(seed, 2, (uint64_t)u));
+      int32_t child = -1;
+      for (int32_t c = u + 1; c < n && child < 0; ++c)
+        if (parent_idx[c] == u && tokens[c] == x) child = c;
+      if (child < 0) break;
+      path[len++] = child;
+      u = child;
+    }
+    *next_token = x;
+    *path_len = len;
+    free(pc);
     free(depth);
     return SSDREF_OK;
   }

@@ -58,6 +58,7 @@ extern "C" {
 #define SSDREF_ACCEPT_SAMPLE_WOR 1 /* siblings were drawn without replacement */
 #define SSDREF_ACCEPT_SAMPLE_IID 2 /* siblings were drawn independently      */
 #define SSDREF_ACCEPT_SAMPLE_DET 3 /* siblings were chosen, not drawn (e.g. the draft's top tokens) */
+#define SSDREF_ACCEPT_SAMPLE_CDF 4 /* uniforms drawn first, one per node; inverse-CDF coupling */
 
 typedef struct {
   int32_t n_layer, d_model, n_head, d_mlp, vocab, n_pos;
@@ -152,7 +153,16 @@ int ssdref_tree_accept(int32_t mode, const int32_t *tokens, const int32_t *paren
  *    (draft_probs must be NULL): each child in turn is accepted with
  *    probability r(x) / Z (the residual target mass at its token); on
  *    rejection that token's mass is removed.  The extra token is drawn from
- *    the residual, as in the other sampling modes. */
+ *    the residual, as in the other sampling modes.
+ *  mode SAMPLE_CDF (Sec. 4 suggests drawing the multinomial CDF samples
+ *    first and assembling the batch around them; draft_probs must be NULL):
+ *    node u's uniform is U_u = ssdref_uniform(seed, 2, u), known before the
+ *    tree is built.  At node u the oracle's token is x = the smallest id
+ *    whose running target sum (ascending id, fp64) exceeds U_u (if rounding
+ *    leaves none, the last id with positive target).  The walk moves to the
+ *    first child (lowest index) whose token is x; when none is, x is the
+ *    extra token.  Every emitted token is then an exact draw from the
+ *    target given the tokens before it, whatever tree was assembled. */
 int ssdref_tree_accept_k(int32_t mode, const int32_t *tokens, const int32_t *parent_idx, int32_t n_nodes,
                          int32_t vocab, const float *draft_probs, const float *logits, double temperature,
                          int32_t top_k, uint64_t seed, int32_t *path, int32_t *path_len, int32_t *next_token);
