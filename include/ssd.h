@@ -61,8 +61,10 @@ typedef enum {
   SSD_ACCEPT_GREEDY = 0,     /* argmax walk                                          */
   SSD_ACCEPT_SAMPLE_WOR = 1, /* rejection sampling; siblings were drawn without replacement */
   SSD_ACCEPT_SAMPLE_IID = 2, /* rejection sampling; siblings were drawn independently       */
-  SSD_ACCEPT_SAMPLE_DET = 3  /* rejection sampling; siblings were chosen (e.g. the draft's top
+  SSD_ACCEPT_SAMPLE_DET = 3, /* rejection sampling; siblings were chosen (e.g. the draft's top
                                 tokens), each proposed with certainty: no draft rows      */
+  SSD_ACCEPT_SAMPLE_CDF = 4  /* CDF-first: one uniform per node, drawn before the tree is
+                                built; the oracle's token by inverse CDF (no draft rows)   */
 } ssd_accept_mode;
 
 typedef struct {
@@ -197,6 +199,17 @@ ssd_status ssd_tree_verify_greedy(const ssd_model *m, ssd_kv *kv, int32_t prefix
  *    from Philox4x64-10 keyed by (rng_seed, 0) with counter
  *    (child index, 0, 0, 0) for the test of that child, and (rng_seed, 1)
  *    with counter (last node) for the extra token.
+ *  CDF-first (SSD_ACCEPT_SAMPLE_CDF, draft_probs NULL; Sec. 4 suggests
+ *    drawing the multinomial CDF samples first and assembling the batch
+ *    around them): node u's uniform U_u comes from key (rng_seed, 2),
+ *    counter (u, 0, 0, 0) (ssd_uniform gives it on the host, before the
+ *    tree is built).  The oracle's token at u is the smallest token id whose
+ *    running target sum (ascending id) exceeds U_u; the walk moves to the
+ *    first child (lowest index) carrying it, and where none does it is the
+ *    extra token.  Each emitted token is an exact draw from the target given
+ *    the ones before it provided the tree obeys one rule: U_u may decide u's
+ *    children, but no node's index, token or presence may depend on its own
+ *    uniform or its descendants'.
  * Outputs (device): accepted_path[0..*path_len-1] root first (path[0] = 0),
  * *next_token.  Emitted tokens are tokens[path[1..]] then next_token.
  * draft_probs must be non-NULL exactly for the two drawn modes; top_k < 0 is
@@ -319,6 +332,13 @@ typedef struct {
 
 ssd_status ssd_kv_set_options(ssd_kv *kv, const ssd_options *opt);
 ssd_status ssd_kv_get_options(const ssd_kv *kv, ssd_options *opt);
+
+/* The uniform ssd_tree_accept draws (Philox4x64-10 with key (seed, stream)
+ * and counter (counter, 0, 0, 0); the top 53 bits of the first output word
+ * times 2^-53), computed on the host.  A CDF-first tree builder
+ * (SSD_ACCEPT_SAMPLE_CDF) reads node u's uniform as ssd_uniform(rng_seed, 2,
+ * u) before the tree is verified.  Pure host function. */
+double ssd_uniform(uint64_t seed, uint64_t stream, uint64_t counter);
 
 const char *ssd_status_string(ssd_status s);
 const char *ssd_last_error(void);

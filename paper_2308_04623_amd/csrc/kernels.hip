@@ -1952,8 +1952,11 @@ __device__ __forceinline__ unsigned mono_key(float f) {
 // leaves, *path_len is set to 0 and err (when given) counts it.
 // mode: 1 siblings drawn without replacement from draft row u, 2 drawn
 // independently, 3 chosen (each child proposed with certainty; no draft
-// rows).  topk > 0 restricts every target to the row's topk largest logits
-// (ties at the cut to the lower id).
+// rows), 4 CDF-first (no draft rows: the oracle's token at node u is the
+// inverse CDF of its target at u's own uniform, stream 2, and the walk
+// follows the first child carrying it; two rounds per node visited).
+// topk > 0 restricts every target to the row's topk largest logits (ties at
+// the cut to the lower id).
 
 constexpr int SW_THREADS = 256, SW_SLICE = 2048, SW_PER = SW_SLICE / SW_THREADS, SW_MAXG = 64, SW_REC = 4;
 constexpr int SW_MAXN = 1024;  // nodes (the tree's parents sit in LDS)
@@ -2111,6 +2114,90 @@ __device__ __forceinline__ int sw_next_child(const int* par_l, int N, int u, int
   return r;
 }
 
+// The smallest v whose running sum of w exceeds target, summed per thread
+// in index order, per slice over threads in order, then over slices in order
+// (if rounding leaves none, the last v with positive w), returned to every
+// workgroup: one round for the slice sums, one for the pick of the slice's
+// owner.  ok turns false (in every thread) on an abort or timeout.
+__device__ int sw_pick_all(const SwArgs& a, SwState& st, int g, int G, const double* w, double target, int b0,
+                           double* cs, double* red, double (*gb)[SW_REC], int* shi, bool& ok) {
+  const int tid = threadIdx.x;
+  double c1 = 0.0;
+  int lastpos = -1;
+#pragma unroll
+  for (int i = 0; i < SW_PER; ++i) {
+    const double wv = w[tid * SW_PER + i];
+    c1 += wv;
+    if (wv > 0.0) lastpos = b0 + i;
+  }
+  cs[tid] = c1;
+  const int lp = (int)sw_max((double)lastpos, red);
+  int par = st.k & 1;
+  if (tid == 0) {
+    double Wg = 0.0;
+    for (int t = 0; t < SW_THREADS; ++t) Wg += cs[t];
+    double* rc = sw_rec(st, par, g);
+    sw_st(st, rc, Wg);
+    sw_st(st, rc + 1, (double)lp);
+  }
+  ok = sw_round(a, st, g, shi + 1);
+  if (!ok) return -1;
+  sw_gather(st, par, G, gb);
+  if (tid == 0) {
+    double run = 0.0;
+    int gx = -1, choice = -1;
+    for (int gg = 0; gg < G; ++gg) {
+      if (run + gb[gg][0] > target) {
+        gx = gg;
+        break;
+      }
+      run += gb[gg][0];
+    }
+    if (gx == g) {
+      double c2 = run;
+      for (int t = 0; t < SW_THREADS && choice < 0; ++t) {
+        if (c2 + cs[t] > target) {
+          double c3 = c2;
+          for (int i = 0; i < SW_PER; ++i) {
+            c3 += w[t * SW_PER + i];
+            if (c3 > target) {
+              choice = g * SW_SLICE + t * SW_PER + i;
+              break;
+            }
+          }
+        }
+        c2 += cs[t];
+      }
+      if (choice < 0) choice = lp >= 0 ? lp : g * SW_SLICE;
+    } else if (gx < 0) {
+      // rounding left no crossing: the last token with positive weight
+      choice = 0;
+      for (int gg = G - 1; gg >= 0; --gg)
+        if (gb[gg][1] >= 0.0) {
+          choice = (int)gb[gg][1];
+          break;
+        }
+    }
+    shi[5] = gx;
+    shi[6] = choice;
+  }
+  __syncthreads();
+  const int gx = shi[5];
+  if (gx < 0) {
+    const int x = shi[6];
+    __syncthreads();
+    return x;
+  }
+  par = st.k & 1;
+  if (tid == 0) sw_st(st, sw_rec(st, par, g), g == gx ? (double)shi[6] : 0.0);
+  ok = sw_round(a, st, g, shi + 1);
+  if (!ok) return -1;
+  sw_gather(st, par, G, gb);
+  const int x = (int)gb[gx][0];
+  __syncthreads();
+  return x;
+}
+
 __global__ __launch_bounds__(SW_THREADS) void sample_accept_kernel(SwArgs a) {
   if (blockIdx.x & 7) return;  // (see Placement above)
   __shared__ double r[SW_SLICE], p[SW_SLICE], q[SW_SLICE];
@@ -2123,7 +2210,7 @@ __global__ __launch_bounds__(SW_THREADS) void sample_accept_kernel(SwArgs a) {
   const int tid = threadIdx.x, g = blockIdx.x >> 3, G = a.G, V = a.V;
   for (int i = tid; i < a.N; i += SW_THREADS) par_l[i] = a.parents[i];
   const int b0 = g * SW_SLICE + tid * SW_PER;  // this thread's first vocabulary index
-  const bool wor = a.mode == 1, det = a.mode == 3;
+  const bool wor = a.mode == 1, det = a.mode == 3, cdf = a.mode == 4;
   const bool cut = a.topk > 0 && a.topk < V;
   SwState st;
   st.ctl = (unsigned*)a.work;
@@ -2145,7 +2232,7 @@ __global__ __launch_bounds__(SW_THREADS) void sample_accept_kernel(SwArgs a) {
     st.local = same;
     __syncthreads();
   }
-  int u = 0, len = 1;
+  int u = 0, len = 1, cdf_x = 0;
   if (ok && g == 0 && tid == 0) a.path[0] = 0;
   double Z = 1.0, Zq = 0.0;
   while (ok) {
@@ -2159,7 +2246,7 @@ __global__ __launch_bounds__(SW_THREADS) void sample_accept_kernel(SwArgs a) {
       lg[i] = v < V ? a.logits[(size_t)u * V + v] : 0.f;
       keep[i] = v < V;
       key[i] = mono_key(lg[i]);
-      q[tid * SW_PER + i] = (!det && v < V) ? (double)a.draft[(size_t)u * V + v] : 0.0;
+      q[tid * SW_PER + i] = (!det && !cdf && v < V) ? (double)a.draft[(size_t)u * V + v] : 0.0;
     }
     if (cut) {
       // radix select of the topk-th largest key over all slices, 8 bits a pass
@@ -2279,8 +2366,20 @@ __global__ __launch_bounds__(SW_THREADS) void sample_accept_kernel(SwArgs a) {
     __syncthreads();
     Z = 1.0;
     int accepted = -1;
+    if (cdf) {
+      // ---- the oracle's token at u: the inverse CDF of p at u's own
+      // uniform; the walk follows the first child that carries it
+      cdf_x = sw_pick_all(a, st, g, G, p, philox_uniform(a.seed, 2, (uint64_t)u), b0, cs, red, gb, shi, ok);
+      if (!ok) break;
+      for (int c = sw_next_child(par_l, a.N, u, u, shmin); c < a.N; c = sw_next_child(par_l, a.N, u, c, shmin))
+        if (a.tokens[c] == cdf_x) {
+          accepted = c;
+          break;
+        }
+    }
     // ---- the children of u, in index order
-    for (int c = sw_next_child(par_l, a.N, u, u, shmin); c < a.N; c = sw_next_child(par_l, a.N, u, c, shmin)) {
+    for (int c = cdf ? a.N : sw_next_child(par_l, a.N, u, u, shmin); c < a.N;
+         c = sw_next_child(par_l, a.N, u, c, shmin)) {
       const int x = a.tokens[c];
       const int owner = x / SW_SLICE, xl = x - owner * SW_SLICE;
       // this slice's residual as it would be after rejecting x
@@ -2354,7 +2453,13 @@ __global__ __launch_bounds__(SW_THREADS) void sample_accept_kernel(SwArgs a) {
     u = accepted;
     __syncthreads();
   }
-  if (ok) {
+  if (ok && cdf) {
+    // ---- extra token: the oracle's token at the node the walk stopped at
+    if (g == 0 && tid == 0) {
+      *a.next = cdf_x;
+      *a.path_len = len;
+    }
+  } else if (ok) {
     // ---- extra token: the smallest v whose running sum of w exceeds U2 * Z
     // (w = r, or p when rounding left no residual mass), summed per thread in
     // index order, per slice over threads in order, then over slices in order
@@ -2444,7 +2549,7 @@ size_t sample_work_bytes() { return kSwBytes; }
 hipError_t launch_sample_accept(const int* tokens, const int* parents, int N, int V, const float* logits,
                                 const float* draft, double temperature, uint64_t seed, int mode, int topk, void* work,
                                 unsigned* err, int* path, int* path_len, int* next, hipStream_t s) {
-  if (mode < 1 || mode > 3 || (mode == 3) != (draft == nullptr)) return hipErrorInvalidValue;
+  if (mode < 1 || mode > 4 || (mode >= 3) != (draft == nullptr)) return hipErrorInvalidValue;
   const int G = (V + SW_SLICE - 1) / SW_SLICE;
   if (V <= 0 || G > SW_MAXG || N <= 0 || N > SW_MAXN || !work) return hipErrorInvalidValue;
   SwArgs a{tokens, parents, N, V, G, logits, draft, temperature, seed, mode, topk, path, path_len, next,

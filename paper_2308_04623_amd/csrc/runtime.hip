@@ -1136,7 +1136,7 @@ extern "C" ssd_status ssd_topk(ssd_kv* kv, const float* logits, int32_t n_rows, 
 static ssd_status check_accept_mode(const ssd_tree* tree, const float* draft_probs) {
   const int mode = tree->mode;
   if (mode != SSD_ACCEPT_GREEDY && mode != SSD_ACCEPT_SAMPLE_WOR && mode != SSD_ACCEPT_SAMPLE_IID &&
-      mode != SSD_ACCEPT_SAMPLE_DET)
+      mode != SSD_ACCEPT_SAMPLE_DET && mode != SSD_ACCEPT_SAMPLE_CDF)
     return fail(SSD_E_INVALID_ARG, "unknown accept mode");
   const bool drawn = mode == SSD_ACCEPT_SAMPLE_WOR || mode == SSD_ACCEPT_SAMPLE_IID;
   if (drawn && !draft_probs) return fail(SSD_E_INVALID_ARG, "draft_probs required when siblings were drawn");
@@ -1348,4 +1348,28 @@ extern "C" ssd_status ssd_model_q8_matrix(const ssd_model* m, int32_t which, int
       codes[(size_t)r * K + k] = (int8_t)((int)f[(((size_t)rb * KC + kc) * 64 + lane) * 8 + k % 8] - 128);
     }
   return SSD_OK;
+}
+
+// ------------------------------------------------------------------ host uniforms
+
+// Philox4x64-10 (Salmon, Moraes, Dror, Shaw, SC'11): ten rounds of two 64x64
+// multiplies with the published multipliers, the key bumped by the published
+// Weyl constants between rounds; the same generator the accept kernels run.
+extern "C" double ssd_uniform(uint64_t seed, uint64_t stream, uint64_t counter) {
+  const uint64_t M0 = 0xD2E7470EE14C6C93ull, M1 = 0xCA5A826395121157ull;
+  const uint64_t W0 = 0x9E3779B97F4A7C15ull, W1 = 0xBB67AE8584CAA73Bull;
+  uint64_t c0 = counter, c1 = 0, c2 = 0, c3 = 0, k0 = seed, k1 = stream;
+  for (int r = 0; r < 10; ++r) {
+    if (r) {
+      k0 += W0;
+      k1 += W1;
+    }
+    const unsigned __int128 p0 = (unsigned __int128)M0 * c0, p1 = (unsigned __int128)M1 * c2;
+    const uint64_t n0 = (uint64_t)(p1 >> 64) ^ c1 ^ k0, n2 = (uint64_t)(p0 >> 64) ^ c3 ^ k1;
+    c1 = (uint64_t)p1;
+    c3 = (uint64_t)p0;
+    c0 = n0;
+    c2 = n2;
+  }
+  return (double)(c0 >> 11) * 0x1.0p-53;
 }

@@ -186,7 +186,7 @@ hipError_t launch_greedy_from_parts(const unsigned* parts, int G, int N, const i
                                     const int* depth, int* path, int* path_len, int* next, hipStream_t s);
 hipError_t launch_greedy_walk(const int* tokens, const int* parents, const int* depth, int N, const int* g,
                               int* path, int* path_len, int* next, hipStream_t s);
-// mode: 1 without replacement, 2 independent, 3 chosen (draft == nullptr);
+// mode: 1 without replacement, 2 independent, 3 chosen, 4 CDF-first (3, 4: draft == nullptr);
 // topk > 0 restricts the targets to each row's topk largest logits
 // rejection sampling down the tree on ceil(V / 2048) workgroups that trade
 // slice sums through work (sample_work_bytes(), zeroed once before the first

@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(_HERE, "libssd.so")
 
 OK, E_INVALID_ARG, E_INVALID_TREE, E_CAPACITY, E_DEVICE, E_UNSUPPORTED = 0, -1, -2, -3, -4, -5
 F32, BF16 = 0, 1
-GREEDY, SAMPLE_WOR, SAMPLE_IID, SAMPLE_DET = 0, 1, 2, 3
+GREEDY, SAMPLE_WOR, SAMPLE_IID, SAMPLE_DET, SAMPLE_CDF = 0, 1, 2, 3, 4
 GEMM_AUTO, GEMM_VEC, GEMM_MFMA = 0, 1, 2
 
 LAYER_TENSORS = ("ln1_g", "ln1_b", "w_qkv", "b_qkv", "w_o", "b_o",
@@ -31,7 +31,7 @@ EXPORTS = ("ssd_model_create", "ssd_model_create_q8", "ssd_model_destroy", "ssd_
            "ssd_graph_capture_verify", "ssd_graph_launch", "ssd_graph_destroy", "ssd_validate_tree",
            "ssd_tree_prep", "ssd_kv_set_options", "ssd_kv_get_options", "ssd_status_string", "ssd_last_error",
            "ssd_model_prefix_view", "ssd_topk", "ssd_tree_accept_noalloc", "ssd_tree_verify_greedy",
-           "ssd_graph_capture_verify_greedy")
+           "ssd_graph_capture_verify_greedy", "ssd_uniform")
 # and every function include/ssd_diag.h declares (measurement and diagnostics)
 DIAG_EXPORTS = ("ssd_launch_gemm", "ssd_verify_path", "ssd_fused_plan", "ssd_kv_set_trace", "ssd_model_q8_matrix")
 
@@ -109,6 +109,7 @@ def lib():
             "ssd_model_prefix_view": [vp, C.c_int32, C.POINTER(vp)],
             "ssd_topk": [vp, vp, C.c_int32, C.c_int32, vp, vp, vp, vp],
             "ssd_status_string": [C.c_int],
+            "ssd_uniform": [C.c_uint64, C.c_uint64, C.c_uint64],
             "ssd_last_error": [],
         }
         for name, args in sig.items():
@@ -118,6 +119,7 @@ def lib():
         for name in ("ssd_model_destroy", "ssd_kv_destroy", "ssd_graph_destroy"):
             getattr(L, name).restype = None
         L.ssd_status_string.restype = C.c_char_p
+        L.ssd_uniform.restype = C.c_double
         L.ssd_last_error.restype = C.c_char_p
         _lib = L
     return _lib
@@ -182,6 +184,11 @@ def accept_noalloc(tokens, parent_idx, logits, out, mode: int = GREEDY, draft_pr
                                          C.c_void_p(path.data_ptr()), C.c_void_p(plen.data_ptr()),
                                          C.c_void_p(nxt.data_ptr()), _stream(stream)), "ssd_tree_accept_noalloc")
     return path, plen, nxt
+
+
+def uniform(seed: int, stream: int, counter: int) -> float:
+    """ssd_uniform: the accept walk's uniform for (seed, stream, counter)."""
+    return float(lib().ssd_uniform(seed, stream, counter))
 
 
 def kv_bytes(cfg, max_ctx: int, max_nodes: int) -> Tuple[int, int]:

@@ -403,3 +403,76 @@ def test_sampling_accept_topk_and_chosen_siblings_bit_exact(wide, ssd, torch, V,
         assert int(nxt.item()) == on, trial
         if k == 1:   # the target is the argmax: every emitted token is one
             assert on == int(np.lexsort((np.arange(V), -lg[op[-1]]))[0])
+
+
+from tests.test_oracle_sampling_variants import topk_target  # noqa: E402
+
+
+def _cdf_pick_host(w, U):
+    """Smallest id whose running sum (ascending id) exceeds U (else the last
+    positive id): the test's own inverse CDF, for building trees."""
+    c = np.cumsum(np.asarray(w, np.float64))
+    i = int(np.searchsorted(c, U, side="right"))
+    return i if i < len(w) else int(np.flatnonzero(np.asarray(w) > 0)[-1])
+
+
+def _cdf_first_tree(lg_rows_for, V, seed, branching, n_max, ssd, offsets=(0.0, 0.1, -0.1)):
+    """CDF-first assembly (breadth first, indices in creation order): node
+    u's children are the inverse-CDF picks of a draft row at U_u + offsets,
+    U_u = ssd_uniform(seed, 2, u) read on the host before the tree exists;
+    the draft row of node u is lg_rows_for(u, token)."""
+    toks, par, frontier = [int(lg_rows_for.root)], [-1], [0]
+    for b in branching:
+        nxt = []
+        for u in frontier:
+            q = lg_rows_for(u, toks[u])
+            U = ssd.uniform(seed, 2, u)
+            kids = []
+            for o in offsets:
+                x = _cdf_pick_host(q, (U + o) % 1.0)
+                if x not in kids:
+                    kids.append(x)
+            for x in kids[:b]:
+                if len(toks) < n_max:
+                    toks.append(x)
+                    par.append(u)
+                    nxt.append(len(toks) - 1)
+        frontier = nxt
+    return np.array(toks, np.int32), np.array(par, np.int32)
+
+
+@pytest.mark.parametrize("V", [512, 50257])
+@pytest.mark.parametrize("k,T", [(0, 1.0), (50, 1.0), (0, 0.7)])
+def test_sampling_accept_cdf_first_bit_exact(wide, ssd, torch, V, k, T):
+    """CDF-first sampling (uniforms drawn before the tree is built, the
+    oracle's token by inverse CDF at each node's uniform): trees assembled
+    around the uniforms from a draft close to the target (so walks go deep),
+    path and extra token bit-exact against the oracle on identical logits."""
+    cfg, s = wide
+    g = np.random.default_rng(V + k)
+    deep = 0
+    for trial in range(8):
+        n_max = 40 if trial % 2 else 200
+        lg = np.round(g.standard_normal((n_max, V)) * 2.0, 1).astype(np.float32)
+        # node u's draft row: the target row u itself (even trials: the
+        # draft's pick at U_u is the oracle's token but for rounding, so the
+        # walks go deep) or the target of slightly perturbed logits
+        noise = 0.0 if trial % 2 == 0 else 0.05
+        dl = lg + (g.standard_normal(lg.shape) * noise).astype(np.float32)
+
+        def rows(u, tok):
+            return topk_target(dl[u], k, T)
+        rows.root = int(g.integers(V))
+        toks, par = _cdf_first_tree(rows, V, trial, [3, 2, 2, 2, 1, 1], n_max, ssd)
+        n = len(par)
+        dlg = torch.from_numpy(np.ascontiguousarray(lg[:n])).cuda()
+        path, plen, nxt = s.accept(toks, par, dlg, mode=ssd.SAMPLE_CDF, temperature=T, seed=trial, top_k=k)
+        op, on = oracle.tree_accept(oracle.SAMPLE_CDF, toks, par, lg[:n], None, T, trial, top_k=k)
+        assert path[:int(plen.item())].cpu().numpy().tolist() == op.tolist(), trial
+        assert int(nxt.item()) == on, trial
+        deep += len(op) - 1
+    assert s.error_count() == 0
+    assert deep >= 8          # the walks follow the assembled trees
+    # draft rows are refused in this mode
+    with pytest.raises(ssd.SSDError):
+        s.accept([0, 1], [-1, 0], dlg[:2], mode=ssd.SAMPLE_CDF, draft_probs=dlg[:2])

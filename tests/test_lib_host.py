@@ -132,3 +132,16 @@ def test_fused_plan_balances_gpt2l_xcds():
 def test_fused_plan_rejects_other_head_dims():
     with pytest.raises(ssd.SSDError):
         ssd.fused_plan(4, 128, 512, 512, 1)  # head dimension 32
+
+
+def test_host_uniform_equals_the_oracle_generator():
+    """ssd_uniform (host, product code) against the oracle's Philox4x64-10
+    uniform, itself pinned against numpy's Philox: bit for bit."""
+    import oracle
+    g = np.random.default_rng(1)
+    for _ in range(2000):
+        seed, stream, n = (int(x) for x in g.integers(0, 2 ** 63, 3))
+        stream %= 4
+        assert ssd.uniform(seed, stream, n) == oracle.uniform(seed, stream, n)
+    for seed, stream, n in ((0, 0, 0), (2 ** 64 - 1, 2, 2 ** 64 - 1), (7, 2, 255)):
+        assert ssd.uniform(seed, stream, n) == oracle.uniform(seed, stream, n)
