@@ -333,6 +333,21 @@ typedef struct {
 ssd_status ssd_kv_set_options(ssd_kv *kv, const ssd_options *opt);
 ssd_status ssd_kv_get_options(const ssd_kv *kv, ssd_options *opt);
 
+/* Inverse-CDF picks for CDF-first tree assembly (Sec. 4: draw the
+ * multinomial CDF samples first, then assemble the batch around them): for
+ * query q, tokens[q] (device) is the token drawn from
+ * softmax(logits[rows[q]] / temperature) over the row's vocab entries at the
+ * uniform uniforms[q], by inverse CDF in ascending token id (the order
+ * SSD_ACCEPT_SAMPLE_CDF draws the oracle's tokens in).  logits:
+ * [n_rows][vocab] device, vocab at most the model's; rows, uniforms: HOST
+ * arrays of n_queries (1..64), read before the call returns.  Errors:
+ * SSD_E_INVALID_ARG (null, vocab outside [1, the model's vocab], a row
+ * outside [0, n_rows), a uniform outside [0, 1), temperature <= 0,
+ * n_queries outside [1, 64]), SSD_E_CAPACITY (n_rows outside
+ * [1, max_nodes]), SSD_E_DEVICE. */
+ssd_status ssd_cdf_pick(ssd_kv *kv, const float *logits, int32_t n_rows, int32_t vocab, float temperature,
+                        int32_t n_queries, const int32_t *rows, const double *uniforms, int32_t *tokens, void *stream);
+
 /* The uniform ssd_tree_accept draws (Philox4x64-10 with key (seed, stream)
  * and counter (counter, 0, 0, 0); the top 53 bits of the first output word
  * times 2^-53), computed on the host.  A CDF-first tree builder

@@ -87,6 +87,8 @@ def _bind(L):
     L.ssdref_uniform.argtypes = [C.c_uint64, C.c_uint64, C.c_uint64]
     L.ssdref_uniform.restype = C.c_double
     L.ssdref_quantize_q8.argtypes = [C.POINTER(C.c_uint16), C.c_int32, C.c_int32, _I8P, _F32P]
+    L.ssdref_cdf_pick.argtypes = [C.POINTER(C.c_float), C.c_int32, C.c_double, C.c_double]
+    L.ssdref_cdf_pick.restype = C.c_int32
     L.ssdref_round_bf16.argtypes = [C.c_double]
     L.ssdref_round_bf16.restype = C.c_uint16
     return L
@@ -275,6 +277,16 @@ def tree_accept(mode: int, tokens: Sequence[int], parent_idx: Sequence[int], log
                                     _ptr(plen, C.POINTER(C.c_int32)), _ptr(nxt, C.POINTER(C.c_int32)))
     _check(rc, "tree_accept")
     return path[:plen[0]].copy(), int(nxt[0])
+
+
+def cdf_pick(row: np.ndarray, temperature: float, U: float) -> int:
+    """ssdref_cdf_pick: the token drawn from softmax(row / T) at U by inverse
+    CDF in ascending token id."""
+    r = np.ascontiguousarray(row, dtype=np.float32)
+    x = lib().ssdref_cdf_pick(r.ctypes.data_as(C.POINTER(C.c_float)), len(r), float(temperature), float(U))
+    if x < 0:
+        raise OracleError(-1, "cdf_pick")
+    return int(x)
 
 
 def philox4x64_10(key: Sequence[int], ctr: Sequence[int]) -> np.ndarray:

@@ -626,3 +626,12 @@ int ssdref_tree_accept_k(int32_t mode, const int32_t *tokens, const int32_t *par
   free(depth);
   return SSDREF_OK;
 }
+
+int32_t ssdref_cdf_pick(const float *row, int32_t vocab, double temperature, double U) {
+  if (!row || vocab <= 0 || !(temperature > 0.0) || !(U >= 0.0 && U < 1.0)) return -1;
+  double *p = (double *)malloc(sizeof(double) * vocab);
+  softmax_t(row, vocab, temperature, 0, p);
+  const int32_t x = sample_cdf(p, vocab, 1.0, U);
+  free(p);
+  return x;
+}

@@ -167,6 +167,12 @@ int ssdref_tree_accept_k(int32_t mode, const int32_t *tokens, const int32_t *par
                          int32_t vocab, const float *draft_probs, const float *logits, double temperature,
                          int32_t top_k, uint64_t seed, int32_t *path, int32_t *path_len, int32_t *next_token);
 
+/* The token drawn from softmax(row / temperature) (whole vocabulary, fp64)
+ * at uniform U by inverse CDF in ascending token id: the oracle's token of
+ * SAMPLE_CDF at a node, here at a given uniform (CDF-first tree assembly
+ * picks the draft's tokens this way).  Returns -1 on invalid input. */
+int32_t ssdref_cdf_pick(const float *row, int32_t vocab, double temperature, double U);
+
 /* Philox4x64-10 (Salmon, Moraes, Dror, Shaw, SC'11): out = bijection(ctr; key). */
 void ssdref_philox4x64_10(const uint64_t key[2], const uint64_t ctr[4], uint64_t out[4]);
 

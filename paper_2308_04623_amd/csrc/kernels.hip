@@ -1885,6 +1885,87 @@ hipError_t launch_greedy_walk(const int* tokens, const int* parents, const int* 
   return hipGetLastError();
 }
 
+// ------------------------------------------------------------------ inverse-CDF picks
+//
+// For CDF-first tree assembly: query q draws from softmax(logits[rows[q]] / T)
+// over the whole vocabulary at the uniform U[q] by inverse CDF in ascending
+// token id.  One workgroup per query: thread t owns the contiguous ids
+// [t C, t C + C); the row's maximum, then each thread's sum of the
+// normalised probabilities in id order, then thread 0 walks the threads'
+// sums in order to the crossing and scans that thread's ids (fp64
+// throughout).  If rounding leaves no crossing, the last id with positive
+// probability.
+constexpr int kPickThreads = 1024;
+
+__global__ __launch_bounds__(kPickThreads) void cdf_pick_kernel(CdfPickArgs a) {
+  __shared__ double part[kPickThreads];
+  __shared__ double red[kPickThreads / 64];
+  const int q = blockIdx.x, tid = threadIdx.x, V = a.V;
+  const float* row = a.logits + (size_t)a.rows[q] * V;
+  const int C = (V + kPickThreads - 1) / kPickThreads, v0 = tid * C, v1 = min(V, v0 + C);
+  double mx = -INFINITY;
+  for (int v = v0; v < v1; ++v) mx = fmax(mx, (double)row[v] / a.T);
+  for (int o = 32; o > 0; o >>= 1) mx = fmax(mx, __shfl_xor(mx, o));
+  if ((tid & 63) == 0) red[tid >> 6] = mx;
+  __syncthreads();
+  if (tid == 0) {
+    double m = red[0];
+    for (int w = 1; w < kPickThreads / 64; ++w) m = fmax(m, red[w]);
+    red[0] = m;
+  }
+  __syncthreads();
+  mx = red[0];
+  double e = 0.0;
+  for (int v = v0; v < v1; ++v) e += exp((double)row[v] / a.T - mx);
+  part[tid] = e;
+  __syncthreads();
+  if (tid == 0) {
+    double S = 0.0;
+    for (int t = 0; t < kPickThreads; ++t) S += part[t];
+    red[1] = S;
+  }
+  __syncthreads();
+  const double S = red[1];
+  double c = 0.0;
+  for (int v = v0; v < v1; ++v) c += exp((double)row[v] / a.T - mx) / S;
+  __syncthreads();
+  part[tid] = c;
+  __syncthreads();
+  if (tid == 0) {
+    const double U = a.U[q];
+    double run = 0.0;
+    int pick = -1;
+    for (int t = 0; t < kPickThreads && pick < 0; ++t) {
+      if (run + part[t] > U) {
+        double c3 = run;
+        for (int v = t * C; v < min(V, t * C + C); ++v) {
+          c3 += exp((double)row[v] / a.T - mx) / S;
+          if (c3 > U) {
+            pick = v;
+            break;
+          }
+        }
+      }
+      run += part[t];
+    }
+    if (pick < 0) {
+      pick = 0;
+      for (int v = V - 1; v >= 0; --v)
+        if (exp((double)row[v] / a.T - mx) / S > 0.0) {
+          pick = v;
+          break;
+        }
+    }
+    a.out[q] = pick;
+  }
+}
+
+hipError_t launch_cdf_pick(const CdfPickArgs& a, hipStream_t s) {
+  if (a.n < 1 || a.n > kMaxPicks || a.V < 1 || !(a.T > 0.f)) return hipErrorInvalidValue;
+  cdf_pick_kernel<<<a.n, kPickThreads, 0, s>>>(a);
+  return hipGetLastError();
+}
+
 // ------------------------------------------------------------------ accept: rejection sampling
 //
 // Philox4x64-10 (Salmon, Moraes, Dror, Shaw, SC'11): 10 rounds of two 64x64

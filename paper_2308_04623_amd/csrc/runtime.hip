@@ -1373,3 +1373,29 @@ extern "C" double ssd_uniform(uint64_t seed, uint64_t stream, uint64_t counter) 
   }
   return (double)(c0 >> 11) * 0x1.0p-53;
 }
+
+// ------------------------------------------------------------------ inverse-CDF picks
+
+extern "C" ssd_status ssd_cdf_pick(ssd_kv* kv, const float* logits, int32_t n_rows, int32_t vocab, float temperature,
+                                   int32_t n_queries, const int32_t* rows, const double* uniforms, int32_t* tokens,
+                                   void* stream) {
+  if (!kv || !logits || !rows || !uniforms || !tokens) return fail(SSD_E_INVALID_ARG, "null argument");
+  if (n_rows < 1 || n_rows > kv->max_nodes) return fail(SSD_E_CAPACITY, "n_rows outside [1, max_nodes]");
+  if (vocab < 1 || vocab > kv->m->cfg.vocab) return fail(SSD_E_INVALID_ARG, "vocab outside [1, the model's vocab]");
+  if (n_queries < 1 || n_queries > kMaxPicks) return fail(SSD_E_INVALID_ARG, "n_queries outside [1, 64]");
+  if (!(temperature > 0.f)) return fail(SSD_E_INVALID_ARG, "temperature must be positive");
+  CdfPickArgs a{};
+  a.logits = logits;
+  a.V = vocab;
+  a.n = n_queries;
+  a.T = temperature;
+  a.out = tokens;
+  for (int q = 0; q < n_queries; ++q) {
+    if (rows[q] < 0 || rows[q] >= n_rows) return fail(SSD_E_INVALID_ARG, "row outside [0, n_rows)");
+    if (!(uniforms[q] >= 0.0 && uniforms[q] < 1.0)) return fail(SSD_E_INVALID_ARG, "uniform outside [0, 1)");
+    a.rows[q] = rows[q];
+    a.U[q] = uniforms[q];
+  }
+  HIP_TRY(launch_cdf_pick(a, (hipStream_t)stream));
+  return SSD_OK;
+}

@@ -198,6 +198,19 @@ size_t sample_work_bytes();
 hipError_t launch_sample_accept(const int* tokens, const int* parents, int N, int V, const float* logits,
                                 const float* draft, double temperature, uint64_t seed, int mode, int topk, void* work,
                                 unsigned* err, int* path, int* path_len, int* next, hipStream_t s);
+// inverse-CDF picks for CDF-first tree assembly: out[q] = the token drawn
+// from softmax(logits[rows[q]] / T) (whole vocabulary V) at uniform U[q], by
+// ascending token id
+constexpr int kMaxPicks = 64;
+struct CdfPickArgs {
+  const float* logits;
+  int V, n;
+  float T;
+  int rows[kMaxPicks];
+  double U[kMaxPicks];
+  int* out;
+};
+hipError_t launch_cdf_pick(const CdfPickArgs& a, hipStream_t s);
 hipError_t launch_commit(int f32, void* kc, void* vc, const void* kt, const void* vt, int LH, int max_ctx,
                          int max_nodes, int DH, int P, const int* path, const int* path_len, unsigned* err,
                          hipStream_t s);

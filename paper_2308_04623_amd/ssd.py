@@ -31,7 +31,7 @@ EXPORTS = ("ssd_model_create", "ssd_model_create_q8", "ssd_model_destroy", "ssd_
            "ssd_graph_capture_verify", "ssd_graph_launch", "ssd_graph_destroy", "ssd_validate_tree",
            "ssd_tree_prep", "ssd_kv_set_options", "ssd_kv_get_options", "ssd_status_string", "ssd_last_error",
            "ssd_model_prefix_view", "ssd_topk", "ssd_tree_accept_noalloc", "ssd_tree_verify_greedy",
-           "ssd_graph_capture_verify_greedy", "ssd_uniform")
+           "ssd_graph_capture_verify_greedy", "ssd_uniform", "ssd_cdf_pick")
 # and every function include/ssd_diag.h declares (measurement and diagnostics)
 DIAG_EXPORTS = ("ssd_launch_gemm", "ssd_verify_path", "ssd_fused_plan", "ssd_kv_set_trace", "ssd_model_q8_matrix")
 
@@ -110,6 +110,7 @@ def lib():
             "ssd_topk": [vp, vp, C.c_int32, C.c_int32, vp, vp, vp, vp],
             "ssd_status_string": [C.c_int],
             "ssd_uniform": [C.c_uint64, C.c_uint64, C.c_uint64],
+            "ssd_cdf_pick": [vp, vp, C.c_int32, C.c_int32, C.c_float, C.c_int32, vp, vp, vp, vp],
             "ssd_last_error": [],
         }
         for name, args in sig.items():
@@ -462,6 +463,22 @@ class Session:
         _check(lib().ssd_topk(self.handle, C.c_void_p(logits.data_ptr()), n, k, C.c_void_p(idx.data_ptr()),
                               C.c_void_p(val.data_ptr()), C.c_void_p(lse.data_ptr()), _stream(stream)), "ssd_topk")
         return idx, val, lse
+
+    def cdf_pick(self, logits, rows, uniforms, temperature: float = 1.0, n_rows: Optional[int] = None,
+                 stream=None):
+        """ssd_cdf_pick: device int32 tokens, query q drawn from
+        softmax(logits[rows[q]] / temperature) at uniforms[q] by inverse CDF
+        (ascending token id)."""
+        torch = _torch()
+        r = _i32(rows)
+        u = np.ascontiguousarray(uniforms, dtype=np.float64)
+        n = logits.shape[0] if n_rows is None else n_rows
+        out = torch.empty(len(r), dtype=torch.int32, device=self.model.device)
+        _check(lib().ssd_cdf_pick(self.handle, C.c_void_p(logits.data_ptr()), n, int(logits.shape[1]),
+                                  float(temperature), len(r),
+                                  C.c_void_p(r.ctypes.data), C.c_void_p(u.ctypes.data), C.c_void_p(out.data_ptr()),
+                                  _stream(stream)), "ssd_cdf_pick")
+        return out
 
     def set_trace(self, buf=None):
         """Stage timestamps of the persistent pass into buf (device uint64/int64

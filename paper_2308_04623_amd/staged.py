@@ -18,6 +18,16 @@ candidates.  Here:
 Greedy acceptance makes the emitted sequence the oracle's greedy sequence
 whatever the trees (Sec. 2.3), which the tests check against plain decoding.
 
+CDF-first sampling (Sec. 4 suggests drawing the multinomial CDF samples
+first and assembling the batch around them): every oracle-tree node u owns
+the uniform U_u = ssd_uniform(seed, 2, u), read before the tree exists.  The
+oracle's token at u will be the inverse CDF of its target at U_u
+(SSD_ACCEPT_SAMPLE_CDF), so u's children are the draft's own inverse-CDF
+picks at U_u and a few nearby uniforms: the tokens the oracle is likely to
+draw there.  Nodes are numbered in breadth-first creation order and a node's
+uniform only decides its children, which keeps every emitted token an exact
+draw from the oracle's target.
+
 The policy code here is pure host logic over small arrays; the model work
 goes through a backend (the GPU library in this module, the CPU oracle in the
 tests).
@@ -36,6 +46,7 @@ DRAFT_TOP = 2                # endorsement and expansion width
 BIGRAM_TOP = 8
 MAX_BIGRAM_NODES = 32
 MAX_ORACLE_NODES = 64
+CDF_OFFSETS = (0.0, 0.05, -0.05)  # CDF-first children: the draft's picks at U_u + these
 
 
 # ---------------------------------------------------------------- draft^2: bigram table
@@ -145,6 +156,53 @@ def oracle_tree(toks: np.ndarray, par: np.ndarray, top_idx: np.ndarray, top_val:
     return t_out, p_out, int(endorsed.sum())
 
 
+def cdf_first_tree(bt: np.ndarray, bp: np.ndarray, seed: int, uniform, pick, offsets: Sequence[float] = CDF_OFFSETS,
+                   cap: int = MAX_ORACLE_NODES) -> Tuple[np.ndarray, np.ndarray]:
+    """CDF-first oracle tree over a draft pass on the bigram tree (bt, bp).
+
+    Oracle node u (numbered in breadth-first creation order) stands for a
+    bigram node b(u) the draft ran on, or for a leaf.  A node with a bigram
+    node gets as children the draft's picks at U_u + offsets (wrapped into
+    [0, 1), duplicates dropped): uniform(u) gives U_u, pick(rows, us) the
+    draft's inverse-CDF tokens of bigram rows at uniforms.  A child maps to
+    the first bigram child of b(u) with its token, or is a leaf.  Levels are
+    picked in one batch each; creation stops at cap nodes.  Returns tokens
+    and parents."""
+    kids = [[] for _ in range(len(bt))]
+    for i in range(1, len(bt)):
+        kids[int(bp[i])].append(i)
+    toks, par, big = [int(bt[0])], [-1], [0]
+    level = [0]
+    while level and len(toks) < cap:
+        rows, us, owner = [], [], []
+        for u in level:
+            if big[u] < 0:
+                continue
+            U = uniform(u)
+            for o in offsets:
+                rows.append(big[u])
+                us.append((U + o) % 1.0)
+                owner.append(u)
+        picked = pick(rows, us) if rows else []
+        nxt = []
+        by_owner = {}
+        for u, t in zip(owner, picked):
+            lst = by_owner.setdefault(u, [])
+            if int(t) not in lst:
+                lst.append(int(t))
+        for u in level:
+            for t in by_owner.get(u, []):
+                if len(toks) >= cap:
+                    break
+                match = [k for k in kids[big[u]] if int(bt[k]) == t]
+                toks.append(t)
+                par.append(u)
+                big.append(match[0] if match else -1)
+                nxt.append(len(toks) - 1)
+        level = nxt
+    return np.array(toks, np.int32), np.array(par, np.int32)
+
+
 # ---------------------------------------------------------------- decoding loops
 
 @dataclass
@@ -235,6 +293,31 @@ def staged_sample(backend, P: int, root: int, n_new: int, succ: np.ndarray, top_
     return st
 
 
+def staged_sample_cdf(backend, P: int, root: int, n_new: int, succ: np.ndarray, temperature: float = 1.0,
+                      seed0: int = 0) -> DecodeStats:
+    """Staged speculation with CDF-first sampling over the whole vocabulary:
+    one draft pass over the bigram tree, the oracle tree assembled around
+    each node's pre-drawn uniform from the draft's inverse-CDF picks, and the
+    walk of SSD_ACCEPT_SAMPLE_CDF; every emitted token is an exact draw from
+    the oracle's softmax(logits / temperature)."""
+    st = DecodeStats()
+    t0 = time.perf_counter()
+    while len(st.tokens) < n_new:
+        seed = seed0 + st.steps
+        bt, bp = bigram_tree(root, succ)
+        ot, op = backend.cdf_tree(P, bt, bp, seed, temperature)
+        path, nxt = backend.oracle_step(P, ot, op, sample=(0, temperature, seed), cdf=True)
+        P += len(path)
+        st.tokens += [int(ot[i]) for i in path[1:]] + [int(nxt)]
+        st.steps += 1
+        st.accepted.append(len(path) - 1)
+        st.oracle_nodes.append(len(ot))
+        root = int(nxt)
+    st.tokens = st.tokens[:n_new]
+    st.seconds = time.perf_counter() - t0
+    return st
+
+
 # ---------------------------------------------------------------- GPU backend (libssd)
 
 class GpuBackend:
@@ -281,18 +364,35 @@ class GpuBackend:
         self._check_errors(self.d)
         return idx.cpu().numpy(), val.cpu().numpy(), lse.cpu().numpy()
 
-    def oracle_step(self, P: int, toks: np.ndarray, par: np.ndarray, sample=None):
+    def cdf_tree(self, P: int, bt: np.ndarray, bp: np.ndarray, seed: int, temperature: float):
+        """One draft pass over the bigram tree, then the CDF-first oracle
+        tree from its logits (ssd_uniform, ssd_cdf_pick)."""
+        from . import ssd
+        lg = self.d.verify(P, bt, bp)
+        n = len(bt)
+
+        def pick(rows, us):
+            out = []
+            for s0 in range(0, len(rows), 64):
+                out += self.d.cdf_pick(lg, rows[s0:s0 + 64], us[s0:s0 + 64], temperature, n).cpu().tolist()
+            return out
+        ot, op = cdf_first_tree(bt, bp, seed, lambda u: ssd.uniform(seed, 2, u), pick)
+        self._check_errors(self.d)
+        return ot, op
+
+    def oracle_step(self, P: int, toks: np.ndarray, par: np.ndarray, sample=None, cdf: bool = False):
         """Verify, accept and commit; greedy, or with sample = (top_k,
         temperature, seed) rejection sampling of children chosen by the
-        draft (SSD_ACCEPT_SAMPLE_DET)."""
+        draft (SSD_ACCEPT_SAMPLE_DET), or with cdf=True the CDF-first walk
+        (SSD_ACCEPT_SAMPLE_CDF)."""
         from . import ssd
         if sample is None:
             lg, path, plen, nxt = self.o.verify_greedy(P, toks, par)
         else:
             top_k, temperature, seed = sample
             lg = self.o.verify(P, toks, par)
-            path, plen, nxt = self.o.accept(toks, par, lg, mode=ssd.SAMPLE_DET, temperature=temperature, seed=seed,
-                                            top_k=top_k)
+            path, plen, nxt = self.o.accept(toks, par, lg, mode=ssd.SAMPLE_CDF if cdf else ssd.SAMPLE_DET,
+                                            temperature=temperature, seed=seed, top_k=top_k)
         self.o.commit(P, path, plen)
         self._check_errors(self.o)
         n = int(plen.item())

@@ -476,3 +476,24 @@ def test_sampling_accept_cdf_first_bit_exact(wide, ssd, torch, V, k, T):
     # draft rows are refused in this mode
     with pytest.raises(ssd.SSDError):
         s.accept([0, 1], [-1, 0], dlg[:2], mode=ssd.SAMPLE_CDF, draft_probs=dlg[:2])
+
+
+@pytest.mark.parametrize("V", [512, 50257])
+@pytest.mark.parametrize("T", [1.0, 0.7])
+def test_cdf_pick_bit_exact(wide, ssd, torch, V, T):
+    """ssd_cdf_pick (the draft's inverse-CDF picks for CDF-first assembly)
+    against the oracle's pick: 64 queries over 40 rows, tokens equal."""
+    cfg, s = wide
+    g = np.random.default_rng(V + int(T * 10))
+    lg = np.round(g.standard_normal((40, V)) * 2.0, 1).astype(np.float32)
+    rows = g.integers(0, 40, 64).astype(np.int32)
+    us = g.random(64)
+    us[:3] = [0.0, 0.999999999, 0.5]
+    dlg = torch.from_numpy(lg).cuda()
+    got = s.cdf_pick(dlg, rows, us, T).cpu().numpy()
+    want = [oracle.cdf_pick(lg[r], T, u) for r, u in zip(rows, us)]
+    assert got.tolist() == want
+    for bad in (dict(rows=[40], us=[0.5]), dict(rows=[0], us=[1.0]), dict(rows=[0], us=[-0.1]),
+                dict(rows=list(range(65)), us=[0.5] * 65)):
+        with pytest.raises(ssd.SSDError):
+            s.cdf_pick(dlg, np.array(bad["rows"]) % 65, bad["us"], T, n_rows=40)

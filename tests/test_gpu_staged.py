@@ -215,3 +215,46 @@ def test_staged_sampling_top1_is_greedy_and_top50_runs(ssd, torch):
     s50 = S.staged_sample(b4, P4, int(prompt[-1]), n_new, succ, top_k=50, seed0=3)
     assert len(s50.tokens) == n_new and all(0 <= t < cfg.vocab for t in s50.tokens)
     assert b4.o.error_count() == 0 and b4.d.error_count() == 0
+
+
+def test_staged_cdf_first_sampling(ssd, torch):
+    """CDF-first sampling (uniforms drawn first, trees assembled from the
+    draft's inverse-CDF picks, SSD_ACCEPT_SAMPLE_CDF): at T = 0.001 the
+    target is the argmax up to a precision tie, so the loop emits the plain
+    greedy sequence (a divergence only where the plain step's top-2 gap is
+    below 0.05, where T = 0.001 leaves real mass on the runner-up); the
+    assembled trees are followed (tree tokens accepted); at T = 1 it runs
+    clean."""
+    cfg = W.TINY.with_(dtype="bf16")
+    w = W.make_weights(cfg, 0, perturb_affine=True)
+    m = ssd.Model(cfg, w)
+    draft = m.prefix_view(1)
+    prompt_len, n_new = 40, 32
+    prompt = W.prefix_tokens(prompt_len, cfg.vocab, seed=5)
+    max_ctx = prompt_len + n_new + 80
+
+    def backend(gaps=False):
+        o = ssd.Session(m, max_ctx, 64)
+        d = ssd.Session(draft, max_ctx, 64, o.k_cache, o.v_cache)
+        b = S.GpuBackend(o, d, record_gaps=gaps)
+        return b, b.prefill(prompt[:-1])
+
+    b, P = backend()
+    stream = S.bigram_stream(cfg.vocab, 2048, seed=4)
+    preds = np.concatenate([b.greedy_predictions(stream[i:i + 64]) for i in range(0, 2048, 64)])
+    succ = S.bigram_table(stream, preds, cfg.vocab)
+    bp_, Pp = backend(gaps=True)
+    plain = S.plain_greedy(bp_, Pp, int(prompt[-1]), n_new)
+    b1, P1 = backend()
+    cold = S.staged_sample_cdf(b1, P1, int(prompt[-1]), n_new, succ, temperature=0.001, seed0=3)
+    n = min(len(cold.tokens), len(plain.tokens))
+    for i in range(n):
+        if cold.tokens[i] != plain.tokens[i]:
+            assert bp_.gaps[i] < 0.05, (i, cold.tokens[i], plain.tokens[i], bp_.gaps[i])
+            break
+    assert sum(cold.accepted) > 0
+    b2, P2 = backend()
+    warm = S.staged_sample_cdf(b2, P2, int(prompt[-1]), n_new, succ, temperature=1.0, seed0=5)
+    assert len(warm.tokens) == n_new and all(0 <= t < cfg.vocab for t in warm.tokens)
+    for bb in (b1, b2):
+        assert bb.o.error_count() == 0 and bb.d.error_count() == 0

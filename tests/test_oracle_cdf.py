@@ -157,3 +157,17 @@ def test_monte_carlo_detects_planted_cdf_mistakes(mutant, k):
     nz = exp > 0
     bad = counts[~nz].sum() > 0 or _chi2_p(counts[nz], exp[nz]) < 1e-6
     assert bad, mutant
+
+
+def test_cdf_pick_is_the_lone_root_draw():
+    """ssdref_cdf_pick at a node's own uniform is the SAMPLE_CDF draw there
+    (pinned above), for full-vocabulary targets."""
+    g = np.random.default_rng(12)
+    for s in range(200):
+        V = int(g.integers(2, 300))
+        T = float(g.choice([0.5, 1.0, 1.7]))
+        lg = (g.standard_normal((1, V)) * 2).astype(np.float32)
+        _, want = oracle.tree_accept(CDF, [0], [-1], lg, None, T, s)
+        assert oracle.cdf_pick(lg[0], T, oracle.uniform(s, 2, 0)) == want, s
+    with pytest.raises(oracle.OracleError):
+        oracle.cdf_pick(np.zeros(4, np.float32), 1.0, 1.0)

@@ -3,6 +3,7 @@ the draft^2 bigram table, the bigram tree, the oracle tree built from one
 draft pass (hand-computed cases), and staged greedy decoding emitting exactly
 the plain greedy sequence with the oracle as backend."""
 import numpy as np
+import pytest
 
 import oracle
 from paper_2308_04623_amd import staged as S
@@ -94,3 +95,47 @@ def test_staged_greedy_equals_plain_greedy_on_the_oracle():
     st = S.staged_greedy(backend(), len(prompt) - 1, int(prompt[-1]), n_new, succ)
     assert st.tokens == plain.tokens
     assert st.steps <= n_new and all(1 <= n <= S.MAX_ORACLE_NODES for n in st.oracle_nodes)
+
+
+def test_cdf_first_tree_hand_case():
+    """Breadth-first numbering, children from the picks at U_u + offsets
+    (duplicates dropped), bigram matches expandable, others leaves, cap."""
+    bt = np.array([5, 1, 2, 3], np.int32)
+    bp = np.array([-1, 0, 0, 1], np.int32)
+    picks = {(0, 0.5): 2, (0, 0.6): 9, (0, 0.4): 2, (2, 0.25): 7, (2, 0.35): 7, (2, 0.15): 8}
+    us = {0: 0.5, 1: 0.25}
+    pick = lambda rows, u: [picks[(r, round(x, 6))] for r, x in zip(rows, u)]
+    t, p = S.cdf_first_tree(bt, bp, 0, lambda u: us[u], pick, offsets=(0.0, 0.1, -0.1))
+    # root -> 2 (bigram node 2, expandable), 9 (leaf); node 1 (token 2) -> 7, 8
+    assert t.tolist() == [5, 2, 9, 7, 8] and p.tolist() == [-1, 0, 0, 1, 1]
+    t, p = S.cdf_first_tree(bt, bp, 0, lambda u: us[u], pick, offsets=(0.0, 0.1, -0.1), cap=4)
+    assert t.tolist() == [5, 2, 9, 7]
+
+
+@pytest.mark.slow
+def test_cdf_first_trees_keep_the_target_exact():
+    """The staged loop's CDF-first assembly with the oracle's SAMPLE_CDF walk:
+    over a Markov-table target on 6 tokens (draft = another table), the
+    joint law of the first three emitted tokens equals the target's
+    (chi-square), and the trees are followed."""
+    from tests.test_oracle_accept import V6, _cdf_pick, _chi2_p, _markov_tables
+    p_tab, q_tab = _markov_tables()
+    logit_tab = np.log(p_tab).astype(np.float32)
+    succ = np.stack([np.lexsort((np.arange(V6), -q_tab[v].astype(np.float64))) for v in range(V6)]).astype(np.int32)
+    trials, x0, hits = 12000, 2, 0
+    counts = np.zeros((V6, V6, V6))
+    for t in range(trials):
+        seq, step = [x0], 0
+        while len(seq) < 4:
+            seed = t * 8 + step
+            bt, bp = S.bigram_tree(seq[-1], succ, branch=(3, 2, 1), cap=12)
+            pick = lambda rows, us: [_cdf_pick(q_tab[bt[r]].astype(np.float64), 1.0, U) for r, U in zip(rows, us)]
+            ot, op = S.cdf_first_tree(bt, bp, seed, lambda u: oracle.uniform(seed, 2, u), pick, cap=16)
+            path, nxt = oracle.tree_accept(oracle.SAMPLE_CDF, ot, op, logit_tab[ot], None, 1.0, seed)
+            hits += len(path) - 1
+            seq += [int(ot[i]) for i in path[1:]] + [int(nxt)]
+            step += 1
+        counts[seq[1], seq[2], seq[3]] += 1
+    want = np.einsum("a,ab,bc->abc", p_tab[x0], p_tab, p_tab).ravel() * trials
+    assert _chi2_p(counts.ravel(), want) > 1e-3
+    assert hits > trials // 2
