@@ -290,6 +290,15 @@ def end_to_end(ssd, W, cfg, model, N_NEW, PROMPT):
     st_s = S.staged_sample(b_ss, P5, int(prompt[-1]), N_NEW, succ, top_k=50, seed0=11)
     log(f"end to end, top-50 sampling: plain {N_NEW / plain_s.seconds:.1f} tok/s, staged "
         f"{N_NEW / st_s.seconds:.1f} tok/s, accepted {sum(st_s.accepted)} in {st_s.steps} steps")
+    # CDF-first sampling over the whole vocabulary at T = 1: uniforms drawn
+    # first, trees assembled from the draft's inverse-CDF picks around them
+    # (SSD_ACCEPT_SAMPLE_CDF); plain steps draw from the same target
+    b_pc, P6 = backend()
+    plain_c = S.plain_sample(b_pc, P6, int(prompt[-1]), N_NEW, top_k=0, seed0=13)
+    b_sc, P7 = backend()
+    st_c = S.staged_sample_cdf(b_sc, P7, int(prompt[-1]), N_NEW, succ, temperature=1.0, seed0=13)
+    log(f"end to end, CDF-first sampling: plain {N_NEW / plain_c.seconds:.1f} tok/s, staged "
+        f"{N_NEW / st_c.seconds:.1f} tok/s, accepted {sum(st_c.accepted)} in {st_c.steps} steps")
     log(f"end to end: plain {N_NEW / plain.seconds:.1f} tok/s, staged {N_NEW / st.seconds:.1f} tok/s, "
         f"accepted {sum(st.accepted)} in {st.steps} steps, agree {agree}/{N_NEW}"
         + ("" if gap is None else f", plain top-2 gap at the divergence {gap:.3g}"))
@@ -305,7 +314,11 @@ def end_to_end(ssd, W, cfg, model, N_NEW, PROMPT):
             "top50_sampling": {"plain_tokens_per_s": round(N_NEW / plain_s.seconds, 1),
                                "staged_tokens_per_s": round(N_NEW / st_s.seconds, 1), "staged_steps": st_s.steps,
                                "accepted_tree_tokens": int(sum(st_s.accepted)),
-                               "mean_oracle_tree_nodes": round(float(np.mean(st_s.oracle_nodes)), 1)}}
+                               "mean_oracle_tree_nodes": round(float(np.mean(st_s.oracle_nodes)), 1)},
+            "cdf_first_sampling": {"plain_tokens_per_s": round(N_NEW / plain_c.seconds, 1),
+                                   "staged_tokens_per_s": round(N_NEW / st_c.seconds, 1),
+                                   "staged_steps": st_c.steps, "accepted_tree_tokens": int(sum(st_c.accepted)),
+                                   "mean_oracle_tree_nodes": round(float(np.mean(st_c.oracle_nodes)), 1)}}
 
 
 STAGES = ["LN1", "QKV", "ATT", "WO", "LN2", "FC", "WPR"]
@@ -615,6 +628,7 @@ def main():
         for name, kw in (("wor", dict(mode=ssd.SAMPLE_WOR, draft_probs=q5)),
                          ("wor_top50", dict(mode=ssd.SAMPLE_WOR, draft_probs=q5, top_k=50)),
                          ("chosen_top50", dict(mode=ssd.SAMPLE_DET, top_k=50)),
+                         ("cdf_first", dict(mode=ssd.SAMPLE_CDF)),
                          ("greedy", dict())):
             acc[name] = round(time_calls(lambda: s5.accept(tok5, par5, lg5, out=out5, seed=3, **kw), 10), 1)
         b5 = pass_bytes(cfg, n5, p5, args.q8)
