@@ -15,14 +15,32 @@ HIPCC_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
 
 
 def build(verbose: bool = False) -> str:
+    """Compiles the three sources in parallel (one hipcc per file, -fPIC
+    objects next to the library), then links them."""
     hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-    cmd = [hipcc, *HIPCC_FLAGS, "-I", os.path.join(ROOT, "include"), *SOURCES, "-o", OUT + ".tmp"]
-    r = subprocess.run(cmd, capture_output=True, text=True)
+    inc = ["-I", os.path.join(ROOT, "include")]
+    compile_flags = [f for f in HIPCC_FLAGS if f != "-shared"]
+    objs = [os.path.join(HERE, "csrc", os.path.basename(src) + ".o") for src in SOURCES]
+    procs = [subprocess.Popen([hipcc, *compile_flags, *inc, "-c", src, "-o", obj + ".tmp"],
+                              stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True)
+             for src, obj in zip(SOURCES, objs)]
+    failed = False
+    for p in procs:
+        out, err = p.communicate()
+        if p.returncode != 0:
+            sys.stderr.write(out + err)
+            failed = True
+        elif verbose:
+            sys.stderr.write(err)
+    if failed:
+        raise RuntimeError("hipcc failed")
+    for obj in objs:
+        os.replace(obj + ".tmp", obj)
+    r = subprocess.run([hipcc, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", OUT + ".tmp"],
+                       capture_output=True, text=True)
     if r.returncode != 0:
         sys.stderr.write(r.stdout + r.stderr)
-        raise RuntimeError("hipcc failed")
-    if verbose:
-        sys.stderr.write(r.stderr)
+        raise RuntimeError("hipcc link failed")
     os.replace(OUT + ".tmp", OUT)
     return OUT
 
