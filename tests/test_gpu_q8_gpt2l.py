@@ -7,8 +7,9 @@ pass, default pass mode).
   matrices bit-exact.
 - Every row and every logit (2e-2 max-abs) at 32 nodes ([4,2,2,1]) over a
   512-token prefix, 64 nodes over 1024 (both the persistent pass) and 128
-  nodes over 512 (one kernel per sub-layer), best-first trees; the
-  session's error counter at 0; greedy accept bit-exact on the GPU's logits.
+  nodes over 512 (one kernel per sub-layer), best-first trees, and the
+  256-node [8,4,2,2,1] tree over a 2048-token prefix; the session's error
+  counter at 0; greedy accept bit-exact on the GPU's logits.
 The prefix caches are synthetic N(0, 0.7) K/V."""
 import os
 
@@ -33,7 +34,7 @@ def torch():
 @pytest.fixture(scope="module")
 def big(torch):
     from paper_2308_04623_amd import ssd
-    cfg = W.GPT2L
+    cfg = W.GPT2L_LONG
     print("generating GPT-2-L weights", flush=True)
     w = W.make_weights(cfg, 0)
     om = oracle.Model(cfg, w, q8=True)
@@ -96,3 +97,12 @@ def test_gpt2l_q8_128_nodes_full_tree(big, torch):
     toks, par = W.best_first_tree(128, seed=3, vocab=cfg.vocab)
     toks[0] = 17
     _check_tree(big, torch, 512, toks, par, 128, seed=4)
+
+
+def test_gpt2l_q8_c5_256_nodes_prefix2048(big, torch):
+    """The stress point: a 256-node tree [8,4,2,2,1,...] over a 2048-token
+    prefix, every logit (the wide-tree GEMM kernel on 8-bit fragments)."""
+    cfg = big[0]
+    par = W.branching_tree([8, 4, 2, 2, 1], 256)
+    toks = W.tree_tokens(par, cfg.vocab, seed=6)
+    _check_tree(big, torch, 2048, toks, par, 256, seed=5)
