@@ -1,6 +1,6 @@
 """The allocation-free accept entry point (ssd_tree_accept_noalloc) against
 ssd_tree_accept on the same device logits, through the C ABI: greedy and
-both sampling modes, bit-exact paths and tokens, on two calls in a row
+every sampling mode, bit-exact paths and tokens, on two calls in a row
 (the second with fewer nodes and a smaller vocabulary, so the shared
 scratch holds a larger call's leftovers), plus its limits."""
 import numpy as np
@@ -40,17 +40,18 @@ def _case(g, n, V, greedy_hint):
     return toks, par, lg, q
 
 
-@pytest.mark.parametrize("mode", ["greedy", "wor", "iid", "det"])
+@pytest.mark.parametrize("mode", ["greedy", "wor", "iid", "det", "cdf"])
 def test_noalloc_accept_equals_session_accept(env, mode):
     torch, ssd, s = env
-    md = {"greedy": ssd.GREEDY, "wor": ssd.SAMPLE_WOR, "iid": ssd.SAMPLE_IID, "det": ssd.SAMPLE_DET}[mode]
-    top_k = 50 if mode == "det" else 0
+    md = {"greedy": ssd.GREEDY, "wor": ssd.SAMPLE_WOR, "iid": ssd.SAMPLE_IID, "det": ssd.SAMPLE_DET,
+          "cdf": ssd.SAMPLE_CDF}[mode]
+    top_k = 50 if mode in ("det", "cdf") else 0
     g = np.random.default_rng(len(mode))
     for call, (n, V) in enumerate([(256, 50257), (24, 3000)]):
         print(f"noalloc {mode} call {call}: n={n} V={V}", flush=True)
         toks, par, lg, q = _case(g, n, V, mode == "greedy")
         dlg = torch.from_numpy(lg).cuda()
-        dq = None if mode in ("greedy", "det") else torch.from_numpy(q).cuda()
+        dq = None if mode in ("greedy", "det", "cdf") else torch.from_numpy(q).cuda()
         a = s.accept(toks, par, dlg, mode=md, draft_probs=dq, temperature=1.0, seed=call, top_k=top_k)
         b = ssd.accept_noalloc(toks, par, dlg, _outs(torch, n), mode=md, draft_probs=dq, temperature=1.0, seed=call,
                                top_k=top_k)
