@@ -281,6 +281,13 @@ def end_to_end(ssd, W, cfg, model, N_NEW, PROMPT):
         b_gap, P3 = backend(record_gaps=True)
         S.plain_greedy(b_gap, P3, int(prompt[-1]), agree + 1)
         gap = b_gap.gaps[agree]
+    # the same reusing the draft's work: the oracle verifies the endorsed
+    # subtree only, from layer 4 on
+    b_r, P8 = backend()
+    st_r = S.staged_greedy_reuse(b_r, P8, int(prompt[-1]), N_NEW, succ)
+    agree_r = next((i for i, (a, b) in enumerate(zip(st_r.tokens, plain.tokens)) if a != b), N_NEW)
+    log(f"end to end, greedy with draft reuse: staged {N_NEW / st_r.seconds:.1f} tok/s, accepted "
+        f"{sum(st_r.accepted)} in {st_r.steps} steps, agree {agree_r}/{N_NEW}")
     # the same with top-k sampling (k = 50, T = 1): plain steps draw from the
     # oracle's top-k target; staged steps accept the draft's chosen children
     # by rejection sampling against it, so both emit that law (Sec. 2.3)
@@ -315,6 +322,10 @@ def end_to_end(ssd, W, cfg, model, N_NEW, PROMPT):
                                "staged_tokens_per_s": round(N_NEW / st_s.seconds, 1), "staged_steps": st_s.steps,
                                "accepted_tree_tokens": int(sum(st_s.accepted)),
                                "mean_oracle_tree_nodes": round(float(np.mean(st_s.oracle_nodes)), 1)},
+            "greedy_draft_reuse": {"staged_tokens_per_s": round(N_NEW / st_r.seconds, 1), "staged_steps": st_r.steps,
+                                   "accepted_tree_tokens": int(sum(st_r.accepted)),
+                                   "mean_oracle_tree_nodes": round(float(np.mean(st_r.oracle_nodes)), 1),
+                                   "tokens_equal_to_plain": agree_r},
             "cdf_first_sampling": {"plain_tokens_per_s": round(N_NEW / plain_c.seconds, 1),
                                    "staged_tokens_per_s": round(N_NEW / st_c.seconds, 1),
                                    "staged_steps": st_c.steps, "accepted_tree_tokens": int(sum(st_c.accepted)),
@@ -699,6 +710,40 @@ def main():
         s8.close()
         m8.close()
 
+    reuse = None
+    if not args.no_sweep:
+        # the oracle pass started at layer 4 from the 4-layer draft's
+        # residual stream and K/V (ssd_tree_reuse, then
+        # ssd_tree_verify_from) against the pass from the embedding, on the
+        # same best-first trees; eager calls both (host staging included),
+        # and the hand-over's own time
+        view = model.prefix_view(4)
+        ds = ssd.Session(view, max_ctx, max_nodes, sess.k_cache, sess.v_cache)
+        pts_r = []
+        for n_s in (1, 16, 32, 64):
+            tt, pp = W.best_first_tree(n_s, seed=3, vocab=cfg.vocab)
+            tt[0] = int(toks[0])
+            rows = np.arange(n_s, dtype=np.int32)
+            lg_a = torch.empty((n_s, cfg.vocab), dtype=torch.float32, device="cuda")
+            lg_b = torch.empty_like(lg_a)
+            ds.verify(P, tt, pp)
+            xr = ds.reuse_into(sess, rows)
+            us_from = time_calls(lambda: sess.verify_from(P, tt, pp, 4, xr, logits=lg_a), 30)
+            us_full = time_calls(lambda: sess.verify(P, tt, pp, logits=lg_b), 30)
+            us_hand = time_calls(lambda: ds.reuse_into(sess, rows), 30)
+            torch.cuda.synchronize()
+            pts_r.append({"nodes": n_s, "prefix": P, "us_from_layer4": round(us_from, 1),
+                          "us_from_embedding": round(us_full, 1), "us_handover": round(us_hand, 1),
+                          "logits_bitwise_equal": bool(torch.equal(lg_a, lg_b)),
+                          "path": "persistent" if sess.verify_path(n_s) == ssd.PASS_FUSED else "per-sub-layer"})
+        if sess.error_count() or ds.error_count():
+            raise SystemExit("a session's error counter grew during the reuse points")
+        ds.close()
+        reuse = {"workload": "oracle pass over a best-first tree the 4-layer draft already ran, started at layer 4 "
+                             "from the draft's residual stream and layer 0-3 K/V, against the pass from the "
+                             "embedding (eager calls)", "points": pts_r}
+        log(f"draft reuse: {pts_r}")
+
     e2e = None
     if not args.no_e2e:
         e2e = end_to_end(ssd, W, cfg, model, N_NEW=256, PROMPT=128)
@@ -763,6 +808,7 @@ def main():
         "pass_algorithmic_bytes": B,
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "draft_reuse": reuse,
         "end_to_end": e2e,
         "sweep": sweep,
         "sweep_summary": crossover,

@@ -182,6 +182,42 @@ ssd_status ssd_tree_verify_greedy(const ssd_model *m, ssd_kv *kv, int32_t prefix
                                   const int32_t *parent_idx, int32_t n_nodes, float *logits, int32_t *accepted_path,
                                   int32_t *path_len, int32_t *next_token, void *stream);
 
+/* The verification pass from layer start_layer on, for a tree whose first
+ * layers a draft already ran.  The paper does not describe this (its draft,
+ * Sec. 3.2 and 4, is a separate small model): it applies when the draft is
+ * ssd_model_prefix_view of this model, whose layers are this model's first
+ * ones, so their outputs for a node are the oracle's.  x_in ([n_nodes][d_model] fp32,
+ * device) is every node's residual stream at the input of start_layer, and
+ * the session's tree scratch rows 0..n_nodes-1 must already hold the nodes'
+ * K/V of layers 0..start_layer-1 (ssd_tree_reuse provides both).  Layers
+ * start_layer.. then run exactly as in ssd_tree_verify, which a pass from
+ * layer 0 is.  With accepted_path, path_len and next_token all set, the
+ * greedy walk of ssd_tree_verify_greedy follows; all NULL, none.  Errors:
+ * as ssd_tree_verify, plus SSD_E_INVALID_ARG for start_layer outside
+ * [0, n_layer), a NULL x_in with start_layer > 0, or greedy outputs only
+ * partly set. */
+ssd_status ssd_tree_verify_from(const ssd_model *m, ssd_kv *kv, int32_t prefix_len, const int32_t *tree_tokens,
+                                const int32_t *parent_idx, int32_t n_nodes, int32_t start_layer, const float *x_in,
+                                float *logits, int32_t *accepted_path, int32_t *path_len, int32_t *next_token,
+                                void *stream);
+
+/* Hands a draft pass's work to the oracle's session for ssd_tree_verify_from:
+ * for i < n, the tree K/V rows at src's tree scratch row src_rows[i] of
+ * every layer that src's last pass ran (the last ssd_tree_verify,
+ * ssd_tree_verify_greedy, ssd_tree_verify_from or graph launch on src) go
+ * to dst's tree scratch row i, and the residual stream that pass left for
+ * node src_rows[i] (after its last layer) goes to x_out[i] ([n][d_model]
+ * fp32, device); ssd_tree_verify_from then starts at that layer count.
+ * The model of that pass must be a layer prefix of dst's
+ * (ssd_model_prefix_view), and the two sessions' tree scratch buffers must
+ * not overlap.  Enqueue on the stream of that pass, after it.
+ * 1 <= n <= min(256, dst's max_nodes); src_rows is a HOST array, each
+ * below the node count of src's last pass.  Errors: SSD_E_INVALID_ARG
+ * (null, src == dst, shapes, no pass yet, a row outside the last pass),
+ * SSD_E_CAPACITY, SSD_E_DEVICE. */
+ssd_status ssd_tree_reuse(const ssd_kv *src, ssd_kv *dst, int32_t n, const int32_t *src_rows, float *x_out,
+                          void *stream);
+
 /* Accept/reject walk (Sec. 2.3, 3.1) over logits from ssd_tree_verify.
  *  greedy: a node is kept when its parent is kept and its token is the
  *    parent's argmax (lowest token id on ties); the deepest kept node (lowest

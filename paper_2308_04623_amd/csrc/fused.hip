@@ -472,7 +472,7 @@ __device__ __forceinline__ void xs_add(const FusedArgs& a, int k, int n, int o, 
 // Wave 0 polls with nothing else in flight (a wave's loads complete in
 // order, so anything issued before would delay the poll); every load of
 // every row is issued together right after it.
-template <int C, int R>
+template <int C, int R, bool RE>
 __device__ __forceinline__ bool ln_rows_q(const FusedArgs& a, const Wg& w, const WaitSpec& ws, int n0, int mode,
                                           gptr<uint16_t> bias, int kin, unsigned zmask, gptr<uint16_t> g,
                                           gptr<uint16_t> b, uint16_t* act) {
@@ -507,7 +507,15 @@ __device__ __forceinline__ bool ln_rows_q(const FusedArgs& a, const Wg& w, const
     gr[i] = g4[cc[i]];
     br[i] = b4[cc[i]];
   }
-  if (mode == 0) {
+  if (RE && mode == 0) {
+    // the pass starts at a later layer: the rows' residual stream as given
+#pragma unroll
+    for (int j = 0; j < R; ++j) {
+      const gptr<f32x4> xi = (gptr<f32x4>)opq(a.x_in + (size_t)nr[j] * d);
+#pragma unroll
+      for (int i = 0; i < C; ++i) v[j][i] = xi[cc[i]];
+    }
+  } else if (mode == 0) {
     u32x2 tr[R][C], pr[R][C];
 #pragma unroll
     for (int j = 0; j < R; ++j) {
@@ -764,7 +772,7 @@ __device__ __forceinline__ void stage_frags(gptr<u32x4> W, const int* rbs, int n
 
 // Run by waves 0..3 together: the LayerNorm rows, then the stage is
 // published (the four waves' stores complete, then wave 0 writes the flag).
-template <bool Q8>
+template <bool Q8, bool RE>
 __device__ __forceinline__ bool do_pre(const FusedArgs& a, const Wg& w, const PreSpec& ps) {
   if (ps.kind == 0) return true;
   bool ok = true;
@@ -772,11 +780,11 @@ __device__ __forceinline__ bool do_pre(const FusedArgs& a, const Wg& w, const Pr
     // this rank's rows: w.r and (at more than 32 nodes) w.r + 32, together
     const bool two = w.r + kFRanks < a.N;
     if (a.d <= 1024)
-      ok = two ? ln_rows_q<1, 2>(a, w, ps.ws, w.r, ps.mode, ps.bias, ps.kin, ps.zmask, ps.g, ps.b, ps.act)
-               : ln_rows_q<1, 1>(a, w, ps.ws, w.r, ps.mode, ps.bias, ps.kin, ps.zmask, ps.g, ps.b, ps.act);
+      ok = two ? ln_rows_q<1, 2, RE>(a, w, ps.ws, w.r, ps.mode, ps.bias, ps.kin, ps.zmask, ps.g, ps.b, ps.act)
+               : ln_rows_q<1, 1, RE>(a, w, ps.ws, w.r, ps.mode, ps.bias, ps.kin, ps.zmask, ps.g, ps.b, ps.act);
     else
-      ok = two ? ln_rows_q<2, 2>(a, w, ps.ws, w.r, ps.mode, ps.bias, ps.kin, ps.zmask, ps.g, ps.b, ps.act)
-               : ln_rows_q<2, 1>(a, w, ps.ws, w.r, ps.mode, ps.bias, ps.kin, ps.zmask, ps.g, ps.b, ps.act);
+      ok = two ? ln_rows_q<2, 2, RE>(a, w, ps.ws, w.r, ps.mode, ps.bias, ps.kin, ps.zmask, ps.g, ps.b, ps.act)
+               : ln_rows_q<2, 1, RE>(a, w, ps.ws, w.r, ps.mode, ps.bias, ps.kin, ps.zmask, ps.g, ps.b, ps.act);
   }
   if (!ok) return false;
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -843,7 +851,7 @@ struct HeadBest {
 // last one and are not stored.  Q8: the matrix is in 8-bit fragments (512 B,
 // widened to float16 in registers) followed by its rows' float32 scales
 // ([ceil(M / 16) 16]); each output is scaled by its row's before the bias.
-template <int NT, int RB, int U, bool Q8>
+template <int NT, int RB, int U, bool Q8, bool RE>
 __device__ __forceinline__ bool gemm_rb(const FusedArgs& a, const Wg& w, const WaitSpec& ws, int epi, int l,
                                         const int* rbs, int rb_first, int nrb, gptr<uint16_t> bias, gptr<u32x4> Wp,
                                         int KC, int M, int kc0, int kc1, const uint16_t* act, int act_kc,
@@ -920,7 +928,7 @@ __device__ __forceinline__ bool gemm_rb(const FusedArgs& a, const Wg& w, const W
   // (the loads sit in the branch wave 0 does not take, so the weight
   // registers are not live across the pre-stage's code)
   if (wv < QW) {
-    bool ok = do_pre<Q8>(a, w, ps);
+    bool ok = do_pre<Q8, RE>(a, w, ps);
     if (wv == 0) {
       stamp(a, w, ws.sl, ws.sfid, 0);
       if (ok && ws.on) ok = poll_w0(a, w, ws.id, ws.wx, ws.tag);
@@ -1005,11 +1013,11 @@ __device__ __forceinline__ bool gemm_rb(const FusedArgs& a, const Wg& w, const W
 // two keep 6; four row blocks keep 8 at one tile, 5 at two, 3 at four: deeper
 // would spill); three code bodies serve every stage
 // Runs the pre-stage (wave 0) when the workgroup has no GEMM task.
-template <bool Q8>
+template <bool Q8, bool RE>
 __device__ __forceinline__ bool pre_only(const FusedArgs& a, const Wg& w, const PreSpec& ps) {
   if (ps.kind == 0) return true;
   if (threadIdx.x < QW * 64) {
-    const bool ok = do_pre<Q8>(a, w, ps);
+    const bool ok = do_pre<Q8, RE>(a, w, ps);
     if (threadIdx.x == 0) w.sh[0] = ok;
   }
   lds_barrier();
@@ -1018,20 +1026,20 @@ __device__ __forceinline__ bool pre_only(const FusedArgs& a, const Wg& w, const 
   return ok;
 }
 
-template <int NT, bool Q8>
+template <int NT, bool Q8, bool RE>
 __device__ __forceinline__ bool gemm_task(const FusedArgs& a, const Wg& w, const WaitSpec& ws, int epi, int l,
                                           const int* rbs, int rb_first, int nrb, gptr<uint16_t> bias,
                                           gptr<u32x4> Wp, int KC, int M, int kc0, int kc1, const uint16_t* act,
                                           int act_kc, float* red, const PreSpec& ps, int wofs,
                                           HeadBest& hb, bool track) {
-  if (nrb <= 0) return pre_only<Q8>(a, w, ps);
+  if (nrb <= 0) return pre_only<Q8, RE>(a, w, ps);
   if (nrb == 1)
-    return gemm_rb<NT, 1, NT <= 2 ? 10 : 8, Q8>(a, w, ws, epi, l, rbs, rb_first, 1, bias, Wp, KC, M, kc0, kc1, act,
+    return gemm_rb<NT, 1, NT <= 2 ? 10 : 8, Q8, RE>(a, w, ws, epi, l, rbs, rb_first, 1, bias, Wp, KC, M, kc0, kc1, act,
                                            act_kc, red, ps, wofs, hb, track);
   if (nrb == 2)
-    return gemm_rb<NT, 2, NT <= 2 ? 10 : 6, Q8>(a, w, ws, epi, l, rbs, rb_first, 2, bias, Wp, KC, M, kc0, kc1, act,
+    return gemm_rb<NT, 2, NT <= 2 ? 10 : 6, Q8, RE>(a, w, ws, epi, l, rbs, rb_first, 2, bias, Wp, KC, M, kc0, kc1, act,
                                            act_kc, red, ps, wofs, hb, track);
-  return gemm_rb<NT, 4, NT == 1 ? 8 : NT == 2 ? 5 : 3, Q8>(a, w, ws, epi, l, rbs, rb_first, nrb, bias, Wp, KC, M, kc0,
+  return gemm_rb<NT, 4, NT == 1 ? 8 : NT == 2 ? 5 : 3, Q8, RE>(a, w, ws, epi, l, rbs, rb_first, nrb, bias, Wp, KC, M, kc0,
                                                             kc1, act, act_kc, red, ps, wofs, hb, track);
 }
 
@@ -1346,7 +1354,7 @@ __device__ __forceinline__ bool att_root_unit(const FusedArgs& a, const Wg& w, c
 
 // ------------------------------------------------------------------ compute workgroups
 
-template <int NT, bool Q8>
+template <int NT, bool Q8, bool RE>
 __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* lds) {
   int* sh = (int*)(lds + A_REGION + A_PART_BYTES + A_Q_BYTES);  // 32 words
   int* lplan = sh + 32;                                            // [kPlanStride]
@@ -1432,8 +1440,8 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
   const int wo_ofs = A_REGION + A_PART_BYTES + A_Q_BYTES + 256 + L * kLwSlots * 8;
   const bool wo_staged = NT >= 2 && n_wo > 0 && n_wo * (kh1 - kh0) <= WO_FRAGS;
   HeadBest hbest{{-INFINITY, -INFINITY}, {0x7fffffff, 0x7fffffff}};
-  const int nst = L * 8 + 2;
-  for (int st = 0; st < nst; ++st) {
+  const int nst = L * 8 + 2, L0 = RE ? a.l0 : 0;  // (L0: the first layer this pass runs)
+  for (int st = L0 * 8; st < nst; ++st) {
     const int l = st < L * 8 ? st / 8 : L;
     const int kind = st < L * 8 ? st % 8 : 8 + (st - L * 8);
     if (kind == 1 || kind == 3 || kind == 6 || kind == 9) continue;  // run with the stage before them, or none
@@ -1487,10 +1495,10 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
       stamp(a, w, l, fid, 0);
       const WaitSpec ws{wo ? FS_ATT : FS_FC, w.x, tag_of(w, l, wo ? FS_ATT : FS_FC), true, l, fid};
       PreSpec nopre{};
-      const bool ok = wo ? gemm_task<NT, Q8>(a, w, ws, FE_WO, l, p + PL_WO + 1, 0, n_wo, G<uint16_t>(nullptr),
+      const bool ok = wo ? gemm_task<NT, Q8, RE>(a, w, ws, FE_WO, l, p + PL_WO + 1, 0, n_wo, G<uint16_t>(nullptr),
                                          G<u32x4>(lw(w, l, LW_O)), KCd, d, kh0, kh1, a.fo, KCd, red, nopre,
                                          wo_staged ? wo_ofs : 0, hbest, false)
-                         : gemm_task<NT, Q8>(a, w, ws, FE_WPR, l, p + PL_WPR + 1, 0, n_wpr, G<uint16_t>(nullptr),
+                         : gemm_task<NT, Q8, RE>(a, w, ws, FE_WPR, l, p + PL_WPR + 1, 0, n_wpr, G<uint16_t>(nullptr),
                                          G<u32x4>(lw(w, l, LW_PR)), KCm, d, kf0, kf1, a.ff, KCm, red, nopre,
                                          wpr_staged ? WST : 0, hbest, false);
       if (!ok) goto out;
@@ -1513,7 +1521,7 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
     ps.l = l;
     ps.kind = 1;
     ps.fid = kind == 5 ? FS_LN2 : FS_LN1;
-    ps.mode = (kind == 0 && l == 0) ? 0 : 1;
+    ps.mode = (kind == 0 && l == L0) ? 0 : 1;
     if (kind == 5) {
       if (wpr_staged && !wpr_early) {
         ps.wn = n_wpr;
@@ -1542,11 +1550,12 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
         ps.wW = G<u32x4>(lw(w, l, LW_O));
       }
       const int lp = kind == 8 ? L - 1 : max(l - 1, 0);
-      ps.ws = WaitSpec{FS_WPR, -1, tag_of(w, lp, FS_WPR), kind == 8 || l > 0, l, FS_LN1};
+      ps.ws = WaitSpec{FS_WPR, -1, tag_of(w, lp, FS_WPR), kind == 8 || l > L0, l, FS_LN1};
       ps.bias = G<uint16_t>(lw(w, lp, LB_PR));
       ps.kin = 2 * lp + 1;
-      // sub-layer 2lp's buffer; the first layer clears the first two
-      ps.zmask = ps.mode == 0 ? 3u : 1u << ((2 * lp) % 3);
+      // sub-layer 2lp's buffer; the pass's first layer clears the two its
+      // own sub-layers add into
+      ps.zmask = ps.mode == 0 ? (1u << ((2 * l) % 3)) | (1u << ((2 * l + 1) % 3)) : 1u << ((2 * lp) % 3);
       ps.g = kind == 8 ? G<uint16_t>(a.lnf_g) : G<uint16_t>(lw(w, l, LN1G));
       ps.b = kind == 8 ? G<uint16_t>(a.lnf_b) : G<uint16_t>(lw(w, l, LN1B));
       ps.act = act1;
@@ -1568,8 +1577,8 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
     {
       // (the first QKV stage waits for every XCD's first LayerNorm, which
       // clears the first two sum buffers: see xs_zero)
-      const WaitSpec gws{ps.fid, (kind == 0 && l == 0) ? -1 : w.x, tag_of(w, l, ps.fid), true, l, gfid};
-      if (!gemm_task<NT, Q8>(a, w, gws, epi, l, rbs, rb_first, nrb, bias, Wm, KCd, Mo, k0, k1, act, KCd, red, ps, 0,
+      const WaitSpec gws{ps.fid, (kind == 0 && l == L0) ? -1 : w.x, tag_of(w, l, ps.fid), true, l, gfid};
+      if (!gemm_task<NT, Q8, RE>(a, w, gws, epi, l, rbs, rb_first, nrb, bias, Wm, KCd, Mo, k0, k1, act, KCd, red, ps, 0,
                          hbest, kind == 8))
         goto out;
     }
@@ -1578,7 +1587,7 @@ __device__ __forceinline__ void compute_wg(const FusedArgs& a, unsigned char* ld
       const WaitSpec none{0, 0, 0u, false, l, gfid};
       PreSpec nopre{};
       for (int b0 = hb0 + 4, j = 1; b0 < hb1; b0 += 4, ++j) {
-        if (!gemm_task<NT, Q8>(a, w, none, FE_HEAD, L, nullptr, b0, min(4, hb1 - b0), G<uint16_t>(nullptr),
+        if (!gemm_task<NT, Q8, RE>(a, w, none, FE_HEAD, L, nullptr, b0, min(4, hb1 - b0), G<uint16_t>(nullptr),
                            G<u32x4>(a.p_head), KCd, a.V, 0, KCd, act1, KCd, red, nopre, 0, hbest, true))
           goto out;
       }
@@ -1619,10 +1628,11 @@ out:
 }
 
 
-template <int NT, bool Q8>
+// RE: the pass starts at layer a.l0 from the residual stream a.x_in
+template <int NT, bool Q8, bool RE>
 __global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(2))) void pass_kernel(FusedArgs a) {
   extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
-  compute_wg<NT, Q8>(a, lds);
+  compute_wg<NT, Q8, RE>(a, lds);
 }
 
 }  // namespace fz
@@ -1748,11 +1758,15 @@ bool fused_plan(int H, int d, int M, int V, int ntiles, int* tab, int* xh, int* 
 
 hipError_t fused_prepare() {
   const int lds = (int)fused_lds_bytes(kFMaxL);
-  const void* fns[6] = {(const void*)fz::pass_kernel<1, false>, (const void*)fz::pass_kernel<2, false>,
-                        (const void*)fz::pass_kernel<4, false>, (const void*)fz::pass_kernel<1, true>,
-                        (const void*)fz::pass_kernel<2, true>,  (const void*)fz::pass_kernel<4, true>};
+  const void* fns[] = {
+      (const void*)fz::pass_kernel<1, false, false>, (const void*)fz::pass_kernel<2, false, false>,
+      (const void*)fz::pass_kernel<4, false, false>, (const void*)fz::pass_kernel<1, true, false>,
+      (const void*)fz::pass_kernel<2, true, false>,  (const void*)fz::pass_kernel<4, true, false>,
+      (const void*)fz::pass_kernel<1, false, true>,  (const void*)fz::pass_kernel<2, false, true>,
+      (const void*)fz::pass_kernel<4, false, true>,  (const void*)fz::pass_kernel<1, true, true>,
+      (const void*)fz::pass_kernel<2, true, true>,   (const void*)fz::pass_kernel<4, true, true>};
   hipError_t e = hipSuccess;
-  for (int i = 0; i < 6 && e == hipSuccess; ++i)
+  for (size_t i = 0; i < sizeof(fns) / sizeof(fns[0]) && e == hipSuccess; ++i)
     e = hipFuncSetAttribute(fns[i], hipFuncAttributeMaxDynamicSharedMemorySize, lds);
   return e;
 }
@@ -1767,23 +1781,29 @@ static_assert(fz::A_REGION + fz::A_PART_BYTES + fz::A_Q_BYTES + 128 + kPlanStrid
                       fz::WO_FRAGS * 1024 <= 160 * 1024,
               "the persistent pass's LDS must fit a gfx950 workgroup (160 KB)");
 
+template <bool Q8, bool RE>
+static void launch_tiles(const FusedArgs& a, int nt, dim3 grid, size_t lds, hipStream_t s) {
+  switch (nt) {
+    case 1: fz::pass_kernel<1, Q8, RE><<<grid, fz::NTH, lds, s>>>(a); break;
+    case 2: fz::pass_kernel<2, Q8, RE><<<grid, fz::NTH, lds, s>>>(a); break;
+    default: fz::pass_kernel<4, Q8, RE><<<grid, fz::NTH, lds, s>>>(a); break;
+  }
+}
+
 hipError_t launch_fused(const FusedArgs& a, hipStream_t s) {
   if (a.N <= 0 || a.N > kFMaxN || a.d % 32 || a.M % 32 || a.d > 2048 || a.H * fz::DH != a.d) return hipErrorInvalidValue;
+  if (a.l0 < 0 || a.l0 >= a.L || (a.l0 > 0 && !a.x_in)) return hipErrorInvalidValue;
   const int nt = (a.N + 15) / 16;
   const size_t lds = fused_lds_bytes(a.L);
   const dim3 grid(kFGroups);
+  // (the variants: 16- or 8-bit weights, a pass from the embedding or from
+  // a later layer's residual stream)
   if (a.q8) {
-    switch (nt) {
-      case 1: fz::pass_kernel<1, true><<<grid, fz::NTH, lds, s>>>(a); break;
-      case 2: fz::pass_kernel<2, true><<<grid, fz::NTH, lds, s>>>(a); break;
-      default: fz::pass_kernel<4, true><<<grid, fz::NTH, lds, s>>>(a); break;
-    }
+    if (a.l0 > 0) launch_tiles<true, true>(a, nt, grid, lds, s);
+    else launch_tiles<true, false>(a, nt, grid, lds, s);
   } else {
-    switch (nt) {
-      case 1: fz::pass_kernel<1, false><<<grid, fz::NTH, lds, s>>>(a); break;
-      case 2: fz::pass_kernel<2, false><<<grid, fz::NTH, lds, s>>>(a); break;
-      default: fz::pass_kernel<4, false><<<grid, fz::NTH, lds, s>>>(a); break;
-    }
+    if (a.l0 > 0) launch_tiles<false, true>(a, nt, grid, lds, s);
+    else launch_tiles<false, false>(a, nt, grid, lds, s);
   }
   return hipGetLastError();
 }

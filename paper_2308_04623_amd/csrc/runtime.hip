@@ -130,6 +130,10 @@ struct ssd_kv {
   void* fz_ws = nullptr;
   FusedArgs fz{};                      // workspace pointers, XCD ranges
   int* fz_plan[5] = {};                // device plans per 16-node tile count (1..4)
+  // the last enqueued pass: where it left its residual stream (fz.xr or x),
+  // its node count and its model's layer count (0: none yet)
+  bool resid_fused = false;
+  int last_n = 0, last_layers = 0;
 };
 
 struct ssd_graph {
@@ -761,8 +765,12 @@ static int resid_splits(const ssd_model* m, int path, int n, int rows, int K) {
   return S;
 }
 
+// l0 > 0: the pass starts at layer l0 from the residual stream x_in
+// ([n][d] fp32, device), the tree scratch already holding the nodes' K/V of
+// layers below l0.
 static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int32_t n, const char* stage_host,
-                                 size_t stage_used, float* logits, hipStream_t s) {
+                                 size_t stage_used, float* logits, hipStream_t s, int l0 = 0,
+                                 const float* x_in = nullptr) {
   const ssd_config& c = m->cfg;
   const int d = c.d_model, H = c.n_head, DH = m->dh, M = c.d_mlp, V = c.vocab, L = c.n_layer;
   const int maxn = kv->max_nodes;
@@ -803,14 +811,25 @@ static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int3
     a.logits = logits;
     a.plan = kv->fz_plan[(n + 15) / 16];
     a.att_units = (P + kFAttRows - 1) / kFAttRows;
+    a.l0 = l0;
+    a.x_in = l0 > 0 ? x_in : nullptr;
     HIP_TRY(launch_fused(a, s));
+    kv->resid_fused = true;
+    kv->last_n = n;
+    kv->last_layers = L;
     return SSD_OK;
   }
   if (kv->pass_mode == 2) return fail(SSD_E_UNSUPPORTED, "the persistent pass does not apply to this model, session or tree");
   const int gp = kv->gemm_path;
   const bool q8 = m->q8;
-  unsigned long long* sig = f32 ? nullptr : kv->d_sig;  // pass signals (bf16 models)
-  HIP_TRY(launch_embed(f32, m->wte, m->wpe, d_tok, d_pos, n, d, kv->x, sig, kv->d_xcc0, s));
+  // pass signals (bf16 models; none for a pass that starts past layer 0,
+  // which runs without the prefetcher)
+  unsigned long long* sig = f32 || l0 > 0 ? nullptr : kv->d_sig;
+  kv->resid_fused = false;
+  kv->last_n = n;
+  kv->last_layers = L;
+  if (l0 > 0) HIP_TRY(hipMemcpyAsync(kv->x, x_in, (size_t)n * d * 4, hipMemcpyDeviceToDevice, s));
+  else HIP_TRY(launch_embed(f32, m->wte, m->wpe, d_tok, d_pos, n, d, kv->x, sig, kv->d_xcc0, s));
 
   // GEMM-input leading dimensions (fp32: row stride; bf16: k-steps)
   const int ld_d = f32 ? d : d / 32, ld_m = f32 ? M : M / 32;
@@ -823,7 +842,7 @@ static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int3
 
   int pend_S = 0;               // partials waiting to be added to x
   const void* pend_bias = nullptr;
-  for (int l = 0; l < L; ++l) {
+  for (int l = l0; l < L; ++l) {
     HIP_TRY(launch_ln(f32, kv->x, n, d, kv->part, pend_S, pstride, pend_bias, m->ln1_g[l], m->ln1_b[l], c.ln_eps,
                       kv->act_a, ld_d, sig, kv->d_err, s));
     Epi e{};
@@ -937,14 +956,17 @@ static ssd_status enqueue_greedy_after_pass(const ssd_model* m, ssd_kv* kv, int3
   return SSD_OK;
 }
 
-extern "C" ssd_status ssd_tree_verify_greedy(const ssd_model* m, ssd_kv* kv, int32_t prefix_len,
-                                             const int32_t* tree_tokens, const int32_t* parent_idx, int32_t n_nodes,
-                                             float* logits, int32_t* accepted_path, int32_t* path_len,
-                                             int32_t* next_token, void* stream) {
-  if (!accepted_path || !path_len || !next_token) return fail(SSD_E_INVALID_ARG, "null output");
+// The eager verification entry points: the pass (from layer l0, see
+// enqueue_verify), then with accepted_path set the greedy walk.
+static ssd_status verify_entry(const ssd_model* m, ssd_kv* kv, int32_t prefix_len, const int32_t* tree_tokens,
+                               const int32_t* parent_idx, int32_t n_nodes, int32_t l0, const float* x_in,
+                               float* logits, int32_t* accepted_path, int32_t* path_len, int32_t* next_token,
+                               void* stream) {
   int32_t md = 0;
   ssd_status st = check_verify_args(m, kv, prefix_len, tree_tokens, parent_idx, n_nodes, logits, &md);
   if (st != SSD_OK) return st;
+  if (l0 < 0 || l0 >= m->cfg.n_layer) return fail(SSD_E_INVALID_ARG, "start_layer outside [0, n_layer)");
+  if (l0 > 0 && !x_in) return fail(SSD_E_INVALID_ARG, "null x_in with start_layer > 0");
   hipStream_t s = (hipStream_t)stream;
   char* host = nullptr;
   int slot = -1;
@@ -952,28 +974,40 @@ extern "C" ssd_status ssd_tree_verify_greedy(const ssd_model* m, ssd_kv* kv, int
   if (st != SSD_OK) return st;
   const size_t used = fill_stage(host, prefix_len, tree_tokens, parent_idx, n_nodes, kv->max_nodes);
   const bool fused = use_fused(m, kv, n_nodes);
-  st = start_pass_prefetch(m, kv, n_nodes, fused, kv->gemm_path);
-  if (st == SSD_OK) st = enqueue_verify(m, kv, prefix_len, n_nodes, host, used, logits, s);
-  if (st == SSD_OK) st = enqueue_greedy_after_pass(m, kv, n_nodes, fused, logits, accepted_path, path_len, next_token, s);
+  // (a pass from a later layer runs without the weight prefetcher, whose
+  // signal schedule assumes every layer)
+  if (l0 == 0) st = start_pass_prefetch(m, kv, n_nodes, fused, kv->gemm_path);
+  if (st == SSD_OK) st = enqueue_verify(m, kv, prefix_len, n_nodes, host, used, logits, s, l0, x_in);
+  if (st == SSD_OK && accepted_path)
+    st = enqueue_greedy_after_pass(m, kv, n_nodes, fused, logits, accepted_path, path_len, next_token, s);
   ssd_status st2 = release_slot(kv, slot, s);
   return st != SSD_OK ? st : st2;
 }
 
+extern "C" ssd_status ssd_tree_verify_greedy(const ssd_model* m, ssd_kv* kv, int32_t prefix_len,
+                                             const int32_t* tree_tokens, const int32_t* parent_idx, int32_t n_nodes,
+                                             float* logits, int32_t* accepted_path, int32_t* path_len,
+                                             int32_t* next_token, void* stream) {
+  if (!accepted_path || !path_len || !next_token) return fail(SSD_E_INVALID_ARG, "null output");
+  return verify_entry(m, kv, prefix_len, tree_tokens, parent_idx, n_nodes, 0, nullptr, logits, accepted_path,
+                      path_len, next_token, stream);
+}
+
 extern "C" ssd_status ssd_tree_verify(const ssd_model* m, ssd_kv* kv, int32_t prefix_len, const int32_t* tree_tokens,
                                       const int32_t* parent_idx, int32_t n_nodes, float* logits, void* stream) {
-  int32_t md = 0;
-  ssd_status st = check_verify_args(m, kv, prefix_len, tree_tokens, parent_idx, n_nodes, logits, &md);
-  if (st != SSD_OK) return st;
-  hipStream_t s = (hipStream_t)stream;
-  char* host = nullptr;
-  int slot = -1;
-  st = acquire_slot(kv, &host, &slot);
-  if (st != SSD_OK) return st;
-  const size_t used = fill_stage(host, prefix_len, tree_tokens, parent_idx, n_nodes, kv->max_nodes);
-  st = start_pass_prefetch(m, kv, n_nodes, use_fused(m, kv, n_nodes), kv->gemm_path);
-  if (st == SSD_OK) st = enqueue_verify(m, kv, prefix_len, n_nodes, host, used, logits, s);
-  ssd_status st2 = release_slot(kv, slot, s);
-  return st != SSD_OK ? st : st2;
+  return verify_entry(m, kv, prefix_len, tree_tokens, parent_idx, n_nodes, 0, nullptr, logits, nullptr, nullptr,
+                      nullptr, stream);
+}
+
+extern "C" ssd_status ssd_tree_verify_from(const ssd_model* m, ssd_kv* kv, int32_t prefix_len,
+                                           const int32_t* tree_tokens, const int32_t* parent_idx, int32_t n_nodes,
+                                           int32_t start_layer, const float* x_in, float* logits,
+                                           int32_t* accepted_path, int32_t* path_len, int32_t* next_token,
+                                           void* stream) {
+  if (!accepted_path != !path_len || !accepted_path != !next_token)
+    return fail(SSD_E_INVALID_ARG, "the greedy outputs must be all set or all NULL");
+  return verify_entry(m, kv, prefix_len, tree_tokens, parent_idx, n_nodes, start_layer, x_in, logits, accepted_path,
+                      path_len, next_token, stream);
 }
 
 static ssd_status capture_pass(const ssd_model* m, ssd_kv* kv, int32_t prefix_len, const int32_t* tree_tokens,
@@ -1027,7 +1061,7 @@ static ssd_status capture_pass(const ssd_model* m, ssd_kv* kv, int32_t prefix_le
     ssd_graph_destroy(g);
     return fail(SSD_E_DEVICE, std::string("hipStreamBeginCapture: ") + hipGetErrorString(e));
   }
-  st = enqueue_verify(m, kv, prefix_len, n_nodes, g->pinned, used, logits, cs);
+  st = enqueue_verify(m, kv, prefix_len, n_nodes, g->pinned, used, logits, cs, 0, nullptr);
   if (st == SSD_OK && path) st = enqueue_greedy_after_pass(m, kv, n_nodes, g->fused, logits, path, path_len, next, cs);
   hipGraph_t graph = nullptr;
   e = hipStreamEndCapture(cs, &graph);
@@ -1052,6 +1086,9 @@ extern "C" ssd_status ssd_graph_launch(ssd_graph* g, void* stream) {
   const ssd_status st = start_pass_prefetch(g->m, g->kv, g->n, g->fused, g->gemm_path);
   if (st != SSD_OK) return st;
   HIP_TRY(hipGraphLaunch(g->exec, (hipStream_t)stream));
+  g->kv->resid_fused = g->fused;
+  g->kv->last_n = g->n;
+  g->kv->last_layers = g->m->cfg.n_layer;
   return SSD_OK;
 }
 
@@ -1397,5 +1434,64 @@ extern "C" ssd_status ssd_cdf_pick(ssd_kv* kv, const float* logits, int32_t n_ro
     a.U[q] = uniforms[q];
   }
   HIP_TRY(launch_cdf_pick(a, (hipStream_t)stream));
+  return SSD_OK;
+}
+
+// ------------------------------------------------------------------ draft work reused by the oracle pass
+
+// Block i copies node src_rows[i]'s tree K/V rows of the first LH / H layers
+// and its residual row into the destination's slot i.
+constexpr int kMaxReuse = 256;
+struct ReuseArgs {
+  const unsigned char *ks, *vs;
+  unsigned char *kd, *vd;
+  const float* xs;
+  float* xd;
+  int LH, src_rows, dst_rows, row_bytes, d;
+  int rows[kMaxReuse];
+};
+
+__global__ __launch_bounds__(256) void tree_reuse_kernel(ReuseArgs a) {
+  const int i = blockIdx.x, sr = a.rows[i];
+  const int per = a.row_bytes / 16;  // 16-byte pieces of a K or V row
+  for (int t = threadIdx.x; t < a.LH * per; t += 256) {
+    const int lh = t / per, c = t - lh * per;
+    const size_t so = ((size_t)lh * a.src_rows + sr) * a.row_bytes + 16 * c;
+    const size_t dof = ((size_t)lh * a.dst_rows + i) * a.row_bytes + 16 * c;
+    *(uint4*)(a.kd + dof) = *(const uint4*)(a.ks + so);
+    *(uint4*)(a.vd + dof) = *(const uint4*)(a.vs + so);
+  }
+  for (int t = threadIdx.x; t < a.d; t += 256) a.xd[(size_t)i * a.d + t] = a.xs[(size_t)sr * a.d + t];
+}
+
+extern "C" ssd_status ssd_tree_reuse(const ssd_kv* src, ssd_kv* dst, int32_t n, const int32_t* src_rows, float* x_out,
+                                     void* stream) {
+  if (!src || !dst || !src_rows || !x_out) return fail(SSD_E_INVALID_ARG, "null argument");
+  if (src == dst) return fail(SSD_E_INVALID_ARG, "source and destination sessions must differ");
+  const ssd_config &cs = src->m->cfg, &cd = dst->m->cfg;
+  if (!same_shape_prefix(cs, cd)) return fail(SSD_E_INVALID_ARG, "the source model is not a layer prefix of the destination's");
+  if (n < 1 || n > kMaxReuse || n > dst->max_nodes) return fail(SSD_E_CAPACITY, "n outside [1, min(256, max_nodes)]");
+  if (src->last_layers < 1 || src->last_layers > cd.n_layer)
+    return fail(SSD_E_INVALID_ARG, "no pass of a layer prefix of the destination's model ran on the source session");
+  ReuseArgs a{};
+  for (int i = 0; i < n; ++i) {
+    if (src_rows[i] < 0 || src_rows[i] >= src->last_n)
+      return fail(SSD_E_INVALID_ARG, "a source row outside the source session's last pass");
+    a.rows[i] = src_rows[i];
+  }
+  const int es = cs.dtype == SSD_F32 ? 4 : 2, dh = cs.d_model / cs.n_head;
+  a.ks = (const unsigned char*)src->kt;
+  a.vs = (const unsigned char*)src->vt;
+  a.kd = (unsigned char*)dst->kt;
+  a.vd = (unsigned char*)dst->vt;
+  a.LH = src->last_layers * cs.n_head;
+  a.src_rows = src->max_nodes;
+  a.dst_rows = dst->max_nodes;
+  a.row_bytes = dh * es;
+  a.d = cs.d_model;
+  a.xs = src->resid_fused ? src->fz.xr : src->x;  // (the persistent pass: XCD 0's copy, rows of kFMaxN)
+  a.xd = x_out;
+  tree_reuse_kernel<<<n, 256, 0, (hipStream_t)stream>>>(a);
+  HIP_TRY(hipGetLastError());
   return SSD_OK;
 }

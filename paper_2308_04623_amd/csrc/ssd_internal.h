@@ -271,6 +271,8 @@ struct FusedArgs {
   unsigned long long timeout;  // s_memrealtime ticks (100 MHz) before a wait gives up
   unsigned long long* trace;  // stage timestamps [kFGroups][L + 1][kFStages][3], or nullptr
   int q8;                   // 8-bit weights: each packed matrix is 8-bit fragments followed by its row scales
+  int l0;                   // the first layer the pass runs (0: from the embedding)
+  const float* x_in;        // l0 > 0: [N][d] residual stream at layer l0's input (row = node slot)
 };
 
 // Work split of the fused pass for a model shape and 16-node tile count:

@@ -31,7 +31,8 @@ EXPORTS = ("ssd_model_create", "ssd_model_create_q8", "ssd_model_destroy", "ssd_
            "ssd_graph_capture_verify", "ssd_graph_launch", "ssd_graph_destroy", "ssd_validate_tree",
            "ssd_tree_prep", "ssd_kv_set_options", "ssd_kv_get_options", "ssd_status_string", "ssd_last_error",
            "ssd_model_prefix_view", "ssd_topk", "ssd_tree_accept_noalloc", "ssd_tree_verify_greedy",
-           "ssd_graph_capture_verify_greedy", "ssd_uniform", "ssd_cdf_pick")
+           "ssd_graph_capture_verify_greedy", "ssd_uniform", "ssd_cdf_pick", "ssd_tree_verify_from",
+           "ssd_tree_reuse")
 # and every function include/ssd_diag.h declares (measurement and diagnostics)
 DIAG_EXPORTS = ("ssd_launch_gemm", "ssd_verify_path", "ssd_fused_plan", "ssd_kv_set_trace", "ssd_model_q8_matrix")
 
@@ -110,6 +111,8 @@ def lib():
             "ssd_topk": [vp, vp, C.c_int32, C.c_int32, vp, vp, vp, vp],
             "ssd_status_string": [C.c_int],
             "ssd_uniform": [C.c_uint64, C.c_uint64, C.c_uint64],
+            "ssd_tree_verify_from": [vp, vp, C.c_int32, i32p, i32p, C.c_int32, C.c_int32, vp, vp, vp, vp, vp, vp],
+            "ssd_tree_reuse": [vp, vp, C.c_int32, vp, vp, vp],
             "ssd_cdf_pick": [vp, vp, C.c_int32, C.c_int32, C.c_float, C.c_int32, vp, vp, vp, vp],
             "ssd_last_error": [],
         }
@@ -463,6 +466,33 @@ class Session:
         _check(lib().ssd_topk(self.handle, C.c_void_p(logits.data_ptr()), n, k, C.c_void_p(idx.data_ptr()),
                               C.c_void_p(val.data_ptr()), C.c_void_p(lse.data_ptr()), _stream(stream)), "ssd_topk")
         return idx, val, lse
+
+    def verify_from(self, prefix_len: int, tokens, parent_idx, start_layer: int, x_in, logits=None, greedy=False,
+                    stream=None):
+        """ssd_tree_verify_from: logits, or with greedy=True (logits, path,
+        path_len, next_token)."""
+        torch = _torch()
+        t, p = _i32(tokens), _i32(parent_idx)
+        n = len(t)
+        if logits is None:
+            logits = torch.empty((n, self.model.cfg.vocab), dtype=torch.float32, device=self.model.device)
+        outs = self._accept_outs(n, None) if greedy else None
+        gp = [C.c_void_p(o.data_ptr()) for o in outs] if greedy else [C.c_void_p(0)] * 3
+        _check(lib().ssd_tree_verify_from(self.model.handle, self.handle, prefix_len, _p32(t), _p32(p), n,
+                                          start_layer, C.c_void_p(x_in.data_ptr() if x_in is not None else 0),
+                                          C.c_void_p(logits.data_ptr()), *gp, _stream(stream)),
+               "ssd_tree_verify_from")
+        return (logits,) + tuple(outs) if greedy else logits
+
+    def reuse_into(self, dst: "Session", src_rows, stream=None):
+        """ssd_tree_reuse from this (draft) session into dst: returns the
+        residual rows x [n][d_model] (device fp32) for dst.verify_from."""
+        torch = _torch()
+        r = _i32(src_rows)
+        x = torch.empty((len(r), self.model.cfg.d_model), dtype=torch.float32, device=self.model.device)
+        _check(lib().ssd_tree_reuse(self.handle, dst.handle, len(r), C.c_void_p(r.ctypes.data),
+                                    C.c_void_p(x.data_ptr()), _stream(stream)), "ssd_tree_reuse")
+        return x
 
     def cdf_pick(self, logits, rows, uniforms, temperature: float = 1.0, n_rows: Optional[int] = None,
                  stream=None):

@@ -156,6 +156,22 @@ def oracle_tree(toks: np.ndarray, par: np.ndarray, top_idx: np.ndarray, top_val:
     return t_out, p_out, int(endorsed.sum())
 
 
+def endorsed_subtree(toks: np.ndarray, par: np.ndarray, top_idx: np.ndarray,
+                     top: int = DRAFT_TOP) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """The bigram nodes the draft endorses (the root; a node whose parent is
+    endorsed and whose token is among the parent's `top` draft tokens), in
+    bigram order: their bigram indices, tokens and renumbered parents.  The
+    draft ran on every one of them, so its work on them can be reused."""
+    keep, pos = [0], {0: 0}
+    for i in range(1, len(toks)):
+        p = int(par[i])
+        if p in pos and int(toks[i]) in set(int(t) for t in top_idx[p, :top]):
+            pos[i] = len(keep)
+            keep.append(i)
+    k = np.array(keep, np.int32)
+    return k, toks[k].astype(np.int32), np.array([-1] + [pos[int(par[i])] for i in keep[1:]], np.int32)
+
+
 def cdf_first_tree(bt: np.ndarray, bp: np.ndarray, seed: int, uniform, pick, offsets: Sequence[float] = CDF_OFFSETS,
                    cap: int = MAX_ORACLE_NODES) -> Tuple[np.ndarray, np.ndarray]:
     """CDF-first oracle tree over a draft pass on the bigram tree (bt, bp).
@@ -245,6 +261,34 @@ def staged_greedy(backend, P: int, root: int, n_new: int, succ: np.ndarray) -> D
         st.accepted.append(len(path) - 1)
         st.oracle_nodes.append(len(ot))
         st.endorsed.append(n_end)
+        root = int(nxt)
+    st.tokens = st.tokens[:n_new]
+    st.seconds = time.perf_counter() - t0
+    return st
+
+
+def staged_greedy_reuse(backend, P: int, root: int, n_new: int, succ: np.ndarray) -> DecodeStats:
+    """Staged speculation (Sec. 3.2) that reuses the draft's work, which the
+    paper does not describe: with the draft being the oracle's first layers,
+    the oracle verifies the subtree of the bigram tree the draft endorses,
+    starting from the draft's residual stream and layer K/V (ssd_tree_reuse,
+    ssd_tree_verify_from), so its pass skips the draft's layers for every
+    node.  The price: no leaves past the endorsed nodes (the draft did not
+    run on them).  Greedy acceptance keeps the emitted sequence the plain
+    greedy one."""
+    st = DecodeStats()
+    t0 = time.perf_counter()
+    while len(st.tokens) < n_new:
+        bt, bp = bigram_tree(root, succ)
+        top_idx, _, _ = backend.draft_top(P, bt, bp, DRAFT_TOP)
+        keep, ot, op = endorsed_subtree(bt, bp, top_idx)
+        path, nxt = backend.oracle_step_reuse(P, ot, op, keep)
+        P += len(path)
+        st.tokens += [int(ot[i]) for i in path[1:]] + [int(nxt)]
+        st.steps += 1
+        st.accepted.append(len(path) - 1)
+        st.oracle_nodes.append(len(ot))
+        st.endorsed.append(len(ot))
         root = int(nxt)
     st.tokens = st.tokens[:n_new]
     st.seconds = time.perf_counter() - t0
@@ -402,6 +446,16 @@ class GpuBackend:
             v = val[int(p[-1])].cpu().numpy()
             self.gaps.append(float(v[0] - v[1]))
         return p, int(nxt.item())
+
+    def oracle_step_reuse(self, P: int, toks: np.ndarray, par: np.ndarray, draft_rows: np.ndarray):
+        """Verify from the draft's last layer on (the draft's last pass ran on
+        every node: draft_rows are their slots there), greedy accept, commit."""
+        x = self.d.reuse_into(self.o, draft_rows)
+        lg, path, plen, nxt = self.o.verify_from(P, toks, par, self.d.model.cfg.n_layer, x, greedy=True)
+        self.o.commit(P, path, plen)
+        self._check_errors(self.o)
+        n = int(plen.item())
+        return path[:n].cpu().numpy().astype(np.int32), int(nxt.item())
 
     def greedy_predictions(self, window_tokens: np.ndarray) -> np.ndarray:
         """The draft's greedy next token at every position of a window fed as

@@ -100,6 +100,8 @@ def check_pass(H, d, M, V, L, N, P, max_ctx, max_nodes, q8=False):
                           (b * MAXN + n) * d + (x + 1) * (d // 8) - 1, sizes["xacc"])
                 c.rng(f"{tag} act row", act_base + act_index(n, 0, KCd), act_base + act_index(n, d - 4, KCd) + 3,
                       sizes["act"])
+                # a pass from a later layer: the row of the given residual stream [N][d]
+                c.rng(f"{tag} x_in row", n * d, n * d + d - 1, N * d)
             # GEMM tasks: weights of each row block, activation fragments of
             # every tile (and the 8-bit copies' row scales)
             for slot, wname, kc0, kc1, KC, actn, rows_out in (

@@ -60,6 +60,29 @@ def test_oracle_tree_hand_case():
     assert t4.tolist() == [7, 10, 30, 12] and p4.tolist() == [-1, 0, 1, 1]
 
 
+def test_endorsed_subtree_hand_case():
+    toks, par, top_idx, _, _ = _hand_case()
+    keep, t, p = S.endorsed_subtree(toks, par, top_idx)
+    # root, node 1 (10 in the root's top-2), node 3 (12 in node 1's top-2)
+    assert keep.tolist() == [0, 1, 3] and t.tolist() == [7, 10, 12] and p.tolist() == [-1, 0, 1]
+    keep1, _, _ = S.endorsed_subtree(toks, par, top_idx, top=1)   # 12 is node 1's second choice
+    assert keep1.tolist() == [0, 1]
+
+
+def test_endorsed_subtree_matches_oracle_tree_count():
+    g = np.random.default_rng(2)
+    for s in range(50):
+        n = int(g.integers(1, 32))
+        par = np.array([-1] + [int(g.integers(0, i)) for i in range(1, n)], np.int32)
+        toks = g.integers(0, 6, n).astype(np.int32)
+        top_idx = g.integers(0, 6, (n, 2)).astype(np.int32)
+        keep, t, p = S.endorsed_subtree(toks, par, top_idx)
+        _, _, n_end = S.oracle_tree(toks, par, top_idx, np.zeros((n, 2), np.float32), np.zeros(n, np.float32))
+        assert len(keep) == n_end
+        assert np.array_equal(t, toks[keep])
+        assert all(p[i] < i and keep[p[i]] == par[keep[i]] for i in range(1, len(keep)))
+
+
 def test_oracle_tree_uses_log_probabilities():
     toks, par, top_idx, top_val, lse = _hand_case()
     lse = np.array([0.0, 5.0, 0.0, 0.0], np.float32)   # node 1's children become unlikely
