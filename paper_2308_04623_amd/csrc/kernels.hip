@@ -1150,23 +1150,22 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnArgs a) {
 
 // ---- bf16 models: two kernels, the first on the matrix cores
 //
-// attn_split_kernel, blocks [0, H * nsplit): (head h, prefix chunk c) of CL
-//   cache rows.  The chunk's K rows and V^T are staged in LDS once; wave w
-//   takes the 16-node tiles w, w + nw, ... of the tree against them.
-//   S^T = K Q^T and O^T = V^T P^T run on v_mfma_f32_16x16x32_bf16 (q and p
-//   split into bf16 hi + lo, K and V exact) 32 keys at a time with an online
-//   softmax.  The K operand's rows are ordered so that lane l ends up holding
-//   the scores of keys 8(l/16)..+7 of node l%16, which is exactly its slot of
-//   the P^T operand.
-// attn_split_kernel, blocks [H * nsplit, ...): the root paths.  Half-wave per
-//   (node, head): its ancestors and itself from the tree scratch on the vector
-//   ALU, root first, 32 keys per batch with the batch's V rows in LDS.
-// Each leaves a part (max, sum of exponentials, unnormalised output) per
-// (head, slot, node): slots 0 .. nsplit-1 the prefix chunks, slot nsplit the
-// root path.
-// attn_merge_kernel: per (node, head), the parts merged in slot order and
-// written in the next GEMM's input layout.  The chunking depends on P only,
-// so a node's result does not depend on the rest of the tree.
+// attn_split_kernel, block (head h, prefix chunk c) of CL cache rows, 8
+//   waves.  The chunk's K rows and V^T are staged in LDS once (all its loads
+//   in flight together, two per thread); wave w takes the 16-node tiles w,
+//   w + 8, ... of the tree against them.  S^T = K Q^T and
+//   O^T = V^T P^T run on v_mfma_f32_16x16x32_bf16 (q and p split into bf16
+//   hi + lo, K and V exact) 32 keys at a time with an online softmax.  The K
+//   operand's rows are ordered so that lane l ends up holding the scores of
+//   keys 8(l/16)..+7 of node l%16, which is exactly its slot of the P^T
+//   operand.  Each leaves a part (max, sum of exponentials, unnormalised
+//   output) per (head, chunk, node).
+// attn_merge_kernel: DH threads (one per output dim) per (node, head): the
+//   chunks' parts merged in chunk order, then the node's root path (its
+//   ancestors and itself in the tree scratch, root first) folded in RK keys
+//   at a time, each score a butterfly sum over the DH threads; the output
+//   is written in the next GEMM's input layout.  The chunking depends on P
+//   only, so a node's result does not depend on the rest of the tree.
 
 constexpr int AT_STAGE = kAttnMaxChunk;  // cache rows staged per block
 constexpr int AT_MAXW = 8;               // waves per block
@@ -1203,7 +1202,7 @@ template <int DH>
 __device__ __forceinline__ void attn_prefix_chunk(const AttnArgs& a, uint16_t* lds, int h, int c) {
   constexpr int KS = DH + 8;        // LDS row stride of K (elements)
   constexpr int VS = AT_STAGE + 8;  // LDS row stride of V^T (elements)
-  constexpr int MAXU = AT_STAGE * DH / 8 / 64;  // 16-byte units per thread, one wave
+  constexpr int MAXU = (AT_STAGE * DH / 8 + 64 * AT_MAXW - 1) / (64 * AT_MAXW);  // 16-byte units per thread
   uint16_t* ks = lds;
   uint16_t* vts = lds + AT_STAGE * KS;
   const int tid = threadIdx.x, nt = blockDim.x, nw = nt >> 6, w = tid >> 6, lane = tid & 63;
@@ -1254,7 +1253,7 @@ __device__ __forceinline__ void attn_prefix_chunk(const AttnArgs& a, uint16_t* l
     }
   }
   __syncthreads();
-  const int ns = a.nsplit + 1;
+  const int ns = a.nsplit;
   for (int t = w; t < ntiles; t += nw) {
     if (t != w) load_q(t);
     u32x4 qh[DH / 32], ql[DH / 32];
@@ -1330,118 +1329,30 @@ __device__ __forceinline__ void attn_prefix_chunk(const AttnArgs& a, uint16_t* l
 }
 
 template <int DH>
-__device__ __forceinline__ void attn_root_path(const AttnArgs& a, uint16_t* lds, float (*qrow)[2][DH], int h, int grp) {
-  constexpr int DPL = DH / 32;  // output dims per lane of a half-wave
-  const int tid = threadIdx.x, nw = blockDim.x >> 6, w = tid >> 6, lane = tid & 63;
-  const int hw = lane >> 5, hl = lane & 31;
-  const int n = grp * 2 * nw + 2 * w + hw;  // this half-wave's node
-  const int rnc = min(n, a.N - 1);
-  // first 32 path entries at a fixed stride: no dependent index load
-  int rkey = a.path32[(size_t)rnc * kPath32 + hl];
-  const int rdep = a.depth[rnc];
-  {
-    const float* qp = a.q + (size_t)rnc * a.d + h * DH + hl * DPL;
-#pragma unroll
-    for (int e = 0; e < DPL; ++e) qrow[w][hw][hl * DPL + e] = qp[e];
-  }
-  const uint16_t* ktb = (const uint16_t*)a.kt + (size_t)h * a.max_nodes * DH;
-  const uint16_t* vtb = (const uint16_t*)a.vt + (size_t)h * a.max_nodes * DH;
-  u32x4 rk[DH / 8], rv[DH / 8];
-#pragma unroll
-  for (int j = 0; j < DH / 8; ++j) {
-    rk[j] = *(const u32x4*)(ktb + (size_t)rkey * DH + 8 * j);
-    rv[j] = *(const u32x4*)(vtb + (size_t)rkey * DH + 8 * j);
-  }
-  uint16_t* rvl = lds + (2 * w + hw) * 32 * DH;  // [32 keys][DH] of this half-wave
-  float rm = -INFINITY, rl = 0.f, ro[DPL];
-#pragma unroll
-  for (int e = 0; e < DPL; ++e) ro[e] = 0.f;
-  const int rbatches = (max(rdep, __shfl_xor(rdep, 32)) + 32) / 32;  // wave-uniform
-  for (int bt = 0; bt < rbatches; ++bt) {
-    const int j = 32 * bt + hl;
-    if (bt > 0) {
-      rkey = a.ancl[a.anc_off[rnc] + min(j, rdep)];
-#pragma unroll
-      for (int jj = 0; jj < DH / 8; ++jj) {
-        rk[jj] = *(const u32x4*)(ktb + (size_t)rkey * DH + 8 * jj);
-        rv[jj] = *(const u32x4*)(vtb + (size_t)rkey * DH + 8 * jj);
-      }
-    }
-#pragma unroll
-    for (int jj = 0; jj < DH / 8; ++jj) *(u32x4*)(rvl + hl * DH + 8 * jj) = rv[jj];
-    wave_sync_lds();  // qrow (first batch) and this batch's V rows
-    float dot = 0.f;
-#pragma unroll
-    for (int c8 = 0; c8 < DH / 8; ++c8) {
-      const f32x4 qa = *(const f32x4*)&qrow[w][hw][8 * c8];
-      const f32x4 qb = *(const f32x4*)&qrow[w][hw][8 * c8 + 4];
-      const u32x4 ku = rk[c8];
-      dot = fmaf(qa[0], __uint_as_float(ku[0] << 16), dot);
-      dot = fmaf(qa[1], __uint_as_float(ku[0] & 0xffff0000u), dot);
-      dot = fmaf(qa[2], __uint_as_float(ku[1] << 16), dot);
-      dot = fmaf(qa[3], __uint_as_float(ku[1] & 0xffff0000u), dot);
-      dot = fmaf(qb[0], __uint_as_float(ku[2] << 16), dot);
-      dot = fmaf(qb[1], __uint_as_float(ku[2] & 0xffff0000u), dot);
-      dot = fmaf(qb[2], __uint_as_float(ku[3] << 16), dot);
-      dot = fmaf(qb[3], __uint_as_float(ku[3] & 0xffff0000u), dot);
-    }
-    const bool kvalid = j <= rdep;
-    const float sc = kvalid ? dot * a.scale : -INFINITY;
-    float mb = sc;
-#pragma unroll
-    for (int off = 1; off < 32; off <<= 1) mb = fmaxf(mb, __shfl_xor(mb, off));
-    const float mn = fmaxf(rm, mb);
-    const float alpha = __expf(rm - mn);
-    const float p = kvalid ? __expf(sc - mn) : 0.f;
-    float ps = p;
-#pragma unroll
-    for (int off = 1; off < 32; off <<= 1) ps += __shfl_xor(ps, off);
-    rl = fmaf(rl, alpha, ps);
-    rm = mn;
-    // lane hl covers dims DPL hl .. +DPL; keys of the batch in order
-    const int cnt = min(32, rdep + 1 - 32 * bt);
-    const int cmax = max(cnt, __shfl_xor(cnt, 32));  // wave-uniform
-    float acc[DPL];
-#pragma unroll
-    for (int e = 0; e < DPL; ++e) acc[e] = 0.f;
-    for (int jj = 0; jj < cmax; ++jj) {
-      const float pj = jj < cnt ? __shfl(p, (hw << 5) + jj) : 0.f;
-      const uint16_t* vr2 = rvl + jj * DH + DPL * hl;
-#pragma unroll
-      for (int e = 0; e < DPL; ++e) acc[e] = fmaf(pj, bf2f(vr2[e]), acc[e]);
-    }
-#pragma unroll
-    for (int e = 0; e < DPL; ++e) ro[e] = fmaf(ro[e], alpha, acc[e]);
-    wave_sync_lds();  // the batch's V rows are read before the next batch overwrites them
-  }
-  if (n < a.N) {
-    unsigned char* rec =
-        (unsigned char*)a.part + (((size_t)h * (a.nsplit + 1) + a.nsplit) * a.N + n) * part_bytes<DH>();
-    if (hl == 0) *(f32x2_t*)rec = (f32x2_t){rm, rl};
-    if constexpr (DPL == 2) *(uint32_t*)(rec + 16 + 4 * hl) = f16pair(ro[0], ro[1]);
-    else *(uint16_t*)(rec + 16 + 2 * hl) = __builtin_bit_cast(uint16_t, (_Float16)ro[0]);
-  }
-}
-
-template <int DH>
 __global__ __launch_bounds__(64 * AT_MAXW) void attn_split_kernel(AttnArgs a) {
-  constexpr int PFX = AT_STAGE * (DH + 8) + DH * (AT_STAGE + 8);  // K rows + V^T
-  constexpr int ROOT = AT_MAXW * 2 * 32 * DH;                     // 32 V rows per half-wave
-  __shared__ __align__(16) uint16_t lds[PFX > ROOT ? PFX : ROOT];
-  __shared__ __align__(16) float qrow[AT_MAXW][2][DH];
+  __shared__ __align__(16) uint16_t lds[AT_STAGE * (DH + 8) + DH * (AT_STAGE + 8)];  // K rows + V^T
   pass_signal(a.sig);
-  const int npre = a.H * a.nsplit;
-  if ((int)blockIdx.x < npre) attn_prefix_chunk<DH>(a, lds, blockIdx.x % a.H, blockIdx.x / a.H);
-  else attn_root_path<DH>(a, lds, qrow, (blockIdx.x - npre) % a.H, (blockIdx.x - npre) / a.H);
+  // (an empty prefix launches one block, for the pass signal only)
+  if ((int)blockIdx.x < a.H * a.nsplit) attn_prefix_chunk<DH>(a, lds, blockIdx.x % a.H, blockIdx.x / a.H);
 }
 
 template <int DH>
 __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
-  constexpr int RB = part_bytes<DH>(), PER = 256 / DH, B = 16;
+  constexpr int RB = part_bytes<DH>(), PER = 256 / DH, B = 16, RK = 8;
   pass_signal(a.sig);
   const int pair = blockIdx.x * PER + threadIdx.x / DH, dd = threadIdx.x % DH;
-  if (pair >= a.N * a.H) return;
-  const int n = pair / a.H, h = pair - n * a.H, ns = a.nsplit + 1;
+  if (pair >= a.N * a.H) return;  // (a whole pair's DH threads together)
+  const int n = pair / a.H, h = pair - n * a.H, ns = a.nsplit;
+  // the root path's first RK keys and this dim's query go out with the parts
+  // (path32 is padded with the node itself, so every entry is a valid row)
+  const int* p32 = a.path32 + (size_t)n * kPath32;
+  const uint16_t* ktb = (const uint16_t*)a.kt + (size_t)h * a.max_nodes * DH + dd;
+  const uint16_t* vtb = (const uint16_t*)a.vt + (size_t)h * a.max_nodes * DH + dd;
+  const int rdep = a.depth[n];
+  const float qd = a.q[(size_t)n * a.d + h * DH + dd];
+  int key[RK];
+#pragma unroll
+  for (int jj = 0; jj < RK; ++jj) key[jj] = p32[jj];
   const size_t cs = (size_t)a.N * RB;
   const unsigned char* rec = (const unsigned char*)a.part + ((size_t)h * ns * a.N + n) * RB;
   float M = -INFINITY, L = 0.f, O = 0.f;
@@ -1464,6 +1375,44 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
       M = mn;
     }
   }
+  // the root path, root first, RK keys per batch
+  for (int j0 = 0; j0 <= rdep; j0 += RK) {
+    if (j0 > 0) {
+#pragma unroll
+      for (int jj = 0; jj < RK; ++jj) {
+        const int j = min(j0 + jj, rdep);
+        key[jj] = j < kPath32 ? p32[j] : a.ancl[a.anc_off[n] + j];
+      }
+    }
+    float s[RK], vv[RK];
+#pragma unroll
+    for (int jj = 0; jj < RK; ++jj) {
+      s[jj] = qd * bf2f(ktb[(size_t)key[jj] * DH]);
+      vv[jj] = bf2f(vtb[(size_t)key[jj] * DH]);
+    }
+    // (a butterfly leaves the same sum in every thread of the pair)
+#pragma unroll
+    for (int off = 1; off < DH; off <<= 1)
+#pragma unroll
+      for (int jj = 0; jj < RK; ++jj) s[jj] += __shfl_xor(s[jj], off);
+    float mb = -INFINITY;
+#pragma unroll
+    for (int jj = 0; jj < RK; ++jj) {
+      s[jj] = j0 + jj <= rdep ? s[jj] * a.scale : -INFINITY;
+      mb = fmaxf(mb, s[jj]);
+    }
+    const float mn = fmaxf(M, mb), al = __expf(M - mn);
+    float ps = 0.f, po = 0.f;
+#pragma unroll
+    for (int jj = 0; jj < RK; ++jj) {
+      const float p = __expf(s[jj] - mn);
+      ps += p;
+      po = fmaf(p, vv[jj], po);
+    }
+    L = fmaf(L, al, ps);
+    O = fmaf(O, al, po);
+    M = mn;
+  }
   st_act((uint16_t*)a.out, n, h * DH + dd, a.ldo, O / L, a.err);
 }
 
@@ -1472,14 +1421,13 @@ hipError_t launch_attn(int f32, int DH, const AttnArgs& a, hipStream_t s) {
     if (a.N <= 0 || a.N > a.max_nodes || (DH != 64 && DH != 32)) return hipErrorInvalidValue;
     if (a.P > 0 && (a.CL <= 0 || a.CL > AT_STAGE || a.CL % 32 || a.nsplit != (a.P + a.CL - 1) / a.CL))
       return hipErrorInvalidValue;
-    const int nw = min(AT_MAXW, (a.N + 15) / 16);
-    const int blocks = a.H * a.nsplit + a.H * ((a.N + 2 * nw - 1) / (2 * nw));
+    const int blocks = max(1, a.H * a.nsplit);
     const int mblocks = (a.N * a.H * DH + 255) / 256;
     if (DH == 64) {
-      attn_split_kernel<64><<<blocks, 64 * nw, 0, s>>>(a);
+      attn_split_kernel<64><<<blocks, 64 * AT_MAXW, 0, s>>>(a);
       attn_merge_kernel<64><<<mblocks, 256, 0, s>>>(a);
     } else {
-      attn_split_kernel<32><<<blocks, 64 * nw, 0, s>>>(a);
+      attn_split_kernel<32><<<blocks, 64 * AT_MAXW, 0, s>>>(a);
       attn_merge_kernel<32><<<mblocks, 256, 0, s>>>(a);
     }
     return hipGetLastError();

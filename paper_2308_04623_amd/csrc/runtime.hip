@@ -540,9 +540,9 @@ extern "C" ssd_status ssd_kv_create(const ssd_model* m, int32_t max_ctx, int32_t
   const size_t o_f = take(planes * kv->npad * M * es);
   const size_t o_part = take((size_t)kMaxSplits * max_nodes * d * 4);  // split-K partials
   // attention partials: fp32 models (H, 64-row tiles, node, DH + 2); bf16
-  // models (H, prefix chunks + root path, node, DH + 4)
+  // models (H, prefix chunks, node, DH + 4)
   const size_t ap_f32 = (size_t)c.n_head * ((max_ctx + 63) / 64) * max_nodes * (m->dh + 2);
-  const size_t ap_bf16 = (size_t)c.n_head * (attn_max_nsplit(max_ctx) + 1) * max_nodes * (m->dh + 4);
+  const size_t ap_bf16 = (size_t)c.n_head * attn_max_nsplit(max_ctx) * max_nodes * (m->dh + 4);
   const size_t o_apart = take((m->f32 ? ap_f32 : ap_bf16) * 4);
   const size_t o_tree = take(stage_bytes(max_nodes));
   const size_t o_at = take((size_t)3 * max_nodes * 4), o_am = take((size_t)max_nodes * 4);

@@ -106,9 +106,8 @@ struct AttnArgs {
   void* out;            // attention output in the GEMM-input layout
   int ldo;              // GEMM-input leading dimension (fp32: d, bf16: d / 32)
   float* part;          // fp32 models: prefix partials [H][S][N][DH + 2] (max, sum of exp, output);
-                        // bf16 models: parts [H][nsplit + 1][N] of 16 + 2 DH bytes (max and sum
-                        // float32, 8 bytes of padding, output float16), slots 0 .. nsplit-1
-                        // the prefix chunks, slot nsplit the root path
+                        // bf16 models: parts [H][nsplit][N] of 16 + 2 DH bytes (max and sum
+                        // float32, 8 bytes of padding, output float16), one per prefix chunk
   int S;                // fp32 models: prefix tiles of 64 cache rows
   int N, P, d, H, max_ctx, max_nodes;
   float scale;
