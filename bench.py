@@ -80,7 +80,10 @@ def cpu_model():
 
 
 COPY_BYTES = 256 << 20
-FC_KERNEL = "gemm_kernel<2, 2, 2,"  # MLP up-projection + GELU at 17..32 nodes (matrix cores)
+def fc_kernel(n):
+    """The MLP up-projection + GELU GEMM's kernel at n nodes (matrix cores):
+    one-or-two-row-block tiles up to 64 nodes, the wide-tree kernel above."""
+    return "gemm2d_kernel<2, 2, 2, 4," if n > 64 else "gemm_kernel<2, 2, 2,"
 PASS_KERNEL = "pass_kernel"         # the persistent single-launch pass
 
 
@@ -140,7 +143,7 @@ def traffic_path(fused):
 
 
 def write_traffic(fetch_dir, write_dir, n, fused):
-    kname = PASS_KERNEL if fused else FC_KERNEL
+    kname = PASS_KERNEL if fused else fc_kernel(n)
     out = {"kernel_source": kernel_source_hash(fused), "kernel": kname, "nodes": n, "copy_bytes": COPY_BYTES}
     for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
         per = _per_kernel(_counter_rows(d), counter)
