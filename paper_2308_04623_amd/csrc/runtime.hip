@@ -542,7 +542,7 @@ extern "C" ssd_status ssd_kv_create(const ssd_model* m, int32_t max_ctx, int32_t
   // attention partials: fp32 models (H, 64-row tiles, node, DH + 2); bf16
   // models (H, prefix chunks, node, DH + 4)
   const size_t ap_f32 = (size_t)c.n_head * ((max_ctx + 63) / 64) * max_nodes * (m->dh + 2);
-  const size_t ap_bf16 = (size_t)c.n_head * attn_max_nsplit(max_ctx) * max_nodes * (m->dh + 4);
+  const size_t ap_bf16 = (size_t)c.n_head * attn_max_nsplit(max_ctx, c.n_head) * max_nodes * (m->dh + 4);
   const size_t o_apart = take((m->f32 ? ap_f32 : ap_bf16) * 4);
   const size_t o_tree = take(stage_bytes(max_nodes));
   const size_t o_at = take((size_t)3 * max_nodes * 4), o_am = take((size_t)max_nodes * 4);
@@ -881,8 +881,8 @@ static ssd_status enqueue_verify(const ssd_model* m, ssd_kv* kv, int32_t P, int3
     a.max_ctx = kv->max_ctx;
     a.max_nodes = maxn;
     a.scale = 1.0f / std::sqrt((float)DH);
-    a.CL = attn_chunk(P);
-    a.nsplit = attn_nsplit(P);
+    a.CL = attn_chunk(P, H);
+    a.nsplit = attn_nsplit(P, H);
     a.sig = sig;
     a.err = kv->d_err;
     HIP_TRY(launch_attn(f32, DH, a, s));

@@ -112,30 +112,32 @@ struct AttnArgs {
   int N, P, d, H, max_ctx, max_nodes;
   float scale;
   // bf16 models
-  int CL;               // cache rows per prefix chunk (attn_chunk(P))
-  int nsplit;           // prefix chunks (attn_nsplit(P))
+  int CL;               // cache rows per prefix chunk (attn_chunk(P, H))
+  int nsplit;           // prefix chunks (attn_nsplit(P, H))
   unsigned long long* sig;  // pass signal counter (nullptr: none); both kernels signal
   unsigned* err;            // session error counter: float16 outputs out of range (nullptr: none)
 };
 
 // bf16 attention: cache rows per prefix chunk, a multiple of 32 between 64
-// and kAttnMaxChunk: 64 up to P = 1024, then about P / 16 (at most 16 chunks
-// up to P = 2048).  A function of the prefix length only, so that a node's
-// result does not depend on the tree.
-constexpr int kAttnMaxChunk = 128;
-inline int attn_chunk(int P) {
-  int c = (P + 15) / 16;
+// and kAttnMaxChunk, as few rows as keep the split kernel's H x nsplit
+// blocks within one per CU (256) where the prefix allows: 64 up to
+// P = 768 at 20 heads, 192 at P = 2048.  A function of the prefix length and
+// the head count only, so that a node's result does not depend on the tree.
+constexpr int kAttnMaxChunk = 256;
+inline int attn_chunk(int P, int H) {
+  const int per = 256 / H > 0 ? 256 / H : 1;  // chunks per head
+  int c = (P + per - 1) / per;
   c = (c + 31) / 32 * 32;
   if (c < 64) c = 64;
   if (c > kAttnMaxChunk) c = kAttnMaxChunk;
   return c;
 }
-inline int attn_nsplit(int P) { return P > 0 ? (P + attn_chunk(P) - 1) / attn_chunk(P) : 0; }
+inline int attn_nsplit(int P, int H) { return P > 0 ? (P + attn_chunk(P, H) - 1) / attn_chunk(P, H) : 0; }
 // most prefix chunks for any P <= max_ctx
-inline int attn_max_nsplit(int max_ctx) {
+inline int attn_max_nsplit(int max_ctx, int H) {
   int mx = 0;
-  for (int P = 1; P <= max_ctx; P += (P < 8192 ? 1 : 256)) mx = attn_nsplit(P) > mx ? attn_nsplit(P) : mx;
-  return attn_nsplit(max_ctx) > mx ? attn_nsplit(max_ctx) : mx;
+  for (int P = 1; P <= max_ctx; P += (P < 8192 ? 1 : 256)) mx = attn_nsplit(P, H) > mx ? attn_nsplit(P, H) : mx;
+  return attn_nsplit(max_ctx, H) > mx ? attn_nsplit(max_ctx, H) : mx;
 }
 
 // ---- launchers (kernels.hip); all enqueue on `s` and return the launch status
