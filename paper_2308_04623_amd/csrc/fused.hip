@@ -729,6 +729,13 @@ constexpr int WST = 16 * 1024;                              // LDS offset of the
 constexpr int WST_FRAGS = (73728 + 34816 + 4096 - WST) / 1024;  // 1 KB fragments that fit below sh
 constexpr int WO_FRAGS = 24;  // the out-projection's staged fragments, above the parameter table
 
+// Every weight fragment is read by exactly one workgroup of the pass, once,
+// so weights are loaded non-temporal (the nt cache-policy bit; for the
+// register loads __builtin_nontemporal_load): streaming about 4.9 MB through
+// each XCD's 4 MB L2 per layer would otherwise evict the residual copies,
+// activations and attention parts the next stages read back.
+constexpr int kWeightCpol = 2;
+
 // Copies weight fragments f = wv - 1, wv - 1 + nw, ... < n * nk (row block
 // rbs[f / nk] (an LDS list), k-step k0 + f % nk of a matrix of KC k-steps)
 // into LDS at dst + f * fragment bytes, by waves 1.. of a stage (nw of them).
@@ -745,7 +752,7 @@ __device__ __forceinline__ void stage_frags(gptr<u32x4> W, const int* rbs, int n
       const int r = f / nk, k = k0 + f - r * nk;
       const int rb = ((const __attribute__((address_space(3))) int*)rbs)[r];
       __builtin_amdgcn_global_load_lds((const void*)(Wv + ((size_t)rb * KC + k) * 64),
-                                       (lds_void*)(dst + (size_t)f * 1024), 16, 0, 0);
+                                       (lds_void*)(dst + (size_t)f * 1024), 16, 0, kWeightCpol);
     }
   } else {
     // two consecutive k-steps of a row block are 1 KB contiguous in memory
@@ -760,11 +767,12 @@ __device__ __forceinline__ void stage_frags(gptr<u32x4> W, const int* rbs, int n
       const int rb = ((const __attribute__((address_space(3))) int*)rbs)[r];
       unsigned char* d = dst + (size_t)(r * nk + 2 * j) * 512;
       if (j < np) {
-        __builtin_amdgcn_global_load_lds((const void*)(W16 + ((size_t)rb * KC + k) * 32), (lds_void*)d, 16, 0, 0);
+        __builtin_amdgcn_global_load_lds((const void*)(W16 + ((size_t)rb * KC + k) * 32), (lds_void*)d, 16, 0,
+                                         kWeightCpol);
       } else {
         const gptr<unsigned> src = W4 + ((size_t)rb * KC + k) * 128;
-        __builtin_amdgcn_global_load_lds((const void*)src, (lds_void*)d, 4, 0, 0);
-        __builtin_amdgcn_global_load_lds((const void*)(src + 64), (lds_void*)(d + 256), 4, 0, 0);
+        __builtin_amdgcn_global_load_lds((const void*)src, (lds_void*)d, 4, 0, kWeightCpol);
+        __builtin_amdgcn_global_load_lds((const void*)(src + 64), (lds_void*)(d + 256), 4, 0, kWeightCpol);
       }
     }
   }
@@ -903,8 +911,9 @@ __device__ __forceinline__ bool gemm_rb(const FusedArgs& a, const Wg& w, const W
 #pragma unroll
       for (int r = 0; r < RB; ++r) wq[u][r] = wl[(min(r, nrb - 1) * nk + (kc - kc0)) * 64];
     } else {
+      // (non-temporal: see kWeightCpol)
 #pragma unroll
-      for (int r = 0; r < RB; ++r) wq[u][r] = wb[r][(size_t)kc * 64];
+      for (int r = 0; r < RB; ++r) wq[u][r] = __builtin_nontemporal_load(&wb[r][(size_t)kc * 64]);
     }
   };
   auto load_a = [&](int s, int u) {
