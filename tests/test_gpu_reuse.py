@@ -15,6 +15,9 @@ may then start at the draft's last layer.
 - Staged greedy decoding with reuse emits the plain greedy sequence: on the
   tiny float32 model the oracle's own, token for token.
 - GPT-2-L at 32 nodes (4-layer draft): bitwise equal to the full pass.
+- The 8-bit weight model (its own start-layer variant of the persistent
+  pass): bitwise equal to the full pass, and the oracle's 8-bit mode within
+  2e-2, on both paths.
 """
 import numpy as np
 import pytest
@@ -46,12 +49,12 @@ def ssd(torch):
 class Pair:
     """An oracle model, its first-layers draft view, and two sessions on one cache."""
 
-    def __init__(self, ssd, cfg, n_draft, P=64, max_ctx=160, max_nodes=64, seed=0):
+    def __init__(self, ssd, cfg, n_draft, P=64, max_ctx=160, max_nodes=64, seed=0, q8=False):
         self.cfg, self.P, self.ld = cfg, P, n_draft
         self.w = W.make_weights(cfg, seed, perturb_affine=True)
-        self.om = oracle.Model(cfg, self.w)
+        self.om = oracle.Model(cfg, self.w, q8=q8)
         self.kc, self.vc = W.random_kv_cache(cfg, max_ctx, P, seed=3)
-        self.m = ssd.Model(cfg, self.w)
+        self.m = ssd.Model(cfg, self.w, q8=q8)
         self.view = self.m.prefix_view(n_draft)
         self.o = ssd.Session(self.m, max_ctx, max_nodes, ssd.to_device(self.kc, cfg), ssd.to_device(self.vc, cfg))
         self.d = ssd.Session(self.view, max_ctx, max_nodes, self.o.k_cache, self.o.v_cache)
@@ -65,6 +68,11 @@ class Pair:
 @pytest.fixture(scope="module")
 def small(ssd):
     return Pair(ssd, SMALL, 1)
+
+
+@pytest.fixture(scope="module")
+def small_q8(ssd):
+    return Pair(ssd, SMALL, 1, q8=True)
 
 
 @pytest.fixture(scope="module")
@@ -118,6 +126,21 @@ def test_reuse_per_sub_layer_path(small, tiny, ssd, torch, pair_name):
     assert np.abs(got - pair.oracle_logits(t, p)).max() < TOL
     assert np.abs(got - lg_f.cpu().numpy()).max() < 1e-2
     assert torch.equal(lg_g, lg_r)
+    op, on = oracle.tree_accept(oracle.GREEDY, t, p, got)
+    assert path[:int(plen.item())].cpu().tolist() == op.tolist() and int(nxt.item()) == on
+
+
+@pytest.mark.parametrize("mode", ["fused", "kernels"])
+def test_reuse_q8_model(small_q8, ssd, torch, mode):
+    pm = ssd.PASS_FUSED if mode == "fused" else ssd.PASS_KERNELS
+    t, p, lg_r, lg_g, (path, plen, nxt), lg_f = _run(small_q8, ssd, torch, pm, 6, 44)
+    if mode == "fused":
+        assert torch.equal(lg_r, lg_f)
+    else:
+        assert np.abs(lg_r.cpu().numpy() - lg_f.cpu().numpy()).max() < 1e-2
+    assert torch.equal(lg_g, lg_r)
+    got = lg_r.cpu().numpy()
+    assert np.abs(got - small_q8.oracle_logits(t, p)).max() < TOL
     op, on = oracle.tree_accept(oracle.GREEDY, t, p, got)
     assert path[:int(plen.item())].cpu().tolist() == op.tolist() and int(nxt.item()) == on
 
