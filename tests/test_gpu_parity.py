@@ -375,6 +375,35 @@ def test_float16_range_is_checked(ssd, torch):
     s.close()
 
 
+@pytest.mark.slow
+def test_attention_largest_prefix_chunk(ssd, torch):
+    """The one-kernel-per-sub-layer attention at its largest chunk: 32 heads
+    over a 2000-token prefix make the chunk 256 cache rows (8 per head), the
+    most the split kernel stages; every logit of a 20-node tree against the
+    oracle (2e-2), and the greedy walk on them."""
+    cfg = W.GPT2Config(n_layer=1, d_model=2048, n_head=32, d_mlp=256, vocab=512, n_pos=2100, dtype="bf16")
+    w = W.make_weights(cfg, 4, perturb_affine=True)
+    P = 2000
+    kc, vc = W.random_kv_cache(cfg, P + 32, P, seed=9)
+    m = ssd.Model(cfg, w)
+    s = ssd.Session(m, P + 32, 32, ssd.to_device(kc, cfg), ssd.to_device(vc, cfg))
+    par = W.branching_tree([4, 2, 2, 1], 20)
+    toks = W.tree_tokens(par, cfg.vocab, seed=3)
+    with s.options(pass_mode=ssd.PASS_KERNELS):
+        lg = s.verify(P, toks, par)
+        path, plen, nxt = s.accept(toks, par, lg)
+        torch.cuda.synchronize()
+    assert s.error_count() == 0
+    om = oracle.Model(cfg, w)
+    ref = oracle.tree_verify(om, kc, vc, P, toks, par, om.kv(32), om.kv(32))
+    got = lg.cpu().numpy()
+    assert np.abs(got - ref).max() < 2e-2
+    op, on = oracle.tree_accept(oracle.GREEDY, toks, par, got)
+    assert path[:int(plen.item())].cpu().tolist() == op.tolist() and int(nxt.item()) == on
+    s.close()
+    m.close()
+
+
 @pytest.mark.parametrize("V", [512, 50257])
 @pytest.mark.parametrize("mode", ["wor", "iid", "det"])
 @pytest.mark.parametrize("k", [1, 50])
