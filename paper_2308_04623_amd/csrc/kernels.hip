@@ -81,6 +81,20 @@ __device__ __forceinline__ void st_act<uint16_t>(uint16_t* p, int n, int k, int 
   p[f * 512 + ((n & 15) + 16 * ((k & 31) >> 3)) * 8 + (k & 7)] = __builtin_bit_cast(uint16_t, (_Float16)v);
 }
 __device__ __forceinline__ float h2f(uint16_t h) { return (float)__builtin_bit_cast(_Float16, h); }
+// four consecutive columns k .. k + 3 (k a multiple of 4) of row n in the
+// GEMM-input layout: one 8-byte store, out-of-range values counted as st_act does
+__device__ __forceinline__ void st_act4_u16(uint16_t* p, int n, int k, int ld, const float (&v)[4], unsigned* err) {
+  const size_t f = (size_t)(n >> 4) * ld + (k >> 5);
+  const bool bad = !(fabsf(v[0]) <= 65504.f) || !(fabsf(v[1]) <= 65504.f) || !(fabsf(v[2]) <= 65504.f) ||
+                   !(fabsf(v[3]) <= 65504.f);
+  const unsigned long long m = __builtin_amdgcn_ballot_w64(bad);
+  if (m && err && (int)__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u)) == __builtin_ctzll(m)) atomicAdd(err, 1u);
+  const uint32_t lo = (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)v[0]) |
+                      ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)v[1]) << 16);
+  const uint32_t hi = (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)v[2]) |
+                      ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)v[3]) << 16);
+  *(u32x2*)(p + f * 512 + ((n & 15) + 16 * ((k & 31) >> 3)) * 8 + (k & 7)) = (u32x2){lo, hi};
+}
 
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
@@ -1160,11 +1174,12 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnArgs a) {
 //   keys 8(l/16)..+7 of node l%16, which is exactly its slot of the P^T
 //   operand.  Each leaves a part (max, sum of exponentials, unnormalised
 //   output) per (head, chunk, node).
-// attn_merge_kernel: DH threads (one per output dim) per (node, head): the
+// attn_merge_kernel: DH / 4 threads (four output dims each) per (node, head): the
 //   chunks' parts merged in chunk order, then the node's root path (its
 //   ancestors and itself in the tree scratch, root first) folded in RK keys
-//   at a time, each score a butterfly sum over the DH threads; the output
-//   is written in the next GEMM's input layout.  The chunking depends on P
+//   at a time, each score four products per thread then a butterfly sum
+//   over the pair's threads; the output is written in the next GEMM's input
+//   layout, four columns per store.  The chunking depends on P
 //   only, so a node's result does not depend on the rest of the tree.
 
 constexpr int AT_STAGE = kAttnMaxChunk;  // cache rows staged per block
@@ -1338,32 +1353,33 @@ __global__ __launch_bounds__(64 * AT_MAXW) void attn_split_kernel(AttnArgs a) {
 
 template <int DH>
 __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
-  constexpr int RB = part_bytes<DH>(), PER = 256 / DH, B = 16, RK = 8;
+  // TPP threads per (node, head), DPT = 4 consecutive dims each
+  constexpr int RB = part_bytes<DH>(), DPT = 4, TPP = DH / DPT, PER = 256 / TPP, B = 16, RK = 8;
   pass_signal(a.sig);
-  const int pair = blockIdx.x * PER + threadIdx.x / DH, dd = threadIdx.x % DH;
-  if (pair >= a.N * a.H) return;  // (a whole pair's DH threads together)
+  const int pair = blockIdx.x * PER + threadIdx.x / TPP, d0 = DPT * (threadIdx.x % TPP);
+  if (pair >= a.N * a.H) return;  // (a whole pair's threads together)
   const int n = pair / a.H, h = pair - n * a.H, ns = a.nsplit;
-  // the root path's first RK keys and this dim's query go out with the parts
+  // the root path's first RK keys and these dims' query go out with the parts
   // (path32 is padded with the node itself, so every entry is a valid row)
   const int* p32 = a.path32 + (size_t)n * kPath32;
-  const uint16_t* ktb = (const uint16_t*)a.kt + (size_t)h * a.max_nodes * DH + dd;
-  const uint16_t* vtb = (const uint16_t*)a.vt + (size_t)h * a.max_nodes * DH + dd;
+  const uint16_t* ktb = (const uint16_t*)a.kt + (size_t)h * a.max_nodes * DH + d0;
+  const uint16_t* vtb = (const uint16_t*)a.vt + (size_t)h * a.max_nodes * DH + d0;
   const int rdep = a.depth[n];
-  const float qd = a.q[(size_t)n * a.d + h * DH + dd];
+  const f32x4 q4 = *(const f32x4*)(a.q + (size_t)n * a.d + h * DH + d0);
   int key[RK];
 #pragma unroll
   for (int jj = 0; jj < RK; ++jj) key[jj] = p32[jj];
   const size_t cs = (size_t)a.N * RB;
   const unsigned char* rec = (const unsigned char*)a.part + ((size_t)h * ns * a.N + n) * RB;
-  float M = -INFINITY, L = 0.f, O = 0.f;
+  float M = -INFINITY, L = 0.f, O[DPT] = {0.f, 0.f, 0.f, 0.f};
   for (int c0 = 0; c0 < ns; c0 += B) {
     f32x2_t ml[B];
-    float ov[B];
+    u32x2 ov[B];
 #pragma unroll
     for (int j = 0; j < B; ++j) {
       const int cc = min(c0 + j, ns - 1);
       ml[j] = *(const f32x2_t*)(rec + cc * cs);
-      ov[j] = (float)__builtin_bit_cast(_Float16, *(const uint16_t*)(rec + cc * cs + 16 + 2 * dd));
+      ov[j] = *(const u32x2*)(rec + cc * cs + 16 + 2 * d0);
     }
 #pragma unroll
     for (int j = 0; j < B; ++j) {
@@ -1371,7 +1387,10 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
       const float mn = fmaxf(M, ml[j][0]);
       const float al = __expf(M - mn), wj = __expf(ml[j][0] - mn);
       L = fmaf(L, al, ml[j][1] * wj);
-      O = fmaf(O, al, ov[j] * wj);
+      const float o4[DPT] = {h2f((uint16_t)(ov[j][0] & 0xffffu)), h2f((uint16_t)(ov[j][0] >> 16)),
+                             h2f((uint16_t)(ov[j][1] & 0xffffu)), h2f((uint16_t)(ov[j][1] >> 16))};
+#pragma unroll
+      for (int e = 0; e < DPT; ++e) O[e] = fmaf(O[e], al, o4[e] * wj);
       M = mn;
     }
   }
@@ -1384,15 +1403,20 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
         key[jj] = j < kPath32 ? p32[j] : a.ancl[a.anc_off[n] + j];
       }
     }
-    float s[RK], vv[RK];
+    u32x2 k4[RK], v4[RK];
 #pragma unroll
     for (int jj = 0; jj < RK; ++jj) {
-      s[jj] = qd * bf2f(ktb[(size_t)key[jj] * DH]);
-      vv[jj] = bf2f(vtb[(size_t)key[jj] * DH]);
+      k4[jj] = *(const u32x2*)(ktb + (size_t)key[jj] * DH);
+      v4[jj] = *(const u32x2*)(vtb + (size_t)key[jj] * DH);
     }
+    float s[RK];
+#pragma unroll
+    for (int jj = 0; jj < RK; ++jj)
+      s[jj] = (q4[0] * __uint_as_float(k4[jj][0] << 16) + q4[1] * __uint_as_float(k4[jj][0] & 0xffff0000u)) +
+              (q4[2] * __uint_as_float(k4[jj][1] << 16) + q4[3] * __uint_as_float(k4[jj][1] & 0xffff0000u));
     // (a butterfly leaves the same sum in every thread of the pair)
 #pragma unroll
-    for (int off = 1; off < DH; off <<= 1)
+    for (int off = 1; off < TPP; off <<= 1)
 #pragma unroll
       for (int jj = 0; jj < RK; ++jj) s[jj] += __shfl_xor(s[jj], off);
     float mb = -INFINITY;
@@ -1402,18 +1426,23 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
       mb = fmaxf(mb, s[jj]);
     }
     const float mn = fmaxf(M, mb), al = __expf(M - mn);
-    float ps = 0.f, po = 0.f;
+    float ps = 0.f, po[DPT] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int jj = 0; jj < RK; ++jj) {
       const float p = __expf(s[jj] - mn);
       ps += p;
-      po = fmaf(p, vv[jj], po);
+      const float v[DPT] = {__uint_as_float(v4[jj][0] << 16), __uint_as_float(v4[jj][0] & 0xffff0000u),
+                            __uint_as_float(v4[jj][1] << 16), __uint_as_float(v4[jj][1] & 0xffff0000u)};
+#pragma unroll
+      for (int e = 0; e < DPT; ++e) po[e] = fmaf(p, v[e], po[e]);
     }
     L = fmaf(L, al, ps);
-    O = fmaf(O, al, po);
+#pragma unroll
+    for (int e = 0; e < DPT; ++e) O[e] = fmaf(O[e], al, po[e]);
     M = mn;
   }
-  st_act((uint16_t*)a.out, n, h * DH + dd, a.ldo, O / L, a.err);
+  const float outv[DPT] = {O[0] / L, O[1] / L, O[2] / L, O[3] / L};
+  st_act4_u16((uint16_t*)a.out, n, h * DH + d0, a.ldo, outv, a.err);
 }
 
 hipError_t launch_attn(int f32, int DH, const AttnArgs& a, hipStream_t s) {
@@ -1422,7 +1451,7 @@ hipError_t launch_attn(int f32, int DH, const AttnArgs& a, hipStream_t s) {
     if (a.P > 0 && (a.CL <= 0 || a.CL > AT_STAGE || a.CL % 32 || a.nsplit != (a.P + a.CL - 1) / a.CL))
       return hipErrorInvalidValue;
     const int blocks = max(1, a.H * a.nsplit);
-    const int mblocks = (a.N * a.H * DH + 255) / 256;
+    const int mblocks = (a.N * a.H * (DH / 4) + 255) / 256;
     if (DH == 64) {
       attn_split_kernel<64><<<blocks, 64 * AT_MAXW, 0, s>>>(a);
       attn_merge_kernel<64><<<mblocks, 256, 0, s>>>(a);
