@@ -166,14 +166,35 @@ hipError_t launch_embed(int f32, const void* wte, const void* wpe, const int* to
 
 // ------------------------------------------------------------------ residual + LayerNorm
 //
-// One workgroup per node, the row held in registers (E = ceil(d / 256)
-// elements per thread):
+// One workgroup per node, the row held in registers: thread t owns the
+// column groups 4t .. 4t+3, 4(t+256) .. 4(t+256)+3, ... (E groups, E =
+// ceil(d / 1024); d is a multiple of 32), so every load is 8 or 16 bytes and a
+// bf16 model's activation store is one 8-byte write:
 //   if S > 0:  x[n] += bias + part[0][n] + ... + part[S-1][n]   (split-K sums of the
 //              previous residual GEMM, added in split order), written back;
 //   a[n] = (x[n] - mean) / sqrt(var + eps) * g + b   (biased variance).
 // Every load is issued (clamped to the row) before any of them is used, so
 // the row costs one memory round trip.  SPL is the split count when known at
-// compile time (0, 4 or 8), else -1 and the loop runs to S.
+// compile time (0, 1, 2, 4 or 8), else -1 and the loop runs to S.
+
+template <typename T> __device__ __forceinline__ void ld4(const T* p, size_t k, float (&o)[4]);
+template <> __device__ __forceinline__ void ld4<float>(const float* p, size_t k, float (&o)[4]) {
+  const f32x4 v = *(const f32x4*)(p + k);
+  o[0] = v.x; o[1] = v.y; o[2] = v.z; o[3] = v.w;
+}
+template <> __device__ __forceinline__ void ld4<uint16_t>(const uint16_t* p, size_t k, float (&o)[4]) {
+  const u32x2 v = *(const u32x2*)(p + k);
+  o[0] = __uint_as_float(v.x << 16); o[1] = __uint_as_float(v.x & 0xffff0000u);
+  o[2] = __uint_as_float(v.y << 16); o[3] = __uint_as_float(v.y & 0xffff0000u);
+}
+template <typename T> __device__ __forceinline__ void st_act4(T* p, int n, int k, int ld, const float (&v)[4], unsigned* err);
+template <> __device__ __forceinline__ void st_act4<float>(float* p, int n, int k, int ld, const float (&v)[4], unsigned*) {
+  *(f32x4*)(p + (size_t)n * ld + k) = (f32x4){v[0], v[1], v[2], v[3]};
+}
+template <>
+__device__ __forceinline__ void st_act4<uint16_t>(uint16_t* p, int n, int k, int ld, const float (&v)[4], unsigned* err) {
+  st_act4_u16(p, n, k, ld, v, err);
+}
 
 template <typename T, typename OUT, int E, int SPL>
 __global__ __launch_bounds__(256) void ln_resid_kernel(float* __restrict__ x, int d, const float* __restrict__ part,
@@ -184,53 +205,69 @@ __global__ __launch_bounds__(256) void ln_resid_kernel(float* __restrict__ x, in
   constexpr int PS = SPL > 0 ? SPL : 1;
   __shared__ float red[4];
   pass_signal(sig);
-  const int n = blockIdx.x, tid = threadIdx.x;
+  const int n = blockIdx.x, tid = threadIdx.x, nc = d >> 2;
   float* xr = x + (size_t)n * d;
   const float* pr = part + (size_t)n * d;
-  float v[E];
-  T gw[E], bw[E], cw[E];
-  float pv[E][PS];
+  float v[E][4], gw[E][4], bw[E][4], cw[E][4];
+  float pv[E][PS][4];
 #pragma unroll
   for (int i = 0; i < E; ++i) {
-    const int k = min(tid + i * 256, d - 1);
-    v[i] = xr[k];
-    gw[i] = g[k];
-    bw[i] = b[k];
+    const size_t k = 4 * (size_t)min(tid + i * 256, nc - 1);
+    ld4(xr, k, v[i]);
+    ld4(g, k, gw[i]);
+    ld4(b, k, bw[i]);
     if constexpr (SPL > 0) {
-      cw[i] = bias[k];
+      ld4(bias, k, cw[i]);
 #pragma unroll
-      for (int sp = 0; sp < SPL; ++sp) pv[i][sp] = pr[sp * pstride + k];
+      for (int sp = 0; sp < SPL; ++sp) ld4(pr + sp * pstride, k, pv[i][sp]);
     }
   }
   float s = 0.f;
 #pragma unroll
   for (int i = 0; i < E; ++i) {
-    const int k = tid + i * 256;
+    const int c = tid + i * 256;
     if constexpr (SPL != 0) {
-      float acc;
+      float acc[4];
       if constexpr (SPL > 0) {
-        acc = ldT(cw, i);
 #pragma unroll
-        for (int sp = 0; sp < SPL; ++sp) acc += pv[i][sp];
+        for (int j = 0; j < 4; ++j) {
+          acc[j] = cw[i][j];
+#pragma unroll
+          for (int sp = 0; sp < SPL; ++sp) acc[j] += pv[i][sp][j];
+        }
       } else {
-        acc = ldT(bias, min(k, d - 1));
-        for (int sp = 0; sp < S; ++sp) acc += pr[sp * pstride + min(k, d - 1)];
+        const size_t k = 4 * (size_t)min(c, nc - 1);
+        ld4(bias, k, acc);
+        for (int sp = 0; sp < S; ++sp) {
+          float p4[4];
+          ld4(pr + sp * pstride, k, p4);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) acc[j] += p4[j];
+        }
       }
-      v[i] += acc;
-      if (k < d) xr[k] = v[i];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) v[i][j] += acc[j];
+      if (c < nc) *(f32x4*)(xr + 4 * c) = (f32x4){v[i][0], v[i][1], v[i][2], v[i][3]};
     }
-    if (k < d) s += v[i];
+    if (c < nc) s += (v[i][0] + v[i][1]) + (v[i][2] + v[i][3]);
   }
   const float mean = block_sum256(s, red) / d;
   float q = 0.f;
 #pragma unroll
   for (int i = 0; i < E; ++i)
-    if (tid + i * 256 < d) q += (v[i] - mean) * (v[i] - mean);
+    if (tid + i * 256 < nc) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) q += (v[i][j] - mean) * (v[i][j] - mean);
+    }
   const float den = sqrtf(block_sum256(q, red) / d + eps);
 #pragma unroll
   for (int i = 0; i < E; ++i) {
-    const int k = tid + i * 256;
-    if (k < d) st_act(a, n, k, lda, (v[i] - mean) / den * ldT(gw, i) + ldT(bw, i), err);
+    const int c = tid + i * 256;
+    float o[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) o[j] = (v[i][j] - mean) / den * gw[i][j] + bw[i][j];
+    // (the bf16 store's error ballot runs over the in-range lanes only)
+    if (c < nc) st_act4(a, n, 4 * c, lda, o, err);
   }
 }
 
@@ -257,15 +294,10 @@ template <typename T>
 static hipError_t ln_go_e(float* x, int N, int d, const float* part, int S, size_t pstride, const void* bias,
                           const void* g, const void* b, float eps, void* a, int lda, unsigned long long* sig,
                           unsigned* err, hipStream_t s) {
-  switch ((d + 255) / 256) {
+  if (d % 32) return hipErrorInvalidValue;
+  switch ((d + 1023) / 1024) {
     case 1: ln_go_s<T, 1>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, err, s); break;
     case 2: ln_go_s<T, 2>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, err, s); break;
-    case 3: ln_go_s<T, 3>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, err, s); break;
-    case 4: ln_go_s<T, 4>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, err, s); break;
-    case 5: ln_go_s<T, 5>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, err, s); break;
-    case 6: ln_go_s<T, 6>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, err, s); break;
-    case 7: ln_go_s<T, 7>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, err, s); break;
-    case 8: ln_go_s<T, 8>(x, N, d, part, S, pstride, bias, g, b, eps, a, lda, sig, err, s); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
