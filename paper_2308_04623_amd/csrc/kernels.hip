@@ -1383,10 +1383,14 @@ __global__ __launch_bounds__(64 * AT_MAXW) void attn_split_kernel(AttnArgs a) {
   if ((int)blockIdx.x < a.H * a.nsplit) attn_prefix_chunk<DH>(a, lds, blockIdx.x % a.H, blockIdx.x / a.H);
 }
 
+// one wave per block: at 128 nodes x 20 heads that is 640 blocks, so every CU
+// takes part (256-thread blocks left 96 of the 256 CUs idle)
+constexpr int kMergeThreads = 64;
+
 template <int DH>
-__global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
+__global__ __launch_bounds__(kMergeThreads) void attn_merge_kernel(AttnArgs a) {
   // TPP threads per (node, head), DPT = 4 consecutive dims each
-  constexpr int RB = part_bytes<DH>(), DPT = 4, TPP = DH / DPT, PER = 256 / TPP, B = 16, RK = 8;
+  constexpr int RB = part_bytes<DH>(), DPT = 4, TPP = DH / DPT, PER = kMergeThreads / TPP, B = 16, RK = 8;
   pass_signal(a.sig);
   const int pair = blockIdx.x * PER + threadIdx.x / TPP, d0 = DPT * (threadIdx.x % TPP);
   if (pair >= a.N * a.H) return;  // (a whole pair's threads together)
@@ -1483,13 +1487,13 @@ hipError_t launch_attn(int f32, int DH, const AttnArgs& a, hipStream_t s) {
     if (a.P > 0 && (a.CL <= 0 || a.CL > AT_STAGE || a.CL % 32 || a.nsplit != (a.P + a.CL - 1) / a.CL))
       return hipErrorInvalidValue;
     const int blocks = max(1, a.H * a.nsplit);
-    const int mblocks = (a.N * a.H * (DH / 4) + 255) / 256;
+    const int mblocks = (a.N * a.H * (DH / 4) + kMergeThreads - 1) / kMergeThreads;
     if (DH == 64) {
       attn_split_kernel<64><<<blocks, 64 * AT_MAXW, 0, s>>>(a);
-      attn_merge_kernel<64><<<mblocks, 256, 0, s>>>(a);
+      attn_merge_kernel<64><<<mblocks, kMergeThreads, 0, s>>>(a);
     } else {
       attn_split_kernel<32><<<blocks, 64 * AT_MAXW, 0, s>>>(a);
-      attn_merge_kernel<32><<<mblocks, 256, 0, s>>>(a);
+      attn_merge_kernel<32><<<mblocks, kMergeThreads, 0, s>>>(a);
     }
     return hipGetLastError();
   }
