@@ -871,7 +871,15 @@ static hipError_t launch_gemm_wide(int kind, const void* Wp, int M, int K, const
   switch (rbt) {
     case 1: gemm2d_go<1, 2, 4>(kind, W, KC, RBtot, NT, kcs, gx, gt, gy, act, ep, s); break;
     case 2: gemm2d_go<2, 2, 4>(kind, W, KC, RBtot, NT, kcs, gx, gt, gy, act, ep, s); break;
-    case 4: gemm2d_go<4, 2, 4>(kind, W, KC, RBtot, NT, kcs, gx, gt, gy, act, ep, s); break;
+    case 4:
+      // (QKV at more than 128 nodes: 8 waves, each with half the k-steps, measured
+      // faster there; the other kinds and smaller trees are faster with 4)
+      if (kind == EPI_QKV)
+        gemm2d_launch<4, EPI_QKV, 2, 8>(dim3(8 * ((gx + 7) / 8) * gt * gy), W, KC, RBtot, NT, kcs, gx, gt, gy, act,
+                                        ep, s);
+      else
+        gemm2d_go<4, 2, 4>(kind, W, KC, RBtot, NT, kcs, gx, gt, gy, act, ep, s);
+      break;
     default: gemm2d_go<8, 1, 4>(kind, W, KC, RBtot, NT, kcs, gx, gt, gy, act, ep, s); break;
   }
   return hipGetLastError();
