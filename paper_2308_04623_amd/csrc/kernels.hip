@@ -1256,7 +1256,12 @@ __device__ __forceinline__ uint32_t f16pair(float a, float b) {
 template <int DH>
 __device__ __forceinline__ void attn_prefix_chunk(const AttnArgs& a, uint16_t* lds, int h, int c) {
   constexpr int KS = DH + 8;        // LDS row stride of K (elements)
-  constexpr int VS = AT_STAGE + 8;  // LDS row stride of V^T (elements)
+  // LDS row stride of V^T (elements).  Row d holds key k at position
+  // k ^ (8 ((d / 16) % 8)): the swizzle moves whole 8-key groups inside their
+  // 32-key block (so an operand read of 8 keys stays one aligned 16-byte read,
+  // and the 16 rows of one read share the swizzle), and it sends the staging
+  // stores of one key's 64 dims, 8 rows apart, to different banks.
+  constexpr int VS = AT_STAGE + 8;
   constexpr int MAXU = (AT_STAGE * DH / 8 + 64 * AT_MAXW - 1) / (64 * AT_MAXW);  // 16-byte units per thread
   uint16_t* ks = lds;
   uint16_t* vts = lds + AT_STAGE * KS;
@@ -1299,11 +1304,12 @@ __device__ __forceinline__ void attn_prefix_chunk(const AttnArgs& a, uint16_t* l
       const bool ok = r < nk;
       const u32x4 kk = ok ? kr[j] : (u32x4){0, 0, 0, 0};
       const u32x4 vv = ok ? vr[j] : (u32x4){0, 0, 0, 0};
+      const int vsw = 8 * ((c8 >> 1) & 7);  // V^T key swizzle of rows 8 c8 .. 8 c8 + 7
       *(u32x4*)(ks + r * KS + 8 * c8) = kk;
 #pragma unroll
       for (int e2 = 0; e2 < 4; ++e2) {
-        vts[(8 * c8 + 2 * e2) * VS + r] = (uint16_t)(vv[e2] & 0xffffu);
-        vts[(8 * c8 + 2 * e2 + 1) * VS + r] = (uint16_t)(vv[e2] >> 16);
+        vts[(8 * c8 + 2 * e2) * VS + (r ^ vsw)] = (uint16_t)(vv[e2] & 0xffffu);
+        vts[(8 * c8 + 2 * e2 + 1) * VS + (r ^ vsw)] = (uint16_t)(vv[e2] >> 16);
       }
     }
   }
@@ -1364,7 +1370,7 @@ __device__ __forceinline__ void attn_prefix_chunk(const AttnArgs& a, uint16_t* l
       pack_hilo8(pv, ph, pl);
 #pragma unroll
       for (int tt = 0; tt < DH / 16; ++tt) {
-        const u32x4 va = *(const u32x4*)(vts + (16 * tt + i) * VS + 32 * sb + 8 * g);
+        const u32x4 va = *(const u32x4*)(vts + (16 * tt + i) * VS + ((32 * sb + 8 * g) ^ (8 * (tt & 7))));
         o[tt] = o[tt] * alpha;
         o[tt] = mfma16(va, ph, o[tt]);
         o[tt] = mfma16(va, pl, o[tt]);
